@@ -1,0 +1,169 @@
+"""CPU oracle for wavefront decoding of a spatial autoregressive context model.
+
+TEST INFRASTRUCTURE ONLY: the tests, the smoke check and the benchmark's
+CPU-baseline leg may import this package; the GPU product path never does,
+and this package never imports the GPU path.
+
+* ``wf_oracle.c`` -- plain sequential decode/encode of the latent grid in a
+  given topological order (raster by default, Sec. III-A, Eq. 2), with the 5x5
+  causal masked-conv context (Appendix A, Def. 1, R = 2) and the 1x1 entropy
+  parameter network (Sec. II-B, Eq. 1); fp64 accumulation, fp32 storage.
+* ``schedule.py`` -- the dependency DAG of the mask (Eq. 3, Def. 1), its ASAP
+  levels and critical path, and a brute-force search over linear schedules
+  (Sec. III-B, Eq. 5-7; Appendix A, Thm. 1).
+"""
+import ctypes
+import os
+import subprocess
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_SRC = os.path.join(_HERE, "wf_oracle.c")
+_LIB = os.path.join(_HERE, "liboracle.so")
+_lib = None
+
+
+def build():
+    """Compile the C oracle with gcc (-O2, no fast-math, single thread)."""
+    cmd = ["gcc", "-O2", "-std=c11", "-fPIC", "-shared", "-Wall", "-Wextra",
+           "-fno-fast-math", "-ffp-contract=off", "-o", _LIB, _SRC, "-lm"]
+    subprocess.run(cmd, check=True)
+    return _LIB
+
+
+class _Model(ctypes.Structure):
+    _fields_ = [
+        ("H", ctypes.c_int32), ("W", ctypes.c_int32), ("M", ctypes.c_int32),
+        ("B", ctypes.c_int32), ("K", ctypes.c_int32),
+        ("d1", ctypes.c_int32), ("d2", ctypes.c_int32),
+        ("relaxed", ctypes.c_int32), ("bf16", ctypes.c_int32),
+        ("slope", ctypes.c_float),
+        ("ctx_w", ctypes.c_void_p), ("ctx_b", ctypes.c_void_p),
+        ("w1", ctypes.c_void_p), ("b1", ctypes.c_void_p),
+        ("w2", ctypes.c_void_p), ("b2", ctypes.c_void_p),
+        ("w3", ctypes.c_void_p), ("b3", ctypes.c_void_p),
+        ("table", ctypes.c_void_p), ("L", ctypes.c_int32),
+    ]
+
+
+class _Out(ctypes.Structure):
+    _fields_ = [
+        ("y_hat", ctypes.c_void_p), ("mean", ctypes.c_void_p),
+        ("scale", ctypes.c_void_p), ("idx", ctypes.c_void_p),
+        ("weight", ctypes.c_void_p), ("comp_mean", ctypes.c_void_p),
+    ]
+
+
+def _load():
+    global _lib
+    if _lib is None:
+        if not os.path.exists(_LIB) or os.path.getmtime(_LIB) < os.path.getmtime(_SRC):
+            build()
+        lib = ctypes.CDLL(_LIB)
+        lib.oracle_run.argtypes = [ctypes.POINTER(_Model), ctypes.c_void_p, ctypes.c_void_p,
+                                   ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int64,
+                                   ctypes.POINTER(_Out)]
+        lib.oracle_run.restype = ctypes.c_int
+        lib.oracle_eval.argtypes = [ctypes.POINTER(_Model), ctypes.c_void_p, ctypes.c_void_p,
+                                    ctypes.c_void_p, ctypes.c_int64, ctypes.POINTER(_Out)]
+        lib.oracle_eval.restype = ctypes.c_int
+        _lib = lib
+    return _lib
+
+
+def _f32(a):
+    return np.ascontiguousarray(a, dtype=np.float32)
+
+
+def _ptr(a):
+    return None if a is None else a.ctypes.data
+
+
+class Model:
+    """Model description for the oracle.  ``weights`` is a dict with keys
+    ctx_w [2M][M][5][5], ctx_b [2M], w1 [d1][4M], b1, w2 [d2][d1], b2,
+    w3 [n3][d2], b3 (PyTorch layouts); ``table`` is the scale table."""
+
+    def __init__(self, weights, table, H, W, B=1, K=1, relaxed=False, bf16=False,
+                 slope=0.01):
+        self.arrays = {k: _f32(v) for k, v in weights.items()}
+        self.table = _f32(table)
+        M = self.arrays["ctx_w"].shape[1]
+        d1 = self.arrays["w1"].shape[0]
+        d2 = self.arrays["w2"].shape[0]
+        n3 = self.arrays["w3"].shape[0]
+        if n3 != (2 if K == 1 else 9) * M:
+            raise ValueError("w3 rows do not match K and M")
+        self.H, self.W, self.M, self.B, self.K = H, W, M, B, K
+        self.d1, self.d2 = d1, d2
+        a = self.arrays
+        self._m = _Model(H, W, M, B, K, d1, d2, int(relaxed), int(bf16), slope,
+                         _ptr(a["ctx_w"]), _ptr(a["ctx_b"]), _ptr(a["w1"]), _ptr(a["b1"]),
+                         _ptr(a["w2"]), _ptr(a["b2"]), _ptr(a["w3"]), _ptr(a["b3"]),
+                         _ptr(self.table), len(self.table))
+
+    def _alloc(self, n):
+        M, K = self.M, self.K
+        outs = {
+            "y_hat": np.zeros((n, M), np.float32),
+            "mean": np.zeros((n, M), np.float32),
+            "scale": np.zeros((n, K, M), np.float32),
+            "idx": np.zeros((n, K, M), np.int32),
+            "weight": np.zeros((n, K, M), np.float32),
+            "comp_mean": np.zeros((n, K, M), np.float32),
+        }
+        c = _Out(*(_ptr(outs[k]) for k in ("y_hat", "mean", "scale", "idx", "weight", "comp_mean")))
+        return outs, c
+
+    def _shape(self, outs):
+        B, H, W = self.B, self.H, self.W
+        return {k: v.reshape((B, H, W) + v.shape[1:]) for k, v in outs.items()}
+
+    def decode(self, psi, sym, order=None):
+        """Sequential decode from int32 symbols [B][H][W][M]; returns a dict of
+        NHWC arrays y_hat, mean, scale, idx, weight, comp_mean (the last four
+        with a component axis of length K before the channel axis)."""
+        return self._run(psi, np.ascontiguousarray(sym, dtype=np.int32).copy(), None, order)[0]
+
+    def encode(self, psi, y, order=None):
+        """Sequential encode of y [B][H][W][M]; returns (outputs, symbols)."""
+        sym = np.zeros((self.B, self.H, self.W, self.M), np.int32)
+        return self._run(psi, sym, _f32(y), order)
+
+    def _run(self, psi, sym, y, order):
+        psi = _f32(psi)
+        n = self.B * self.H * self.W
+        if psi.size != n * 2 * self.M or sym.size != n * self.M:
+            raise ValueError("psi / symbol shape mismatch")
+        outs, c = self._alloc(n)
+        ordp = None
+        if order is not None:
+            order = np.ascontiguousarray(order, dtype=np.int64)
+            ordp = order.ctypes.data
+        rc = _load().oracle_run(ctypes.byref(self._m), _ptr(psi), sym.ctypes.data,
+                                _ptr(y), ordp, n if order is None else len(order),
+                                ctypes.byref(c))
+        if rc != 0:
+            raise RuntimeError("oracle_run failed")
+        return self._shape(outs), sym.reshape(self.B, self.H, self.W, self.M)
+
+    def eval(self, y_hat, psi, lats=None):
+        """Teacher-forced parameters from a given reconstruction, at the listed
+        flat latent indices (all latents when None).  Returns flat arrays
+        indexed like ``lats``."""
+        y_hat = _f32(y_hat)
+        psi = _f32(psi)
+        latp = None
+        n = self.B * self.H * self.W
+        if lats is not None:
+            lats = np.ascontiguousarray(lats, dtype=np.int64)
+            latp = lats.ctypes.data
+            n = len(lats)
+        outs, c = self._alloc(n)
+        rc = _load().oracle_eval(ctypes.byref(self._m), _ptr(y_hat), _ptr(psi), latp, n,
+                                 ctypes.byref(c))
+        if rc != 0:
+            raise RuntimeError("oracle_eval failed")
+        outs.pop("y_hat")
+        return outs

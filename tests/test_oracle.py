@@ -1,0 +1,298 @@
+"""Pins of the CPU oracle against definitions it does not share code with.
+
+Each check ties the oracle to something fixed outside it:
+
+* library fixed point: the oracle's final reconstruction, pushed once through
+  a library masked conv2d (torch, fp64) whose mask comes from the context
+  cells printed in Fig. 2(d), then numpy matmuls, LeakyReLU, scipy softmax and
+  numpy searchsorted, must give back the oracle's means, scales, indices and
+  y_hat - mean = symbol (Sec. III-A: each latent's parameters are a function
+  of its causal context, Eq. 1-2);
+* order invariance: raster, wavefront and random topological orders give
+  bit-identical results (Sec. III-A, Eq. 4), while a non-topological order does
+  not;
+* encode/decode round trip, batch independence, the relaxed mask as zeroed
+  taps, a context-free model in closed form, and round-half-to-even ties.
+"""
+import os
+
+import numpy as np
+import pytest
+import scipy.special
+import torch
+
+import oracle
+from oracle import schedule as S
+from paper_2607_19082_amd import inputs
+
+GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
+
+
+def fig2d_mask(relaxed=False):
+    """5x5 mask built from the context cells printed in Fig. 2(d)."""
+    focus, cells = None, []
+    with open(os.path.join(GOLDEN, "fig2d_wavefront_5x5_lambda3_8x8.txt")) as f:
+        for line in f:
+            if line.startswith("focus"):
+                focus = [int(v) for v in line.split()[1:]]
+            elif line.startswith("context"):
+                cells.append([int(v) for v in line.split()[1:]])
+    mask = np.zeros((5, 5))
+    for r, c in cells:
+        dy, dx = r - focus[0], c - focus[1]
+        if relaxed and dx == 2 and dy in (-1, -2):
+            continue
+        mask[dy + 2, dx + 2] = 1.0
+    return mask
+
+
+def bf16_round(a):
+    return torch.from_numpy(np.asarray(a, np.float32)).to(torch.bfloat16).to(torch.float32).numpy()
+
+
+def library_params(w, table, y_hat, psi, K, relaxed=False, bf16=False, slope=0.01):
+    """Per-latent parameters from a fixed reconstruction, built from library
+    routines in fp64 (the 'obviously right' form of the per-latent function)."""
+    B, H, Wd, M = y_hat.shape
+    op = bf16_round if bf16 else (lambda a: np.asarray(a, np.float32))
+    cw = op(w["ctx_w"]).astype(np.float64) * fig2d_mask(relaxed)[None, None]
+    x = torch.from_numpy(op(y_hat).astype(np.float64)).permute(0, 3, 1, 2)
+    ctx = torch.nn.functional.conv2d(x, torch.from_numpy(cw), torch.from_numpy(w["ctx_b"].astype(np.float64)),
+                                     padding=2).permute(0, 2, 3, 1).numpy()
+    h0 = np.concatenate([psi.astype(np.float64), ctx], axis=-1)
+    h0 = op(h0.astype(np.float32)).astype(np.float64) if bf16 else h0
+
+    def layer(h, wm, bv, act):
+        z = h @ op(wm).astype(np.float64).T + bv.astype(np.float64)
+        if act:
+            z = torch.nn.functional.leaky_relu(torch.from_numpy(z), slope).numpy()
+        return z
+
+    h1 = layer(h0, w["w1"], w["b1"], True)
+    h1 = op(h1.astype(np.float32)).astype(np.float64) if bf16 else h1
+    h2 = layer(h1, w["w2"], w["b2"], True)
+    h2 = op(h2.astype(np.float32)).astype(np.float64) if bf16 else h2
+    o = layer(h2, w["w3"], w["b3"], False)
+    if K == 1:
+        mu = o[..., :M]
+        sig = o[..., M:2 * M][..., None, :]
+        wgt = np.ones_like(sig)
+        cm = mu[..., None, :]
+    else:
+        lg = o[..., :3 * M].reshape(B, H, Wd, 3, M)
+        cm = o[..., 3 * M:6 * M].reshape(B, H, Wd, 3, M)
+        sig = o[..., 6 * M:9 * M].reshape(B, H, Wd, 3, M)
+        wgt = scipy.special.softmax(lg, axis=3)
+        mu = (wgt * cm).sum(axis=3)
+    sig = np.maximum(sig, table[0])
+    idx = np.searchsorted(table[:-1].astype(np.float64), sig, side="left")
+    return dict(mean=mu, scale=sig, idx=idx, weight=wgt, comp_mean=cm)
+
+
+def small_case(M=8, K=1, H=6, W=7, B=1, lap_b=2.0, clip=32, seed_shift=0, zero_ctx=False):
+    w = inputs.make_weights(M, K, seed=0 + seed_shift)
+    if zero_ctx:
+        w["ctx_w"][:] = 0
+    table = inputs.scale_table()
+    psi = inputs.make_psi(B, H, W, M, seed=1 + seed_shift)
+    sym = inputs.make_symbols(B, H, W, M, lap_b, clip, seed=2 + seed_shift)
+    return w, table, psi, sym
+
+
+def near_boundary(table, sig, rel=1e-5):
+    """Scales within rel of a table level; a scale clamped to table[0] is
+    exactly at the floor on both sides and is not counted."""
+    t = table[:-1].astype(np.float64)[None, :]
+    s = np.asarray(sig, np.float64).reshape(-1, 1)
+    near = (np.abs(s - t) <= rel * t).any(axis=1)
+    near &= s[:, 0] != np.float64(table[0])
+    return near.reshape(np.shape(sig))
+
+
+def check_fixed_point(out, sym, w, table, psi, K, relaxed=False, bf16=False, atol=2e-5):
+    lib = library_params(w, table, out["y_hat"], psi, K, relaxed, bf16)
+    np.testing.assert_allclose(out["mean"], lib["mean"], rtol=0, atol=atol)
+    np.testing.assert_allclose(out["scale"], lib["scale"], rtol=0, atol=atol)
+    np.testing.assert_allclose(out["weight"], lib["weight"], rtol=0, atol=atol)
+    np.testing.assert_allclose(out["comp_mean"], lib["comp_mean"], rtol=0, atol=atol)
+    np.testing.assert_allclose(out["y_hat"] - lib["mean"], sym, rtol=0, atol=atol)
+    nb = near_boundary(table, out["scale"])
+    assert np.array_equal(out["idx"][~nb], lib["idx"][~nb])
+    assert nb.mean() < 0.01
+
+
+@pytest.mark.parametrize("K", [1, 3])
+@pytest.mark.parametrize("relaxed", [False, True])
+def test_fixed_point_against_library(K, relaxed):
+    w, table, psi, sym = small_case(M=8, K=K, H=6, W=7)
+    m = oracle.Model(w, table, 6, 7, 1, K, relaxed=relaxed)
+    out = m.decode(psi, sym)
+    check_fixed_point(out, sym, w, table, psi, K, relaxed)
+    # the recurrence is non-trivial: context matters
+    assert np.abs(out["mean"]).max() > 0.1
+
+
+def test_fixed_point_bf16():
+    w, table, psi, sym = small_case(M=16, K=1, H=5, W=6)
+    m = oracle.Model(w, table, 5, 6, 1, 1, bf16=True)
+    out = m.decode(psi, sym)
+    check_fixed_point(out, sym, w, table, psi, 1, bf16=True, atol=5e-5)
+    # and it differs from fp32 by the bf16 operand rounding, not more
+    ref = oracle.Model(w, table, 5, 6, 1, 1).decode(psi, sym)
+    d = np.abs(ref["mean"] - out["mean"]).max()
+    assert 1e-4 < d < 0.1
+
+
+def random_topological_order(H, W, B, ds, rng):
+    es = S.edges(H, W, ds)
+    preds = {(i, j): [] for i in range(H) for j in range(W)}
+    for s, d in es:
+        preds[d].append(s)
+    done, order = set(), []
+    ready = [(i, j) for (i, j), p in preds.items() if not p]
+    while ready:
+        k = rng.integers(len(ready))
+        v = ready.pop(k)
+        done.add(v)
+        order.append(v)
+        for (i, j), p in preds.items():
+            if (i, j) not in done and (i, j) not in ready and all(q in done for q in p):
+                ready.append((i, j))
+    assert len(order) == H * W
+    flat = []
+    for b in range(B):
+        flat += [b * H * W + i * W + j for i, j in order]
+    return np.array(flat, np.int64)
+
+
+@pytest.mark.parametrize("K", [1, 3])
+def test_order_invariance(K):
+    H, W, B = 6, 8, 2
+    w, table, psi, sym = small_case(M=8, K=K, H=H, W=W, B=B)
+    m = oracle.Model(w, table, H, W, B, K)
+    ref = m.decode(psi, sym)
+    rank = S.linear_rank(H, W, 3, 1)
+    wf = sorted(((rank[i][j], i, j) for i in range(H) for j in range(W)))
+    wf_order = np.array([b * H * W + i * W + j for b in range(B) for _, i, j in wf], np.int64)
+    rng = np.random.default_rng(5)
+    orders = [wf_order, random_topological_order(H, W, B, S.dependence_vectors(5), rng)]
+    for order in orders:
+        got = m.decode(psi, sym, order=order)
+        for k in ref:
+            assert np.array_equal(got[k], ref[k]), k
+    # a column-major order breaks the dependencies and must change the result
+    cm = np.array([b * H * W + i * W + j for b in range(B) for j in range(W) for i in range(H)], np.int64)
+    bad = m.decode(psi, sym, order=cm)
+    assert not np.array_equal(bad["mean"], ref["mean"])
+
+
+@pytest.mark.parametrize("K", [1, 3])
+def test_encode_roundtrip(K):
+    H, W, B, M = 5, 7, 1, 8
+    w, table, psi, sym = small_case(M=M, K=K, H=H, W=W, B=B)
+    m = oracle.Model(w, table, H, W, B, K)
+    dec = m.decode(psi, sym)
+    u = inputs.make_noise(B, H, W, M)
+    y = inputs.encoder_input(sym, u, dec["mean"])
+    enc, s = m.encode(psi, y)
+    assert np.array_equal(s, sym)
+    for k in dec:
+        assert np.array_equal(enc[k], dec[k]), k
+
+
+def test_batch_independence():
+    H, W, B, M = 5, 6, 3, 8
+    w, table, psi, sym = small_case(M=M, H=H, W=W, B=B)
+    full = oracle.Model(w, table, H, W, B, 1).decode(psi, sym)
+    one = oracle.Model(w, table, H, W, 1, 1)
+    for b in range(B):
+        got = one.decode(psi[b:b + 1], sym[b:b + 1])
+        for k in got:
+            assert np.array_equal(got[k][0], full[k][b]), k
+
+
+def test_relaxed_equals_zeroed_taps():
+    H, W, M = 6, 7, 8
+    w, table, psi, sym = small_case(M=M, H=H, W=W)
+    relaxed = oracle.Model(w, table, H, W, 1, 1, relaxed=True).decode(psi, sym)
+    wz = {k: v.copy() for k, v in w.items()}
+    wz["ctx_w"][:, :, 0, 4] = 0   # tap (-2, +2)
+    wz["ctx_w"][:, :, 1, 4] = 0   # tap (-1, +2)
+    full = oracle.Model(wz, table, H, W, 1, 1).decode(psi, sym)
+    for k in full:
+        assert np.array_equal(full[k], relaxed[k]), k
+    plain = oracle.Model(w, table, H, W, 1, 1).decode(psi, sym)
+    assert not np.array_equal(plain["mean"], relaxed["mean"])
+
+
+def test_masked_positions_ignored():
+    # weights at the 13 non-causal positions of the 5x5 kernel have no effect
+    H, W, M = 5, 6, 8
+    w, table, psi, sym = small_case(M=M, H=H, W=W)
+    ref = oracle.Model(w, table, H, W, 1, 1).decode(psi, sym)
+    w2 = {k: v.copy() for k, v in w.items()}
+    w2["ctx_w"] = w2["ctx_w"] * fig2d_mask()[None, None].astype(np.float32)
+    got = oracle.Model(w2, table, H, W, 1, 1).decode(psi, sym)
+    for k in ref:
+        assert np.array_equal(got[k], ref[k]), k
+
+
+def test_context_free_closed_form():
+    # with a zero context kernel every latent is independent: one MLP pass on
+    # [psi ; ctx_b] per latent, computed directly here
+    H, W, M = 4, 5, 8
+    w, table, psi, sym = small_case(M=M, H=H, W=W, zero_ctx=True)
+    out = oracle.Model(w, table, H, W, 1, 1).decode(psi, sym)
+    h0 = np.concatenate([psi.astype(np.float64), np.broadcast_to(w["ctx_b"], psi.shape[:-1] + (2 * M,))], -1)
+    lr = lambda z: np.where(z >= 0, z, 0.01 * z)
+    h1 = lr(h0 @ w["w1"].T.astype(np.float64) + w["b1"])
+    h2 = lr(h1 @ w["w2"].T.astype(np.float64) + w["b2"])
+    o = h2 @ w["w3"].T.astype(np.float64) + w["b3"]
+    np.testing.assert_allclose(out["mean"], o[..., :M], atol=2e-5, rtol=0)
+    np.testing.assert_allclose(out["scale"][..., 0, :], np.maximum(o[..., M:], table[0]), atol=2e-5, rtol=0)
+
+
+def test_rounding_ties_to_even_and_index_extremes():
+    # all weights zero: mean = b3[:M], raw scale = b3[M:] for every latent
+    H, W, M = 2, 3, 8
+    w, table, psi, sym = small_case(M=M, H=H, W=W)
+    for k in w:
+        if k != "b3":
+            w[k][:] = 0
+    w["b3"][:M] = 0.25
+    mid = np.float32(np.sqrt(np.float64(table[61]) * np.float64(table[62])))
+    raw = np.array([-3.0, 0.0, 0.05, 0.11, 0.12, mid, 256.0, 1e6], np.float32)
+    w["b3"][M:] = raw
+    m = oracle.Model(w, table, H, W, 1, 1)
+    frac = np.array([0.5, 1.5, 2.5, -0.5, -1.5, 0.49, 0.51, 3.5], np.float32)
+    y = np.broadcast_to(frac + np.float32(0.25), (1, H, W, M)).astype(np.float32)
+    enc, s = m.encode(psi, y)
+    assert np.array_equal(s[0, 0, 0], np.array([0, 2, 2, 0, -2, 0, 1, 4], np.int32))
+    # scale floor and index rule: #{l <= L-2 : T_l < sigma}
+    sig = enc["scale"][0, 0, 0, 0]
+    idx = enc["idx"][0, 0, 0, 0]
+    assert np.array_equal(sig, np.maximum(raw, table[0]))
+    assert idx[0] == 0 and idx[1] == 0 and idx[3] == 0      # at or below T_0
+    assert idx[4] == 1                                        # just above T_0
+    assert idx[5] == 62 and idx[6] == 63 and idx[7] == 63     # top of the table
+
+
+def test_scale_table():
+    t = inputs.scale_table()
+    assert t.dtype == np.float32 and len(t) == 64
+    assert abs(t[0] - 0.11) < 1e-7 and abs(t[-1] - 256.0) < 1e-4
+    r = t[1:].astype(np.float64) / t[:-1]
+    assert np.allclose(r, (256 / 0.11) ** (1 / 63), rtol=1e-6)
+    assert np.all(np.diff(t) > 0)
+
+
+def test_teacher_forced_eval_matches_run():
+    H, W, M = 5, 6, 8
+    w, table, psi, sym = small_case(M=M, K=3, H=H, W=W)
+    m = oracle.Model(w, table, H, W, 1, 3)
+    out = m.decode(psi, sym)
+    lats = np.array([0, 7, 13, 29], np.int64)
+    ev = m.eval(out["y_hat"], psi, lats)
+    for k in ("mean", "scale", "idx", "weight", "comp_mean"):
+        flat = out[k].reshape((H * W,) + out[k].shape[3:])
+        assert np.array_equal(ev[k], flat[lats]), k
