@@ -1,0 +1,174 @@
+/*
+ * wf.h -- C-ABI of libwf: wavefront decoding and encoding of a spatial
+ * autoregressive context model on one MI355X (gfx950) GPU.
+ *
+ * The method (Murai et al., "Wavefront Parallelization for Efficient Learned
+ * Image Compression"): the latents of an H x W grid form a DAG whose edges are
+ * the causal taps of a 5x5 masked convolution (Sec. III-A, Eq. 3; Appendix A,
+ * Def. 1).  The linear rank t(i,j) = lambda*i + j with the smallest shear
+ * lambda that satisfies the hyperplane condition (Sec. III-B, Eq. 5-7) is a
+ * valid schedule with W + lambda*(H-1) steps, optimal when W >= lambda
+ * (Appendix A, Thm. 1).  All latents of one step (a wavefront) are decoded
+ * together: their causal taps are gathered from the reconstruction
+ * (Sec. III-C, selective im2col), the masked-conv context and the 1x1
+ * entropy-parameter network are evaluated as batched products, and the
+ * reconstruction y_hat is written before the next step starts.
+ *
+ * Conventions for every entry point:
+ *  - Return value: WF_OK (0) or a negative wf_status; wf_last_error() then
+ *    holds a message for the calling thread.  No exception crosses the ABI.
+ *  - Arguments are validated before any work is enqueued; a rejected call
+ *    changes nothing.
+ *  - "host" pointers are read during the call only; "device" pointers must
+ *    stay valid until the enqueued work on the given stream has finished.
+ *  - All arrays are dense, row-major, NHWC (channel innermost).
+ */
+#ifndef WF_H
+#define WF_H
+
+#include <stdint.h>
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+    WF_OK = 0,
+    WF_E_INVALID = -1,      /* bad argument (NULL, non-positive size, ...)     */
+    WF_E_UNSUPPORTED = -2,  /* valid but not supported by this build           */
+    WF_E_HIP = -3,          /* a HIP runtime call failed                       */
+    WF_E_NOMEM = -4,        /* device or host allocation failed                */
+    WF_E_TIMEOUT = -5       /* a device-side wait exceeded its spin budget     */
+} wf_status;
+
+/* Tap sets of the 5x5 causal mask (Def. 1 with R = 2). */
+typedef enum {
+    WF_MASK_FULL = 0,       /* 12 taps: rows -2,-1 with dx in [-2,2]; (0,-2), (0,-1); lambda = 3 */
+    WF_MASK_RELAXED = 1     /* 10 taps: the full mask without (-1,+2) and (-2,+2); lambda = 2    */
+} wf_mask;
+
+typedef enum {
+    WF_FP32 = 0,            /* fp32 operands, fp32 accumulate                           */
+    WF_BF16 = 1             /* bf16 (round-to-nearest-even) operands, fp32 accumulate   */
+} wf_precision;
+
+typedef enum {
+    WF_DRIVER_STREAM = 0,   /* per-step kernel launches, enqueued one by one on the stream */
+    WF_DRIVER_GRAPH = 1,    /* the same per-step kernels, replayed from one HIP graph      */
+    WF_DRIVER_PERSISTENT = 2/* one cooperative kernel, device-wide barrier per step         */
+} wf_driver;
+
+/*
+ * Model and problem description.  All weight arrays are HOST memory in
+ * PyTorch layouts and are copied (and repacked) by wf_plan.
+ *   ctx_w [2M][M][5][5]  masked 5x5 conv weight (masked positions are ignored)
+ *   ctx_b [2M]
+ *   w1 [d1][4M], b1 [d1]   layer 1 input is [psi (2M) ; ctx (2M)]
+ *   w2 [d2][d1], b2 [d2]
+ *   w3 [n3][d2], b3 [n3]   n3 = 2M for K = 1 (rows: mean | scale),
+ *                          n3 = 9M for K = 3 (rows: weight | mean | scale,
+ *                          each block component-major: block*3M + k*M + c)
+ *   scale_table [L]        strictly increasing, positive
+ * Hidden layers use LeakyReLU with slope lrelu_slope; the last layer is linear.
+ */
+typedef struct {
+    int32_t H, W;           /* latent rows and columns                              */
+    int32_t M;              /* latent channels; multiple of 16                       */
+    int32_t B;              /* images decoded together on one wavefront sweep        */
+    int32_t K;              /* 1: mean-scale Gaussian; 3: 3-component mixture        */
+    int32_t d1, d2;         /* hidden widths of the entropy-parameter network        */
+    int32_t mask;           /* wf_mask                                               */
+    int32_t precision;      /* wf_precision                                          */
+    int32_t driver;         /* wf_driver                                             */
+    float lrelu_slope;
+    const float *ctx_w, *ctx_b;
+    const float *w1, *b1, *w2, *b2, *w3, *b3;
+    const float *scale_table;
+    int32_t L;              /* table length, 2 <= L <= 256                            */
+} wf_desc;
+
+/*
+ * Per-call outputs, all DEVICE memory owned by the caller.
+ *   y_hat     [B][H][W][M]     reconstruction (s + mean); also the AR state
+ *   mean      [B][H][W][M]     dequantisation offset (mixture mean for K = 3)
+ *   scale     [B][H][W][K][M]  max(raw scale, scale_table[0])
+ *   idx       [B][H][W][K][M]  #{l in [0, L-2] : scale_table[l] < scale}
+ *   weight    [B][H][W][K][M]  mixture weights (K = 3 only; NULL for K = 1)
+ *   comp_mean [B][H][W][K][M]  component means (K = 3 only; NULL for K = 1)
+ */
+typedef struct {
+    float *y_hat, *mean, *scale;
+    int32_t *idx;
+    float *weight, *comp_mean;
+} wf_out;
+
+typedef struct wf_plan_s *wf_plan_t;
+
+/*
+ * Schedule of an H x W grid under a mask (host only; no GPU needed).
+ * Writes step_of[i*W + j] = lambda*i + j (HOST array of H*W int32, may be
+ * NULL) and *n_steps = W + lambda*(H-1), where lambda is the least integer
+ * shear with lambda*di + dj > 0 for every dependence vector of the mask
+ * (Sec. III-B, Eq. 6-7).  Also writes *lambda_out when non-NULL.
+ * Errors: WF_E_INVALID for H < 1, W < 1, an unknown mask or a NULL n_steps;
+ * WF_E_UNSUPPORTED when W < lambda (Thm. 1 needs W >= lambda for optimality).
+ */
+int wf_schedule(int32_t H, int32_t W, int32_t mask, int32_t *step_of,
+                int32_t *n_steps, int32_t *lambda_out);
+
+/*
+ * Validate a description without touching the GPU.  Returns WF_OK or the
+ * error wf_plan would return for it before allocating anything.
+ */
+int wf_validate(const wf_desc *desc);
+
+/*
+ * Build a plan: schedule and step lists, weights repacked into the kernels'
+ * tile layouts on the device, the scale table, the workspace, and (for the
+ * graph driver) the instantiated graph.  Synchronous; uses the current HIP
+ * device.  On success *out owns all of it until wf_plan_destroy.
+ */
+int wf_plan(const wf_desc *desc, wf_plan_t *out);
+
+/* Copy the plan's schedule out (HOST array of H*W int32) and step count. */
+int wf_plan_schedule(wf_plan_t plan, int32_t *step_of, int32_t *n_steps);
+
+/*
+ * Decode: for every step t = 0..T-1 and every latent on wavefront t, compute
+ * the parameters from the already written y_hat and write
+ * y_hat = (float)sym + mean.
+ *   psi [B][H][W][2M] DEVICE fp32 hyperprior parameters
+ *   sym [B][H][W][M]  DEVICE int32 symbols
+ * Asynchronous on `stream`; one call in flight per plan (the plan's
+ * workspace is shared by its calls).
+ */
+int wf_decode(wf_plan_t plan, const float *psi, const int32_t *sym,
+              const wf_out *out, hipStream_t stream);
+
+/*
+ * Encode: as decode, but the symbol is sym_out = rint(y - mean) (fp32
+ * subtract, round half to even) and y_hat = (float)sym_out + mean.
+ *   y       [B][H][W][M] DEVICE fp32 latents
+ *   sym_out [B][H][W][M] DEVICE int32
+ */
+int wf_encode(wf_plan_t plan, const float *psi, const float *y, int32_t *sym_out,
+              const wf_out *out, hipStream_t stream);
+
+/*
+ * Wait for `stream` and report a device-side error recorded by the plan's
+ * kernels (WF_E_TIMEOUT when a bounded device-wide wait gave up).  Clears the
+ * recorded error.
+ */
+int wf_plan_sync(wf_plan_t plan, hipStream_t stream);
+
+/* Release everything the plan owns.  NULL is ignored. */
+void wf_plan_destroy(wf_plan_t plan);
+
+/* Message of the last failed call on this thread ("" if none). */
+const char *wf_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* WF_H */

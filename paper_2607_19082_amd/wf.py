@@ -1,0 +1,213 @@
+"""Python binding of libwf (ctypes): argument marshalling only.
+
+Every step of the decode/encode runs in the library's HIP kernels; this module
+only checks tensor shapes/dtypes/devices and passes raw device pointers and the
+current HIP stream.  It raises if the library is missing; there is no fallback.
+"""
+import ctypes
+import os
+
+import numpy as np
+
+_PKG = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_PKG, "libwf.so")
+
+WF_OK, WF_E_INVALID, WF_E_UNSUPPORTED, WF_E_HIP, WF_E_NOMEM, WF_E_TIMEOUT = 0, -1, -2, -3, -4, -5
+MASK = {"full": 0, "relaxed": 1}
+PRECISION = {"fp32": 0, "bf16": 1}
+DRIVER = {"stream": 0, "graph": 1, "persistent": 2}
+
+EXPORTS = ["wf_schedule", "wf_validate", "wf_plan", "wf_plan_schedule", "wf_decode",
+           "wf_encode", "wf_plan_sync", "wf_plan_destroy", "wf_last_error"]
+
+
+class WfError(RuntimeError):
+    def __init__(self, code, msg):
+        super().__init__(f"libwf error {code}: {msg}")
+        self.code = code
+
+
+class Desc(ctypes.Structure):
+    _fields_ = [
+        ("H", ctypes.c_int32), ("W", ctypes.c_int32), ("M", ctypes.c_int32),
+        ("B", ctypes.c_int32), ("K", ctypes.c_int32),
+        ("d1", ctypes.c_int32), ("d2", ctypes.c_int32),
+        ("mask", ctypes.c_int32), ("precision", ctypes.c_int32), ("driver", ctypes.c_int32),
+        ("lrelu_slope", ctypes.c_float),
+        ("ctx_w", ctypes.c_void_p), ("ctx_b", ctypes.c_void_p),
+        ("w1", ctypes.c_void_p), ("b1", ctypes.c_void_p),
+        ("w2", ctypes.c_void_p), ("b2", ctypes.c_void_p),
+        ("w3", ctypes.c_void_p), ("b3", ctypes.c_void_p),
+        ("scale_table", ctypes.c_void_p), ("L", ctypes.c_int32),
+    ]
+
+
+class Out(ctypes.Structure):
+    _fields_ = [
+        ("y_hat", ctypes.c_void_p), ("mean", ctypes.c_void_p), ("scale", ctypes.c_void_p),
+        ("idx", ctypes.c_void_p), ("weight", ctypes.c_void_p), ("comp_mean", ctypes.c_void_p),
+    ]
+
+
+_lib = None
+
+
+def lib():
+    """Load libwf.so (raises if it has not been built)."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise RuntimeError(f"{LIB_PATH} is missing: build it with paper_2607_19082_amd.build.build()")
+        L = ctypes.CDLL(LIB_PATH)
+        P = ctypes.c_void_p
+        L.wf_schedule.argtypes = [ctypes.c_int32, ctypes.c_int32, ctypes.c_int32, P, P, P]
+        L.wf_validate.argtypes = [ctypes.POINTER(Desc)]
+        L.wf_plan.argtypes = [ctypes.POINTER(Desc), ctypes.POINTER(ctypes.c_void_p)]
+        L.wf_plan_schedule.argtypes = [P, P, P]
+        L.wf_decode.argtypes = [P, P, P, ctypes.POINTER(Out), P]
+        L.wf_encode.argtypes = [P, P, P, P, ctypes.POINTER(Out), P]
+        L.wf_plan_sync.argtypes = [P, P]
+        L.wf_plan_destroy.argtypes = [P]
+        L.wf_plan_destroy.restype = None
+        L.wf_last_error.restype = ctypes.c_char_p
+        for name in EXPORTS[:-2]:
+            getattr(L, name).restype = ctypes.c_int
+        _lib = L
+    return _lib
+
+
+def _check(rc):
+    if rc != WF_OK:
+        raise WfError(rc, lib().wf_last_error().decode())
+
+
+def schedule(H, W, mask="full"):
+    """(step_of [H][W] int32, n_steps, lambda) from the library's host planner."""
+    step = np.zeros((H, W), np.int32)
+    n = ctypes.c_int32()
+    lam = ctypes.c_int32()
+    _check(lib().wf_schedule(H, W, MASK[mask], step.ctypes.data, ctypes.byref(n), ctypes.byref(lam)))
+    return step, n.value, lam.value
+
+
+def make_desc(weights, table, H, W, B=1, K=1, mask="full", precision="fp32", driver="stream",
+              slope=0.01):
+    """Build a Desc plus the host arrays it points to (keep both alive)."""
+    arrs = {k: np.ascontiguousarray(v, dtype=np.float32) for k, v in weights.items()}
+    arrs["table"] = np.ascontiguousarray(table, dtype=np.float32)
+    M = arrs["ctx_w"].shape[1]
+    d = Desc(H, W, M, B, K, arrs["w1"].shape[0], arrs["w2"].shape[0], MASK[mask],
+             PRECISION[precision], DRIVER[driver], slope,
+             arrs["ctx_w"].ctypes.data, arrs["ctx_b"].ctypes.data,
+             arrs["w1"].ctypes.data, arrs["b1"].ctypes.data,
+             arrs["w2"].ctypes.data, arrs["b2"].ctypes.data,
+             arrs["w3"].ctypes.data, arrs["b3"].ctypes.data,
+             arrs["table"].ctypes.data, len(arrs["table"]))
+    return d, arrs
+
+
+def validate(desc):
+    return lib().wf_validate(ctypes.byref(desc))
+
+
+def _stream_handle(stream):
+    import torch
+    s = stream if stream is not None else torch.cuda.current_stream()
+    return ctypes.c_void_p(s.cuda_stream)
+
+
+class Plan:
+    """A plan for one model and grid shape.  Inputs/outputs are torch tensors
+    on the current HIP device; calls are asynchronous on the given (default:
+    current) torch stream."""
+
+    def __init__(self, weights, table, H, W, B=1, K=1, mask="full", precision="fp32",
+                 driver="stream", slope=0.01):
+        self.desc, self._arrs = make_desc(weights, table, H, W, B, K, mask, precision, driver, slope)
+        self.H, self.W, self.B, self.K = H, W, B, K
+        self.M = self.desc.M
+        h = ctypes.c_void_p()
+        _check(lib().wf_plan(ctypes.byref(self.desc), ctypes.byref(h)))
+        self._h = h
+        self._arrs = None  # the plan holds device copies
+
+    def close(self):
+        if getattr(self, "_h", None):
+            lib().wf_plan_destroy(self._h)
+            self._h = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+    def schedule(self):
+        step = np.zeros((self.H, self.W), np.int32)
+        n = ctypes.c_int32()
+        _check(lib().wf_plan_schedule(self._h, step.ctypes.data, ctypes.byref(n)))
+        return step, n.value
+
+    def alloc_out(self):
+        import torch
+        B, H, W, M, K = self.B, self.H, self.W, self.M, self.K
+        dev = torch.device("cuda", torch.cuda.current_device())
+        o = {
+            "y_hat": torch.empty((B, H, W, M), dtype=torch.float32, device=dev),
+            "mean": torch.empty((B, H, W, M), dtype=torch.float32, device=dev),
+            "scale": torch.empty((B, H, W, K, M), dtype=torch.float32, device=dev),
+            "idx": torch.empty((B, H, W, K, M), dtype=torch.int32, device=dev),
+        }
+        if K == 3:
+            o["weight"] = torch.empty((B, H, W, K, M), dtype=torch.float32, device=dev)
+            o["comp_mean"] = torch.empty((B, H, W, K, M), dtype=torch.float32, device=dev)
+        return o
+
+    def _check_tensor(self, t, shape, dtype, name):
+        import torch
+        if not isinstance(t, torch.Tensor) or not t.is_cuda:
+            raise TypeError(f"{name} must be a CUDA (HIP) tensor")
+        if t.dtype != dtype or tuple(t.shape) != tuple(shape) or not t.is_contiguous():
+            raise ValueError(f"{name}: expected contiguous {dtype} {tuple(shape)}, got {t.dtype} {tuple(t.shape)}")
+        return ctypes.c_void_p(t.data_ptr())
+
+    def _out_struct(self, out):
+        import torch
+        B, H, W, M, K = self.B, self.H, self.W, self.M, self.K
+        f = torch.float32
+        ptrs = [self._check_tensor(out["y_hat"], (B, H, W, M), f, "y_hat"),
+                self._check_tensor(out["mean"], (B, H, W, M), f, "mean"),
+                self._check_tensor(out["scale"], (B, H, W, K, M), f, "scale"),
+                self._check_tensor(out["idx"], (B, H, W, K, M), torch.int32, "idx")]
+        if K == 3:
+            ptrs += [self._check_tensor(out["weight"], (B, H, W, K, M), f, "weight"),
+                     self._check_tensor(out["comp_mean"], (B, H, W, K, M), f, "comp_mean")]
+        else:
+            ptrs += [None, None]
+        return Out(*[p.value if p is not None else None for p in ptrs])
+
+    def decode(self, psi, sym, out=None, stream=None):
+        import torch
+        B, H, W, M = self.B, self.H, self.W, self.M
+        out = out if out is not None else self.alloc_out()
+        p_psi = self._check_tensor(psi, (B, H, W, 2 * M), torch.float32, "psi")
+        p_sym = self._check_tensor(sym, (B, H, W, M), torch.int32, "sym")
+        o = self._out_struct(out)
+        _check(lib().wf_decode(self._h, p_psi, p_sym, ctypes.byref(o), _stream_handle(stream)))
+        return out
+
+    def encode(self, psi, y, out=None, sym_out=None, stream=None):
+        import torch
+        B, H, W, M = self.B, self.H, self.W, self.M
+        out = out if out is not None else self.alloc_out()
+        if sym_out is None:
+            sym_out = torch.empty((B, H, W, M), dtype=torch.int32, device=y.device)
+        p_psi = self._check_tensor(psi, (B, H, W, 2 * M), torch.float32, "psi")
+        p_y = self._check_tensor(y, (B, H, W, M), torch.float32, "y")
+        p_s = self._check_tensor(sym_out, (B, H, W, M), torch.int32, "sym_out")
+        o = self._out_struct(out)
+        _check(lib().wf_encode(self._h, p_psi, p_y, p_s, ctypes.byref(o), _stream_handle(stream)))
+        return out, sym_out
+
+    def sync(self, stream=None):
+        _check(lib().wf_plan_sync(self._h, _stream_handle(stream)))

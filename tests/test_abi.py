@@ -1,0 +1,127 @@
+"""Host-side checks of the C-ABI library (no GPU needed).
+
+The library must load, export every function that include/wf.h declares,
+produce the same schedule as the brute-force schedule oracle (bit-exact), and
+reject bad descriptions with the documented status codes before touching the
+GPU.
+"""
+import ctypes
+import os
+import re
+
+import numpy as np
+import pytest
+
+from oracle import schedule as S
+from paper_2607_19082_amd import inputs, wf
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+@pytest.fixture(scope="module")
+def lib():
+    if not os.path.exists(wf.LIB_PATH):
+        from paper_2607_19082_amd import build
+        build.build()
+    return wf.lib()
+
+
+def declared_functions():
+    src = open(os.path.join(ROOT, "include", "wf.h")).read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    return sorted(set(re.findall(r"^\s*(?:int|void|const char\s*\*)\s*\*?\s*(wf_\w+)\s*\(", src, flags=re.M)))
+
+
+def test_exports_every_declared_symbol(lib):
+    names = declared_functions()
+    assert len(names) >= 9
+    for n in names:
+        assert hasattr(lib, n), n
+    assert sorted(wf.EXPORTS) == names
+
+
+@pytest.mark.parametrize("mask,relaxed,lam", [("full", False, 3), ("relaxed", True, 2)])
+def test_schedule_matches_oracle(lib, mask, relaxed, lam):
+    ds = S.dependence_vectors(5, relaxed=relaxed)
+    for H in range(1, 10):
+        for W in range(lam, 12):
+            step, n, got_lam = wf.schedule(H, W, mask)
+            assert got_lam == lam
+            asap = np.array(S.asap_levels(H, W, ds), np.int32)
+            assert np.array_equal(step, asap)
+            assert n == S.critical_path_steps(H, W, ds) == W + lam * (H - 1)
+
+
+@pytest.mark.parametrize("H,W,mask", [(135, 240, "full"), (68, 120, "relaxed"), (32, 48, "full")])
+def test_schedule_workload_sizes(lib, H, W, mask):
+    step, n, lam = wf.schedule(H, W, mask)
+    assert n == W + lam * (H - 1)
+    assert n == {(135, 240): 642, (68, 120): 254, (32, 48): 141}[(H, W)]
+    # every edge of the DAG goes forward in time (vectorised Eq. 4 check)
+    for di, dj in S.dependence_vectors(5, relaxed=(mask == "relaxed")):
+        if dj > 0:
+            a, b = step[di:, dj:], step[:H - di, :W - dj]
+        elif dj < 0:
+            a, b = step[di:, :W + dj], step[:H - di, -dj:]
+        else:
+            a, b = step[di:, :], step[:H - di, :]
+        assert np.all(a > b)
+
+
+def test_schedule_errors(lib):
+    n = ctypes.c_int32()
+    assert lib.wf_schedule(0, 5, 0, None, ctypes.byref(n), None) == wf.WF_E_INVALID
+    assert lib.wf_schedule(5, 5, 7, None, ctypes.byref(n), None) == wf.WF_E_INVALID
+    assert lib.wf_schedule(5, 5, 0, None, None, None) == wf.WF_E_INVALID
+    assert lib.wf_schedule(5, 2, 0, None, ctypes.byref(n), None) == wf.WF_E_UNSUPPORTED
+    assert lib.wf_schedule(5, 1, 1, None, ctypes.byref(n), None) == wf.WF_E_UNSUPPORTED
+    assert lib.wf_schedule(5, 2, 1, None, ctypes.byref(n), None) == wf.WF_OK
+    assert b"shear" in lib.wf_last_error()
+
+
+def _desc(**kw):
+    M = kw.pop("M", 16)
+    K = kw.get("K", 1)
+    w = inputs.make_weights(M, K)
+    base = dict(H=4, W=5, B=1, K=K)
+    base.update(kw)
+    return wf.make_desc(w, inputs.scale_table(), **base)
+
+
+def test_validate(lib):
+    d, keep = _desc()
+    assert wf.validate(d) == wf.WF_OK
+    d, keep = _desc(W=2)
+    assert wf.validate(d) == wf.WF_E_UNSUPPORTED
+    d, keep = _desc(M=8)
+    assert wf.validate(d) == wf.WF_E_UNSUPPORTED
+    d, keep = _desc()
+    d.K = 2
+    assert wf.validate(d) == wf.WF_E_INVALID
+    d, keep = _desc()
+    d.w2 = None
+    assert wf.validate(d) == wf.WF_E_INVALID
+    d, keep = _desc()
+    d.H = 0
+    assert wf.validate(d) == wf.WF_E_INVALID
+    d, keep = _desc()
+    d.mask = 3
+    assert wf.validate(d) == wf.WF_E_INVALID
+    d, keep = _desc()
+    d.driver = 9
+    assert wf.validate(d) == wf.WF_E_INVALID
+    t = keep["table"]
+    t[5] = t[4]
+    assert wf.validate(d) == wf.WF_E_INVALID
+    assert lib.wf_validate(None) == wf.WF_E_INVALID
+    assert len(lib.wf_last_error()) > 0
+
+
+def test_null_arguments_rejected(lib):
+    out = wf.Out()
+    assert lib.wf_decode(None, None, None, ctypes.byref(out), None) == wf.WF_E_INVALID
+    assert lib.wf_encode(None, None, None, None, ctypes.byref(out), None) == wf.WF_E_INVALID
+    assert lib.wf_plan(None, None) == wf.WF_E_INVALID
+    assert lib.wf_plan_sync(None, None) == wf.WF_E_INVALID
+    assert lib.wf_plan_schedule(None, None, None) == wf.WF_E_INVALID
+    lib.wf_plan_destroy(None)

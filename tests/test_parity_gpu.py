@@ -1,0 +1,125 @@
+"""GPU parity: the HIP path (through the C-ABI) against the CPU oracle on the
+same seeded inputs.
+
+Global parity compares every output of a whole decode (and encode) with the
+oracle's sequential raster decode.  At the full workload sizes, where the
+oracle's whole decode is too slow for a test, the oracle's per-latent function
+is evaluated on the GPU's own final reconstruction at sampled latents
+(teacher-forced), which also catches any tap read before it was written.
+Bars: 1e-4 absolute on floats; symbols bit-exact; scale indices identical
+except scales within 1e-4 relative of a table level (counted).
+"""
+import sys
+
+import numpy as np
+import pytest
+
+from paper_2607_19082_amd import inputs, wf
+
+from gpu_helpers import (compare, gpu_plan, make_case, oracle_model, sample_latents,
+                         teacher_forced, to_np)
+
+pytestmark = pytest.mark.gpu
+
+torch = pytest.importorskip("torch")
+
+
+@pytest.fixture(scope="module", autouse=True)
+def device():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    wf.lib()  # fails loudly when the library is missing
+    torch.cuda.set_device(0)
+    return torch.device("cuda", 0)
+
+
+def log(msg):
+    print(msg, flush=True)
+    sys.stdout.flush()
+
+
+def run_decode(cfg, w, table, psi, sym, driver="stream", precision="fp32"):
+    plan = gpu_plan(cfg, w, table, driver, precision)
+    psi_d = torch.from_numpy(psi).cuda()
+    sym_d = torch.from_numpy(sym).cuda()
+    out = plan.decode(psi_d, sym_d)
+    plan.sync()
+    res = to_np(out)
+    plan.close()
+    return res
+
+
+def run_encode(cfg, w, table, psi, y, driver="stream", precision="fp32"):
+    plan = gpu_plan(cfg, w, table, driver, precision)
+    out, s = plan.encode(torch.from_numpy(psi).cuda(), torch.from_numpy(y).cuda())
+    plan.sync()
+    res, s = to_np(out), s.cpu().numpy()
+    plan.close()
+    return res, s
+
+
+SMALL = [
+    # (workload, H, W, B): ragged grids that span several 16-row tiles
+    ("minnen-16x16-m192", 7, 9, 1),
+    ("minnen-16x16-m192", 5, 3, 2),
+    ("cheng-gmm3-1080p-120x68-m192", 6, 11, 1),
+    ("minnen-relaxed-b8-120x68-m192", 5, 7, 3),
+    ("minnen-hr-4k-240x135-m320", 4, 10, 1),
+]
+
+
+@pytest.mark.parametrize("name,H,W,B", SMALL)
+def test_small_decode_encode(name, H, W, B):
+    log(f"case {name} H={H} W={W} B={B}")
+    cfg, w, table, psi, sym = make_case(name, H=H, W=W, B=B)
+    model = oracle_model(cfg, w, table)
+    ref = model.decode(psi, sym)
+    got = run_decode(cfg, w, table, psi, sym)
+    log(compare(got, ref, table, cfg["K"]))
+    u = inputs.make_noise(cfg["B"], cfg["H"], cfg["W"], cfg["M"])
+    y = inputs.encoder_input(sym, u, ref["mean"])
+    got_e, s = run_encode(cfg, w, table, psi, y)
+    assert np.array_equal(s, sym)
+    log(compare(got_e, ref, table, cfg["K"]))
+
+
+@pytest.mark.parametrize("name", ["minnen-16x16-m192", "minnen-kodak-48x32-m192"])
+def test_full_decode_encode(name):
+    log(f"case {name} full size")
+    cfg, w, table, psi, sym = make_case(name)
+    model = oracle_model(cfg, w, table)
+    ref = model.decode(psi, sym)
+    got = run_decode(cfg, w, table, psi, sym)
+    log(compare(got, ref, table, cfg["K"]))
+    u = inputs.make_noise(cfg["B"], cfg["H"], cfg["W"], cfg["M"])
+    y = inputs.encoder_input(sym, u, ref["mean"])
+    got_e, s = run_encode(cfg, w, table, psi, y)
+    assert np.array_equal(s, sym)
+    log(compare(got_e, ref, table, cfg["K"]))
+
+
+@pytest.mark.parametrize("name,H,W,B", [
+    ("cheng-gmm3-1080p-120x68-m192", 14, 24, 1),
+    ("minnen-relaxed-b8-120x68-m192", 9, 16, 8),
+    ("minnen-hr-4k-240x135-m320", 9, 20, 1),
+])
+def test_reduced_global(name, H, W, B):
+    log(f"case {name} reduced H={H} W={W} B={B}")
+    cfg, w, table, psi, sym = make_case(name, H=H, W=W, B=B)
+    ref = oracle_model(cfg, w, table).decode(psi, sym)
+    got = run_decode(cfg, w, table, psi, sym)
+    log(compare(got, ref, table, cfg["K"]))
+
+
+@pytest.mark.parametrize("name,n", [
+    ("cheng-gmm3-1080p-120x68-m192", 600),
+    ("minnen-relaxed-b8-120x68-m192", 600),
+    ("minnen-hr-4k-240x135-m320", 300),
+])
+def test_full_size_teacher_forced(name, n):
+    log(f"case {name} full size, teacher-forced sample of {n}")
+    cfg, w, table, psi, sym = make_case(name)
+    got = run_decode(cfg, w, table, psi, sym)
+    model = oracle_model(cfg, w, table)
+    lats = sample_latents(cfg, n)
+    log(teacher_forced(cfg, got, psi, sym, model, lats, table))
