@@ -55,7 +55,7 @@ def main():
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--workload", default="minnen-hr-4k-240x135-m320")
-    ap.add_argument("--driver", default="stream", choices=["stream", "graph", "persistent"])
+    ap.add_argument("--driver", default="graph", choices=["stream", "graph", "persistent"])
     ap.add_argument("--precision", default="fp32", choices=["fp32", "bf16"])
     ap.add_argument("--cpu-rows", type=int, default=8, help="rows of the CPU-oracle sample (0: skip)")
     args = ap.parse_args()

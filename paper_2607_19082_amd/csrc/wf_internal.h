@@ -12,57 +12,63 @@
 namespace wf {
 
 constexpr int kMaxTaps = 12;
+constexpr int kMaxNew = 2;           // taps written by the immediately preceding step
 constexpr int kTile = 16;            // MFMA tile edge (rows and columns)
 constexpr int kMaxTable = 256;
+constexpr int kXcds = 8;             // accelerator complex dies of an MI355X
+constexpr int kBarrierWords = 512;   // barrier counters of the persistent driver
 
 // Set the calling thread's error message and return `code`.
 int fail(int code, const std::string& msg);
 
-// Rows of one wavefront step: B images x n latents each.  Row r belongs to
-// image r / n and to grid position order[ptr + r % n].
-struct StepRows {
-    int n;
-    int ptr;
-    int nrows;
-};
-
-// One batched product of a step: out[r][col] += sum_k A[r][k] * Wt[k][col]
-// over the k-range of this launch's z-slice.  A is produced on the fly from
-// one of three sources (see ASource).
-enum ASource { A_TAPS = 0, A_PSI_CTX = 1, A_HIDDEN = 2 };
-
-struct GemmArgs {
-    const float* wp;        // packed weights [Np/16][Kp/16][64 lanes][4]
-    int nkb;                // Kp / 16
-    int kb_per_split;       // k-blocks per z-slice
-    float* out;             // raw fp32 sums [rows][ldo], accumulated atomically
-    int ldo;
-    const float* y_hat;     // A_TAPS source, NHWC [B][H][W][M]
-    const float* psi;       // A_PSI_CTX first half, [B][H][W][2M]
-    const float* in;        // dense raw input [rows][ldi] (ctx or hidden sums)
-    int ldi;
-    const float* in_bias;   // added to `in` on load (padded with zeros)
-    float slope;            // LeakyReLU slope applied on load (A_HIDDEN)
-    int H, W, M;
-    const int* order;       // grid positions of all steps, step-major
-    int dy[kMaxTaps], dx[kMaxTaps];
-};
-
-struct EpiArgs {
-    float* o;               // raw last-layer sums [rows][ldo]; cleared after reading
-    int ldo;
-    const float* b3;        // [n3]
-    const float* table;     // [L]
-    int L, M, K, H, W;
-    const int* order;
+// Pointers of one decode/encode call.  They live in plan-owned device memory
+// and are written by a one-thread kernel before the step kernels run, so a
+// captured graph of step kernels serves every call.
+struct CallPtrs {
+    const float* psi;       // [B][H][W][2M]
     const int32_t* sym;     // decode input
     const float* y;         // encode input
     int32_t* sym_out;       // encode output
-    int encode;
     float *y_hat, *mean, *scale, *weight, *cmean;
     int32_t* idx;
-    float* clr[3];          // raw buffers to clear for the next step
-    int clr_ld[3];
+    int encode;
+};
+
+// Plan constants passed by value to every step kernel.
+//
+// Taps are split by age.  A tap (dy,dx) of the latent decoded at step t was
+// written at step t - delta with delta = lambda*(-dy) - dx.  The "new" taps
+// (delta = 1) are gathered on the critical path; every "old" tap (delta >= 2)
+// is pushed forward by its producer one step after the producer is decoded:
+// slot[o] of the consumer receives (W1[:, 2M:] . Wc[tap o]) . y_hat[producer],
+// i.e. the old tap's share of layer 1 (the context conv and the context half
+// of layer 1 are both linear, so their product is folded at plan time).
+struct StepArgs {
+    int H, W, M, B, K, L, lambda;
+    int Np1, Np2, n3;
+    int n_new, n_old, nring;
+    int new_dy[kMaxNew], new_dx[kMaxNew];
+    int old_dy[kMaxTaps], old_dx[kMaxTaps], old_delta[kMaxTaps];
+    float slope;
+    const int* order;       // grid positions of all steps, step-major, by row
+    const int* step_ptr;    // [T]
+    const int* step_n;      // [T] latents per image on the step
+    const int* step_i0;     // [T] first grid row on the step
+    const float* wp_hoist;  // packed W1[:, :2M]                      [Np1/16][2M/16]
+    const float* b_hoist;   // b1 + W1[:, 2M:] . bc                    [Np1]
+    const float* wp_new;    // packed folded weights of the new taps   [Np1/16][n_new*M/16]
+    const float* wp_old;    // packed folded weights of the old taps   [n_old*Np1/16][M/16]
+    const float* wp2;       // packed W2                               [Np2/16][Np1/16]
+    const float* b2;        // [Np2]
+    const float* wp3;       // packed W3                               [n3/16][Np2/16]
+    const float* b3;        // [n3]
+    const float* table;     // [L]
+    float* p1;              // [B*H*W][Np1] hoisted layer-1 part
+    float* h1;              // [max_rows][Np1]
+    float* h2;              // [max_rows][Np2]
+    float* slots;           // [nring][max_rows][n_old][Np1]
+    int max_rows;
+    const CallPtrs* cp;
 };
 
 struct Plan {
@@ -73,22 +79,35 @@ struct Plan {
     int lambda, T, ntaps;
     int dy[kMaxTaps], dx[kMaxTaps];
     std::vector<int32_t> step_of;        // [H*W]
-    std::vector<int> step_ptr, step_n;   // [T]
+    std::vector<int> step_ptr, step_n, step_i0;   // [T]
     int max_rows;
-    // padded widths
     int Np1, Np2;                        // d1, d2 rounded up to 16
-    // device memory
-    int device;
-    int* d_order = nullptr;
-    float *d_wc = nullptr, *d_w1 = nullptr, *d_w2 = nullptr, *d_w3 = nullptr;
-    float *d_bc = nullptr, *d_b1 = nullptr, *d_b2 = nullptr, *d_b3 = nullptr;
-    float* d_table = nullptr;
-    float *d_ctx = nullptr, *d_h1 = nullptr, *d_h2 = nullptr, *d_o = nullptr;
+    StepArgs args;                       // device pointers filled in
+    // device memory owned by the plan
+    int device = 0;
+    std::vector<void*> owned;
+    CallPtrs* d_call = nullptr;
     int* d_err = nullptr;
+    // persistent driver
+    unsigned* d_bar = nullptr;
+    int grid = 0;
+    long long spin_budget = 100000000;   // wall-clock ticks (100 MHz): 1 s
+    // graph driver
+    hipStream_t cap_stream = nullptr;
+    hipGraph_t graph = nullptr;
+    hipGraphExec_t graph_exec = nullptr;
 };
 
-// Launch every kernel of one decode/encode call on `stream` (per-step driver).
-int run_steps(Plan& p, const float* psi, const int32_t* sym, const float* y,
-              int32_t* sym_out, const wf_out* out, hipStream_t stream);
+// Enqueue the kernels of one call after its pointers were published to
+// p.d_call (used directly by the stream driver and captured by the graph
+// driver).
+int enqueue_steps(Plan& p, hipStream_t stream);
+// Publish the call's pointers to p.d_call on `stream`.
+int enqueue_set_call(Plan& p, const CallPtrs& c, hipStream_t stream);
+// The pre-loop product of the hyperprior half of layer 1.
+int enqueue_hoist(Plan& p, hipStream_t stream);
+// Persistent driver: grid size (checked co-residency) and one call.
+int persistent_grid(Plan& p, int* grid);
+int enqueue_persistent(Plan& p, hipStream_t stream);
 
 }  // namespace wf

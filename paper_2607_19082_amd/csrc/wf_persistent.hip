@@ -1,0 +1,120 @@
+// Persistent driver: one cooperative launch runs every wavefront step; the
+// three phases of a step are separated by a device-wide barrier instead of
+// kernel boundaries.  Each workgroup loops over the jobs of a phase with a
+// stride of the grid size (a multiple of 8, so a job's XCD placement is the
+// same as in the per-step kernels), and all data that crosses workgroups
+// inside the launch (h1, h2, y_hat, pushed slots) moves through agent-coherent
+// (sc1) buffer accesses.
+#include "wf_device.h"
+
+namespace wf {
+
+// Two-level barrier: the workgroups of residue class x = block % 8 count into
+// counter x; the last of them bumps the top counter, which every workgroup
+// waits on.  Counters only grow: barrier k completes when the top counter
+// reaches k * (number of classes).  A wait longer than `budget` wall-clock
+// ticks records WF_E_TIMEOUT in *err; every workgroup that sees a recorded
+// error leaves the kernel at its next barrier, so the grid always drains.
+__device__ __forceinline__ bool grid_barrier(unsigned* ctr, unsigned k, int* err, long long budget,
+                                             int* bail) {
+    __builtin_amdgcn_s_waitcnt(0);  // this wave's coherent stores have landed
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        const unsigned G = gridDim.x;
+        const unsigned x = blockIdx.x % kXcds;
+        const unsigned ng = G < (unsigned)kXcds ? G : (unsigned)kXcds;
+        const unsigned per = (G - x + kXcds - 1) / kXcds;
+        const unsigned old = __hip_atomic_fetch_add(ctr + 32 * (1 + x), 1u, __ATOMIC_RELAXED,
+                                                    __HIP_MEMORY_SCOPE_AGENT);
+        if (old + 1 == k * per) __hip_atomic_fetch_add(ctr, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        int flag = 0;
+        const long long t0 = wall_clock64();
+        unsigned it = 0;
+        while (__hip_atomic_load(ctr, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) < k * ng) {
+            if ((++it & 255u) == 0) {
+                if (__hip_atomic_load(err, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) != 0) {
+                    flag = 1;
+                    break;
+                }
+                if (wall_clock64() - t0 > budget) {
+                    __hip_atomic_store(err, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                    flag = 1;
+                    break;
+                }
+            }
+        }
+        *bail = flag;
+    }
+    __syncthreads();
+    return *bail == 0;
+}
+
+template <int KC>
+__global__ __launch_bounds__(256) void k_persistent(StepArgs a, int T, unsigned* ctr, int* err,
+                                                    long long budget) {
+    __shared__ f4 red[kWaves][64];
+    __shared__ L3Smem<KC> sm;
+    __shared__ int bail;
+    for (int l = threadIdx.x; l < a.L; l += blockDim.x) sm.tab[l] = a.table[l];
+    __syncthreads();
+    const int G = gridDim.x;
+    unsigned k = 0;
+    StepRows prev{0, 0, 0, 0};
+    for (int t = 0; t < T; ++t) {
+        const StepRows s = step_rows(a.H, a.W, a.B, a.lambda, t);
+        const int nb1 = phase_a_l1_blocks(a, s);
+        const int nbp = t >= 1 ? phase_a_push_blocks(a, prev, T) : 0;
+        for (int b = blockIdx.x; b < nb1 + nbp; b += G) {
+            if (b >= nb1)
+                push_job<true>(a, prev, b - nb1);
+            else
+                l1_job<true>(a, s, b, red);
+        }
+        if (!grid_barrier(ctr, ++k, err, budget, &bail)) return;
+        const int nb2 = phase_b_blocks(a, s);
+        for (int b = blockIdx.x; b < nb2; b += G) l2_job<true>(a, s, b, red);
+        if (!grid_barrier(ctr, ++k, err, budget, &bail)) return;
+        const int nb3 = phase_c_blocks(a, s);
+        for (int b = blockIdx.x; b < nb3; b += G) l3_job<KC, true>(a, s, b, sm);
+        if (!grid_barrier(ctr, ++k, err, budget, &bail)) return;
+        prev = s;
+    }
+}
+
+__global__ void k_zero_u32(unsigned* p, int n) {
+    for (int i = threadIdx.x; i < n; i += blockDim.x) p[i] = 0u;
+}
+
+static const void* persistent_fn(int K) {
+    return K == 1 ? (const void*)k_persistent<1> : (const void*)k_persistent<3>;
+}
+
+// Grid size of the persistent kernel: one workgroup per CU, rounded down to a
+// multiple of 8 (XCD placement), if that many are co-resident.
+int persistent_grid(Plan& p, int* grid) {
+    int dev = 0, cus = 0, per_cu = 0;
+    hipError_t e = hipGetDevice(&dev);
+    if (e == hipSuccess) e = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);
+    if (e == hipSuccess)
+        e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, persistent_fn(p.K), 256, 0);
+    if (e != hipSuccess) return fail(WF_E_HIP, std::string("occupancy query: ") + hipGetErrorString(e));
+    if (per_cu < 1 || cus < kXcds) return fail(WF_E_UNSUPPORTED, "persistent kernel cannot be resident");
+    *grid = cus / kXcds * kXcds;
+    return WF_OK;
+}
+
+int enqueue_persistent(Plan& p, hipStream_t stream) {
+    enqueue_hoist(p, stream);
+    hipLaunchKernelGGL(k_zero_u32, dim3(1), dim3(256), 0, stream, p.d_bar, kBarrierWords);
+    StepArgs a = p.args;
+    int T = p.T;
+    unsigned* ctr = p.d_bar;
+    int* err = p.d_err;
+    long long budget = p.spin_budget;
+    void* args[] = {&a, &T, &ctr, &err, &budget};
+    hipError_t e = hipLaunchCooperativeKernel(persistent_fn(p.K), dim3(p.grid), dim3(256), args, 0, stream);
+    if (e != hipSuccess) return fail(WF_E_HIP, std::string("cooperative launch: ") + hipGetErrorString(e));
+    return WF_OK;
+}
+
+}  // namespace wf

@@ -84,7 +84,6 @@ static int check_desc(const wf_desc* d) {
     if (lat * 2 * d->M > (1LL << 31) - 1 || lat * 3 * d->M > (1LL << 31) - 1)
         return fail(WF_E_UNSUPPORTED, "problem too large for 32-bit element indexing");
     if (d->precision == WF_BF16) return fail(WF_E_UNSUPPORTED, "bf16 operands are not built yet");
-    if (d->driver != WF_DRIVER_STREAM) return fail(WF_E_UNSUPPORTED, "driver not built yet");
     return WF_OK;
 }
 
@@ -111,19 +110,50 @@ static std::vector<float> pack_panel(int K, int N, F wt) {
 }
 
 template <class T>
-static int upload(T** dst, const T* src, size_t n) {
+static int upload(Plan* p, T** dst, const T* src, size_t n) {
     WF_HIP(hipMalloc((void**)dst, n * sizeof(T)));
+    p->owned.push_back((void*)*dst);
     WF_HIP(hipMemcpy(*dst, src, n * sizeof(T), hipMemcpyHostToDevice));
+    return WF_OK;
+}
+
+template <class T>
+static int alloc(Plan* p, T** dst, size_t n) {
+    WF_HIP(hipMalloc((void**)dst, n * sizeof(T)));
+    p->owned.push_back((void*)*dst);
     return WF_OK;
 }
 
 static void free_plan(Plan* p) {
     if (!p) return;
-    void* ptrs[] = {p->d_order, p->d_wc, p->d_w1, p->d_w2, p->d_w3, p->d_bc, p->d_b1,
-                    p->d_b2, p->d_b3, p->d_table, p->d_ctx, p->d_h1, p->d_h2, p->d_o, p->d_err};
-    for (void* q : ptrs)
+    if (p->graph_exec) (void)hipGraphExecDestroy(p->graph_exec);
+    if (p->graph) (void)hipGraphDestroy(p->graph);
+    if (p->cap_stream) (void)hipStreamDestroy(p->cap_stream);
+    for (void* q : p->owned)
         if (q) (void)hipFree(q);
     delete p;
+}
+
+// Folded layer-1 weights of one tap: F[c][n] = sum_o W1[n][2M + o] * Wc[o][c][tap]
+// (fp64 accumulation), for c < M, n < d1.
+static void fold_tap(const wf_desc* d, int dy, int dx, std::vector<double>& out) {
+    const int M = d->M, d1 = d->d1;
+    std::vector<double> wc((size_t)2 * M * M);
+    for (int o = 0; o < 2 * M; ++o)
+        for (int c = 0; c < M; ++c)
+            wc[(size_t)o * M + c] = d->ctx_w[(((size_t)o * M + c) * 5 + (dy + 2)) * 5 + (dx + 2)];
+    out.assign((size_t)M * d1, 0.0);
+    std::vector<double> acc(M);
+    for (int n = 0; n < d1; ++n) {
+        std::fill(acc.begin(), acc.end(), 0.0);
+        const float* w1b = d->w1 + (size_t)n * 4 * M + 2 * M;
+        for (int o = 0; o < 2 * M; ++o) {
+            const double w = w1b[o];
+            const double* row = &wc[(size_t)o * M];
+            for (int c = 0; c < M; ++c) acc[c] += w * row[c];
+        }
+        for (int c = 0; c < M; ++c) out[(size_t)c * d1 + n] = acc[c];
+    }
 }
 
 static int build_plan(const wf_desc* d, Plan* p) {
@@ -133,18 +163,20 @@ static int build_plan(const wf_desc* d, Plan* p) {
     p->L = d->L; p->slope = d->lrelu_slope;
     p->ntaps = mask_taps(d->mask, p->dy, p->dx);
     p->lambda = least_shear(p->ntaps, p->dy, p->dx);
-    const int H = p->H, W = p->W, M = p->M;
-    p->T = W + p->lambda * (H - 1);
+    const int H = p->H, W = p->W, M = p->M, lam = p->lambda;
+    p->T = W + lam * (H - 1);
 
     // Wavefront step lists: positions with lambda*i + j == t, by ascending row.
     p->step_of.resize((size_t)H * W);
     p->step_ptr.assign(p->T, 0);
     p->step_n.assign(p->T, 0);
+    p->step_i0.assign(p->T, H);
     for (int i = 0; i < H; ++i)
         for (int j = 0; j < W; ++j) {
-            int t = p->lambda * i + j;
+            int t = lam * i + j;
             p->step_of[(size_t)i * W + j] = t;
             p->step_n[t]++;
+            p->step_i0[t] = std::min(p->step_i0[t], i);
         }
     std::vector<int> order((size_t)H * W);
     int maxn = 0;
@@ -157,49 +189,135 @@ static int build_plan(const wf_desc* d, Plan* p) {
         std::vector<int> fill(p->T, 0);
         for (int i = 0; i < H; ++i)
             for (int j = 0; j < W; ++j) {
-                int t = p->lambda * i + j;
+                int t = lam * i + j;
                 order[p->step_ptr[t] + fill[t]++] = i * W + j;
             }
     }
     p->max_rows = p->B * maxn;
     p->Np1 = round16(p->d1);
     p->Np2 = round16(p->d2);
+    const int d1 = p->d1, Np1 = p->Np1;
+
+    StepArgs& a = p->args;
+    a = StepArgs{};
+    a.H = H; a.W = W; a.M = M; a.B = p->B; a.K = p->K; a.L = p->L; a.lambda = lam;
+    a.Np1 = Np1; a.Np2 = p->Np2; a.n3 = p->n3; a.slope = p->slope; a.max_rows = p->max_rows;
+
+    // Split the taps by age (delta = steps between producer and consumer).
+    int maxdelta = 0;
+    std::vector<int> new_taps, old_taps;
+    for (int k = 0; k < p->ntaps; ++k) {
+        const int delta = lam * (-p->dy[k]) - p->dx[k];
+        maxdelta = std::max(maxdelta, delta);
+        (delta == 1 ? new_taps : old_taps).push_back(k);
+    }
+    if ((int)new_taps.size() > kMaxNew) return fail(WF_E_UNSUPPORTED, "more than two taps of age one");
+    a.n_new = (int)new_taps.size();
+    a.n_old = (int)old_taps.size();
+    a.nring = maxdelta + 1;
+    for (int s = 0; s < a.n_new; ++s) {
+        a.new_dy[s] = p->dy[new_taps[s]];
+        a.new_dx[s] = p->dx[new_taps[s]];
+    }
+    for (int o = 0; o < a.n_old; ++o) {
+        a.old_dy[o] = p->dy[old_taps[o]];
+        a.old_dx[o] = p->dx[old_taps[o]];
+        a.old_delta[o] = lam * (-a.old_dy[o]) - a.old_dx[o];
+    }
 
     WF_HIP(hipGetDevice(&p->device));
     int rc;
-    if ((rc = upload(&p->d_order, order.data(), order.size())) != WF_OK) return rc;
+    int *d_order, *d_ptr, *d_n, *d_i0;
+    if ((rc = upload(p, &d_order, order.data(), order.size())) != WF_OK) return rc;
+    if ((rc = upload(p, &d_ptr, p->step_ptr.data(), p->step_ptr.size())) != WF_OK) return rc;
+    if ((rc = upload(p, &d_n, p->step_n.data(), p->step_n.size())) != WF_OK) return rc;
+    if ((rc = upload(p, &d_i0, p->step_i0.data(), p->step_i0.size())) != WF_OK) return rc;
+    a.order = d_order; a.step_ptr = d_ptr; a.step_n = d_n; a.step_i0 = d_i0;
 
-    // Context conv as a GEMM over the causal taps: k = tap*M + c, n = output channel.
-    const int Kc = p->ntaps * M;
-    auto wc = pack_panel(Kc, 2 * M, [&](int k, int n) {
-        int tap = k / M, c = k % M;
-        return d->ctx_w[(((size_t)n * M + c) * 5 + (p->dy[tap] + 2)) * 5 + (p->dx[tap] + 2)];
+    // Fold the context conv into the context half of layer 1, tap by tap.
+    std::vector<std::vector<double>> fold(p->ntaps);
+    for (int k = 0; k < p->ntaps; ++k) fold_tap(d, p->dy[k], p->dx[k], fold[k]);
+
+    auto w_hoist = pack_panel(2 * M, d1, [&](int k, int n) { return d->w1[(size_t)n * 4 * M + k]; });
+    std::vector<float> b_hoist(Np1, 0.0f);
+    for (int n = 0; n < d1; ++n) {
+        double acc = d->b1[n];
+        const float* w1b = d->w1 + (size_t)n * 4 * M + 2 * M;
+        for (int o = 0; o < 2 * M; ++o) acc += (double)w1b[o] * (double)d->ctx_b[o];
+        b_hoist[n] = (float)acc;
+    }
+    auto w_new = pack_panel(a.n_new * M, d1, [&](int k, int n) {
+        return (float)fold[new_taps[k / M]][(size_t)(k % M) * d1 + n];
     });
-    auto w1 = pack_panel(4 * M, p->d1, [&](int k, int n) { return d->w1[(size_t)n * 4 * M + k]; });
-    auto w2 = pack_panel(p->d1, p->d2, [&](int k, int n) { return d->w2[(size_t)n * p->d1 + k]; });
+    auto w_old = pack_panel(M, a.n_old * Np1, [&](int k, int col) {
+        const int o = col / Np1, n = col % Np1;
+        return n < d1 ? (float)fold[old_taps[o]][(size_t)k * d1 + n] : 0.0f;
+    });
+    fold.clear();
+    auto w2 = pack_panel(d1, p->d2, [&](int k, int n) { return d->w2[(size_t)n * d1 + k]; });
     auto w3 = pack_panel(p->d2, p->n3, [&](int k, int n) { return d->w3[(size_t)n * p->d2 + k]; });
-    if ((rc = upload(&p->d_wc, wc.data(), wc.size())) != WF_OK) return rc;
-    if ((rc = upload(&p->d_w1, w1.data(), w1.size())) != WF_OK) return rc;
-    if ((rc = upload(&p->d_w2, w2.data(), w2.size())) != WF_OK) return rc;
-    if ((rc = upload(&p->d_w3, w3.data(), w3.size())) != WF_OK) return rc;
-
-    std::vector<float> b1(p->Np1, 0.0f), b2(p->Np2, 0.0f);
-    std::copy(d->b1, d->b1 + p->d1, b1.begin());
+    std::vector<float> b2(p->Np2, 0.0f);
     std::copy(d->b2, d->b2 + p->d2, b2.begin());
-    if ((rc = upload(&p->d_bc, d->ctx_b, (size_t)2 * M)) != WF_OK) return rc;
-    if ((rc = upload(&p->d_b1, b1.data(), b1.size())) != WF_OK) return rc;
-    if ((rc = upload(&p->d_b2, b2.data(), b2.size())) != WF_OK) return rc;
-    if ((rc = upload(&p->d_b3, d->b3, (size_t)p->n3)) != WF_OK) return rc;
-    if ((rc = upload(&p->d_table, d->scale_table, (size_t)p->L)) != WF_OK) return rc;
+
+    float *f;
+    if ((rc = upload(p, &f, w_hoist.data(), w_hoist.size())) != WF_OK) return rc;
+    a.wp_hoist = f;
+    if ((rc = upload(p, &f, b_hoist.data(), b_hoist.size())) != WF_OK) return rc;
+    a.b_hoist = f;
+    if ((rc = upload(p, &f, w_new.data(), w_new.size())) != WF_OK) return rc;
+    a.wp_new = f;
+    if ((rc = upload(p, &f, w_old.data(), w_old.size())) != WF_OK) return rc;
+    a.wp_old = f;
+    if ((rc = upload(p, &f, w2.data(), w2.size())) != WF_OK) return rc;
+    a.wp2 = f;
+    if ((rc = upload(p, &f, b2.data(), b2.size())) != WF_OK) return rc;
+    a.b2 = f;
+    if ((rc = upload(p, &f, w3.data(), w3.size())) != WF_OK) return rc;
+    a.wp3 = f;
+    if ((rc = upload(p, &f, d->b3, (size_t)p->n3)) != WF_OK) return rc;
+    a.b3 = f;
+    if ((rc = upload(p, &f, d->scale_table, (size_t)p->L)) != WF_OK) return rc;
+    a.table = f;
 
     const size_t R = (size_t)p->max_rows;
-    WF_HIP(hipMalloc((void**)&p->d_ctx, R * 2 * M * sizeof(float)));
-    WF_HIP(hipMalloc((void**)&p->d_h1, R * p->Np1 * sizeof(float)));
-    WF_HIP(hipMalloc((void**)&p->d_h2, R * p->Np2 * sizeof(float)));
-    WF_HIP(hipMalloc((void**)&p->d_o, R * p->n3 * sizeof(float)));
-    WF_HIP(hipMalloc((void**)&p->d_err, sizeof(int)));
+    const size_t nlat = (size_t)p->B * H * W;
+    if ((rc = alloc(p, &a.h1, R * Np1)) != WF_OK) return rc;
+    if ((rc = alloc(p, &a.h2, R * p->Np2)) != WF_OK) return rc;
+    if ((rc = alloc(p, &a.p1, nlat * Np1)) != WF_OK) return rc;
+    if ((rc = alloc(p, &a.slots, (size_t)a.nring * R * std::max(1, a.n_old) * Np1)) != WF_OK) return rc;
+    if ((rc = alloc(p, &p->d_call, 1)) != WF_OK) return rc;
+    WF_HIP(hipMemset(p->d_call, 0, sizeof(CallPtrs)));
+    a.cp = p->d_call;
+    if ((rc = alloc(p, &p->d_err, 1)) != WF_OK) return rc;
     WF_HIP(hipMemset(p->d_err, 0, sizeof(int)));
+    if (p->driver == WF_DRIVER_PERSISTENT) {
+        // agent-coherent buffer accesses address at most 2 GiB per array
+        const size_t lim = (size_t)1 << 31;
+        if (nlat * M * sizeof(float) >= lim || R * Np1 * sizeof(float) >= lim ||
+            (size_t)a.nring * R * std::max(1, a.n_old) * Np1 * sizeof(float) >= lim)
+            return fail(WF_E_UNSUPPORTED, "an array exceeds 2 GiB (persistent driver)");
+        if ((rc = persistent_grid(*p, &p->grid)) != WF_OK) return rc;
+        if ((rc = alloc(p, &p->d_bar, kBarrierWords)) != WF_OK) return rc;
+        WF_HIP(hipMemset(p->d_bar, 0, kBarrierWords * sizeof(unsigned)));
+    }
     WF_HIP(hipDeviceSynchronize());
+
+    if (p->driver == WF_DRIVER_GRAPH) {
+        // Capture every kernel of one call once; calls only republish their
+        // pointers to d_call and replay the graph.
+        WF_HIP(hipStreamCreateWithFlags(&p->cap_stream, hipStreamNonBlocking));
+        WF_HIP(hipStreamBeginCapture(p->cap_stream, hipStreamCaptureModeThreadLocal));
+        int erc = enqueue_steps(*p, p->cap_stream);
+        hipGraph_t g = nullptr;
+        hipError_t e = hipStreamEndCapture(p->cap_stream, &g);
+        if (erc != WF_OK) {
+            if (g) (void)hipGraphDestroy(g);
+            return erc;
+        }
+        if (e != hipSuccess) return fail(WF_E_HIP, std::string("graph capture: ") + hipGetErrorString(e));
+        p->graph = g;
+        WF_HIP(hipGraphInstantiate(&p->graph_exec, p->graph, nullptr, nullptr, 0));
+    }
     return WF_OK;
 }
 
@@ -266,13 +384,33 @@ static int check_out(const Plan* p, const wf_out* out) {
     return WF_OK;
 }
 
+static int run_call(Plan* p, const CallPtrs& c, hipStream_t stream) {
+    int rc = enqueue_set_call(*p, c, stream);
+    if (rc != WF_OK) return rc;
+    if (p->driver == WF_DRIVER_GRAPH) {
+        WF_HIP(hipGraphLaunch(p->graph_exec, stream));
+        return WF_OK;
+    }
+    if (p->driver == WF_DRIVER_PERSISTENT) return enqueue_persistent(*p, stream);
+    return enqueue_steps(*p, stream);
+}
+
+static CallPtrs call_ptrs(const float* psi, const int32_t* sym, const float* y, int32_t* sym_out,
+                          const wf_out* out) {
+    CallPtrs c{};
+    c.psi = psi; c.sym = sym; c.y = y; c.sym_out = sym_out; c.encode = y != nullptr;
+    c.y_hat = out->y_hat; c.mean = out->mean; c.scale = out->scale; c.idx = out->idx;
+    c.weight = out->weight; c.cmean = out->comp_mean;
+    return c;
+}
+
 int wf_decode(wf_plan_t plan, const float* psi, const int32_t* sym, const wf_out* out,
               hipStream_t stream) {
     if (!plan || !psi || !sym) return fail(WF_E_INVALID, "plan, psi or sym is NULL");
     Plan* p = reinterpret_cast<Plan*>(plan);
     int rc = check_out(p, out);
     if (rc != WF_OK) return rc;
-    return run_steps(*p, psi, sym, nullptr, nullptr, out, stream);
+    return run_call(p, call_ptrs(psi, sym, nullptr, nullptr, out), stream);
 }
 
 int wf_encode(wf_plan_t plan, const float* psi, const float* y, int32_t* sym_out,
@@ -281,7 +419,7 @@ int wf_encode(wf_plan_t plan, const float* psi, const float* y, int32_t* sym_out
     Plan* p = reinterpret_cast<Plan*>(plan);
     int rc = check_out(p, out);
     if (rc != WF_OK) return rc;
-    return run_steps(*p, psi, nullptr, y, sym_out, out, stream);
+    return run_call(p, call_ptrs(psi, nullptr, y, sym_out, out), stream);
 }
 
 int wf_plan_sync(wf_plan_t plan, hipStream_t stream) {

@@ -68,32 +68,37 @@ SMALL = [
 ]
 
 
+DRIVERS = ["stream", "graph", "persistent"]
+
+
+@pytest.mark.parametrize("driver", DRIVERS)
 @pytest.mark.parametrize("name,H,W,B", SMALL)
-def test_small_decode_encode(name, H, W, B):
-    log(f"case {name} H={H} W={W} B={B}")
+def test_small_decode_encode(name, H, W, B, driver):
+    log(f"case {name} H={H} W={W} B={B} driver={driver}")
     cfg, w, table, psi, sym = make_case(name, H=H, W=W, B=B)
     model = oracle_model(cfg, w, table)
     ref = model.decode(psi, sym)
-    got = run_decode(cfg, w, table, psi, sym)
+    got = run_decode(cfg, w, table, psi, sym, driver)
     log(compare(got, ref, table, cfg["K"]))
     u = inputs.make_noise(cfg["B"], cfg["H"], cfg["W"], cfg["M"])
     y = inputs.encoder_input(sym, u, ref["mean"])
-    got_e, s = run_encode(cfg, w, table, psi, y)
+    got_e, s = run_encode(cfg, w, table, psi, y, driver)
     assert np.array_equal(s, sym)
     log(compare(got_e, ref, table, cfg["K"]))
 
 
+@pytest.mark.parametrize("driver", DRIVERS)
 @pytest.mark.parametrize("name", ["minnen-16x16-m192", "minnen-kodak-48x32-m192"])
-def test_full_decode_encode(name):
-    log(f"case {name} full size")
+def test_full_decode_encode(name, driver):
+    log(f"case {name} full size driver={driver}")
     cfg, w, table, psi, sym = make_case(name)
     model = oracle_model(cfg, w, table)
     ref = model.decode(psi, sym)
-    got = run_decode(cfg, w, table, psi, sym)
+    got = run_decode(cfg, w, table, psi, sym, driver)
     log(compare(got, ref, table, cfg["K"]))
     u = inputs.make_noise(cfg["B"], cfg["H"], cfg["W"], cfg["M"])
     y = inputs.encoder_input(sym, u, ref["mean"])
-    got_e, s = run_encode(cfg, w, table, psi, y)
+    got_e, s = run_encode(cfg, w, table, psi, y, driver)
     assert np.array_equal(s, sym)
     log(compare(got_e, ref, table, cfg["K"]))
 
@@ -103,11 +108,12 @@ def test_full_decode_encode(name):
     ("minnen-relaxed-b8-120x68-m192", 9, 16, 8),
     ("minnen-hr-4k-240x135-m320", 9, 20, 1),
 ])
-def test_reduced_global(name, H, W, B):
-    log(f"case {name} reduced H={H} W={W} B={B}")
+@pytest.mark.parametrize("driver", ["graph", "persistent"])
+def test_reduced_global(name, H, W, B, driver):
+    log(f"case {name} reduced H={H} W={W} B={B} driver={driver}")
     cfg, w, table, psi, sym = make_case(name, H=H, W=W, B=B)
     ref = oracle_model(cfg, w, table).decode(psi, sym)
-    got = run_decode(cfg, w, table, psi, sym)
+    got = run_decode(cfg, w, table, psi, sym, driver)
     log(compare(got, ref, table, cfg["K"]))
 
 
@@ -116,10 +122,36 @@ def test_reduced_global(name, H, W, B):
     ("minnen-relaxed-b8-120x68-m192", 600),
     ("minnen-hr-4k-240x135-m320", 300),
 ])
-def test_full_size_teacher_forced(name, n):
-    log(f"case {name} full size, teacher-forced sample of {n}")
+@pytest.mark.parametrize("driver", ["graph", "persistent"])
+def test_full_size_teacher_forced(name, n, driver):
+    log(f"case {name} full size, teacher-forced sample of {n}, driver={driver}")
     cfg, w, table, psi, sym = make_case(name)
-    got = run_decode(cfg, w, table, psi, sym)
+    got = run_decode(cfg, w, table, psi, sym, driver)
     model = oracle_model(cfg, w, table)
     lats = sample_latents(cfg, n)
     log(teacher_forced(cfg, got, psi, sym, model, lats, table))
+
+
+def test_graph_replays_match_and_reuse_plan():
+    # one graph plan, several calls with different buffers and both
+    # directions, with eager work and syncs in between: every replay must
+    # match the oracle
+    cfg, w, table, psi, sym = make_case("minnen-16x16-m192", H=6, W=8, B=1)
+    model = oracle_model(cfg, w, table)
+    ref = model.decode(psi, sym)
+    plan = gpu_plan(cfg, w, table, "graph")
+    psi_d = torch.from_numpy(psi).cuda()
+    sym_d = torch.from_numpy(sym).cuda()
+    u = inputs.make_noise(cfg["B"], cfg["H"], cfg["W"], cfg["M"])
+    y_d = torch.from_numpy(inputs.encoder_input(sym, u, ref["mean"])).cuda()
+    for it in range(3):
+        out = plan.decode(psi_d, sym_d)
+        plan.sync()
+        compare(to_np(out), ref, table, cfg["K"])
+        junk = torch.randn(1000, device="cuda").sum().item()  # eager work between replays
+        assert np.isfinite(junk)
+        out_e, s = plan.encode(psi_d, y_d)
+        plan.sync()
+        assert np.array_equal(s.cpu().numpy(), sym)
+        compare(to_np(out_e), ref, table, cfg["K"])
+    plan.close()
