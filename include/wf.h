@@ -156,6 +156,20 @@ int wf_encode(wf_plan_t plan, const float *psi, const float *y, int32_t *sym_out
               const wf_out *out, hipStream_t stream);
 
 /*
+ * Measurement hook of the persistent driver (WF_E_UNSUPPORTED for others).
+ * With `stamps` non-NULL (DEVICE int64 array of `capacity` entries) every
+ * later call records the device wall clock (100 MHz ticks) at each
+ * device-wide barrier k = 0, 1, ...: entry k*(G+1) + g is the time workgroup g
+ * arrived at barrier k, entry k*(G+1) + G the time workgroup 0 left it, where
+ * G is the grid size written to *grid.  A call has 1 + 3*T barriers; *needed
+ * receives the entries that takes (either output may be NULL).  Entries past
+ * `capacity` are not written.  stamps == NULL turns recording off.  The array
+ * stays owned by the caller and must outlive the calls that record into it.
+ */
+int wf_plan_trace(wf_plan_t plan, int64_t *stamps, int64_t capacity, int64_t *needed,
+                  int32_t *grid);
+
+/*
  * Wait for `stream` and report a device-side error recorded by the plan's
  * kernels (WF_E_TIMEOUT when a bounded device-wide wait gave up).  Clears the
  * recorded error.

@@ -2,14 +2,15 @@
 // MFMA tile engine and the work of the three phases of a wavefront step.
 //
 // For step t (Sec. III-C):
-//   phase A  h1 = lrelu(P1 + sum of pushed old-tap slots + F_new . new taps)
-//            and the push of step t-1: every latent of step t-1 adds
-//            F_o . y_hat into slot o of each later latent that has it as old
-//            tap o
+//   phase A  h1 = lrelu(P1 + [new taps ; ctx_old(t)] . [F_new ; W1b])
 //   phase B  h2 = lrelu(W2 . h1 + b2)
-//   phase C  o  = W3 . h2 + b3  -> mean / scale / index, y_hat = s + mean
-// with P1 = b1 + W1[:, 2M:] . bc + W1[:, :2M] . psi hoisted before the loop
-// and F = W1[:, 2M:] . Wc[tap] the per-tap folded weights.
+//   phase C  o  = W3 . h2 + b3 -> mean / scale / index, y_hat = s + mean
+// and, spread over the three phases to even out their work, the kCtxParts
+// k-parts of ctx_old(t+1) (see ctxo_split).
+// with P1 = b1 + W1b . bc + W1[:, :2M] . psi hoisted before the loop,
+// W1b = W1[:, 2M:], F_new = W1b . Wc[new taps] folded at plan time, and
+// ctx_old(t+1) = Wc[old taps] . y_hat[old taps] for the latents of step t+1
+// (its inputs were all written by step t-1 or earlier).
 //
 // Every product runs on fp32 MFMA (v_mfma_f32_16x16x4f32).  Each wave issues
 // all operand loads of its k-range before its first MFMA, and the epilogue
@@ -18,9 +19,9 @@
 // computed on the same XCD, which then streams only its slice of the weights.
 //
 // COH selects how data produced by other workgroups of the same launch is
-// accessed: with COH the activations, the reconstruction and the pushed slots
-// are written and read with agent-coherent (sc1) buffer operations, so the
-// persistent kernel needs no cache flush between its phases.
+// accessed: with COH the activations, the reconstruction and the old-tap
+// context are written and read with agent-coherent (sc1) buffer operations, so
+// the persistent kernel needs no cache flush between its phases.
 #pragma once
 
 #include "wf_internal.h"
@@ -29,8 +30,10 @@ namespace wf {
 
 typedef float f4 __attribute__((ext_vector_type(4)));
 
-constexpr int kWaves = 4;
-constexpr int kKbw = 20;   // k-blocks (16 values of k) loaded by a wave before its MFMAs
+constexpr int kWaves = 4;              // waves per workgroup; they split a tile's k-blocks
+constexpr int kThreads = 64 * kWaves;
+constexpr int kCtxParts = 3;  // k-parts of the old-tap context product
+constexpr int kKbw = 10;   // k-blocks (16 values of k) loaded by a wave before its MFMAs
 constexpr int kSc1 = 16;   // cache-policy bits of an agent-coherent buffer access
 
 __device__ __forceinline__ f4 mfma_k16(f4 a, f4 b, f4 acc) {
@@ -47,25 +50,38 @@ __device__ __forceinline__ float lrelu(float v, float s) { return v >= 0.0f ? v 
 
 __device__ __forceinline__ f4 zero4() { return f4{0.0f, 0.0f, 0.0f, 0.0f}; }
 
-// Raw buffer resource over [p, p + 2 GiB): out-of-range accesses return zero.
+// Raw buffer resource over [p, p + kBufBytes): accesses at or past kBufBytes
+// return zero.  Every base pointer used here is the same for the whole wave;
+// reading it from the first lane keeps the descriptor in scalar registers.
 __device__ __forceinline__ __amdgpu_buffer_rsrc_t rsrc(const void* p) {
-    return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(p), (short)0, 0x7fffffff, 0x00020000);
+    const unsigned long long v = reinterpret_cast<unsigned long long>(p);
+    const unsigned lo = __builtin_amdgcn_readfirstlane((unsigned)v);
+    const unsigned hi = __builtin_amdgcn_readfirstlane((unsigned)(v >> 32));
+    void* u = reinterpret_cast<void*>(((unsigned long long)hi << 32) | lo);
+    return __builtin_amdgcn_make_buffer_rsrc(u, (short)0, kBufBytes, 0x00020000);
 }
 
-// Loads/stores of data written by other workgroups of the same launch.
-// (the buffer builtins move raw 32-bit words: bit casts, not conversions)
-typedef unsigned u4 __attribute__((ext_vector_type(4)));
+// Activation loads go through raw buffer instructions: an invalid element
+// (row past the step, tap outside the grid) is given an offset past the end
+// of the 2 GiB window, which the buffer unit answers with zeros.  The loaders
+// are therefore branch-free and a wave's loads can all be in flight at once.
+// With COH the access is agent-coherent (sc1), for data written by other
+// workgroups of the same launch.  (The buffer builtins move raw 32-bit words:
+// bit casts, not conversions.)
+// kOob lies past the window under either range rule (offset >= size, or
+// offset + access size > size).
+constexpr int kOob = 0x7ffffff0;
+static_assert(kOob >= kBufBytes + 16, "the sentinel offset must be out of range");
+
 template <bool COH>
-__device__ __forceinline__ f4 ld4(const float* base, size_t idx) {
-    if (COH)
-        return __builtin_bit_cast(f4, __builtin_amdgcn_raw_buffer_load_b128(rsrc(base), (int)(idx * 4), 0, kSc1));
-    return *reinterpret_cast<const f4*>(base + idx);
+__device__ __forceinline__ f4 ld4(const float* base, size_t idx, bool ok = true) {
+    const int off = ok ? (int)(idx * 4) : kOob;
+    return __builtin_bit_cast(f4, __builtin_amdgcn_raw_buffer_load_b128(rsrc(base), off, 0, COH ? kSc1 : 0));
 }
 template <bool COH>
-__device__ __forceinline__ float ld1(const float* base, size_t idx) {
-    if (COH)
-        return __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(rsrc(base), (int)(idx * 4), 0, kSc1));
-    return base[idx];
+__device__ __forceinline__ float ld1(const float* base, size_t idx, bool ok = true) {
+    const int off = ok ? (int)(idx * 4) : kOob;
+    return __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(rsrc(base), off, 0, COH ? kSc1 : 0));
 }
 template <bool COH>
 __device__ __forceinline__ void st1(float* base, size_t idx, float v) {
@@ -141,25 +157,61 @@ __host__ __device__ __forceinline__ int xcd_blocks(int nct, int nrt) {
 
 __host__ __device__ __forceinline__ int ntiles(int n) { return (n + kTile - 1) / kTile; }
 
-// Block counts of the three phases of a step.
-__host__ __device__ __forceinline__ int phase_a_l1_blocks(const StepArgs& a, const StepRows& s) {
+// Block counts of the jobs of a step.
+__host__ __device__ __forceinline__ int l1_blocks(const StepArgs& a, const StepRows& s) {
     return xcd_blocks(a.Np1 / kTile, ntiles(s.nrows));
 }
-__host__ __device__ __forceinline__ int phase_a_push_blocks(const StepArgs& a, const StepRows& sp, int T) {
-    // the push of step sp.t is needed when a consumer step sp.t + 2 exists
-    if (a.n_old == 0 || sp.nrows == 0 || sp.t + 2 >= T) return 0;
-    return xcd_blocks((a.n_old * a.Np1 / kTile + kWaves - 1) / kWaves, ntiles(sp.nrows));
-}
-__host__ __device__ __forceinline__ int phase_b_blocks(const StepArgs& a, const StepRows& s) {
+__host__ __device__ __forceinline__ int l2_blocks(const StepArgs& a, const StepRows& s) {
     return xcd_blocks(a.Np2 / kTile, ntiles(s.nrows));
 }
-__host__ __device__ __forceinline__ int phase_c_blocks(const StepArgs& a, const StepRows& s) {
+__host__ __device__ __forceinline__ int l3_blocks(const StepArgs& a, const StepRows& s) {
+    return xcd_blocks(2 * a.M / kTile, ntiles(s.nrows));
+}
+// one k-part of the old-tap context of the latents of step s (nrows may be 0)
+__host__ __device__ __forceinline__ int ctxo_blocks(const StepArgs& a, const StepRows& s) {
+    if (a.n_old == 0 || s.nrows == 0) return 0;
     return xcd_blocks(2 * a.M / kTile, ntiles(s.nrows));
 }
 
+// Which of the kCtxParts * nc old-tap context jobs of the next step ride along
+// with each phase: phase A takes jobs [0, c1), B [c1, c2), C [c2, total).
+// The cuts equalise the k-blocks each phase streams (a job of phase A, B, C
+// and of the old-tap context costs ka, kb, kc, ko k-blocks), so that every
+// phase holds about the same work; they are multiples of 8, which keeps every
+// job on the XCD its column tile belongs to.
+struct CtxSplit {
+    int c1, c2, total;
+};
+__host__ __device__ __forceinline__ CtxSplit ctxo_split(int nc, int nb1, int nb2, int nb3, int ka, int kb, int kc,
+                                                        int ko) {
+    CtxSplit c;
+    c.total = kCtxParts * nc;
+    const long long wa = (long long)nb1 * ka, wb = (long long)nb2 * kb, wc = (long long)nb3 * kc;
+    const long long each = (wa + wb + wc + (long long)c.total * ko) / 3;
+    auto fill = [&](long long w, int left) {
+        long long j = ko > 0 && each > w ? (each - w) / ko : 0;
+        if (j > left) j = left;
+        return (int)(j / kXcds * kXcds);
+    };
+    c.c1 = fill(wa, c.total);
+    c.c2 = c.c1 + fill(wb, c.total - c.c1);
+    return c;
+}
+
+// k-blocks streamed by one job of each kind (the l3 jobs stream a value
+// group's column tiles: K=1 one, K=3 up to six).
+__host__ __device__ __forceinline__ void job_costs(const StepArgs& a, int* ka, int* kb, int* kc, int* ko) {
+    *ka = (a.n_new * a.M + 2 * a.M) / kTile;
+    *kb = a.Np1 / kTile;
+    *kc = a.Np2 / kTile * (a.K == 1 ? 1 : 4);
+    *ko = a.n_old * a.M / kTile / kCtxParts;
+}
+
 // A wave's partial 16x16 tile over k-blocks [kb0, kb1): w points at the
-// lane's operand of k-block 0 of the tile's packed weight column; all loads
-// of up to kKbw k-blocks are issued before the MFMAs that use them.
+// lane's operand of k-block 0 of the tile's packed weight column.  The loads
+// of up to kKbw k-blocks are issued before the MFMAs that use them (indices
+// past the range are clamped, so every load is unconditional); la(kb) must
+// be branch-free.
 template <class LoadA>
 __device__ __forceinline__ f4 wave_dot(const f4* __restrict__ w, int kb0, int kb1, LoadA la) {
     f4 acc = zero4();
@@ -167,11 +219,9 @@ __device__ __forceinline__ f4 wave_dot(const f4* __restrict__ w, int kb0, int kb
         f4 av[kKbw], bv[kKbw];
 #pragma unroll
         for (int u = 0; u < kKbw; ++u) {
-            const int k = kc + u;
-            if (k < kb1) {
-                av[u] = la(k);
-                bv[u] = w[(size_t)k * 64];
-            }
+            const int k = min(kc + u, kb1 - 1);
+            av[u] = la(k);
+            bv[u] = w[(size_t)k * 64];
         }
 #pragma unroll
         for (int u = 0; u < kKbw; ++u)
@@ -180,88 +230,104 @@ __device__ __forceinline__ f4 wave_dot(const f4* __restrict__ w, int kb0, int kb
     return acc;
 }
 
-// The four waves of a block split the k-blocks of one tile; afterwards every
-// wave holds the full sum of tile row 4*(lane/16) + wave, column lane%16.
-// Ends with a block barrier, so `red` may be reused right away.
-template <class LoadA>
-__device__ __forceinline__ float block_tile(f4 (*red)[64], const float* __restrict__ wp, int nkb, int ct,
-                                            LoadA la) {
+// The four waves of a block split the k-blocks [klo, khi) (default: all nkb)
+// of one tile; k-blocks below `ksplit` are loaded by la_lo, the rest by la_hi.
+// Afterwards waves 0..3 hold the full sum of tile row 4*(lane/16) + wave,
+// column lane%16 (the other waves get 0).  Ends with a block barrier, so `red`
+// may be reused.
+template <class LoadLo, class LoadHi>
+__device__ __forceinline__ float block_tile2(f4 (*red)[64], const float* __restrict__ wp, int nkb, int ct,
+                                             int ksplit, LoadLo la_lo, LoadHi la_hi, int klo = 0, int khi = -1) {
     const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
-    const int per = (nkb + kWaves - 1) / kWaves;
-    const int kb0 = min(nkb, wave * per), kb1 = min(nkb, kb0 + per);
+    if (khi < 0) khi = nkb;
+    const int per = (khi - klo + kWaves - 1) / kWaves;
+    const int kb0 = min(khi, klo + wave * per), kb1 = min(khi, kb0 + per);
     const f4* w = reinterpret_cast<const f4*>(wp) + (size_t)ct * nkb * 64 + lane;
-    red[wave][lane] = wave_dot(w, kb0, kb1, la);
+    f4 acc = wave_dot(w, kb0, min(kb1, ksplit), la_lo);
+    acc += wave_dot(w, max(kb0, ksplit), kb1, la_hi);
+    red[wave][lane] = acc;
     __syncthreads();
-    const float v = red[0][lane][wave] + red[1][lane][wave] + red[2][lane][wave] + red[3][lane][wave];
+    float v = 0.0f;
+    if (wave < 4) {
+#pragma unroll
+        for (int w2 = 0; w2 < kWaves; ++w2) v += red[w2][lane][wave];
+    }
     __syncthreads();
     return v;
 }
 
-// ---------------------------------------------------------------------------
-// Phase A, push part: producer step sp, one wave per column tile of the
-// old-tap weights (four consecutive tiles per block).
-template <bool COH>
-__device__ __forceinline__ void push_job(const StepArgs& a, const StepRows& sp, int b) {
-    const int nct = a.n_old * a.Np1 / kTile;
-    const Job jb = xcd_job(b, (nct + kWaves - 1) / kWaves, ntiles(sp.nrows));
-    if (!jb.valid) return;
-    const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63, kq = lane >> 4;
-    const int ct = jb.ct * kWaves + wave;
-    if (ct >= nct) return;
-    const int M = a.M;
-    const Row w = step_row(a, sp, jb.rt * kTile + (lane & 15));
-    const float* yh = a.cp->y_hat;
-    const size_t ybase = w.lat * M + kq * 4;
-    auto la = [&](int kb) -> f4 { return w.valid ? ld4<COH>(yh, ybase + kb * kTile) : zero4(); };
-    const f4* wv = reinterpret_cast<const f4*>(a.wp_old) + (size_t)ct * (M / kTile) * 64 + lane;
-    const f4 acc = wave_dot(wv, 0, M / kTile, la);
-    const int col = ct * kTile + (lane & 15);
-    const int o = col / a.Np1, n = col - o * a.Np1;
-    const int dy = a.old_dy[o], dx = a.old_dx[o], tc = sp.t + a.old_delta[o];
-    int ci0, cn;
-    step_span(a.H, a.W, a.lambda, tc, ci0, cn);
-    const size_t ring = (size_t)(tc % a.nring) * a.max_rows;
-#pragma unroll
-    for (int q = 0; q < 4; ++q) {
-        const Row v = step_row(a, sp, jb.rt * kTile + kq * 4 + q);
-        if (!v.valid) continue;
-        const int ic = v.i - dy, jc = v.j - dx;   // the consumer
-        if (ic >= a.H || jc < 0 || jc >= a.W) continue;
-        const size_t rc = (size_t)v.b * cn + (ic - ci0);
-        st1<COH>(a.slots, ((ring + rc) * a.n_old + o) * a.Np1 + n, acc[q]);
-    }
+template <class LoadA>
+__device__ __forceinline__ float block_tile(f4 (*red)[64], const float* __restrict__ wp, int nkb, int ct,
+                                            LoadA la, int klo = 0, int khi = -1) {
+    return block_tile2(red, wp, nkb, ct, nkb, la, la, klo, khi);
 }
 
-// Phase A, layer-1 part: block b of the layer-1 jobs of step s.
+// ---------------------------------------------------------------------------
+// Job j of the old-tap context of the latents of step s: k-part part = j / nc
+// (a contiguous range of the k-blocks of the gathered old taps, tap-major)
+// of block j % nc:  ctxo[part][r][n] = sum_{k in part} taps[r][k] Wc[k][n].
+template <bool COH>
+__device__ __forceinline__ void ctxo_job(const StepArgs& a, const StepRows& s, int j, int nc, f4 (*red)[64]) {
+    const int part = j / nc, b = j - part * nc;
+    const int M = a.M;
+    const Job jb = xcd_job(b, 2 * M / kTile, ntiles(s.nrows));
+    if (!jb.valid) return;
+    const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63, kq = lane >> 4;
+    const Row w = step_row(a, s, jb.rt * kTile + (lane & 15));
+    const float* yh = a.cp->y_hat;
+    auto la = [&](int kb) -> f4 {
+        const int tap = kb * kTile / M;   // a k-block never straddles two taps
+        const int c = kb * kTile - tap * M + kq * 4;
+        const int row = tap < a.old_n0 ? 0 : (tap < a.old_n0 + a.old_n1 ? 1 : 2);
+        const int dx = tap - (row == 0 ? 0 : (row == 1 ? a.old_n0 : a.old_n0 + a.old_n1)) - 2;
+        const int ii = w.i + row - 2, jj = w.j + dx;
+        const bool ok = w.valid && ii >= 0 && jj >= 0 && jj < a.W;
+        return ld4<COH>(yh, (((size_t)w.b * a.H + ii) * a.W + jj) * M + c, ok);
+    };
+    const int nkb = a.n_old * M / kTile;
+    const int klo = nkb * part / kCtxParts, khi = nkb * (part + 1) / kCtxParts;
+    const float acc = block_tile(red, a.wp_old, nkb, jb.ct, la, klo, khi);
+    const int n = jb.ct * kTile + (lane & 15);
+    const int ro = wave < 4 ? jb.rt * kTile + kq * 4 + wave : s.nrows;
+    // double-buffered by step parity: jobs for step s.t may run while layer 1
+    // of step s.t - 1 still reads the other half
+    const size_t slot = (size_t)((s.t & 1) * kCtxParts + part) * a.max_rows + ro;
+    if (ro < s.nrows) st1<COH>(a.ctxo, slot * 2 * M + n, acc);
+}
+
+// Phase A: layer 1 of step s.
 template <bool COH>
 __device__ __forceinline__ void l1_job(const StepArgs& a, const StepRows& s, int b, f4 (*red)[64]) {
     const Job jb = xcd_job(b, a.Np1 / kTile, ntiles(s.nrows));
     if (!jb.valid) return;
     const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63, kq = lane >> 4;
     const int M = a.M;
-    // epilogue operands first: hoisted part and pushed slots of this wave's row
+    // epilogue operand first: the hoisted part of this wave's row
     const int n = jb.ct * kTile + (lane & 15);
-    const int ro = jb.rt * kTile + kq * 4 + wave;
+    const int ro = wave < 4 ? jb.rt * kTile + kq * 4 + wave : s.nrows;   // epilogue row of this wave
     const Row v = step_row(a, s, ro);
-    float z = 0.0f;
-    if (v.valid) {
-        z = a.p1[v.lat * a.Np1 + n];
-        const size_t sl = (((size_t)(s.t % a.nring) * a.max_rows + ro) * a.n_old) * a.Np1 + n;
-        for (int o = 0; o < a.n_old; ++o) {
-            const int ii = v.i + a.old_dy[o], jj = v.j + a.old_dx[o];
-            if (ii >= 0 && jj >= 0 && jj < a.W) z += ld1<COH>(a.slots, sl + (size_t)o * a.Np1);
-        }
-    }
-    const Row w = step_row(a, s, jb.rt * kTile + (lane & 15));
+    const float z = v.valid ? a.p1[v.lat * a.Np1 + n] : 0.0f;
+    const int r = jb.rt * kTile + (lane & 15);
+    const Row w = step_row(a, s, r);
     const float* yh = a.cp->y_hat;
-    auto la = [&](int kb) -> f4 {
-        const int k0 = kb * kTile + kq * 4;
-        const int tap = k0 >= M ? 1 : 0, c = k0 - tap * M;
-        const int ii = w.i + a.new_dy[tap], jj = w.j + a.new_dx[tap];
-        if (!w.valid || ii < 0 || jj < 0 || jj >= a.W) return zero4();
-        return ld4<COH>(yh, (((size_t)w.b * a.H + ii) * a.W + jj) * M + c);
+    const int knew = a.n_new * M;
+    const size_t cpart = (size_t)a.max_rows * 2 * M;
+    const size_t cbase = (size_t)(s.t & 1) * kCtxParts * cpart + (size_t)r * 2 * M + kq * 4;
+    auto la_new = [&](int kb) -> f4 {
+        const int tap = kb * kTile >= M ? 1 : 0;
+        const int c = kb * kTile - tap * M + kq * 4;
+        const int ii = w.i - 1 + tap, jj = w.j + (tap ? -1 : a.new_dx0);
+        const bool ok = w.valid && ii >= 0 && jj >= 0 && jj < a.W;
+        return ld4<COH>(yh, (((size_t)w.b * a.H + ii) * a.W + jj) * M + c, ok);
     };
-    const float acc = block_tile(red, a.wp_new, a.n_new * M / kTile, jb.ct, la);
+    auto la_ctx = [&](int kb) -> f4 {
+        const size_t q = cbase + (kb * kTile - knew);
+        f4 v = ld4<COH>(a.ctxo, q, w.valid);
+#pragma unroll
+        for (int part = 1; part < kCtxParts; ++part) v += ld4<COH>(a.ctxo, q + part * cpart, w.valid);
+        return v;
+    };
+    const float acc = block_tile2(red, a.wp_l1, (knew + 2 * M) / kTile, jb.ct, knew / kTile, la_new, la_ctx);
     if (v.valid) st1<COH>(a.h1, (size_t)ro * a.Np1 + n, lrelu(acc + z, a.slope));
 }
 
@@ -276,10 +342,10 @@ __device__ __forceinline__ void l2_job(const StepArgs& a, const StepRows& s, int
     const int r = jb.rt * kTile + (lane & 15);
     const bool valid = r < s.nrows;
     const size_t base = (size_t)r * a.Np1 + kq * 4;
-    auto la = [&](int kb) -> f4 { return valid ? ld4<COH>(a.h1, base + kb * kTile) : zero4(); };
+    auto la = [&](int kb) -> f4 { return ld4<COH>(a.h1, base + kb * kTile, valid); };
     const float acc = block_tile(red, a.wp2, a.Np1 / kTile, jb.ct, la);
     const int ro = jb.rt * kTile + kq * 4 + wave;
-    if (ro < s.nrows) st1<COH>(a.h2, (size_t)ro * a.Np2 + n, lrelu(acc + bias, a.slope));
+    if (wave < 4 && ro < s.nrows) st1<COH>(a.h2, (size_t)ro * a.Np2 + n, lrelu(acc + bias, a.slope));
 }
 
 __device__ __forceinline__ int scale_index(const float* tab, int L, float sg) {
@@ -319,7 +385,7 @@ __device__ __forceinline__ void l3_job(const StepArgs& a, const StepRows& s, int
     // epilogue operands of this wave's row first
     const CallPtrs* cp = a.cp;
     const int c = cg * kTile + (lane & 15);
-    const int ro = rt * kTile + kq * 4 + wave;
+    const int ro = wave < 4 ? rt * kTile + kq * 4 + wave : s.nrows;   // epilogue row of this wave
     const Row v = step_row(a, s, ro);
     const size_t oq = v.lat * M + c;
     float bias[NTM];
@@ -345,7 +411,7 @@ __device__ __forceinline__ void l3_job(const StepArgs& a, const StepRows& s, int
     const int NT = vg == 0 ? NT0 : NT1;
     int cols[NTM];
 #pragma unroll
-    for (int t = 0; t < NTM; ++t) cols[t] = (vg == 0 ? t : (KC == 1 ? 1 : 6 + t)) * G + cg;
+    for (int t = 0; t < NTM; ++t) cols[t] = (vg == 0 ? t : (KC == 1 ? 1 : 6 + (t < NT1 ? t : 0))) * G + cg;
     f4 acc[NTM];
 #pragma unroll
     for (int t = 0; t < NTM; ++t) acc[t] = zero4();
@@ -353,13 +419,10 @@ __device__ __forceinline__ void l3_job(const StepArgs& a, const StepRows& s, int
         f4 av[KBW], bv[KBW][NTM];
 #pragma unroll
         for (int u = 0; u < KBW; ++u) {
-            const int k = kc + u;
-            if (k < kb1) {
-                av[u] = valid ? ld4<COH>(a.h2, hbase + k * kTile) : zero4();
+            const int k = min(kc + u, kb1 - 1);
+            av[u] = ld4<COH>(a.h2, hbase + k * kTile, valid);
 #pragma unroll
-                for (int t = 0; t < NTM; ++t)
-                    if (t < NT) bv[u][t] = wv[((size_t)cols[t] * nkb + k) * 64];
-            }
+            for (int t = 0; t < NTM; ++t) bv[u][t] = wv[((size_t)cols[t] * nkb + k) * 64];
         }
 #pragma unroll
         for (int u = 0; u < KBW; ++u)
@@ -373,9 +436,13 @@ __device__ __forceinline__ void l3_job(const StepArgs& a, const StepRows& s, int
     __syncthreads();
     float o[NTM];
 #pragma unroll
-    for (int t = 0; t < NTM; ++t)
-        o[t] = sm.red[0][t][lane][wave] + sm.red[1][t][lane][wave] + sm.red[2][t][lane][wave] +
-               sm.red[3][t][lane][wave] + bias[t];
+    for (int t = 0; t < NTM; ++t) {
+        o[t] = bias[t];
+        if (wave < 4) {
+#pragma unroll
+            for (int w2 = 0; w2 < kWaves; ++w2) o[t] += sm.red[w2][t][lane][wave];
+        }
+    }
     __syncthreads();
     if (!v.valid) return;
 

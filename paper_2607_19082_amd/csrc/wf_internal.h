@@ -17,6 +17,7 @@ constexpr int kTile = 16;            // MFMA tile edge (rows and columns)
 constexpr int kMaxTable = 256;
 constexpr int kXcds = 8;             // accelerator complex dies of an MI355X
 constexpr int kBarrierWords = 512;   // barrier counters of the persistent driver
+constexpr int kBufBytes = 0x7fff0000; // window of a raw buffer access (arrays must fit)
 
 // Set the calling thread's error message and return `code`.
 int fail(int code, const std::string& msg);
@@ -37,36 +38,38 @@ struct CallPtrs {
 // Plan constants passed by value to every step kernel.
 //
 // Taps are split by age.  A tap (dy,dx) of the latent decoded at step t was
-// written at step t - delta with delta = lambda*(-dy) - dx.  The "new" taps
-// (delta = 1) are gathered on the critical path; every "old" tap (delta >= 2)
-// is pushed forward by its producer one step after the producer is decoded:
-// slot[o] of the consumer receives (W1[:, 2M:] . Wc[tap o]) . y_hat[producer],
-// i.e. the old tap's share of layer 1 (the context conv and the context half
-// of layer 1 are both linear, so their product is folded at plan time).
+// written at step t - delta with delta = lambda*(-dy) - dx.  Only the "new"
+// taps (delta = 1) are gathered on the critical path of step t; the context
+// sum over the "old" taps (delta >= 2) of step t+1's latents only needs
+// y_hat of steps <= t-1, so it is computed during step t, off the critical
+// path, in k-parts.  Layer 1 of step t then reads
+//   [new taps (n_new*M) ; old-tap context (2M)]
+// against [W1[:, 2M:] . Wc[new taps] ; W1[:, 2M:]] (the new taps' conv and the
+// context half of layer 1 are both linear, so their product is folded at plan
+// time; the context bias is folded into the hoisted part).
 struct StepArgs {
     int H, W, M, B, K, L, lambda;
     int Np1, Np2, n3;
-    int n_new, n_old, nring;
-    int new_dy[kMaxNew], new_dx[kMaxNew];
-    int old_dy[kMaxTaps], old_dx[kMaxTaps], old_delta[kMaxTaps];
+    int n_new, n_old;
+    // Tap geometry, as scalars so that kernels compute a tap's offset without
+    // indexing memory.  Old taps, tap-major: the first old_n0 lie in row -2,
+    // the next old_n1 in row -1, the rest in row 0; each row's run starts at
+    // dx = -2 and is contiguous.  New taps: (-1, new_dx0) and (0, -1).
+    int old_n0, old_n1, new_dx0;
     float slope;
-    const int* order;       // grid positions of all steps, step-major, by row
-    const int* step_ptr;    // [T]
-    const int* step_n;      // [T] latents per image on the step
-    const int* step_i0;     // [T] first grid row on the step
-    const float* wp_hoist;  // packed W1[:, :2M]                      [Np1/16][2M/16]
-    const float* b_hoist;   // b1 + W1[:, 2M:] . bc                    [Np1]
-    const float* wp_new;    // packed folded weights of the new taps   [Np1/16][n_new*M/16]
-    const float* wp_old;    // packed folded weights of the old taps   [n_old*Np1/16][M/16]
-    const float* wp2;       // packed W2                               [Np2/16][Np1/16]
+    const float* wp_hoist;  // packed W1[:, :2M]                          [Np1/16][2M/16]
+    const float* b_hoist;   // b1 + W1[:, 2M:] . bc                        [Np1]
+    const float* wp_l1;     // packed [W1b.Wc[new] ; W1b]                  [Np1/16][(n_new*M + 2M)/16]
+    const float* wp_old;    // packed Wc over the old taps                 [2M/16][n_old*M/16]
+    const float* wp2;       // packed W2                                   [Np2/16][Np1/16]
     const float* b2;        // [Np2]
-    const float* wp3;       // packed W3                               [n3/16][Np2/16]
+    const float* wp3;       // packed W3                                   [n3/16][Np2/16]
     const float* b3;        // [n3]
     const float* table;     // [L]
     float* p1;              // [B*H*W][Np1] hoisted layer-1 part
     float* h1;              // [max_rows][Np1]
     float* h2;              // [max_rows][Np2]
-    float* slots;           // [nring][max_rows][n_old][Np1]
+    float* ctxo;            // [2][3][max_rows][2M] old-tap context k-parts, by step parity
     int max_rows;
     const CallPtrs* cp;
 };
@@ -79,7 +82,6 @@ struct Plan {
     int lambda, T, ntaps;
     int dy[kMaxTaps], dx[kMaxTaps];
     std::vector<int32_t> step_of;        // [H*W]
-    std::vector<int> step_ptr, step_n, step_i0;   // [T]
     int max_rows;
     int Np1, Np2;                        // d1, d2 rounded up to 16
     StepArgs args;                       // device pointers filled in
@@ -92,6 +94,8 @@ struct Plan {
     unsigned* d_bar = nullptr;
     int grid = 0;
     long long spin_budget = 100000000;   // wall-clock ticks (100 MHz): 1 s
+    long long* stamps = nullptr;         // optional barrier trace
+    long long stamps_cap = 0;
     // graph driver
     hipStream_t cap_stream = nullptr;
     hipGraph_t graph = nullptr;

@@ -3,7 +3,7 @@
 // kernel boundaries.  Each workgroup loops over the jobs of a phase with a
 // stride of the grid size (a multiple of 8, so a job's XCD placement is the
 // same as in the per-step kernels), and all data that crosses workgroups
-// inside the launch (h1, h2, y_hat, pushed slots) moves through agent-coherent
+// inside the launch (h1, h2, y_hat, old-tap context) moves through agent-coherent
 // (sc1) buffer accesses.
 #include "wf_device.h"
 
@@ -15,11 +15,18 @@ namespace wf {
 // reaches k * (number of classes).  A wait longer than `budget` wall-clock
 // ticks records WF_E_TIMEOUT in *err; every workgroup that sees a recorded
 // error leaves the kernel at its next barrier, so the grid always drains.
+struct Trace {
+    long long* stamps;   // optional: arrival/leave wall-clock ticks per barrier
+    long long cap;
+};
+
 __device__ __forceinline__ bool grid_barrier(unsigned* ctr, unsigned k, int* err, long long budget,
-                                             int* bail) {
+                                             int* bail, const Trace& tr) {
     __builtin_amdgcn_s_waitcnt(0);  // this wave's coherent stores have landed
     __syncthreads();
     if (threadIdx.x == 0) {
+        const long long slot = (long long)(k - 1) * (gridDim.x + 1);
+        if (tr.stamps && slot + gridDim.x < tr.cap) tr.stamps[slot + blockIdx.x] = wall_clock64();
         const unsigned G = gridDim.x;
         const unsigned x = blockIdx.x % kXcds;
         const unsigned ng = G < (unsigned)kXcds ? G : (unsigned)kXcds;
@@ -44,14 +51,15 @@ __device__ __forceinline__ bool grid_barrier(unsigned* ctr, unsigned k, int* err
             }
         }
         *bail = flag;
+        if (tr.stamps && blockIdx.x == 0 && slot + gridDim.x < tr.cap) tr.stamps[slot + gridDim.x] = wall_clock64();
     }
     __syncthreads();
     return *bail == 0;
 }
 
 template <int KC>
-__global__ __launch_bounds__(256) void k_persistent(StepArgs a, int T, unsigned* ctr, int* err,
-                                                    long long budget) {
+__global__ __launch_bounds__(kThreads) void k_persistent(StepArgs a, int T, unsigned* ctr, int* err,
+                                                    long long budget, Trace tr) {
     __shared__ f4 red[kWaves][64];
     __shared__ L3Smem<KC> sm;
     __shared__ int bail;
@@ -59,25 +67,44 @@ __global__ __launch_bounds__(256) void k_persistent(StepArgs a, int T, unsigned*
     __syncthreads();
     const int G = gridDim.x;
     unsigned k = 0;
-    StepRows prev{0, 0, 0, 0};
+    // old-tap context of step 0 (no old tap of step 0 lies in the grid, but
+    // the general form keeps the loop uniform)
+    {
+        const StepRows s0 = step_rows(a.H, a.W, a.B, a.lambda, 0);
+        const int nc = ctxo_blocks(a, s0);
+        for (int b = blockIdx.x; b < kCtxParts * nc; b += G) ctxo_job<true>(a, s0, b, nc, red);
+        if (!grid_barrier(ctr, ++k, err, budget, &bail, tr)) return;
+    }
     for (int t = 0; t < T; ++t) {
         const StepRows s = step_rows(a.H, a.W, a.B, a.lambda, t);
-        const int nb1 = phase_a_l1_blocks(a, s);
-        const int nbp = t >= 1 ? phase_a_push_blocks(a, prev, T) : 0;
-        for (int b = blockIdx.x; b < nb1 + nbp; b += G) {
-            if (b >= nb1)
-                push_job<true>(a, prev, b - nb1);
-            else
+        StepRows s1{t + 1, 0, 0, 0};
+        if (t + 1 < T) s1 = step_rows(a.H, a.W, a.B, a.lambda, t + 1);
+        const int nc = ctxo_blocks(a, s1);
+        const int nb1 = l1_blocks(a, s), nb2 = l2_blocks(a, s), nb3 = l3_blocks(a, s);
+        int ka, kb, kc, ko;
+        job_costs(a, &ka, &kb, &kc, &ko);
+        const CtxSplit cs = ctxo_split(nc, nb1, nb2, nb3, ka, kb, kc, ko);
+        for (int b = blockIdx.x; b < nb1 + cs.c1; b += G) {
+            if (b < nb1)
                 l1_job<true>(a, s, b, red);
+            else
+                ctxo_job<true>(a, s1, b - nb1, nc, red);
         }
-        if (!grid_barrier(ctr, ++k, err, budget, &bail)) return;
-        const int nb2 = phase_b_blocks(a, s);
-        for (int b = blockIdx.x; b < nb2; b += G) l2_job<true>(a, s, b, red);
-        if (!grid_barrier(ctr, ++k, err, budget, &bail)) return;
-        const int nb3 = phase_c_blocks(a, s);
-        for (int b = blockIdx.x; b < nb3; b += G) l3_job<KC, true>(a, s, b, sm);
-        if (!grid_barrier(ctr, ++k, err, budget, &bail)) return;
-        prev = s;
+        if (!grid_barrier(ctr, ++k, err, budget, &bail, tr)) return;
+        for (int b = blockIdx.x; b < nb2 + cs.c2 - cs.c1; b += G) {
+            if (b < nb2)
+                l2_job<true>(a, s, b, red);
+            else
+                ctxo_job<true>(a, s1, cs.c1 + b - nb2, nc, red);
+        }
+        if (!grid_barrier(ctr, ++k, err, budget, &bail, tr)) return;
+        for (int b = blockIdx.x; b < nb3 + cs.total - cs.c2; b += G) {
+            if (b < nb3)
+                l3_job<KC, true>(a, s, b, sm);
+            else
+                ctxo_job<true>(a, s1, cs.c2 + b - nb3, nc, red);
+        }
+        if (!grid_barrier(ctr, ++k, err, budget, &bail, tr)) return;
     }
 }
 
@@ -89,17 +116,17 @@ static const void* persistent_fn(int K) {
     return K == 1 ? (const void*)k_persistent<1> : (const void*)k_persistent<3>;
 }
 
-// Grid size of the persistent kernel: one workgroup per CU, rounded down to a
-// multiple of 8 (XCD placement), if that many are co-resident.
+// Grid size of the persistent kernel: two workgroups per CU when they fit (one
+// hides the other's memory latency), else one; a multiple of 8 (XCD placement).
 int persistent_grid(Plan& p, int* grid) {
     int dev = 0, cus = 0, per_cu = 0;
     hipError_t e = hipGetDevice(&dev);
     if (e == hipSuccess) e = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);
     if (e == hipSuccess)
-        e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, persistent_fn(p.K), 256, 0);
+        e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, persistent_fn(p.K), kThreads, 0);
     if (e != hipSuccess) return fail(WF_E_HIP, std::string("occupancy query: ") + hipGetErrorString(e));
     if (per_cu < 1 || cus < kXcds) return fail(WF_E_UNSUPPORTED, "persistent kernel cannot be resident");
-    *grid = cus / kXcds * kXcds;
+    *grid = cus * (per_cu >= 2 ? 2 : 1) / kXcds * kXcds;
     return WF_OK;
 }
 
@@ -111,8 +138,9 @@ int enqueue_persistent(Plan& p, hipStream_t stream) {
     unsigned* ctr = p.d_bar;
     int* err = p.d_err;
     long long budget = p.spin_budget;
-    void* args[] = {&a, &T, &ctr, &err, &budget};
-    hipError_t e = hipLaunchCooperativeKernel(persistent_fn(p.K), dim3(p.grid), dim3(256), args, 0, stream);
+    Trace tr{p.stamps, p.stamps_cap};
+    void* args[] = {&a, &T, &ctr, &err, &budget, &tr};
+    hipError_t e = hipLaunchCooperativeKernel(persistent_fn(p.K), dim3(p.grid), dim3(kThreads), args, 0, stream);
     if (e != hipSuccess) return fail(WF_E_HIP, std::string("cooperative launch: ") + hipGetErrorString(e));
     return WF_OK;
 }

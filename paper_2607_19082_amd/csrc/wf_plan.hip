@@ -80,9 +80,11 @@ static int check_desc(const wf_desc* d) {
     int nt = mask_taps(d->mask, dy, dx);
     int lam = least_shear(nt, dy, dx);
     if (d->W < lam) return fail(WF_E_UNSUPPORTED, "W must be at least the shear factor (Thm. 1)");
+    // every array the kernels read through raw buffer instructions (psi, y_hat,
+    // the per-step activations) must fit the buffer window
     const long long lat = (long long)d->B * d->H * d->W;
-    if (lat * 2 * d->M > (1LL << 31) - 1 || lat * 3 * d->M > (1LL << 31) - 1)
-        return fail(WF_E_UNSUPPORTED, "problem too large for 32-bit element indexing");
+    if (lat * 2 * d->M * 4 >= kBufBytes || lat * 3 * d->M > (1LL << 31) - 1)
+        return fail(WF_E_UNSUPPORTED, "problem too large for the 2 GiB buffer window");
     if (d->precision == WF_BF16) return fail(WF_E_UNSUPPORTED, "bf16 operands are not built yet");
     return WF_OK;
 }
@@ -166,33 +168,18 @@ static int build_plan(const wf_desc* d, Plan* p) {
     const int H = p->H, W = p->W, M = p->M, lam = p->lambda;
     p->T = W + lam * (H - 1);
 
-    // Wavefront step lists: positions with lambda*i + j == t, by ascending row.
+    // Wavefront steps: the latents with lambda*i + j == t; a step's rows are
+    // its latents by ascending grid row, image-major.
     p->step_of.resize((size_t)H * W);
-    p->step_ptr.assign(p->T, 0);
-    p->step_n.assign(p->T, 0);
-    p->step_i0.assign(p->T, H);
+    std::vector<int> step_n(p->T, 0);
     for (int i = 0; i < H; ++i)
         for (int j = 0; j < W; ++j) {
-            int t = lam * i + j;
+            const int t = lam * i + j;
             p->step_of[(size_t)i * W + j] = t;
-            p->step_n[t]++;
-            p->step_i0[t] = std::min(p->step_i0[t], i);
+            step_n[t]++;
         }
-    std::vector<int> order((size_t)H * W);
     int maxn = 0;
-    for (int t = 0, acc = 0; t < p->T; ++t) {
-        p->step_ptr[t] = acc;
-        acc += p->step_n[t];
-        maxn = std::max(maxn, p->step_n[t]);
-    }
-    {
-        std::vector<int> fill(p->T, 0);
-        for (int i = 0; i < H; ++i)
-            for (int j = 0; j < W; ++j) {
-                int t = lam * i + j;
-                order[p->step_ptr[t] + fill[t]++] = i * W + j;
-            }
-    }
+    for (int t = 0; t < p->T; ++t) maxn = std::max(maxn, step_n[t]);
     p->max_rows = p->B * maxn;
     p->Np1 = round16(p->d1);
     p->Np2 = round16(p->d2);
@@ -204,39 +191,36 @@ static int build_plan(const wf_desc* d, Plan* p) {
     a.Np1 = Np1; a.Np2 = p->Np2; a.n3 = p->n3; a.slope = p->slope; a.max_rows = p->max_rows;
 
     // Split the taps by age (delta = steps between producer and consumer).
-    int maxdelta = 0;
     std::vector<int> new_taps, old_taps;
     for (int k = 0; k < p->ntaps; ++k) {
         const int delta = lam * (-p->dy[k]) - p->dx[k];
-        maxdelta = std::max(maxdelta, delta);
         (delta == 1 ? new_taps : old_taps).push_back(k);
     }
-    if ((int)new_taps.size() > kMaxNew) return fail(WF_E_UNSUPPORTED, "more than two taps of age one");
+    if ((int)new_taps.size() != kMaxNew) return fail(WF_E_UNSUPPORTED, "mask must have two taps of age one");
     a.n_new = (int)new_taps.size();
     a.n_old = (int)old_taps.size();
-    a.nring = maxdelta + 1;
-    for (int s = 0; s < a.n_new; ++s) {
-        a.new_dy[s] = p->dy[new_taps[s]];
-        a.new_dx[s] = p->dx[new_taps[s]];
+    a.old_n0 = a.old_n1 = 0;
+    for (int o : old_taps) {
+        if (p->dy[o] == -2) a.old_n0++;
+        if (p->dy[o] == -1) a.old_n1++;
     }
+    a.new_dx0 = p->dx[new_taps[0]];
+    // the kernels rebuild every tap from these scalars: check that they can
     for (int o = 0; o < a.n_old; ++o) {
-        a.old_dy[o] = p->dy[old_taps[o]];
-        a.old_dx[o] = p->dx[old_taps[o]];
-        a.old_delta[o] = lam * (-a.old_dy[o]) - a.old_dx[o];
+        const int dy = o < a.old_n0 ? -2 : (o < a.old_n0 + a.old_n1 ? -1 : 0);
+        const int dx = o < a.old_n0 ? o - 2 : (o < a.old_n0 + a.old_n1 ? o - a.old_n0 - 2 : o - a.old_n0 - a.old_n1 - 2);
+        if (p->dy[old_taps[o]] != dy || p->dx[old_taps[o]] != dx)
+            return fail(WF_E_UNSUPPORTED, "old taps are not row-contiguous from dx = -2");
     }
+    if (p->dy[new_taps[0]] != -1 || p->dy[new_taps[1]] != 0 || p->dx[new_taps[1]] != -1)
+        return fail(WF_E_UNSUPPORTED, "unexpected new taps");
 
     WF_HIP(hipGetDevice(&p->device));
     int rc;
-    int *d_order, *d_ptr, *d_n, *d_i0;
-    if ((rc = upload(p, &d_order, order.data(), order.size())) != WF_OK) return rc;
-    if ((rc = upload(p, &d_ptr, p->step_ptr.data(), p->step_ptr.size())) != WF_OK) return rc;
-    if ((rc = upload(p, &d_n, p->step_n.data(), p->step_n.size())) != WF_OK) return rc;
-    if ((rc = upload(p, &d_i0, p->step_i0.data(), p->step_i0.size())) != WF_OK) return rc;
-    a.order = d_order; a.step_ptr = d_ptr; a.step_n = d_n; a.step_i0 = d_i0;
 
-    // Fold the context conv into the context half of layer 1, tap by tap.
-    std::vector<std::vector<double>> fold(p->ntaps);
-    for (int k = 0; k < p->ntaps; ++k) fold_tap(d, p->dy[k], p->dx[k], fold[k]);
+    // Fold the new taps' conv into the context half of layer 1.
+    std::vector<std::vector<double>> fold(a.n_new);
+    for (int k = 0; k < a.n_new; ++k) fold_tap(d, p->dy[new_taps[k]], p->dx[new_taps[k]], fold[k]);
 
     auto w_hoist = pack_panel(2 * M, d1, [&](int k, int n) { return d->w1[(size_t)n * 4 * M + k]; });
     std::vector<float> b_hoist(Np1, 0.0f);
@@ -246,14 +230,16 @@ static int build_plan(const wf_desc* d, Plan* p) {
         for (int o = 0; o < 2 * M; ++o) acc += (double)w1b[o] * (double)d->ctx_b[o];
         b_hoist[n] = (float)acc;
     }
-    auto w_new = pack_panel(a.n_new * M, d1, [&](int k, int n) {
-        return (float)fold[new_taps[k / M]][(size_t)(k % M) * d1 + n];
-    });
-    auto w_old = pack_panel(M, a.n_old * Np1, [&](int k, int col) {
-        const int o = col / Np1, n = col % Np1;
-        return n < d1 ? (float)fold[old_taps[o]][(size_t)k * d1 + n] : 0.0f;
+    const int knew = a.n_new * M;
+    auto w_l1 = pack_panel(knew + 2 * M, d1, [&](int k, int n) {
+        if (k < knew) return (float)fold[k / M][(size_t)(k % M) * d1 + n];
+        return d->w1[(size_t)n * 4 * M + 2 * M + (k - knew)];
     });
     fold.clear();
+    auto w_old = pack_panel(a.n_old * M, 2 * M, [&](int k, int n) {
+        const int o = k / M, c = k % M;
+        return d->ctx_w[(((size_t)n * M + c) * 5 + (p->dy[old_taps[o]] + 2)) * 5 + (p->dx[old_taps[o]] + 2)];
+    });
     auto w2 = pack_panel(d1, p->d2, [&](int k, int n) { return d->w2[(size_t)n * d1 + k]; });
     auto w3 = pack_panel(p->d2, p->n3, [&](int k, int n) { return d->w3[(size_t)n * p->d2 + k]; });
     std::vector<float> b2(p->Np2, 0.0f);
@@ -264,8 +250,8 @@ static int build_plan(const wf_desc* d, Plan* p) {
     a.wp_hoist = f;
     if ((rc = upload(p, &f, b_hoist.data(), b_hoist.size())) != WF_OK) return rc;
     a.b_hoist = f;
-    if ((rc = upload(p, &f, w_new.data(), w_new.size())) != WF_OK) return rc;
-    a.wp_new = f;
+    if ((rc = upload(p, &f, w_l1.data(), w_l1.size())) != WF_OK) return rc;
+    a.wp_l1 = f;
     if ((rc = upload(p, &f, w_old.data(), w_old.size())) != WF_OK) return rc;
     a.wp_old = f;
     if ((rc = upload(p, &f, w2.data(), w2.size())) != WF_OK) return rc;
@@ -284,18 +270,13 @@ static int build_plan(const wf_desc* d, Plan* p) {
     if ((rc = alloc(p, &a.h1, R * Np1)) != WF_OK) return rc;
     if ((rc = alloc(p, &a.h2, R * p->Np2)) != WF_OK) return rc;
     if ((rc = alloc(p, &a.p1, nlat * Np1)) != WF_OK) return rc;
-    if ((rc = alloc(p, &a.slots, (size_t)a.nring * R * std::max(1, a.n_old) * Np1)) != WF_OK) return rc;
+    if ((rc = alloc(p, &a.ctxo, (size_t)2 * 3 * R * 2 * M)) != WF_OK) return rc;
     if ((rc = alloc(p, &p->d_call, 1)) != WF_OK) return rc;
     WF_HIP(hipMemset(p->d_call, 0, sizeof(CallPtrs)));
     a.cp = p->d_call;
     if ((rc = alloc(p, &p->d_err, 1)) != WF_OK) return rc;
     WF_HIP(hipMemset(p->d_err, 0, sizeof(int)));
     if (p->driver == WF_DRIVER_PERSISTENT) {
-        // agent-coherent buffer accesses address at most 2 GiB per array
-        const size_t lim = (size_t)1 << 31;
-        if (nlat * M * sizeof(float) >= lim || R * Np1 * sizeof(float) >= lim ||
-            (size_t)a.nring * R * std::max(1, a.n_old) * Np1 * sizeof(float) >= lim)
-            return fail(WF_E_UNSUPPORTED, "an array exceeds 2 GiB (persistent driver)");
         if ((rc = persistent_grid(*p, &p->grid)) != WF_OK) return rc;
         if ((rc = alloc(p, &p->d_bar, kBarrierWords)) != WF_OK) return rc;
         WF_HIP(hipMemset(p->d_bar, 0, kBarrierWords * sizeof(unsigned)));
@@ -420,6 +401,18 @@ int wf_encode(wf_plan_t plan, const float* psi, const float* y, int32_t* sym_out
     int rc = check_out(p, out);
     if (rc != WF_OK) return rc;
     return run_call(p, call_ptrs(psi, nullptr, y, sym_out, out), stream);
+}
+
+int wf_plan_trace(wf_plan_t plan, int64_t* stamps, int64_t capacity, int64_t* needed, int32_t* grid) {
+    if (!plan) return fail(WF_E_INVALID, "plan is NULL");
+    Plan* p = reinterpret_cast<Plan*>(plan);
+    if (p->driver != WF_DRIVER_PERSISTENT) return fail(WF_E_UNSUPPORTED, "tracing needs the persistent driver");
+    if (stamps && capacity < 0) return fail(WF_E_INVALID, "negative capacity");
+    p->stamps = reinterpret_cast<long long*>(stamps);
+    p->stamps_cap = stamps ? capacity : 0;
+    if (needed) *needed = (int64_t)(1 + 3 * (int64_t)p->T) * (p->grid + 1);
+    if (grid) *grid = p->grid;
+    return WF_OK;
 }
 
 int wf_plan_sync(wf_plan_t plan, hipStream_t stream) {

@@ -5,39 +5,55 @@
 namespace wf {
 
 // Pre-loop: P1[lat][n] = b_hoist[n] + sum_k psi[lat][k] * W1[n][k]  (k < 2M)
-__global__ __launch_bounds__(256) void k_hoist(int nlat, StepArgs a) {
+__global__ __launch_bounds__(kThreads) void k_hoist(int nlat, StepArgs a) {
     __shared__ f4 red[kWaves][64];
     const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63, kq = lane >> 4;
     const int ct = blockIdx.x, rt = blockIdx.y;
     const int r = rt * kTile + (lane & 15);
-    const float* __restrict__ psi = a.cp->psi + (size_t)r * 2 * a.M + kq * 4;
+    const float* psi = a.cp->psi;
+    const size_t base = (size_t)r * 2 * a.M + kq * 4;
     const int n = ct * kTile + (lane & 15);
     const float bias = a.b_hoist[n];
-    auto la = [&](int kb) -> f4 {
-        return r < nlat ? *reinterpret_cast<const f4*>(psi + kb * kTile) : zero4();
-    };
+    auto la = [&](int kb) -> f4 { return ld4<false>(psi, base + kb * kTile, r < nlat); };
     const float v = block_tile(red, a.wp_hoist, 2 * a.M / kTile, ct, la);
     const int ro = rt * kTile + kq * 4 + wave;
-    if (ro < nlat) a.p1[(size_t)ro * a.Np1 + n] = v + bias;
+    if (wave < 4 && ro < nlat) a.p1[(size_t)ro * a.Np1 + n] = v + bias;
 }
 
-// Phase A: layer 1 of step s (blocks [0, nb1)) and the push of step sp.
-__global__ __launch_bounds__(256) void k_phase_a(StepRows s, StepRows sp, int nb1, StepArgs a) {
+// Phase A: layer 1 of step s (blocks [0, nb)), then old-tap context jobs
+// [j0, ...) of step s1.
+__global__ __launch_bounds__(kThreads) void k_phase_a(StepRows s, StepRows s1, int nb, int j0, int nc, StepArgs a) {
     __shared__ f4 red[kWaves][64];
-    if ((int)blockIdx.x >= nb1)
-        push_job<false>(a, sp, blockIdx.x - nb1);
-    else
+    if ((int)blockIdx.x < nb)
         l1_job<false>(a, s, blockIdx.x, red);
+    else
+        ctxo_job<false>(a, s1, j0 + blockIdx.x - nb, nc, red);
 }
 
-__global__ __launch_bounds__(256) void k_phase_b(StepRows s, StepArgs a) {
+// Old-tap context jobs of step s1 only (before the first step).
+__global__ __launch_bounds__(kThreads) void k_ctxo(StepRows s1, int nc, StepArgs a) {
     __shared__ f4 red[kWaves][64];
-    l2_job<false>(a, s, blockIdx.x, red);
+    ctxo_job<false>(a, s1, blockIdx.x, nc, red);
 }
 
+// Phase B: layer 2 of step s, then old-tap context jobs.
+__global__ __launch_bounds__(kThreads) void k_phase_b(StepRows s, StepRows s1, int nb, int j0, int nc, StepArgs a) {
+    __shared__ f4 red[kWaves][64];
+    if ((int)blockIdx.x < nb)
+        l2_job<false>(a, s, blockIdx.x, red);
+    else
+        ctxo_job<false>(a, s1, j0 + blockIdx.x - nb, nc, red);
+}
+
+// Phase C: layer 3 and the epilogue of step s, then old-tap context jobs.
 template <int KC>
-__global__ __launch_bounds__(256) void k_phase_c(StepRows s, StepArgs a) {
+__global__ __launch_bounds__(kThreads) void k_phase_c(StepRows s, StepRows s1, int nb, int j0, int nc, StepArgs a) {
     __shared__ L3Smem<KC> sm;
+    __shared__ f4 red[kWaves][64];
+    if ((int)blockIdx.x >= nb) {
+        ctxo_job<false>(a, s1, j0 + blockIdx.x - nb, nc, red);
+        return;
+    }
     for (int l = threadIdx.x; l < a.L; l += blockDim.x) sm.tab[l] = a.table[l];
     __syncthreads();
     l3_job<KC, false>(a, s, blockIdx.x, sm);
@@ -54,25 +70,39 @@ int enqueue_set_call(Plan& p, const CallPtrs& c, hipStream_t stream) {
 
 int enqueue_hoist(Plan& p, hipStream_t stream) {
     const int nlat = p.B * p.H * p.W;
-    hipLaunchKernelGGL(k_hoist, dim3(p.Np1 / kTile, ntiles(nlat)), dim3(256), 0, stream, nlat, p.args);
+    hipLaunchKernelGGL(k_hoist, dim3(p.Np1 / kTile, ntiles(nlat)), dim3(kThreads), 0, stream, nlat, p.args);
     return WF_OK;
+}
+
+// Rows of step t, or an empty step past the end.
+static StepRows rows_of(const Plan& p, int t) {
+    if (t >= p.T) return StepRows{t, 0, 0, 0};
+    return step_rows(p.H, p.W, p.B, p.lambda, t);
 }
 
 int enqueue_steps(Plan& p, hipStream_t stream) {
     const StepArgs& a = p.args;
     enqueue_hoist(p, stream);
-    StepRows prev{0, 0, 0, 0};
+    {
+        const StepRows s0 = rows_of(p, 0);
+        const int nc = ctxo_blocks(a, s0);
+        if (nc > 0) hipLaunchKernelGGL(k_ctxo, dim3(kCtxParts * nc), dim3(kThreads), 0, stream, s0, nc, a);
+    }
     for (int t = 0; t < p.T; ++t) {
-        const StepRows s = step_rows(p.H, p.W, p.B, p.lambda, t);
-        const int nb1 = phase_a_l1_blocks(a, s);
-        const int nbp = t >= 1 ? phase_a_push_blocks(a, prev, p.T) : 0;
-        hipLaunchKernelGGL(k_phase_a, dim3(nb1 + nbp), dim3(256), 0, stream, s, prev, nb1, a);
-        hipLaunchKernelGGL(k_phase_b, dim3(phase_b_blocks(a, s)), dim3(256), 0, stream, s, a);
+        const StepRows s = rows_of(p, t), s1 = rows_of(p, t + 1);
+        const int nc = ctxo_blocks(a, s1);
+        const int nb1 = l1_blocks(a, s), nb2 = l2_blocks(a, s), nb3 = l3_blocks(a, s);
+        int ka, kb, kc, ko;
+        job_costs(a, &ka, &kb, &kc, &ko);
+        const CtxSplit cs = ctxo_split(nc, nb1, nb2, nb3, ka, kb, kc, ko);
+        hipLaunchKernelGGL(k_phase_a, dim3(nb1 + cs.c1), dim3(kThreads), 0, stream, s, s1, nb1, 0, nc, a);
+        hipLaunchKernelGGL(k_phase_b, dim3(nb2 + cs.c2 - cs.c1), dim3(kThreads), 0, stream, s, s1, nb2, cs.c1, nc, a);
         if (p.K == 1)
-            hipLaunchKernelGGL(k_phase_c<1>, dim3(phase_c_blocks(a, s)), dim3(256), 0, stream, s, a);
+            hipLaunchKernelGGL(k_phase_c<1>, dim3(nb3 + cs.total - cs.c2), dim3(kThreads), 0, stream, s, s1, nb3, cs.c2,
+                               nc, a);
         else
-            hipLaunchKernelGGL(k_phase_c<3>, dim3(phase_c_blocks(a, s)), dim3(256), 0, stream, s, a);
-        prev = s;
+            hipLaunchKernelGGL(k_phase_c<3>, dim3(nb3 + cs.total - cs.c2), dim3(kThreads), 0, stream, s, s1, nb3, cs.c2,
+                               nc, a);
     }
     hipError_t err = hipGetLastError();
     if (err != hipSuccess) return fail(WF_E_HIP, std::string("kernel launch: ") + hipGetErrorString(err));

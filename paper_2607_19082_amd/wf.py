@@ -18,7 +18,7 @@ PRECISION = {"fp32": 0, "bf16": 1}
 DRIVER = {"stream": 0, "graph": 1, "persistent": 2}
 
 EXPORTS = ["wf_schedule", "wf_validate", "wf_plan", "wf_plan_schedule", "wf_decode",
-           "wf_encode", "wf_plan_sync", "wf_plan_destroy", "wf_last_error"]
+           "wf_encode", "wf_plan_trace", "wf_plan_sync", "wf_plan_destroy", "wf_last_error"]
 
 
 class WfError(RuntimeError):
@@ -66,6 +66,7 @@ def lib():
         L.wf_plan_schedule.argtypes = [P, P, P]
         L.wf_decode.argtypes = [P, P, P, ctypes.POINTER(Out), P]
         L.wf_encode.argtypes = [P, P, P, P, ctypes.POINTER(Out), P]
+        L.wf_plan_trace.argtypes = [P, P, ctypes.c_int64, P, P]
         L.wf_plan_sync.argtypes = [P, P]
         L.wf_plan_destroy.argtypes = [P]
         L.wf_plan_destroy.restype = None
@@ -208,6 +209,16 @@ class Plan:
         o = self._out_struct(out)
         _check(lib().wf_encode(self._h, p_psi, p_y, p_s, ctypes.byref(o), _stream_handle(stream)))
         return out, sym_out
+
+    def trace(self, stamps=None):
+        """Record barrier timestamps of later calls into the int64 CUDA tensor
+        `stamps` (None: stop).  Returns (entries needed per call, grid)."""
+        needed = ctypes.c_int64()
+        grid = ctypes.c_int32()
+        ptr = ctypes.c_void_p(stamps.data_ptr()) if stamps is not None else None
+        cap = stamps.numel() if stamps is not None else 0
+        _check(lib().wf_plan_trace(self._h, ptr, cap, ctypes.byref(needed), ctypes.byref(grid)))
+        return needed.value, grid.value
 
     def sync(self, stream=None):
         _check(lib().wf_plan_sync(self._h, _stream_handle(stream)))
