@@ -1,10 +1,18 @@
-"""Benchmark: wavefront decode of one 3840x2160 image's latent (240x135, M=320)
-through the C-ABI, on one GPU.
+"""Benchmark: wavefront decode of one 3840x2160 image's latent (240x135 latents,
+M = 320 channels) through the C-ABI, on one MI355X.
 
-One step = one whole decode of the latent grid (every wavefront step: tap
-gather, context product, entropy-parameter network, parameter epilogue and the
-y_hat write).  Inputs are seeded synthetic arrays already resident in HBM.
-Prints one JSON line.
+One step = one whole decode of the latent grid: every wavefront step's tap
+gather, context product, entropy-parameter network, parameter epilogue and
+y_hat write, plus the pre-loop hyperprior product.  Inputs are seeded
+synthetic arrays (weights N(0, 1/fan_in), hyperprior params N(0, 1), Laplace
+symbols) already resident in HBM.  Prints one JSON line.
+
+roofline: with the persistent driver one decode is one kernel launch
+(k_persistent; two tiny set-up kernels ride along, < 0.1% of the time), timed
+with HIP events on the launch stream; achieved = algorithmic FLOPs of a decode
+/ that time, against the dense fp32 (or bf16) MFMA peak.  latency_roofline
+adds the dependency floor: T_roof = hoist / peak + sum over steps of
+max(F_t / peak, L_floor), with L_floor the measured minimal dependent hop.
 """
 import argparse
 import json
@@ -19,20 +27,36 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 PEAK_TFLOPS = {"fp32": 157.3, "bf16": 2500.0}
+DEFAULT_WORKLOAD = "minnen-hr-4k-240x135-m320"
 
 
 def flops_per_latent(cfg):
-    """Algorithmic FLOPs of one latent: 2 x MACs of the context product over
-    the causal taps and of the three network layers."""
+    """Algorithmic FLOPs of one latent (2 x MACs): the context product over the
+    causal taps and the three layers of the entropy-parameter network."""
     M, d1, d2, n3 = cfg["M"], cfg["d1"], cfg["d2"], cfg["n3"]
     taps = 10 if cfg["relaxed"] else 12
     macs = taps * M * 2 * M + 4 * M * d1 + d1 * d2 + d2 * n3
     return 2 * macs
 
 
+def hoistable_flops_per_latent(cfg):
+    """The hyperprior half of layer 1 (computed before the step loop)."""
+    return 2 * 2 * cfg["M"] * cfg["d1"]
+
+
+def step_rows(cfg):
+    H, W, B = cfg["H"], cfg["W"], cfg["B"]
+    lam = 2 if cfg["relaxed"] else 3
+    T = W + lam * (H - 1)
+    rows = np.zeros(T, np.int64)
+    for i in range(H):
+        rows[lam * i:lam * i + W] += B
+    return rows
+
+
 def cpu_baseline(name, rows):
-    """Time the CPU oracle decoding the top `rows` rows of the same workload
-    (the AR dependencies point up and left, so this is an exact decode of
+    """Time the CPU oracle decoding the top `rows` grid rows of the same
+    workload (the causal taps point up and left, so this is an exact decode of
     those latents)."""
     import oracle
     from paper_2607_19082_amd import inputs
@@ -43,10 +67,34 @@ def cpu_baseline(name, rows):
     m.decode(psi, sym)
     dt = time.perf_counter() - t0
     n = cfg["B"] * rows * cfg["W"]
+    cpu = platform.processor() or platform.machine()
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    cpu = line.split(":", 1)[1].strip()
+                    break
+    except OSError:
+        pass
     return {"value": n / dt, "unit": "latents/s", "cores": 1, "kind": "oracle",
-            "sample": f"sequential raster decode of the top {rows} rows ({n} latents) of {name}, "
-                      f"single thread, {dt:.1f} s; host {platform.processor() or platform.machine()}, "
-                      f"{os.cpu_count()} logical cpus"}
+            "sample": f"sequential raster decode (fp64 accumulate) of the top {rows} grid rows "
+                      f"({n} latents) of {name}, one thread, {dt:.1f} s, on {cpu} "
+                      f"({os.cpu_count()} logical cpus)",
+            "ms_per_image_extrapolated": dt * 1e3 * (cfg["H"] / rows)}
+
+
+def timed_calls(fn, steps, stream, torch):
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+          for _ in range(steps)]
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for a, b in ev:
+        a.record(stream)
+        fn()
+        b.record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    return wall, [a.elapsed_time(b) for a, b in ev]
 
 
 def main():
@@ -54,13 +102,15 @@ def main():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=3)
-    ap.add_argument("--workload", default="minnen-hr-4k-240x135-m320")
-    ap.add_argument("--driver", default="graph", choices=["stream", "graph", "persistent"])
+    ap.add_argument("--workload", default=DEFAULT_WORKLOAD)
+    ap.add_argument("--driver", default="persistent", choices=["stream", "graph", "persistent"])
     ap.add_argument("--precision", default="fp32", choices=["fp32", "bf16"])
-    ap.add_argument("--cpu-rows", type=int, default=8, help="rows of the CPU-oracle sample (0: skip)")
+    ap.add_argument("--cpu-rows", type=int, default=8, help="grid rows of the CPU-oracle sample (0: skip)")
+    ap.add_argument("--no-encode", action="store_true")
     args = ap.parse_args()
     if args.gpus != 1:
-        print(json.dumps({"error": "this build runs on one GPU only; --gpus must be 1"}))
+        print(json.dumps({"error": "this build runs on one GPU only (--gpus 1); a multi-GPU run is not "
+                                   "part of it"}))
         sys.exit(2)
 
     import torch
@@ -77,33 +127,50 @@ def main():
     out = plan.alloc_out()
     stream = torch.cuda.current_stream()
 
-    for _ in range(args.warmup):
+    def dec():
         plan.decode(psi_d, sym_d, out=out, stream=stream)
+
+    for _ in range(args.warmup):
+        dec()
+    plan.sync(stream)
+    wall, per = timed_calls(dec, args.steps, stream, torch)
     plan.sync(stream)
 
-    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
-          for _ in range(args.steps)]
-    torch.cuda.synchronize()
-    t0 = time.perf_counter()
-    for a, b in ev:
-        a.record(stream)
-        plan.decode(psi_d, sym_d, out=out, stream=stream)
-        b.record(stream)
-    torch.cuda.synchronize()
-    wall = time.perf_counter() - t0
-    plan.sync(stream)
-    per = [a.elapsed_time(b) for a, b in ev]  # ms, HIP events on the launch stream
+    rec_enc = None
+    if not args.no_encode:
+        u = inputs.make_noise(cfg["B"], cfg["H"], cfg["W"], cfg["M"])
+        y_d = (torch.from_numpy(sym.astype(np.float32) + u).cuda() + out["mean"]).contiguous()
+        out_e = plan.alloc_out()
+        sym_o = torch.empty_like(sym_d)
+
+        def enc():
+            plan.encode(psi_d, y_d, out=out_e, sym_out=sym_o, stream=stream)
+
+        enc()
+        plan.sync(stream)
+        ewall, eper = timed_calls(enc, max(3, args.steps // 4), stream, torch)
+        plan.sync(stream)
+        rec_enc = {"ms_per_image": ewall * 1e3 / max(3, args.steps // 4) / cfg["B"],
+                   "symbols_match_decode": bool(torch.equal(sym_o, sym_d))}
+
+    node_us, bar_us = plan.measure_floor()
+    plan.close()
 
     lat = cfg["B"] * cfg["H"] * cfg["W"]
     ms = wall * 1e3 / args.steps
     value = lat / (ms * 1e-3)
     fl = flops_per_latent(cfg) * lat
     dec_ms = float(np.mean(per))
-    achieved = fl / (dec_ms * 1e-3) / 1e12
     peak = PEAK_TFLOPS[args.precision]
-    T = cfg["W"] + (2 if cfg["relaxed"] else 3) * (cfg["H"] - 1)
+    achieved = fl / (dec_ms * 1e-3) / 1e12
+    rows = step_rows(cfg)
+    lfloor = min(x for x in (node_us, bar_us) if x > 0)
+    f_step = rows * (flops_per_latent(cfg) - hoistable_flops_per_latent(cfg))
+    t_roof_s = (hoistable_flops_per_latent(cfg) * lat) / (peak * 1e12) + np.maximum(
+        f_step / (peak * 1e12), lfloor * 1e-6).sum()
+    T = len(rows)
     rec = {
-        "metric": "latents/s of a whole-image wavefront decode (ms per image in ms_per_step)",
+        "metric": "latents/s of a whole-image wavefront decode (ms per image = ms_per_step)",
         "value": value,
         "unit": "latents/s",
         "n_gpus": 1,
@@ -119,15 +186,19 @@ def main():
                    "B": cfg["B"], "K": cfg["K"], "mask": "relaxed" if cfg["relaxed"] else "full",
                    "steps_T": T, "driver": args.driver, "precision": args.precision,
                    "parallelism": "single GPU"},
-        "roofline": {"bound": "mfma", "kernel": "whole decode (all step kernels, per decode call)",
-                     "achieved": achieved, "peak": peak, "unit": "TFLOP/s",
+        "roofline": {"bound": "mfma", "achieved": achieved, "peak": peak, "unit": "TFLOP/s",
                      "frac": achieved / peak, "traffic": None,
-                     "algorithmic_gflop_per_decode": fl / 1e9, "decode_ms_events": dec_ms,
+                     "kernel": "k_persistent (one launch = one decode)" if args.driver == "persistent"
+                     else "whole decode (all step kernels of one call)",
+                     "algorithmic_gflop_per_launch": fl / 1e9, "launch_ms_events": dec_ms,
                      "mfma_floor_ms": fl / (peak * 1e12) * 1e3},
+        "latency_roofline": {"L_floor_us": lfloor, "graph_node_us": node_us, "barrier_round_us": bar_us,
+                             "hops_per_step_algorithmic": 1, "T_roof_ms": t_roof_s * 1e3,
+                             "frac": t_roof_s * 1e3 / dec_ms},
         "latents_per_s": value,
         "ms_per_image": ms / cfg["B"],
+        "encode": rec_enc,
     }
-    plan.close()
     if args.cpu_rows > 0:
         rec["cpu_baseline"] = cpu_baseline(args.workload, args.cpu_rows)
     print(json.dumps(rec), flush=True)

@@ -170,6 +170,17 @@ int wf_plan_trace(wf_plan_t plan, int64_t *stamps, int64_t capacity, int64_t *ne
                   int32_t *grid);
 
 /*
+ * Latency floor of one dependent step hop on the current device, measured
+ * synchronously on a private stream: *node_us is the per-node time of a chain
+ * of 512 empty kernels replayed from a HIP graph, *barrier_us the time of one
+ * empty round of the persistent driver's device-wide barrier over its grid
+ * (-1 when that grid cannot be resident).  Measurement support for the
+ * latency-aware roofline; it touches no plan state except the device error
+ * word (a barrier timeout is recorded there as for a call).
+ */
+int wf_measure_floor(wf_plan_t plan, float *node_us, float *barrier_us);
+
+/*
  * Wait for `stream` and report a device-side error recorded by the plan's
  * kernels (WF_E_TIMEOUT when a bounded device-wide wait gave up).  Clears the
  * recorded error.

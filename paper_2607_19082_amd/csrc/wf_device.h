@@ -263,6 +263,30 @@ __device__ __forceinline__ float block_tile(f4 (*red)[64], const float* __restri
 }
 
 // ---------------------------------------------------------------------------
+// Pre-loop job b: P1[lat][n] = b_hoist[n] + sum_k psi[lat][k] * W1[n][k]
+// (k < 2M) for one 16x16 tile of the nlat x Np1 product.
+__host__ __device__ __forceinline__ int hoist_blocks(const StepArgs& a) {
+    return xcd_blocks(a.Np1 / kTile, ntiles(a.B * a.H * a.W));
+}
+
+template <bool COH>
+__device__ __forceinline__ void hoist_job(const StepArgs& a, int b, f4 (*red)[64]) {
+    const int nlat = a.B * a.H * a.W;
+    const Job jb = xcd_job(b, a.Np1 / kTile, ntiles(nlat));
+    if (!jb.valid) return;
+    const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63, kq = lane >> 4;
+    const int r = jb.rt * kTile + (lane & 15);
+    const float* psi = a.cp->psi;
+    const size_t base = (size_t)r * 2 * a.M + kq * 4;
+    const int n = jb.ct * kTile + (lane & 15);
+    const float bias = a.b_hoist[n];
+    auto la = [&](int kb) -> f4 { return ld4<false>(psi, base + kb * kTile, r < nlat); };
+    const float v = block_tile(red, a.wp_hoist, 2 * a.M / kTile, jb.ct, la);
+    const int ro = jb.rt * kTile + kq * 4 + wave;
+    if (wave < 4 && ro < nlat) st1<COH>(a.p1, (size_t)ro * a.Np1 + n, v + bias);
+}
+
+// ---------------------------------------------------------------------------
 // Job j of the old-tap context of the latents of step s: k-part part = j / nc
 // (a contiguous range of the k-blocks of the gathered old taps, tap-major)
 // of block j % nc:  ctxo[part][r][n] = sum_{k in part} taps[r][k] Wc[k][n].
@@ -306,7 +330,7 @@ __device__ __forceinline__ void l1_job(const StepArgs& a, const StepRows& s, int
     const int n = jb.ct * kTile + (lane & 15);
     const int ro = wave < 4 ? jb.rt * kTile + kq * 4 + wave : s.nrows;   // epilogue row of this wave
     const Row v = step_row(a, s, ro);
-    const float z = v.valid ? a.p1[v.lat * a.Np1 + n] : 0.0f;
+    const float z = ld1<COH>(a.p1, v.lat * a.Np1 + n, v.valid);
     const int r = jb.rt * kTile + (lane & 15);
     const Row w = step_row(a, s, r);
     const float* yh = a.cp->y_hat;

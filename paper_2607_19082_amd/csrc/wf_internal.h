@@ -113,5 +113,7 @@ int enqueue_hoist(Plan& p, hipStream_t stream);
 // Persistent driver: grid size (checked co-residency) and one call.
 int persistent_grid(Plan& p, int* grid);
 int enqueue_persistent(Plan& p, hipStream_t stream);
+// Latency floor of one dependent step hop (see wf_measure_floor).
+int measure_floor(Plan& p, float* node_us, float* barrier_us);
 
 }  // namespace wf

@@ -67,9 +67,12 @@ __global__ __launch_bounds__(kThreads) void k_persistent(StepArgs a, int T, unsi
     __syncthreads();
     const int G = gridDim.x;
     unsigned k = 0;
+    // pre-loop: the hyperprior half of layer 1 for every latent, and the
     // old-tap context of step 0 (no old tap of step 0 lies in the grid, but
     // the general form keeps the loop uniform)
     {
+        const int nh = hoist_blocks(a);
+        for (int b = blockIdx.x; b < nh; b += G) hoist_job<true>(a, b, red);
         const StepRows s0 = step_rows(a.H, a.W, a.B, a.lambda, 0);
         const int nc = ctxo_blocks(a, s0);
         for (int b = blockIdx.x; b < kCtxParts * nc; b += G) ctxo_job<true>(a, s0, b, nc, red);
@@ -131,7 +134,6 @@ int persistent_grid(Plan& p, int* grid) {
 }
 
 int enqueue_persistent(Plan& p, hipStream_t stream) {
-    enqueue_hoist(p, stream);
     hipLaunchKernelGGL(k_zero_u32, dim3(1), dim3(256), 0, stream, p.d_bar, kBarrierWords);
     StepArgs a = p.args;
     int T = p.T;
@@ -143,6 +145,83 @@ int enqueue_persistent(Plan& p, hipStream_t stream) {
     hipError_t e = hipLaunchCooperativeKernel(persistent_fn(p.K), dim3(p.grid), dim3(kThreads), args, 0, stream);
     if (e != hipSuccess) return fail(WF_E_HIP, std::string("cooperative launch: ") + hipGetErrorString(e));
     return WF_OK;
+}
+
+__global__ void k_empty(int* p) {
+    if (p && threadIdx.x == 0 && blockIdx.x == 0 && p[0] == 12345) p[1] = 1;
+}
+
+// `rounds` empty device-wide barrier rounds over the whole grid.
+__global__ __launch_bounds__(kThreads) void k_barrier_rounds(unsigned* ctr, int* err, long long budget, int rounds) {
+    __shared__ int bail;
+    const Trace tr{nullptr, 0};
+    for (int r = 1; r <= rounds; ++r)
+        if (!grid_barrier(ctr, (unsigned)r, err, budget, &bail, tr)) return;
+}
+
+int measure_floor(Plan& p, float* node_us, float* barrier_us) {
+#define WF_FLOOR(call)                                                                      \
+    do {                                                                                    \
+        hipError_t e_ = (call);                                                             \
+        if (e_ != hipSuccess) {                                                             \
+            if (g) (void)hipGraphDestroy(g);                                                \
+            if (ge) (void)hipGraphExecDestroy(ge);                                          \
+            if (st) (void)hipStreamDestroy(st);                                             \
+            if (e0) (void)hipEventDestroy(e0);                                              \
+            if (e1) (void)hipEventDestroy(e1);                                              \
+            return fail(WF_E_HIP, std::string(#call) + ": " + hipGetErrorString(e_));       \
+        }                                                                                   \
+    } while (0)
+    hipStream_t st = nullptr;
+    hipGraph_t g = nullptr;
+    hipGraphExec_t ge = nullptr;
+    hipEvent_t e0 = nullptr, e1 = nullptr;
+    const int nodes = 512, rounds = 1024;
+    float ms = 0.0f;
+    WF_FLOOR(hipStreamCreateWithFlags(&st, hipStreamNonBlocking));
+    WF_FLOOR(hipEventCreate(&e0));
+    WF_FLOOR(hipEventCreate(&e1));
+    // (i) a chain of empty kernels replayed from a graph: per-node latency
+    WF_FLOOR(hipStreamBeginCapture(st, hipStreamCaptureModeThreadLocal));
+    for (int i = 0; i < nodes; ++i) hipLaunchKernelGGL(k_empty, dim3(1), dim3(64), 0, st, nullptr);
+    WF_FLOOR(hipStreamEndCapture(st, &g));
+    WF_FLOOR(hipGraphInstantiate(&ge, g, nullptr, nullptr, 0));
+    WF_FLOOR(hipGraphLaunch(ge, st));
+    WF_FLOOR(hipEventRecord(e0, st));
+    WF_FLOOR(hipGraphLaunch(ge, st));
+    WF_FLOOR(hipEventRecord(e1, st));
+    WF_FLOOR(hipEventSynchronize(e1));
+    WF_FLOOR(hipEventElapsedTime(&ms, e0, e1));
+    *node_us = ms * 1e3f / nodes;
+    // (ii) empty device-wide barrier rounds over the persistent grid
+    *barrier_us = -1.0f;
+    int grid = p.grid;
+    if (grid == 0 && persistent_grid(p, &grid) != WF_OK) grid = 0;
+    if (grid > 0) {
+        unsigned* ctr = nullptr;
+        WF_FLOOR(hipMalloc((void**)&ctr, kBarrierWords * sizeof(unsigned)));
+        int* err = p.d_err;
+        long long budget = p.spin_budget;
+        int r = rounds;
+        void* args[] = {&ctr, &err, &budget, &r};
+        hipError_t e = hipMemsetAsync(ctr, 0, kBarrierWords * sizeof(unsigned), st);
+        if (e == hipSuccess) e = hipEventRecord(e0, st);
+        if (e == hipSuccess)
+            e = hipLaunchCooperativeKernel((const void*)k_barrier_rounds, dim3(grid), dim3(kThreads), args, 0, st);
+        if (e == hipSuccess) e = hipEventRecord(e1, st);
+        if (e == hipSuccess) e = hipEventSynchronize(e1);
+        if (e == hipSuccess) e = hipEventElapsedTime(&ms, e0, e1);
+        (void)hipFree(ctr);
+        WF_FLOOR(e);
+        *barrier_us = ms * 1e3f / rounds;
+    }
+    (void)hipGraphExecDestroy(ge);
+    (void)hipGraphDestroy(g);
+    (void)hipEventDestroy(e0);
+    (void)hipEventDestroy(e1);
+    (void)hipStreamDestroy(st);
+    return WF_OK;
+#undef WF_FLOOR
 }
 
 }  // namespace wf

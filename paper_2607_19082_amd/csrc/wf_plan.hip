@@ -52,6 +52,8 @@ static int least_shear(int ntaps, const int* dy, const int* dx) {
     return -1;
 }
 
+static int round16(int v) { return (v + kTile - 1) / kTile * kTile; }
+
 static int check_desc(const wf_desc* d) {
     if (!d) return fail(WF_E_INVALID, "desc is NULL");
     if (d->H < 1 || d->W < 1 || d->M < 1 || d->B < 1)
@@ -83,13 +85,12 @@ static int check_desc(const wf_desc* d) {
     // every array the kernels read through raw buffer instructions (psi, y_hat,
     // the per-step activations) must fit the buffer window
     const long long lat = (long long)d->B * d->H * d->W;
-    if (lat * 2 * d->M * 4 >= kBufBytes || lat * 3 * d->M > (1LL << 31) - 1)
+    if (lat * 2 * d->M * 4 >= kBufBytes || lat * round16(d->d1) * 4 >= kBufBytes ||
+        lat * 3 * d->M > (1LL << 31) - 1)
         return fail(WF_E_UNSUPPORTED, "problem too large for the 2 GiB buffer window");
     if (d->precision == WF_BF16) return fail(WF_E_UNSUPPORTED, "bf16 operands are not built yet");
     return WF_OK;
 }
-
-static int round16(int v) { return (v + kTile - 1) / kTile * kTile; }
 
 // Pack Wt[k][n] (k < K, n < N; zero beyond) into the MFMA operand order used
 // by the step kernels: for column tile ct and k-block kb (16 values of k),
@@ -413,6 +414,11 @@ int wf_plan_trace(wf_plan_t plan, int64_t* stamps, int64_t capacity, int64_t* ne
     if (needed) *needed = (int64_t)(1 + 3 * (int64_t)p->T) * (p->grid + 1);
     if (grid) *grid = p->grid;
     return WF_OK;
+}
+
+int wf_measure_floor(wf_plan_t plan, float* node_us, float* barrier_us) {
+    if (!plan || !node_us || !barrier_us) return fail(WF_E_INVALID, "plan or an output is NULL");
+    return measure_floor(*reinterpret_cast<Plan*>(plan), node_us, barrier_us);
 }
 
 int wf_plan_sync(wf_plan_t plan, hipStream_t stream) {

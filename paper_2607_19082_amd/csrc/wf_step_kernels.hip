@@ -4,20 +4,10 @@
 
 namespace wf {
 
-// Pre-loop: P1[lat][n] = b_hoist[n] + sum_k psi[lat][k] * W1[n][k]  (k < 2M)
-__global__ __launch_bounds__(kThreads) void k_hoist(int nlat, StepArgs a) {
+// Pre-loop: the hyperprior half of layer 1 for every latent.
+__global__ __launch_bounds__(kThreads) void k_hoist(StepArgs a) {
     __shared__ f4 red[kWaves][64];
-    const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63, kq = lane >> 4;
-    const int ct = blockIdx.x, rt = blockIdx.y;
-    const int r = rt * kTile + (lane & 15);
-    const float* psi = a.cp->psi;
-    const size_t base = (size_t)r * 2 * a.M + kq * 4;
-    const int n = ct * kTile + (lane & 15);
-    const float bias = a.b_hoist[n];
-    auto la = [&](int kb) -> f4 { return ld4<false>(psi, base + kb * kTile, r < nlat); };
-    const float v = block_tile(red, a.wp_hoist, 2 * a.M / kTile, ct, la);
-    const int ro = rt * kTile + kq * 4 + wave;
-    if (wave < 4 && ro < nlat) a.p1[(size_t)ro * a.Np1 + n] = v + bias;
+    hoist_job<false>(a, blockIdx.x, red);
 }
 
 // Phase A: layer 1 of step s (blocks [0, nb)), then old-tap context jobs
@@ -69,8 +59,7 @@ int enqueue_set_call(Plan& p, const CallPtrs& c, hipStream_t stream) {
 }
 
 int enqueue_hoist(Plan& p, hipStream_t stream) {
-    const int nlat = p.B * p.H * p.W;
-    hipLaunchKernelGGL(k_hoist, dim3(p.Np1 / kTile, ntiles(nlat)), dim3(kThreads), 0, stream, nlat, p.args);
+    hipLaunchKernelGGL(k_hoist, dim3(hoist_blocks(p.args)), dim3(kThreads), 0, stream, p.args);
     return WF_OK;
 }
 

@@ -18,7 +18,8 @@ PRECISION = {"fp32": 0, "bf16": 1}
 DRIVER = {"stream": 0, "graph": 1, "persistent": 2}
 
 EXPORTS = ["wf_schedule", "wf_validate", "wf_plan", "wf_plan_schedule", "wf_decode",
-           "wf_encode", "wf_plan_trace", "wf_plan_sync", "wf_plan_destroy", "wf_last_error"]
+           "wf_encode", "wf_plan_trace", "wf_measure_floor", "wf_plan_sync", "wf_plan_destroy",
+           "wf_last_error"]
 
 
 class WfError(RuntimeError):
@@ -67,6 +68,7 @@ def lib():
         L.wf_decode.argtypes = [P, P, P, ctypes.POINTER(Out), P]
         L.wf_encode.argtypes = [P, P, P, P, ctypes.POINTER(Out), P]
         L.wf_plan_trace.argtypes = [P, P, ctypes.c_int64, P, P]
+        L.wf_measure_floor.argtypes = [P, P, P]
         L.wf_plan_sync.argtypes = [P, P]
         L.wf_plan_destroy.argtypes = [P]
         L.wf_plan_destroy.restype = None
@@ -219,6 +221,13 @@ class Plan:
         cap = stamps.numel() if stamps is not None else 0
         _check(lib().wf_plan_trace(self._h, ptr, cap, ctypes.byref(needed), ctypes.byref(grid)))
         return needed.value, grid.value
+
+    def measure_floor(self):
+        """(graph node us, barrier round us) latency floors on this device."""
+        node = ctypes.c_float()
+        bar = ctypes.c_float()
+        _check(lib().wf_measure_floor(self._h, ctypes.byref(node), ctypes.byref(bar)))
+        return node.value, bar.value
 
     def sync(self, stream=None):
         _check(lib().wf_plan_sync(self._h, _stream_handle(stream)))
