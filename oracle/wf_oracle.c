@@ -18,10 +18,15 @@
  * bits (Sec. III-A); the wavefront order of Sec. III-B is one of them.
  *
  * Arithmetic: every dot product is accumulated in fp64 starting from the
- * bias, and every stored vector is rounded to fp32.  In bf16 mode every GEMM
- * operand (weights, gathered taps, hyperprior params, context, hidden
- * activations) is first rounded to bf16 (round half to even); biases and the
- * parameter epilogue stay fp32.
+ * bias, and every stored vector is rounded to fp32.  In bf16 mode every weight
+ * is rounded to bf16 (round half to even), and every activation operand
+ * (gathered taps, hyperprior params, context, hidden activations) is carried
+ * as the sum of two bf16 values, hi = bf16(x) and lo = bf16(x - hi), which
+ * holds x to about 2^-17 relative; biases and the parameter epilogue stay
+ * fp32.  (Rounding the activations to one bf16 each makes the decode
+ * ill-conditioned: a 1e-6 difference in accumulation order re-rounds a tap by
+ * a whole bf16 step and the change spreads along the wavefront, so two
+ * correct evaluations no longer agree to 1e-2.)
  *
  * Readings where the paper is silent (each also listed in the design notes):
  *  - out-of-image taps contribute zero (Def. 1 keeps only in-image edges);
@@ -45,7 +50,7 @@ typedef struct {
     int32_t H, W, M, B, K;      /* rows, cols, channels, images, mixture comps */
     int32_t d1, d2;             /* hidden widths of the parameter network     */
     int32_t relaxed;            /* 1: drop taps (-1,+2) and (-2,+2)           */
-    int32_t bf16;               /* 1: round GEMM operands to bf16             */
+    int32_t bf16;               /* 1: bf16 weights, activations as bf16 pairs */
     float slope;                /* LeakyReLU negative slope                   */
     const float *ctx_w;         /* [2M][M][5][5]                              */
     const float *ctx_b;         /* [2M]                                       */
@@ -81,9 +86,20 @@ static float to_bf16(float v)
     return v;
 }
 
-static float operand(const oracle_model *m, float v)
+/* A weight operand: rounded to bf16 in bf16 mode. */
+static double weight_op(const oracle_model *m, float w)
 {
-    return m->bf16 ? to_bf16(v) : v;
+    return (double)(m->bf16 ? to_bf16(w) : w);
+}
+
+/* An activation operand: hi + lo, two bf16 values, in bf16 mode (x - hi is
+ * exact in fp32, and so is hi + lo). */
+static double act_op(const oracle_model *m, float x)
+{
+    if (!m->bf16) return (double)x;
+    float hi = to_bf16(x);
+    float lo = to_bf16(x - hi);
+    return (double)hi + (double)lo;
 }
 
 /* Is the causal tap (dy,dx) part of the mask?  The 5x5 causal mask keeps
@@ -135,7 +151,7 @@ static void latent_params(const oracle_model *m, const float *y_hat,
                 const float *src = y_hat + (((size_t)b * H + ii) * W + jj) * M;
                 for (int c = 0; c < M; ++c) {
                     float w = m->ctx_w[(((size_t)oc * M + c) * 5 + (dy + 2)) * 5 + (dx + 2)];
-                    acc += (double)operand(m, w) * (double)operand(m, src[c]);
+                    acc += weight_op(m, w) * act_op(m, src[c]);
                 }
             }
         }
@@ -147,20 +163,20 @@ static void latent_params(const oracle_model *m, const float *y_hat,
     for (int n = 0; n < m->d1; ++n) {
         double acc = (double)m->b1[n];
         for (int k = 0; k < 4 * M; ++k)
-            acc += (double)operand(m, m->w1[(size_t)n * 4 * M + k]) * (double)operand(m, h0[k]);
+            acc += weight_op(m, m->w1[(size_t)n * 4 * M + k]) * act_op(m, h0[k]);
         h1[n] = lrelu(m, (float)acc);
     }
     for (int n = 0; n < m->d2; ++n) {
         double acc = (double)m->b2[n];
         for (int k = 0; k < m->d1; ++k)
-            acc += (double)operand(m, m->w2[(size_t)n * m->d1 + k]) * (double)operand(m, h1[k]);
+            acc += weight_op(m, m->w2[(size_t)n * m->d1 + k]) * act_op(m, h1[k]);
         h2[n] = lrelu(m, (float)acc);
     }
     const size_t n3 = n3_of(m);
     for (size_t n = 0; n < n3; ++n) {
         double acc = (double)m->b3[n];
         for (int k = 0; k < m->d2; ++k)
-            acc += (double)operand(m, m->w3[n * m->d2 + k]) * (double)operand(m, h2[k]);
+            acc += weight_op(m, m->w3[n * m->d2 + k]) * act_op(m, h2[k]);
         o[n] = (float)acc;
     }
 

@@ -50,17 +50,25 @@ def bf16_round(a):
     return torch.from_numpy(np.asarray(a, np.float32)).to(torch.bfloat16).to(torch.float32).numpy()
 
 
+def bf16_pair(a):
+    """An activation as the sum of two bf16 values: hi = bf16(a), lo = bf16(a - hi)."""
+    a = np.asarray(a, np.float32)
+    hi = bf16_round(a)
+    return hi.astype(np.float64) + bf16_round(a - hi).astype(np.float64)
+
+
 def library_params(w, table, y_hat, psi, K, relaxed=False, bf16=False, slope=0.01):
     """Per-latent parameters from a fixed reconstruction, built from library
     routines in fp64 (the 'obviously right' form of the per-latent function)."""
     B, H, Wd, M = y_hat.shape
-    op = bf16_round if bf16 else (lambda a: np.asarray(a, np.float32))
+    op = bf16_round if bf16 else (lambda a: np.asarray(a, np.float32))          # weights
+    act = bf16_pair if bf16 else (lambda a: np.asarray(a, np.float32))          # activations
     cw = op(w["ctx_w"]).astype(np.float64) * fig2d_mask(relaxed)[None, None]
-    x = torch.from_numpy(op(y_hat).astype(np.float64)).permute(0, 3, 1, 2)
+    x = torch.from_numpy(act(y_hat).astype(np.float64)).permute(0, 3, 1, 2)
     ctx = torch.nn.functional.conv2d(x, torch.from_numpy(cw), torch.from_numpy(w["ctx_b"].astype(np.float64)),
                                      padding=2).permute(0, 2, 3, 1).numpy()
     h0 = np.concatenate([psi.astype(np.float64), ctx], axis=-1)
-    h0 = op(h0.astype(np.float32)).astype(np.float64) if bf16 else h0
+    h0 = act(h0.astype(np.float32)).astype(np.float64) if bf16 else h0
 
     def layer(h, wm, bv, act):
         z = h @ op(wm).astype(np.float64).T + bv.astype(np.float64)
@@ -69,9 +77,9 @@ def library_params(w, table, y_hat, psi, K, relaxed=False, bf16=False, slope=0.0
         return z
 
     h1 = layer(h0, w["w1"], w["b1"], True)
-    h1 = op(h1.astype(np.float32)).astype(np.float64) if bf16 else h1
+    h1 = act(h1.astype(np.float32)).astype(np.float64) if bf16 else h1
     h2 = layer(h1, w["w2"], w["b2"], True)
-    h2 = op(h2.astype(np.float32)).astype(np.float64) if bf16 else h2
+    h2 = act(h2.astype(np.float32)).astype(np.float64) if bf16 else h2
     o = layer(h2, w["w3"], w["b3"], False)
     if K == 1:
         mu = o[..., :M]
@@ -137,10 +145,27 @@ def test_fixed_point_bf16():
     m = oracle.Model(w, table, 5, 6, 1, 1, bf16=True)
     out = m.decode(psi, sym)
     check_fixed_point(out, sym, w, table, psi, 1, bf16=True, atol=5e-5)
-    # and it differs from fp32 by the bf16 operand rounding, not more
+    # and it differs from fp32 by the bf16 weight rounding, not more
     ref = oracle.Model(w, table, 5, 6, 1, 1).decode(psi, sym)
     d = np.abs(ref["mean"] - out["mean"]).max()
     assert 1e-4 < d < 0.1
+
+
+def test_bf16_rounds_weights_only_to_one_bf16():
+    # With weights that are already bf16 numbers, bf16 mode only re-represents
+    # the activations as bf16 pairs (about 2^-17 relative): it must then agree
+    # with fp32 mode far below one bf16 step of an activation.  Rounding the
+    # activations to a single bf16 would differ by ~1e-2 here.
+    w, table, psi, sym = small_case(M=16, K=3, H=5, W=6)
+    wb = {k: (bf16_round(v) if k in ("ctx_w", "w1", "w2", "w3") else v) for k, v in w.items()}
+    a = oracle.Model(wb, table, 5, 6, 1, 3, bf16=True).decode(psi, sym)
+    b = oracle.Model(wb, table, 5, 6, 1, 3).decode(psi, sym)
+    for k in ("mean", "scale", "comp_mean", "weight"):
+        assert np.abs(a[k] - b[k]).max() < 2e-4, k
+    # the pair holds an activation to 2^-16 relative, one bf16 only to 2^-9
+    x = np.random.default_rng(5).normal(0, 3, 10000).astype(np.float32)
+    assert np.all(np.abs(bf16_pair(x) - x) <= 2.0 ** -16 * np.abs(x))
+    assert np.abs(bf16_round(x) - x).max() > 2.0 ** -12 * np.abs(x).max()
 
 
 def random_topological_order(H, W, B, ds, rng):
