@@ -48,9 +48,15 @@ typedef enum {
     WF_MASK_RELAXED = 1     /* 10 taps: the full mask without (-1,+2) and (-2,+2); lambda = 2    */
 } wf_mask;
 
+/* Operand precision of every product (the paper fixes none; fp32 is the
+ * reference).  WF_BF16 runs every product on bf16 MFMA with fp32 accumulation:
+ * weights are rounded to bf16 (round to nearest even); each activation (taps,
+ * hyperprior params, context, hidden vectors) is carried as the pair
+ * hi = bf16(x), lo = bf16(x - hi), about 2^-17 relative, so the weights are
+ * the only coarse rounding.  Needs M a multiple of 32. */
 typedef enum {
     WF_FP32 = 0,            /* fp32 operands, fp32 accumulate                           */
-    WF_BF16 = 1             /* bf16 (round-to-nearest-even) operands, fp32 accumulate   */
+    WF_BF16 = 1             /* bf16 weights, bf16-pair activations, fp32 accumulate     */
 } wf_precision;
 
 typedef enum {

@@ -1,19 +1,30 @@
 // Device code shared by the per-step kernels and the persistent kernel: the
-// MFMA tile engine and the work of the three phases of a wavefront step.
+// MFMA tile engine and the work of the phases of a wavefront step.
 //
-// For step t (Sec. III-C):
+// fp32 operands, step t (Sec. III-C), three phases:
 //   phase A  h1 = lrelu(P1 + [new taps ; ctx_old(t)] . [F_new ; W1b])
 //   phase B  h2 = lrelu(W2 . h1 + b2)
 //   phase C  o  = W3 . h2 + b3 -> mean / scale / index, y_hat = s + mean
-// and, spread over the three phases to even out their work, the kCtxParts
-// k-parts of ctx_old(t+1) (see ctxo_split).
 // with P1 = b1 + W1b . bc + W1[:, :2M] . psi hoisted before the loop,
 // W1b = W1[:, 2M:], F_new = W1b . Wc[new taps] folded at plan time, and
 // ctx_old(t+1) = Wc[old taps] . y_hat[old taps] for the latents of step t+1
 // (its inputs were all written by step t-1 or earlier).
 //
-// Every product runs on fp32 MFMA (v_mfma_f32_16x16x4f32).  Each wave issues
-// all operand loads of its k-range before its first MFMA, and the epilogue
+// bf16 operands (weights rounded to bf16, every activation carried as a pair
+// of bf16 values hi = bf16(x), lo = bf16(x - hi), fp32 accumulation): the
+// context vector is an activation operand of its own, so it is formed before
+// layer 1 and the fold above does not apply; four phases:
+//   phase N  ctx = pair(bc + ctx_old(t) + Wc[new] . pair(y_hat[new taps]))
+//   phase A  h1  = pair(lrelu(P1 + W1b . ctx)),  P1 = b1 + W1[:, :2M] . pair(psi)
+//   phase B  h2  = pair(lrelu(W2 . h1 + b2))
+//   phase C  as above; also keeps the pair form of y_hat for the tap gathers.
+// A pair array holds each row as [hi plane (n values) | lo plane (n values)].
+// In both, the kCtxParts k-parts of ctx_old(t+1) ride along with the phases
+// of step t, spread to even out their work (see ctxo_split).
+//
+// Every product runs on MFMA: fp32 v_mfma_f32_16x16x4f32 (four chained per
+// 16 values of k) or bf16 v_mfma_f32_16x16x32_bf16.  Each wave issues all
+// operand loads of its k-range before its first MFMA, and the epilogue
 // operands are fetched before the products.  Jobs are placed XCD-aware:
 // block b runs on XCD b % 8, and each column tile of a weight matrix is always
 // computed on the same XCD, which then streams only its slice of the weights.
@@ -29,12 +40,20 @@
 namespace wf {
 
 typedef float f4 __attribute__((ext_vector_type(4)));
+typedef __bf16 b8 __attribute__((ext_vector_type(8)));
+struct b8x2 {   // eight activation values as bf16 pairs
+    b8 hi, lo;
+};
 
 constexpr int kWaves = 4;              // waves per workgroup; they split a tile's k-blocks
 constexpr int kThreads = 64 * kWaves;
 constexpr int kCtxParts = 3;  // k-parts of the old-tap context product
-constexpr int kKbw = 10;   // k-blocks (16 values of k) loaded by a wave before its MFMAs
+constexpr int kKbw = 10;   // k-blocks loaded by a wave before its MFMAs
 constexpr int kSc1 = 16;   // cache-policy bits of an agent-coherent buffer access
+constexpr int kMaxPhases = 4;
+
+// Phases of a step, in order; fp32 runs PH_A..PH_C, bf16 PH_N..PH_C.
+enum { PH_N = 0, PH_A = 1, PH_B = 2, PH_C = 3 };
 
 __device__ __forceinline__ f4 mfma_k16(f4 a, f4 b, f4 acc) {
     // Lane l supplies A[l%16][4*(l/16)+q] and B[4*(l/16)+q][l%16] for the q-th
@@ -46,9 +65,57 @@ __device__ __forceinline__ f4 mfma_k16(f4 a, f4 b, f4 acc) {
     return acc;
 }
 
+// Operand precisions.  A k-block is the k extent of one lane operand of a
+// 16x16 tile (16 values for fp32, 32 for bf16); lane l supplies A row l%16 /
+// B column l%16 at the k-group l/16 of the block, 4 (fp32) or 8 (bf16)
+// consecutive k, so one 16-byte load per lane per k-block feeds B (and A, or
+// each half of a bf16 activation pair).  The products only need A and B to
+// use the same k order, which the packing of the weights and the activation
+// loads share.  A bf16 k-block is two MFMAs: weights times hi, times lo.
+struct PF32 {
+    using A = f4;   // activation operand
+    using B = f4;   // weight operand
+    static constexpr int kK = 16;
+    static constexpr bool kBf16 = false;
+    static constexpr int kFirst = PH_A;
+    static constexpr int kL3Kbw1 = 16, kL3Kbw3 = 4;   // k-blocks in flight per l3 wave (K = 1, 3)
+    __device__ static __forceinline__ f4 mma(A a, B b, f4 acc) { return mfma_k16(a, b, acc); }
+};
+struct PBF16 {
+    using A = b8x2;
+    using B = b8;
+    static constexpr int kK = 32;
+    static constexpr bool kBf16 = true;
+    static constexpr int kFirst = PH_N;
+    static constexpr int kL3Kbw1 = 8, kL3Kbw3 = 3;
+    __device__ static __forceinline__ f4 mma(A a, B b, f4 acc) {
+        acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a.hi, b, acc, 0, 0, 0);
+        return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a.lo, b, acc, 0, 0, 0);
+    }
+};
+
 __device__ __forceinline__ float lrelu(float v, float s) { return v >= 0.0f ? v : s * v; }
 
 __device__ __forceinline__ f4 zero4() { return f4{0.0f, 0.0f, 0.0f, 0.0f}; }
+
+// fp32 -> bf16, round to nearest even (v_cvt_pk_bf16_f32 in the default mode).
+__device__ __forceinline__ uint16_t bf16_bits(float v) { return __builtin_bit_cast(uint16_t, (__bf16)v); }
+__device__ __forceinline__ float bf16_value(uint16_t h) { return __builtin_bit_cast(float, (unsigned)h << 16); }
+
+__device__ __forceinline__ b8 to_b8(f4 a, f4 b) {
+    b8 r;
+    r[0] = (__bf16)a.x; r[1] = (__bf16)a.y; r[2] = (__bf16)a.z; r[3] = (__bf16)a.w;
+    r[4] = (__bf16)b.x; r[5] = (__bf16)b.y; r[6] = (__bf16)b.z; r[7] = (__bf16)b.w;
+    return r;
+}
+
+// Eight fp32 values as bf16 pairs (x - hi is exact in fp32).
+__device__ __forceinline__ b8x2 split8(f4 a, f4 b) {
+    const b8 hi = to_b8(a, b);
+    const f4 ha{(float)hi[0], (float)hi[1], (float)hi[2], (float)hi[3]};
+    const f4 hb{(float)hi[4], (float)hi[5], (float)hi[6], (float)hi[7]};
+    return b8x2{hi, to_b8(a - ha, b - hb)};
+}
 
 // Raw buffer resource over [p, p + kBufBytes): accesses at or past kBufBytes
 // return zero.  Every base pointer used here is the same for the whole wave;
@@ -83,12 +150,55 @@ __device__ __forceinline__ float ld1(const float* base, size_t idx, bool ok = tr
     const int off = ok ? (int)(idx * 4) : kOob;
     return __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(rsrc(base), off, 0, COH ? kSc1 : 0));
 }
+// eight bf16 values at element idx of a bf16 array
+template <bool COH>
+__device__ __forceinline__ b8 ld8h(const uint16_t* base, size_t idx, bool ok = true) {
+    const int off = ok ? (int)(idx * 2) : kOob;
+    return __builtin_bit_cast(b8, __builtin_amdgcn_raw_buffer_load_b128(rsrc(base), off, 0, COH ? kSc1 : 0));
+}
 template <bool COH>
 __device__ __forceinline__ void st1(float* base, size_t idx, float v) {
     if (COH)
         __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(unsigned, v), rsrc(base), (int)(idx * 4), 0, kSc1);
     else
         base[idx] = v;
+}
+template <bool COH>
+__device__ __forceinline__ void st1h(uint16_t* base, size_t idx, uint16_t h) {
+    if (COH)
+        __builtin_amdgcn_raw_buffer_store_b16(h, rsrc(base), (int)(idx * 2), 0, kSc1);
+    else
+        base[idx] = h;
+}
+
+// Activation arrays: fp32 rows of n values, or bf16 pair rows of 2n values
+// ([hi plane | lo plane]).  act_row is the first element of row r.
+template <class P>
+__device__ __forceinline__ size_t act_row(size_t r, int n) {
+    return r * (size_t)n * (P::kBf16 ? 2 : 1);
+}
+// A operand of k-block kb of the row starting at element `row` (n values).
+template <class P, bool COH>
+__device__ __forceinline__ typename P::A ld_act(const void* base, size_t row, int n, int kb, int kq, bool ok) {
+    if constexpr (P::kBf16) {
+        const uint16_t* h = static_cast<const uint16_t*>(base);
+        const size_t q = row + (size_t)kb * 32 + kq * 8;
+        return b8x2{ld8h<COH>(h, q, ok), ld8h<COH>(h, q + n, ok)};
+    } else {
+        return ld4<COH>(static_cast<const float*>(base), row + (size_t)kb * 16 + kq * 4, ok);
+    }
+}
+// Store value v of column col of the row starting at element `row`.
+template <class P, bool COH>
+__device__ __forceinline__ void st_act(void* base, size_t row, int n, int col, float v) {
+    if constexpr (P::kBf16) {
+        uint16_t* h = static_cast<uint16_t*>(base);
+        const uint16_t hi = bf16_bits(v);
+        st1h<COH>(h, row + col, hi);
+        st1h<COH>(h, row + n + col, bf16_bits(v - bf16_value(hi)));
+    } else {
+        st1<COH>(static_cast<float*>(base), row + col, v);
+    }
 }
 
 // Rows of one step: B images x n latents; row r is image r / n, grid row
@@ -157,15 +267,17 @@ __host__ __device__ __forceinline__ int xcd_blocks(int nct, int nrt) {
 
 __host__ __device__ __forceinline__ int ntiles(int n) { return (n + kTile - 1) / kTile; }
 
-// Block counts of the jobs of a step.
-__host__ __device__ __forceinline__ int l1_blocks(const StepArgs& a, const StepRows& s) {
-    return xcd_blocks(a.Np1 / kTile, ntiles(s.nrows));
+// Output column tiles of the main job of each phase.
+__host__ __device__ __forceinline__ int phase_cols(const StepArgs& a, int ph) {
+    switch (ph) {
+        case PH_N: return 2 * a.M / kTile;
+        case PH_A: return a.Np1 / kTile;
+        case PH_B: return a.Np2 / kTile;
+        default: return 2 * a.M / kTile;   // PH_C: value group x channel group
+    }
 }
-__host__ __device__ __forceinline__ int l2_blocks(const StepArgs& a, const StepRows& s) {
-    return xcd_blocks(a.Np2 / kTile, ntiles(s.nrows));
-}
-__host__ __device__ __forceinline__ int l3_blocks(const StepArgs& a, const StepRows& s) {
-    return xcd_blocks(2 * a.M / kTile, ntiles(s.nrows));
+__host__ __device__ __forceinline__ int phase_blocks(const StepArgs& a, const StepRows& s, int ph) {
+    return xcd_blocks(phase_cols(a, ph), ntiles(s.nrows));
 }
 // one k-part of the old-tap context of the latents of step s (nrows may be 0)
 __host__ __device__ __forceinline__ int ctxo_blocks(const StepArgs& a, const StepRows& s) {
@@ -173,38 +285,60 @@ __host__ __device__ __forceinline__ int ctxo_blocks(const StepArgs& a, const Ste
     return xcd_blocks(2 * a.M / kTile, ntiles(s.nrows));
 }
 
-// Which of the kCtxParts * nc old-tap context jobs of the next step ride along
-// with each phase: phase A takes jobs [0, c1), B [c1, c2), C [c2, total).
-// The cuts equalise the k-blocks each phase streams (a job of phase A, B, C
-// and of the old-tap context costs ka, kb, kc, ko k-blocks), so that every
-// phase holds about the same work; they are multiples of 8, which keeps every
-// job on the XCD its column tile belongs to.
-struct CtxSplit {
-    int c1, c2, total;
-};
-__host__ __device__ __forceinline__ CtxSplit ctxo_split(int nc, int nb1, int nb2, int nb3, int ka, int kb, int kc,
-                                                        int ko) {
-    CtxSplit c;
-    c.total = kCtxParts * nc;
-    const long long wa = (long long)nb1 * ka, wb = (long long)nb2 * kb, wc = (long long)nb3 * kc;
-    const long long each = (wa + wb + wc + (long long)c.total * ko) / 3;
-    auto fill = [&](long long w, int left) {
-        long long j = ko > 0 && each > w ? (each - w) / ko : 0;
-        if (j > left) j = left;
-        return (int)(j / kXcds * kXcds);
-    };
-    c.c1 = fill(wa, c.total);
-    c.c2 = c.c1 + fill(wb, c.total - c.c1);
-    return c;
+// k-blocks streamed by one job of each phase and of the old-tap context (the
+// l3 jobs stream a value group's column tiles: K=1 one, K=3 up to six).
+template <class P>
+__host__ __device__ __forceinline__ void job_costs(const StepArgs& a, int* kph, int* ko) {
+    constexpr int kK = P::kK;
+    kph[PH_N] = a.n_new * a.M / kK;
+    kph[PH_A] = P::kBf16 ? 2 * a.M / kK : (a.n_new * a.M + 2 * a.M) / kK;
+    kph[PH_B] = a.Np1 / kK;
+    kph[PH_C] = a.Np2 / kK * (a.K == 1 ? 1 : 4);
+    *ko = a.n_old * a.M / kK / kCtxParts;
 }
 
-// k-blocks streamed by one job of each kind (the l3 jobs stream a value
-// group's column tiles: K=1 one, K=3 up to six).
-__host__ __device__ __forceinline__ void job_costs(const StepArgs& a, int* ka, int* kb, int* kc, int* ko) {
-    *ka = (a.n_new * a.M + 2 * a.M) / kTile;
-    *kb = a.Np1 / kTile;
-    *kc = a.Np2 / kTile * (a.K == 1 ? 1 : 4);
-    *ko = a.n_old * a.M / kTile / kCtxParts;
+// The work of one step: main blocks of each phase and which of the
+// kCtxParts * nc old-tap context jobs of the next step ride along with it:
+// phase ph takes jobs [cut[ph], cut[ph + 1]).  The cuts equalise the k-blocks
+// each phase streams, so that every phase holds about the same work; they
+// are multiples of 8, which keeps every job on the XCD its column tile
+// belongs to.
+struct StepWork {
+    int nb[kMaxPhases];
+    int cut[kMaxPhases + 1];
+    int nc;
+    // element i by selects (a runtime index into a local array would put the
+    // array in scratch memory)
+    __host__ __device__ __forceinline__ int blocks(int i) const {
+        return i == 0 ? nb[0] : i == 1 ? nb[1] : i == 2 ? nb[2] : nb[3];
+    }
+    __host__ __device__ __forceinline__ int first(int i) const {
+        return i == 0 ? cut[0] : i == 1 ? cut[1] : i == 2 ? cut[2] : i == 3 ? cut[3] : cut[4];
+    }
+};
+template <class P>
+__host__ __device__ __forceinline__ StepWork step_work(const StepArgs& a, const StepRows& s, const StepRows& s1) {
+    StepWork w;
+    int kph[kMaxPhases], ko;
+    job_costs<P>(a, kph, &ko);
+    w.nc = ctxo_blocks(a, s1);
+    const int total = kCtxParts * w.nc;
+    long long sum = (long long)total * ko;
+    for (int ph = 0; ph < kMaxPhases; ++ph) {
+        w.nb[ph] = ph < P::kFirst ? 0 : phase_blocks(a, s, ph);
+        sum += (long long)w.nb[ph] * kph[ph];
+    }
+    const long long each = sum / (kMaxPhases - P::kFirst);
+    for (int ph = 0; ph <= P::kFirst; ++ph) w.cut[ph] = 0;
+    for (int ph = P::kFirst; ph < kMaxPhases - 1; ++ph) {
+        const long long own = (long long)w.nb[ph] * kph[ph];
+        const int left = total - w.cut[ph];
+        long long j = ko > 0 && each > own ? (each - own) / ko : 0;
+        if (j > left) j = left;
+        w.cut[ph + 1] = w.cut[ph] + (int)(j / kXcds * kXcds);
+    }
+    w.cut[kMaxPhases] = total;
+    return w;
 }
 
 // A wave's partial 16x16 tile over k-blocks [kb0, kb1): w points at the
@@ -212,11 +346,12 @@ __host__ __device__ __forceinline__ void job_costs(const StepArgs& a, int* ka, i
 // of up to kKbw k-blocks are issued before the MFMAs that use them (indices
 // past the range are clamped, so every load is unconditional); la(kb) must
 // be branch-free.
-template <class LoadA>
-__device__ __forceinline__ f4 wave_dot(const f4* __restrict__ w, int kb0, int kb1, LoadA la) {
+template <class P, class LoadA>
+__device__ __forceinline__ f4 wave_dot(const typename P::B* __restrict__ w, int kb0, int kb1, LoadA la) {
     f4 acc = zero4();
     for (int kc = kb0; kc < kb1; kc += kKbw) {
-        f4 av[kKbw], bv[kKbw];
+        typename P::A av[kKbw];
+        typename P::B bv[kKbw];
 #pragma unroll
         for (int u = 0; u < kKbw; ++u) {
             const int k = min(kc + u, kb1 - 1);
@@ -225,7 +360,7 @@ __device__ __forceinline__ f4 wave_dot(const f4* __restrict__ w, int kb0, int kb
         }
 #pragma unroll
         for (int u = 0; u < kKbw; ++u)
-            if (kc + u < kb1) acc = mfma_k16(av[u], bv[u], acc);
+            if (kc + u < kb1) acc = P::mma(av[u], bv[u], acc);
     }
     return acc;
 }
@@ -235,16 +370,16 @@ __device__ __forceinline__ f4 wave_dot(const f4* __restrict__ w, int kb0, int kb
 // Afterwards waves 0..3 hold the full sum of tile row 4*(lane/16) + wave,
 // column lane%16 (the other waves get 0).  Ends with a block barrier, so `red`
 // may be reused.
-template <class LoadLo, class LoadHi>
-__device__ __forceinline__ float block_tile2(f4 (*red)[64], const float* __restrict__ wp, int nkb, int ct,
+template <class P, class LoadLo, class LoadHi>
+__device__ __forceinline__ float block_tile2(f4 (*red)[64], const void* __restrict__ wp, int nkb, int ct,
                                              int ksplit, LoadLo la_lo, LoadHi la_hi, int klo = 0, int khi = -1) {
     const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
     if (khi < 0) khi = nkb;
     const int per = (khi - klo + kWaves - 1) / kWaves;
     const int kb0 = min(khi, klo + wave * per), kb1 = min(khi, kb0 + per);
-    const f4* w = reinterpret_cast<const f4*>(wp) + (size_t)ct * nkb * 64 + lane;
-    f4 acc = wave_dot(w, kb0, min(kb1, ksplit), la_lo);
-    acc += wave_dot(w, max(kb0, ksplit), kb1, la_hi);
+    const typename P::B* w = static_cast<const typename P::B*>(wp) + (size_t)ct * nkb * 64 + lane;
+    f4 acc = wave_dot<P>(w, kb0, min(kb1, ksplit), la_lo);
+    acc += wave_dot<P>(w, max(kb0, ksplit), kb1, la_hi);
     red[wave][lane] = acc;
     __syncthreads();
     float v = 0.0f;
@@ -256,10 +391,10 @@ __device__ __forceinline__ float block_tile2(f4 (*red)[64], const float* __restr
     return v;
 }
 
-template <class LoadA>
-__device__ __forceinline__ float block_tile(f4 (*red)[64], const float* __restrict__ wp, int nkb, int ct,
+template <class P, class LoadA>
+__device__ __forceinline__ float block_tile(f4 (*red)[64], const void* __restrict__ wp, int nkb, int ct,
                                             LoadA la, int klo = 0, int khi = -1) {
-    return block_tile2(red, wp, nkb, ct, nkb, la, la, klo, khi);
+    return block_tile2<P>(red, wp, nkb, ct, nkb, la, la, klo, khi);
 }
 
 // ---------------------------------------------------------------------------
@@ -269,7 +404,7 @@ __host__ __device__ __forceinline__ int hoist_blocks(const StepArgs& a) {
     return xcd_blocks(a.Np1 / kTile, ntiles(a.B * a.H * a.W));
 }
 
-template <bool COH>
+template <class P, bool COH>
 __device__ __forceinline__ void hoist_job(const StepArgs& a, int b, f4 (*red)[64]) {
     const int nlat = a.B * a.H * a.W;
     const Job jb = xcd_job(b, a.Np1 / kTile, ntiles(nlat));
@@ -277,20 +412,57 @@ __device__ __forceinline__ void hoist_job(const StepArgs& a, int b, f4 (*red)[64
     const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63, kq = lane >> 4;
     const int r = jb.rt * kTile + (lane & 15);
     const float* psi = a.cp->psi;
-    const size_t base = (size_t)r * 2 * a.M + kq * 4;
     const int n = jb.ct * kTile + (lane & 15);
     const float bias = a.b_hoist[n];
-    auto la = [&](int kb) -> f4 { return ld4<false>(psi, base + kb * kTile, r < nlat); };
-    const float v = block_tile(red, a.wp_hoist, 2 * a.M / kTile, jb.ct, la);
+    float v;
+    if constexpr (P::kBf16) {
+        const size_t base = (size_t)r * 2 * a.M + kq * 8;
+        auto la = [&](int kb) -> b8x2 {
+            return split8(ld4<false>(psi, base + kb * 32, r < nlat), ld4<false>(psi, base + kb * 32 + 4, r < nlat));
+        };
+        v = block_tile<P>(red, a.wp_hoist, 2 * a.M / P::kK, jb.ct, la);
+    } else {
+        const size_t base = (size_t)r * 2 * a.M + kq * 4;
+        auto la = [&](int kb) -> f4 { return ld4<false>(psi, base + kb * kTile, r < nlat); };
+        v = block_tile<P>(red, a.wp_hoist, 2 * a.M / P::kK, jb.ct, la);
+    }
     const int ro = jb.rt * kTile + kq * 4 + wave;
     if (wave < 4 && ro < nlat) st1<COH>(a.p1, (size_t)ro * a.Np1 + n, v + bias);
+}
+
+// Tap gather of k-block kb of a row's taps (fp32: y_hat, bf16: its pair
+// form), for the old taps (tap-major, `old` true) or the new taps.  A k-block
+// never straddles two taps (M is a multiple of the k-block).
+template <class P, bool COH>
+__device__ __forceinline__ typename P::A ld_tap(const StepArgs& a, const Row& w, int kb, int kq, bool old) {
+    const int M = a.M;
+    const int tap = kb * P::kK / M;
+    const int c = kb * P::kK - tap * M + kq * (P::kK / 4);
+    int dy, dx;
+    if (old) {
+        const int row = tap < a.old_n0 ? 0 : (tap < a.old_n0 + a.old_n1 ? 1 : 2);
+        dx = tap - (row == 0 ? 0 : (row == 1 ? a.old_n0 : a.old_n0 + a.old_n1)) - 2;
+        dy = row - 2;
+    } else {
+        dy = tap - 1;
+        dx = tap ? -1 : a.new_dx0;
+    }
+    const int ii = w.i + dy, jj = w.j + dx;
+    const bool ok = w.valid && ii >= 0 && jj >= 0 && jj < a.W;
+    const size_t lat = ((size_t)w.b * a.H + ii) * a.W + jj;
+    if constexpr (P::kBf16) {
+        const size_t q = lat * 2 * M + c;
+        return b8x2{ld8h<COH>(a.ybf, q, ok), ld8h<COH>(a.ybf, q + M, ok)};
+    } else {
+        return ld4<COH>(a.cp->y_hat, lat * M + c, ok);
+    }
 }
 
 // ---------------------------------------------------------------------------
 // Job j of the old-tap context of the latents of step s: k-part part = j / nc
 // (a contiguous range of the k-blocks of the gathered old taps, tap-major)
 // of block j % nc:  ctxo[part][r][n] = sum_{k in part} taps[r][k] Wc[k][n].
-template <bool COH>
+template <class P, bool COH>
 __device__ __forceinline__ void ctxo_job(const StepArgs& a, const StepRows& s, int j, int nc, f4 (*red)[64]) {
     const int part = j / nc, b = j - part * nc;
     const int M = a.M;
@@ -298,30 +470,21 @@ __device__ __forceinline__ void ctxo_job(const StepArgs& a, const StepRows& s, i
     if (!jb.valid) return;
     const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63, kq = lane >> 4;
     const Row w = step_row(a, s, jb.rt * kTile + (lane & 15));
-    const float* yh = a.cp->y_hat;
-    auto la = [&](int kb) -> f4 {
-        const int tap = kb * kTile / M;   // a k-block never straddles two taps
-        const int c = kb * kTile - tap * M + kq * 4;
-        const int row = tap < a.old_n0 ? 0 : (tap < a.old_n0 + a.old_n1 ? 1 : 2);
-        const int dx = tap - (row == 0 ? 0 : (row == 1 ? a.old_n0 : a.old_n0 + a.old_n1)) - 2;
-        const int ii = w.i + row - 2, jj = w.j + dx;
-        const bool ok = w.valid && ii >= 0 && jj >= 0 && jj < a.W;
-        return ld4<COH>(yh, (((size_t)w.b * a.H + ii) * a.W + jj) * M + c, ok);
-    };
-    const int nkb = a.n_old * M / kTile;
+    auto la = [&](int kb) { return ld_tap<P, COH>(a, w, kb, kq, true); };
+    const int nkb = a.n_old * M / P::kK;
     const int klo = nkb * part / kCtxParts, khi = nkb * (part + 1) / kCtxParts;
-    const float acc = block_tile(red, a.wp_old, nkb, jb.ct, la, klo, khi);
+    const float acc = block_tile<P>(red, a.wp_old, nkb, jb.ct, la, klo, khi);
     const int n = jb.ct * kTile + (lane & 15);
     const int ro = wave < 4 ? jb.rt * kTile + kq * 4 + wave : s.nrows;
-    // double-buffered by step parity: jobs for step s.t may run while layer 1
-    // of step s.t - 1 still reads the other half
+    // double-buffered by step parity: jobs for step s.t may run while the
+    // context of step s.t - 1 is still being read from the other half
     const size_t slot = (size_t)((s.t & 1) * kCtxParts + part) * a.max_rows + ro;
     if (ro < s.nrows) st1<COH>(a.ctxo, slot * 2 * M + n, acc);
 }
 
-// Phase A: layer 1 of step s.
+// Phase A, fp32: layer 1 of step s over [new taps ; old-tap context].
 template <bool COH>
-__device__ __forceinline__ void l1_job(const StepArgs& a, const StepRows& s, int b, f4 (*red)[64]) {
+__device__ __forceinline__ void l1_fold_job(const StepArgs& a, const StepRows& s, int b, f4 (*red)[64]) {
     const Job jb = xcd_job(b, a.Np1 / kTile, ntiles(s.nrows));
     if (!jb.valid) return;
     const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63, kq = lane >> 4;
@@ -333,17 +496,10 @@ __device__ __forceinline__ void l1_job(const StepArgs& a, const StepRows& s, int
     const float z = ld1<COH>(a.p1, v.lat * a.Np1 + n, v.valid);
     const int r = jb.rt * kTile + (lane & 15);
     const Row w = step_row(a, s, r);
-    const float* yh = a.cp->y_hat;
     const int knew = a.n_new * M;
     const size_t cpart = (size_t)a.max_rows * 2 * M;
     const size_t cbase = (size_t)(s.t & 1) * kCtxParts * cpart + (size_t)r * 2 * M + kq * 4;
-    auto la_new = [&](int kb) -> f4 {
-        const int tap = kb * kTile >= M ? 1 : 0;
-        const int c = kb * kTile - tap * M + kq * 4;
-        const int ii = w.i - 1 + tap, jj = w.j + (tap ? -1 : a.new_dx0);
-        const bool ok = w.valid && ii >= 0 && jj >= 0 && jj < a.W;
-        return ld4<COH>(yh, (((size_t)w.b * a.H + ii) * a.W + jj) * M + c, ok);
-    };
+    auto la_new = [&](int kb) { return ld_tap<PF32, COH>(a, w, kb, kq, false); };
     auto la_ctx = [&](int kb) -> f4 {
         const size_t q = cbase + (kb * kTile - knew);
         f4 v = ld4<COH>(a.ctxo, q, w.valid);
@@ -351,12 +507,53 @@ __device__ __forceinline__ void l1_job(const StepArgs& a, const StepRows& s, int
         for (int part = 1; part < kCtxParts; ++part) v += ld4<COH>(a.ctxo, q + part * cpart, w.valid);
         return v;
     };
-    const float acc = block_tile2(red, a.wp_l1, (knew + 2 * M) / kTile, jb.ct, knew / kTile, la_new, la_ctx);
-    if (v.valid) st1<COH>(a.h1, (size_t)ro * a.Np1 + n, lrelu(acc + z, a.slope));
+    const float acc = block_tile2<PF32>(red, a.wp_l1, (knew + 2 * M) / kTile, jb.ct, knew / kTile, la_new, la_ctx);
+    if (v.valid) st1<COH>(static_cast<float*>(a.h1), (size_t)ro * a.Np1 + n, lrelu(acc + z, a.slope));
+}
+
+// Phase N, bf16: the context vector of step s, rounded to bf16.
+template <bool COH>
+__device__ __forceinline__ void ctxn_job(const StepArgs& a, const StepRows& s, int b, f4 (*red)[64]) {
+    const int M = a.M;
+    const Job jb = xcd_job(b, 2 * M / kTile, ntiles(s.nrows));
+    if (!jb.valid) return;
+    const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63, kq = lane >> 4;
+    // epilogue operands first: bias and the old-tap context parts
+    const int n = jb.ct * kTile + (lane & 15);
+    const int ro = wave < 4 ? jb.rt * kTile + kq * 4 + wave : s.nrows;
+    const bool vo = ro < s.nrows;
+    const size_t cpart = (size_t)a.max_rows * 2 * M;
+    const size_t cq = (size_t)(s.t & 1) * kCtxParts * cpart + (size_t)ro * 2 * M + n;
+    float z = a.bc[n];
+#pragma unroll
+    for (int part = 0; part < kCtxParts; ++part) z += ld1<COH>(a.ctxo, cq + part * cpart, vo && a.n_old > 0);
+    const Row w = step_row(a, s, jb.rt * kTile + (lane & 15));
+    auto la = [&](int kb) { return ld_tap<PBF16, COH>(a, w, kb, kq, false); };
+    const float acc = block_tile<PBF16>(red, a.wp_new, a.n_new * M / PBF16::kK, jb.ct, la);
+    if (vo) st_act<PBF16, COH>(a.ctxb, act_row<PBF16>(ro, 2 * M), 2 * M, n, acc + z);
+}
+
+// Phase A, bf16: layer 1 of step s over the bf16 context vector.
+template <bool COH>
+__device__ __forceinline__ void l1_ctx_job(const StepArgs& a, const StepRows& s, int b, f4 (*red)[64]) {
+    const Job jb = xcd_job(b, a.Np1 / kTile, ntiles(s.nrows));
+    if (!jb.valid) return;
+    const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63, kq = lane >> 4;
+    const int M = a.M;
+    const int n = jb.ct * kTile + (lane & 15);
+    const int ro = wave < 4 ? jb.rt * kTile + kq * 4 + wave : s.nrows;
+    const Row v = step_row(a, s, ro);
+    const float z = ld1<COH>(a.p1, v.lat * a.Np1 + n, v.valid);
+    const int r = jb.rt * kTile + (lane & 15);
+    const bool valid = r < s.nrows;
+    const size_t row = act_row<PBF16>(r, 2 * M);
+    auto la = [&](int kb) { return ld_act<PBF16, COH>(a.ctxb, row, 2 * M, kb, kq, valid); };
+    const float acc = block_tile<PBF16>(red, a.wp_l1, 2 * M / PBF16::kK, jb.ct, la);
+    if (v.valid) st_act<PBF16, COH>(a.h1, act_row<PBF16>(ro, a.Np1), a.Np1, n, lrelu(acc + z, a.slope));
 }
 
 // Phase B: layer 2.
-template <bool COH>
+template <class P, bool COH>
 __device__ __forceinline__ void l2_job(const StepArgs& a, const StepRows& s, int b, f4 (*red)[64]) {
     const Job jb = xcd_job(b, a.Np2 / kTile, ntiles(s.nrows));
     if (!jb.valid) return;
@@ -365,11 +562,11 @@ __device__ __forceinline__ void l2_job(const StepArgs& a, const StepRows& s, int
     const float bias = a.b2[n];
     const int r = jb.rt * kTile + (lane & 15);
     const bool valid = r < s.nrows;
-    const size_t base = (size_t)r * a.Np1 + kq * 4;
-    auto la = [&](int kb) -> f4 { return ld4<COH>(a.h1, base + kb * kTile, valid); };
-    const float acc = block_tile(red, a.wp2, a.Np1 / kTile, jb.ct, la);
+    const size_t row = act_row<P>(r, a.Np1);
+    auto la = [&](int kb) { return ld_act<P, COH>(a.h1, row, a.Np1, kb, kq, valid); };
+    const float acc = block_tile<P>(red, a.wp2, a.Np1 / P::kK, jb.ct, la);
     const int ro = jb.rt * kTile + kq * 4 + wave;
-    if (wave < 4 && ro < s.nrows) st1<COH>(a.h2, (size_t)ro * a.Np2 + n, lrelu(acc + bias, a.slope));
+    if (wave < 4 && ro < s.nrows) st_act<P, COH>(a.h2, act_row<P>(ro, a.Np2), a.Np2, n, lrelu(acc + bias, a.slope));
 }
 
 __device__ __forceinline__ int scale_index(const float* tab, int L, float sg) {
@@ -396,10 +593,12 @@ struct L3Smem {
 // channel group cg (16 channels), value group vg (0: the columns the mean
 // needs -- K=1: mean, K=3: 3 logits and 3 component means; 1: the scales).
 // The scale table must already be in sm.tab.
-template <int KC, bool COH>
+template <class P, int KC, bool COH>
 __device__ __forceinline__ void l3_job(const StepArgs& a, const StepRows& s, int b, L3Smem<KC>& sm) {
+    using A = typename P::A;
+    using Bw = typename P::B;
     constexpr int NT0 = L3Smem<KC>::NT0, NT1 = L3Smem<KC>::NT1, NTM = L3Smem<KC>::NTM;
-    constexpr int KBW = KC == 1 ? 16 : 4;
+    constexpr int KBW = KC == 1 ? P::kL3Kbw1 : P::kL3Kbw3;
     const int M = a.M, G = M / kTile;
     const Job jb = xcd_job(b, 2 * G, ntiles(s.nrows));
     if (!jb.valid) return;
@@ -425,13 +624,13 @@ __device__ __forceinline__ void l3_job(const StepArgs& a, const StepRows& s, int
         for (int t = 0; t < NT1; ++t) bias[t] = a.b3[(KC == 1 ? M : (6 + t) * M) + c];
     }
 
-    const int nkb = a.Np2 / kTile;
+    const int nkb = a.Np2 / P::kK;
     const int per = (nkb + kWaves - 1) / kWaves;
     const int kb0 = min(nkb, wave * per), kb1 = min(nkb, kb0 + per);
     const int r = rt * kTile + (lane & 15);
     const bool valid = r < s.nrows;
-    const size_t hbase = (size_t)r * a.Np2 + kq * 4;
-    const f4* __restrict__ wv = reinterpret_cast<const f4*>(a.wp3) + lane;
+    const size_t hrow = act_row<P>(r, a.Np2);
+    const Bw* __restrict__ wv = static_cast<const Bw*>(a.wp3) + lane;
     const int NT = vg == 0 ? NT0 : NT1;
     int cols[NTM];
 #pragma unroll
@@ -440,11 +639,12 @@ __device__ __forceinline__ void l3_job(const StepArgs& a, const StepRows& s, int
 #pragma unroll
     for (int t = 0; t < NTM; ++t) acc[t] = zero4();
     for (int kc = kb0; kc < kb1; kc += KBW) {
-        f4 av[KBW], bv[KBW][NTM];
+        A av[KBW];
+        Bw bv[KBW][NTM];
 #pragma unroll
         for (int u = 0; u < KBW; ++u) {
             const int k = min(kc + u, kb1 - 1);
-            av[u] = ld4<COH>(a.h2, hbase + k * kTile, valid);
+            av[u] = ld_act<P, COH>(a.h2, hrow, a.Np2, k, kq, valid);
 #pragma unroll
             for (int t = 0; t < NTM; ++t) bv[u][t] = wv[((size_t)cols[t] * nkb + k) * 64];
         }
@@ -453,7 +653,7 @@ __device__ __forceinline__ void l3_job(const StepArgs& a, const StepRows& s, int
             if (kc + u < kb1)
 #pragma unroll
                 for (int t = 0; t < NTM; ++t)
-                    if (t < NT) acc[t] = mfma_k16(av[u], bv[u][t], acc[t]);
+                    if (t < NT) acc[t] = P::mma(av[u], bv[u][t], acc[t]);
     }
 #pragma unroll
     for (int t = 0; t < NTM; ++t) sm.red[wave][t][lane] = acc[t];
@@ -483,7 +683,7 @@ __device__ __forceinline__ void l3_job(const StepArgs& a, const StepRows& s, int
         return;
     }
     float mu;
-    if (KC == 1) {
+    if constexpr (KC == 1) {
         mu = o[0];
     } else {
         const float mx = fmaxf(o[0], fmaxf(o[1], o[2]));
@@ -512,6 +712,23 @@ __device__ __forceinline__ void l3_job(const StepArgs& a, const StepRows& s, int
     }
     cp->mean[oq] = mu;
     st1<COH>(cp->y_hat, oq, sv + mu);
+    if constexpr (P::kBf16) st_act<P, COH>(a.ybf, act_row<P>(lat, M), M, c, sv + mu);
+}
+
+// The main job of phase ph (sm.tab must hold the scale table for PH_C).
+template <class P, int KC, bool COH>
+__device__ __forceinline__ void phase_job(int ph, const StepArgs& a, const StepRows& s, int b, f4 (*red)[64],
+                                          L3Smem<KC>& sm) {
+    if constexpr (P::kBf16) {
+        if (ph == PH_N) ctxn_job<COH>(a, s, b, red);
+        else if (ph == PH_A) l1_ctx_job<COH>(a, s, b, red);
+        else if (ph == PH_B) l2_job<P, COH>(a, s, b, red);
+        else l3_job<P, KC, COH>(a, s, b, sm);
+    } else {
+        if (ph == PH_A) l1_fold_job<COH>(a, s, b, red);
+        else if (ph == PH_B) l2_job<P, COH>(a, s, b, red);
+        else l3_job<P, KC, COH>(a, s, b, sm);
+    }
 }
 
 }  // namespace wf

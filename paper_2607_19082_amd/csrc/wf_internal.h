@@ -42,11 +42,19 @@ struct CallPtrs {
 // taps (delta = 1) are gathered on the critical path of step t; the context
 // sum over the "old" taps (delta >= 2) of step t+1's latents only needs
 // y_hat of steps <= t-1, so it is computed during step t, off the critical
-// path, in k-parts.  Layer 1 of step t then reads
-//   [new taps (n_new*M) ; old-tap context (2M)]
+// path, in k-parts.
+//
+// fp32: layer 1 of step t reads [new taps (n_new*M) ; old-tap context (2M)]
 // against [W1[:, 2M:] . Wc[new taps] ; W1[:, 2M:]] (the new taps' conv and the
 // context half of layer 1 are both linear, so their product is folded at plan
 // time; the context bias is folded into the hoisted part).
+// bf16: the context vector is an activation operand of its own (a bf16
+// pair); it is formed from the new taps against Wc[new taps], plus the bias
+// and the old-tap context, and layer 1 reads it against W1[:, 2M:].
+//
+// Packed weights (wp_*) hold 16-byte lane operands per (column tile, k-block):
+// fp32 k-blocks of 16, bf16 k-blocks of 32.  Np1, Np2 are d1, d2 rounded up to
+// a whole k-block.
 struct StepArgs {
     int H, W, M, B, K, L, lambda;
     int Np1, Np2, n3;
@@ -57,19 +65,24 @@ struct StepArgs {
     // dx = -2 and is contiguous.  New taps: (-1, new_dx0) and (0, -1).
     int old_n0, old_n1, new_dx0;
     float slope;
-    const float* wp_hoist;  // packed W1[:, :2M]                          [Np1/16][2M/16]
-    const float* b_hoist;   // b1 + W1[:, 2M:] . bc                        [Np1]
-    const float* wp_l1;     // packed [W1b.Wc[new] ; W1b]                  [Np1/16][(n_new*M + 2M)/16]
-    const float* wp_old;    // packed Wc over the old taps                 [2M/16][n_old*M/16]
-    const float* wp2;       // packed W2                                   [Np2/16][Np1/16]
+    const void* wp_hoist;   // packed W1[:, :2M]                           [Np1/16][2M/kb]
+    const float* b_hoist;   // fp32: b1 + W1[:, 2M:] . bc; bf16: b1        [Np1]
+    const void* wp_l1;      // fp32: packed [W1b.Wc[new] ; W1b]            [Np1/16][(n_new*M + 2M)/16]
+                            // bf16: packed W1b                            [Np1/16][2M/32]
+    const void* wp_new;     // bf16: packed Wc over the new taps           [2M/16][n_new*M/32]
+    const float* bc;        // bf16: context bias                          [2M]
+    const void* wp_old;     // packed Wc over the old taps                 [2M/16][n_old*M/kb]
+    const void* wp2;        // packed W2                                   [Np2/16][Np1/kb]
     const float* b2;        // [Np2]
-    const float* wp3;       // packed W3                                   [n3/16][Np2/16]
+    const void* wp3;        // packed W3                                   [n3/16][Np2/kb]
     const float* b3;        // [n3]
     const float* table;     // [L]
     float* p1;              // [B*H*W][Np1] hoisted layer-1 part
-    float* h1;              // [max_rows][Np1]
-    float* h2;              // [max_rows][Np2]
+    void* h1;               // [max_rows][Np1]  fp32, or bf16 pairs [max_rows][2][Np1]
+    void* h2;               // [max_rows][Np2]  fp32, or bf16 pairs [max_rows][2][Np2]
     float* ctxo;            // [2][3][max_rows][2M] old-tap context k-parts, by step parity
+    uint16_t* ctxb;         // bf16: [max_rows][2][2M] context vector of the step (pairs)
+    uint16_t* ybf;          // bf16: [B*H*W][2][M] y_hat as bf16 pairs (tap source)
     int max_rows;
     const CallPtrs* cp;
 };
@@ -83,7 +96,8 @@ struct Plan {
     int dy[kMaxTaps], dx[kMaxTaps];
     std::vector<int32_t> step_of;        // [H*W]
     int max_rows;
-    int Np1, Np2;                        // d1, d2 rounded up to 16
+    int Np1, Np2;                        // d1, d2 rounded up to a whole k-block
+    int nph;                             // phases per step: 3 (fp32) or 4 (bf16)
     StepArgs args;                       // device pointers filled in
     // device memory owned by the plan
     int device = 0;

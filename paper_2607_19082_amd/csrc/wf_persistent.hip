@@ -1,5 +1,5 @@
 // Persistent driver: one cooperative launch runs every wavefront step; the
-// three phases of a step are separated by a device-wide barrier instead of
+// phases of a step are separated by a device-wide barrier instead of
 // kernel boundaries.  Each workgroup loops over the jobs of a phase with a
 // stride of the grid size (a multiple of 8, so a job's XCD placement is the
 // same as in the per-step kernels), and all data that crosses workgroups
@@ -57,7 +57,7 @@ __device__ __forceinline__ bool grid_barrier(unsigned* ctr, unsigned k, int* err
     return *bail == 0;
 }
 
-template <int KC>
+template <class P, int KC>
 __global__ __launch_bounds__(kThreads) void k_persistent(StepArgs a, int T, unsigned* ctr, int* err,
                                                     long long budget, Trace tr) {
     __shared__ f4 red[kWaves][64];
@@ -72,42 +72,27 @@ __global__ __launch_bounds__(kThreads) void k_persistent(StepArgs a, int T, unsi
     // the general form keeps the loop uniform)
     {
         const int nh = hoist_blocks(a);
-        for (int b = blockIdx.x; b < nh; b += G) hoist_job<true>(a, b, red);
+        for (int b = blockIdx.x; b < nh; b += G) hoist_job<P, true>(a, b, red);
         const StepRows s0 = step_rows(a.H, a.W, a.B, a.lambda, 0);
         const int nc = ctxo_blocks(a, s0);
-        for (int b = blockIdx.x; b < kCtxParts * nc; b += G) ctxo_job<true>(a, s0, b, nc, red);
+        for (int b = blockIdx.x; b < kCtxParts * nc; b += G) ctxo_job<P, true>(a, s0, b, nc, red);
         if (!grid_barrier(ctr, ++k, err, budget, &bail, tr)) return;
     }
     for (int t = 0; t < T; ++t) {
         const StepRows s = step_rows(a.H, a.W, a.B, a.lambda, t);
         StepRows s1{t + 1, 0, 0, 0};
         if (t + 1 < T) s1 = step_rows(a.H, a.W, a.B, a.lambda, t + 1);
-        const int nc = ctxo_blocks(a, s1);
-        const int nb1 = l1_blocks(a, s), nb2 = l2_blocks(a, s), nb3 = l3_blocks(a, s);
-        int ka, kb, kc, ko;
-        job_costs(a, &ka, &kb, &kc, &ko);
-        const CtxSplit cs = ctxo_split(nc, nb1, nb2, nb3, ka, kb, kc, ko);
-        for (int b = blockIdx.x; b < nb1 + cs.c1; b += G) {
-            if (b < nb1)
-                l1_job<true>(a, s, b, red);
-            else
-                ctxo_job<true>(a, s1, b - nb1, nc, red);
+        const StepWork w = step_work<P>(a, s, s1);
+        for (int ph = P::kFirst; ph < kMaxPhases; ++ph) {
+            const int nb = w.blocks(ph), j0 = w.first(ph);
+            for (int b = blockIdx.x; b < nb + w.first(ph + 1) - j0; b += G) {
+                if (b < nb)
+                    phase_job<P, KC, true>(ph, a, s, b, red, sm);
+                else
+                    ctxo_job<P, true>(a, s1, j0 + b - nb, w.nc, red);
+            }
+            if (!grid_barrier(ctr, ++k, err, budget, &bail, tr)) return;
         }
-        if (!grid_barrier(ctr, ++k, err, budget, &bail, tr)) return;
-        for (int b = blockIdx.x; b < nb2 + cs.c2 - cs.c1; b += G) {
-            if (b < nb2)
-                l2_job<true>(a, s, b, red);
-            else
-                ctxo_job<true>(a, s1, cs.c1 + b - nb2, nc, red);
-        }
-        if (!grid_barrier(ctr, ++k, err, budget, &bail, tr)) return;
-        for (int b = blockIdx.x; b < nb3 + cs.total - cs.c2; b += G) {
-            if (b < nb3)
-                l3_job<KC, true>(a, s, b, sm);
-            else
-                ctxo_job<true>(a, s1, cs.c2 + b - nb3, nc, red);
-        }
-        if (!grid_barrier(ctr, ++k, err, budget, &bail, tr)) return;
     }
 }
 
@@ -115,8 +100,10 @@ __global__ void k_zero_u32(unsigned* p, int n) {
     for (int i = threadIdx.x; i < n; i += blockDim.x) p[i] = 0u;
 }
 
-static const void* persistent_fn(int K) {
-    return K == 1 ? (const void*)k_persistent<1> : (const void*)k_persistent<3>;
+static const void* persistent_fn(const Plan& p) {
+    if (p.precision == WF_BF16)
+        return p.K == 1 ? (const void*)k_persistent<PBF16, 1> : (const void*)k_persistent<PBF16, 3>;
+    return p.K == 1 ? (const void*)k_persistent<PF32, 1> : (const void*)k_persistent<PF32, 3>;
 }
 
 // Grid size of the persistent kernel: two workgroups per CU when they fit (one
@@ -126,7 +113,7 @@ int persistent_grid(Plan& p, int* grid) {
     hipError_t e = hipGetDevice(&dev);
     if (e == hipSuccess) e = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);
     if (e == hipSuccess)
-        e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, persistent_fn(p.K), kThreads, 0);
+        e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, persistent_fn(p), kThreads, 0);
     if (e != hipSuccess) return fail(WF_E_HIP, std::string("occupancy query: ") + hipGetErrorString(e));
     if (per_cu < 1 || cus < kXcds) return fail(WF_E_UNSUPPORTED, "persistent kernel cannot be resident");
     *grid = cus * (per_cu >= 2 ? 2 : 1) / kXcds * kXcds;
@@ -142,7 +129,7 @@ int enqueue_persistent(Plan& p, hipStream_t stream) {
     long long budget = p.spin_budget;
     Trace tr{p.stamps, p.stamps_cap};
     void* args[] = {&a, &T, &ctr, &err, &budget, &tr};
-    hipError_t e = hipLaunchCooperativeKernel(persistent_fn(p.K), dim3(p.grid), dim3(kThreads), args, 0, stream);
+    hipError_t e = hipLaunchCooperativeKernel(persistent_fn(p), dim3(p.grid), dim3(kThreads), args, 0, stream);
     if (e != hipSuccess) return fail(WF_E_HIP, std::string("cooperative launch: ") + hipGetErrorString(e));
     return WF_OK;
 }

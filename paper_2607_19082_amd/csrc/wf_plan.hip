@@ -4,6 +4,7 @@
 #include <cmath>
 #include <cstring>
 #include <new>
+#include <type_traits>
 
 #include "wf_internal.h"
 
@@ -52,7 +53,10 @@ static int least_shear(int ntaps, const int* dy, const int* dx) {
     return -1;
 }
 
-static int round16(int v) { return (v + kTile - 1) / kTile * kTile; }
+static int round_up(int v, int m) { return (v + m - 1) / m * m; }
+static int round16(int v) { return round_up(v, kTile); }
+// k-block of the packed operands: 16 values of k for fp32, 32 for bf16
+static int kblock(int precision) { return precision == WF_BF16 ? 32 : 16; }
 
 static int check_desc(const wf_desc* d) {
     if (!d) return fail(WF_E_INVALID, "desc is NULL");
@@ -85,10 +89,11 @@ static int check_desc(const wf_desc* d) {
     // every array the kernels read through raw buffer instructions (psi, y_hat,
     // the per-step activations) must fit the buffer window
     const long long lat = (long long)d->B * d->H * d->W;
-    if (lat * 2 * d->M * 4 >= kBufBytes || lat * round16(d->d1) * 4 >= kBufBytes ||
+    if (lat * 2 * d->M * 4 >= kBufBytes || lat * round_up(d->d1, kblock(d->precision)) * 4 >= kBufBytes ||
         lat * 3 * d->M > (1LL << 31) - 1)
         return fail(WF_E_UNSUPPORTED, "problem too large for the 2 GiB buffer window");
-    if (d->precision == WF_BF16) return fail(WF_E_UNSUPPORTED, "bf16 operands are not built yet");
+    // a k-block of the tap gathers must not straddle two taps
+    if (d->M % kblock(d->precision) != 0) return fail(WF_E_UNSUPPORTED, "bf16 operands need M a multiple of 32");
     return WF_OK;
 }
 
@@ -108,6 +113,34 @@ static std::vector<float> pack_panel(int K, int N, F wt) {
                     int n = ct * kTile + l % 16;
                     float v = (k < K && n < N) ? wt(k, n) : 0.0f;
                     out[(((size_t)ct * nkb + kb) * 64 + l) * 4 + q] = v;
+                }
+    return out;
+}
+
+// bf16 bits of v, round to nearest even (finite inputs).
+static uint16_t bf16_round(float v) {
+    uint32_t u;
+    std::memcpy(&u, &v, 4);
+    u += 0x7fffu + ((u >> 16) & 1u);
+    return (uint16_t)(u >> 16);
+}
+
+// The same for bf16 operands, k-blocks of 32: lane l holds
+// Wt[kb*32 + (l/16)*8 + q][ct*16 + l%16] for q = 0..7, rounded to bf16.  Np
+// (a multiple of 16, at least N) is the padded column count the kernels use.
+template <class F>
+static std::vector<uint16_t> pack_panel_bf16(int K, int N, int Np, F wt) {
+    const int Kp = round_up(K, 32);
+    const int nkb = Kp / 32;
+    std::vector<uint16_t> out((size_t)Np * Kp, 0);
+    for (int ct = 0; ct < Np / kTile; ++ct)
+        for (int kb = 0; kb < nkb; ++kb)
+            for (int l = 0; l < 64; ++l)
+                for (int q = 0; q < 8; ++q) {
+                    int k = kb * 32 + (l / 16) * 8 + q;
+                    int n = ct * kTile + l % 16;
+                    float v = (k < K && n < N) ? wt(k, n) : 0.0f;
+                    out[(((size_t)ct * nkb + kb) * 64 + l) * 8 + q] = bf16_round(v);
                 }
     return out;
 }
@@ -182,8 +215,10 @@ static int build_plan(const wf_desc* d, Plan* p) {
     int maxn = 0;
     for (int t = 0; t < p->T; ++t) maxn = std::max(maxn, step_n[t]);
     p->max_rows = p->B * maxn;
-    p->Np1 = round16(p->d1);
-    p->Np2 = round16(p->d2);
+    const bool bf = p->precision == WF_BF16;
+    p->Np1 = round_up(p->d1, kblock(p->precision));
+    p->Np2 = round_up(p->d2, kblock(p->precision));
+    p->nph = bf ? 4 : 3;
     const int d1 = p->d1, Np1 = p->Np1;
 
     StepArgs& a = p->args;
@@ -219,48 +254,71 @@ static int build_plan(const wf_desc* d, Plan* p) {
     WF_HIP(hipGetDevice(&p->device));
     int rc;
 
-    // Fold the new taps' conv into the context half of layer 1.
-    std::vector<std::vector<double>> fold(a.n_new);
-    for (int k = 0; k < a.n_new; ++k) fold_tap(d, p->dy[new_taps[k]], p->dx[new_taps[k]], fold[k]);
-
-    auto w_hoist = pack_panel(2 * M, d1, [&](int k, int n) { return d->w1[(size_t)n * 4 * M + k]; });
+    float* f;
+    // upload a packed panel after checking that it holds exactly the
+    // (column tile, k-block) lane operands the kernels read from it
+    const int kbk = kblock(p->precision);
+    auto put = [&](const void** dst, int cols, int kdim, const auto& v) -> int {
+        using T = typename std::decay_t<decltype(v)>::value_type;
+        if (kdim % kbk != 0 || v.size() != (size_t)(cols / kTile) * (kdim / kbk) * 64 * (16 / sizeof(T)))
+            return fail(WF_E_UNSUPPORTED, "internal: packed panel does not match the kernels' tiling");
+        T* q = nullptr;
+        int r = upload(p, &q, v.data(), v.size());
+        *dst = q;
+        return r;
+    };
+    auto wc_of = [&](const std::vector<int>& taps) {
+        return [&, taps](int k, int n) {
+            const int o = k / M, c = k % M;
+            return d->ctx_w[(((size_t)n * M + c) * 5 + (p->dy[taps[o]] + 2)) * 5 + (p->dx[taps[o]] + 2)];
+        };
+    };
+    auto w1a = [&](int k, int n) { return d->w1[(size_t)n * 4 * M + k]; };
+    auto w1b = [&](int k, int n) { return d->w1[(size_t)n * 4 * M + 2 * M + k]; };
+    auto w2f = [&](int k, int n) { return d->w2[(size_t)n * d1 + k]; };
+    auto w3f = [&](int k, int n) { return d->w3[(size_t)n * p->d2 + k]; };
     std::vector<float> b_hoist(Np1, 0.0f);
-    for (int n = 0; n < d1; ++n) {
-        double acc = d->b1[n];
-        const float* w1b = d->w1 + (size_t)n * 4 * M + 2 * M;
-        for (int o = 0; o < 2 * M; ++o) acc += (double)w1b[o] * (double)d->ctx_b[o];
-        b_hoist[n] = (float)acc;
+    if (bf) {
+        // bf16: the context bias stays in the context vector (it is rounded
+        // with it); no fold.
+        std::copy(d->b1, d->b1 + d1, b_hoist.begin());
+        if ((rc = put(&a.wp_hoist, Np1, 2 * M, pack_panel_bf16(2 * M, d1, Np1, w1a))) != WF_OK) return rc;
+        if ((rc = put(&a.wp_l1, Np1, 2 * M, pack_panel_bf16(2 * M, d1, Np1, w1b))) != WF_OK) return rc;
+        if ((rc = put(&a.wp_new, 2 * M, a.n_new * M, pack_panel_bf16(a.n_new * M, 2 * M, 2 * M, wc_of(new_taps)))) != WF_OK) return rc;
+        if ((rc = put(&a.wp_old, 2 * M, a.n_old * M, pack_panel_bf16(a.n_old * M, 2 * M, 2 * M, wc_of(old_taps)))) != WF_OK) return rc;
+        if ((rc = put(&a.wp2, p->Np2, Np1, pack_panel_bf16(d1, p->d2, p->Np2, w2f))) != WF_OK) return rc;
+        if ((rc = put(&a.wp3, p->n3, p->Np2, pack_panel_bf16(p->d2, p->n3, p->n3, w3f))) != WF_OK) return rc;
+        if ((rc = upload(p, &f, d->ctx_b, (size_t)2 * M)) != WF_OK) return rc;
+        a.bc = f;
+    } else {
+        // Fold the new taps' conv into the context half of layer 1, and the
+        // context bias into the hoisted part.
+        std::vector<std::vector<double>> fold(a.n_new);
+        for (int k = 0; k < a.n_new; ++k) fold_tap(d, p->dy[new_taps[k]], p->dx[new_taps[k]], fold[k]);
+        for (int n = 0; n < d1; ++n) {
+            double acc = d->b1[n];
+            const float* w1r = d->w1 + (size_t)n * 4 * M + 2 * M;
+            for (int o = 0; o < 2 * M; ++o) acc += (double)w1r[o] * (double)d->ctx_b[o];
+            b_hoist[n] = (float)acc;
+        }
+        const int knew = a.n_new * M;
+        if ((rc = put(&a.wp_hoist, Np1, 2 * M, pack_panel(2 * M, d1, w1a))) != WF_OK) return rc;
+        if ((rc = put(&a.wp_l1, Np1, knew + 2 * M, pack_panel(knew + 2 * M, d1, [&](int k, int n) {
+                 if (k < knew) return (float)fold[k / M][(size_t)(k % M) * d1 + n];
+                 return w1b(k - knew, n);
+             }))) != WF_OK)
+            return rc;
+        fold.clear();
+        if ((rc = put(&a.wp_old, 2 * M, a.n_old * M, pack_panel(a.n_old * M, 2 * M, wc_of(old_taps)))) != WF_OK) return rc;
+        if ((rc = put(&a.wp2, p->Np2, Np1, pack_panel(d1, p->d2, w2f))) != WF_OK) return rc;
+        if ((rc = put(&a.wp3, p->n3, p->Np2, pack_panel(p->d2, p->n3, w3f))) != WF_OK) return rc;
     }
-    const int knew = a.n_new * M;
-    auto w_l1 = pack_panel(knew + 2 * M, d1, [&](int k, int n) {
-        if (k < knew) return (float)fold[k / M][(size_t)(k % M) * d1 + n];
-        return d->w1[(size_t)n * 4 * M + 2 * M + (k - knew)];
-    });
-    fold.clear();
-    auto w_old = pack_panel(a.n_old * M, 2 * M, [&](int k, int n) {
-        const int o = k / M, c = k % M;
-        return d->ctx_w[(((size_t)n * M + c) * 5 + (p->dy[old_taps[o]] + 2)) * 5 + (p->dx[old_taps[o]] + 2)];
-    });
-    auto w2 = pack_panel(d1, p->d2, [&](int k, int n) { return d->w2[(size_t)n * d1 + k]; });
-    auto w3 = pack_panel(p->d2, p->n3, [&](int k, int n) { return d->w3[(size_t)n * p->d2 + k]; });
     std::vector<float> b2(p->Np2, 0.0f);
     std::copy(d->b2, d->b2 + p->d2, b2.begin());
-
-    float *f;
-    if ((rc = upload(p, &f, w_hoist.data(), w_hoist.size())) != WF_OK) return rc;
-    a.wp_hoist = f;
     if ((rc = upload(p, &f, b_hoist.data(), b_hoist.size())) != WF_OK) return rc;
     a.b_hoist = f;
-    if ((rc = upload(p, &f, w_l1.data(), w_l1.size())) != WF_OK) return rc;
-    a.wp_l1 = f;
-    if ((rc = upload(p, &f, w_old.data(), w_old.size())) != WF_OK) return rc;
-    a.wp_old = f;
-    if ((rc = upload(p, &f, w2.data(), w2.size())) != WF_OK) return rc;
-    a.wp2 = f;
     if ((rc = upload(p, &f, b2.data(), b2.size())) != WF_OK) return rc;
     a.b2 = f;
-    if ((rc = upload(p, &f, w3.data(), w3.size())) != WF_OK) return rc;
-    a.wp3 = f;
     if ((rc = upload(p, &f, d->b3, (size_t)p->n3)) != WF_OK) return rc;
     a.b3 = f;
     if ((rc = upload(p, &f, d->scale_table, (size_t)p->L)) != WF_OK) return rc;
@@ -268,10 +326,17 @@ static int build_plan(const wf_desc* d, Plan* p) {
 
     const size_t R = (size_t)p->max_rows;
     const size_t nlat = (size_t)p->B * H * W;
-    if ((rc = alloc(p, &a.h1, R * Np1)) != WF_OK) return rc;
-    if ((rc = alloc(p, &a.h2, R * p->Np2)) != WF_OK) return rc;
+    float *h1 = nullptr, *h2 = nullptr;
+    if ((rc = alloc(p, &h1, R * Np1)) != WF_OK) return rc;
+    if ((rc = alloc(p, &h2, R * p->Np2)) != WF_OK) return rc;
+    a.h1 = h1;
+    a.h2 = h2;
     if ((rc = alloc(p, &a.p1, nlat * Np1)) != WF_OK) return rc;
     if ((rc = alloc(p, &a.ctxo, (size_t)2 * 3 * R * 2 * M)) != WF_OK) return rc;
+    if (bf) {
+        if ((rc = alloc(p, &a.ctxb, R * 2 * 2 * M)) != WF_OK) return rc;
+        if ((rc = alloc(p, &a.ybf, nlat * 2 * M)) != WF_OK) return rc;
+    }
     if ((rc = alloc(p, &p->d_call, 1)) != WF_OK) return rc;
     WF_HIP(hipMemset(p->d_call, 0, sizeof(CallPtrs)));
     a.cp = p->d_call;
@@ -411,7 +476,7 @@ int wf_plan_trace(wf_plan_t plan, int64_t* stamps, int64_t capacity, int64_t* ne
     if (stamps && capacity < 0) return fail(WF_E_INVALID, "negative capacity");
     p->stamps = reinterpret_cast<long long*>(stamps);
     p->stamps_cap = stamps ? capacity : 0;
-    if (needed) *needed = (int64_t)(1 + 3 * (int64_t)p->T) * (p->grid + 1);
+    if (needed) *needed = (int64_t)(1 + p->nph * (int64_t)p->T) * (p->grid + 1);
     if (grid) *grid = p->grid;
     return WF_OK;
 }

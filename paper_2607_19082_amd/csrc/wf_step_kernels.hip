@@ -5,48 +5,35 @@
 namespace wf {
 
 // Pre-loop: the hyperprior half of layer 1 for every latent.
+template <class P>
 __global__ __launch_bounds__(kThreads) void k_hoist(StepArgs a) {
     __shared__ f4 red[kWaves][64];
-    hoist_job<false>(a, blockIdx.x, red);
-}
-
-// Phase A: layer 1 of step s (blocks [0, nb)), then old-tap context jobs
-// [j0, ...) of step s1.
-__global__ __launch_bounds__(kThreads) void k_phase_a(StepRows s, StepRows s1, int nb, int j0, int nc, StepArgs a) {
-    __shared__ f4 red[kWaves][64];
-    if ((int)blockIdx.x < nb)
-        l1_job<false>(a, s, blockIdx.x, red);
-    else
-        ctxo_job<false>(a, s1, j0 + blockIdx.x - nb, nc, red);
+    hoist_job<P, false>(a, blockIdx.x, red);
 }
 
 // Old-tap context jobs of step s1 only (before the first step).
+template <class P>
 __global__ __launch_bounds__(kThreads) void k_ctxo(StepRows s1, int nc, StepArgs a) {
     __shared__ f4 red[kWaves][64];
-    ctxo_job<false>(a, s1, blockIdx.x, nc, red);
+    ctxo_job<P, false>(a, s1, blockIdx.x, nc, red);
 }
 
-// Phase B: layer 2 of step s, then old-tap context jobs.
-__global__ __launch_bounds__(kThreads) void k_phase_b(StepRows s, StepRows s1, int nb, int j0, int nc, StepArgs a) {
+// Phase ph of step s (blocks [0, nb)), then old-tap context jobs [j0, ...)
+// of step s1.
+template <class P, int KC>
+__global__ __launch_bounds__(kThreads) void k_phase(int ph, StepRows s, StepRows s1, int nb, int j0, int nc,
+                                                    StepArgs a) {
     __shared__ f4 red[kWaves][64];
-    if ((int)blockIdx.x < nb)
-        l2_job<false>(a, s, blockIdx.x, red);
-    else
-        ctxo_job<false>(a, s1, j0 + blockIdx.x - nb, nc, red);
-}
-
-// Phase C: layer 3 and the epilogue of step s, then old-tap context jobs.
-template <int KC>
-__global__ __launch_bounds__(kThreads) void k_phase_c(StepRows s, StepRows s1, int nb, int j0, int nc, StepArgs a) {
     __shared__ L3Smem<KC> sm;
-    __shared__ f4 red[kWaves][64];
     if ((int)blockIdx.x >= nb) {
-        ctxo_job<false>(a, s1, j0 + blockIdx.x - nb, nc, red);
+        ctxo_job<P, false>(a, s1, j0 + blockIdx.x - nb, nc, red);
         return;
     }
-    for (int l = threadIdx.x; l < a.L; l += blockDim.x) sm.tab[l] = a.table[l];
-    __syncthreads();
-    l3_job<KC, false>(a, s, blockIdx.x, sm);
+    if (ph == PH_C) {
+        for (int l = threadIdx.x; l < a.L; l += blockDim.x) sm.tab[l] = a.table[l];
+        __syncthreads();
+    }
+    phase_job<P, KC, false>(ph, a, s, blockIdx.x, red, sm);
 }
 
 __global__ void k_set_call(CallPtrs* dst, CallPtrs v) {
@@ -58,8 +45,16 @@ int enqueue_set_call(Plan& p, const CallPtrs& c, hipStream_t stream) {
     return WF_OK;
 }
 
+template <class P>
+static void launch_hoist(Plan& p, hipStream_t stream) {
+    hipLaunchKernelGGL(k_hoist<P>, dim3(hoist_blocks(p.args)), dim3(kThreads), 0, stream, p.args);
+}
+
 int enqueue_hoist(Plan& p, hipStream_t stream) {
-    hipLaunchKernelGGL(k_hoist, dim3(hoist_blocks(p.args)), dim3(kThreads), 0, stream, p.args);
+    if (p.precision == WF_BF16)
+        launch_hoist<PBF16>(p, stream);
+    else
+        launch_hoist<PF32>(p, stream);
     return WF_OK;
 }
 
@@ -69,29 +64,33 @@ static StepRows rows_of(const Plan& p, int t) {
     return step_rows(p.H, p.W, p.B, p.lambda, t);
 }
 
-int enqueue_steps(Plan& p, hipStream_t stream) {
+template <class P, int KC>
+static void launch_steps(Plan& p, hipStream_t stream) {
     const StepArgs& a = p.args;
-    enqueue_hoist(p, stream);
+    launch_hoist<P>(p, stream);
     {
         const StepRows s0 = rows_of(p, 0);
         const int nc = ctxo_blocks(a, s0);
-        if (nc > 0) hipLaunchKernelGGL(k_ctxo, dim3(kCtxParts * nc), dim3(kThreads), 0, stream, s0, nc, a);
+        if (nc > 0) hipLaunchKernelGGL(k_ctxo<P>, dim3(kCtxParts * nc), dim3(kThreads), 0, stream, s0, nc, a);
     }
     for (int t = 0; t < p.T; ++t) {
         const StepRows s = rows_of(p, t), s1 = rows_of(p, t + 1);
-        const int nc = ctxo_blocks(a, s1);
-        const int nb1 = l1_blocks(a, s), nb2 = l2_blocks(a, s), nb3 = l3_blocks(a, s);
-        int ka, kb, kc, ko;
-        job_costs(a, &ka, &kb, &kc, &ko);
-        const CtxSplit cs = ctxo_split(nc, nb1, nb2, nb3, ka, kb, kc, ko);
-        hipLaunchKernelGGL(k_phase_a, dim3(nb1 + cs.c1), dim3(kThreads), 0, stream, s, s1, nb1, 0, nc, a);
-        hipLaunchKernelGGL(k_phase_b, dim3(nb2 + cs.c2 - cs.c1), dim3(kThreads), 0, stream, s, s1, nb2, cs.c1, nc, a);
-        if (p.K == 1)
-            hipLaunchKernelGGL(k_phase_c<1>, dim3(nb3 + cs.total - cs.c2), dim3(kThreads), 0, stream, s, s1, nb3, cs.c2,
-                               nc, a);
-        else
-            hipLaunchKernelGGL(k_phase_c<3>, dim3(nb3 + cs.total - cs.c2), dim3(kThreads), 0, stream, s, s1, nb3, cs.c2,
-                               nc, a);
+        const StepWork w = step_work<P>(a, s, s1);
+        for (int ph = P::kFirst; ph < kMaxPhases; ++ph) {
+            const int n = w.nb[ph] + w.cut[ph + 1] - w.cut[ph];
+            hipLaunchKernelGGL((k_phase<P, KC>), dim3(n), dim3(kThreads), 0, stream, ph, s, s1, w.nb[ph],
+                               w.cut[ph], w.nc, a);
+        }
+    }
+}
+
+int enqueue_steps(Plan& p, hipStream_t stream) {
+    if (p.precision == WF_BF16) {
+        if (p.K == 1) launch_steps<PBF16, 1>(p, stream);
+        else launch_steps<PBF16, 3>(p, stream);
+    } else {
+        if (p.K == 1) launch_steps<PF32, 1>(p, stream);
+        else launch_steps<PF32, 3>(p, stream);
     }
     hipError_t err = hipGetLastError();
     if (err != hipSuccess) return fail(WF_E_HIP, std::string("kernel launch: ") + hipGetErrorString(err));

@@ -95,6 +95,13 @@ def test_validate(lib):
     assert wf.validate(d) == wf.WF_E_UNSUPPORTED
     d, keep = _desc(M=8)
     assert wf.validate(d) == wf.WF_E_UNSUPPORTED
+    # bf16 operands: a k-block of 32 channels must not straddle two taps
+    d, keep = _desc(M=32, precision="bf16")
+    assert wf.validate(d) == wf.WF_OK
+    d, keep = _desc(M=48, precision="bf16")
+    assert wf.validate(d) == wf.WF_E_UNSUPPORTED
+    d, keep = _desc(M=48)
+    assert wf.validate(d) == wf.WF_OK
     d, keep = _desc()
     d.K = 2
     assert wf.validate(d) == wf.WF_E_INVALID

@@ -17,7 +17,7 @@ import pytest
 from paper_2607_19082_amd import inputs, wf
 
 from gpu_helpers import (compare, gpu_plan, make_case, oracle_model, sample_latents,
-                         teacher_forced, to_np)
+                         teacher_forced, to_np, top_rows_check)
 
 pytestmark = pytest.mark.gpu
 
@@ -117,16 +117,17 @@ def test_reduced_global(name, H, W, B, driver):
     log(compare(got, ref, table, cfg["K"]))
 
 
-@pytest.mark.parametrize("name,n", [
-    ("cheng-gmm3-1080p-120x68-m192", 600),
-    ("minnen-relaxed-b8-120x68-m192", 600),
-    ("minnen-hr-4k-240x135-m320", 300),
+@pytest.mark.parametrize("name,n,rows", [
+    ("cheng-gmm3-1080p-120x68-m192", 600, 6),
+    ("minnen-relaxed-b8-120x68-m192", 600, 3),
+    ("minnen-hr-4k-240x135-m320", 300, 5),
 ])
 @pytest.mark.parametrize("driver", ["graph", "persistent"])
-def test_full_size_teacher_forced(name, n, driver):
-    log(f"case {name} full size, teacher-forced sample of {n}, driver={driver}")
+def test_full_size_teacher_forced(name, n, rows, driver):
+    log(f"case {name} full size, top {rows} rows + teacher-forced sample of {n}, driver={driver}")
     cfg, w, table, psi, sym = make_case(name)
     got = run_decode(cfg, w, table, psi, sym, driver)
+    log(top_rows_check(cfg, w, table, psi, sym, got, rows))
     model = oracle_model(cfg, w, table)
     lats = sample_latents(cfg, n)
     log(teacher_forced(cfg, got, psi, sym, model, lats, table))
