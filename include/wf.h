@@ -167,8 +167,10 @@ int wf_encode(wf_plan_t plan, const float *psi, const float *y, int32_t *sym_out
  * later call records the device wall clock (100 MHz ticks) at each
  * device-wide barrier k = 0, 1, ...: entry k*(G+1) + g is the time workgroup g
  * arrived at barrier k, entry k*(G+1) + G the time workgroup 0 left it, where
- * G is the grid size written to *grid.  A call has 1 + 3*T barriers; *needed
- * receives the entries that takes (either output may be NULL).  Entries past
+ * G is the grid size written to *grid.  A call has 2 + 3*T barriers with
+ * fp32 operands (two before the first step, then one per phase) and 1 + 4*T
+ * with bf16; *needed receives the entries that takes (either output may be
+ * NULL).  Entries past
  * `capacity` are not written.  stamps == NULL turns recording off.  The array
  * stays owned by the caller and must outlive the calls that record into it.
  */

@@ -18,7 +18,8 @@
 //   phase A  h1  = pair(lrelu(P1 + W1b . ctx)),  P1 = b1 + W1[:, :2M] . pair(psi)
 //   phase B  h2  = pair(lrelu(W2 . h1 + b2))
 //   phase C  as above; also keeps the pair form of y_hat for the tap gathers.
-// A pair array holds each row as [hi plane (n values) | lo plane (n values)].
+// A pair array holds each row of n values as n/32 blocks of [32 hi | 32 lo]
+// (one 128-byte line per k-block: an operand's two loads share a line).
 // In both, the kCtxParts k-parts of ctx_old(t+1) ride along with the phases
 // of step t, spread to even out their work (see ctxo_split).
 //
@@ -48,9 +49,9 @@ struct b8x2 {   // eight activation values as bf16 pairs
 constexpr int kWaves = 4;              // waves per workgroup; they split a tile's k-blocks
 constexpr int kThreads = 64 * kWaves;
 constexpr int kCtxParts = 3;  // k-parts of the old-tap context product
-constexpr int kKbw = 10;   // k-blocks loaded by a wave before its MFMAs
 constexpr int kSc1 = 16;   // cache-policy bits of an agent-coherent buffer access
 constexpr int kMaxPhases = 4;
+constexpr int kMaxC = kColsF32 > kColsBf16 ? kColsF32 : kColsBf16;   // most column tiles of one job (rows of the reduction buffer: kWaves * kMaxC)
 
 // Phases of a step, in order; fp32 runs PH_A..PH_C, bf16 PH_N..PH_C.
 enum { PH_N = 0, PH_A = 1, PH_B = 2, PH_C = 3 };
@@ -78,7 +79,9 @@ struct PF32 {
     static constexpr int kK = 16;
     static constexpr bool kBf16 = false;
     static constexpr int kFirst = PH_A;
-    static constexpr int kL3Kbw1 = 16, kL3Kbw3 = 4;   // k-blocks in flight per l3 wave (K = 1, 3)
+    static constexpr int kC = kColsF32;               // column tiles of one job (A loaded once for all)
+    static constexpr int kKbw = 10;                   // k-blocks a wave loads before its MFMAs
+    static constexpr int kL3Kbw1 = 16, kL3Kbw3 = 4;   // the same for l3 (K = 1, 3)
     __device__ static __forceinline__ f4 mma(A a, B b, f4 acc) { return mfma_k16(a, b, acc); }
 };
 struct PBF16 {
@@ -87,6 +90,8 @@ struct PBF16 {
     static constexpr int kK = 32;
     static constexpr bool kBf16 = true;
     static constexpr int kFirst = PH_N;
+    static constexpr int kC = kColsBf16;
+    static constexpr int kKbw = 6;
     static constexpr int kL3Kbw1 = 8, kL3Kbw3 = 3;
     __device__ static __forceinline__ f4 mma(A a, B b, f4 acc) {
         acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a.hi, b, acc, 0, 0, 0);
@@ -95,6 +100,11 @@ struct PBF16 {
 };
 
 __device__ __forceinline__ float lrelu(float v, float s) { return v >= 0.0f ? v : s * v; }
+
+// The wave's index in its workgroup, as a wave-uniform value: k-ranges and
+// tap geometry derived from it then live in scalar registers and scalar
+// branches, not in per-lane arithmetic under exec masks.
+__device__ __forceinline__ int wave_id() { return __builtin_amdgcn_readfirstlane(threadIdx.x >> 6); }
 
 __device__ __forceinline__ f4 zero4() { return f4{0.0f, 0.0f, 0.0f, 0.0f}; }
 
@@ -172,7 +182,8 @@ __device__ __forceinline__ void st1h(uint16_t* base, size_t idx, uint16_t h) {
 }
 
 // Activation arrays: fp32 rows of n values, or bf16 pair rows of 2n values
-// ([hi plane | lo plane]).  act_row is the first element of row r.
+// (per k-block of 32 values: 32 hi then 32 lo).  act_row is the first
+// element of row r.
 template <class P>
 __device__ __forceinline__ size_t act_row(size_t r, int n) {
     return r * (size_t)n * (P::kBf16 ? 2 : 1);
@@ -182,8 +193,8 @@ template <class P, bool COH>
 __device__ __forceinline__ typename P::A ld_act(const void* base, size_t row, int n, int kb, int kq, bool ok) {
     if constexpr (P::kBf16) {
         const uint16_t* h = static_cast<const uint16_t*>(base);
-        const size_t q = row + (size_t)kb * 32 + kq * 8;
-        return b8x2{ld8h<COH>(h, q, ok), ld8h<COH>(h, q + n, ok)};
+        const size_t q = row + (size_t)kb * 64 + kq * 8;
+        return b8x2{ld8h<COH>(h, q, ok), ld8h<COH>(h, q + 32, ok)};
     } else {
         return ld4<COH>(static_cast<const float*>(base), row + (size_t)kb * 16 + kq * 4, ok);
     }
@@ -194,8 +205,9 @@ __device__ __forceinline__ void st_act(void* base, size_t row, int n, int col, f
     if constexpr (P::kBf16) {
         uint16_t* h = static_cast<uint16_t*>(base);
         const uint16_t hi = bf16_bits(v);
-        st1h<COH>(h, row + col, hi);
-        st1h<COH>(h, row + n + col, bf16_bits(v - bf16_value(hi)));
+        const size_t q = row + (size_t)(col >> 5) * 64 + (col & 31);
+        st1h<COH>(h, q, hi);
+        st1h<COH>(h, q + 32, bf16_bits(v - bf16_value(hi)));
     } else {
         st1<COH>(static_cast<float*>(base), row + col, v);
     }
@@ -267,42 +279,40 @@ __host__ __device__ __forceinline__ int xcd_blocks(int nct, int nrt) {
 
 __host__ __device__ __forceinline__ int ntiles(int n) { return (n + kTile - 1) / kTile; }
 
-// Output column tiles of the main job of each phase.
+// Jobs compute kC adjacent column tiles ("a column group") of one 16-row
+// tile: the activation operand is loaded once for all of them.  Column
+// groups of the main job of each phase (l3 keeps its own grouping: value
+// group x channel tile).
+template <class P>
 __host__ __device__ __forceinline__ int phase_cols(const StepArgs& a, int ph) {
     switch (ph) {
-        case PH_N: return 2 * a.M / kTile;
-        case PH_A: return a.Np1 / kTile;
-        case PH_B: return a.Np2 / kTile;
-        default: return 2 * a.M / kTile;   // PH_C: value group x channel group
+        case PH_N: return 2 * a.M / kTile / P::kC;
+        case PH_A: return a.Np1 / kTile / P::kC;
+        case PH_B: return a.Np2 / kTile / P::kC;
+        default: return 2 * a.M / kTile;   // PH_C: value group x channel tile
     }
 }
+template <class P>
 __host__ __device__ __forceinline__ int phase_blocks(const StepArgs& a, const StepRows& s, int ph) {
-    return xcd_blocks(phase_cols(a, ph), ntiles(s.nrows));
+    return xcd_blocks(phase_cols<P>(a, ph), ntiles(s.nrows));
 }
 // one k-part of the old-tap context of the latents of step s (nrows may be 0)
+template <class P>
 __host__ __device__ __forceinline__ int ctxo_blocks(const StepArgs& a, const StepRows& s) {
     if (a.n_old == 0 || s.nrows == 0) return 0;
-    return xcd_blocks(2 * a.M / kTile, ntiles(s.nrows));
-}
-
-// k-blocks streamed by one job of each phase and of the old-tap context (the
-// l3 jobs stream a value group's column tiles: K=1 one, K=3 up to six).
-template <class P>
-__host__ __device__ __forceinline__ void job_costs(const StepArgs& a, int* kph, int* ko) {
-    constexpr int kK = P::kK;
-    kph[PH_N] = a.n_new * a.M / kK;
-    kph[PH_A] = P::kBf16 ? 2 * a.M / kK : (a.n_new * a.M + 2 * a.M) / kK;
-    kph[PH_B] = a.Np1 / kK;
-    kph[PH_C] = a.Np2 / kK * (a.K == 1 ? 1 : 4);
-    *ko = a.n_old * a.M / kK / kCtxParts;
+    return xcd_blocks(2 * a.M / kTile / P::kC, ntiles(s.nrows));
 }
 
 // The work of one step: main blocks of each phase and which of the
 // kCtxParts * nc old-tap context jobs of the next step ride along with it:
-// phase ph takes jobs [cut[ph], cut[ph + 1]).  The cuts equalise the k-blocks
-// each phase streams, so that every phase holds about the same work; they
-// are multiples of 8, which keeps every job on the XCD its column tile
-// belongs to.
+// phase ph takes jobs [cut[ph], cut[ph + 1]) (part-major: job j is part
+// j / nc).  A phase lasts as long as its busiest workgroup, so the context
+// jobs first fill the slots left free in the last round of each phase's own
+// jobs (a.slots workgroups run at once); only what is left adds rounds,
+// spread evenly over the phases.  With fp32 the last part's jobs all run in
+// the last phase, after the other parts, and add them in (see ctxo_job).
+// Cuts are multiples of 8, which keeps every job on the XCD its column tile
+// belongs to (nc and every phase's block count are multiples of 8).
 struct StepWork {
     int nb[kMaxPhases];
     int cut[kMaxPhases + 1];
@@ -318,116 +328,148 @@ struct StepWork {
 };
 template <class P>
 __host__ __device__ __forceinline__ StepWork step_work(const StepArgs& a, const StepRows& s, const StepRows& s1) {
+    // phases that share the context jobs, and the jobs they share
+    constexpr int last = P::kBf16 ? kMaxPhases : PH_C;
+    constexpr int nph = last - P::kFirst;
     StepWork w;
-    int kph[kMaxPhases], ko;
-    job_costs<P>(a, kph, &ko);
-    w.nc = ctxo_blocks(a, s1);
-    const int total = kCtxParts * w.nc;
-    long long sum = (long long)total * ko;
+    w.nc = ctxo_blocks<P>(a, s1);
+    const int G = a.slots;
+    int left = (P::kBf16 ? kCtxParts : kCtxParts - 1) * w.nc;
+    int take[kMaxPhases];
+#pragma unroll
     for (int ph = 0; ph < kMaxPhases; ++ph) {
-        w.nb[ph] = ph < P::kFirst ? 0 : phase_blocks(a, s, ph);
-        sum += (long long)w.nb[ph] * kph[ph];
+        w.nb[ph] = ph < P::kFirst ? 0 : phase_blocks<P>(a, s, ph);
+        const int nb = w.nb[ph];
+        const int free_slots = nb > 0 ? ((nb + G - 1) / G * G - nb) / kXcds * kXcds : 0;
+        take[ph] = ph < P::kFirst || ph >= last ? 0 : (left < free_slots ? left : free_slots);
+        left -= take[ph];
     }
-    const long long each = sum / (kMaxPhases - P::kFirst);
-    for (int ph = 0; ph <= P::kFirst; ++ph) w.cut[ph] = 0;
-    for (int ph = P::kFirst; ph < kMaxPhases - 1; ++ph) {
-        const long long own = (long long)w.nb[ph] * kph[ph];
-        const int left = total - w.cut[ph];
-        long long j = ko > 0 && each > own ? (each - own) / ko : 0;
-        if (j > left) j = left;
-        w.cut[ph + 1] = w.cut[ph] + (int)(j / kXcds * kXcds);
+    const int extra = ((left + nph - 1) / nph + kXcds - 1) / kXcds * kXcds;
+    w.cut[0] = 0;
+#pragma unroll
+    for (int ph = 0; ph < kMaxPhases; ++ph) {
+        if (ph >= P::kFirst && ph < last) {
+            const int e = left < extra ? left : extra;
+            take[ph] += e;
+            left -= e;
+        }
+        if (!P::kBf16 && ph == PH_C) take[ph] = w.nc;   // the last part
+        w.cut[ph + 1] = w.cut[ph] + take[ph];
     }
-    w.cut[kMaxPhases] = total;
     return w;
 }
 
-// A wave's partial 16x16 tile over k-blocks [kb0, kb1): w points at the
-// lane's operand of k-block 0 of the tile's packed weight column.  The loads
-// of up to kKbw k-blocks are issued before the MFMAs that use them (indices
-// past the range are clamped, so every load is unconditional); la(kb) must
-// be branch-free.
+// A wave's partial sums of kC 16x16 tiles over k-blocks [kb0, kb1): w points
+// at the lane's operand of k-block 0 of the first tile's packed weight column
+// (tile c at w + c * ws).  The loads of up to P::kKbw k-blocks are issued
+// before the MFMAs that use them (indices past the range are clamped, so every
+// load is unconditional); la(kb) must be branch-free.  Each activation operand
+// feeds kC independent MFMA chains.
 template <class P, class LoadA>
-__device__ __forceinline__ f4 wave_dot(const typename P::B* __restrict__ w, int kb0, int kb1, LoadA la) {
-    f4 acc = zero4();
+__device__ __forceinline__ void wave_dot(const typename P::B* __restrict__ w, size_t ws, int kb0, int kb1, LoadA la,
+                                         f4 (&acc)[P::kC]) {
+    constexpr int kKbw = P::kKbw, C = P::kC;
     for (int kc = kb0; kc < kb1; kc += kKbw) {
         typename P::A av[kKbw];
-        typename P::B bv[kKbw];
+        typename P::B bv[kKbw][C];
 #pragma unroll
         for (int u = 0; u < kKbw; ++u) {
             const int k = min(kc + u, kb1 - 1);
             av[u] = la(k);
-            bv[u] = w[(size_t)k * 64];
+#pragma unroll
+            for (int c = 0; c < C; ++c) bv[u][c] = w[c * ws + (size_t)k * 64];
         }
 #pragma unroll
         for (int u = 0; u < kKbw; ++u)
-            if (kc + u < kb1) acc = P::mma(av[u], bv[u], acc);
+            if (kc + u < kb1)
+#pragma unroll
+                for (int c = 0; c < C; ++c) acc[c] = P::mma(av[u], bv[u][c], acc[c]);
     }
-    return acc;
 }
 
 // The four waves of a block split the k-blocks [klo, khi) (default: all nkb)
-// of one tile; k-blocks below `ksplit` are loaded by la_lo, the rest by la_hi.
-// Afterwards waves 0..3 hold the full sum of tile row 4*(lane/16) + wave,
-// column lane%16 (the other waves get 0).  Ends with a block barrier, so `red`
-// may be reused.
+// of column group cg; k-blocks below `ksplit` are loaded by la_lo, the rest
+// by la_hi.  Afterwards waves 0..3 hold in v[c] the full sum of tile c's row
+// 4*(lane/16) + wave, column lane%16 (the other waves get 0).  red holds
+// kWaves * kC rows.  Ends with a block barrier, so `red` may be reused.
 template <class P, class LoadLo, class LoadHi>
-__device__ __forceinline__ float block_tile2(f4 (*red)[64], const void* __restrict__ wp, int nkb, int ct,
-                                             int ksplit, LoadLo la_lo, LoadHi la_hi, int klo = 0, int khi = -1) {
-    const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+__device__ __forceinline__ void block_tiles2(f4 (*red)[64], const void* __restrict__ wp, int nkb, int cg, int ksplit,
+                                             LoadLo la_lo, LoadHi la_hi, float (&v)[P::kC], int klo = 0,
+                                             int khi = -1) {
+    constexpr int C = P::kC;
+    const int wave = wave_id(), lane = threadIdx.x & 63;
     if (khi < 0) khi = nkb;
     const int per = (khi - klo + kWaves - 1) / kWaves;
     const int kb0 = min(khi, klo + wave * per), kb1 = min(khi, kb0 + per);
-    const typename P::B* w = static_cast<const typename P::B*>(wp) + (size_t)ct * nkb * 64 + lane;
-    f4 acc = wave_dot<P>(w, kb0, min(kb1, ksplit), la_lo);
-    acc += wave_dot<P>(w, max(kb0, ksplit), kb1, la_hi);
-    red[wave][lane] = acc;
-    __syncthreads();
-    float v = 0.0f;
-    if (wave < 4) {
+    const size_t ws = (size_t)nkb * 64;
+    const typename P::B* w = static_cast<const typename P::B*>(wp) + (size_t)cg * C * ws + lane;
+    f4 acc[C];
 #pragma unroll
-        for (int w2 = 0; w2 < kWaves; ++w2) v += red[w2][lane][wave];
+    for (int c = 0; c < C; ++c) acc[c] = zero4();
+    wave_dot<P>(w, ws, kb0, min(kb1, ksplit), la_lo, acc);
+    wave_dot<P>(w, ws, max(kb0, ksplit), kb1, la_hi, acc);
+#pragma unroll
+    for (int c = 0; c < C; ++c) red[wave * C + c][lane] = acc[c];
+    __syncthreads();
+#pragma unroll
+    for (int c = 0; c < C; ++c) {
+        v[c] = 0.0f;
+        if (wave < 4) {
+#pragma unroll
+            for (int w2 = 0; w2 < kWaves; ++w2) v[c] += red[w2 * C + c][lane][wave];
+        }
     }
     __syncthreads();
-    return v;
 }
 
 template <class P, class LoadA>
-__device__ __forceinline__ float block_tile(f4 (*red)[64], const void* __restrict__ wp, int nkb, int ct,
-                                            LoadA la, int klo = 0, int khi = -1) {
-    return block_tile2<P>(red, wp, nkb, ct, nkb, la, la, klo, khi);
+__device__ __forceinline__ void block_tiles(f4 (*red)[64], const void* __restrict__ wp, int nkb, int cg, LoadA la,
+                                            float (&v)[P::kC], int klo = 0, int khi = -1) {
+    block_tiles2<P>(red, wp, nkb, cg, nkb, la, la, v, klo, khi);
+}
+
+// Output column of tile c of column group cg for this lane.
+template <class P>
+__device__ __forceinline__ int group_col(int cg, int c) {
+    return (cg * P::kC + c) * kTile + (threadIdx.x & 15);
 }
 
 // ---------------------------------------------------------------------------
 // Pre-loop job b: P1[lat][n] = b_hoist[n] + sum_k psi[lat][k] * W1[n][k]
-// (k < 2M) for one 16x16 tile of the nlat x Np1 product.
+// (k < 2M) for one 16-row tile and column group of the nlat x Np1 product.
+template <class P>
 __host__ __device__ __forceinline__ int hoist_blocks(const StepArgs& a) {
-    return xcd_blocks(a.Np1 / kTile, ntiles(a.B * a.H * a.W));
+    return xcd_blocks(a.Np1 / kTile / P::kC, ntiles(a.B * a.H * a.W));
 }
 
 template <class P, bool COH>
 __device__ __forceinline__ void hoist_job(const StepArgs& a, int b, f4 (*red)[64]) {
+    constexpr int C = P::kC;
     const int nlat = a.B * a.H * a.W;
-    const Job jb = xcd_job(b, a.Np1 / kTile, ntiles(nlat));
+    const Job jb = xcd_job(b, a.Np1 / kTile / C, ntiles(nlat));
     if (!jb.valid) return;
-    const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63, kq = lane >> 4;
+    const int wave = wave_id(), lane = threadIdx.x & 63, kq = lane >> 4;
     const int r = jb.rt * kTile + (lane & 15);
     const float* psi = a.cp->psi;
-    const int n = jb.ct * kTile + (lane & 15);
-    const float bias = a.b_hoist[n];
-    float v;
+    float bias[C], v[C];
+#pragma unroll
+    for (int c = 0; c < C; ++c) bias[c] = a.b_hoist[group_col<P>(jb.ct, c)];
     if constexpr (P::kBf16) {
         const size_t base = (size_t)r * 2 * a.M + kq * 8;
         auto la = [&](int kb) -> b8x2 {
             return split8(ld4<false>(psi, base + kb * 32, r < nlat), ld4<false>(psi, base + kb * 32 + 4, r < nlat));
         };
-        v = block_tile<P>(red, a.wp_hoist, 2 * a.M / P::kK, jb.ct, la);
+        block_tiles<P>(red, a.wp_hoist, 2 * a.M / P::kK, jb.ct, la, v);
     } else {
         const size_t base = (size_t)r * 2 * a.M + kq * 4;
         auto la = [&](int kb) -> f4 { return ld4<false>(psi, base + kb * kTile, r < nlat); };
-        v = block_tile<P>(red, a.wp_hoist, 2 * a.M / P::kK, jb.ct, la);
+        block_tiles<P>(red, a.wp_hoist, 2 * a.M / P::kK, jb.ct, la, v);
     }
     const int ro = jb.rt * kTile + kq * 4 + wave;
-    if (wave < 4 && ro < nlat) st1<COH>(a.p1, (size_t)ro * a.Np1 + n, v + bias);
+    if (wave < 4 && ro < nlat) {
+#pragma unroll
+        for (int c = 0; c < C; ++c) st1<COH>(a.p1, (size_t)ro * a.Np1 + group_col<P>(jb.ct, c), v[c] + bias[c]);
+    }
 }
 
 // Tap gather of k-block kb of a row's taps (fp32: y_hat, bf16: its pair
@@ -451,8 +493,9 @@ __device__ __forceinline__ typename P::A ld_tap(const StepArgs& a, const Row& w,
     const bool ok = w.valid && ii >= 0 && jj >= 0 && jj < a.W;
     const size_t lat = ((size_t)w.b * a.H + ii) * a.W + jj;
     if constexpr (P::kBf16) {
-        const size_t q = lat * 2 * M + c;
-        return b8x2{ld8h<COH>(a.ybf, q, ok), ld8h<COH>(a.ybf, q + M, ok)};
+        // c = 32 * (k-block in the latent's row) + 8 * kq
+        const size_t q = lat * 2 * M + (size_t)(c >> 5) * 64 + (c & 31);
+        return b8x2{ld8h<COH>(a.ybf, q, ok), ld8h<COH>(a.ybf, q + 32, ok)};
     } else {
         return ld4<COH>(a.cp->y_hat, lat * M + c, ok);
     }
@@ -462,111 +505,154 @@ __device__ __forceinline__ typename P::A ld_tap(const StepArgs& a, const Row& w,
 // Job j of the old-tap context of the latents of step s: k-part part = j / nc
 // (a contiguous range of the k-blocks of the gathered old taps, tap-major)
 // of block j % nc:  ctxo[part][r][n] = sum_{k in part} taps[r][k] Wc[k][n].
+// With fp32 the last part runs after the others and stores the whole sum
+// (its own part plus theirs), so layer 1 reads one value per element.
 template <class P, bool COH>
 __device__ __forceinline__ void ctxo_job(const StepArgs& a, const StepRows& s, int j, int nc, f4 (*red)[64]) {
+    constexpr int C = P::kC;
     const int part = j / nc, b = j - part * nc;
     const int M = a.M;
-    const Job jb = xcd_job(b, 2 * M / kTile, ntiles(s.nrows));
+    const Job jb = xcd_job(b, 2 * M / kTile / C, ntiles(s.nrows));
     if (!jb.valid) return;
-    const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63, kq = lane >> 4;
+    const int wave = wave_id(), lane = threadIdx.x & 63, kq = lane >> 4;
+    const int ro = wave < 4 ? jb.rt * kTile + kq * 4 + wave : s.nrows;
+    const bool vo = ro < s.nrows;
+    // double-buffered by step parity: jobs for step s.t may run while the
+    // context of step s.t - 1 is still being read from the other half
+    const size_t cpart = (size_t)a.max_rows * 2 * M;
+    const size_t q = (size_t)(s.t & 1) * kCtxParts * cpart + (size_t)ro * 2 * M;
+    float prev[C], v[C];
+#pragma unroll
+    for (int c = 0; c < C; ++c) {
+        prev[c] = 0.0f;
+        if (!P::kBf16 && part == kCtxParts - 1) {
+#pragma unroll
+            for (int p2 = 0; p2 < kCtxParts - 1; ++p2)
+                prev[c] += ld1<COH>(a.ctxo, q + p2 * cpart + group_col<P>(jb.ct, c), vo);
+        }
+    }
     const Row w = step_row(a, s, jb.rt * kTile + (lane & 15));
     auto la = [&](int kb) { return ld_tap<P, COH>(a, w, kb, kq, true); };
     const int nkb = a.n_old * M / P::kK;
     const int klo = nkb * part / kCtxParts, khi = nkb * (part + 1) / kCtxParts;
-    const float acc = block_tile<P>(red, a.wp_old, nkb, jb.ct, la, klo, khi);
-    const int n = jb.ct * kTile + (lane & 15);
-    const int ro = wave < 4 ? jb.rt * kTile + kq * 4 + wave : s.nrows;
-    // double-buffered by step parity: jobs for step s.t may run while the
-    // context of step s.t - 1 is still being read from the other half
-    const size_t slot = (size_t)((s.t & 1) * kCtxParts + part) * a.max_rows + ro;
-    if (ro < s.nrows) st1<COH>(a.ctxo, slot * 2 * M + n, acc);
+    block_tiles<P>(red, a.wp_old, nkb, jb.ct, la, v, klo, khi);
+    if (vo) {
+#pragma unroll
+        for (int c = 0; c < C; ++c) st1<COH>(a.ctxo, q + part * cpart + group_col<P>(jb.ct, c), v[c] + prev[c]);
+    }
 }
 
 // Phase A, fp32: layer 1 of step s over [new taps ; old-tap context].
 template <bool COH>
 __device__ __forceinline__ void l1_fold_job(const StepArgs& a, const StepRows& s, int b, f4 (*red)[64]) {
-    const Job jb = xcd_job(b, a.Np1 / kTile, ntiles(s.nrows));
+    constexpr int C = PF32::kC;
+    const Job jb = xcd_job(b, a.Np1 / kTile / C, ntiles(s.nrows));
     if (!jb.valid) return;
-    const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63, kq = lane >> 4;
+    const int wave = wave_id(), lane = threadIdx.x & 63, kq = lane >> 4;
     const int M = a.M;
-    // epilogue operand first: the hoisted part of this wave's row
-    const int n = jb.ct * kTile + (lane & 15);
+    // epilogue operands first: the hoisted part of this wave's row
     const int ro = wave < 4 ? jb.rt * kTile + kq * 4 + wave : s.nrows;   // epilogue row of this wave
     const Row v = step_row(a, s, ro);
-    const float z = ld1<COH>(a.p1, v.lat * a.Np1 + n, v.valid);
+    float z[C], acc[C];
+#pragma unroll
+    for (int c = 0; c < C; ++c) z[c] = ld1<COH>(a.p1, v.lat * a.Np1 + group_col<PF32>(jb.ct, c), v.valid);
     const int r = jb.rt * kTile + (lane & 15);
     const Row w = step_row(a, s, r);
     const int knew = a.n_new * M;
     const size_t cpart = (size_t)a.max_rows * 2 * M;
-    const size_t cbase = (size_t)(s.t & 1) * kCtxParts * cpart + (size_t)r * 2 * M + kq * 4;
+    // the old-tap context: the last part's slot holds the whole sum
+    const size_t cbase = ((size_t)(s.t & 1) * kCtxParts + kCtxParts - 1) * cpart + (size_t)r * 2 * M + kq * 4;
     auto la_new = [&](int kb) { return ld_tap<PF32, COH>(a, w, kb, kq, false); };
-    auto la_ctx = [&](int kb) -> f4 {
-        const size_t q = cbase + (kb * kTile - knew);
-        f4 v = ld4<COH>(a.ctxo, q, w.valid);
+    auto la_ctx = [&](int kb) -> f4 { return ld4<COH>(a.ctxo, cbase + (kb * kTile - knew), w.valid); };
+    block_tiles2<PF32>(red, a.wp_l1, (knew + 2 * M) / kTile, jb.ct, knew / kTile, la_new, la_ctx, acc);
+    if (v.valid) {
 #pragma unroll
-        for (int part = 1; part < kCtxParts; ++part) v += ld4<COH>(a.ctxo, q + part * cpart, w.valid);
-        return v;
-    };
-    const float acc = block_tile2<PF32>(red, a.wp_l1, (knew + 2 * M) / kTile, jb.ct, knew / kTile, la_new, la_ctx);
-    if (v.valid) st1<COH>(static_cast<float*>(a.h1), (size_t)ro * a.Np1 + n, lrelu(acc + z, a.slope));
+        for (int c = 0; c < C; ++c)
+            st1<COH>(static_cast<float*>(a.h1), (size_t)ro * a.Np1 + group_col<PF32>(jb.ct, c),
+                     lrelu(acc[c] + z[c], a.slope));
+    }
 }
 
-// Phase N, bf16: the context vector of step s, rounded to bf16.
+// Phase N, bf16: the context vector of step s, as bf16 pairs.
 template <bool COH>
 __device__ __forceinline__ void ctxn_job(const StepArgs& a, const StepRows& s, int b, f4 (*red)[64]) {
+    constexpr int C = PBF16::kC;
     const int M = a.M;
-    const Job jb = xcd_job(b, 2 * M / kTile, ntiles(s.nrows));
+    const Job jb = xcd_job(b, 2 * M / kTile / C, ntiles(s.nrows));
     if (!jb.valid) return;
-    const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63, kq = lane >> 4;
+    const int wave = wave_id(), lane = threadIdx.x & 63, kq = lane >> 4;
     // epilogue operands first: bias and the old-tap context parts
-    const int n = jb.ct * kTile + (lane & 15);
     const int ro = wave < 4 ? jb.rt * kTile + kq * 4 + wave : s.nrows;
     const bool vo = ro < s.nrows;
     const size_t cpart = (size_t)a.max_rows * 2 * M;
-    const size_t cq = (size_t)(s.t & 1) * kCtxParts * cpart + (size_t)ro * 2 * M + n;
-    float z = a.bc[n];
+    const size_t cq = (size_t)(s.t & 1) * kCtxParts * cpart + (size_t)ro * 2 * M;
+    float z[C], acc[C];
 #pragma unroll
-    for (int part = 0; part < kCtxParts; ++part) z += ld1<COH>(a.ctxo, cq + part * cpart, vo && a.n_old > 0);
+    for (int c = 0; c < C; ++c) {
+        const int n = group_col<PBF16>(jb.ct, c);
+        z[c] = a.bc[n];
+#pragma unroll
+        for (int part = 0; part < kCtxParts; ++part)
+            z[c] += ld1<COH>(a.ctxo, cq + part * cpart + n, vo && a.n_old > 0);
+    }
     const Row w = step_row(a, s, jb.rt * kTile + (lane & 15));
     auto la = [&](int kb) { return ld_tap<PBF16, COH>(a, w, kb, kq, false); };
-    const float acc = block_tile<PBF16>(red, a.wp_new, a.n_new * M / PBF16::kK, jb.ct, la);
-    if (vo) st_act<PBF16, COH>(a.ctxb, act_row<PBF16>(ro, 2 * M), 2 * M, n, acc + z);
+    block_tiles<PBF16>(red, a.wp_new, a.n_new * M / PBF16::kK, jb.ct, la, acc);
+    if (vo) {
+#pragma unroll
+        for (int c = 0; c < C; ++c)
+            st_act<PBF16, COH>(a.ctxb, act_row<PBF16>(ro, 2 * M), 2 * M, group_col<PBF16>(jb.ct, c), acc[c] + z[c]);
+    }
 }
 
-// Phase A, bf16: layer 1 of step s over the bf16 context vector.
+// Phase A, bf16: layer 1 of step s over the context vector.
 template <bool COH>
 __device__ __forceinline__ void l1_ctx_job(const StepArgs& a, const StepRows& s, int b, f4 (*red)[64]) {
-    const Job jb = xcd_job(b, a.Np1 / kTile, ntiles(s.nrows));
+    constexpr int C = PBF16::kC;
+    const Job jb = xcd_job(b, a.Np1 / kTile / C, ntiles(s.nrows));
     if (!jb.valid) return;
-    const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63, kq = lane >> 4;
+    const int wave = wave_id(), lane = threadIdx.x & 63, kq = lane >> 4;
     const int M = a.M;
-    const int n = jb.ct * kTile + (lane & 15);
     const int ro = wave < 4 ? jb.rt * kTile + kq * 4 + wave : s.nrows;
     const Row v = step_row(a, s, ro);
-    const float z = ld1<COH>(a.p1, v.lat * a.Np1 + n, v.valid);
+    float z[C], acc[C];
+#pragma unroll
+    for (int c = 0; c < C; ++c) z[c] = ld1<COH>(a.p1, v.lat * a.Np1 + group_col<PBF16>(jb.ct, c), v.valid);
     const int r = jb.rt * kTile + (lane & 15);
     const bool valid = r < s.nrows;
     const size_t row = act_row<PBF16>(r, 2 * M);
     auto la = [&](int kb) { return ld_act<PBF16, COH>(a.ctxb, row, 2 * M, kb, kq, valid); };
-    const float acc = block_tile<PBF16>(red, a.wp_l1, 2 * M / PBF16::kK, jb.ct, la);
-    if (v.valid) st_act<PBF16, COH>(a.h1, act_row<PBF16>(ro, a.Np1), a.Np1, n, lrelu(acc + z, a.slope));
+    block_tiles<PBF16>(red, a.wp_l1, 2 * M / PBF16::kK, jb.ct, la, acc);
+    if (v.valid) {
+#pragma unroll
+        for (int c = 0; c < C; ++c)
+            st_act<PBF16, COH>(a.h1, act_row<PBF16>(ro, a.Np1), a.Np1, group_col<PBF16>(jb.ct, c),
+                               lrelu(acc[c] + z[c], a.slope));
+    }
 }
 
 // Phase B: layer 2.
 template <class P, bool COH>
 __device__ __forceinline__ void l2_job(const StepArgs& a, const StepRows& s, int b, f4 (*red)[64]) {
-    const Job jb = xcd_job(b, a.Np2 / kTile, ntiles(s.nrows));
+    constexpr int C = P::kC;
+    const Job jb = xcd_job(b, a.Np2 / kTile / C, ntiles(s.nrows));
     if (!jb.valid) return;
-    const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63, kq = lane >> 4;
-    const int n = jb.ct * kTile + (lane & 15);
-    const float bias = a.b2[n];
+    const int wave = wave_id(), lane = threadIdx.x & 63, kq = lane >> 4;
+    float bias[C], acc[C];
+#pragma unroll
+    for (int c = 0; c < C; ++c) bias[c] = a.b2[group_col<P>(jb.ct, c)];
     const int r = jb.rt * kTile + (lane & 15);
     const bool valid = r < s.nrows;
     const size_t row = act_row<P>(r, a.Np1);
     auto la = [&](int kb) { return ld_act<P, COH>(a.h1, row, a.Np1, kb, kq, valid); };
-    const float acc = block_tile<P>(red, a.wp2, a.Np1 / P::kK, jb.ct, la);
+    block_tiles<P>(red, a.wp2, a.Np1 / P::kK, jb.ct, la, acc);
     const int ro = jb.rt * kTile + kq * 4 + wave;
-    if (wave < 4 && ro < s.nrows) st_act<P, COH>(a.h2, act_row<P>(ro, a.Np2), a.Np2, n, lrelu(acc + bias, a.slope));
+    if (wave < 4 && ro < s.nrows) {
+#pragma unroll
+        for (int c = 0; c < C; ++c)
+            st_act<P, COH>(a.h2, act_row<P>(ro, a.Np2), a.Np2, group_col<P>(jb.ct, c),
+                           lrelu(acc[c] + bias[c], a.slope));
+    }
 }
 
 __device__ __forceinline__ int scale_index(const float* tab, int L, float sg) {
@@ -603,7 +689,7 @@ __device__ __forceinline__ void l3_job(const StepArgs& a, const StepRows& s, int
     const Job jb = xcd_job(b, 2 * G, ntiles(s.nrows));
     if (!jb.valid) return;
     const int vg = jb.ct / G, cg = jb.ct - vg * G, rt = jb.rt;
-    const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63, kq = lane >> 4;
+    const int wave = wave_id(), lane = threadIdx.x & 63, kq = lane >> 4;
 
     // epilogue operands of this wave's row first
     const CallPtrs* cp = a.cp;

@@ -14,6 +14,8 @@ namespace wf {
 constexpr int kMaxTaps = 12;
 constexpr int kMaxNew = 2;           // taps written by the immediately preceding step
 constexpr int kTile = 16;            // MFMA tile edge (rows and columns)
+constexpr int kColsF32 = 2;          // column tiles of one job, fp32 operands
+constexpr int kColsBf16 = 4;         // the same, bf16 operands
 constexpr int kMaxTable = 256;
 constexpr int kXcds = 8;             // accelerator complex dies of an MI355X
 constexpr int kBarrierWords = 512;   // barrier counters of the persistent driver
@@ -54,7 +56,7 @@ struct CallPtrs {
 //
 // Packed weights (wp_*) hold 16-byte lane operands per (column tile, k-block):
 // fp32 k-blocks of 16, bf16 k-blocks of 32.  Np1, Np2 are d1, d2 rounded up to
-// a whole k-block.
+// a whole k-block and a whole column group (kColsF32 / kColsBf16 tiles).
 struct StepArgs {
     int H, W, M, B, K, L, lambda;
     int Np1, Np2, n3;
@@ -78,12 +80,13 @@ struct StepArgs {
     const float* b3;        // [n3]
     const float* table;     // [L]
     float* p1;              // [B*H*W][Np1] hoisted layer-1 part
-    void* h1;               // [max_rows][Np1]  fp32, or bf16 pairs [max_rows][2][Np1]
-    void* h2;               // [max_rows][Np2]  fp32, or bf16 pairs [max_rows][2][Np2]
+    void* h1;               // [max_rows][Np1]  fp32, or bf16 pairs [max_rows][Np1/32][2][32]
+    void* h2;               // [max_rows][Np2]  fp32, or bf16 pairs [max_rows][Np2/32][2][32]
     float* ctxo;            // [2][3][max_rows][2M] old-tap context k-parts, by step parity
-    uint16_t* ctxb;         // bf16: [max_rows][2][2M] context vector of the step (pairs)
-    uint16_t* ybf;          // bf16: [B*H*W][2][M] y_hat as bf16 pairs (tap source)
+    uint16_t* ctxb;         // bf16: [max_rows][2M/32][2][32] context vector of the step (pairs)
+    uint16_t* ybf;          // bf16: [B*H*W][M/32][2][32] y_hat as bf16 pairs (tap source)
     int max_rows;
+    int slots;              // workgroups resident at once (jobs of one round)
     const CallPtrs* cp;
 };
 

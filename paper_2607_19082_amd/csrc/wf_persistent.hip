@@ -57,10 +57,12 @@ __device__ __forceinline__ bool grid_barrier(unsigned* ctr, unsigned k, int* err
     return *bail == 0;
 }
 
+// Two workgroups per CU (one hides the other's load latency): at most 256
+// registers per lane.
 template <class P, int KC>
-__global__ __launch_bounds__(kThreads) void k_persistent(StepArgs a, int T, unsigned* ctr, int* err,
+__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2))) void k_persistent(StepArgs a, int T, unsigned* ctr, int* err,
                                                     long long budget, Trace tr) {
-    __shared__ f4 red[kWaves][64];
+    __shared__ f4 red[kWaves * kMaxC][64];
     __shared__ L3Smem<KC> sm;
     __shared__ int bail;
     for (int l = threadIdx.x; l < a.L; l += blockDim.x) sm.tab[l] = a.table[l];
@@ -71,12 +73,18 @@ __global__ __launch_bounds__(kThreads) void k_persistent(StepArgs a, int T, unsi
     // old-tap context of step 0 (no old tap of step 0 lies in the grid, but
     // the general form keeps the loop uniform)
     {
-        const int nh = hoist_blocks(a);
+        const int nh = hoist_blocks<P>(a);
         for (int b = blockIdx.x; b < nh; b += G) hoist_job<P, true>(a, b, red);
         const StepRows s0 = step_rows(a.H, a.W, a.B, a.lambda, 0);
-        const int nc = ctxo_blocks(a, s0);
-        for (int b = blockIdx.x; b < kCtxParts * nc; b += G) ctxo_job<P, true>(a, s0, b, nc, red);
+        const int nc = ctxo_blocks<P>(a, s0);
+        // fp32: the last part adds the others, so it runs after them
+        const int split = P::kBf16 ? kCtxParts * nc : (kCtxParts - 1) * nc;
+        for (int b = blockIdx.x; b < split; b += G) ctxo_job<P, true>(a, s0, b, nc, red);
         if (!grid_barrier(ctr, ++k, err, budget, &bail, tr)) return;
+        if (!P::kBf16) {
+            for (int b = split + blockIdx.x; b < kCtxParts * nc; b += G) ctxo_job<P, true>(a, s0, b, nc, red);
+            if (!grid_barrier(ctr, ++k, err, budget, &bail, tr)) return;
+        }
     }
     for (int t = 0; t < T; ++t) {
         const StepRows s = step_rows(a.H, a.W, a.B, a.lambda, t);

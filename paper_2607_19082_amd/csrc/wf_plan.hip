@@ -57,6 +57,9 @@ static int round_up(int v, int m) { return (v + m - 1) / m * m; }
 static int round16(int v) { return round_up(v, kTile); }
 // k-block of the packed operands: 16 values of k for fp32, 32 for bf16
 static int kblock(int precision) { return precision == WF_BF16 ? 32 : 16; }
+// columns of one job's column group (kC tiles of 16): d1, d2 are padded to it
+static int colgroup(int precision) { return kTile * (precision == WF_BF16 ? kColsBf16 : kColsF32); }
+static int padded(int d, int precision) { return round_up(round_up(d, kblock(precision)), colgroup(precision)); }
 
 static int check_desc(const wf_desc* d) {
     if (!d) return fail(WF_E_INVALID, "desc is NULL");
@@ -89,7 +92,7 @@ static int check_desc(const wf_desc* d) {
     // every array the kernels read through raw buffer instructions (psi, y_hat,
     // the per-step activations) must fit the buffer window
     const long long lat = (long long)d->B * d->H * d->W;
-    if (lat * 2 * d->M * 4 >= kBufBytes || lat * round_up(d->d1, kblock(d->precision)) * 4 >= kBufBytes ||
+    if (lat * 2 * d->M * 4 >= kBufBytes || lat * padded(d->d1, d->precision) * 4 >= kBufBytes ||
         lat * 3 * d->M > (1LL << 31) - 1)
         return fail(WF_E_UNSUPPORTED, "problem too large for the 2 GiB buffer window");
     // a k-block of the tap gathers must not straddle two taps
@@ -97,12 +100,12 @@ static int check_desc(const wf_desc* d) {
     return WF_OK;
 }
 
-// Pack Wt[k][n] (k < K, n < N; zero beyond) into the MFMA operand order used
-// by the step kernels: for column tile ct and k-block kb (16 values of k),
-// lane l holds Wt[kb*16 + (l/16)*4 + q][ct*16 + l%16] for q = 0..3.
+// Pack Wt[k][n] (k < K, n < N; zero up to the padded sizes Kp, Np the
+// kernels use) into the MFMA operand order of the step kernels: for column
+// tile ct and k-block kb (16 values of k), lane l holds
+// Wt[kb*16 + (l/16)*4 + q][ct*16 + l%16] for q = 0..3.
 template <class F>
-static std::vector<float> pack_panel(int K, int N, F wt) {
-    const int Kp = round16(K), Np = round16(N);
+static std::vector<float> pack_panel(int K, int N, int Kp, int Np, F wt) {
     const int nkb = Kp / kTile;
     std::vector<float> out((size_t)Np * Kp, 0.0f);
     for (int ct = 0; ct < Np / kTile; ++ct)
@@ -126,11 +129,9 @@ static uint16_t bf16_round(float v) {
 }
 
 // The same for bf16 operands, k-blocks of 32: lane l holds
-// Wt[kb*32 + (l/16)*8 + q][ct*16 + l%16] for q = 0..7, rounded to bf16.  Np
-// (a multiple of 16, at least N) is the padded column count the kernels use.
+// Wt[kb*32 + (l/16)*8 + q][ct*16 + l%16] for q = 0..7, rounded to bf16.
 template <class F>
-static std::vector<uint16_t> pack_panel_bf16(int K, int N, int Np, F wt) {
-    const int Kp = round_up(K, 32);
+static std::vector<uint16_t> pack_panel_bf16(int K, int N, int Kp, int Np, F wt) {
     const int nkb = Kp / 32;
     std::vector<uint16_t> out((size_t)Np * Kp, 0);
     for (int ct = 0; ct < Np / kTile; ++ct)
@@ -216,8 +217,8 @@ static int build_plan(const wf_desc* d, Plan* p) {
     for (int t = 0; t < p->T; ++t) maxn = std::max(maxn, step_n[t]);
     p->max_rows = p->B * maxn;
     const bool bf = p->precision == WF_BF16;
-    p->Np1 = round_up(p->d1, kblock(p->precision));
-    p->Np2 = round_up(p->d2, kblock(p->precision));
+    p->Np1 = padded(p->d1, p->precision);
+    p->Np2 = padded(p->d2, p->precision);
     p->nph = bf ? 4 : 3;
     const int d1 = p->d1, Np1 = p->Np1;
 
@@ -282,12 +283,13 @@ static int build_plan(const wf_desc* d, Plan* p) {
         // bf16: the context bias stays in the context vector (it is rounded
         // with it); no fold.
         std::copy(d->b1, d->b1 + d1, b_hoist.begin());
-        if ((rc = put(&a.wp_hoist, Np1, 2 * M, pack_panel_bf16(2 * M, d1, Np1, w1a))) != WF_OK) return rc;
-        if ((rc = put(&a.wp_l1, Np1, 2 * M, pack_panel_bf16(2 * M, d1, Np1, w1b))) != WF_OK) return rc;
-        if ((rc = put(&a.wp_new, 2 * M, a.n_new * M, pack_panel_bf16(a.n_new * M, 2 * M, 2 * M, wc_of(new_taps)))) != WF_OK) return rc;
-        if ((rc = put(&a.wp_old, 2 * M, a.n_old * M, pack_panel_bf16(a.n_old * M, 2 * M, 2 * M, wc_of(old_taps)))) != WF_OK) return rc;
-        if ((rc = put(&a.wp2, p->Np2, Np1, pack_panel_bf16(d1, p->d2, p->Np2, w2f))) != WF_OK) return rc;
-        if ((rc = put(&a.wp3, p->n3, p->Np2, pack_panel_bf16(p->d2, p->n3, p->n3, w3f))) != WF_OK) return rc;
+        const int kn = a.n_new * M, ko = a.n_old * M, Np2 = p->Np2, n3 = p->n3;
+        if ((rc = put(&a.wp_hoist, Np1, 2 * M, pack_panel_bf16(2 * M, d1, 2 * M, Np1, w1a))) != WF_OK) return rc;
+        if ((rc = put(&a.wp_l1, Np1, 2 * M, pack_panel_bf16(2 * M, d1, 2 * M, Np1, w1b))) != WF_OK) return rc;
+        if ((rc = put(&a.wp_new, 2 * M, kn, pack_panel_bf16(kn, 2 * M, kn, 2 * M, wc_of(new_taps)))) != WF_OK) return rc;
+        if ((rc = put(&a.wp_old, 2 * M, ko, pack_panel_bf16(ko, 2 * M, ko, 2 * M, wc_of(old_taps)))) != WF_OK) return rc;
+        if ((rc = put(&a.wp2, Np2, Np1, pack_panel_bf16(d1, p->d2, Np1, Np2, w2f))) != WF_OK) return rc;
+        if ((rc = put(&a.wp3, n3, Np2, pack_panel_bf16(p->d2, n3, Np2, n3, w3f))) != WF_OK) return rc;
         if ((rc = upload(p, &f, d->ctx_b, (size_t)2 * M)) != WF_OK) return rc;
         a.bc = f;
     } else {
@@ -302,16 +304,17 @@ static int build_plan(const wf_desc* d, Plan* p) {
             b_hoist[n] = (float)acc;
         }
         const int knew = a.n_new * M;
-        if ((rc = put(&a.wp_hoist, Np1, 2 * M, pack_panel(2 * M, d1, w1a))) != WF_OK) return rc;
-        if ((rc = put(&a.wp_l1, Np1, knew + 2 * M, pack_panel(knew + 2 * M, d1, [&](int k, int n) {
+        const int ko = a.n_old * M, Np2 = p->Np2, n3 = p->n3;
+        if ((rc = put(&a.wp_hoist, Np1, 2 * M, pack_panel(2 * M, d1, 2 * M, Np1, w1a))) != WF_OK) return rc;
+        if ((rc = put(&a.wp_l1, Np1, knew + 2 * M, pack_panel(knew + 2 * M, d1, knew + 2 * M, Np1, [&](int k, int n) {
                  if (k < knew) return (float)fold[k / M][(size_t)(k % M) * d1 + n];
                  return w1b(k - knew, n);
              }))) != WF_OK)
             return rc;
         fold.clear();
-        if ((rc = put(&a.wp_old, 2 * M, a.n_old * M, pack_panel(a.n_old * M, 2 * M, wc_of(old_taps)))) != WF_OK) return rc;
-        if ((rc = put(&a.wp2, p->Np2, Np1, pack_panel(d1, p->d2, w2f))) != WF_OK) return rc;
-        if ((rc = put(&a.wp3, p->n3, p->Np2, pack_panel(p->d2, p->n3, w3f))) != WF_OK) return rc;
+        if ((rc = put(&a.wp_old, 2 * M, ko, pack_panel(ko, 2 * M, ko, 2 * M, wc_of(old_taps)))) != WF_OK) return rc;
+        if ((rc = put(&a.wp2, Np2, Np1, pack_panel(d1, p->d2, Np1, Np2, w2f))) != WF_OK) return rc;
+        if ((rc = put(&a.wp3, n3, Np2, pack_panel(p->d2, n3, Np2, n3, w3f))) != WF_OK) return rc;
     }
     std::vector<float> b2(p->Np2, 0.0f);
     std::copy(d->b2, d->b2 + p->d2, b2.begin());
@@ -342,8 +345,11 @@ static int build_plan(const wf_desc* d, Plan* p) {
     a.cp = p->d_call;
     if ((rc = alloc(p, &p->d_err, 1)) != WF_OK) return rc;
     WF_HIP(hipMemset(p->d_err, 0, sizeof(int)));
+    // one round of jobs: the persistent grid (two workgroups per CU); the
+    // per-step kernels have the same residency
+    if ((rc = persistent_grid(*p, &a.slots)) != WF_OK) return rc;
     if (p->driver == WF_DRIVER_PERSISTENT) {
-        if ((rc = persistent_grid(*p, &p->grid)) != WF_OK) return rc;
+        p->grid = a.slots;
         if ((rc = alloc(p, &p->d_bar, kBarrierWords)) != WF_OK) return rc;
         WF_HIP(hipMemset(p->d_bar, 0, kBarrierWords * sizeof(unsigned)));
     }
@@ -476,7 +482,9 @@ int wf_plan_trace(wf_plan_t plan, int64_t* stamps, int64_t capacity, int64_t* ne
     if (stamps && capacity < 0) return fail(WF_E_INVALID, "negative capacity");
     p->stamps = reinterpret_cast<long long*>(stamps);
     p->stamps_cap = stamps ? capacity : 0;
-    if (needed) *needed = (int64_t)(1 + p->nph * (int64_t)p->T) * (p->grid + 1);
+    // barriers: the prologue (two with fp32) and one per phase of every step
+    const int64_t pro = p->precision == WF_BF16 ? 1 : 2;
+    if (needed) *needed = (int64_t)(pro + p->nph * (int64_t)p->T) * (p->grid + 1);
     if (grid) *grid = p->grid;
     return WF_OK;
 }

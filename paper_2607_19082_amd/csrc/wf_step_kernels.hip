@@ -7,15 +7,15 @@ namespace wf {
 // Pre-loop: the hyperprior half of layer 1 for every latent.
 template <class P>
 __global__ __launch_bounds__(kThreads) void k_hoist(StepArgs a) {
-    __shared__ f4 red[kWaves][64];
+    __shared__ f4 red[kWaves * kMaxC][64];
     hoist_job<P, false>(a, blockIdx.x, red);
 }
 
-// Old-tap context jobs of step s1 only (before the first step).
+// Old-tap context jobs [j0, ...) of step s1 only (before the first step).
 template <class P>
-__global__ __launch_bounds__(kThreads) void k_ctxo(StepRows s1, int nc, StepArgs a) {
-    __shared__ f4 red[kWaves][64];
-    ctxo_job<P, false>(a, s1, blockIdx.x, nc, red);
+__global__ __launch_bounds__(kThreads) void k_ctxo(StepRows s1, int j0, int nc, StepArgs a) {
+    __shared__ f4 red[kWaves * kMaxC][64];
+    ctxo_job<P, false>(a, s1, j0 + blockIdx.x, nc, red);
 }
 
 // Phase ph of step s (blocks [0, nb)), then old-tap context jobs [j0, ...)
@@ -23,7 +23,7 @@ __global__ __launch_bounds__(kThreads) void k_ctxo(StepRows s1, int nc, StepArgs
 template <class P, int KC>
 __global__ __launch_bounds__(kThreads) void k_phase(int ph, StepRows s, StepRows s1, int nb, int j0, int nc,
                                                     StepArgs a) {
-    __shared__ f4 red[kWaves][64];
+    __shared__ f4 red[kWaves * kMaxC][64];
     __shared__ L3Smem<KC> sm;
     if ((int)blockIdx.x >= nb) {
         ctxo_job<P, false>(a, s1, j0 + blockIdx.x - nb, nc, red);
@@ -47,7 +47,7 @@ int enqueue_set_call(Plan& p, const CallPtrs& c, hipStream_t stream) {
 
 template <class P>
 static void launch_hoist(Plan& p, hipStream_t stream) {
-    hipLaunchKernelGGL(k_hoist<P>, dim3(hoist_blocks(p.args)), dim3(kThreads), 0, stream, p.args);
+    hipLaunchKernelGGL(k_hoist<P>, dim3(hoist_blocks<P>(p.args)), dim3(kThreads), 0, stream, p.args);
 }
 
 int enqueue_hoist(Plan& p, hipStream_t stream) {
@@ -70,8 +70,15 @@ static void launch_steps(Plan& p, hipStream_t stream) {
     launch_hoist<P>(p, stream);
     {
         const StepRows s0 = rows_of(p, 0);
-        const int nc = ctxo_blocks(a, s0);
-        if (nc > 0) hipLaunchKernelGGL(k_ctxo<P>, dim3(kCtxParts * nc), dim3(kThreads), 0, stream, s0, nc, a);
+        const int nc = ctxo_blocks<P>(a, s0);
+        // fp32: the last part adds the others, so it runs after them
+        const int split = P::kBf16 ? kCtxParts * nc : (kCtxParts - 1) * nc;
+        if (nc > 0) {
+            hipLaunchKernelGGL(k_ctxo<P>, dim3(split), dim3(kThreads), 0, stream, s0, 0, nc, a);
+            if (split < kCtxParts * nc)
+                hipLaunchKernelGGL(k_ctxo<P>, dim3(kCtxParts * nc - split), dim3(kThreads), 0, stream, s0, split, nc,
+                                   a);
+        }
     }
     for (int t = 0; t < p.T; ++t) {
         const StepRows s = rows_of(p, t), s1 = rows_of(p, t + 1);
