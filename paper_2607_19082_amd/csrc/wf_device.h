@@ -18,8 +18,7 @@
 //   phase A  h1  = pair(lrelu(P1 + W1b . ctx)),  P1 = b1 + W1[:, :2M] . pair(psi)
 //   phase B  h2  = pair(lrelu(W2 . h1 + b2))
 //   phase C  as above; also keeps the pair form of y_hat for the tap gathers.
-// A pair array holds each row of n values as n/32 blocks of [32 hi | 32 lo]
-// (one 128-byte line per k-block: an operand's two loads share a line).
+// Pair arrays: see tile_idx and st_pair_row.
 // In both, the kCtxParts k-parts of ctx_old(t+1) ride along with the phases
 // of step t, spread to even out their work (see ctxo_split).
 //
@@ -91,7 +90,7 @@ struct PBF16 {
     static constexpr bool kBf16 = true;
     static constexpr int kFirst = PH_N;
     static constexpr int kC = kColsBf16;
-    static constexpr int kKbw = 6;
+    static constexpr int kKbw = 10;
     static constexpr int kL3Kbw1 = 8, kL3Kbw3 = 3;
     __device__ static __forceinline__ f4 mma(A a, B b, f4 acc) {
         acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a.hi, b, acc, 0, 0, 0);
@@ -181,36 +180,55 @@ __device__ __forceinline__ void st1h(uint16_t* base, size_t idx, uint16_t h) {
         base[idx] = h;
 }
 
-// Activation arrays: fp32 rows of n values, or bf16 pair rows of 2n values
-// (per k-block of 32 values: 32 hi then 32 lo).  act_row is the first
-// element of row r.
+// The per-step activation arrays (h1, h2, the bf16 context vector and the
+// fp32 old-tap context parts) are kept in MFMA operand order: for 16-row tile
+// rt and k-block kb of rows of n values, the 64 lanes' 16-byte A operands lie
+// next to each other (fp32: 1 KB per block; bf16 pairs: 1 KB of hi halves,
+// then 1 KB of lo halves), so every A load is one contiguous 1 KB.  tile_idx
+// is the element index of (row r, column c) (bf16: of its hi half; the lo
+// half is 512 elements further).
 template <class P>
-__device__ __forceinline__ size_t act_row(size_t r, int n) {
-    return r * (size_t)n * (P::kBf16 ? 2 : 1);
+__device__ __forceinline__ size_t tile_idx(int r, int c, int n) {
+    if constexpr (P::kBf16)
+        return ((size_t)(r >> 4) * (n >> 5) + (c >> 5)) * 1024 + (((c & 31) >> 3) * 16 + (r & 15)) * 8 + (c & 7);
+    else
+        return ((size_t)(r >> 4) * (n >> 4) + (c >> 4)) * 256 + (((c & 15) >> 2) * 16 + (r & 15)) * 4 + (c & 3);
 }
-// A operand of k-block kb of the row starting at element `row` (n values).
+// A operand of k-block kb of row tile rt.
 template <class P, bool COH>
-__device__ __forceinline__ typename P::A ld_act(const void* base, size_t row, int n, int kb, int kq, bool ok) {
+__device__ __forceinline__ typename P::A ld_tile(const void* base, int rt, int n, int kb, bool ok) {
+    const int lane = threadIdx.x & 63;
     if constexpr (P::kBf16) {
         const uint16_t* h = static_cast<const uint16_t*>(base);
-        const size_t q = row + (size_t)kb * 64 + kq * 8;
-        return b8x2{ld8h<COH>(h, q, ok), ld8h<COH>(h, q + 32, ok)};
+        const size_t q = ((size_t)rt * (n >> 5) + kb) * 1024 + lane * 8;
+        return b8x2{ld8h<COH>(h, q, ok), ld8h<COH>(h, q + 512, ok)};
     } else {
-        return ld4<COH>(static_cast<const float*>(base), row + (size_t)kb * 16 + kq * 4, ok);
+        return ld4<COH>(static_cast<const float*>(base), ((size_t)rt * (n >> 4) + kb) * 256 + lane * 4, ok);
     }
 }
-// Store value v of column col of the row starting at element `row`.
+// Store value v of element (r, c).
 template <class P, bool COH>
-__device__ __forceinline__ void st_act(void* base, size_t row, int n, int col, float v) {
+__device__ __forceinline__ void st_tile(void* base, int r, int n, int c, float v) {
+    const size_t q = tile_idx<P>(r, c, n);
     if constexpr (P::kBf16) {
         uint16_t* h = static_cast<uint16_t*>(base);
         const uint16_t hi = bf16_bits(v);
-        const size_t q = row + (size_t)(col >> 5) * 64 + (col & 31);
         st1h<COH>(h, q, hi);
-        st1h<COH>(h, q + 32, bf16_bits(v - bf16_value(hi)));
+        st1h<COH>(h, q + 512, bf16_bits(v - bf16_value(hi)));
     } else {
-        st1<COH>(static_cast<float*>(base), row + col, v);
+        st1<COH>(static_cast<float*>(base), q, v);
     }
+}
+
+// The bf16 pair copy of y_hat (the tap source) keeps one row of M values per
+// latent, as n/32 blocks of [32 hi | 32 lo] (an operand's two loads share a
+// 128-byte line); store value v of channel c of the row starting at `row`.
+template <bool COH>
+__device__ __forceinline__ void st_pair_row(uint16_t* h, size_t row, int c, float v) {
+    const uint16_t hi = bf16_bits(v);
+    const size_t q = row + (size_t)(c >> 5) * 64 + (c & 31);
+    st1h<COH>(h, q, hi);
+    st1h<COH>(h, q + 32, bf16_bits(v - bf16_value(hi)));
 }
 
 // Rows of one step: B images x n latents; row r is image r / n, grid row
@@ -307,8 +325,9 @@ __host__ __device__ __forceinline__ int ctxo_blocks(const StepArgs& a, const Ste
 // kCtxParts * nc old-tap context jobs of the next step ride along with it:
 // phase ph takes jobs [cut[ph], cut[ph + 1]) (part-major: job j is part
 // j / nc).  A phase lasts as long as its busiest workgroup, so the context
-// jobs first fill the slots left free in the last round of each phase's own
-// jobs (a.slots workgroups run at once); only what is left adds rounds,
+// jobs are shared evenly among the phases as far as the slots left free in
+// the last round of each phase's own jobs allow (a.slots workgroups run at
+// once), then fill the remaining free slots; only what is left adds rounds,
 // spread evenly over the phases.  With fp32 the last part's jobs all run in
 // the last phase, after the other parts, and add them in (see ctxo_job).
 // Cuts are multiples of 8, which keeps every job on the XCD its column tile
@@ -335,14 +354,24 @@ __host__ __device__ __forceinline__ StepWork step_work(const StepArgs& a, const 
     w.nc = ctxo_blocks<P>(a, s1);
     const int G = a.slots;
     int left = (P::kBf16 ? kCtxParts : kCtxParts - 1) * w.nc;
-    int take[kMaxPhases];
+    // an even share per phase first (less contention), within free slots
+    const int share = ((left + nph - 1) / nph + kXcds - 1) / kXcds * kXcds;
+    int take[kMaxPhases], free_slots[kMaxPhases];
 #pragma unroll
     for (int ph = 0; ph < kMaxPhases; ++ph) {
         w.nb[ph] = ph < P::kFirst ? 0 : phase_blocks<P>(a, s, ph);
         const int nb = w.nb[ph];
-        const int free_slots = nb > 0 ? ((nb + G - 1) / G * G - nb) / kXcds * kXcds : 0;
-        take[ph] = ph < P::kFirst || ph >= last ? 0 : (left < free_slots ? left : free_slots);
+        free_slots[ph] = ph < P::kFirst || ph >= last || nb == 0 ? 0 : ((nb + G - 1) / G * G - nb) / kXcds * kXcds;
+        int t = left < share ? left : share;
+        take[ph] = t < free_slots[ph] ? t : free_slots[ph];
+        free_slots[ph] -= take[ph];
         left -= take[ph];
+    }
+#pragma unroll
+    for (int ph = 0; ph < kMaxPhases; ++ph) {
+        const int t = left < free_slots[ph] ? left : free_slots[ph];
+        take[ph] += t;
+        left -= t;
     }
     const int extra = ((left + nph - 1) / nph + kXcds - 1) / kXcds * kXcds;
     w.cut[0] = 0;
@@ -520,15 +549,15 @@ __device__ __forceinline__ void ctxo_job(const StepArgs& a, const StepRows& s, i
     // double-buffered by step parity: jobs for step s.t may run while the
     // context of step s.t - 1 is still being read from the other half
     const size_t cpart = (size_t)a.max_rows * 2 * M;
-    const size_t q = (size_t)(s.t & 1) * kCtxParts * cpart + (size_t)ro * 2 * M;
+    const size_t q = (size_t)(s.t & 1) * kCtxParts * cpart;
     float prev[C], v[C];
 #pragma unroll
     for (int c = 0; c < C; ++c) {
         prev[c] = 0.0f;
         if (!P::kBf16 && part == kCtxParts - 1) {
+            const size_t e = q + tile_idx<PF32>(ro, group_col<P>(jb.ct, c), 2 * M);
 #pragma unroll
-            for (int p2 = 0; p2 < kCtxParts - 1; ++p2)
-                prev[c] += ld1<COH>(a.ctxo, q + p2 * cpart + group_col<P>(jb.ct, c), vo);
+            for (int p2 = 0; p2 < kCtxParts - 1; ++p2) prev[c] += ld1<COH>(a.ctxo, e + p2 * cpart, vo);
         }
     }
     const Row w = step_row(a, s, jb.rt * kTile + (lane & 15));
@@ -538,7 +567,8 @@ __device__ __forceinline__ void ctxo_job(const StepArgs& a, const StepRows& s, i
     block_tiles<P>(red, a.wp_old, nkb, jb.ct, la, v, klo, khi);
     if (vo) {
 #pragma unroll
-        for (int c = 0; c < C; ++c) st1<COH>(a.ctxo, q + part * cpart + group_col<P>(jb.ct, c), v[c] + prev[c]);
+        for (int c = 0; c < C; ++c)
+            st1<COH>(a.ctxo, q + part * cpart + tile_idx<PF32>(ro, group_col<P>(jb.ct, c), 2 * M), v[c] + prev[c]);
     }
 }
 
@@ -561,15 +591,15 @@ __device__ __forceinline__ void l1_fold_job(const StepArgs& a, const StepRows& s
     const int knew = a.n_new * M;
     const size_t cpart = (size_t)a.max_rows * 2 * M;
     // the old-tap context: the last part's slot holds the whole sum
-    const size_t cbase = ((size_t)(s.t & 1) * kCtxParts + kCtxParts - 1) * cpart + (size_t)r * 2 * M + kq * 4;
+    const float* ctx = a.ctxo + ((size_t)(s.t & 1) * kCtxParts + kCtxParts - 1) * cpart;
+    const int kbn = knew / kTile;
     auto la_new = [&](int kb) { return ld_tap<PF32, COH>(a, w, kb, kq, false); };
-    auto la_ctx = [&](int kb) -> f4 { return ld4<COH>(a.ctxo, cbase + (kb * kTile - knew), w.valid); };
+    auto la_ctx = [&](int kb) -> f4 { return ld_tile<PF32, COH>(ctx, jb.rt, 2 * M, kb - kbn, w.valid); };
     block_tiles2<PF32>(red, a.wp_l1, (knew + 2 * M) / kTile, jb.ct, knew / kTile, la_new, la_ctx, acc);
     if (v.valid) {
 #pragma unroll
         for (int c = 0; c < C; ++c)
-            st1<COH>(static_cast<float*>(a.h1), (size_t)ro * a.Np1 + group_col<PF32>(jb.ct, c),
-                     lrelu(acc[c] + z[c], a.slope));
+            st_tile<PF32, COH>(a.h1, ro, a.Np1, group_col<PF32>(jb.ct, c), lrelu(acc[c] + z[c], a.slope));
     }
 }
 
@@ -585,15 +615,15 @@ __device__ __forceinline__ void ctxn_job(const StepArgs& a, const StepRows& s, i
     const int ro = wave < 4 ? jb.rt * kTile + kq * 4 + wave : s.nrows;
     const bool vo = ro < s.nrows;
     const size_t cpart = (size_t)a.max_rows * 2 * M;
-    const size_t cq = (size_t)(s.t & 1) * kCtxParts * cpart + (size_t)ro * 2 * M;
+    const size_t cq = (size_t)(s.t & 1) * kCtxParts * cpart;
     float z[C], acc[C];
 #pragma unroll
     for (int c = 0; c < C; ++c) {
         const int n = group_col<PBF16>(jb.ct, c);
+        const size_t e = cq + tile_idx<PF32>(ro, n, 2 * M);
         z[c] = a.bc[n];
 #pragma unroll
-        for (int part = 0; part < kCtxParts; ++part)
-            z[c] += ld1<COH>(a.ctxo, cq + part * cpart + n, vo && a.n_old > 0);
+        for (int part = 0; part < kCtxParts; ++part) z[c] += ld1<COH>(a.ctxo, e + part * cpart, vo && a.n_old > 0);
     }
     const Row w = step_row(a, s, jb.rt * kTile + (lane & 15));
     auto la = [&](int kb) { return ld_tap<PBF16, COH>(a, w, kb, kq, false); };
@@ -601,7 +631,7 @@ __device__ __forceinline__ void ctxn_job(const StepArgs& a, const StepRows& s, i
     if (vo) {
 #pragma unroll
         for (int c = 0; c < C; ++c)
-            st_act<PBF16, COH>(a.ctxb, act_row<PBF16>(ro, 2 * M), 2 * M, group_col<PBF16>(jb.ct, c), acc[c] + z[c]);
+            st_tile<PBF16, COH>(a.ctxb, ro, 2 * M, group_col<PBF16>(jb.ct, c), acc[c] + z[c]);
     }
 }
 
@@ -620,14 +650,12 @@ __device__ __forceinline__ void l1_ctx_job(const StepArgs& a, const StepRows& s,
     for (int c = 0; c < C; ++c) z[c] = ld1<COH>(a.p1, v.lat * a.Np1 + group_col<PBF16>(jb.ct, c), v.valid);
     const int r = jb.rt * kTile + (lane & 15);
     const bool valid = r < s.nrows;
-    const size_t row = act_row<PBF16>(r, 2 * M);
-    auto la = [&](int kb) { return ld_act<PBF16, COH>(a.ctxb, row, 2 * M, kb, kq, valid); };
+    auto la = [&](int kb) { return ld_tile<PBF16, COH>(a.ctxb, jb.rt, 2 * M, kb, valid); };
     block_tiles<PBF16>(red, a.wp_l1, 2 * M / PBF16::kK, jb.ct, la, acc);
     if (v.valid) {
 #pragma unroll
         for (int c = 0; c < C; ++c)
-            st_act<PBF16, COH>(a.h1, act_row<PBF16>(ro, a.Np1), a.Np1, group_col<PBF16>(jb.ct, c),
-                               lrelu(acc[c] + z[c], a.slope));
+            st_tile<PBF16, COH>(a.h1, ro, a.Np1, group_col<PBF16>(jb.ct, c), lrelu(acc[c] + z[c], a.slope));
     }
 }
 
@@ -643,15 +671,13 @@ __device__ __forceinline__ void l2_job(const StepArgs& a, const StepRows& s, int
     for (int c = 0; c < C; ++c) bias[c] = a.b2[group_col<P>(jb.ct, c)];
     const int r = jb.rt * kTile + (lane & 15);
     const bool valid = r < s.nrows;
-    const size_t row = act_row<P>(r, a.Np1);
-    auto la = [&](int kb) { return ld_act<P, COH>(a.h1, row, a.Np1, kb, kq, valid); };
+    auto la = [&](int kb) { return ld_tile<P, COH>(a.h1, jb.rt, a.Np1, kb, valid); };
     block_tiles<P>(red, a.wp2, a.Np1 / P::kK, jb.ct, la, acc);
     const int ro = jb.rt * kTile + kq * 4 + wave;
     if (wave < 4 && ro < s.nrows) {
 #pragma unroll
         for (int c = 0; c < C; ++c)
-            st_act<P, COH>(a.h2, act_row<P>(ro, a.Np2), a.Np2, group_col<P>(jb.ct, c),
-                           lrelu(acc[c] + bias[c], a.slope));
+            st_tile<P, COH>(a.h2, ro, a.Np2, group_col<P>(jb.ct, c), lrelu(acc[c] + bias[c], a.slope));
     }
 }
 
@@ -715,7 +741,6 @@ __device__ __forceinline__ void l3_job(const StepArgs& a, const StepRows& s, int
     const int kb0 = min(nkb, wave * per), kb1 = min(nkb, kb0 + per);
     const int r = rt * kTile + (lane & 15);
     const bool valid = r < s.nrows;
-    const size_t hrow = act_row<P>(r, a.Np2);
     const Bw* __restrict__ wv = static_cast<const Bw*>(a.wp3) + lane;
     const int NT = vg == 0 ? NT0 : NT1;
     int cols[NTM];
@@ -730,7 +755,7 @@ __device__ __forceinline__ void l3_job(const StepArgs& a, const StepRows& s, int
 #pragma unroll
         for (int u = 0; u < KBW; ++u) {
             const int k = min(kc + u, kb1 - 1);
-            av[u] = ld_act<P, COH>(a.h2, hrow, a.Np2, k, kq, valid);
+            av[u] = ld_tile<P, COH>(a.h2, rt, a.Np2, k, valid);
 #pragma unroll
             for (int t = 0; t < NTM; ++t) bv[u][t] = wv[((size_t)cols[t] * nkb + k) * 64];
         }
@@ -798,7 +823,7 @@ __device__ __forceinline__ void l3_job(const StepArgs& a, const StepRows& s, int
     }
     cp->mean[oq] = mu;
     st1<COH>(cp->y_hat, oq, sv + mu);
-    if constexpr (P::kBf16) st_act<P, COH>(a.ybf, act_row<P>(lat, M), M, c, sv + mu);
+    if constexpr (P::kBf16) st_pair_row<COH>(a.ybf, lat * 2 * M, c, sv + mu);
 }
 
 // The main job of phase ph (sm.tab must hold the scale table for PH_C).

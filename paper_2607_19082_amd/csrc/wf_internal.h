@@ -14,8 +14,8 @@ namespace wf {
 constexpr int kMaxTaps = 12;
 constexpr int kMaxNew = 2;           // taps written by the immediately preceding step
 constexpr int kTile = 16;            // MFMA tile edge (rows and columns)
-constexpr int kColsF32 = 2;          // column tiles of one job, fp32 operands
-constexpr int kColsBf16 = 4;         // the same, bf16 operands
+constexpr int kColsF32 = 1;          // column tiles of one job, fp32 operands
+constexpr int kColsBf16 = 2;         // the same, bf16 operands
 constexpr int kMaxTable = 256;
 constexpr int kXcds = 8;             // accelerator complex dies of an MI355X
 constexpr int kBarrierWords = 512;   // barrier counters of the persistent driver
@@ -80,12 +80,13 @@ struct StepArgs {
     const float* b3;        // [n3]
     const float* table;     // [L]
     float* p1;              // [B*H*W][Np1] hoisted layer-1 part
-    void* h1;               // [max_rows][Np1]  fp32, or bf16 pairs [max_rows][Np1/32][2][32]
-    void* h2;               // [max_rows][Np2]  fp32, or bf16 pairs [max_rows][Np2/32][2][32]
-    float* ctxo;            // [2][3][max_rows][2M] old-tap context k-parts, by step parity
-    uint16_t* ctxb;         // bf16: [max_rows][2M/32][2][32] context vector of the step (pairs)
+    // per-step activations, max_rows x n in MFMA operand order (tile_idx):
+    void* h1;               // n = Np1, fp32 or bf16 pairs
+    void* h2;               // n = Np2, fp32 or bf16 pairs
+    float* ctxo;            // [2][3] x (n = 2M) old-tap context k-parts, by step parity
+    uint16_t* ctxb;         // bf16: n = 2M, the context vector of the step (pairs)
     uint16_t* ybf;          // bf16: [B*H*W][M/32][2][32] y_hat as bf16 pairs (tap source)
-    int max_rows;
+    int max_rows;           // rows of the widest step, rounded up to 16
     int slots;              // workgroups resident at once (jobs of one round)
     const CallPtrs* cp;
 };

@@ -215,7 +215,7 @@ static int build_plan(const wf_desc* d, Plan* p) {
         }
     int maxn = 0;
     for (int t = 0; t < p->T; ++t) maxn = std::max(maxn, step_n[t]);
-    p->max_rows = p->B * maxn;
+    p->max_rows = round16(p->B * maxn);   // whole 16-row tiles (tiled activation arrays)
     const bool bf = p->precision == WF_BF16;
     p->Np1 = padded(p->d1, p->precision);
     p->Np2 = padded(p->d2, p->precision);
