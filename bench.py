@@ -7,14 +7,23 @@ y_hat write, plus the pre-loop hyperprior product.  Inputs are seeded
 synthetic arrays (weights N(0, 1/fan_in), hyperprior params N(0, 1), Laplace
 symbols) already resident in HBM.  Prints one JSON line.
 
-roofline: with the persistent driver one decode is one kernel launch
-(k_persistent; two tiny set-up kernels ride along, < 0.1% of the time), timed
-with HIP events on the launch stream; achieved = algorithmic FLOPs of a decode
-/ that time, against the dense fp32 (or bf16) MFMA peak.  latency_roofline
-adds the dependency floor: T_roof = hoist / peak + sum over steps of
-max(F_t / peak, L_floor), with L_floor the measured minimal dependent hop.
+roofline: one decode is one launch of the plan's HIP graph (graph driver: the
+hoist, two context kernels and one kernel per phase of every step) or of
+k_persistent (persistent driver), timed with HIP events on the launch stream;
+achieved = algorithmic FLOPs of a decode / that time, against the dense fp32
+(or bf16) MFMA peak.  traffic = HBM bytes of one decode from the committed
+rocprofv3 FETCH_SIZE / WRITE_SIZE summary for this workload, precision and
+driver, scaled by the counters' reading for a plain copy of known size; null
+when no summary exists or the kernel sources changed since it was taken.
+latency_roofline adds the dependency floor: T_roof = hoist / peak + sum over
+steps of max(F_t / peak, L_floor), with L_floor the measured minimal
+dependent hop.
+
+--summarize-traffic writes such a summary from rocprofv3 --pmc outputs.
 """
 import argparse
+import glob
+import hashlib
 import json
 import os
 import platform
@@ -28,6 +37,72 @@ sys.path.insert(0, ROOT)
 
 PEAK_TFLOPS = {"fp32": 157.3, "bf16": 2500.0}
 DEFAULT_WORKLOAD = "minnen-hr-4k-240x135-m320"
+CSRC = os.path.join(ROOT, "paper_2607_19082_amd", "csrc")
+PROFILES = os.path.join(ROOT, "profiles")
+# kernels of one decode call (the rest of a bench run: the floor probes, torch)
+DECODE_KERNELS = ("wf::k_phase", "wf::k_hoist", "wf::k_ctxo", "wf::k_set_call", "wf::k_persistent", "wf::k_zero_u32")
+
+
+def source_hash():
+    """sha256 over the kernel sources: counters taken on other sources are stale."""
+    h = hashlib.sha256()
+    for f in sorted(glob.glob(os.path.join(CSRC, "*.h")) + glob.glob(os.path.join(CSRC, "*.hip"))):
+        h.update(os.path.basename(f).encode())
+        with open(f, "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()
+
+
+def traffic_file(workload, precision, driver):
+    return os.path.join(PROFILES, f"traffic_{workload}_{precision}_{driver}.md")
+
+
+def read_traffic(workload, precision, driver):
+    """HBM bytes of one decode from the committed counter summary, or None."""
+    path = traffic_file(workload, precision, driver)
+    if not os.path.exists(path):
+        return None
+    vals = {}
+    with open(path) as f:
+        for line in f:
+            if line.startswith("- ") and ": " in line:
+                k, v = line[2:].strip().split(": ", 1)
+                vals[k] = v.strip("`")
+    if vals.get("source_sha256") != source_hash():
+        return None
+    return float(vals["hbm_bytes_per_decode"])
+
+
+def _pmc_rows(d):
+    import sqlite3
+    db = glob.glob(os.path.join(d, "**", "*results.db"), recursive=True)[0]
+    con = sqlite3.connect(db)
+    return list(con.execute("select kernel_name, counter_name, value from counters_collection"))
+
+
+def summarize_traffic(fetch_dir, write_dir, cal_fetch_dir, cal_write_dir, cal_bytes, out, command):
+    """Per-decode HBM bytes from rocprofv3 --pmc FETCH_SIZE / WRITE_SIZE runs
+    (KiB per dispatch), each scaled by the same counter's reading for a plain
+    copy of cal_bytes bytes."""
+    def total(d, cname, pred):
+        return sum(v for k, c, v in _pmc_rows(d) if c == cname and pred(k))
+    is_copy = lambda k: "copyBuffer" in k or "copy" in k.lower()
+    f_cal = cal_bytes / (1024.0 * total(cal_fetch_dir, "FETCH_SIZE", is_copy))
+    w_cal = cal_bytes / (1024.0 * total(cal_write_dir, "WRITE_SIZE", is_copy))
+    is_dec = lambda k: any(x in k for x in DECODE_KERNELS)
+    decodes = sum(1 for k, c, v in _pmc_rows(fetch_dir) if c == "FETCH_SIZE" and "k_set_call" in k)
+    fetch = total(fetch_dir, "FETCH_SIZE", is_dec) * 1024.0 * f_cal / decodes
+    write = total(write_dir, "WRITE_SIZE", is_dec) * 1024.0 * w_cal / decodes
+    with open(out, "w") as f:
+        f.write("# HBM traffic of one decode (rocprofv3 counters)\n\n")
+        f.write("FETCH_SIZE and WRITE_SIZE summed over the dispatches of the decode call(s), per decode,\n")
+        f.write("each scaled by the counter's reading for a plain device copy of a known size.\n\n")
+        f.write(f"- decodes_profiled: {decodes}\n- fetch_scale: {f_cal:.4f}\n- write_scale: {w_cal:.4f}\n")
+        f.write(f"- fetch_bytes_per_decode: {fetch:.0f}\n- write_bytes_per_decode: {write:.0f}\n")
+        f.write(f"- hbm_bytes_per_decode: {fetch + write:.0f}\n- source_sha256: `{source_hash()}`\n\n")
+        f.write("Commands:\n\n```\n" + command + "\n```\n")
+    print(json.dumps({"fetch_scale": f_cal, "write_scale": w_cal, "fetch": fetch, "write": write,
+                      "decodes": decodes}))
 
 
 def flops_per_latent(cfg):
@@ -103,11 +178,19 @@ def main():
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--workload", default=DEFAULT_WORKLOAD)
-    ap.add_argument("--driver", default="persistent", choices=["stream", "graph", "persistent"])
+    ap.add_argument("--driver", default="graph", choices=["stream", "graph", "persistent"])
     ap.add_argument("--precision", default="fp32", choices=["fp32", "bf16"])
     ap.add_argument("--cpu-rows", type=int, default=8, help="grid rows of the CPU-oracle sample (0: skip)")
     ap.add_argument("--no-encode", action="store_true")
+    ap.add_argument("--summarize-traffic", nargs=4, metavar=("FETCH_DIR", "WRITE_DIR", "CAL_FETCH_DIR", "CAL_WRITE_DIR"),
+                    help="write the traffic summary of this workload/precision/driver from rocprofv3 outputs")
+    ap.add_argument("--cal-bytes", type=float, default=float(1 << 30))
+    ap.add_argument("--command", default="", help="the commands that made the counter outputs (recorded)")
     args = ap.parse_args()
+    if args.summarize_traffic:
+        summarize_traffic(*args.summarize_traffic, args.cal_bytes,
+                          traffic_file(args.workload, args.precision, args.driver), args.command)
+        return
     if args.gpus != 1:
         print(json.dumps({"error": "this build runs on one GPU only (--gpus 1); a multi-GPU run is not "
                                    "part of it"}))
@@ -164,6 +247,7 @@ def main():
     peak = PEAK_TFLOPS[args.precision]
     achieved = fl / (dec_ms * 1e-3) / 1e12
     rows = step_rows(cfg)
+    traffic = read_traffic(args.workload, args.precision, args.driver)
     lfloor = min(x for x in (node_us, bar_us) if x > 0)
     f_step = rows * (flops_per_latent(cfg) - hoistable_flops_per_latent(cfg))
     t_roof_s = (hoistable_flops_per_latent(cfg) * lat) / (peak * 1e12) + np.maximum(
@@ -187,9 +271,12 @@ def main():
                    "steps_T": T, "driver": args.driver, "precision": args.precision,
                    "parallelism": "single GPU"},
         "roofline": {"bound": "mfma", "achieved": achieved, "peak": peak, "unit": "TFLOP/s",
-                     "frac": achieved / peak, "traffic": None,
-                     "kernel": "k_persistent (one launch = one decode)" if args.driver == "persistent"
-                     else "whole decode (all step kernels of one call)",
+                     "frac": achieved / peak, "traffic": traffic,
+                     "traffic_unit": "HBM bytes per launch (one decode)",
+                     "traffic_GBps": None if traffic is None else traffic / (dec_ms * 1e-3) / 1e9,
+                     "kernel": {"persistent": "k_persistent (one launch = one decode)",
+                                "graph": "one replay of the decode graph (hoist, context, one k_phase per phase)",
+                                "stream": "all kernels of one decode call"}[args.driver],
                      "algorithmic_gflop_per_launch": fl / 1e9, "launch_ms_events": dec_ms,
                      "mfma_floor_ms": fl / (peak * 1e12) * 1e3},
         "latency_roofline": {"L_floor_us": lfloor, "graph_node_us": node_us, "barrier_round_us": bar_us,
