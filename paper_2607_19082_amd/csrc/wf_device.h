@@ -19,7 +19,7 @@
 //   phase B  h2  = pair(lrelu(W2 . h1 + b2))
 //   phase C  as above; also keeps the pair form of y_hat for the tap gathers.
 // Pair arrays: see tile_idx and st_pair_row.
-// In both, the kCtxParts k-parts of ctx_old(t+1) ride along with the phases
+// In both, the k-parts (P::kParts) of ctx_old(t+1) ride along with the phases
 // of step t, spread to even out their work (see ctxo_split).
 //
 // Every product runs on MFMA: fp32 v_mfma_f32_16x16x4f32 (four chained per
@@ -47,7 +47,6 @@ struct b8x2 {   // eight activation values as bf16 pairs
 
 constexpr int kWaves = 4;              // waves per workgroup; they split a tile's k-blocks
 constexpr int kThreads = 64 * kWaves;
-constexpr int kCtxParts = 3;  // k-parts of the old-tap context product
 constexpr int kSc1 = 16;   // cache-policy bits of an agent-coherent buffer access
 constexpr int kMaxPhases = 4;
 constexpr int kMaxC = kColsF32 > kColsBf16 ? kColsF32 : kColsBf16;   // most column tiles of one job (rows of the reduction buffer: kWaves * kMaxC)
@@ -79,6 +78,7 @@ struct PF32 {
     static constexpr bool kBf16 = false;
     static constexpr int kFirst = PH_A;
     static constexpr int kC = kColsF32;               // column tiles of one job (A loaded once for all)
+    static constexpr int kParts = kCtxPartsF32;       // k-parts of the old-tap context
     static constexpr int kKbw = 10;                   // k-blocks a wave loads before its MFMAs
     static constexpr int kL3Kbw1 = 16, kL3Kbw3 = 4;   // the same for l3 (K = 1, 3)
     __device__ static __forceinline__ f4 mma(A a, B b, f4 acc) { return mfma_k16(a, b, acc); }
@@ -90,6 +90,7 @@ struct PBF16 {
     static constexpr bool kBf16 = true;
     static constexpr int kFirst = PH_N;
     static constexpr int kC = kColsBf16;
+    static constexpr int kParts = kCtxPartsBf16;
     static constexpr int kKbw = 10;
     static constexpr int kL3Kbw1 = 8, kL3Kbw3 = 3;
     __device__ static __forceinline__ f4 mma(A a, B b, f4 acc) {
@@ -322,7 +323,7 @@ __host__ __device__ __forceinline__ int ctxo_blocks(const StepArgs& a, const Ste
 }
 
 // The work of one step: main blocks of each phase and which of the
-// kCtxParts * nc old-tap context jobs of the next step ride along with it:
+// kParts * nc old-tap context jobs of the next step ride along with it:
 // phase ph takes jobs [cut[ph], cut[ph + 1]) (part-major: job j is part
 // j / nc).  A phase lasts as long as its busiest workgroup, so the context
 // jobs are shared evenly among the phases as far as the slots left free in
@@ -353,7 +354,7 @@ __host__ __device__ __forceinline__ StepWork step_work(const StepArgs& a, const 
     StepWork w;
     w.nc = ctxo_blocks<P>(a, s1);
     const int G = a.slots;
-    int left = (P::kBf16 ? kCtxParts : kCtxParts - 1) * w.nc;
+    int left = (P::kBf16 ? P::kParts : P::kParts - 1) * w.nc;
     // an even share per phase first (less contention), within free slots
     const int share = ((left + nph - 1) / nph + kXcds - 1) / kXcds * kXcds;
     int take[kMaxPhases], free_slots[kMaxPhases];
@@ -549,21 +550,21 @@ __device__ __forceinline__ void ctxo_job(const StepArgs& a, const StepRows& s, i
     // double-buffered by step parity: jobs for step s.t may run while the
     // context of step s.t - 1 is still being read from the other half
     const size_t cpart = (size_t)a.max_rows * 2 * M;
-    const size_t q = (size_t)(s.t & 1) * kCtxParts * cpart;
+    const size_t q = (size_t)(s.t & 1) * P::kParts * cpart;
     float prev[C], v[C];
 #pragma unroll
     for (int c = 0; c < C; ++c) {
         prev[c] = 0.0f;
-        if (!P::kBf16 && part == kCtxParts - 1) {
+        if (!P::kBf16 && part == P::kParts - 1) {
             const size_t e = q + tile_idx<PF32>(ro, group_col<P>(jb.ct, c), 2 * M);
 #pragma unroll
-            for (int p2 = 0; p2 < kCtxParts - 1; ++p2) prev[c] += ld1<COH>(a.ctxo, e + p2 * cpart, vo);
+            for (int p2 = 0; p2 < P::kParts - 1; ++p2) prev[c] += ld1<COH>(a.ctxo, e + p2 * cpart, vo);
         }
     }
     const Row w = step_row(a, s, jb.rt * kTile + (lane & 15));
     auto la = [&](int kb) { return ld_tap<P, COH>(a, w, kb, kq, true); };
     const int nkb = a.n_old * M / P::kK;
-    const int klo = nkb * part / kCtxParts, khi = nkb * (part + 1) / kCtxParts;
+    const int klo = nkb * part / P::kParts, khi = nkb * (part + 1) / P::kParts;
     block_tiles<P>(red, a.wp_old, nkb, jb.ct, la, v, klo, khi);
     if (vo) {
 #pragma unroll
@@ -591,7 +592,8 @@ __device__ __forceinline__ void l1_fold_job(const StepArgs& a, const StepRows& s
     const int knew = a.n_new * M;
     const size_t cpart = (size_t)a.max_rows * 2 * M;
     // the old-tap context: the last part's slot holds the whole sum
-    const float* ctx = a.ctxo + ((size_t)(s.t & 1) * kCtxParts + kCtxParts - 1) * cpart;
+    constexpr int NP = PF32::kParts;
+    const float* ctx = a.ctxo + ((size_t)(s.t & 1) * NP + NP - 1) * cpart;
     const int kbn = knew / kTile;
     auto la_new = [&](int kb) { return ld_tap<PF32, COH>(a, w, kb, kq, false); };
     auto la_ctx = [&](int kb) -> f4 { return ld_tile<PF32, COH>(ctx, jb.rt, 2 * M, kb - kbn, w.valid); };
@@ -615,7 +617,8 @@ __device__ __forceinline__ void ctxn_job(const StepArgs& a, const StepRows& s, i
     const int ro = wave < 4 ? jb.rt * kTile + kq * 4 + wave : s.nrows;
     const bool vo = ro < s.nrows;
     const size_t cpart = (size_t)a.max_rows * 2 * M;
-    const size_t cq = (size_t)(s.t & 1) * kCtxParts * cpart;
+    constexpr int NP = PBF16::kParts;
+    const size_t cq = (size_t)(s.t & 1) * NP * cpart;
     float z[C], acc[C];
 #pragma unroll
     for (int c = 0; c < C; ++c) {
@@ -623,7 +626,7 @@ __device__ __forceinline__ void ctxn_job(const StepArgs& a, const StepRows& s, i
         const size_t e = cq + tile_idx<PF32>(ro, n, 2 * M);
         z[c] = a.bc[n];
 #pragma unroll
-        for (int part = 0; part < kCtxParts; ++part) z[c] += ld1<COH>(a.ctxo, e + part * cpart, vo && a.n_old > 0);
+        for (int part = 0; part < NP; ++part) z[c] += ld1<COH>(a.ctxo, e + part * cpart, vo && a.n_old > 0);
     }
     const Row w = step_row(a, s, jb.rt * kTile + (lane & 15));
     auto la = [&](int kb) { return ld_tap<PBF16, COH>(a, w, kb, kq, false); };

@@ -14,6 +14,9 @@ namespace wf {
 constexpr int kMaxTaps = 12;
 constexpr int kMaxNew = 2;           // taps written by the immediately preceding step
 constexpr int kTile = 16;            // MFMA tile edge (rows and columns)
+constexpr int kCtxPartsF32 = 6;      // k-parts of the old-tap context product, fp32 operands
+constexpr int kCtxPartsBf16 = 3;     // the same, bf16 operands
+constexpr int kCtxPartsMax = kCtxPartsF32 > kCtxPartsBf16 ? kCtxPartsF32 : kCtxPartsBf16;
 constexpr int kColsF32 = 1;          // column tiles of one job, fp32 operands
 constexpr int kColsBf16 = 2;         // the same, bf16 operands
 constexpr int kMaxTable = 256;
@@ -83,7 +86,7 @@ struct StepArgs {
     // per-step activations, max_rows x n in MFMA operand order (tile_idx):
     void* h1;               // n = Np1, fp32 or bf16 pairs
     void* h2;               // n = Np2, fp32 or bf16 pairs
-    float* ctxo;            // [2][3] x (n = 2M) old-tap context k-parts, by step parity
+    float* ctxo;            // [2][parts] x (n = 2M) old-tap context k-parts, by step parity
     uint16_t* ctxb;         // bf16: n = 2M, the context vector of the step (pairs)
     uint16_t* ybf;          // bf16: [B*H*W][M/32][2][32] y_hat as bf16 pairs (tap source)
     int max_rows;           // rows of the widest step, rounded up to 16

@@ -335,7 +335,7 @@ static int build_plan(const wf_desc* d, Plan* p) {
     a.h1 = h1;
     a.h2 = h2;
     if ((rc = alloc(p, &a.p1, nlat * Np1)) != WF_OK) return rc;
-    if ((rc = alloc(p, &a.ctxo, (size_t)2 * 3 * R * 2 * M)) != WF_OK) return rc;
+    if ((rc = alloc(p, &a.ctxo, (size_t)2 * kCtxPartsMax * R * 2 * M)) != WF_OK) return rc;
     if (bf) {
         if ((rc = alloc(p, &a.ctxb, R * 2 * 2 * M)) != WF_OK) return rc;
         if ((rc = alloc(p, &a.ybf, nlat * 2 * M)) != WF_OK) return rc;
