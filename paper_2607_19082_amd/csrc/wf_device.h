@@ -466,39 +466,89 @@ __device__ __forceinline__ int group_col(int cg, int c) {
 
 // ---------------------------------------------------------------------------
 // Pre-loop job b: P1[lat][n] = b_hoist[n] + sum_k psi[lat][k] * W1[n][k]
-// (k < 2M) for one 16-row tile and column group of the nlat x Np1 product.
-template <class P>
+// (k < 2M), a plain dense product over all latents.  A workgroup computes a
+// 64-latent x 64-column block; each wave a 32 x 32 quarter (2 x 2 MFMA tiles)
+// over the whole K, so every operand load feeds two MFMA chains and no
+// cross-wave reduction is needed.  Column blocks are placed XCD-aware.
+constexpr int kHoistTiles = 4;   // 16-row / 16-column tiles per workgroup edge
+
 __host__ __device__ __forceinline__ int hoist_blocks(const StepArgs& a) {
-    return xcd_blocks(a.Np1 / kTile / P::kC, ntiles(a.B * a.H * a.W));
+    const int ncb = (a.Np1 / kTile + kHoistTiles - 1) / kHoistTiles;
+    const int nrb = (a.B * a.H * a.W + kTile * kHoistTiles - 1) / (kTile * kHoistTiles);
+    return xcd_blocks(ncb, nrb);
 }
 
 template <class P, bool COH>
-__device__ __forceinline__ void hoist_job(const StepArgs& a, int b, f4 (*red)[64]) {
-    constexpr int C = P::kC;
+__device__ __forceinline__ void hoist_job(const StepArgs& a, int b) {
+    using A = typename P::A;
+    using Bw = typename P::B;
+    constexpr int KB = P::kBf16 ? 6 : 8;   // k-blocks in flight per wave
     const int nlat = a.B * a.H * a.W;
-    const Job jb = xcd_job(b, a.Np1 / kTile / C, ntiles(nlat));
+    const int nct = a.Np1 / kTile;
+    const int ncb = (nct + kHoistTiles - 1) / kHoistTiles;
+    const Job jb = xcd_job(b, ncb, (nlat + kTile * kHoistTiles - 1) / (kTile * kHoistTiles));
     if (!jb.valid) return;
     const int wave = wave_id(), lane = threadIdx.x & 63, kq = lane >> 4;
-    const int r = jb.rt * kTile + (lane & 15);
+    const int rt0 = jb.rt * kHoistTiles + (wave >> 1) * 2;      // this wave's two row tiles
+    const int ct0 = jb.ct * kHoistTiles + (wave & 1) * 2;       // and two column tiles
     const float* psi = a.cp->psi;
-    float bias[C], v[C];
+    const int nkb = 2 * a.M / P::kK;
+    int r[2];
+    bool rv[2], cv[2];
+    const Bw* w[2];
 #pragma unroll
-    for (int c = 0; c < C; ++c) bias[c] = a.b_hoist[group_col<P>(jb.ct, c)];
-    if constexpr (P::kBf16) {
-        const size_t base = (size_t)r * 2 * a.M + kq * 8;
-        auto la = [&](int kb) -> b8x2 {
-            return split8(ld4<false>(psi, base + kb * 32, r < nlat), ld4<false>(psi, base + kb * 32 + 4, r < nlat));
-        };
-        block_tiles<P>(red, a.wp_hoist, 2 * a.M / P::kK, jb.ct, la, v);
-    } else {
-        const size_t base = (size_t)r * 2 * a.M + kq * 4;
-        auto la = [&](int kb) -> f4 { return ld4<false>(psi, base + kb * kTile, r < nlat); };
-        block_tiles<P>(red, a.wp_hoist, 2 * a.M / P::kK, jb.ct, la, v);
+    for (int i = 0; i < 2; ++i) {
+        r[i] = (rt0 + i) * kTile + (lane & 15);
+        rv[i] = r[i] < nlat;
+        cv[i] = ct0 + i < nct;                                   // wave-uniform
+        w[i] = static_cast<const Bw*>(a.wp_hoist) + (size_t)(cv[i] ? ct0 + i : 0) * nkb * 64 + lane;
     }
-    const int ro = jb.rt * kTile + kq * 4 + wave;
-    if (wave < 4 && ro < nlat) {
+    auto la = [&](int i, int kb) -> A {
+        if constexpr (P::kBf16) {
+            const size_t q = (size_t)r[i] * 2 * a.M + kb * 32 + kq * 8;
+            return split8(ld4<false>(psi, q, rv[i]), ld4<false>(psi, q + 4, rv[i]));
+        } else {
+            return ld4<false>(psi, (size_t)r[i] * 2 * a.M + kb * kTile + kq * 4, rv[i]);
+        }
+    };
+    f4 acc[2][2];
 #pragma unroll
-        for (int c = 0; c < C; ++c) st1<COH>(a.p1, (size_t)ro * a.Np1 + group_col<P>(jb.ct, c), v[c] + bias[c]);
+    for (int i = 0; i < 2; ++i)
+#pragma unroll
+        for (int j = 0; j < 2; ++j) acc[i][j] = zero4();
+    for (int kc = 0; kc < nkb; kc += KB) {
+        A av[KB][2];
+        Bw bv[KB][2];
+#pragma unroll
+        for (int u = 0; u < KB; ++u) {
+            const int k = min(kc + u, nkb - 1);
+#pragma unroll
+            for (int i = 0; i < 2; ++i) {
+                av[u][i] = la(i, k);
+                bv[u][i] = w[i][(size_t)k * 64];
+            }
+        }
+#pragma unroll
+        for (int u = 0; u < KB; ++u)
+            if (kc + u < nkb)
+#pragma unroll
+                for (int i = 0; i < 2; ++i)
+#pragma unroll
+                    for (int j = 0; j < 2; ++j) acc[i][j] = P::mma(av[u][i], bv[u][j], acc[i][j]);
+    }
+    // lane holds rows 4*(lane/16) + q of each tile, column lane%16
+#pragma unroll
+    for (int j = 0; j < 2; ++j) {
+        if (!cv[j]) continue;
+        const int n = (ct0 + j) * kTile + (lane & 15);
+        const float bias = a.b_hoist[n];
+#pragma unroll
+        for (int i = 0; i < 2; ++i)
+#pragma unroll
+            for (int q = 0; q < 4; ++q) {
+                const int ro = (rt0 + i) * kTile + kq * 4 + q;
+                if (ro < nlat) st1<COH>(a.p1, (size_t)ro * a.Np1 + n, acc[i][j][q] + bias);
+            }
     }
 }
 

@@ -7,8 +7,7 @@ namespace wf {
 // Pre-loop: the hyperprior half of layer 1 for every latent.
 template <class P>
 __global__ __launch_bounds__(kThreads) void k_hoist(StepArgs a) {
-    __shared__ f4 red[kWaves * kMaxC][64];
-    hoist_job<P, false>(a, blockIdx.x, red);
+    hoist_job<P, false>(a, blockIdx.x);
 }
 
 // Old-tap context jobs [j0, ...) of step s1 only (before the first step).
@@ -47,7 +46,7 @@ int enqueue_set_call(Plan& p, const CallPtrs& c, hipStream_t stream) {
 
 template <class P>
 static void launch_hoist(Plan& p, hipStream_t stream) {
-    hipLaunchKernelGGL(k_hoist<P>, dim3(hoist_blocks<P>(p.args)), dim3(kThreads), 0, stream, p.args);
+    hipLaunchKernelGGL(k_hoist<P>, dim3(hoist_blocks(p.args)), dim3(kThreads), 0, stream, p.args);
 }
 
 int enqueue_hoist(Plan& p, hipStream_t stream) {
