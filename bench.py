@@ -40,7 +40,8 @@ DEFAULT_WORKLOAD = "minnen-hr-4k-240x135-m320"
 CSRC = os.path.join(ROOT, "paper_2607_19082_amd", "csrc")
 PROFILES = os.path.join(ROOT, "profiles")
 # kernels of one decode call (the rest of a bench run: the floor probes, torch)
-DECODE_KERNELS = ("wf::k_phase", "wf::k_hoist", "wf::k_ctxo", "wf::k_set_call", "wf::k_persistent", "wf::k_zero_u32")
+DECODE_KERNELS = ("wf::k_phase", "wf::k_hoist", "wf::k_ctxo", "wf::k_set_call", "wf::k_persistent", "wf::k_zero_u32",
+                  "wf::k_dataflow", "wf::k_zero_u128")
 
 
 def source_hash():
@@ -178,7 +179,7 @@ def main():
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--workload", default=DEFAULT_WORKLOAD)
-    ap.add_argument("--driver", default="graph", choices=["stream", "graph", "persistent"])
+    ap.add_argument("--driver", default="graph", choices=["stream", "graph", "persistent", "dataflow"])
     ap.add_argument("--precision", default="fp32", choices=["fp32", "bf16"])
     ap.add_argument("--cpu-rows", type=int, default=8, help="grid rows of the CPU-oracle sample (0: skip)")
     ap.add_argument("--no-encode", action="store_true")
@@ -275,6 +276,7 @@ def main():
                      "traffic_unit": "HBM bytes per launch (one decode)",
                      "traffic_GBps": None if traffic is None else traffic / (dec_ms * 1e-3) / 1e9,
                      "kernel": {"persistent": "k_persistent (one launch = one decode)",
+                                "dataflow": "one decode call: counter reset, hoist and one k_dataflow launch",
                                 "graph": "one replay of the decode graph (hoist, context, one k_phase per phase)",
                                 "stream": "all kernels of one decode call"}[args.driver],
                      "algorithmic_gflop_per_launch": fl / 1e9, "launch_ms_events": dec_ms,

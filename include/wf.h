@@ -62,7 +62,9 @@ typedef enum {
 typedef enum {
     WF_DRIVER_STREAM = 0,   /* per-step kernel launches, enqueued one by one on the stream */
     WF_DRIVER_GRAPH = 1,    /* the same per-step kernels, replayed from one HIP graph      */
-    WF_DRIVER_PERSISTENT = 2/* one cooperative kernel, device-wide barrier per step         */
+    WF_DRIVER_PERSISTENT = 2,/* one cooperative kernel, device-wide barrier per phase      */
+    WF_DRIVER_DATAFLOW = 3  /* one cooperative kernel; every job waits only for the jobs it
+                               depends on (per-step, per-row-tile completion counters)     */
 } wf_driver;
 
 /*
@@ -162,17 +164,21 @@ int wf_encode(wf_plan_t plan, const float *psi, const float *y, int32_t *sym_out
               const wf_out *out, hipStream_t stream);
 
 /*
- * Measurement hook of the persistent driver (WF_E_UNSUPPORTED for others).
- * With `stamps` non-NULL (DEVICE int64 array of `capacity` entries) every
- * later call records the device wall clock (100 MHz ticks) at each
- * device-wide barrier k = 0, 1, ...: entry k*(G+1) + g is the time workgroup g
- * arrived at barrier k, entry k*(G+1) + G the time workgroup 0 left it, where
- * G is the grid size written to *grid.  A call has 2 + 3*T barriers with
- * fp32 operands (two before the first step, then one per phase) and 1 + 4*T
- * with bf16; *needed receives the entries that takes (either output may be
- * NULL).  Entries past
- * `capacity` are not written.  stamps == NULL turns recording off.  The array
- * stays owned by the caller and must outlive the calls that record into it.
+ * Measurement hook of the persistent and dataflow drivers (WF_E_UNSUPPORTED
+ * for the others).  With `stamps` non-NULL (DEVICE int64 array of `capacity`
+ * entries) every later call records the device wall clock (100 MHz ticks):
+ *  - persistent: at each device-wide barrier k = 0, 1, ...: entry k*(G+1) + g
+ *    is the time workgroup g arrived at barrier k, entry k*(G+1) + G the time
+ *    workgroup 0 left it.  A call has 2 + 3*T barriers with fp32 operands (two
+ *    before the first step, then one per phase) and 1 + 4*T with bf16.
+ *  - dataflow: three entries per job, 3*j + {0, 1, 2} = the time the job's
+ *    workgroup started waiting for its inputs, the time they were complete,
+ *    and the time its results had landed; j is the job's position in the
+ *    plan's job lists (XCD classes 0..7 in turn, each in its topological order).
+ * G is the grid size written to *grid; *needed receives the entries a call
+ * takes (either output may be NULL).  Entries past `capacity` are not
+ * written.  stamps == NULL turns recording off.  The array stays owned by
+ * the caller and must outlive the calls that record into it.
  */
 int wf_plan_trace(wf_plan_t plan, int64_t *stamps, int64_t capacity, int64_t *needed,
                   int32_t *grid);

@@ -274,6 +274,11 @@ __host__ __device__ __forceinline__ StepRows step_rows(int H, int W, int B, int 
     return s;
 }
 
+// The layer-2 output of step s: h2 for even steps, h2b for odd ones (the
+// dataflow driver double-buffers it by step parity; the other drivers pass
+// the same array twice).
+__device__ __forceinline__ void* h2_of(const StepArgs& a, const StepRows& s) { return (s.t & 1) ? a.h2b : a.h2; }
+
 // XCD-aware job of block b: column tile ct (always on XCD ct % 8) and row
 // tile rt, for kXcds * ceil(nct / kXcds) * nrt blocks.
 struct Job {
@@ -588,33 +593,31 @@ __device__ __forceinline__ typename P::A ld_tap(const StepArgs& a, const Row& w,
 // With fp32 the last part runs after the others and stores the whole sum
 // (its own part plus theirs), so layer 1 reads one value per element.
 template <class P, bool COH>
-__device__ __forceinline__ void ctxo_job(const StepArgs& a, const StepRows& s, int j, int nc, f4 (*red)[64]) {
+__device__ __forceinline__ void ctxo_tile(const StepArgs& a, const StepRows& s, int part, Job jb, f4 (*red)[64]) {
     constexpr int C = P::kC;
-    const int part = j / nc, b = j - part * nc;
     const int M = a.M;
-    const Job jb = xcd_job(b, 2 * M / kTile / C, ntiles(s.nrows));
-    if (!jb.valid) return;
     const int wave = wave_id(), lane = threadIdx.x & 63, kq = lane >> 4;
     const int ro = wave < 4 ? jb.rt * kTile + kq * 4 + wave : s.nrows;
     const bool vo = ro < s.nrows;
     // double-buffered by step parity: jobs for step s.t may run while the
     // context of step s.t - 1 is still being read from the other half
     const size_t cpart = (size_t)a.max_rows * 2 * M;
-    const size_t q = (size_t)(s.t & 1) * P::kParts * cpart;
+    const int NP = a.ctx_parts;
+    const size_t q = (size_t)(s.t & 1) * NP * cpart;
     float prev[C], v[C];
 #pragma unroll
     for (int c = 0; c < C; ++c) {
         prev[c] = 0.0f;
-        if (!P::kBf16 && part == P::kParts - 1) {
+        if (!P::kBf16 && part == NP - 1) {
             const size_t e = q + tile_idx<PF32>(ro, group_col<P>(jb.ct, c), 2 * M);
 #pragma unroll
-            for (int p2 = 0; p2 < P::kParts - 1; ++p2) prev[c] += ld1<COH>(a.ctxo, e + p2 * cpart, vo);
+            for (int p2 = 0; p2 < NP - 1; ++p2) prev[c] += ld1<COH>(a.ctxo, e + p2 * cpart, vo);
         }
     }
     const Row w = step_row(a, s, jb.rt * kTile + (lane & 15));
     auto la = [&](int kb) { return ld_tap<P, COH>(a, w, kb, kq, true); };
     const int nkb = a.n_old * M / P::kK;
-    const int klo = nkb * part / P::kParts, khi = nkb * (part + 1) / P::kParts;
+    const int klo = nkb * part / NP, khi = nkb * (part + 1) / NP;
     block_tiles<P>(red, a.wp_old, nkb, jb.ct, la, v, klo, khi);
     if (vo) {
 #pragma unroll
@@ -622,13 +625,17 @@ __device__ __forceinline__ void ctxo_job(const StepArgs& a, const StepRows& s, i
             st1<COH>(a.ctxo, q + part * cpart + tile_idx<PF32>(ro, group_col<P>(jb.ct, c), 2 * M), v[c] + prev[c]);
     }
 }
+template <class P, bool COH>
+__device__ __forceinline__ void ctxo_job(const StepArgs& a, const StepRows& s, int j, int nc, f4 (*red)[64]) {
+    const int part = j / nc;
+    const Job jb = xcd_job(j - part * nc, 2 * a.M / kTile / P::kC, ntiles(s.nrows));
+    if (jb.valid) ctxo_tile<P, COH>(a, s, part, jb, red);
+}
 
 // Phase A, fp32: layer 1 of step s over [new taps ; old-tap context].
 template <bool COH>
-__device__ __forceinline__ void l1_fold_job(const StepArgs& a, const StepRows& s, int b, f4 (*red)[64]) {
+__device__ __forceinline__ void l1_fold_tile(const StepArgs& a, const StepRows& s, Job jb, f4 (*red)[64]) {
     constexpr int C = PF32::kC;
-    const Job jb = xcd_job(b, a.Np1 / kTile / C, ntiles(s.nrows));
-    if (!jb.valid) return;
     const int wave = wave_id(), lane = threadIdx.x & 63, kq = lane >> 4;
     const int M = a.M;
     // epilogue operands first: the hoisted part of this wave's row
@@ -642,7 +649,7 @@ __device__ __forceinline__ void l1_fold_job(const StepArgs& a, const StepRows& s
     const int knew = a.n_new * M;
     const size_t cpart = (size_t)a.max_rows * 2 * M;
     // the old-tap context: the last part's slot holds the whole sum
-    constexpr int NP = PF32::kParts;
+    const int NP = a.ctx_parts;
     const float* ctx = a.ctxo + ((size_t)(s.t & 1) * NP + NP - 1) * cpart;
     const int kbn = knew / kTile;
     auto la_new = [&](int kb) { return ld_tap<PF32, COH>(a, w, kb, kq, false); };
@@ -654,20 +661,23 @@ __device__ __forceinline__ void l1_fold_job(const StepArgs& a, const StepRows& s
             st_tile<PF32, COH>(a.h1, ro, a.Np1, group_col<PF32>(jb.ct, c), lrelu(acc[c] + z[c], a.slope));
     }
 }
+template <bool COH>
+__device__ __forceinline__ void l1_fold_job(const StepArgs& a, const StepRows& s, int b, f4 (*red)[64]) {
+    const Job jb = xcd_job(b, a.Np1 / kTile / PF32::kC, ntiles(s.nrows));
+    if (jb.valid) l1_fold_tile<COH>(a, s, jb, red);
+}
 
 // Phase N, bf16: the context vector of step s, as bf16 pairs.
 template <bool COH>
-__device__ __forceinline__ void ctxn_job(const StepArgs& a, const StepRows& s, int b, f4 (*red)[64]) {
+__device__ __forceinline__ void ctxn_tile(const StepArgs& a, const StepRows& s, Job jb, f4 (*red)[64]) {
     constexpr int C = PBF16::kC;
     const int M = a.M;
-    const Job jb = xcd_job(b, 2 * M / kTile / C, ntiles(s.nrows));
-    if (!jb.valid) return;
     const int wave = wave_id(), lane = threadIdx.x & 63, kq = lane >> 4;
     // epilogue operands first: bias and the old-tap context parts
     const int ro = wave < 4 ? jb.rt * kTile + kq * 4 + wave : s.nrows;
     const bool vo = ro < s.nrows;
     const size_t cpart = (size_t)a.max_rows * 2 * M;
-    constexpr int NP = PBF16::kParts;
+    const int NP = a.ctx_parts;
     const size_t cq = (size_t)(s.t & 1) * NP * cpart;
     float z[C], acc[C];
 #pragma unroll
@@ -687,13 +697,16 @@ __device__ __forceinline__ void ctxn_job(const StepArgs& a, const StepRows& s, i
             st_tile<PBF16, COH>(a.ctxb, ro, 2 * M, group_col<PBF16>(jb.ct, c), acc[c] + z[c]);
     }
 }
+template <bool COH>
+__device__ __forceinline__ void ctxn_job(const StepArgs& a, const StepRows& s, int b, f4 (*red)[64]) {
+    const Job jb = xcd_job(b, 2 * a.M / kTile / PBF16::kC, ntiles(s.nrows));
+    if (jb.valid) ctxn_tile<COH>(a, s, jb, red);
+}
 
 // Phase A, bf16: layer 1 of step s over the context vector.
 template <bool COH>
-__device__ __forceinline__ void l1_ctx_job(const StepArgs& a, const StepRows& s, int b, f4 (*red)[64]) {
+__device__ __forceinline__ void l1_ctx_tile(const StepArgs& a, const StepRows& s, Job jb, f4 (*red)[64]) {
     constexpr int C = PBF16::kC;
-    const Job jb = xcd_job(b, a.Np1 / kTile / C, ntiles(s.nrows));
-    if (!jb.valid) return;
     const int wave = wave_id(), lane = threadIdx.x & 63, kq = lane >> 4;
     const int M = a.M;
     const int ro = wave < 4 ? jb.rt * kTile + kq * 4 + wave : s.nrows;
@@ -711,13 +724,16 @@ __device__ __forceinline__ void l1_ctx_job(const StepArgs& a, const StepRows& s,
             st_tile<PBF16, COH>(a.h1, ro, a.Np1, group_col<PBF16>(jb.ct, c), lrelu(acc[c] + z[c], a.slope));
     }
 }
+template <bool COH>
+__device__ __forceinline__ void l1_ctx_job(const StepArgs& a, const StepRows& s, int b, f4 (*red)[64]) {
+    const Job jb = xcd_job(b, a.Np1 / kTile / PBF16::kC, ntiles(s.nrows));
+    if (jb.valid) l1_ctx_tile<COH>(a, s, jb, red);
+}
 
 // Phase B: layer 2.
 template <class P, bool COH>
-__device__ __forceinline__ void l2_job(const StepArgs& a, const StepRows& s, int b, f4 (*red)[64]) {
+__device__ __forceinline__ void l2_tile(const StepArgs& a, const StepRows& s, Job jb, f4 (*red)[64]) {
     constexpr int C = P::kC;
-    const Job jb = xcd_job(b, a.Np2 / kTile / C, ntiles(s.nrows));
-    if (!jb.valid) return;
     const int wave = wave_id(), lane = threadIdx.x & 63, kq = lane >> 4;
     float bias[C], acc[C];
 #pragma unroll
@@ -730,8 +746,13 @@ __device__ __forceinline__ void l2_job(const StepArgs& a, const StepRows& s, int
     if (wave < 4 && ro < s.nrows) {
 #pragma unroll
         for (int c = 0; c < C; ++c)
-            st_tile<P, COH>(a.h2, ro, a.Np2, group_col<P>(jb.ct, c), lrelu(acc[c] + bias[c], a.slope));
+            st_tile<P, COH>(h2_of(a, s), ro, a.Np2, group_col<P>(jb.ct, c), lrelu(acc[c] + bias[c], a.slope));
     }
+}
+template <class P, bool COH>
+__device__ __forceinline__ void l2_job(const StepArgs& a, const StepRows& s, int b, f4 (*red)[64]) {
+    const Job jb = xcd_job(b, a.Np2 / kTile / P::kC, ntiles(s.nrows));
+    if (jb.valid) l2_tile<P, COH>(a, s, jb, red);
 }
 
 __device__ __forceinline__ int scale_index(const float* tab, int L, float sg) {
@@ -759,14 +780,12 @@ struct L3Smem {
 // needs -- K=1: mean, K=3: 3 logits and 3 component means; 1: the scales).
 // The scale table must already be in sm.tab.
 template <class P, int KC, bool COH>
-__device__ __forceinline__ void l3_job(const StepArgs& a, const StepRows& s, int b, L3Smem<KC>& sm) {
+__device__ __forceinline__ void l3_tile(const StepArgs& a, const StepRows& s, Job jb, L3Smem<KC>& sm) {
     using A = typename P::A;
     using Bw = typename P::B;
     constexpr int NT0 = L3Smem<KC>::NT0, NT1 = L3Smem<KC>::NT1, NTM = L3Smem<KC>::NTM;
     constexpr int KBW = KC == 1 ? P::kL3Kbw1 : P::kL3Kbw3;
     const int M = a.M, G = M / kTile;
-    const Job jb = xcd_job(b, 2 * G, ntiles(s.nrows));
-    if (!jb.valid) return;
     const int vg = jb.ct / G, cg = jb.ct - vg * G, rt = jb.rt;
     const int wave = wave_id(), lane = threadIdx.x & 63, kq = lane >> 4;
 
@@ -795,6 +814,7 @@ __device__ __forceinline__ void l3_job(const StepArgs& a, const StepRows& s, int
     const int r = rt * kTile + (lane & 15);
     const bool valid = r < s.nrows;
     const Bw* __restrict__ wv = static_cast<const Bw*>(a.wp3) + lane;
+    const void* h2 = h2_of(a, s);
     const int NT = vg == 0 ? NT0 : NT1;
     int cols[NTM];
 #pragma unroll
@@ -808,7 +828,7 @@ __device__ __forceinline__ void l3_job(const StepArgs& a, const StepRows& s, int
 #pragma unroll
         for (int u = 0; u < KBW; ++u) {
             const int k = min(kc + u, kb1 - 1);
-            av[u] = ld_tile<P, COH>(a.h2, rt, a.Np2, k, valid);
+            av[u] = ld_tile<P, COH>(h2, rt, a.Np2, k, valid);
 #pragma unroll
             for (int t = 0; t < NTM; ++t) bv[u][t] = wv[((size_t)cols[t] * nkb + k) * 64];
         }
@@ -877,6 +897,11 @@ __device__ __forceinline__ void l3_job(const StepArgs& a, const StepRows& s, int
     cp->mean[oq] = mu;
     st1<COH>(cp->y_hat, oq, sv + mu);
     if constexpr (P::kBf16) st_pair_row<COH>(a.ybf, lat * 2 * M, c, sv + mu);
+}
+template <class P, int KC, bool COH>
+__device__ __forceinline__ void l3_job(const StepArgs& a, const StepRows& s, int b, L3Smem<KC>& sm) {
+    const Job jb = xcd_job(b, 2 * (a.M / kTile), ntiles(s.nrows));
+    if (jb.valid) l3_tile<P, KC, COH>(a, s, jb, sm);
 }
 
 // The main job of phase ph (sm.tab must hold the scale table for PH_C).

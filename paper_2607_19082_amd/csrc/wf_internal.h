@@ -16,13 +16,46 @@ constexpr int kMaxNew = 2;           // taps written by the immediately precedin
 constexpr int kTile = 16;            // MFMA tile edge (rows and columns)
 constexpr int kCtxPartsF32 = 6;      // k-parts of the old-tap context product, fp32 operands
 constexpr int kCtxPartsBf16 = 3;     // the same, bf16 operands
+constexpr int kDfCtxParts = 3;       // the same for the dataflow driver (its context jobs run
+                                     // in a pool of their own, where fewer, longer jobs pay)
 constexpr int kCtxPartsMax = kCtxPartsF32 > kCtxPartsBf16 ? kCtxPartsF32 : kCtxPartsBf16;
+static_assert(kDfCtxParts <= kCtxPartsMax, "context k-parts exceed the buffer");
 constexpr int kColsF32 = 1;          // column tiles of one job, fp32 operands
 constexpr int kColsBf16 = 2;         // the same, bf16 operands
 constexpr int kMaxTable = 256;
 constexpr int kXcds = 8;             // accelerator complex dies of an MI355X
 constexpr int kBarrierWords = 512;   // barrier counters of the persistent driver
 constexpr int kBufBytes = 0x7fff0000; // window of a raw buffer access (arrays must fit)
+constexpr int kDfSlotWords = 16;     // dataflow counter slots: one per 64 bytes
+
+// Job kinds of the dataflow driver (see wf_dataflow.hip).
+enum JobKind { JK_CTX = 0, JK_CTXL = 1, JK_N = 2, JK_A = 3, JK_B = 4, JK_C0 = 5, JK_C1 = 6, kJobKinds = 7 };
+
+// Column tiles ct in [lo, hi) with ct % 8 == x.
+__host__ __device__ __forceinline__ int cnt_range(int lo, int hi, int x) {
+    auto upto = [](int n, int x) { return n > x ? (n - x + kXcds - 1) / kXcds : 0; };
+    return upto(hi, x) - upto(lo, x);
+}
+
+// Dataflow driver state passed to its kernel: the per-XCD-class job lists
+// (job code {t, kind | part << 4 | rt << 8 | ct << 16}) and the counters.
+// Counter group (t, kind, rt) counts the finished jobs of that step, kind and
+// row tile; rt = nrt_max holds the step's total (kept for JK_C0 and JK_C1).
+// Each group has one slot per XCD class, bumped by the jobs of that class.
+// Two pools of workgroups take jobs from separate lists: workgroups
+// [0, ncrit) the critical chain (N, A, B, C0, C1), the others the old-tap
+// context (CTX, CTXL), so that a critical job never waits behind context work
+// queued in its workgroup's list.
+struct DfArgs {
+    const int2* jobs;
+    int off[2 * kXcds + 1]; // list x (critical) is jobs[off[x], off[x+1]), list 8 + x (context) follows
+    int ncrit;              // workgroups of the critical pool (a multiple of 8)
+    unsigned* cnt;
+    size_t cnt_words;
+    int nrt_max;            // 16-row tiles of the widest step
+    long long* stamps;      // optional trace: 3 wall-clock ticks per job (see wf_plan_trace)
+    long long stamps_cap;
+};
 
 // Set the calling thread's error message and return `code`.
 int fail(int code, const std::string& msg);
@@ -64,6 +97,7 @@ struct StepArgs {
     int H, W, M, B, K, L, lambda;
     int Np1, Np2, n3;
     int n_new, n_old;
+    int ctx_parts;          // k-parts of the old-tap context product (per driver, precision)
     // Tap geometry, as scalars so that kernels compute a tap's offset without
     // indexing memory.  Old taps, tap-major: the first old_n0 lie in row -2,
     // the next old_n1 in row -1, the rest in row 0; each row's run starts at
@@ -85,7 +119,8 @@ struct StepArgs {
     float* p1;              // [B*H*W][Np1] hoisted layer-1 part
     // per-step activations, max_rows x n in MFMA operand order (tile_idx):
     void* h1;               // n = Np1, fp32 or bf16 pairs
-    void* h2;               // n = Np2, fp32 or bf16 pairs
+    void* h2;               // n = Np2, fp32 or bf16 pairs (even steps)
+    void* h2b;              // the same for odd steps (dataflow driver; else == h2)
     float* ctxo;            // [2][parts] x (n = 2M) old-tap context k-parts, by step parity
     uint16_t* ctxb;         // bf16: n = 2M, the context vector of the step (pairs)
     uint16_t* ybf;          // bf16: [B*H*W][M/32][2][32] y_hat as bf16 pairs (tap source)
@@ -117,6 +152,8 @@ struct Plan {
     long long spin_budget = 100000000;   // wall-clock ticks (100 MHz): 1 s
     long long* stamps = nullptr;         // optional barrier trace
     long long stamps_cap = 0;
+    // dataflow driver
+    DfArgs df{};
     // graph driver
     hipStream_t cap_stream = nullptr;
     hipGraph_t graph = nullptr;
@@ -134,6 +171,12 @@ int enqueue_hoist(Plan& p, hipStream_t stream);
 // Persistent driver: grid size (checked co-residency) and one call.
 int persistent_grid(Plan& p, int* grid);
 int enqueue_persistent(Plan& p, hipStream_t stream);
+// Dataflow driver: job lists of the plan, and one call.
+int build_dataflow(Plan& p, std::vector<int2>& lists, DfArgs& d);
+int enqueue_dataflow(Plan& p, hipStream_t stream);
+const void* dataflow_fn(const Plan& p);
+// Grid of a cooperative kernel: two workgroups per CU when they fit, else one.
+int coop_grid(Plan& p, const void* fn, int* grid);
 // Latency floor of one dependent step hop (see wf_measure_floor).
 int measure_floor(Plan& p, float* node_us, float* barrier_us);
 

@@ -116,12 +116,15 @@ static const void* persistent_fn(const Plan& p) {
 
 // Grid size of the persistent kernel: two workgroups per CU when they fit (one
 // hides the other's memory latency), else one; a multiple of 8 (XCD placement).
-int persistent_grid(Plan& p, int* grid) {
+int persistent_grid(Plan& p, int* grid) { return coop_grid(p, persistent_fn(p), grid); }
+
+int coop_grid(Plan& p, const void* fn, int* grid) {
+    (void)p;
     int dev = 0, cus = 0, per_cu = 0;
     hipError_t e = hipGetDevice(&dev);
     if (e == hipSuccess) e = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);
     if (e == hipSuccess)
-        e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, persistent_fn(p), kThreads, 0);
+        e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, fn, kThreads, 0);
     if (e != hipSuccess) return fail(WF_E_HIP, std::string("occupancy query: ") + hipGetErrorString(e));
     if (per_cu < 1 || cus < kXcds) return fail(WF_E_UNSUPPORTED, "persistent kernel cannot be resident");
     *grid = cus * (per_cu >= 2 ? 2 : 1) / kXcds * kXcds;

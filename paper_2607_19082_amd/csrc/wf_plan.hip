@@ -71,7 +71,7 @@ static int check_desc(const wf_desc* d) {
         return fail(WF_E_INVALID, "unknown mask");
     if (d->precision != WF_FP32 && d->precision != WF_BF16)
         return fail(WF_E_INVALID, "unknown precision");
-    if (d->driver < WF_DRIVER_STREAM || d->driver > WF_DRIVER_PERSISTENT)
+    if (d->driver < WF_DRIVER_STREAM || d->driver > WF_DRIVER_DATAFLOW)
         return fail(WF_E_INVALID, "unknown driver");
     if (!d->ctx_w || !d->ctx_b || !d->w1 || !d->b1 || !d->w2 || !d->b2 || !d->w3 || !d->b3 ||
         !d->scale_table)
@@ -235,6 +235,7 @@ static int build_plan(const wf_desc* d, Plan* p) {
     }
     if ((int)new_taps.size() != kMaxNew) return fail(WF_E_UNSUPPORTED, "mask must have two taps of age one");
     a.n_new = (int)new_taps.size();
+    a.ctx_parts = p->driver == WF_DRIVER_DATAFLOW ? kDfCtxParts : (bf ? kCtxPartsBf16 : kCtxPartsF32);
     a.n_old = (int)old_taps.size();
     a.old_n0 = a.old_n1 = 0;
     for (int o : old_taps) {
@@ -334,6 +335,13 @@ static int build_plan(const wf_desc* d, Plan* p) {
     if ((rc = alloc(p, &h2, R * p->Np2)) != WF_OK) return rc;
     a.h1 = h1;
     a.h2 = h2;
+    a.h2b = h2;
+    if (p->driver == WF_DRIVER_DATAFLOW) {
+        // the dataflow driver double-buffers layer 2's output by step parity
+        float* h2b = nullptr;
+        if ((rc = alloc(p, &h2b, R * p->Np2)) != WF_OK) return rc;
+        a.h2b = h2b;
+    }
     if ((rc = alloc(p, &a.p1, nlat * Np1)) != WF_OK) return rc;
     if ((rc = alloc(p, &a.ctxo, (size_t)2 * kCtxPartsMax * R * 2 * M)) != WF_OK) return rc;
     if (bf) {
@@ -352,6 +360,19 @@ static int build_plan(const wf_desc* d, Plan* p) {
         p->grid = a.slots;
         if ((rc = alloc(p, &p->d_bar, kBarrierWords)) != WF_OK) return rc;
         WF_HIP(hipMemset(p->d_bar, 0, kBarrierWords * sizeof(unsigned)));
+    }
+    if (p->driver == WF_DRIVER_DATAFLOW) {
+        std::vector<int2> lists;
+        if ((rc = build_dataflow(*p, lists, p->df)) != WF_OK) return rc;
+        int2* jobs = nullptr;
+        if ((rc = upload(p, &jobs, lists.data(), lists.size())) != WF_OK) return rc;
+        p->df.jobs = jobs;
+        if ((rc = alloc(p, &p->df.cnt, p->df.cnt_words)) != WF_OK) return rc;
+        if ((rc = coop_grid(*p, dataflow_fn(*p), &p->grid)) != WF_OK) return rc;
+        // half of the grid runs the critical chain (one workgroup per CU when
+        // two fit), the other half the old-tap context
+        p->df.ncrit = p->grid >= 2 * kXcds ? p->grid / 2 / kXcds * kXcds : p->grid;
+        if (p->df.ncrit == p->grid) return fail(WF_E_UNSUPPORTED, "dataflow driver needs at least 16 workgroups");
     }
     WF_HIP(hipDeviceSynchronize());
 
@@ -445,6 +466,7 @@ static int run_call(Plan* p, const CallPtrs& c, hipStream_t stream) {
         return WF_OK;
     }
     if (p->driver == WF_DRIVER_PERSISTENT) return enqueue_persistent(*p, stream);
+    if (p->driver == WF_DRIVER_DATAFLOW) return enqueue_dataflow(*p, stream);
     return enqueue_steps(*p, stream);
 }
 
@@ -478,10 +500,17 @@ int wf_encode(wf_plan_t plan, const float* psi, const float* y, int32_t* sym_out
 int wf_plan_trace(wf_plan_t plan, int64_t* stamps, int64_t capacity, int64_t* needed, int32_t* grid) {
     if (!plan) return fail(WF_E_INVALID, "plan is NULL");
     Plan* p = reinterpret_cast<Plan*>(plan);
-    if (p->driver != WF_DRIVER_PERSISTENT) return fail(WF_E_UNSUPPORTED, "tracing needs the persistent driver");
+    if (p->driver != WF_DRIVER_PERSISTENT && p->driver != WF_DRIVER_DATAFLOW)
+        return fail(WF_E_UNSUPPORTED, "tracing needs the persistent or the dataflow driver");
     if (stamps && capacity < 0) return fail(WF_E_INVALID, "negative capacity");
     p->stamps = reinterpret_cast<long long*>(stamps);
     p->stamps_cap = stamps ? capacity : 0;
+    if (p->driver == WF_DRIVER_DATAFLOW) {
+        // three entries per job of the plan's job lists
+        if (needed) *needed = 3LL * p->df.off[2 * kXcds];
+        if (grid) *grid = p->grid;
+        return WF_OK;
+    }
     // barriers: the prologue (two with fp32) and one per phase of every step
     const int64_t pro = p->precision == WF_BF16 ? 1 : 2;
     if (needed) *needed = (int64_t)(pro + p->nph * (int64_t)p->T) * (p->grid + 1);

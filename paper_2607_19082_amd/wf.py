@@ -15,7 +15,7 @@ LIB_PATH = os.path.join(_PKG, "libwf.so")
 WF_OK, WF_E_INVALID, WF_E_UNSUPPORTED, WF_E_HIP, WF_E_NOMEM, WF_E_TIMEOUT = 0, -1, -2, -3, -4, -5
 MASK = {"full": 0, "relaxed": 1}
 PRECISION = {"fp32": 0, "bf16": 1}
-DRIVER = {"stream": 0, "graph": 1, "persistent": 2}
+DRIVER = {"stream": 0, "graph": 1, "persistent": 2, "dataflow": 3}
 
 EXPORTS = ["wf_schedule", "wf_validate", "wf_plan", "wf_plan_schedule", "wf_decode",
            "wf_encode", "wf_plan_trace", "wf_measure_floor", "wf_plan_sync", "wf_plan_destroy",

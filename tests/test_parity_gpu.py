@@ -68,7 +68,7 @@ SMALL = [
 ]
 
 
-DRIVERS = ["stream", "graph", "persistent"]
+DRIVERS = ["stream", "graph", "persistent", "dataflow"]
 
 
 @pytest.mark.parametrize("driver", DRIVERS)
@@ -108,7 +108,7 @@ def test_full_decode_encode(name, driver):
     ("minnen-relaxed-b8-120x68-m192", 9, 16, 8),
     ("minnen-hr-4k-240x135-m320", 9, 20, 1),
 ])
-@pytest.mark.parametrize("driver", ["graph", "persistent"])
+@pytest.mark.parametrize("driver", ["graph", "persistent", "dataflow"])
 def test_reduced_global(name, H, W, B, driver):
     log(f"case {name} reduced H={H} W={W} B={B} driver={driver}")
     cfg, w, table, psi, sym = make_case(name, H=H, W=W, B=B)
@@ -122,7 +122,7 @@ def test_reduced_global(name, H, W, B, driver):
     ("minnen-relaxed-b8-120x68-m192", 600, 3),
     ("minnen-hr-4k-240x135-m320", 300, 5),
 ])
-@pytest.mark.parametrize("driver", ["graph", "persistent"])
+@pytest.mark.parametrize("driver", ["graph", "persistent", "dataflow"])
 def test_full_size_teacher_forced(name, n, rows, driver):
     log(f"case {name} full size, top {rows} rows + teacher-forced sample of {n}, driver={driver}")
     cfg, w, table, psi, sym = make_case(name)
