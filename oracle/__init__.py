@@ -8,6 +8,9 @@ and this package never imports the GPU path.
   given topological order (raster by default, Sec. III-A, Eq. 2), with the 5x5
   causal masked-conv context (Appendix A, Def. 1, R = 2) and the 1x1 entropy
   parameter network (Sec. II-B, Eq. 1); fp64 accumulation, fp32 storage.
+  With ``group`` N > 1 it is the context-approximation decode of Sec. III-D
+  (Fig. 3): groups of N wavefronts, same-group taps filled with the mean of
+  the decoded taps.
 * ``schedule.py`` -- the dependency DAG of the mask (Eq. 3, Def. 1), its ASAP
   levels and critical path, and a brute-force search over linear schedules
   (Sec. III-B, Eq. 5-7; Appendix A, Thm. 1).
@@ -44,6 +47,7 @@ class _Model(ctypes.Structure):
         ("w2", ctypes.c_void_p), ("b2", ctypes.c_void_p),
         ("w3", ctypes.c_void_p), ("b3", ctypes.c_void_p),
         ("table", ctypes.c_void_p), ("L", ctypes.c_int32),
+        ("group", ctypes.c_int32),
     ]
 
 
@@ -68,6 +72,9 @@ def _load():
         lib.oracle_eval.argtypes = [ctypes.POINTER(_Model), ctypes.c_void_p, ctypes.c_void_p,
                                     ctypes.c_void_p, ctypes.c_int64, ctypes.POINTER(_Out)]
         lib.oracle_eval.restype = ctypes.c_int
+        lib.oracle_tap_status.argtypes = [ctypes.POINTER(_Model), ctypes.c_int, ctypes.c_int,
+                                          ctypes.c_int, ctypes.c_int]
+        lib.oracle_tap_status.restype = ctypes.c_int
         _lib = lib
     return _lib
 
@@ -83,10 +90,12 @@ def _ptr(a):
 class Model:
     """Model description for the oracle.  ``weights`` is a dict with keys
     ctx_w [2M][M][5][5], ctx_b [2M], w1 [d1][4M], b1, w2 [d2][d1], b2,
-    w3 [n3][d2], b3 (PyTorch layouts); ``table`` is the scale table."""
+    w3 [n3][d2], b3 (PyTorch layouts); ``table`` is the scale table.  ``group``
+    N > 1 selects the context-approximation decode with groups of N
+    wavefronts (N <= 1: the exact autoregressive decode)."""
 
     def __init__(self, weights, table, H, W, B=1, K=1, relaxed=False, bf16=False,
-                 slope=0.01):
+                 slope=0.01, group=1):
         self.arrays = {k: _f32(v) for k, v in weights.items()}
         self.table = _f32(table)
         M = self.arrays["ctx_w"].shape[1]
@@ -101,7 +110,14 @@ class Model:
         self._m = _Model(H, W, M, B, K, d1, d2, int(relaxed), int(bf16), slope,
                          _ptr(a["ctx_w"]), _ptr(a["ctx_b"]), _ptr(a["w1"]), _ptr(a["b1"]),
                          _ptr(a["w2"]), _ptr(a["b2"]), _ptr(a["w3"]), _ptr(a["b3"]),
-                         _ptr(self.table), len(self.table))
+                         _ptr(self.table), len(self.table), int(group))
+        self.group = int(group)
+
+    def tap_status(self, i, j, dy, dx):
+        """0: tap (dy,dx) of latent (i,j) lies outside the grid; 1: it was
+        decoded in an earlier group (its value is used); 2: it belongs to the
+        latent's own group (filled with the mean of the decoded taps)."""
+        return _load().oracle_tap_status(ctypes.byref(self._m), i, j, dy, dx)
 
     def _alloc(self, n):
         M, K = self.M, self.K

@@ -100,3 +100,9 @@ def wavefront_sets(rank):
         for j, t in enumerate(row):
             sets.setdefault(t, []).append((i, j))
     return dict(sorted(sets.items()))
+
+
+def group_of(i, j, lam, N):
+    """Group of latent (i, j) when N consecutive wavefronts t = lam*i + j are
+    decoded together (Sec. III-D, Fig. 3): floor(t / N)."""
+    return (lam * i + j) // N

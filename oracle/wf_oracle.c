@@ -40,6 +40,17 @@
  *  - scale = max(raw scale, table[0]); index = number of the first L-1 table
  *    entries strictly below the scale;
  *  - the quantiser rounds half to even.
+ *
+ * Context approximation (Sec. III-D, Fig. 3), when group > 1: the wavefronts
+ * t = lambda*i + j (lambda = 3, or 2 for the relaxed mask; Sec. III-B) are
+ * taken N = group at a time, and all latents of group floor(t / N) are
+ * evaluated together.  A tap of the same group is not yet decoded; it is
+ * replaced, channel by channel, by the mean of the latent's in-image taps of
+ * earlier groups, or by zero when there is none (the paper fills with zero
+ * when nothing is known).  Out-of-image taps stay zero.  Reading taken where
+ * the paper says "local neighborhood": the taps of the causal mask.  The
+ * per-latent function then reads only latents of earlier groups, all of which
+ * precede it in raster order, so a raster pass computes the grouped decode.
  */
 #include <math.h>
 #include <stdint.h>
@@ -59,6 +70,7 @@ typedef struct {
     const float *w3, *b3;       /* [n3][d2], [n3]; n3 = 2M (K=1) or 9M (K=3)  */
     const float *table;         /* [L], strictly increasing                   */
     int32_t L;
+    int32_t group;              /* 0 or 1: exact; N > 1: groups of N wavefronts */
 } oracle_model;
 
 typedef struct {
@@ -112,6 +124,31 @@ static int tap_in_mask(const oracle_model *m, int dy, int dx)
     return 1;
 }
 
+static int shear_of(const oracle_model *m)
+{
+    return m->relaxed ? 2 : 3;
+}
+
+/* Status of tap (dy,dx) of latent (i,j): 0 outside the image, 1 decoded
+ * before the latent's group (its value is used), 2 in the latent's own group
+ * (filled).  Without grouping every in-image tap has status 1. */
+static int tap_status(const oracle_model *m, int i, int j, int dy, int dx)
+{
+    int ii = i + dy, jj = j + dx;
+    if (ii < 0 || ii >= m->H || jj < 0 || jj >= m->W) return 0;
+    if (m->group <= 1) return 1;
+    int lam = shear_of(m);
+    int g = (lam * i + j) / m->group;
+    int gt = (lam * ii + jj) / m->group;
+    return gt < g ? 1 : 2;
+}
+
+/* Exported for the tests: tap_status of the model's grid and grouping. */
+int oracle_tap_status(const oracle_model *m, int i, int j, int dy, int dx)
+{
+    return m ? tap_status(m, i, j, dy, dx) : -1;
+}
+
 static float lrelu(const oracle_model *m, float v)
 {
     return v >= 0.0f ? v : m->slope * v;
@@ -126,7 +163,7 @@ static size_t n3_of(const oracle_model *m)
  * The per-latent function: distribution parameters of latent (b,i,j) from the
  * current reconstruction y_hat and the hyperprior params psi.  Writes
  * mu[M], sigma[K*M], index[K*M], weight[K*M], cmean[K*M] (component-major).
- * scratch must hold 4M + d1 + d2 + n3 floats.
+ * scratch must hold 5M + d1 + d2 + n3 floats.
  */
 static void latent_params(const oracle_model *m, const float *y_hat,
                           const float *psi, int b, int i, int j,
@@ -140,15 +177,34 @@ static void latent_params(const oracle_model *m, const float *y_hat,
     float *o = h2 + m->d2;            /* [n3] */
     const size_t lat = ((size_t)b * H + i) * W + j;
 
+    /* Grouped decode: the fill value of same-group taps, per channel, the
+     * mean of the decoded in-image taps (zero when there is none). */
+    float *fill = o + n3_of(m);       /* [M] */
+    if (m->group > 1) {
+        int known = 0;
+        for (int c = 0; c < M; ++c) fill[c] = 0.0f;
+        double *sum = calloc((size_t)M, sizeof(double));
+        for (int dy = -2; dy <= 0; ++dy)
+            for (int dx = -2; dx <= 2; ++dx) {
+                if (!tap_in_mask(m, dy, dx) || tap_status(m, i, j, dy, dx) != 1) continue;
+                const float *src = y_hat + (((size_t)b * H + i + dy) * W + j + dx) * M;
+                for (int c = 0; c < M; ++c) sum[c] += (double)src[c];
+                ++known;
+            }
+        if (known > 0)
+            for (int c = 0; c < M; ++c) fill[c] = (float)(sum[c] / known);
+        free(sum);
+    }
+
     /* Context: 5x5 masked conv evaluated at (i,j), Def. 1 / Sec. III-C. */
     for (int oc = 0; oc < 2 * M; ++oc) {
         double acc = (double)m->ctx_b[oc];
         for (int dy = -2; dy <= 0; ++dy) {
             for (int dx = -2; dx <= 2; ++dx) {
                 if (!tap_in_mask(m, dy, dx)) continue;
-                int ii = i + dy, jj = j + dx;
-                if (ii < 0 || ii >= H || jj < 0 || jj >= W) continue;
-                const float *src = y_hat + (((size_t)b * H + ii) * W + jj) * M;
+                int st = tap_status(m, i, j, dy, dx);
+                if (st == 0) continue;
+                const float *src = st == 1 ? y_hat + (((size_t)b * H + i + dy) * W + j + dx) * M : fill;
                 for (int c = 0; c < M; ++c) {
                     float w = m->ctx_w[(((size_t)oc * M + c) * 5 + (dy + 2)) * 5 + (dx + 2)];
                     acc += weight_op(m, w) * act_op(m, src[c]);
@@ -218,7 +274,7 @@ static void latent_params(const oracle_model *m, const float *y_hat,
 
 static size_t scratch_floats(const oracle_model *m)
 {
-    return (size_t)4 * m->M + m->d1 + m->d2 + n3_of(m);
+    return (size_t)5 * m->M + m->d1 + m->d2 + n3_of(m);
 }
 
 static void store_params(const oracle_model *m, const oracle_out *out, size_t lat,
