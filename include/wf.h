@@ -94,6 +94,12 @@ typedef struct {
     const float *w1, *b1, *w2, *b2, *w3, *b3;
     const float *scale_table;
     int32_t L;              /* table length, 2 <= L <= 256                            */
+    int32_t group;          /* context approximation (Sec. III-D, Fig. 3): 0 or 1 decodes
+                               exactly; N > 1 decodes N consecutive wavefronts as one
+                               step, each tap in the latent's own group replaced, channel
+                               by channel, by the mean of its decoded in-image taps (zero
+                               when none is decoded).  N > 1 needs the stream or graph
+                               driver (WF_E_UNSUPPORTED otherwise).                      */
 } wf_desc;
 
 /*
@@ -114,7 +120,9 @@ typedef struct {
 typedef struct wf_plan_s *wf_plan_t;
 
 /*
- * Schedule of an H x W grid under a mask (host only; no GPU needed).
+ * Schedule of an H x W grid under a mask (host only; no GPU needed).  This is
+ * the exact schedule; wf_plan_schedule gives a plan's decoding steps, which
+ * are groups floor(t / N) under context approximation.
  * Writes step_of[i*W + j] = lambda*i + j (HOST array of H*W int32, may be
  * NULL) and *n_steps = W + lambda*(H-1), where lambda is the least integer
  * shear with lambda*di + dj > 0 for every dependence vector of the mask
@@ -139,7 +147,9 @@ int wf_validate(const wf_desc *desc);
  */
 int wf_plan(const wf_desc *desc, wf_plan_t *out);
 
-/* Copy the plan's schedule out (HOST array of H*W int32) and step count. */
+/* Copy the plan's schedule out (HOST array of H*W int32): the decoding step
+ * of every latent (its wavefront t, or its group floor(t / N) under context
+ * approximation) and the number of steps. */
 int wf_plan_schedule(wf_plan_t plan, int32_t *step_of, int32_t *n_steps);
 
 /*

@@ -45,14 +45,14 @@ struct b8x2 {   // eight activation values as bf16 pairs
     b8 hi, lo;
 };
 
-constexpr int kWaves = 4;              // waves per workgroup; they split a tile's k-blocks
+constexpr int kWaves = kJobWaves;      // waves per workgroup; they split a tile's k-blocks
 constexpr int kThreads = 64 * kWaves;
 constexpr int kSc1 = 16;   // cache-policy bits of an agent-coherent buffer access
 constexpr int kMaxPhases = 4;
 constexpr int kMaxC = kColsF32 > kColsBf16 ? kColsF32 : kColsBf16;   // most column tiles of one job (rows of the reduction buffer: kWaves * kMaxC)
 
 // Phases of a step, in order; fp32 runs PH_A..PH_C, bf16 PH_N..PH_C.
-enum { PH_N = 0, PH_A = 1, PH_B = 2, PH_C = 3 };
+enum { PH_N = 0, PH_A = 1, PH_B = 2, PH_C = 3, PH_GX = 4, PH_GA = 5 };   // PH_G*: grouped decode
 
 __device__ __forceinline__ f4 mfma_k16(f4 a, f4 b, f4 acc) {
     // Lane l supplies A[l%16][4*(l/16)+q] and B[4*(l/16)+q][l%16] for the q-th
@@ -236,6 +236,7 @@ __device__ __forceinline__ void st_pair_row(uint16_t* h, size_t row, int c, floa
 // i0 + r % n, column t - lambda*i.
 struct StepRows {
     int t, n, i0, nrows;
+    int r0;     // grouped decode: first entry of the step's rows in StepArgs::rowlat
 };
 
 struct Row {
@@ -249,6 +250,17 @@ __device__ __forceinline__ Row step_row(const StepArgs& a, const StepRows& s, in
     w.valid = r < s.nrows;
     w.b = w.i = w.j = 0;
     w.lat = 0;
+    if (a.rowlat) {
+        // grouped decode: the group's rows are listed
+        if (w.valid) {
+            const int lat = a.rowlat[s.r0 + r], hw = a.H * a.W;
+            w.b = lat / hw;
+            w.i = (lat - w.b * hw) / a.W;
+            w.j = lat - w.b * hw - w.i * a.W;
+            w.lat = (size_t)lat;
+        }
+        return w;
+    }
     if (w.valid) {
         w.b = r / s.n;
         w.i = s.i0 + (r - w.b * s.n);
@@ -271,6 +283,7 @@ __host__ __device__ __forceinline__ StepRows step_rows(int H, int W, int B, int 
     s.t = t;
     step_span(H, W, lambda, t, s.i0, s.n);
     s.nrows = B * s.n;
+    s.r0 = 0;
     return s;
 }
 
@@ -904,10 +917,173 @@ __device__ __forceinline__ void l3_job(const StepArgs& a, const StepRows& s, int
     if (jb.valid) l3_tile<P, KC, COH>(a, s, jb, sm);
 }
 
+// ---------------------------------------------------------------------------
+// Context approximation (Sec. III-D): a step is a group of N wavefronts.  A
+// tap of the latent's own group is not decoded yet and is replaced, channel by
+// channel, by the mean of the latent's decoded in-image taps (zero when none
+// is decoded); out-of-grid taps are zero.  Tap k of the mask (raster order).
+__device__ __forceinline__ void mask_tap(const StepArgs& a, int k, int& dy, int& dx) {
+    const int rw = a.row_w;
+    if (k < rw) { dy = -2; dx = k - 2; }
+    else if (k < 2 * rw) { dy = -1; dx = k - rw - 2; }
+    else { dy = 0; dx = k - 2 * rw - 2; }
+}
+
+// Job of the grouped context: k-part `part` of ctx[r][n] = sum over taps and
+// channels of W_c[n][c][tap] x_tap[r][c] for one row tile and column group.
+// The k order of the packed weights is channel-chunk-major (chunk q of kK
+// channels, then the taps), and wave w of part p takes chunk 4p + w: it loads
+// that chunk of every tap, so the fill mean of its channels is formed in
+// registers from the same loads.  The parts are summed by layer 1.
+template <class P, bool COH>
+__device__ __forceinline__ void gctx_tile(const StepArgs& a, const StepRows& s, int part, Job jb, f4 (*red)[64]) {
+    constexpr int C = P::kC, KB = P::kK, CPL = KB / 4;   // channels per lane of a chunk
+    const int wave = wave_id(), lane = threadIdx.x & 63, kq = lane >> 4;
+    const int M = a.M, Q = M / KB, nt = a.ntaps;
+    const int q = part * kWaves + wave;                  // this wave's channel chunk
+    const Row w = step_row(a, s, jb.rt * kTile + (lane & 15));
+    const int g = (a.lambda * w.i + w.j) / a.group;
+    f4 acc[C];
+#pragma unroll
+    for (int c = 0; c < C; ++c) acc[c] = zero4();
+    if (q < Q) {
+        typename P::A x[kMaxTaps];
+        float sum[CPL];
+#pragma unroll
+        for (int e = 0; e < CPL; ++e) sum[e] = 0.0f;
+        unsigned status = 0;                             // 2 bits per tap: 0 out, 1 decoded, 2 filled
+        int known = 0;
+        const int c0 = q * KB + kq * CPL;
+#pragma unroll
+        for (int k = 0; k < kMaxTaps; ++k) {
+            // (every index below is a compile-time constant, so x[] stays in registers)
+            int dy, dx;
+            mask_tap(a, k, dy, dx);
+            const int ii = w.i + dy, jj = w.j + dx;
+            const bool in = k < nt && w.valid && ii >= 0 && jj >= 0 && jj < a.W;
+            const bool dec = in && (a.lambda * ii + jj) / a.group < g;
+            status |= (in ? (dec ? 1u : 2u) : 0u) << (2 * k);
+            known += dec;
+            const size_t lat = ((size_t)w.b * a.H + ii) * a.W + jj;
+            if constexpr (P::kBf16) {
+                const size_t o = lat * 2 * M + (size_t)(c0 >> 5) * 64 + (c0 & 31);
+                x[k] = b8x2{ld8h<COH>(a.ybf, o, dec), ld8h<COH>(a.ybf, o + 32, dec)};
+            } else {
+                x[k] = ld4<COH>(a.cp->y_hat, lat * M + c0, dec);
+            }
+        }
+#pragma unroll
+        for (int k = 0; k < kMaxTaps; ++k) {
+            if constexpr (P::kBf16) {
+#pragma unroll
+                for (int e = 0; e < 8; ++e) sum[e] += (float)x[k].hi[e] + (float)x[k].lo[e];
+            } else {
+                sum[0] += x[k].x; sum[1] += x[k].y; sum[2] += x[k].z; sum[3] += x[k].w;
+            }
+        }
+        float mean[CPL];
+#pragma unroll
+        for (int e = 0; e < CPL; ++e) mean[e] = known > 0 ? sum[e] / (float)known : 0.0f;
+        typename P::A fillv;
+        if constexpr (P::kBf16) fillv = split8(f4{mean[0], mean[1], mean[2], mean[3]}, f4{mean[4], mean[5], mean[6], mean[7]});
+        else fillv = f4{mean[0], mean[1], mean[2], mean[3]};
+        const size_t ws = (size_t)nt * Q * 64;           // one column tile of the packed panel
+        const typename P::B* wp = static_cast<const typename P::B*>(a.wp_all) + (size_t)jb.ct * C * ws + lane;
+#pragma unroll
+        for (int k = 0; k < kMaxTaps; ++k) {
+            if (k >= nt) continue;                       // wave-uniform
+            const unsigned st = (status >> (2 * k)) & 3u;
+            typename P::A v = x[k];
+            if (st == 2u) v = fillv;                     // decoded taps and zeros (out of grid) as loaded
+#pragma unroll
+            for (int c = 0; c < C; ++c) acc[c] = P::mma(v, wp[c * ws + (size_t)(q * nt + k) * 64], acc[c]);
+        }
+    }
+#pragma unroll
+    for (int c = 0; c < C; ++c) red[wave * C + c][lane] = acc[c];
+    __syncthreads();
+    const int ro = wave < 4 ? jb.rt * kTile + kq * 4 + wave : s.nrows;
+    float v[C];
+#pragma unroll
+    for (int c = 0; c < C; ++c) {
+        v[c] = 0.0f;
+        if (wave < 4) {
+#pragma unroll
+            for (int w2 = 0; w2 < kWaves; ++w2) v[c] += red[w2 * C + c][lane][wave];
+        }
+    }
+    __syncthreads();
+    if (ro < s.nrows) {
+        const size_t cpart = (size_t)a.max_rows * 2 * M;
+        const size_t base = ((size_t)(s.t & 1) * a.gparts + part) * cpart;
+#pragma unroll
+        for (int c = 0; c < C; ++c) st1<COH>(a.ctxo, base + tile_idx<PF32>(ro, group_col<P>(jb.ct, c), 2 * M), v[c]);
+    }
+}
+template <class P, bool COH>
+__device__ __forceinline__ void gctx_job(const StepArgs& a, const StepRows& s, int j, int nc, f4 (*red)[64]) {
+    const int part = j / nc;
+    const Job jb = xcd_job(j - part * nc, 2 * a.M / kTile / P::kC, ntiles(s.nrows));
+    if (jb.valid) gctx_tile<P, COH>(a, s, part, jb, red);
+}
+
+// Grouped decode, layer 1 over the context (the sum of the gctx parts):
+// fp32 h1 = lrelu(P1 + W1[:, 2M:] . ctx) (context bias folded into P1, the
+// weights are the second block of the fp32 layer-1 panel); bf16 the context
+// plus its bias is carried as a pair against W1[:, 2M:].
+template <class P, bool COH>
+__device__ __forceinline__ void l1_group_tile(const StepArgs& a, const StepRows& s, Job jb, f4 (*red)[64]) {
+    constexpr int C = P::kC;
+    const int wave = wave_id(), lane = threadIdx.x & 63, kq = lane >> 4;
+    const int M = a.M;
+    const int ro = wave < 4 ? jb.rt * kTile + kq * 4 + wave : s.nrows;
+    const Row v = step_row(a, s, ro);
+    float z[C], acc[C];
+#pragma unroll
+    for (int c = 0; c < C; ++c) z[c] = ld1<COH>(a.p1, v.lat * a.Np1 + group_col<P>(jb.ct, c), v.valid);
+    const int r = jb.rt * kTile + (lane & 15);
+    const bool valid = r < s.nrows;
+    const size_t cpart = (size_t)a.max_rows * 2 * M;
+    const float* ctx = a.ctxo + (size_t)(s.t & 1) * a.gparts * cpart;
+    const int np = a.gparts;
+    if constexpr (P::kBf16) {
+        // 8 context values of row r: two 4-value chunks of the fp32 tile order
+        auto la = [&](int kb) -> b8x2 {
+            const int c0 = kb * 32 + kq * 8;
+            const size_t i0 = tile_idx<PF32>(r, c0, 2 * M), i1 = tile_idx<PF32>(r, c0 + 4, 2 * M);
+            f4 u = ld4<false>(a.bc, c0), t = ld4<false>(a.bc, c0 + 4);
+            for (int p2 = 0; p2 < np; ++p2) {
+                u += ld4<COH>(ctx, i0 + p2 * cpart, valid);
+                t += ld4<COH>(ctx, i1 + p2 * cpart, valid);
+            }
+            return split8(u, t);
+        };
+        block_tiles<PBF16>(red, a.wp_l1, 2 * M / PBF16::kK, jb.ct, la, acc);
+    } else {
+        const int kbn = a.n_new * M / kTile;             // the panel's first block (folded taps) is skipped
+        auto la = [&](int kb) -> f4 {
+            f4 u = zero4();
+            for (int p2 = 0; p2 < np; ++p2) u += ld_tile<PF32, COH>(ctx + p2 * cpart, jb.rt, 2 * M, kb - kbn, valid);
+            return u;
+        };
+        block_tiles<PF32>(red, a.wp_l1, (a.n_new * M + 2 * M) / kTile, jb.ct, la, acc, kbn);
+    }
+    if (v.valid) {
+#pragma unroll
+        for (int c = 0; c < C; ++c)
+            st_tile<P, COH>(a.h1, ro, a.Np1, group_col<P>(jb.ct, c), lrelu(acc[c] + z[c], a.slope));
+    }
+}
+
 // The main job of phase ph (sm.tab must hold the scale table for PH_C).
 template <class P, int KC, bool COH>
 __device__ __forceinline__ void phase_job(int ph, const StepArgs& a, const StepRows& s, int b, f4 (*red)[64],
                                           L3Smem<KC>& sm) {
+    if (ph == PH_GA) {
+        const Job jb = xcd_job(b, a.Np1 / kTile / P::kC, ntiles(s.nrows));
+        if (jb.valid) l1_group_tile<P, COH>(a, s, jb, red);
+        return;
+    }
     if constexpr (P::kBf16) {
         if (ph == PH_N) ctxn_job<COH>(a, s, b, red);
         else if (ph == PH_A) l1_ctx_job<COH>(a, s, b, red);

@@ -14,6 +14,7 @@ namespace wf {
 constexpr int kMaxTaps = 12;
 constexpr int kMaxNew = 2;           // taps written by the immediately preceding step
 constexpr int kTile = 16;            // MFMA tile edge (rows and columns)
+constexpr int kJobWaves = 4;         // waves of one job's workgroup
 constexpr int kCtxPartsF32 = 6;      // k-parts of the old-tap context product, fp32 operands
 constexpr int kCtxPartsBf16 = 3;     // the same, bf16 operands
 constexpr int kDfCtxParts = 3;       // the same for the dataflow driver (its context jobs run
@@ -104,6 +105,14 @@ struct StepArgs {
     // dx = -2 and is contiguous.  New taps: (-1, new_dx0) and (0, -1).
     int old_n0, old_n1, new_dx0;
     float slope;
+    // Context approximation (groups of `group` wavefronts; 1 = exact decode).
+    // A "step" is then a group; its rows are listed in rowlat (latent indices,
+    // from StepRows::r0), its context is the product over all taps (raster
+    // mask order: row_w taps in each of rows -2 and -1 from dx = -2, then
+    // (0,-2), (0,-1)) with same-group taps filled, in gparts k-parts.
+    int group, row_w, ntaps, gparts;
+    const int* rowlat;      // nullptr: rows of wavefront t by grid row
+    const void* wp_all;     // packed Wc over all taps, channel-chunk-major k   [2M/16][ntaps*M/kb]
     const void* wp_hoist;   // packed W1[:, :2M]                           [Np1/16][2M/kb]
     const float* b_hoist;   // fp32: b1 + W1[:, 2M:] . bc; bf16: b1        [Np1]
     const void* wp_l1;      // fp32: packed [W1b.Wc[new] ; W1b]            [Np1/16][(n_new*M + 2M)/16]
@@ -135,6 +144,9 @@ struct Plan {
     float slope;
     // schedule
     int lambda, T, ntaps;
+    int group;                           // wavefronts per decoding step (1: exact)
+    int steps;                           // decoding steps: T, or ceil(T / group)
+    std::vector<int> g_r0, g_n;          // grouped decode: rows of each group in rowlat
     int dy[kMaxTaps], dx[kMaxTaps];
     std::vector<int32_t> step_of;        // [H*W]
     int max_rows;

@@ -88,7 +88,7 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2))
     }
     for (int t = 0; t < T; ++t) {
         const StepRows s = step_rows(a.H, a.W, a.B, a.lambda, t);
-        StepRows s1{t + 1, 0, 0, 0};
+        StepRows s1{t + 1, 0, 0, 0, 0};
         if (t + 1 < T) s1 = step_rows(a.H, a.W, a.B, a.lambda, t + 1);
         const StepWork w = step_work<P>(a, s, s1);
         for (int ph = P::kFirst; ph < kMaxPhases; ++ph) {

@@ -84,6 +84,9 @@ static int check_desc(const wf_desc* d) {
             return fail(WF_E_INVALID, "scale table must be strictly increasing");
     }
     if (!std::isfinite(d->lrelu_slope)) return fail(WF_E_INVALID, "lrelu_slope must be finite");
+    if (d->group < 0) return fail(WF_E_INVALID, "group must be >= 0");
+    if (d->group > 1 && d->driver != WF_DRIVER_STREAM && d->driver != WF_DRIVER_GRAPH)
+        return fail(WF_E_UNSUPPORTED, "context approximation (group > 1) needs the stream or graph driver");
     if (d->M % kTile != 0) return fail(WF_E_UNSUPPORTED, "M must be a multiple of 16");
     int dy[kMaxTaps], dx[kMaxTaps];
     int nt = mask_taps(d->mask, dy, dx);
@@ -202,6 +205,8 @@ static int build_plan(const wf_desc* d, Plan* p) {
     p->lambda = least_shear(p->ntaps, p->dy, p->dx);
     const int H = p->H, W = p->W, M = p->M, lam = p->lambda;
     p->T = W + lam * (H - 1);
+    p->group = d->group > 1 ? d->group : 1;
+    p->steps = (p->T + p->group - 1) / p->group;
 
     // Wavefront steps: the latents with lambda*i + j == t; a step's rows are
     // its latents by ascending grid row, image-major.
@@ -216,6 +221,28 @@ static int build_plan(const wf_desc* d, Plan* p) {
     int maxn = 0;
     for (int t = 0; t < p->T; ++t) maxn = std::max(maxn, step_n[t]);
     p->max_rows = round16(p->B * maxn);   // whole 16-row tiles (tiled activation arrays)
+    // Grouped decode: group g holds the latents with floor(t / N) == g, listed
+    // by image, grid row and column.
+    std::vector<int32_t> rowlat;
+    if (p->group > 1) {
+        const int N = p->group;
+        p->g_r0.assign(p->steps, 0);
+        p->g_n.assign(p->steps, 0);
+        rowlat.reserve((size_t)p->B * H * W);
+        int maxg = 0;
+        for (int g = 0; g < p->steps; ++g) {
+            p->g_r0[g] = (int)rowlat.size();
+            for (int b = 0; b < p->B; ++b)
+                for (int i = 0; i < H; ++i)
+                    for (int j = std::max(0, g * N - lam * i); j < W && lam * i + j < (g + 1) * N; ++j)
+                        rowlat.push_back((int32_t)(((size_t)b * H + i) * W + j));
+            p->g_n[g] = (int)rowlat.size() - p->g_r0[g];
+            maxg = std::max(maxg, p->g_n[g]);
+        }
+        if (rowlat.size() != (size_t)p->B * H * W) return fail(WF_E_UNSUPPORTED, "internal: group rows do not cover the grid");
+        p->max_rows = round16(maxg);
+    }
+    for (size_t q = 0; q < p->step_of.size() && p->group > 1; ++q) p->step_of[q] /= p->group;
     const bool bf = p->precision == WF_BF16;
     p->Np1 = padded(p->d1, p->precision);
     p->Np2 = padded(p->d2, p->precision);
@@ -226,6 +253,10 @@ static int build_plan(const wf_desc* d, Plan* p) {
     a = StepArgs{};
     a.H = H; a.W = W; a.M = M; a.B = p->B; a.K = p->K; a.L = p->L; a.lambda = lam;
     a.Np1 = Np1; a.Np2 = p->Np2; a.n3 = p->n3; a.slope = p->slope; a.max_rows = p->max_rows;
+    a.group = p->group;
+    a.ntaps = p->ntaps;
+    a.row_w = d->mask == WF_MASK_RELAXED ? 4 : 5;
+    a.gparts = (M / kblock(p->precision) + kJobWaves - 1) / kJobWaves;   // one channel chunk per wave of a part
 
     // Split the taps by age (delta = steps between producer and consumer).
     std::vector<int> new_taps, old_taps;
@@ -275,6 +306,22 @@ static int build_plan(const wf_desc* d, Plan* p) {
             return d->ctx_w[(((size_t)n * M + c) * 5 + (p->dy[taps[o]] + 2)) * 5 + (p->dx[taps[o]] + 2)];
         };
     };
+    // all taps, channel-chunk-major k (chunk of kb channels, then the taps):
+    // the grouped decode's context product
+    auto wc_all = [&](int k, int n) {
+        const int per = kbk * p->ntaps;
+        const int q = k / per, rem = k - q * per, tap = rem / kbk, c = q * kbk + rem % kbk;
+        return d->ctx_w[(((size_t)n * M + c) * 5 + (p->dy[tap] + 2)) * 5 + (p->dx[tap] + 2)];
+    };
+    if (p->group > 1) {
+        const int ka = p->ntaps * M;
+        rc = bf ? put(&a.wp_all, 2 * M, ka, pack_panel_bf16(ka, 2 * M, ka, 2 * M, wc_all))
+                : put(&a.wp_all, 2 * M, ka, pack_panel(ka, 2 * M, ka, 2 * M, wc_all));
+        if (rc != WF_OK) return rc;
+        int32_t* rl = nullptr;
+        if ((rc = upload(p, &rl, rowlat.data(), rowlat.size())) != WF_OK) return rc;
+        a.rowlat = rl;
+    }
     auto w1a = [&](int k, int n) { return d->w1[(size_t)n * 4 * M + k]; };
     auto w1b = [&](int k, int n) { return d->w1[(size_t)n * 4 * M + 2 * M + k]; };
     auto w2f = [&](int k, int n) { return d->w2[(size_t)n * d1 + k]; };
@@ -343,7 +390,8 @@ static int build_plan(const wf_desc* d, Plan* p) {
         a.h2b = h2b;
     }
     if ((rc = alloc(p, &a.p1, nlat * Np1)) != WF_OK) return rc;
-    if ((rc = alloc(p, &a.ctxo, (size_t)2 * kCtxPartsMax * R * 2 * M)) != WF_OK) return rc;
+    const int nparts = std::max(kCtxPartsMax, p->group > 1 ? a.gparts : 0);
+    if ((rc = alloc(p, &a.ctxo, (size_t)2 * nparts * R * 2 * M)) != WF_OK) return rc;
     if (bf) {
         if ((rc = alloc(p, &a.ctxb, R * 2 * 2 * M)) != WF_OK) return rc;
         if ((rc = alloc(p, &a.ybf, nlat * 2 * M)) != WF_OK) return rc;
@@ -446,7 +494,7 @@ int wf_plan_schedule(wf_plan_t plan, int32_t* step_of, int32_t* n_steps) {
     if (!plan || !n_steps) return fail(WF_E_INVALID, "plan or n_steps is NULL");
     Plan* p = reinterpret_cast<Plan*>(plan);
     if (step_of) std::copy(p->step_of.begin(), p->step_of.end(), step_of);
-    *n_steps = p->T;
+    *n_steps = p->steps;
     return WF_OK;
 }
 

@@ -17,6 +17,13 @@ __global__ __launch_bounds__(kThreads) void k_ctxo(StepRows s1, int j0, int nc, 
     ctxo_job<P, false>(a, s1, j0 + blockIdx.x, nc, red);
 }
 
+// Grouped decode: the context jobs of group s (all parts).
+template <class P>
+__global__ __launch_bounds__(kThreads) void k_gctx(StepRows s, int nc, StepArgs a) {
+    __shared__ f4 red[kWaves * kMaxC][64];
+    gctx_job<P, false>(a, s, blockIdx.x, nc, red);
+}
+
 // Phase ph of step s (blocks [0, nb)), then old-tap context jobs [j0, ...)
 // of step s1.
 template <class P, int KC>
@@ -59,13 +66,36 @@ int enqueue_hoist(Plan& p, hipStream_t stream) {
 
 // Rows of step t, or an empty step past the end.
 static StepRows rows_of(const Plan& p, int t) {
-    if (t >= p.T) return StepRows{t, 0, 0, 0};
+    if (t >= p.T) return StepRows{t, 0, 0, 0, 0};
     return step_rows(p.H, p.W, p.B, p.lambda, t);
+}
+
+// Grouped decode: per group, the context (with fill), then layers 1-3.
+template <class P, int KC>
+static void launch_groups(Plan& p, hipStream_t stream) {
+    const StepArgs& a = p.args;
+    launch_hoist<P>(p, stream);
+    const int ncx = 2 * a.M / kTile / P::kC;
+    for (int g = 0; g < p.steps; ++g) {
+        const StepRows s{g, 0, 0, p.g_n[g], p.g_r0[g]};
+        const int nrt = ntiles(s.nrows);
+        const int nc = xcd_blocks(ncx, nrt);
+        hipLaunchKernelGGL(k_gctx<P>, dim3(nc * a.gparts), dim3(kThreads), 0, stream, s, nc, a);
+        const int nb[3] = {xcd_blocks(a.Np1 / kTile / P::kC, nrt), phase_blocks<P>(a, s, PH_B),
+                           phase_blocks<P>(a, s, PH_C)};
+        const int ph[3] = {PH_GA, PH_B, PH_C};
+        for (int k = 0; k < 3; ++k)
+            hipLaunchKernelGGL((k_phase<P, KC>), dim3(nb[k]), dim3(kThreads), 0, stream, ph[k], s, s, nb[k], 0, 0, a);
+    }
 }
 
 template <class P, int KC>
 static void launch_steps(Plan& p, hipStream_t stream) {
     const StepArgs& a = p.args;
+    if (p.group > 1) {
+        launch_groups<P, KC>(p, stream);
+        return;
+    }
     launch_hoist<P>(p, stream);
     {
         const StepRows s0 = rows_of(p, 0);

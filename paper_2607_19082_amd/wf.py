@@ -40,6 +40,7 @@ class Desc(ctypes.Structure):
         ("w2", ctypes.c_void_p), ("b2", ctypes.c_void_p),
         ("w3", ctypes.c_void_p), ("b3", ctypes.c_void_p),
         ("scale_table", ctypes.c_void_p), ("L", ctypes.c_int32),
+        ("group", ctypes.c_int32),
     ]
 
 
@@ -94,7 +95,7 @@ def schedule(H, W, mask="full"):
 
 
 def make_desc(weights, table, H, W, B=1, K=1, mask="full", precision="fp32", driver="stream",
-              slope=0.01):
+              slope=0.01, group=1):
     """Build a Desc plus the host arrays it points to (keep both alive)."""
     arrs = {k: np.ascontiguousarray(v, dtype=np.float32) for k, v in weights.items()}
     arrs["table"] = np.ascontiguousarray(table, dtype=np.float32)
@@ -105,7 +106,7 @@ def make_desc(weights, table, H, W, B=1, K=1, mask="full", precision="fp32", dri
              arrs["w1"].ctypes.data, arrs["b1"].ctypes.data,
              arrs["w2"].ctypes.data, arrs["b2"].ctypes.data,
              arrs["w3"].ctypes.data, arrs["b3"].ctypes.data,
-             arrs["table"].ctypes.data, len(arrs["table"]))
+             arrs["table"].ctypes.data, len(arrs["table"]), group)
     return d, arrs
 
 
@@ -125,8 +126,9 @@ class Plan:
     current) torch stream."""
 
     def __init__(self, weights, table, H, W, B=1, K=1, mask="full", precision="fp32",
-                 driver="stream", slope=0.01):
-        self.desc, self._arrs = make_desc(weights, table, H, W, B, K, mask, precision, driver, slope)
+                 driver="stream", slope=0.01, group=1):
+        self.desc, self._arrs = make_desc(weights, table, H, W, B, K, mask, precision, driver, slope, group)
+        self.group = group
         self.H, self.W, self.B, self.K = H, W, B, K
         self.M = self.desc.M
         h = ctypes.c_void_p()

@@ -117,6 +117,16 @@ def test_validate(lib):
     d, keep = _desc()
     d.driver = 9
     assert wf.validate(d) == wf.WF_E_INVALID
+    # context approximation: group size >= 0; groups need a per-step-launch driver
+    d, keep = _desc()
+    d.group = -1
+    assert wf.validate(d) == wf.WF_E_INVALID
+    for drv, want in (("stream", wf.WF_OK), ("graph", wf.WF_OK), ("persistent", wf.WF_E_UNSUPPORTED),
+                      ("dataflow", wf.WF_E_UNSUPPORTED)):
+        d, keep = _desc()
+        d.driver = wf.DRIVER[drv]
+        d.group = 4
+        assert wf.validate(d) == want, drv
     t = keep["table"]
     t[5] = t[4]
     assert wf.validate(d) == wf.WF_E_INVALID
