@@ -8,17 +8,15 @@
 //
 // Jobs (the same tile bodies as the other drivers, with agent-coherent
 // exchange), per step t and 16-row tile rt:
-//   CTX(t)   old-tap context k-parts of step t's latents (fp32: all parts but
-//            the last; bf16: all)            reads y_hat of steps <= t-2
-//   CTXL(t)  fp32: the last part, which adds the others in
-//   N(t)     bf16: the context vector       reads CTX(t), y_hat of step t-1
-//   A(t)     layer 1                         reads CTXL(t) (fp32: and y_hat of
-//                                            step t-1) or N(t) (bf16)
+//   CTX(t)   old-tap context k-parts of step t's latents, all but the last
+//                                            reads y_hat of steps <= t-2
+//   CTXL(t)  the last part, which adds the others in
+//   A(t)     layer 1                         reads CTXL(t) and y_hat of step t-1
 //   B(t)     layer 2                         reads A(t)
 //   C0(t)    layer 3, mean columns: writes mean and y_hat
 //   C1(t)    layer 3, scale columns: writes scale and index
 // The plan lists them in a topological order (every dependency of a job
-// comes earlier in the list), split into a critical list (N, A, B, C0, C1)
+// comes earlier in the list), split into a critical list (A, B, C0, C1)
 // and a context list (CTX, CTXL) per XCD class (the class of a job is its
 // column tile mod 8, as in the other drivers).  Workgroups [0, ncrit) form the
 // critical pool, the rest the context pool; workgroup g of class x = g mod 8
@@ -33,19 +31,18 @@
 // Ordering argument (why the waits below suffice; "C0(s) done" means every
 // C0 job of step s has finished, which transitively means everything of
 // every earlier step that C0 depends on):
-//   - y_hat is written once per latent by C0.  A(t) (fp32) and N(t) (bf16)
-//     read the two newest taps, from step t-1: they wait for C0(t-1).  CTX(t)
-//     reads taps of steps <= t-2: it waits for C0(t-2).  C0(s) done implies
-//     C0(s-1) done (C0(s) <- B(s) <- A(s) <- C0(s-1), bf16 through N(s)).
+//   - y_hat is written once per latent by C0.  A(t) reads the two newest taps,
+//     from step t-1: it waits for C0(t-1).  CTX(t) reads taps of steps
+//     <= t-2: it waits for C0(t-2).  C0(s) done implies C0(s-1) done
+//     (C0(s) <- B(s) <- A(s) <- C0(s-1)).
 //   - h1 (one buffer) is rewritten by A(t); its readers B(t-1) are done once
-//     C0(t-1) is (C0(t-1) <- B(t-1)).  The bf16 context vector (one buffer)
-//     is rewritten by N(t); its readers A(t-1) are done once C0(t-1) is.
+//     C0(t-1) is (C0(t-1) <- B(t-1)).
 //   - h2 is double-buffered by step parity: B(t) rewrites what C0(t-2) and
 //     C1(t-2) read; C0(t-2) is implied by B(t)'s wait for A(t), C1(t-2) is
 //     waited for explicitly.
 //   - The old-tap context is double-buffered by step parity: CTX(t) and
-//     CTXL(t) rewrite what A(t-2) / CTXL(t-2) (bf16: N(t-2)) read, which are
-//     done once C0(t-2) is.
+//     CTXL(t) rewrite what A(t-2) / CTXL(t-2) read, which are done once C0(t-2)
+//     is.
 //   - psi's hoisted part P1 is written by the pre-loop kernel before the launch.
 #include "wf_device.h"
 
@@ -123,7 +120,7 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2))
     const int nct_n = 2 * a.M / kTile / P::kC;           // column groups of the context products
     const int nct_ctx = a.n_old > 0 ? nct_n : 0;         // (the old-tap part exists unless no tap is old)
     const int nct_a = a.Np1 / kTile / P::kC, nct_b = a.Np2 / kTile / P::kC;
-    const int NPX = P::kBf16 ? a.ctx_parts : a.ctx_parts - 1;   // CTX parts
+    const int NPX = a.ctx_parts - 1;                     // CTX parts (the last one is CTXL)
     for (int p = lw; p < n; p += nwg) {
         const int2 c = list[p];
         const int t = c.x, kind = c.y & 15, part = (c.y >> 4) & 15, rt = (c.y >> 8) & 255, ct = c.y >> 16;
@@ -141,17 +138,9 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2))
             case JK_CTXL:
                 w[nw++] = DfWait{df_group(d, t, JK_CTX, rt), 0, nct_ctx, NPX};
                 break;
-            case JK_N:
-                w[nw++] = DfWait{df_group(d, t, JK_CTX, rt), 0, nct_ctx, NPX};
-                if (t >= 1) step_total(t - 1, JK_C0, 0, G);
-                break;
             case JK_A:
-                if constexpr (P::kBf16) {
-                    w[nw++] = DfWait{df_group(d, t, JK_N, rt), 0, nct_n, 1};
-                } else {
-                    w[nw++] = DfWait{df_group(d, t, JK_CTXL, rt), 0, nct_ctx, 1};
-                    if (t >= 1) step_total(t - 1, JK_C0, 0, G);
-                }
+                w[nw++] = DfWait{df_group(d, t, JK_CTXL, rt), 0, nct_ctx, 1};
+                if (t >= 1) step_total(t - 1, JK_C0, 0, G);
                 break;
             case JK_B:
                 w[nw++] = DfWait{df_group(d, t, JK_A, rt), 0, nct_a, 1};
@@ -172,11 +161,8 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2))
             case JK_CTXL:
                 ctxo_tile<P, true>(a, s, kind == JK_CTX ? part : a.ctx_parts - 1, jb, red);
                 break;
-            case JK_N:
-                if constexpr (P::kBf16) ctxn_tile<true>(a, s, jb, red);
-                break;
             case JK_A:
-                if constexpr (P::kBf16) l1_ctx_tile<true>(a, s, jb, red);
+                if constexpr (P::kBf16) l1_fold_bf16_tile<true>(a, s, jb, red);
                 else l1_fold_tile<true>(a, s, jb, red);
                 break;
             case JK_B:
@@ -220,7 +206,7 @@ int build_dataflow(Plan& p, std::vector<int2>& lists, DfArgs& d) {
     const bool bf = p.precision == WF_BF16;
     const int C = bf ? kColsBf16 : kColsF32;
     const int parts = a.ctx_parts;
-    const int npx = bf ? parts : parts - 1;
+    const int npx = parts - 1;
     const int nct_n = 2 * p.M / kTile / C;
     const int nct_ctx = a.n_old > 0 ? nct_n : 0;
     const int nct_a = p.Np1 / kTile / C, nct_b = p.Np2 / kTile / C, nct_c = 2 * (p.M / kTile);
@@ -238,13 +224,12 @@ int build_dataflow(Plan& p, std::vector<int2>& lists, DfArgs& d) {
         for (int part = 0; part < npx; ++part) tiles(t, JK_CTX, part, 0, nct_ctx);
     };
     ctx(0);
-    if (!bf) tiles(0, JK_CTXL, 0, 0, nct_ctx);
+    tiles(0, JK_CTXL, 0, 0, nct_ctx);
     for (int t = 0; t < p.T; ++t) {
-        if (bf) tiles(t, JK_N, 0, 0, nct_n);
         tiles(t, JK_A, 0, 0, nct_a);
         if (t + 1 < p.T) ctx(t + 1);
         tiles(t, JK_B, 0, 0, nct_b);
-        if (!bf && t + 1 < p.T) tiles(t + 1, JK_CTXL, 0, 0, nct_ctx);
+        if (t + 1 < p.T) tiles(t + 1, JK_CTXL, 0, 0, nct_ctx);
         tiles(t, JK_C0, 0, 0, nct_c / 2);
         tiles(t, JK_C1, 0, nct_c / 2, nct_c);
     }

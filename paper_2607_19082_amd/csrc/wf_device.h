@@ -11,16 +11,14 @@
 // (its inputs were all written by step t-1 or earlier).
 //
 // bf16 operands (weights rounded to bf16, every activation carried as a pair
-// of bf16 values hi = bf16(x), lo = bf16(x - hi), fp32 accumulation): the
-// context vector is an activation operand of its own, so it is formed before
-// layer 1 and the fold above does not apply; four phases:
-//   phase N  ctx = pair(bc + ctx_old(t) + Wc[new] . pair(y_hat[new taps]))
-//   phase A  h1  = pair(lrelu(P1 + W1b . ctx)),  P1 = b1 + W1[:, :2M] . pair(psi)
-//   phase B  h2  = pair(lrelu(W2 . h1 + b2))
-//   phase C  as above; also keeps the pair form of y_hat for the tap gathers.
-// Pair arrays: see tile_idx and st_pair_row.
-// In both, the k-parts (P::kParts) of ctx_old(t+1) ride along with the phases
-// of step t, spread to even out their work (see ctxo_split).
+// of bf16 values hi = bf16(x), lo = bf16(x - hi), fp32 accumulation): the same
+// three phases; F_new is formed from the bf16 weights and carried as a bf16
+// pair as well, so the fold adds no coarse rounding, and phase C also keeps the
+// pair form of y_hat for the tap gathers.  Pair arrays: see tile_idx and
+// st_pair_row.
+// The last of the P::kParts k-parts of ctx_old(t+1) adds the others in and
+// runs in phase C; the other parts ride along with the phases of step t,
+// spread to even out their work (see step_work).
 //
 // Every product runs on MFMA: fp32 v_mfma_f32_16x16x4f32 (four chained per
 // 16 values of k) or bf16 v_mfma_f32_16x16x32_bf16.  Each wave issues all
@@ -51,8 +49,8 @@ constexpr int kSc1 = 16;   // cache-policy bits of an agent-coherent buffer acce
 constexpr int kMaxPhases = 4;
 constexpr int kMaxC = kColsF32 > kColsBf16 ? kColsF32 : kColsBf16;   // most column tiles of one job (rows of the reduction buffer: kWaves * kMaxC)
 
-// Phases of a step, in order; fp32 runs PH_A..PH_C, bf16 PH_N..PH_C.
-enum { PH_N = 0, PH_A = 1, PH_B = 2, PH_C = 3, PH_GX = 4, PH_GA = 5 };   // PH_G*: grouped decode
+// Phases of a step, in order: PH_A..PH_C (the grouped decode: PH_GX, PH_GA, PH_B, PH_C).
+enum { PH_A = 1, PH_B = 2, PH_C = 3, PH_GX = 4, PH_GA = 5 };   // PH_G*: grouped decode
 
 __device__ __forceinline__ f4 mfma_k16(f4 a, f4 b, f4 acc) {
     // Lane l supplies A[l%16][4*(l/16)+q] and B[4*(l/16)+q][l%16] for the q-th
@@ -88,7 +86,7 @@ struct PBF16 {
     using B = b8;
     static constexpr int kK = 32;
     static constexpr bool kBf16 = true;
-    static constexpr int kFirst = PH_N;
+    static constexpr int kFirst = PH_A;
     static constexpr int kC = kColsBf16;
     static constexpr int kParts = kCtxPartsBf16;
     static constexpr int kKbw = 10;
@@ -323,7 +321,6 @@ __host__ __device__ __forceinline__ int ntiles(int n) { return (n + kTile - 1) /
 template <class P>
 __host__ __device__ __forceinline__ int phase_cols(const StepArgs& a, int ph) {
     switch (ph) {
-        case PH_N: return 2 * a.M / kTile / P::kC;
         case PH_A: return a.Np1 / kTile / P::kC;
         case PH_B: return a.Np2 / kTile / P::kC;
         default: return 2 * a.M / kTile;   // PH_C: value group x channel tile
@@ -367,12 +364,12 @@ struct StepWork {
 template <class P>
 __host__ __device__ __forceinline__ StepWork step_work(const StepArgs& a, const StepRows& s, const StepRows& s1) {
     // phases that share the context jobs, and the jobs they share
-    constexpr int last = P::kBf16 ? kMaxPhases : PH_C;
+    constexpr int last = PH_C;
     constexpr int nph = last - P::kFirst;
     StepWork w;
     w.nc = ctxo_blocks<P>(a, s1);
     const int G = a.slots;
-    int left = (P::kBf16 ? P::kParts : P::kParts - 1) * w.nc;
+    int left = (P::kParts - 1) * w.nc;
     // an even share per phase first (less contention), within free slots
     const int share = ((left + nph - 1) / nph + kXcds - 1) / kXcds * kXcds;
     int take[kMaxPhases], free_slots[kMaxPhases];
@@ -401,7 +398,7 @@ __host__ __device__ __forceinline__ StepWork step_work(const StepArgs& a, const 
             take[ph] += e;
             left -= e;
         }
-        if (!P::kBf16 && ph == PH_C) take[ph] = w.nc;   // the last part
+        if (ph == PH_C) take[ph] = w.nc;   // the last part
         w.cut[ph + 1] = w.cut[ph] + take[ph];
     }
     return w;
@@ -621,7 +618,7 @@ __device__ __forceinline__ void ctxo_tile(const StepArgs& a, const StepRows& s, 
 #pragma unroll
     for (int c = 0; c < C; ++c) {
         prev[c] = 0.0f;
-        if (!P::kBf16 && part == NP - 1) {
+        if (part == NP - 1) {
             const size_t e = q + tile_idx<PF32>(ro, group_col<P>(jb.ct, c), 2 * M);
 #pragma unroll
             for (int p2 = 0; p2 < NP - 1; ++p2) prev[c] += ld1<COH>(a.ctxo, e + p2 * cpart, vo);
@@ -680,67 +677,106 @@ __device__ __forceinline__ void l1_fold_job(const StepArgs& a, const StepRows& s
     if (jb.valid) l1_fold_tile<COH>(a, s, jb, red);
 }
 
-// Phase N, bf16: the context vector of step s, as bf16 pairs.
+// Phase A, bf16: layer 1 of step s over [new taps ; old-tap context], with the
+// new taps' context folded into layer 1 as for fp32: F = W1[:, 2M:] . Wc[new]
+// is formed from the bf16 weights in fp64 at plan time and carried as a bf16
+// pair F_hi + F_lo (panels wp_new, wp_new_lo), so the fold adds no coarse
+// rounding; a new-tap k-block is hi.F_hi + lo.F_hi + hi.F_lo.  The old-tap
+// context (its last k-part holds the whole sum) is carried as a pair against
+// W1[:, 2M:]; the context bias is folded into P1.
 template <bool COH>
-__device__ __forceinline__ void ctxn_tile(const StepArgs& a, const StepRows& s, Job jb, f4 (*red)[64]) {
-    constexpr int C = PBF16::kC;
-    const int M = a.M;
-    const int wave = wave_id(), lane = threadIdx.x & 63, kq = lane >> 4;
-    // epilogue operands first: bias and the old-tap context parts
-    const int ro = wave < 4 ? jb.rt * kTile + kq * 4 + wave : s.nrows;
-    const bool vo = ro < s.nrows;
-    const size_t cpart = (size_t)a.max_rows * 2 * M;
-    const int NP = a.ctx_parts;
-    const size_t cq = (size_t)(s.t & 1) * NP * cpart;
-    float z[C], acc[C];
-#pragma unroll
-    for (int c = 0; c < C; ++c) {
-        const int n = group_col<PBF16>(jb.ct, c);
-        const size_t e = cq + tile_idx<PF32>(ro, n, 2 * M);
-        z[c] = a.bc[n];
-#pragma unroll
-        for (int part = 0; part < NP; ++part) z[c] += ld1<COH>(a.ctxo, e + part * cpart, vo && a.n_old > 0);
-    }
-    const Row w = step_row(a, s, jb.rt * kTile + (lane & 15));
-    auto la = [&](int kb) { return ld_tap<PBF16, COH>(a, w, kb, kq, false); };
-    block_tiles<PBF16>(red, a.wp_new, a.n_new * M / PBF16::kK, jb.ct, la, acc);
-    if (vo) {
-#pragma unroll
-        for (int c = 0; c < C; ++c)
-            st_tile<PBF16, COH>(a.ctxb, ro, 2 * M, group_col<PBF16>(jb.ct, c), acc[c] + z[c]);
-    }
-}
-template <bool COH>
-__device__ __forceinline__ void ctxn_job(const StepArgs& a, const StepRows& s, int b, f4 (*red)[64]) {
-    const Job jb = xcd_job(b, 2 * a.M / kTile / PBF16::kC, ntiles(s.nrows));
-    if (jb.valid) ctxn_tile<COH>(a, s, jb, red);
-}
-
-// Phase A, bf16: layer 1 of step s over the context vector.
-template <bool COH>
-__device__ __forceinline__ void l1_ctx_tile(const StepArgs& a, const StepRows& s, Job jb, f4 (*red)[64]) {
-    constexpr int C = PBF16::kC;
+__device__ __forceinline__ void l1_fold_bf16_tile(const StepArgs& a, const StepRows& s, Job jb, f4 (*red)[64]) {
+    constexpr int C = PBF16::kC, KBW = 5;
     const int wave = wave_id(), lane = threadIdx.x & 63, kq = lane >> 4;
     const int M = a.M;
+    // epilogue operands first: the hoisted part of this wave's row
     const int ro = wave < 4 ? jb.rt * kTile + kq * 4 + wave : s.nrows;
     const Row v = step_row(a, s, ro);
-    float z[C], acc[C];
+    float z[C];
 #pragma unroll
     for (int c = 0; c < C; ++c) z[c] = ld1<COH>(a.p1, v.lat * a.Np1 + group_col<PBF16>(jb.ct, c), v.valid);
     const int r = jb.rt * kTile + (lane & 15);
-    const bool valid = r < s.nrows;
-    auto la = [&](int kb) { return ld_tile<PBF16, COH>(a.ctxb, jb.rt, 2 * M, kb, valid); };
-    block_tiles<PBF16>(red, a.wp_l1, 2 * M / PBF16::kK, jb.ct, la, acc);
+    const Row w = step_row(a, s, r);
+    const int kbn = a.n_new * M / PBF16::kK, kbc = 2 * M / PBF16::kK, nkb = kbn + kbc;
+    const int per = (nkb + kWaves - 1) / kWaves;
+    const int kb0 = min(nkb, wave * per), kb1 = min(nkb, kb0 + per);
+    const int NP = a.ctx_parts;
+    const size_t cpart = (size_t)a.max_rows * 2 * M;
+    const float* ctx = a.ctxo + ((size_t)(s.t & 1) * NP + NP - 1) * cpart;
+    f4 acc[C];
+#pragma unroll
+    for (int c = 0; c < C; ++c) acc[c] = zero4();
+    {   // new taps against the pair weights
+        const b8* wh = static_cast<const b8*>(a.wp_new) + (size_t)jb.ct * C * kbn * 64 + lane;
+        const b8* wl = static_cast<const b8*>(a.wp_new_lo) + (size_t)jb.ct * C * kbn * 64 + lane;
+        const int e1 = min(kb1, kbn);
+        for (int kc = kb0; kc < e1; kc += KBW) {
+            b8x2 av[KBW];
+            b8 bh[KBW][C], bl[KBW][C];
+#pragma unroll
+            for (int u = 0; u < KBW; ++u) {
+                const int k = min(kc + u, e1 - 1);
+                av[u] = ld_tap<PBF16, COH>(a, w, k, kq, false);
+#pragma unroll
+                for (int c = 0; c < C; ++c) {
+                    bh[u][c] = wh[(size_t)(c * kbn + k) * 64];
+                    bl[u][c] = wl[(size_t)(c * kbn + k) * 64];
+                }
+            }
+#pragma unroll
+            for (int u = 0; u < KBW; ++u)
+                if (kc + u < e1)
+#pragma unroll
+                    for (int c = 0; c < C; ++c) {
+                        acc[c] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av[u].hi, bh[u][c], acc[c], 0, 0, 0);
+                        acc[c] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av[u].lo, bh[u][c], acc[c], 0, 0, 0);
+                        acc[c] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av[u].hi, bl[u][c], acc[c], 0, 0, 0);
+                    }
+        }
+    }
+    {   // the old-tap context: 8 values of row r, two 4-value chunks of the fp32 tile order
+        const b8* w1 = static_cast<const b8*>(a.wp_l1) + (size_t)jb.ct * C * kbc * 64 + lane;
+        for (int kc = max(kb0, kbn); kc < kb1; kc += KBW) {
+            b8x2 av[KBW];
+            b8 bv[KBW][C];
+#pragma unroll
+            for (int u = 0; u < KBW; ++u) {
+                const int kk = min(kc + u, kb1 - 1) - kbn, c0 = kk * PBF16::kK + kq * 8;
+                av[u] = split8(ld4<COH>(ctx, tile_idx<PF32>(r, c0, 2 * M), w.valid),
+                               ld4<COH>(ctx, tile_idx<PF32>(r, c0 + 4, 2 * M), w.valid));
+#pragma unroll
+                for (int c = 0; c < C; ++c) bv[u][c] = w1[(size_t)(c * kbc + kk) * 64];
+            }
+#pragma unroll
+            for (int u = 0; u < KBW; ++u)
+                if (kc + u < kb1)
+#pragma unroll
+                    for (int c = 0; c < C; ++c) acc[c] = PBF16::mma(av[u], bv[u][c], acc[c]);
+        }
+    }
+#pragma unroll
+    for (int c = 0; c < C; ++c) red[wave * C + c][lane] = acc[c];
+    __syncthreads();
+    float o[C];
+#pragma unroll
+    for (int c = 0; c < C; ++c) {
+        o[c] = 0.0f;
+        if (wave < 4) {
+#pragma unroll
+            for (int w2 = 0; w2 < kWaves; ++w2) o[c] += red[w2 * C + c][lane][wave];
+        }
+    }
+    __syncthreads();
     if (v.valid) {
 #pragma unroll
         for (int c = 0; c < C; ++c)
-            st_tile<PBF16, COH>(a.h1, ro, a.Np1, group_col<PBF16>(jb.ct, c), lrelu(acc[c] + z[c], a.slope));
+            st_tile<PBF16, COH>(a.h1, ro, a.Np1, group_col<PBF16>(jb.ct, c), lrelu(o[c] + z[c], a.slope));
     }
 }
 template <bool COH>
-__device__ __forceinline__ void l1_ctx_job(const StepArgs& a, const StepRows& s, int b, f4 (*red)[64]) {
+__device__ __forceinline__ void l1_fold_bf16_job(const StepArgs& a, const StepRows& s, int b, f4 (*red)[64]) {
     const Job jb = xcd_job(b, a.Np1 / kTile / PBF16::kC, ntiles(s.nrows));
-    if (jb.valid) l1_ctx_tile<COH>(a, s, jb, red);
+    if (jb.valid) l1_fold_bf16_tile<COH>(a, s, jb, red);
 }
 
 // Phase B: layer 2.
@@ -1028,9 +1064,9 @@ __device__ __forceinline__ void gctx_job(const StepArgs& a, const StepRows& s, i
 }
 
 // Grouped decode, layer 1 over the context (the sum of the gctx parts):
-// fp32 h1 = lrelu(P1 + W1[:, 2M:] . ctx) (context bias folded into P1, the
-// weights are the second block of the fp32 layer-1 panel); bf16 the context
-// plus its bias is carried as a pair against W1[:, 2M:].
+// h1 = lrelu(P1 + W1[:, 2M:] . ctx), the context bias folded into P1 (fp32:
+// the weights are the second block of the layer-1 panel; bf16: the context is
+// carried as a pair).
 template <class P, bool COH>
 __device__ __forceinline__ void l1_group_tile(const StepArgs& a, const StepRows& s, Job jb, f4 (*red)[64]) {
     constexpr int C = P::kC;
@@ -1051,7 +1087,7 @@ __device__ __forceinline__ void l1_group_tile(const StepArgs& a, const StepRows&
         auto la = [&](int kb) -> b8x2 {
             const int c0 = kb * 32 + kq * 8;
             const size_t i0 = tile_idx<PF32>(r, c0, 2 * M), i1 = tile_idx<PF32>(r, c0 + 4, 2 * M);
-            f4 u = ld4<false>(a.bc, c0), t = ld4<false>(a.bc, c0 + 4);
+            f4 u = zero4(), t = zero4();
             for (int p2 = 0; p2 < np; ++p2) {
                 u += ld4<COH>(ctx, i0 + p2 * cpart, valid);
                 t += ld4<COH>(ctx, i1 + p2 * cpart, valid);
@@ -1085,8 +1121,7 @@ __device__ __forceinline__ void phase_job(int ph, const StepArgs& a, const StepR
         return;
     }
     if constexpr (P::kBf16) {
-        if (ph == PH_N) ctxn_job<COH>(a, s, b, red);
-        else if (ph == PH_A) l1_ctx_job<COH>(a, s, b, red);
+        if (ph == PH_A) l1_fold_bf16_job<COH>(a, s, b, red);
         else if (ph == PH_B) l2_job<P, COH>(a, s, b, red);
         else l3_job<P, KC, COH>(a, s, b, sm);
     } else {

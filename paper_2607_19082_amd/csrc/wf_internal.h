@@ -30,7 +30,7 @@ constexpr int kBufBytes = 0x7fff0000; // window of a raw buffer access (arrays m
 constexpr int kDfSlotWords = 16;     // dataflow counter slots: one per 64 bytes
 
 // Job kinds of the dataflow driver (see wf_dataflow.hip).
-enum JobKind { JK_CTX = 0, JK_CTXL = 1, JK_N = 2, JK_A = 3, JK_B = 4, JK_C0 = 5, JK_C1 = 6, kJobKinds = 7 };
+enum JobKind { JK_CTX = 0, JK_CTXL = 1, JK_A = 2, JK_B = 3, JK_C0 = 4, JK_C1 = 5, kJobKinds = 6 };
 
 // Column tiles ct in [lo, hi) with ct % 8 == x.
 __host__ __device__ __forceinline__ int cnt_range(int lo, int hi, int x) {
@@ -83,13 +83,12 @@ struct CallPtrs {
 // y_hat of steps <= t-1, so it is computed during step t, off the critical
 // path, in k-parts.
 //
-// fp32: layer 1 of step t reads [new taps (n_new*M) ; old-tap context (2M)]
+// Layer 1 of step t reads [new taps (n_new*M) ; old-tap context (2M)]
 // against [W1[:, 2M:] . Wc[new taps] ; W1[:, 2M:]] (the new taps' conv and the
 // context half of layer 1 are both linear, so their product is folded at plan
-// time; the context bias is folded into the hoisted part).
-// bf16: the context vector is an activation operand of its own (a bf16
-// pair); it is formed from the new taps against Wc[new taps], plus the bias
-// and the old-tap context, and layer 1 reads it against W1[:, 2M:].
+// time; the context bias is folded into the hoisted part).  With bf16
+// operands the folded block is formed from the bf16 weights and kept as a
+// bf16 pair (wp_new + wp_new_lo), the rest of the panel is wp_l1.
 //
 // Packed weights (wp_*) hold 16-byte lane operands per (column tile, k-block):
 // fp32 k-blocks of 16, bf16 k-blocks of 32.  Np1, Np2 are d1, d2 rounded up to
@@ -114,11 +113,11 @@ struct StepArgs {
     const int* rowlat;      // nullptr: rows of wavefront t by grid row
     const void* wp_all;     // packed Wc over all taps, channel-chunk-major k   [2M/16][ntaps*M/kb]
     const void* wp_hoist;   // packed W1[:, :2M]                           [Np1/16][2M/kb]
-    const float* b_hoist;   // fp32: b1 + W1[:, 2M:] . bc; bf16: b1        [Np1]
+    const float* b_hoist;   // b1 + W1[:, 2M:] . bc (bf16: the bf16 W1)    [Np1]
     const void* wp_l1;      // fp32: packed [W1b.Wc[new] ; W1b]            [Np1/16][(n_new*M + 2M)/16]
                             // bf16: packed W1b                            [Np1/16][2M/32]
-    const void* wp_new;     // bf16: packed Wc over the new taps           [2M/16][n_new*M/32]
-    const float* bc;        // bf16: context bias                          [2M]
+    const void* wp_new;     // bf16: packed F_new = W1b . Wc[new], hi half [Np1/16][n_new*M/32]
+    const void* wp_new_lo;  // bf16: the same, lo half
     const void* wp_old;     // packed Wc over the old taps                 [2M/16][n_old*M/kb]
     const void* wp2;        // packed W2                                   [Np2/16][Np1/kb]
     const float* b2;        // [Np2]
@@ -131,7 +130,6 @@ struct StepArgs {
     void* h2;               // n = Np2, fp32 or bf16 pairs (even steps)
     void* h2b;              // the same for odd steps (dataflow driver; else == h2)
     float* ctxo;            // [2][parts] x (n = 2M) old-tap context k-parts, by step parity
-    uint16_t* ctxb;         // bf16: n = 2M, the context vector of the step (pairs)
     uint16_t* ybf;          // bf16: [B*H*W][M/32][2][32] y_hat as bf16 pairs (tap source)
     int max_rows;           // rows of the widest step, rounded up to 16
     int slots;              // workgroups resident at once (jobs of one round)

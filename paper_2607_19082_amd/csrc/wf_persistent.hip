@@ -77,14 +77,12 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2))
         for (int b = blockIdx.x; b < nh; b += G) hoist_job<P, true>(a, b);
         const StepRows s0 = step_rows(a.H, a.W, a.B, a.lambda, 0);
         const int nc = ctxo_blocks<P>(a, s0);
-        // fp32: the last part adds the others, so it runs after them
-        const int split = P::kBf16 ? P::kParts * nc : (P::kParts - 1) * nc;
+        // the last part adds the others, so it runs after them
+        const int split = (P::kParts - 1) * nc;
         for (int b = blockIdx.x; b < split; b += G) ctxo_job<P, true>(a, s0, b, nc, red);
         if (!grid_barrier(ctr, ++k, err, budget, &bail, tr)) return;
-        if (!P::kBf16) {
-            for (int b = split + blockIdx.x; b < P::kParts * nc; b += G) ctxo_job<P, true>(a, s0, b, nc, red);
-            if (!grid_barrier(ctr, ++k, err, budget, &bail, tr)) return;
-        }
+        for (int b = split + blockIdx.x; b < P::kParts * nc; b += G) ctxo_job<P, true>(a, s0, b, nc, red);
+        if (!grid_barrier(ctr, ++k, err, budget, &bail, tr)) return;
     }
     for (int t = 0; t < T; ++t) {
         const StepRows s = step_rows(a.H, a.W, a.B, a.lambda, t);

@@ -131,6 +131,14 @@ static uint16_t bf16_round(float v) {
     return (uint16_t)(u >> 16);
 }
 
+// v rounded to bf16, as an fp32 value.
+static float bf16_value_of(float v) {
+    const uint32_t u = (uint32_t)bf16_round(v) << 16;
+    float r;
+    std::memcpy(&r, &u, 4);
+    return r;
+}
+
 // The same for bf16 operands, k-blocks of 32: lane l holds
 // Wt[kb*32 + (l/16)*8 + q][ct*16 + l%16] for q = 0..7, rounded to bf16.
 template <class F>
@@ -175,20 +183,22 @@ static void free_plan(Plan* p) {
 }
 
 // Folded layer-1 weights of one tap: F[c][n] = sum_o W1[n][2M + o] * Wc[o][c][tap]
-// (fp64 accumulation), for c < M, n < d1.
-static void fold_tap(const wf_desc* d, int dy, int dx, std::vector<double>& out) {
+// (fp64 accumulation), for c < M, n < d1; with `bf` both factors are the
+// bf16-rounded weights.
+static void fold_tap(const wf_desc* d, int dy, int dx, bool bf, std::vector<double>& out) {
     const int M = d->M, d1 = d->d1;
+    auto q = [bf](float v) { return (double)(bf ? bf16_value_of(v) : v); };
     std::vector<double> wc((size_t)2 * M * M);
     for (int o = 0; o < 2 * M; ++o)
         for (int c = 0; c < M; ++c)
-            wc[(size_t)o * M + c] = d->ctx_w[(((size_t)o * M + c) * 5 + (dy + 2)) * 5 + (dx + 2)];
+            wc[(size_t)o * M + c] = q(d->ctx_w[(((size_t)o * M + c) * 5 + (dy + 2)) * 5 + (dx + 2)]);
     out.assign((size_t)M * d1, 0.0);
     std::vector<double> acc(M);
     for (int n = 0; n < d1; ++n) {
         std::fill(acc.begin(), acc.end(), 0.0);
         const float* w1b = d->w1 + (size_t)n * 4 * M + 2 * M;
         for (int o = 0; o < 2 * M; ++o) {
-            const double w = w1b[o];
+            const double w = q(w1b[o]);
             const double* row = &wc[(size_t)o * M];
             for (int c = 0; c < M; ++c) acc[c] += w * row[c];
         }
@@ -246,7 +256,7 @@ static int build_plan(const wf_desc* d, Plan* p) {
     const bool bf = p->precision == WF_BF16;
     p->Np1 = padded(p->d1, p->precision);
     p->Np2 = padded(p->d2, p->precision);
-    p->nph = bf ? 4 : 3;
+    p->nph = 3;
     const int d1 = p->d1, Np1 = p->Np1;
 
     StepArgs& a = p->args;
@@ -326,31 +336,34 @@ static int build_plan(const wf_desc* d, Plan* p) {
     auto w1b = [&](int k, int n) { return d->w1[(size_t)n * 4 * M + 2 * M + k]; };
     auto w2f = [&](int k, int n) { return d->w2[(size_t)n * d1 + k]; };
     auto w3f = [&](int k, int n) { return d->w3[(size_t)n * p->d2 + k]; };
+    // Fold the new taps' conv into the context half of layer 1, and the
+    // context bias into the hoisted part (bf16: from the bf16 weights).
     std::vector<float> b_hoist(Np1, 0.0f);
+    std::vector<std::vector<double>> fold(a.n_new);
+    for (int k = 0; k < a.n_new; ++k) fold_tap(d, p->dy[new_taps[k]], p->dx[new_taps[k]], bf, fold[k]);
+    for (int n = 0; n < d1; ++n) {
+        double acc = d->b1[n];
+        const float* w1r = d->w1 + (size_t)n * 4 * M + 2 * M;
+        for (int o = 0; o < 2 * M; ++o) acc += (double)(bf ? bf16_value_of(w1r[o]) : w1r[o]) * (double)d->ctx_b[o];
+        b_hoist[n] = (float)acc;
+    }
     if (bf) {
-        // bf16: the context bias stays in the context vector (it is rounded
-        // with it); no fold.
-        std::copy(d->b1, d->b1 + d1, b_hoist.begin());
         const int kn = a.n_new * M, ko = a.n_old * M, Np2 = p->Np2, n3 = p->n3;
+        // the folded block as a pair: hi = bf16(F), lo = bf16(F - hi)
+        auto f_hi = [&](int k, int n) { return (float)fold[k / M][(size_t)(k % M) * d1 + n]; };
+        auto f_lo = [&](int k, int n) {
+            const double v = fold[k / M][(size_t)(k % M) * d1 + n];
+            return (float)(v - (double)bf16_value_of((float)v));
+        };
         if ((rc = put(&a.wp_hoist, Np1, 2 * M, pack_panel_bf16(2 * M, d1, 2 * M, Np1, w1a))) != WF_OK) return rc;
         if ((rc = put(&a.wp_l1, Np1, 2 * M, pack_panel_bf16(2 * M, d1, 2 * M, Np1, w1b))) != WF_OK) return rc;
-        if ((rc = put(&a.wp_new, 2 * M, kn, pack_panel_bf16(kn, 2 * M, kn, 2 * M, wc_of(new_taps)))) != WF_OK) return rc;
+        if ((rc = put(&a.wp_new, Np1, kn, pack_panel_bf16(kn, d1, kn, Np1, f_hi))) != WF_OK) return rc;
+        if ((rc = put(&a.wp_new_lo, Np1, kn, pack_panel_bf16(kn, d1, kn, Np1, f_lo))) != WF_OK) return rc;
+        fold.clear();
         if ((rc = put(&a.wp_old, 2 * M, ko, pack_panel_bf16(ko, 2 * M, ko, 2 * M, wc_of(old_taps)))) != WF_OK) return rc;
         if ((rc = put(&a.wp2, Np2, Np1, pack_panel_bf16(d1, p->d2, Np1, Np2, w2f))) != WF_OK) return rc;
         if ((rc = put(&a.wp3, n3, Np2, pack_panel_bf16(p->d2, n3, Np2, n3, w3f))) != WF_OK) return rc;
-        if ((rc = upload(p, &f, d->ctx_b, (size_t)2 * M)) != WF_OK) return rc;
-        a.bc = f;
     } else {
-        // Fold the new taps' conv into the context half of layer 1, and the
-        // context bias into the hoisted part.
-        std::vector<std::vector<double>> fold(a.n_new);
-        for (int k = 0; k < a.n_new; ++k) fold_tap(d, p->dy[new_taps[k]], p->dx[new_taps[k]], fold[k]);
-        for (int n = 0; n < d1; ++n) {
-            double acc = d->b1[n];
-            const float* w1r = d->w1 + (size_t)n * 4 * M + 2 * M;
-            for (int o = 0; o < 2 * M; ++o) acc += (double)w1r[o] * (double)d->ctx_b[o];
-            b_hoist[n] = (float)acc;
-        }
         const int knew = a.n_new * M;
         const int ko = a.n_old * M, Np2 = p->Np2, n3 = p->n3;
         if ((rc = put(&a.wp_hoist, Np1, 2 * M, pack_panel(2 * M, d1, 2 * M, Np1, w1a))) != WF_OK) return rc;
@@ -393,7 +406,6 @@ static int build_plan(const wf_desc* d, Plan* p) {
     const int nparts = std::max(kCtxPartsMax, p->group > 1 ? a.gparts : 0);
     if ((rc = alloc(p, &a.ctxo, (size_t)2 * nparts * R * 2 * M)) != WF_OK) return rc;
     if (bf) {
-        if ((rc = alloc(p, &a.ctxb, R * 2 * 2 * M)) != WF_OK) return rc;
         if ((rc = alloc(p, &a.ybf, nlat * 2 * M)) != WF_OK) return rc;
     }
     if ((rc = alloc(p, &p->d_call, 1)) != WF_OK) return rc;
@@ -560,7 +572,7 @@ int wf_plan_trace(wf_plan_t plan, int64_t* stamps, int64_t capacity, int64_t* ne
         return WF_OK;
     }
     // barriers: the prologue (two with fp32) and one per phase of every step
-    const int64_t pro = p->precision == WF_BF16 ? 1 : 2;
+    const int64_t pro = 2;
     if (needed) *needed = (int64_t)(pro + p->nph * (int64_t)p->T) * (p->grid + 1);
     if (grid) *grid = p->grid;
     return WF_OK;

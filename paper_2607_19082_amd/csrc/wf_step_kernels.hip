@@ -100,8 +100,8 @@ static void launch_steps(Plan& p, hipStream_t stream) {
     {
         const StepRows s0 = rows_of(p, 0);
         const int nc = ctxo_blocks<P>(a, s0);
-        // fp32: the last part adds the others, so it runs after them
-        const int split = P::kBf16 ? P::kParts * nc : (P::kParts - 1) * nc;
+        // the last part adds the others, so it runs after them
+        const int split = (P::kParts - 1) * nc;
         if (nc > 0) {
             hipLaunchKernelGGL(k_ctxo<P>, dim3(split), dim3(kThreads), 0, stream, s0, 0, nc, a);
             if (split < P::kParts * nc)
