@@ -106,6 +106,100 @@ def summarize_traffic(fetch_dir, write_dir, cal_fetch_dir, cal_write_dir, cal_by
                       "decodes": decodes}))
 
 
+def summarize_counters(dirs, out, command):
+    """MFMA utilisation and L2 hit rate of the decode's dispatches from
+    rocprofv3 --pmc runs (one counter set per run): MfmaUtil (percent of the
+    SIMDs' cycles with the matrix unit busy) weighted by dispatch duration,
+    and TCC_HIT_sum / (TCC_HIT_sum + TCC_MISS_sum), overall and per kernel."""
+    import sqlite3
+    rows = []
+    for d in dirs:
+        db = glob.glob(os.path.join(d, "**", "*results.db"), recursive=True)[0]
+        con = sqlite3.connect(db)
+        rows += list(con.execute("select kernel_name, counter_name, value, duration from counters_collection"))
+    is_dec = lambda k: any(x in k for x in DECODE_KERNELS)
+    short = lambda k: k.split("(")[0].replace("void ", "")
+    per = {}
+    for k, c, v, dur in rows:
+        if not is_dec(k):
+            continue
+        e = per.setdefault(short(k), {"n": 0, "dur": 0.0, "mfma_w": 0.0, "mfma_dur": 0.0, "hit": 0.0, "miss": 0.0})
+        if c == "MfmaUtil":
+            e["n"] += 1
+            e["dur"] += dur
+            e["mfma_w"] += v * dur
+            e["mfma_dur"] += dur
+        elif c == "TCC_HIT_sum":
+            e["hit"] += v
+        elif c == "TCC_MISS_sum":
+            e["miss"] += v
+    tot = {k: sum(e[k] for e in per.values()) for k in ("dur", "mfma_w", "mfma_dur", "hit", "miss")}
+    mfma = tot["mfma_w"] / tot["mfma_dur"] if tot["mfma_dur"] else float("nan")
+    hit = tot["hit"] / (tot["hit"] + tot["miss"]) if tot["hit"] + tot["miss"] else float("nan")
+    with open(out, "w") as f:
+        f.write("# MFMA utilisation and L2 hit rate of the decode (rocprofv3 counters)\n\n")
+        f.write("MfmaUtil = SQ_VALU_MFMA_BUSY_CYCLES / (GRBM_GUI_ACTIVE x SIMDs), per dispatch, weighted by\n")
+        f.write("dispatch duration; L2 hit rate = TCC_HIT_sum / (TCC_HIT_sum + TCC_MISS_sum).  The counters\n")
+        f.write("serialise the dispatches, so durations here are longer than in a timed run.\n\n")
+        f.write(f"- mfma_util_percent: {mfma:.2f}\n- l2_hit_rate: {hit:.4f}\n- source_sha256: `{source_hash()}`\n\n")
+        f.write("| Kernel | Dispatches | MfmaUtil % | L2 hit rate |\n|---|---|---|---|\n")
+        for k, e in sorted(per.items(), key=lambda kv: -kv[1]["dur"]):
+            mu = e["mfma_w"] / e["mfma_dur"] if e["mfma_dur"] else float("nan")
+            hr = e["hit"] / (e["hit"] + e["miss"]) if e["hit"] + e["miss"] else float("nan")
+            f.write(f"| `{k}` | {e['n']} | {mu:.2f} | {hr:.4f} |\n")
+        f.write("\nCommands:\n\n```\n" + command + "\n```\n")
+    print(json.dumps({"mfma_util_percent": mfma, "l2_hit_rate": hit}))
+
+
+def summarize_stats(stats_dir, log, out, command):
+    """Kernel statistics of a profiled bench run (rocprofv3 --kernel-trace
+    --stats): the per-kernel table, and the decode kernels' time per call next
+    to the HIP-event time of one decode from the same run's bench line."""
+    import csv
+    rows = list(csv.DictReader(open(glob.glob(os.path.join(stats_dir, "**", "*kernel_stats.csv"), recursive=True)[0])))
+    rec = json.loads([l for l in open(log) if l.startswith('{"metric"')][-1])
+    calls = sum(int(r["Calls"]) for r in rows if "k_set_call" in r["Name"])
+    dec = sum(float(r["TotalDurationNs"]) for r in rows if any(x in r["Name"] for x in DECODE_KERNELS))
+    cfg = rec["config"]
+    lines = [f"# Kernel statistics: {cfg['workload']}, {cfg['precision']}, {cfg['driver']} driver"
+             + (f", context approximation N = {cfg['context_approximation_group']}"
+                if cfg.get("context_approximation_group", 1) > 1 else ""), "",
+             "Command (on one MI355X, from the repository root):", "", "```", command, "```", "",
+             f"The run makes {calls} decode/encode calls (warm-up, timed decodes, encodes); per-call kernels appear "
+             f"that many times.  k_empty and k_barrier_rounds are the latency-floor probes of the bench.", "",
+             "| Kernel | Calls | Total (ms) | Average (us) | Min (us) | Max (us) | % |", "|---|---|---|---|---|---|---|"]
+    for r in rows:
+        if float(r["Percentage"]) < 0.05:
+            continue
+        name = r["Name"].split("(")[0].replace("void ", "")
+        lines.append(f"| `{name}` | {r['Calls']} | {float(r['TotalDurationNs']) / 1e6:.2f} | "
+                     f"{float(r['AverageNs']) / 1e3:.2f} | {float(r['MinNs']) / 1e3:.2f} | "
+                     f"{float(r['MaxNs']) / 1e3:.2f} | {float(r['Percentage']):.2f} |")
+    lines += ["", f"Decode kernels per call: {dec / max(calls, 1) / 1e6:.3f} ms of kernel time.  The same run's "
+              f"HIP-event time of one decode (under the profiler) was {rec['roofline']['launch_ms_events']:.3f} ms; "
+              f"bench line: {rec['ms_per_step']:.3f} ms per decode, {rec['value']:.0f} latents/s.  For the graph "
+              "and stream drivers the difference is the gaps between kernels."]
+    with open(out, "w") as f:
+        f.write("\n".join(lines) + "\n")
+    print(json.dumps({"calls": calls, "decode_kernel_ms_per_call": dec / max(calls, 1) / 1e6}))
+
+
+def copy_calibration(nbytes):
+    """A plain device copy of nbytes whose source is not cache resident (the
+    source, then as many bytes of other writes, then the copy): the reference
+    reading for FETCH_SIZE / WRITE_SIZE."""
+    import torch
+    n = int(nbytes) // 4
+    src = torch.ones(n, device="cuda")
+    evict = torch.empty(n, device="cuda")
+    dst = torch.empty_like(src)
+    evict.fill_(2.0)
+    torch.cuda.synchronize()
+    dst.copy_(src)
+    torch.cuda.synchronize()
+    print(json.dumps({"copied_bytes": n * 4}), flush=True)
+
+
 def flops_per_latent(cfg):
     """Algorithmic FLOPs of one latent (2 x MACs): the context product over the
     causal taps and the three layers of the entropy-parameter network."""
@@ -192,8 +286,30 @@ def main():
     ap.add_argument("--summarize-traffic", nargs=4, metavar=("FETCH_DIR", "WRITE_DIR", "CAL_FETCH_DIR", "CAL_WRITE_DIR"),
                     help="write the traffic summary of this workload/precision/driver from rocprofv3 outputs")
     ap.add_argument("--cal-bytes", type=float, default=float(1 << 30))
+    ap.add_argument("--copy-calibration", action="store_true",
+                    help="run only the plain copy of --cal-bytes that calibrates FETCH_SIZE / WRITE_SIZE")
+    ap.add_argument("--summarize-stats", nargs=2, metavar=("STATS_DIR", "BENCH_LOG"),
+                    help="write the kernel-statistics summary of this workload/precision/driver/group from a "
+                         "rocprofv3 --kernel-trace --stats run of bench.py and its output")
+    ap.add_argument("--summarize-counters", nargs="+", metavar="PMC_DIR",
+                    help="write the MFMA-utilisation / L2-hit summary of this workload/precision/driver "
+                         "from rocprofv3 --pmc outputs (MfmaUtil; TCC_HIT_sum TCC_MISS_sum)")
     ap.add_argument("--command", default="", help="the commands that made the counter outputs (recorded)")
     args = ap.parse_args()
+    if args.copy_calibration:
+        copy_calibration(args.cal_bytes)
+        return
+    if args.summarize_stats:
+        g = f"_g{args.group}" if args.group > 1 else ""
+        summarize_stats(*args.summarize_stats,
+                        os.path.join(PROFILES, f"kernels_{args.workload}_{args.precision}_{args.driver}{g}.md"),
+                        args.command)
+        return
+    if args.summarize_counters:
+        summarize_counters(args.summarize_counters,
+                           os.path.join(PROFILES, f"counters_{args.workload}_{args.precision}_{args.driver}.md"),
+                           args.command)
+        return
     if args.summarize_traffic:
         summarize_traffic(*args.summarize_traffic, args.cal_bytes,
                           traffic_file(args.workload, args.precision, args.driver), args.command)

@@ -17,7 +17,7 @@ constexpr int kTile = 16;            // MFMA tile edge (rows and columns)
 constexpr int kJobWaves = 4;         // waves of one job's workgroup
 constexpr int kCtxPartsF32 = 6;      // k-parts of the old-tap context product, fp32 operands
 constexpr int kCtxPartsBf16 = 3;     // the same, bf16 operands
-constexpr int kDfCtxParts = 3;       // the same for the dataflow driver (its context jobs run
+constexpr int kDfCtxParts = 2;       // the same for the dataflow driver (its context jobs run
                                      // in a pool of their own, where fewer, longer jobs pay)
 constexpr int kCtxPartsMax = kCtxPartsF32 > kCtxPartsBf16 ? kCtxPartsF32 : kCtxPartsBf16;
 static_assert(kDfCtxParts <= kCtxPartsMax, "context k-parts exceed the buffer");
