@@ -47,7 +47,7 @@ class _Model(ctypes.Structure):
         ("w2", ctypes.c_void_p), ("b2", ctypes.c_void_p),
         ("w3", ctypes.c_void_p), ("b3", ctypes.c_void_p),
         ("table", ctypes.c_void_p), ("L", ctypes.c_int32),
-        ("group", ctypes.c_int32),
+        ("group", ctypes.c_int32), ("radius", ctypes.c_int32),
     ]
 
 
@@ -92,13 +92,21 @@ class Model:
     ctx_w [2M][M][5][5], ctx_b [2M], w1 [d1][4M], b1, w2 [d2][d1], b2,
     w3 [n3][d2], b3 (PyTorch layouts); ``table`` is the scale table.  ``group``
     N > 1 selects the context-approximation decode with groups of N
-    wavefronts (N <= 1: the exact autoregressive decode)."""
+    wavefronts (N <= 1: the exact autoregressive decode).  The conv weight may
+    be [2M][M][2R+1][2R+1] for any mask radius R (Def. 1); R = 2 is the 5x5
+    mask."""
 
     def __init__(self, weights, table, H, W, B=1, K=1, relaxed=False, bf16=False,
                  slope=0.01, group=1):
         self.arrays = {k: _f32(v) for k, v in weights.items()}
         self.table = _f32(table)
         M = self.arrays["ctx_w"].shape[1]
+        k = self.arrays["ctx_w"].shape[2]
+        if k % 2 != 1 or self.arrays["ctx_w"].shape[3] != k:
+            raise ValueError("ctx_w must be [2M][M][2R+1][2R+1]")
+        self.radius = k // 2
+        if relaxed and self.radius != 2:
+            raise ValueError("the relaxed mask is defined for the 5x5 kernel only")
         d1 = self.arrays["w1"].shape[0]
         d2 = self.arrays["w2"].shape[0]
         n3 = self.arrays["w3"].shape[0]
@@ -110,7 +118,7 @@ class Model:
         self._m = _Model(H, W, M, B, K, d1, d2, int(relaxed), int(bf16), slope,
                          _ptr(a["ctx_w"]), _ptr(a["ctx_b"]), _ptr(a["w1"]), _ptr(a["b1"]),
                          _ptr(a["w2"]), _ptr(a["b2"]), _ptr(a["w3"]), _ptr(a["b3"]),
-                         _ptr(self.table), len(self.table), int(group))
+                         _ptr(self.table), len(self.table), int(group), self.radius)
         self.group = int(group)
 
     def tap_status(self, i, j, dy, dx):

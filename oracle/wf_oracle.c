@@ -8,8 +8,9 @@
  * What it computes (paper, Sec. III-A, Eq. 2-4, and Appendix A, Def. 1): the
  * latent grid is decoded one latent at a time in a given topological order of
  * the dependency DAG (raster order by default, Eq. 2).  For each latent the
- * context is a 5x5 causal masked convolution (Def. 1 with R = 2: the two rows
- * above within horizontal offset 2, and the two latents to the left), then the
+ * context is a (2R+1)x(2R+1) causal masked convolution (Def. 1: the R rows
+ * above within horizontal offset R, and the R latents to the left; R = 2, the
+ * 5x5 mask, unless `radius` says otherwise), then the
  * entropy-parameter network maps [hyperprior params ; context] to the
  * distribution parameters (Sec. II-B, Eq. 1).  Decoding writes y_hat = s + mu
  * for the given integer symbol s; encoding quantises s = round(y - mu) and
@@ -31,7 +32,7 @@
  * Readings where the paper is silent (each also listed in the design notes):
  *  - out-of-image taps contribute zero (Def. 1 keeps only in-image edges);
  *  - the conv is a cross-correlation with bias: tap (dy,dx) uses
- *    weight[o][c][dy+2][dx+2];
+ *    weight[o][c][dy+R][dx+R] of a [2M][M][2R+1][2R+1] weight;
  *  - the network input is [psi ; ctx]; activation is LeakyReLU;
  *  - output channels are [mean | scale] for one Gaussian, and
  *    [weight | mean | scale] (component-major blocks of M) for a 3-component
@@ -71,6 +72,7 @@ typedef struct {
     const float *table;         /* [L], strictly increasing                   */
     int32_t L;
     int32_t group;              /* 0 or 1: exact; N > 1: groups of N wavefronts */
+    int32_t radius;             /* mask radius R (0 means 2); ctx_w is [2M][M][2R+1][2R+1] */
 } oracle_model;
 
 typedef struct {
@@ -114,19 +116,33 @@ static double act_op(const oracle_model *m, float x)
     return (double)hi + (double)lo;
 }
 
-/* Is the causal tap (dy,dx) part of the mask?  The 5x5 causal mask keeps
- * rows dy = -2, -1 with any dx in [-2,2], and dy = 0 with dx in {-2,-1}. */
+static int radius_of(const oracle_model *m)
+{
+    return m->radius > 0 ? m->radius : 2;
+}
+
+/* Is the causal tap (dy,dx) part of the mask?  The (2R+1)^2 causal mask keeps
+ * rows dy = -R..-1 with any dx in [-R,R], and dy = 0 with dx in [-R,-1]. */
 static int tap_in_mask(const oracle_model *m, int dy, int dx)
 {
-    if (dy < -2 || dy > 0 || dx < -2 || dx > 2) return 0;
+    const int R = radius_of(m);
+    if (dy < -R || dy > 0 || dx < -R || dx > R) return 0;
     if (dy == 0 && dx >= 0) return 0;
     if (m->relaxed && dx == 2 && (dy == -1 || dy == -2)) return 0;
     return 1;
 }
 
+/* Weight of output oc, input channel c, tap (dy,dx). */
+static float conv_weight(const oracle_model *m, int oc, int c, int dy, int dx)
+{
+    const int R = radius_of(m), k = 2 * R + 1;
+    return m->ctx_w[(((size_t)oc * m->M + c) * k + (dy + R)) * k + (dx + R)];
+}
+
+/* The least shear of the mask (Sec. III-B): R + 1, or 2 for the relaxed 5x5 mask. */
 static int shear_of(const oracle_model *m)
 {
-    return m->relaxed ? 2 : 3;
+    return m->relaxed ? 2 : radius_of(m) + 1;
 }
 
 /* Status of tap (dy,dx) of latent (i,j): 0 outside the image, 1 decoded
@@ -184,8 +200,9 @@ static void latent_params(const oracle_model *m, const float *y_hat,
         int known = 0;
         for (int c = 0; c < M; ++c) fill[c] = 0.0f;
         double *sum = calloc((size_t)M, sizeof(double));
-        for (int dy = -2; dy <= 0; ++dy)
-            for (int dx = -2; dx <= 2; ++dx) {
+        const int R = radius_of(m);
+        for (int dy = -R; dy <= 0; ++dy)
+            for (int dx = -R; dx <= R; ++dx) {
                 if (!tap_in_mask(m, dy, dx) || tap_status(m, i, j, dy, dx) != 1) continue;
                 const float *src = y_hat + (((size_t)b * H + i + dy) * W + j + dx) * M;
                 for (int c = 0; c < M; ++c) sum[c] += (double)src[c];
@@ -196,19 +213,18 @@ static void latent_params(const oracle_model *m, const float *y_hat,
         free(sum);
     }
 
-    /* Context: 5x5 masked conv evaluated at (i,j), Def. 1 / Sec. III-C. */
+    /* Context: the masked conv evaluated at (i,j), Def. 1 / Sec. III-C. */
+    const int R = radius_of(m);
     for (int oc = 0; oc < 2 * M; ++oc) {
         double acc = (double)m->ctx_b[oc];
-        for (int dy = -2; dy <= 0; ++dy) {
-            for (int dx = -2; dx <= 2; ++dx) {
+        for (int dy = -R; dy <= 0; ++dy) {
+            for (int dx = -R; dx <= R; ++dx) {
                 if (!tap_in_mask(m, dy, dx)) continue;
                 int st = tap_status(m, i, j, dy, dx);
                 if (st == 0) continue;
                 const float *src = st == 1 ? y_hat + (((size_t)b * H + i + dy) * W + j + dx) * M : fill;
-                for (int c = 0; c < M; ++c) {
-                    float w = m->ctx_w[(((size_t)oc * M + c) * 5 + (dy + 2)) * 5 + (dx + 2)];
-                    acc += weight_op(m, w) * act_op(m, src[c]);
-                }
+                for (int c = 0; c < M; ++c)
+                    acc += weight_op(m, conv_weight(m, oc, c, dy, dx)) * act_op(m, src[c]);
             }
         }
         h0[2 * M + oc] = (float)acc;

@@ -47,9 +47,11 @@ def scale_table(levels=64, lo=0.11, hi=256.0):
     return t.astype(np.float32)
 
 
-def make_weights(M, K, seed=0):
+def make_weights(M, K, seed=0, radius=2):
     """Random weights of the context model and the parameter network, in
-    PyTorch layouts: ctx_w [2M][M][5][5], w1 [d1][4M], w2 [d2][d1], w3 [n3][d2]."""
+    PyTorch layouts: ctx_w [2M][M][2R+1][2R+1] (R = radius; 5x5 by default),
+    w1 [d1][4M], w2 [d2][d1], w3 [n3][d2].  fan_in of the conv is its number
+    of causal taps (2R^2 + 2R) times M."""
     d1, d2, n3 = widths(M, K)
     rng = np.random.default_rng(seed)
 
@@ -57,8 +59,9 @@ def make_weights(M, K, seed=0):
         return (rng.standard_normal(shape) / np.sqrt(fan_in)).astype(np.float32)
 
     w = {}
-    w["ctx_w"] = draw((2 * M, M, 5, 5), 12 * M)
-    w["ctx_b"] = draw((2 * M,), 12 * M)
+    k, taps = 2 * radius + 1, 2 * radius * radius + 2 * radius
+    w["ctx_w"] = draw((2 * M, M, k, k), taps * M)
+    w["ctx_b"] = draw((2 * M,), taps * M)
     w["w1"] = draw((d1, 4 * M), 4 * M)
     w["b1"] = draw((d1,), 4 * M)
     w["w2"] = draw((d2, d1), d1)
