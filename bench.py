@@ -200,11 +200,21 @@ def copy_calibration(nbytes):
     print(json.dumps({"copied_bytes": n * 4}), flush=True)
 
 
+# causal taps, shear and kernel radius of each mask (Def. 1; Sec. III-B)
+MASK_TAPS = {"full": 12, "relaxed": 10, "3x3": 4, "7x7": 24}
+MASK_SHEAR = {"full": 3, "relaxed": 2, "3x3": 2, "7x7": 4}
+MASK_RADIUS = {"full": 2, "relaxed": 2, "3x3": 1, "7x7": 3}
+
+
+def mask_of(cfg):
+    return cfg.get("mask") or ("relaxed" if cfg["relaxed"] else "full")
+
+
 def flops_per_latent(cfg):
     """Algorithmic FLOPs of one latent (2 x MACs): the context product over the
     causal taps and the three layers of the entropy-parameter network."""
     M, d1, d2, n3 = cfg["M"], cfg["d1"], cfg["d2"], cfg["n3"]
-    taps = 10 if cfg["relaxed"] else 12
+    taps = MASK_TAPS[mask_of(cfg)]
     macs = taps * M * 2 * M + 4 * M * d1 + d1 * d2 + d2 * n3
     return 2 * macs
 
@@ -218,7 +228,7 @@ def step_rows(cfg, group=1):
     """Latents per decoding step: per wavefront, or per group of `group`
     wavefronts under context approximation."""
     H, W, B = cfg["H"], cfg["W"], cfg["B"]
-    lam = 2 if cfg["relaxed"] else 3
+    lam = MASK_SHEAR[mask_of(cfg)]
     T = W + lam * (H - 1)
     rows = np.zeros(T, np.int64)
     for i in range(H):
@@ -228,13 +238,16 @@ def step_rows(cfg, group=1):
     return rows
 
 
-def cpu_baseline(name, rows):
+def cpu_baseline(name, rows, mask=None):
     """Time the CPU oracle decoding the top `rows` grid rows of the same
     workload (the causal taps point up and left, so this is an exact decode of
     those latents)."""
     import oracle
     from paper_2607_19082_amd import inputs
     cfg, w, table, psi, sym = inputs.make_inputs(name)
+    if mask:
+        cfg["relaxed"] = mask == "relaxed"
+        w = inputs.make_weights(cfg["M"], cfg["K"], radius=MASK_RADIUS[mask])
     psi, sym = psi[:, :rows].copy(), sym[:, :rows].copy()
     m = oracle.Model(w, table, rows, cfg["W"], cfg["B"], cfg["K"], relaxed=cfg["relaxed"])
     t0 = time.perf_counter()
@@ -279,6 +292,8 @@ def main():
     ap.add_argument("--workload", default=DEFAULT_WORKLOAD)
     ap.add_argument("--driver", default="graph", choices=["stream", "graph", "persistent", "dataflow"])
     ap.add_argument("--precision", default="fp32", choices=["fp32", "bf16"])
+    ap.add_argument("--mask", default=None, choices=sorted(MASK_TAPS),
+                    help="causal mask (default: the workload's own), weights drawn for its kernel size")
     ap.add_argument("--group", type=int, default=1,
                     help="context approximation: decode N wavefronts per step (1: exact decode)")
     ap.add_argument("--cpu-rows", type=int, default=8, help="grid rows of the CPU-oracle sample (0: skip)")
@@ -301,8 +316,9 @@ def main():
         return
     if args.summarize_stats:
         g = f"_g{args.group}" if args.group > 1 else ""
+        mk = f"_mask{args.mask}" if args.mask else ""
         summarize_stats(*args.summarize_stats,
-                        os.path.join(PROFILES, f"kernels_{args.workload}_{args.precision}_{args.driver}{g}.md"),
+                        os.path.join(PROFILES, f"kernels_{args.workload}_{args.precision}_{args.driver}{mk}{g}.md"),
                         args.command)
         return
     if args.summarize_counters:
@@ -325,8 +341,12 @@ def main():
     assert torch.cuda.is_available(), "bench needs a GPU"
     torch.cuda.set_device(0)
     cfg, w, table, psi, sym = inputs.make_inputs(args.workload)
-    plan = wf.Plan(w, table, cfg["H"], cfg["W"], cfg["B"], cfg["K"],
-                   mask="relaxed" if cfg["relaxed"] else "full", precision=args.precision,
+    own_mask = args.mask is None or args.mask == mask_of(cfg)
+    if args.mask:
+        cfg["mask"] = args.mask
+        cfg["relaxed"] = args.mask == "relaxed"
+        w = inputs.make_weights(cfg["M"], cfg["K"], radius=MASK_RADIUS[args.mask])
+    plan = wf.Plan(w, table, cfg["H"], cfg["W"], cfg["B"], cfg["K"], mask=mask_of(cfg), precision=args.precision,
                    driver=args.driver, group=args.group)
     psi_d = torch.from_numpy(psi).cuda()
     sym_d = torch.from_numpy(sym).cuda()
@@ -370,8 +390,8 @@ def main():
     peak = PEAK_TFLOPS[args.precision]
     achieved = fl / (dec_ms * 1e-3) / 1e12
     rows = step_rows(cfg, args.group)
-    # the committed counter summaries cover the exact decode only
-    traffic = read_traffic(args.workload, args.precision, args.driver) if args.group == 1 else None
+    # the committed counter summaries cover the exact decode with the workload's own mask only
+    traffic = read_traffic(args.workload, args.precision, args.driver) if args.group == 1 and own_mask else None
     lfloor = min(x for x in (node_us, bar_us) if x > 0)
     f_step = rows * (flops_per_latent(cfg) - hoistable_flops_per_latent(cfg))
     t_roof_s = (hoistable_flops_per_latent(cfg) * lat) / (peak * 1e12) + np.maximum(
@@ -391,7 +411,7 @@ def main():
         "dtype": "f32" if args.precision == "fp32" else "bf16 operands, f32 accumulate",
         "data": "synthetic (seeded N(0,1/fan_in) weights, N(0,1) hyperprior params, Laplace symbols)",
         "config": {"workload": args.workload, "H": cfg["H"], "W": cfg["W"], "M": cfg["M"],
-                   "B": cfg["B"], "K": cfg["K"], "mask": "relaxed" if cfg["relaxed"] else "full",
+                   "B": cfg["B"], "K": cfg["K"], "mask": mask_of(cfg),
                    "steps_T": T, "driver": args.driver, "precision": args.precision,
                    "context_approximation_group": args.group,
                    "parallelism": "single GPU"},
@@ -413,7 +433,7 @@ def main():
         "encode": rec_enc,
     }
     if args.cpu_rows > 0:
-        rec["cpu_baseline"] = cpu_baseline(args.workload, args.cpu_rows)
+        rec["cpu_baseline"] = cpu_baseline(args.workload, args.cpu_rows, args.mask)
     print(json.dumps(rec), flush=True)
 
 

@@ -42,10 +42,13 @@ typedef enum {
     WF_E_TIMEOUT = -5       /* a device-side wait exceeded its spin budget     */
 } wf_status;
 
-/* Tap sets of the 5x5 causal mask (Def. 1 with R = 2). */
+/* Causal masks (Def. 1: a (2R+1)x(2R+1) kernel keeps the R rows above within
+ * horizontal offset R, and the R latents to the left; least shear R + 1). */
 typedef enum {
-    WF_MASK_FULL = 0,       /* 12 taps: rows -2,-1 with dx in [-2,2]; (0,-2), (0,-1); lambda = 3 */
-    WF_MASK_RELAXED = 1     /* 10 taps: the full mask without (-1,+2) and (-2,+2); lambda = 2    */
+    WF_MASK_FULL = 0,       /* 5x5, 12 taps: rows -2,-1 with dx in [-2,2]; (0,-2), (0,-1); lambda = 3 */
+    WF_MASK_RELAXED = 1,    /* 5x5, 10 taps: the full mask without (-1,+2) and (-2,+2); lambda = 2   */
+    WF_MASK_3X3 = 2,        /* 3x3, 4 taps: row -1 with dx in [-1,1]; (0,-1); lambda = 2            */
+    WF_MASK_7X7 = 3         /* 7x7, 24 taps: rows -3..-1 with dx in [-3,3]; (0,-3..-1); lambda = 4  */
 } wf_mask;
 
 /* Operand precision of every product (the paper fixes none; fp32 is the
@@ -70,7 +73,8 @@ typedef enum {
 /*
  * Model and problem description.  All weight arrays are HOST memory in
  * PyTorch layouts and are copied (and repacked) by wf_plan.
- *   ctx_w [2M][M][5][5]  masked 5x5 conv weight (masked positions are ignored)
+ *   ctx_w [2M][M][k][k]  masked conv weight, k = 5 (3, 7 for WF_MASK_3X3 / _7X7);
+ *                        masked positions are ignored
  *   ctx_b [2M]
  *   w1 [d1][4M], b1 [d1]   layer 1 input is [psi (2M) ; ctx (2M)]
  *   w2 [d2][d1], b2 [d2]

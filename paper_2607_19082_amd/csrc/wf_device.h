@@ -577,9 +577,13 @@ __device__ __forceinline__ typename P::A ld_tap(const StepArgs& a, const Row& w,
     const int c = kb * P::kK - tap * M + kq * (P::kK / 4);
     int dy, dx;
     if (old) {
-        const int row = tap < a.old_n0 ? 0 : (tap < a.old_n0 + a.old_n1 ? 1 : 2);
-        dx = tap - (row == 0 ? 0 : (row == 1 ? a.old_n0 : a.old_n0 + a.old_n1)) - 2;
-        dy = row - 2;
+        // the tap's row (0 = row -R) and the row's first tap, wave-uniform
+        // (nested selects: a loop here costs the old-tap jobs many SGPRs)
+        static_assert(kMaxRadius == 3, "rows -3..0");
+        const int row = tap < a.old_start[0] ? 0 : (tap < a.old_start[1] ? 1 : (tap < a.old_start[2] ? 2 : 3));
+        const int first = row == 0 ? 0 : (row == 1 ? a.old_start[0] : (row == 2 ? a.old_start[1] : a.old_start[2]));
+        dy = row - a.R;
+        dx = tap - first - a.R;
     } else {
         dy = tap - 1;
         dx = tap ? -1 : a.new_dx0;
@@ -656,7 +660,7 @@ __device__ __forceinline__ void l1_fold_tile(const StepArgs& a, const StepRows& 
     for (int c = 0; c < C; ++c) z[c] = ld1<COH>(a.p1, v.lat * a.Np1 + group_col<PF32>(jb.ct, c), v.valid);
     const int r = jb.rt * kTile + (lane & 15);
     const Row w = step_row(a, s, r);
-    const int knew = a.n_new * M;
+    const int knew = kMaxNew * M;
     const size_t cpart = (size_t)a.max_rows * 2 * M;
     // the old-tap context: the last part's slot holds the whole sum
     const int NP = a.ctx_parts;
@@ -697,7 +701,7 @@ __device__ __forceinline__ void l1_fold_bf16_tile(const StepArgs& a, const StepR
     for (int c = 0; c < C; ++c) z[c] = ld1<COH>(a.p1, v.lat * a.Np1 + group_col<PBF16>(jb.ct, c), v.valid);
     const int r = jb.rt * kTile + (lane & 15);
     const Row w = step_row(a, s, r);
-    const int kbn = a.n_new * M / PBF16::kK, kbc = 2 * M / PBF16::kK, nkb = kbn + kbc;
+    const int kbn = kMaxNew * M / PBF16::kK, kbc = 2 * M / PBF16::kK, nkb = kbn + kbc;
     const int per = (nkb + kWaves - 1) / kWaves;
     const int kb0 = min(nkb, wave * per), kb1 = min(nkb, kb0 + per);
     const int NP = a.ctx_parts;
@@ -959,10 +963,15 @@ __device__ __forceinline__ void l3_job(const StepArgs& a, const StepRows& s, int
 // channel, by the mean of the latent's decoded in-image taps (zero when none
 // is decoded); out-of-grid taps are zero.  Tap k of the mask (raster order).
 __device__ __forceinline__ void mask_tap(const StepArgs& a, int k, int& dy, int& dx) {
-    const int rw = a.row_w;
-    if (k < rw) { dy = -2; dx = k - 2; }
-    else if (k < 2 * rw) { dy = -1; dx = k - rw - 2; }
-    else { dy = 0; dx = k - 2 * rw - 2; }
+    const int rw = a.row_w, up = a.R * rw;
+    if (k < up) {
+        const int q = k / rw;
+        dy = q - a.R;
+        dx = k - q * rw - a.R;
+    } else {
+        dy = 0;
+        dx = k - up - a.R;
+    }
 }
 
 // Job of the grouped context: k-part `part` of ctx[r][n] = sum over taps and
@@ -970,12 +979,13 @@ __device__ __forceinline__ void mask_tap(const StepArgs& a, int k, int& dy, int&
 // The k order of the packed weights is channel-chunk-major (chunk q of kK
 // channels, then the taps), and wave w of part p takes chunk 4p + w: it loads
 // that chunk of every tap, so the fill mean of its channels is formed in
-// registers from the same loads.  The parts are summed by layer 1.
-template <class P, bool COH>
+// registers from the same loads.  The parts are summed by layer 1.  NT bounds
+// the mask's tap count (the taps stay in registers).
+template <class P, int NT, bool COH>
 __device__ __forceinline__ void gctx_tile(const StepArgs& a, const StepRows& s, int part, Job jb, f4 (*red)[64]) {
     constexpr int C = P::kC, KB = P::kK, CPL = KB / 4;   // channels per lane of a chunk
     const int wave = wave_id(), lane = threadIdx.x & 63, kq = lane >> 4;
-    const int M = a.M, Q = M / KB, nt = a.ntaps;
+    const int M = a.M, Q = M / KB, nt = a.n_old + kMaxNew;
     const int q = part * kWaves + wave;                  // this wave's channel chunk
     const Row w = step_row(a, s, jb.rt * kTile + (lane & 15));
     const int g = (a.lambda * w.i + w.j) / a.group;
@@ -983,22 +993,22 @@ __device__ __forceinline__ void gctx_tile(const StepArgs& a, const StepRows& s, 
 #pragma unroll
     for (int c = 0; c < C; ++c) acc[c] = zero4();
     if (q < Q) {
-        typename P::A x[kMaxTaps];
+        typename P::A x[NT];
         float sum[CPL];
 #pragma unroll
         for (int e = 0; e < CPL; ++e) sum[e] = 0.0f;
-        unsigned status = 0;                             // 2 bits per tap: 0 out, 1 decoded, 2 filled
+        unsigned long long status = 0;                   // 2 bits per tap: 0 out, 1 decoded, 2 filled
         int known = 0;
         const int c0 = q * KB + kq * CPL;
 #pragma unroll
-        for (int k = 0; k < kMaxTaps; ++k) {
+        for (int k = 0; k < NT; ++k) {
             // (every index below is a compile-time constant, so x[] stays in registers)
             int dy, dx;
             mask_tap(a, k, dy, dx);
             const int ii = w.i + dy, jj = w.j + dx;
             const bool in = k < nt && w.valid && ii >= 0 && jj >= 0 && jj < a.W;
             const bool dec = in && (a.lambda * ii + jj) / a.group < g;
-            status |= (in ? (dec ? 1u : 2u) : 0u) << (2 * k);
+            status |= (unsigned long long)(in ? (dec ? 1u : 2u) : 0u) << (2 * k);
             known += dec;
             const size_t lat = ((size_t)w.b * a.H + ii) * a.W + jj;
             if constexpr (P::kBf16) {
@@ -1009,7 +1019,7 @@ __device__ __forceinline__ void gctx_tile(const StepArgs& a, const StepRows& s, 
             }
         }
 #pragma unroll
-        for (int k = 0; k < kMaxTaps; ++k) {
+        for (int k = 0; k < NT; ++k) {
             if constexpr (P::kBf16) {
 #pragma unroll
                 for (int e = 0; e < 8; ++e) sum[e] += (float)x[k].hi[e] + (float)x[k].lo[e];
@@ -1026,9 +1036,9 @@ __device__ __forceinline__ void gctx_tile(const StepArgs& a, const StepRows& s, 
         const size_t ws = (size_t)nt * Q * 64;           // one column tile of the packed panel
         const typename P::B* wp = static_cast<const typename P::B*>(a.wp_all) + (size_t)jb.ct * C * ws + lane;
 #pragma unroll
-        for (int k = 0; k < kMaxTaps; ++k) {
+        for (int k = 0; k < NT; ++k) {
             if (k >= nt) continue;                       // wave-uniform
-            const unsigned st = (status >> (2 * k)) & 3u;
+            const unsigned st = (unsigned)(status >> (2 * k)) & 3u;
             typename P::A v = x[k];
             if (st == 2u) v = fillv;                     // decoded taps and zeros (out of grid) as loaded
 #pragma unroll
@@ -1056,11 +1066,11 @@ __device__ __forceinline__ void gctx_tile(const StepArgs& a, const StepRows& s, 
         for (int c = 0; c < C; ++c) st1<COH>(a.ctxo, base + tile_idx<PF32>(ro, group_col<P>(jb.ct, c), 2 * M), v[c]);
     }
 }
-template <class P, bool COH>
+template <class P, int NT, bool COH>
 __device__ __forceinline__ void gctx_job(const StepArgs& a, const StepRows& s, int j, int nc, f4 (*red)[64]) {
     const int part = j / nc;
     const Job jb = xcd_job(j - part * nc, 2 * a.M / kTile / P::kC, ntiles(s.nrows));
-    if (jb.valid) gctx_tile<P, COH>(a, s, part, jb, red);
+    if (jb.valid) gctx_tile<P, NT, COH>(a, s, part, jb, red);
 }
 
 // Grouped decode, layer 1 over the context (the sum of the gctx parts):
@@ -1096,13 +1106,13 @@ __device__ __forceinline__ void l1_group_tile(const StepArgs& a, const StepRows&
         };
         block_tiles<PBF16>(red, a.wp_l1, 2 * M / PBF16::kK, jb.ct, la, acc);
     } else {
-        const int kbn = a.n_new * M / kTile;             // the panel's first block (folded taps) is skipped
+        const int kbn = kMaxNew * M / kTile;             // the panel's first block (folded taps) is skipped
         auto la = [&](int kb) -> f4 {
             f4 u = zero4();
             for (int p2 = 0; p2 < np; ++p2) u += ld_tile<PF32, COH>(ctx + p2 * cpart, jb.rt, 2 * M, kb - kbn, valid);
             return u;
         };
-        block_tiles<PF32>(red, a.wp_l1, (a.n_new * M + 2 * M) / kTile, jb.ct, la, acc, kbn);
+        block_tiles<PF32>(red, a.wp_l1, (kMaxNew * M + 2 * M) / kTile, jb.ct, la, acc, kbn);
     }
     if (v.valid) {
 #pragma unroll

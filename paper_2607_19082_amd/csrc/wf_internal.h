@@ -11,7 +11,9 @@
 
 namespace wf {
 
-constexpr int kMaxTaps = 12;
+constexpr int kMaxTaps = 24;         // the 7x7 causal mask
+constexpr int kTaps5x5 = 12;         // the 5x5 causal mask
+constexpr int kMaxRadius = 3;
 constexpr int kMaxNew = 2;           // taps written by the immediately preceding step
 constexpr int kTile = 16;            // MFMA tile edge (rows and columns)
 constexpr int kJobWaves = 4;         // waves of one job's workgroup
@@ -83,7 +85,7 @@ struct CallPtrs {
 // y_hat of steps <= t-1, so it is computed during step t, off the critical
 // path, in k-parts.
 //
-// Layer 1 of step t reads [new taps (n_new*M) ; old-tap context (2M)]
+// Layer 1 of step t reads [new taps (kMaxNew*M) ; old-tap context (2M)]
 // against [W1[:, 2M:] . Wc[new taps] ; W1[:, 2M:]] (the new taps' conv and the
 // context half of layer 1 are both linear, so their product is folded at plan
 // time; the context bias is folded into the hoisted part).  With bf16
@@ -96,27 +98,31 @@ struct CallPtrs {
 struct StepArgs {
     int H, W, M, B, K, L, lambda;
     int Np1, Np2, n3;
-    int n_new, n_old;
+    int n_old;              // old taps (the new ones are kMaxNew)
     int ctx_parts;          // k-parts of the old-tap context product (per driver, precision)
     // Tap geometry, as scalars so that kernels compute a tap's offset without
-    // indexing memory.  Old taps, tap-major: the first old_n0 lie in row -2,
-    // the next old_n1 in row -1, the rest in row 0; each row's run starts at
-    // dx = -2 and is contiguous.  New taps: (-1, new_dx0) and (0, -1).
-    int old_n0, old_n1, new_dx0;
+    // indexing memory.  The mask has radius R (rows -R..0).  Old taps are
+    // tap-major by row; old_start[q] is the first old tap of row -R + q + 1
+    // (a sentinel above any tap for rows past 0), the first of row -R is 0;
+    // each row's run starts at dx = -R and is contiguous.  New taps:
+    // (-1, new_dx0) and (0, -1).
+    int R;
+    int old_start[kMaxRadius];
+    int new_dx0;
     float slope;
     // Context approximation (groups of `group` wavefronts; 1 = exact decode).
     // A "step" is then a group; its rows are listed in rowlat (latent indices,
     // from StepRows::r0), its context is the product over all taps (raster
-    // mask order: row_w taps in each of rows -2 and -1 from dx = -2, then
-    // (0,-2), (0,-1)) with same-group taps filled, in gparts k-parts.
-    int group, row_w, ntaps, gparts;
+    // mask order: row_w taps in each of rows -R..-1 from dx = -R, then the R
+    // taps (0,-R)..(0,-1)) with same-group taps filled, in gparts k-parts.
+    int group, row_w, gparts;
     const int* rowlat;      // nullptr: rows of wavefront t by grid row
-    const void* wp_all;     // packed Wc over all taps, channel-chunk-major k   [2M/16][ntaps*M/kb]
+    const void* wp_all;     // packed Wc over all taps, channel-chunk-major k   [2M/16][(n_old+2)*M/kb]
     const void* wp_hoist;   // packed W1[:, :2M]                           [Np1/16][2M/kb]
     const float* b_hoist;   // b1 + W1[:, 2M:] . bc (bf16: the bf16 W1)    [Np1]
-    const void* wp_l1;      // fp32: packed [W1b.Wc[new] ; W1b]            [Np1/16][(n_new*M + 2M)/16]
+    const void* wp_l1;      // fp32: packed [W1b.Wc[new] ; W1b]            [Np1/16][(2M + 2M)/16]
                             // bf16: packed W1b                            [Np1/16][2M/32]
-    const void* wp_new;     // bf16: packed F_new = W1b . Wc[new], hi half [Np1/16][n_new*M/32]
+    const void* wp_new;     // bf16: packed F_new = W1b . Wc[new], hi half [Np1/16][2M/32]
     const void* wp_new_lo;  // bf16: the same, lo half
     const void* wp_old;     // packed Wc over the old taps                 [2M/16][n_old*M/kb]
     const void* wp2;        // packed W2                                   [Np2/16][Np1/kb]

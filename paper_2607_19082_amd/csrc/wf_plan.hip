@@ -24,13 +24,25 @@ int fail(int code, const std::string& msg) {
             return fail(WF_E_HIP, std::string(#call) + ": " + hipGetErrorString(e_)); \
     } while (0)
 
-// Causal taps of the 5x5 mask in kernel raster order (Appendix A, Def. 1,
-// R = 2): the two rows above with |dx| <= 2, then the two latents to the left.
-// The relaxed mask drops (-2,+2) and (-1,+2).
+// Radius R of a mask's (2R+1)x(2R+1) kernel, or -1 for an unknown mask.
+static int mask_radius(int mask) {
+    switch (mask) {
+    case WF_MASK_3X3: return 1;
+    case WF_MASK_FULL:
+    case WF_MASK_RELAXED: return 2;
+    case WF_MASK_7X7: return 3;
+    default: return -1;
+    }
+}
+
+// Causal taps of a mask in kernel raster order (Appendix A, Def. 1): the R
+// rows above with |dx| <= R, then the R latents to the left.  The relaxed 5x5
+// mask drops (-2,+2) and (-1,+2).
 static int mask_taps(int mask, int* dy, int* dx) {
+    const int R = mask_radius(mask);
     int n = 0;
-    for (int y = -2; y <= 0; ++y) {
-        for (int x = -2; x <= 2; ++x) {
+    for (int y = -R; y <= 0; ++y) {
+        for (int x = -R; x <= R; ++x) {
             if (y == 0 && x >= 0) continue;
             if (mask == WF_MASK_RELAXED && x == 2 && (y == -1 || y == -2)) continue;
             dy[n] = y;
@@ -67,8 +79,7 @@ static int check_desc(const wf_desc* d) {
         return fail(WF_E_INVALID, "H, W, M and B must be positive");
     if (d->K != 1 && d->K != 3) return fail(WF_E_INVALID, "K must be 1 or 3");
     if (d->d1 < 1 || d->d2 < 1) return fail(WF_E_INVALID, "d1 and d2 must be positive");
-    if (d->mask != WF_MASK_FULL && d->mask != WF_MASK_RELAXED)
-        return fail(WF_E_INVALID, "unknown mask");
+    if (mask_radius(d->mask) < 0) return fail(WF_E_INVALID, "unknown mask");
     if (d->precision != WF_FP32 && d->precision != WF_BF16)
         return fail(WF_E_INVALID, "unknown precision");
     if (d->driver < WF_DRIVER_STREAM || d->driver > WF_DRIVER_DATAFLOW)
@@ -186,12 +197,12 @@ static void free_plan(Plan* p) {
 // (fp64 accumulation), for c < M, n < d1; with `bf` both factors are the
 // bf16-rounded weights.
 static void fold_tap(const wf_desc* d, int dy, int dx, bool bf, std::vector<double>& out) {
-    const int M = d->M, d1 = d->d1;
+    const int M = d->M, d1 = d->d1, R = mask_radius(d->mask), kw = 2 * R + 1;
     auto q = [bf](float v) { return (double)(bf ? bf16_value_of(v) : v); };
     std::vector<double> wc((size_t)2 * M * M);
     for (int o = 0; o < 2 * M; ++o)
         for (int c = 0; c < M; ++c)
-            wc[(size_t)o * M + c] = q(d->ctx_w[(((size_t)o * M + c) * 5 + (dy + 2)) * 5 + (dx + 2)]);
+            wc[(size_t)o * M + c] = q(d->ctx_w[(((size_t)o * M + c) * kw + (dy + R)) * kw + (dx + R)]);
     out.assign((size_t)M * d1, 0.0);
     std::vector<double> acc(M);
     for (int n = 0; n < d1; ++n) {
@@ -264,8 +275,9 @@ static int build_plan(const wf_desc* d, Plan* p) {
     a.H = H; a.W = W; a.M = M; a.B = p->B; a.K = p->K; a.L = p->L; a.lambda = lam;
     a.Np1 = Np1; a.Np2 = p->Np2; a.n3 = p->n3; a.slope = p->slope; a.max_rows = p->max_rows;
     a.group = p->group;
-    a.ntaps = p->ntaps;
-    a.row_w = d->mask == WF_MASK_RELAXED ? 4 : 5;
+    const int R = mask_radius(d->mask), kw = 2 * R + 1;
+    a.R = R;
+    a.row_w = d->mask == WF_MASK_RELAXED ? 4 : kw;
     a.gparts = (M / kblock(p->precision) + kJobWaves - 1) / kJobWaves;   // one channel chunk per wave of a part
 
     // Split the taps by age (delta = steps between producer and consumer).
@@ -275,21 +287,29 @@ static int build_plan(const wf_desc* d, Plan* p) {
         (delta == 1 ? new_taps : old_taps).push_back(k);
     }
     if ((int)new_taps.size() != kMaxNew) return fail(WF_E_UNSUPPORTED, "mask must have two taps of age one");
-    a.n_new = (int)new_taps.size();
     a.ctx_parts = p->driver == WF_DRIVER_DATAFLOW ? kDfCtxParts : (bf ? kCtxPartsBf16 : kCtxPartsF32);
     a.n_old = (int)old_taps.size();
-    a.old_n0 = a.old_n1 = 0;
-    for (int o : old_taps) {
-        if (p->dy[o] == -2) a.old_n0++;
-        if (p->dy[o] == -1) a.old_n1++;
+    if (R > kMaxRadius) return fail(WF_E_UNSUPPORTED, "internal: mask radius too large");
+    int cnt[kMaxRadius + 1] = {};
+    for (int o : old_taps) cnt[p->dy[o] + R]++;
+    for (int q = 0, first = 0; q < kMaxRadius; ++q) {
+        first += cnt[q];
+        a.old_start[q] = q < R ? first : 1 << 30;
     }
     a.new_dx0 = p->dx[new_taps[0]];
     // the kernels rebuild every tap from these scalars: check that they can
     for (int o = 0; o < a.n_old; ++o) {
-        const int dy = o < a.old_n0 ? -2 : (o < a.old_n0 + a.old_n1 ? -1 : 0);
-        const int dx = o < a.old_n0 ? o - 2 : (o < a.old_n0 + a.old_n1 ? o - a.old_n0 - 2 : o - a.old_n0 - a.old_n1 - 2);
-        if (p->dy[old_taps[o]] != dy || p->dx[old_taps[o]] != dx)
-            return fail(WF_E_UNSUPPORTED, "old taps are not row-contiguous from dx = -2");
+        int row = 0;
+        while (row < kMaxRadius && o >= a.old_start[row]) ++row;
+        const int first = row == 0 ? 0 : a.old_start[row - 1];
+        if (p->dy[old_taps[o]] != row - R || p->dx[old_taps[o]] != o - first - R)
+            return fail(WF_E_UNSUPPORTED, "old taps are not row-contiguous from dx = -R");
+    }
+    for (int k = 0; k < p->ntaps; ++k) {
+        const int up = R * a.row_w;
+        const int dy = k < up ? k / a.row_w - R : 0;
+        const int dx = k < up ? k % a.row_w - R : k - up - R;
+        if (p->dy[k] != dy || p->dx[k] != dx) return fail(WF_E_UNSUPPORTED, "internal: mask is not raster-contiguous");
     }
     if (p->dy[new_taps[0]] != -1 || p->dy[new_taps[1]] != 0 || p->dx[new_taps[1]] != -1)
         return fail(WF_E_UNSUPPORTED, "unexpected new taps");
@@ -313,7 +333,7 @@ static int build_plan(const wf_desc* d, Plan* p) {
     auto wc_of = [&](const std::vector<int>& taps) {
         return [&, taps](int k, int n) {
             const int o = k / M, c = k % M;
-            return d->ctx_w[(((size_t)n * M + c) * 5 + (p->dy[taps[o]] + 2)) * 5 + (p->dx[taps[o]] + 2)];
+            return d->ctx_w[(((size_t)n * M + c) * kw + (p->dy[taps[o]] + R)) * kw + (p->dx[taps[o]] + R)];
         };
     };
     // all taps, channel-chunk-major k (chunk of kb channels, then the taps):
@@ -321,7 +341,7 @@ static int build_plan(const wf_desc* d, Plan* p) {
     auto wc_all = [&](int k, int n) {
         const int per = kbk * p->ntaps;
         const int q = k / per, rem = k - q * per, tap = rem / kbk, c = q * kbk + rem % kbk;
-        return d->ctx_w[(((size_t)n * M + c) * 5 + (p->dy[tap] + 2)) * 5 + (p->dx[tap] + 2)];
+        return d->ctx_w[(((size_t)n * M + c) * kw + (p->dy[tap] + R)) * kw + (p->dx[tap] + R)];
     };
     if (p->group > 1) {
         const int ka = p->ntaps * M;
@@ -339,8 +359,8 @@ static int build_plan(const wf_desc* d, Plan* p) {
     // Fold the new taps' conv into the context half of layer 1, and the
     // context bias into the hoisted part (bf16: from the bf16 weights).
     std::vector<float> b_hoist(Np1, 0.0f);
-    std::vector<std::vector<double>> fold(a.n_new);
-    for (int k = 0; k < a.n_new; ++k) fold_tap(d, p->dy[new_taps[k]], p->dx[new_taps[k]], bf, fold[k]);
+    std::vector<std::vector<double>> fold(kMaxNew);
+    for (int k = 0; k < kMaxNew; ++k) fold_tap(d, p->dy[new_taps[k]], p->dx[new_taps[k]], bf, fold[k]);
     for (int n = 0; n < d1; ++n) {
         double acc = d->b1[n];
         const float* w1r = d->w1 + (size_t)n * 4 * M + 2 * M;
@@ -348,7 +368,7 @@ static int build_plan(const wf_desc* d, Plan* p) {
         b_hoist[n] = (float)acc;
     }
     if (bf) {
-        const int kn = a.n_new * M, ko = a.n_old * M, Np2 = p->Np2, n3 = p->n3;
+        const int kn = kMaxNew * M, ko = a.n_old * M, Np2 = p->Np2, n3 = p->n3;
         // the folded block as a pair: hi = bf16(F), lo = bf16(F - hi)
         auto f_hi = [&](int k, int n) { return (float)fold[k / M][(size_t)(k % M) * d1 + n]; };
         auto f_lo = [&](int k, int n) {
@@ -364,7 +384,7 @@ static int build_plan(const wf_desc* d, Plan* p) {
         if ((rc = put(&a.wp2, Np2, Np1, pack_panel_bf16(d1, p->d2, Np1, Np2, w2f))) != WF_OK) return rc;
         if ((rc = put(&a.wp3, n3, Np2, pack_panel_bf16(p->d2, n3, Np2, n3, w3f))) != WF_OK) return rc;
     } else {
-        const int knew = a.n_new * M;
+        const int knew = kMaxNew * M;
         const int ko = a.n_old * M, Np2 = p->Np2, n3 = p->n3;
         if ((rc = put(&a.wp_hoist, Np1, 2 * M, pack_panel(2 * M, d1, 2 * M, Np1, w1a))) != WF_OK) return rc;
         if ((rc = put(&a.wp_l1, Np1, knew + 2 * M, pack_panel(knew + 2 * M, d1, knew + 2 * M, Np1, [&](int k, int n) {
@@ -388,23 +408,23 @@ static int build_plan(const wf_desc* d, Plan* p) {
     if ((rc = upload(p, &f, d->scale_table, (size_t)p->L)) != WF_OK) return rc;
     a.table = f;
 
-    const size_t R = (size_t)p->max_rows;
+    const size_t MR = (size_t)p->max_rows;
     const size_t nlat = (size_t)p->B * H * W;
     float *h1 = nullptr, *h2 = nullptr;
-    if ((rc = alloc(p, &h1, R * Np1)) != WF_OK) return rc;
-    if ((rc = alloc(p, &h2, R * p->Np2)) != WF_OK) return rc;
+    if ((rc = alloc(p, &h1, MR * Np1)) != WF_OK) return rc;
+    if ((rc = alloc(p, &h2, MR * p->Np2)) != WF_OK) return rc;
     a.h1 = h1;
     a.h2 = h2;
     a.h2b = h2;
     if (p->driver == WF_DRIVER_DATAFLOW) {
         // the dataflow driver double-buffers layer 2's output by step parity
         float* h2b = nullptr;
-        if ((rc = alloc(p, &h2b, R * p->Np2)) != WF_OK) return rc;
+        if ((rc = alloc(p, &h2b, MR * p->Np2)) != WF_OK) return rc;
         a.h2b = h2b;
     }
     if ((rc = alloc(p, &a.p1, nlat * Np1)) != WF_OK) return rc;
     const int nparts = std::max(kCtxPartsMax, p->group > 1 ? a.gparts : 0);
-    if ((rc = alloc(p, &a.ctxo, (size_t)2 * nparts * R * 2 * M)) != WF_OK) return rc;
+    if ((rc = alloc(p, &a.ctxo, (size_t)2 * nparts * MR * 2 * M)) != WF_OK) return rc;
     if (bf) {
         if ((rc = alloc(p, &a.ybf, nlat * 2 * M)) != WF_OK) return rc;
     }
@@ -466,7 +486,7 @@ const char* wf_last_error(void) { return g_err.c_str(); }
 int wf_schedule(int32_t H, int32_t W, int32_t mask, int32_t* step_of, int32_t* n_steps,
                 int32_t* lambda_out) {
     if (H < 1 || W < 1) return fail(WF_E_INVALID, "H and W must be positive");
-    if (mask != WF_MASK_FULL && mask != WF_MASK_RELAXED) return fail(WF_E_INVALID, "unknown mask");
+    if (mask_radius(mask) < 0) return fail(WF_E_INVALID, "unknown mask");
     if (!n_steps) return fail(WF_E_INVALID, "n_steps is NULL");
     int dy[kMaxTaps], dx[kMaxTaps];
     int nt = mask_taps(mask, dy, dx);

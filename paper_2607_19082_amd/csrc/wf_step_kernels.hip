@@ -17,11 +17,12 @@ __global__ __launch_bounds__(kThreads) void k_ctxo(StepRows s1, int j0, int nc, 
     ctxo_job<P, false>(a, s1, j0 + blockIdx.x, nc, red);
 }
 
-// Grouped decode: the context jobs of group s (all parts).
-template <class P>
+// Grouped decode: the context jobs of group s (all parts), for masks of at
+// most NT taps.
+template <class P, int NT>
 __global__ __launch_bounds__(kThreads) void k_gctx(StepRows s, int nc, StepArgs a) {
     __shared__ f4 red[kWaves * kMaxC][64];
-    gctx_job<P, false>(a, s, blockIdx.x, nc, red);
+    gctx_job<P, NT, false>(a, s, blockIdx.x, nc, red);
 }
 
 // Phase ph of step s (blocks [0, nb)), then old-tap context jobs [j0, ...)
@@ -80,12 +81,15 @@ static void launch_groups(Plan& p, hipStream_t stream) {
         const StepRows s{g, 0, 0, p.g_n[g], p.g_r0[g]};
         const int nrt = ntiles(s.nrows);
         const int nc = xcd_blocks(ncx, nrt);
-        hipLaunchKernelGGL(k_gctx<P>, dim3(nc * a.gparts), dim3(kThreads), 0, stream, s, nc, a);
+        if (p.ntaps <= kTaps5x5)
+            hipLaunchKernelGGL((k_gctx<P, kTaps5x5>), dim3(nc * a.gparts), dim3(kThreads), 0, stream, s, nc, p.args);
+        else
+            hipLaunchKernelGGL((k_gctx<P, kMaxTaps>), dim3(nc * a.gparts), dim3(kThreads), 0, stream, s, nc, p.args);
         const int nb[3] = {xcd_blocks(a.Np1 / kTile / P::kC, nrt), phase_blocks<P>(a, s, PH_B),
                            phase_blocks<P>(a, s, PH_C)};
         const int ph[3] = {PH_GA, PH_B, PH_C};
         for (int k = 0; k < 3; ++k)
-            hipLaunchKernelGGL((k_phase<P, KC>), dim3(nb[k]), dim3(kThreads), 0, stream, ph[k], s, s, nb[k], 0, 0, a);
+            hipLaunchKernelGGL((k_phase<P, KC>), dim3(nb[k]), dim3(kThreads), 0, stream, ph[k], s, s, nb[k], 0, 0, p.args);
     }
 }
 
@@ -103,10 +107,10 @@ static void launch_steps(Plan& p, hipStream_t stream) {
         // the last part adds the others, so it runs after them
         const int split = (P::kParts - 1) * nc;
         if (nc > 0) {
-            hipLaunchKernelGGL(k_ctxo<P>, dim3(split), dim3(kThreads), 0, stream, s0, 0, nc, a);
+            hipLaunchKernelGGL(k_ctxo<P>, dim3(split), dim3(kThreads), 0, stream, s0, 0, nc, p.args);
             if (split < P::kParts * nc)
                 hipLaunchKernelGGL(k_ctxo<P>, dim3(P::kParts * nc - split), dim3(kThreads), 0, stream, s0, split, nc,
-                                   a);
+                                   p.args);
         }
     }
     for (int t = 0; t < p.T; ++t) {
@@ -115,7 +119,7 @@ static void launch_steps(Plan& p, hipStream_t stream) {
         for (int ph = P::kFirst; ph < kMaxPhases; ++ph) {
             const int n = w.nb[ph] + w.cut[ph + 1] - w.cut[ph];
             hipLaunchKernelGGL((k_phase<P, KC>), dim3(n), dim3(kThreads), 0, stream, ph, s, s1, w.nb[ph],
-                               w.cut[ph], w.nc, a);
+                               w.cut[ph], w.nc, p.args);
         }
     }
 }

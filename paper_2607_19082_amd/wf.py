@@ -13,7 +13,8 @@ _PKG = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_PKG, "libwf.so")
 
 WF_OK, WF_E_INVALID, WF_E_UNSUPPORTED, WF_E_HIP, WF_E_NOMEM, WF_E_TIMEOUT = 0, -1, -2, -3, -4, -5
-MASK = {"full": 0, "relaxed": 1}
+MASK = {"full": 0, "relaxed": 1, "3x3": 2, "7x7": 3}
+KERNEL = {"full": 5, "relaxed": 5, "3x3": 3, "7x7": 7}   # ctx_w's spatial size per mask
 PRECISION = {"fp32": 0, "bf16": 1}
 DRIVER = {"stream": 0, "graph": 1, "persistent": 2, "dataflow": 3}
 
@@ -100,6 +101,9 @@ def make_desc(weights, table, H, W, B=1, K=1, mask="full", precision="fp32", dri
     arrs = {k: np.ascontiguousarray(v, dtype=np.float32) for k, v in weights.items()}
     arrs["table"] = np.ascontiguousarray(table, dtype=np.float32)
     M = arrs["ctx_w"].shape[1]
+    k = KERNEL[mask]
+    if arrs["ctx_w"].shape != (2 * M, M, k, k):
+        raise ValueError(f"ctx_w must have shape (2M, M, {k}, {k}) for the {mask} mask, got {arrs['ctx_w'].shape}")
     d = Desc(H, W, M, B, K, arrs["w1"].shape[0], arrs["w2"].shape[0], MASK[mask],
              PRECISION[precision], DRIVER[driver], slope,
              arrs["ctx_w"].ctypes.data, arrs["ctx_b"].ctypes.data,

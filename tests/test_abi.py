@@ -40,9 +40,10 @@ def test_exports_every_declared_symbol(lib):
     assert sorted(wf.EXPORTS) == names
 
 
-@pytest.mark.parametrize("mask,relaxed,lam", [("full", False, 3), ("relaxed", True, 2)])
-def test_schedule_matches_oracle(lib, mask, relaxed, lam):
-    ds = S.dependence_vectors(5, relaxed=relaxed)
+@pytest.mark.parametrize("mask,kernel,relaxed,lam", [("full", 5, False, 3), ("relaxed", 5, True, 2),
+                                                     ("3x3", 3, False, 2), ("7x7", 7, False, 4)])
+def test_schedule_matches_oracle(lib, mask, kernel, relaxed, lam):
+    ds = S.dependence_vectors(kernel, relaxed=relaxed)
     for H in range(1, 10):
         for W in range(lam, 12):
             step, n, got_lam = wf.schedule(H, W, mask)
@@ -76,7 +77,12 @@ def test_schedule_errors(lib):
     assert lib.wf_schedule(5, 2, 0, None, ctypes.byref(n), None) == wf.WF_E_UNSUPPORTED
     assert lib.wf_schedule(5, 1, 1, None, ctypes.byref(n), None) == wf.WF_E_UNSUPPORTED
     assert lib.wf_schedule(5, 2, 1, None, ctypes.byref(n), None) == wf.WF_OK
+    assert lib.wf_schedule(5, 1, 2, None, ctypes.byref(n), None) == wf.WF_E_UNSUPPORTED
+    assert lib.wf_schedule(5, 2, 2, None, ctypes.byref(n), None) == wf.WF_OK
+    assert lib.wf_schedule(5, 3, 3, None, ctypes.byref(n), None) == wf.WF_E_UNSUPPORTED
     assert b"shear" in lib.wf_last_error()
+    assert lib.wf_schedule(5, 4, 3, None, ctypes.byref(n), None) == wf.WF_OK
+    assert lib.wf_schedule(5, 5, 4, None, ctypes.byref(n), None) == wf.WF_E_INVALID
 
 
 def _desc(**kw):
@@ -112,7 +118,7 @@ def test_validate(lib):
     d.H = 0
     assert wf.validate(d) == wf.WF_E_INVALID
     d, keep = _desc()
-    d.mask = 3
+    d.mask = 4
     assert wf.validate(d) == wf.WF_E_INVALID
     d, keep = _desc()
     d.driver = 9
@@ -142,3 +148,17 @@ def test_null_arguments_rejected(lib):
     assert lib.wf_plan_sync(None, None) == wf.WF_E_INVALID
     assert lib.wf_plan_schedule(None, None, None) == wf.WF_E_INVALID
     lib.wf_plan_destroy(None)
+
+
+@pytest.mark.parametrize("mask,R,W_min", [("3x3", 1, 2), ("full", 2, 3), ("7x7", 3, 4)])
+def test_masks_of_any_radius(lib, mask, R, W_min):
+    """The (2R+1)x(2R+1) masks validate with weights of their own kernel size;
+    the binding refuses weights of another size before any pointer is read."""
+    w = inputs.make_weights(16, 1, radius=R)
+    d, keep = wf.make_desc(w, inputs.scale_table(), 4, W_min, mask=mask)
+    assert wf.validate(d) == wf.WF_OK
+    d.W = W_min - 1
+    assert wf.validate(d) == wf.WF_E_UNSUPPORTED
+    other = inputs.make_weights(16, 1, radius=1 if R != 1 else 2)
+    with pytest.raises(ValueError):
+        wf.make_desc(other, inputs.scale_table(), 4, W_min, mask=mask)
