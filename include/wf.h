@@ -8,7 +8,9 @@
  * Def. 1).  The linear rank t(i,j) = lambda*i + j with the smallest shear
  * lambda that satisfies the hyperplane condition (Sec. III-B, Eq. 5-7) is a
  * valid schedule with W + lambda*(H-1) steps, optimal when W >= lambda
- * (Appendix A, Thm. 1).  All latents of one step (a wavefront) are decoded
+ * (Appendix A, Thm. 1).  On a narrower grid (W < lambda) every latent
+ * depends on its raster predecessor, so the earliest-possible schedule is the
+ * raster order itself: the shear W, H*W steps.  All latents of one step (a wavefront) are decoded
  * together: their causal taps are gathered from the reconstruction
  * (Sec. III-C, selective im2col), the masked-conv context and the 1x1
  * entropy-parameter network are evaluated as batched products, and the
@@ -70,6 +72,14 @@ typedef enum {
                                depends on (per-step, per-row-tile completion counters)     */
 } wf_driver;
 
+/* Block order of the last layer's output rows (w3, b3).  The kernels use the
+ * native order; a checkpoint whose entropy-parameter head emits the scales
+ * first is imported by naming its order here (the plan permutes the rows). */
+typedef enum {
+    WF_ORDER_NATIVE = 0,       /* K = 1: mean | scale;  K = 3: weight | mean | scale */
+    WF_ORDER_SCALES_FIRST = 1  /* K = 1: scale | mean;  K = 3: scale | mean | weight */
+} wf_param_order;
+
 /*
  * Model and problem description.  All weight arrays are HOST memory in
  * PyTorch layouts and are copied (and repacked) by wf_plan.
@@ -80,7 +90,9 @@ typedef enum {
  *   w2 [d2][d1], b2 [d2]
  *   w3 [n3][d2], b3 [n3]   n3 = 2M for K = 1 (rows: mean | scale),
  *                          n3 = 9M for K = 3 (rows: weight | mean | scale,
- *                          each block component-major: block*3M + k*M + c)
+ *                          each block component-major: block*3M + k*M + c);
+ *                          with param_order = WF_ORDER_SCALES_FIRST the blocks
+ *                          come in the order scale | mean (| weight)
  *   scale_table [L]        strictly increasing, positive
  * Hidden layers use LeakyReLU with slope lrelu_slope; the last layer is linear.
  */
@@ -104,6 +116,7 @@ typedef struct {
                                by channel, by the mean of its decoded in-image taps (zero
                                when none is decoded).  N > 1 needs the stream or graph
                                driver (WF_E_UNSUPPORTED otherwise).                      */
+    int32_t param_order;    /* wf_param_order: block order of the rows of w3 and b3        */
 } wf_desc;
 
 /*
@@ -130,9 +143,10 @@ typedef struct wf_plan_s *wf_plan_t;
  * Writes step_of[i*W + j] = lambda*i + j (HOST array of H*W int32, may be
  * NULL) and *n_steps = W + lambda*(H-1), where lambda is the least integer
  * shear with lambda*di + dj > 0 for every dependence vector of the mask
- * (Sec. III-B, Eq. 6-7).  Also writes *lambda_out when non-NULL.
- * Errors: WF_E_INVALID for H < 1, W < 1, an unknown mask or a NULL n_steps;
- * WF_E_UNSUPPORTED when W < lambda (Thm. 1 needs W >= lambda for optimality).
+ * (Sec. III-B, Eq. 6-7), or W when W is smaller (the raster order, which is
+ * then the earliest-possible schedule).  Also writes *lambda_out when
+ * non-NULL.
+ * Errors: WF_E_INVALID for H < 1, W < 1, an unknown mask or a NULL n_steps.
  */
 int wf_schedule(int32_t H, int32_t W, int32_t mask, int32_t *step_of,
                 int32_t *n_steps, int32_t *lambda_out);

@@ -53,6 +53,12 @@ static int mask_taps(int mask, int* dy, int* dx) {
     return n;
 }
 
+// Shear of the schedule of a W-wide grid: the mask's least shear, or W when
+// the grid is narrower.  Then every latent depends on its raster predecessor
+// (through (0,-1), or (-1, W-1) for the first of a row: W - 1 < lambda - 1 = R),
+// so the raster order t = W*i + j is the earliest-possible schedule.
+static int schedule_shear(int lam, int W) { return W < lam ? W : lam; }
+
 // Least integer shear lambda >= 0 with lambda*di + dj > 0 for every
 // dependence vector d = (-dy, -dx) of the taps (Sec. III-B, Eq. 6-7).
 static int least_shear(int ntaps, const int* dy, const int* dx) {
@@ -96,13 +102,16 @@ static int check_desc(const wf_desc* d) {
     }
     if (!std::isfinite(d->lrelu_slope)) return fail(WF_E_INVALID, "lrelu_slope must be finite");
     if (d->group < 0) return fail(WF_E_INVALID, "group must be >= 0");
+    if (d->param_order != WF_ORDER_NATIVE && d->param_order != WF_ORDER_SCALES_FIRST)
+        return fail(WF_E_INVALID, "unknown param_order");
     if (d->group > 1 && d->driver != WF_DRIVER_STREAM && d->driver != WF_DRIVER_GRAPH)
         return fail(WF_E_UNSUPPORTED, "context approximation (group > 1) needs the stream or graph driver");
     if (d->M % kTile != 0) return fail(WF_E_UNSUPPORTED, "M must be a multiple of 16");
     int dy[kMaxTaps], dx[kMaxTaps];
     int nt = mask_taps(d->mask, dy, dx);
     int lam = least_shear(nt, dy, dx);
-    if (d->W < lam) return fail(WF_E_UNSUPPORTED, "W must be at least the shear factor (Thm. 1)");
+    if (d->W < lam && d->group > 1)
+        return fail(WF_E_UNSUPPORTED, "context approximation needs W at least the shear factor (Thm. 1)");
     // every array the kernels read through raw buffer instructions (psi, y_hat,
     // the per-step activations) must fit the buffer window
     const long long lat = (long long)d->B * d->H * d->W;
@@ -223,7 +232,7 @@ static int build_plan(const wf_desc* d, Plan* p) {
     p->mask = d->mask; p->precision = d->precision; p->driver = d->driver;
     p->L = d->L; p->slope = d->lrelu_slope;
     p->ntaps = mask_taps(d->mask, p->dy, p->dx);
-    p->lambda = least_shear(p->ntaps, p->dy, p->dx);
+    p->lambda = schedule_shear(least_shear(p->ntaps, p->dy, p->dx), d->W);
     const int H = p->H, W = p->W, M = p->M, lam = p->lambda;
     p->T = W + lam * (H - 1);
     p->group = d->group > 1 ? d->group : 1;
@@ -281,9 +290,13 @@ static int build_plan(const wf_desc* d, Plan* p) {
     a.gparts = (M / kblock(p->precision) + kJobWaves - 1) / kJobWaves;   // one channel chunk per wave of a part
 
     // Split the taps by age (delta = steps between producer and consumer).
+    // On a grid narrower than the mask's shear, taps of the rows above at
+    // dx >= W never lie in the grid; the exact decode leaves them out.
     std::vector<int> new_taps, old_taps;
     for (int k = 0; k < p->ntaps; ++k) {
+        if (p->dy[k] < 0 && p->dx[k] >= W) continue;
         const int delta = lam * (-p->dy[k]) - p->dx[k];
+        if (delta < 1) return fail(WF_E_UNSUPPORTED, "internal: a tap is not decoded before its consumer");
         (delta == 1 ? new_taps : old_taps).push_back(k);
     }
     if ((int)new_taps.size() != kMaxNew) return fail(WF_E_UNSUPPORTED, "mask must have two taps of age one");
@@ -355,7 +368,17 @@ static int build_plan(const wf_desc* d, Plan* p) {
     auto w1a = [&](int k, int n) { return d->w1[(size_t)n * 4 * M + k]; };
     auto w1b = [&](int k, int n) { return d->w1[(size_t)n * 4 * M + 2 * M + k]; };
     auto w2f = [&](int k, int n) { return d->w2[(size_t)n * d1 + k]; };
-    auto w3f = [&](int k, int n) { return d->w3[(size_t)n * p->d2 + k]; };
+    // the last layer's rows in the native block order
+    std::vector<int> row3(p->n3);
+    {
+        const int nb = p->K == 1 ? 2 : 3, bs = p->n3 / nb;   // blocks of bs rows
+        for (int b = 0; b < nb; ++b)
+            for (int r = 0; r < bs; ++r)
+                row3[b * bs + r] = (d->param_order == WF_ORDER_SCALES_FIRST ? nb - 1 - b : b) * bs + r;
+    }
+    std::vector<float> b3(p->n3);
+    for (int n = 0; n < p->n3; ++n) b3[n] = d->b3[row3[n]];
+    auto w3f = [&](int k, int n) { return d->w3[(size_t)row3[n] * p->d2 + k]; };
     // Fold the new taps' conv into the context half of layer 1, and the
     // context bias into the hoisted part (bf16: from the bf16 weights).
     std::vector<float> b_hoist(Np1, 0.0f);
@@ -403,7 +426,7 @@ static int build_plan(const wf_desc* d, Plan* p) {
     a.b_hoist = f;
     if ((rc = upload(p, &f, b2.data(), b2.size())) != WF_OK) return rc;
     a.b2 = f;
-    if ((rc = upload(p, &f, d->b3, (size_t)p->n3)) != WF_OK) return rc;
+    if ((rc = upload(p, &f, b3.data(), b3.size())) != WF_OK) return rc;
     a.b3 = f;
     if ((rc = upload(p, &f, d->scale_table, (size_t)p->L)) != WF_OK) return rc;
     a.table = f;
@@ -490,8 +513,7 @@ int wf_schedule(int32_t H, int32_t W, int32_t mask, int32_t* step_of, int32_t* n
     if (!n_steps) return fail(WF_E_INVALID, "n_steps is NULL");
     int dy[kMaxTaps], dx[kMaxTaps];
     int nt = mask_taps(mask, dy, dx);
-    int lam = least_shear(nt, dy, dx);
-    if (W < lam) return fail(WF_E_UNSUPPORTED, "W must be at least the shear factor (Thm. 1)");
+    const int lam = schedule_shear(least_shear(nt, dy, dx), W);
     if (step_of)
         for (int i = 0; i < H; ++i)
             for (int j = 0; j < W; ++j) step_of[(size_t)i * W + j] = lam * i + j;

@@ -14,6 +14,7 @@ LIB_PATH = os.path.join(_PKG, "libwf.so")
 
 WF_OK, WF_E_INVALID, WF_E_UNSUPPORTED, WF_E_HIP, WF_E_NOMEM, WF_E_TIMEOUT = 0, -1, -2, -3, -4, -5
 MASK = {"full": 0, "relaxed": 1, "3x3": 2, "7x7": 3}
+PARAM_ORDER = {"native": 0, "scales_first": 1}
 KERNEL = {"full": 5, "relaxed": 5, "3x3": 3, "7x7": 7}   # ctx_w's spatial size per mask
 PRECISION = {"fp32": 0, "bf16": 1}
 DRIVER = {"stream": 0, "graph": 1, "persistent": 2, "dataflow": 3}
@@ -41,7 +42,7 @@ class Desc(ctypes.Structure):
         ("w2", ctypes.c_void_p), ("b2", ctypes.c_void_p),
         ("w3", ctypes.c_void_p), ("b3", ctypes.c_void_p),
         ("scale_table", ctypes.c_void_p), ("L", ctypes.c_int32),
-        ("group", ctypes.c_int32),
+        ("group", ctypes.c_int32), ("param_order", ctypes.c_int32),
     ]
 
 
@@ -96,7 +97,7 @@ def schedule(H, W, mask="full"):
 
 
 def make_desc(weights, table, H, W, B=1, K=1, mask="full", precision="fp32", driver="stream",
-              slope=0.01, group=1):
+              slope=0.01, group=1, param_order="native"):
     """Build a Desc plus the host arrays it points to (keep both alive)."""
     arrs = {k: np.ascontiguousarray(v, dtype=np.float32) for k, v in weights.items()}
     arrs["table"] = np.ascontiguousarray(table, dtype=np.float32)
@@ -110,7 +111,7 @@ def make_desc(weights, table, H, W, B=1, K=1, mask="full", precision="fp32", dri
              arrs["w1"].ctypes.data, arrs["b1"].ctypes.data,
              arrs["w2"].ctypes.data, arrs["b2"].ctypes.data,
              arrs["w3"].ctypes.data, arrs["b3"].ctypes.data,
-             arrs["table"].ctypes.data, len(arrs["table"]), group)
+             arrs["table"].ctypes.data, len(arrs["table"]), group, PARAM_ORDER[param_order])
     return d, arrs
 
 
@@ -130,8 +131,9 @@ class Plan:
     current) torch stream."""
 
     def __init__(self, weights, table, H, W, B=1, K=1, mask="full", precision="fp32",
-                 driver="stream", slope=0.01, group=1):
-        self.desc, self._arrs = make_desc(weights, table, H, W, B, K, mask, precision, driver, slope, group)
+                 driver="stream", slope=0.01, group=1, param_order="native"):
+        self.desc, self._arrs = make_desc(weights, table, H, W, B, K, mask, precision, driver, slope, group,
+                                          param_order)
         self.group = group
         self.H, self.W, self.B, self.K = H, W, B, K
         self.M = self.desc.M

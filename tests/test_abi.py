@@ -43,14 +43,17 @@ def test_exports_every_declared_symbol(lib):
 @pytest.mark.parametrize("mask,kernel,relaxed,lam", [("full", 5, False, 3), ("relaxed", 5, True, 2),
                                                      ("3x3", 3, False, 2), ("7x7", 7, False, 4)])
 def test_schedule_matches_oracle(lib, mask, kernel, relaxed, lam):
+    """The library's schedule is the earliest-possible one (ASAP levels of the
+    brute-force DAG) on every grid, also those narrower than the shear, where
+    it is the raster order."""
     ds = S.dependence_vectors(kernel, relaxed=relaxed)
     for H in range(1, 10):
-        for W in range(lam, 12):
+        for W in range(1, 12):
             step, n, got_lam = wf.schedule(H, W, mask)
-            assert got_lam == lam
+            assert got_lam == min(lam, W)
             asap = np.array(S.asap_levels(H, W, ds), np.int32)
-            assert np.array_equal(step, asap)
-            assert n == S.critical_path_steps(H, W, ds) == W + lam * (H - 1)
+            assert np.array_equal(step, asap), (H, W)
+            assert n == S.critical_path_steps(H, W, ds) == W + got_lam * (H - 1)
 
 
 @pytest.mark.parametrize("H,W,mask", [(135, 240, "full"), (68, 120, "relaxed"), (32, 48, "full")])
@@ -74,15 +77,12 @@ def test_schedule_errors(lib):
     assert lib.wf_schedule(0, 5, 0, None, ctypes.byref(n), None) == wf.WF_E_INVALID
     assert lib.wf_schedule(5, 5, 7, None, ctypes.byref(n), None) == wf.WF_E_INVALID
     assert lib.wf_schedule(5, 5, 0, None, None, None) == wf.WF_E_INVALID
-    assert lib.wf_schedule(5, 2, 0, None, ctypes.byref(n), None) == wf.WF_E_UNSUPPORTED
-    assert lib.wf_schedule(5, 1, 1, None, ctypes.byref(n), None) == wf.WF_E_UNSUPPORTED
-    assert lib.wf_schedule(5, 2, 1, None, ctypes.byref(n), None) == wf.WF_OK
-    assert lib.wf_schedule(5, 1, 2, None, ctypes.byref(n), None) == wf.WF_E_UNSUPPORTED
-    assert lib.wf_schedule(5, 2, 2, None, ctypes.byref(n), None) == wf.WF_OK
-    assert lib.wf_schedule(5, 3, 3, None, ctypes.byref(n), None) == wf.WF_E_UNSUPPORTED
-    assert b"shear" in lib.wf_last_error()
-    assert lib.wf_schedule(5, 4, 3, None, ctypes.byref(n), None) == wf.WF_OK
     assert lib.wf_schedule(5, 5, 4, None, ctypes.byref(n), None) == wf.WF_E_INVALID
+    # grids narrower than the shear: the raster order, H*W steps
+    lam = ctypes.c_int32()
+    for mask, W in ((0, 2), (1, 1), (2, 1), (3, 3), (3, 1)):
+        assert lib.wf_schedule(5, W, mask, None, ctypes.byref(n), ctypes.byref(lam)) == wf.WF_OK
+        assert (n.value, lam.value) == (5 * W, W)
 
 
 def _desc(**kw):
@@ -97,8 +97,13 @@ def _desc(**kw):
 def test_validate(lib):
     d, keep = _desc()
     assert wf.validate(d) == wf.WF_OK
+    # narrower than the shear: the exact decode runs in raster order, context
+    # approximation (defined on the wavefronts t = lambda*i + j) is refused
     d, keep = _desc(W=2)
+    assert wf.validate(d) == wf.WF_OK
+    d.group = 2
     assert wf.validate(d) == wf.WF_E_UNSUPPORTED
+    assert b"shear" in lib.wf_last_error()
     d, keep = _desc(M=8)
     assert wf.validate(d) == wf.WF_E_UNSUPPORTED
     # bf16 operands: a k-block of 32 channels must not straddle two taps
@@ -122,6 +127,10 @@ def test_validate(lib):
     assert wf.validate(d) == wf.WF_E_INVALID
     d, keep = _desc()
     d.driver = 9
+    assert wf.validate(d) == wf.WF_E_INVALID
+    d, keep = _desc(param_order="scales_first")
+    assert wf.validate(d) == wf.WF_OK
+    d.param_order = 2
     assert wf.validate(d) == wf.WF_E_INVALID
     # context approximation: group size >= 0; groups need a per-step-launch driver
     d, keep = _desc()
@@ -158,6 +167,8 @@ def test_masks_of_any_radius(lib, mask, R, W_min):
     d, keep = wf.make_desc(w, inputs.scale_table(), 4, W_min, mask=mask)
     assert wf.validate(d) == wf.WF_OK
     d.W = W_min - 1
+    assert wf.validate(d) == wf.WF_OK
+    d.group = 3
     assert wf.validate(d) == wf.WF_E_UNSUPPORTED
     other = inputs.make_weights(16, 1, radius=1 if R != 1 else 2)
     with pytest.raises(ValueError):

@@ -1,6 +1,8 @@
 """GPU parity for causal masks of other radii (Appendix A, Def. 1): the 3x3
 mask (R = 1, shear 2) and the 7x7 mask (R = 3, shear 4), through the C-ABI
-against the oracle's decode with the same (2R+1)x(2R+1) weights.
+against the oracle's decode with the same (2R+1)x(2R+1) weights; and grids
+narrower than a mask's shear, which every mask decodes in raster order (the
+earliest-possible schedule there).
 
 Every driver runs the exact decode and encode; the stream and graph drivers
 also run the context-approximation decode (Sec. III-D).  Bars as for the 5x5
@@ -25,7 +27,8 @@ pytestmark = pytest.mark.gpu
 
 torch = pytest.importorskip("torch")
 
-RADIUS = {"3x3": 1, "7x7": 3}
+RADIUS = {"3x3": 1, "7x7": 3, "full": 2, "relaxed": 2}
+SHEAR = {"3x3": 2, "7x7": 4, "full": 3, "relaxed": 2}
 
 
 @pytest.fixture(scope="module", autouse=True)
@@ -49,8 +52,9 @@ def case(name, mask, H=None, W=None, B=None):
     return cfg, w, table, psi, sym
 
 
-def model(cfg, w, table, bf16=False, group=1, H=None):
-    return oracle.Model(w, table, H or cfg["H"], cfg["W"], cfg["B"], cfg["K"], bf16=bf16, group=group)
+def model(cfg, w, table, bf16=False, group=1, H=None, mask=None):
+    return oracle.Model(w, table, H or cfg["H"], cfg["W"], cfg["B"], cfg["K"], relaxed=mask == "relaxed", bf16=bf16,
+                        group=group)
 
 
 def plan(cfg, w, table, mask, driver, precision, group=1):
@@ -60,7 +64,7 @@ def plan(cfg, w, table, mask, driver, precision, group=1):
 
 def check_schedule(p, cfg, mask, group):
     step, n = p.schedule()
-    lam = RADIUS[mask] + 1
+    lam = min(SHEAR[mask], cfg["W"])
     T = cfg["W"] + lam * (cfg["H"] - 1)
     assert n == -(-T // group)
     ii, jj = np.meshgrid(np.arange(cfg["H"]), np.arange(cfg["W"]), indexing="ij")
@@ -70,7 +74,7 @@ def check_schedule(p, cfg, mask, group):
 def decode_encode(cfg, w, table, psi, sym, mask, driver, precision, group):
     bf = precision == "bf16"
     tol = BF16_TOL if bf else FP32_TOL
-    ref = model(cfg, w, table, bf, group).decode(psi, sym)
+    ref = model(cfg, w, table, bf, group, mask=mask).decode(psi, sym)
     p = plan(cfg, w, table, mask, driver, precision, group)
     check_schedule(p, cfg, mask, group)
     out = p.decode(torch.from_numpy(psi).cuda(), torch.from_numpy(sym).cuda())
@@ -113,13 +117,23 @@ def test_mask_grouped_small(name, H, W, B, mask, precision, driver, N):
     decode_encode(cfg, w, table, psi, sym, mask, driver, precision, N)
 
 
-def test_mask_narrow_grid():
-    """W equal to the shear (the narrowest grid the schedule allows)."""
+def test_mask_grid_as_wide_as_the_shear():
     for mask in ("3x3", "7x7"):
-        lam = RADIUS[mask] + 1
-        log(f"mask narrow case W={lam} mask={mask}")
+        lam = SHEAR[mask]
+        log(f"mask case W={lam} mask={mask}")
         cfg, w, table, psi, sym = case("minnen-16x16-m192", mask, 6, lam, 2)
         decode_encode(cfg, w, table, psi, sym, mask, "graph", "fp32", 1)
+
+
+@pytest.mark.parametrize("driver", ["stream", "graph", "persistent", "dataflow"])
+@pytest.mark.parametrize("precision", ["fp32", "bf16"])
+@pytest.mark.parametrize("mask", ["full", "relaxed", "3x3", "7x7"])
+def test_grid_narrower_than_the_shear(mask, precision, driver):
+    """Every W below the shear: one latent per image and step, raster order."""
+    for W in range(1, SHEAR[mask]):
+        log(f"narrow case W={W} mask={mask} precision={precision} driver={driver}")
+        cfg, w, table, psi, sym = case("cheng-gmm3-1080p-120x68-m192", mask, 5, W, 2)
+        decode_encode(cfg, w, table, psi, sym, mask, driver, precision, 1)
 
 
 @pytest.mark.parametrize("mask,precision,N", [("7x7", "fp32", 1), ("7x7", "bf16", 1), ("3x3", "fp32", 1),
