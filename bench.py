@@ -163,7 +163,8 @@ def summarize_stats(stats_dir, log, out, command):
     cfg = rec["config"]
     lines = [f"# Kernel statistics: {cfg['workload']}, {cfg['precision']}, {cfg['driver']} driver"
              + (f", context approximation N = {cfg['context_approximation_group']}"
-                if cfg.get("context_approximation_group", 1) > 1 else ""), "",
+                if cfg.get("context_approximation_group", 1) > 1 else "")
+             + (f", {cfg['mask']} mask" if cfg.get("mask") not in (None, "full", "relaxed") else ""), "",
              "Command (on one MI355X, from the repository root):", "", "```", command, "```", "",
              f"The run makes {calls} decode/encode calls (warm-up, timed decodes, encodes); per-call kernels appear "
              f"that many times.  k_empty and k_barrier_rounds are the latency-floor probes of the bench.", "",
@@ -296,7 +297,7 @@ def main():
                     help="causal mask (default: the workload's own), weights drawn for its kernel size")
     ap.add_argument("--group", type=int, default=1,
                     help="context approximation: decode N wavefronts per step (1: exact decode)")
-    ap.add_argument("--cpu-rows", type=int, default=8, help="grid rows of the CPU-oracle sample (0: skip)")
+    ap.add_argument("--cpu-rows", type=int, default=16, help="grid rows of the CPU-oracle sample (0: skip)")
     ap.add_argument("--no-encode", action="store_true")
     ap.add_argument("--summarize-traffic", nargs=4, metavar=("FETCH_DIR", "WRITE_DIR", "CAL_FETCH_DIR", "CAL_WRITE_DIR"),
                     help="write the traffic summary of this workload/precision/driver from rocprofv3 outputs")
