@@ -11,6 +11,11 @@ and this package never imports the GPU path.
   With ``group`` N > 1 it is the context-approximation decode of Sec. III-D
   (Fig. 3): groups of N wavefronts, same-group taps filled with the mean of
   the decoded taps.
+* ``wf_rans.c`` -- rANS entropy coding of the symbols under the mean-scale
+  Gaussian model (Sec. II-A; the coder the paper pairs with the wavefront
+  decode, Sec. III-C): per-level frequency tables built from the scale
+  table, one stream per (image, grid row, channel), and the model decode that
+  takes its symbols from those streams.
 * ``schedule.py`` -- the dependency DAG of the mask (Eq. 3, Def. 1), its ASAP
   levels and critical path, and a brute-force search over linear schedules
   (Sec. III-B, Eq. 5-7; Appendix A, Thm. 1).
@@ -23,6 +28,7 @@ import numpy as np
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
 _SRC = os.path.join(_HERE, "wf_oracle.c")
+_SRCS = [_SRC, os.path.join(_HERE, "wf_rans.c")]
 _LIB = os.path.join(_HERE, "liboracle.so")
 _lib = None
 
@@ -30,7 +36,7 @@ _lib = None
 def build():
     """Compile the C oracle with gcc (-O2, no fast-math, single thread)."""
     cmd = ["gcc", "-O2", "-std=c11", "-fPIC", "-shared", "-Wall", "-Wextra",
-           "-fno-fast-math", "-ffp-contract=off", "-o", _LIB, _SRC, "-lm"]
+           "-fno-fast-math", "-ffp-contract=off", "-o", _LIB] + _SRCS + ["-lm"]
     subprocess.run(cmd, check=True)
     return _LIB
 
@@ -62,7 +68,8 @@ class _Out(ctypes.Structure):
 def _load():
     global _lib
     if _lib is None:
-        if not os.path.exists(_LIB) or os.path.getmtime(_LIB) < os.path.getmtime(_SRC):
+        srcs = _SRCS + [os.path.join(_HERE, "wf_rans.h")]
+        if not os.path.exists(_LIB) or os.path.getmtime(_LIB) < max(os.path.getmtime(f) for f in srcs):
             build()
         lib = ctypes.CDLL(_LIB)
         lib.oracle_run.argtypes = [ctypes.POINTER(_Model), ctypes.c_void_p, ctypes.c_void_p,
@@ -75,6 +82,18 @@ def _load():
         lib.oracle_tap_status.argtypes = [ctypes.POINTER(_Model), ctypes.c_int, ctypes.c_int,
                                           ctypes.c_int, ctypes.c_int]
         lib.oracle_tap_status.restype = ctypes.c_int
+        lib.oracle_run_bits.argtypes = [ctypes.POINTER(_Model), ctypes.c_void_p, ctypes.c_void_p,
+                                        ctypes.c_void_p, ctypes.c_void_p, ctypes.POINTER(_Out)]
+        lib.oracle_run_bits.restype = ctypes.c_int
+        lib.oracle_rans_tables.argtypes = [ctypes.c_void_p, ctypes.c_int, ctypes.c_void_p, ctypes.c_void_p,
+                                           ctypes.c_void_p, ctypes.c_int64]
+        lib.oracle_rans_tables.restype = ctypes.c_int64
+        lib.oracle_rans_encode.argtypes = [ctypes.c_void_p, ctypes.c_void_p] + [ctypes.c_int] * 4 + [
+            ctypes.c_void_p, ctypes.c_int, ctypes.c_void_p, ctypes.c_int64, ctypes.c_void_p]
+        lib.oracle_rans_encode.restype = ctypes.c_int64
+        lib.oracle_rans_decode.argtypes = [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p] + [ctypes.c_int] * 4 + [
+            ctypes.c_void_p, ctypes.c_int, ctypes.c_void_p]
+        lib.oracle_rans_decode.restype = ctypes.c_int
         _lib = lib
     return _lib
 
@@ -172,6 +191,23 @@ class Model:
             raise RuntimeError("oracle_run failed")
         return self._shape(outs), sym.reshape(self.B, self.H, self.W, self.M)
 
+    def decode_bits(self, psi, bits, offsets):
+        """Decode with the symbols read from rANS streams (``rans_encode``'s
+        layout); K = 1.  Returns (outputs, decoded symbols)."""
+        psi = _f32(psi)
+        bits = np.ascontiguousarray(bits, dtype=np.uint32)
+        offsets = np.ascontiguousarray(offsets, dtype=np.uint32)
+        n = self.B * self.H * self.W
+        if offsets.size != self.B * self.H * self.M + 1:
+            raise ValueError("one offset per stream plus the total")
+        sym = np.zeros((n, self.M), np.int32)
+        outs, c = self._alloc(n)
+        rc = _load().oracle_run_bits(ctypes.byref(self._m), _ptr(psi), bits.ctypes.data, offsets.ctypes.data,
+                                     sym.ctypes.data, ctypes.byref(c))
+        if rc != 0:
+            raise RuntimeError("oracle_run_bits failed")
+        return self._shape(outs), sym.reshape(self.B, self.H, self.W, self.M)
+
     def eval(self, y_hat, psi, lats=None):
         """Teacher-forced parameters from a given reconstruction, at the listed
         flat latent indices (all latents when None).  Returns flat arrays
@@ -191,3 +227,53 @@ class Model:
             raise RuntimeError("oracle_eval failed")
         outs.pop("y_hat")
         return outs
+
+
+def rans_tables(table):
+    """Frequency tables of a scale table: (n [L], base [L+1], cum [base[L]])
+    as built by the oracle's coder."""
+    table = _f32(table)
+    L = len(table)
+    n = np.zeros(L, np.int32)
+    base = np.zeros(L + 1, np.int64)
+    total = _load().oracle_rans_tables(table.ctypes.data, L, n.ctypes.data, base.ctypes.data, None, 0)
+    if total < 0:
+        raise RuntimeError("oracle_rans_tables failed")
+    cum = np.zeros(total, np.uint32)
+    _load().oracle_rans_tables(table.ctypes.data, L, None, None, cum.ctypes.data, total)
+    return n, base, cum
+
+
+def rans_encode(sym, idx, table):
+    """rANS streams of symbols sym [B][H][W][M] at scale indices idx (same
+    shape): one stream per (image, grid row, channel).  Returns (bits uint32,
+    offsets uint32 [B*H*M + 1])."""
+    sym = np.ascontiguousarray(sym, dtype=np.int32)
+    idx = np.ascontiguousarray(idx, dtype=np.int32)
+    table = _f32(table)
+    B, H, W, M = sym.shape
+    offsets = np.zeros(B * H * M + 1, np.uint32)
+    lib = _load()
+    total = lib.oracle_rans_encode(sym.ctypes.data, idx.ctypes.data, B, H, W, M, table.ctypes.data, len(table),
+                                   None, 0, offsets.ctypes.data)
+    if total < 0:
+        raise RuntimeError("oracle_rans_encode failed")
+    bits = np.zeros(max(int(total), 1), np.uint32)
+    if lib.oracle_rans_encode(sym.ctypes.data, idx.ctypes.data, B, H, W, M, table.ctypes.data, len(table),
+                              bits.ctypes.data, len(bits), offsets.ctypes.data) != total:
+        raise RuntimeError("oracle_rans_encode failed")
+    return bits[:total], offsets
+
+
+def rans_decode(bits, offsets, idx, table):
+    """Symbols of rANS streams given the scale indices idx [B][H][W][M]."""
+    idx = np.ascontiguousarray(idx, dtype=np.int32)
+    bits = np.ascontiguousarray(bits, dtype=np.uint32)
+    offsets = np.ascontiguousarray(offsets, dtype=np.uint32)
+    table = _f32(table)
+    B, H, W, M = idx.shape
+    sym = np.zeros(idx.shape, np.int32)
+    if _load().oracle_rans_decode(bits.ctypes.data, offsets.ctypes.data, idx.ctypes.data, B, H, W, M,
+                                  table.ctypes.data, len(table), sym.ctypes.data) != 0:
+        raise RuntimeError("oracle_rans_decode failed")
+    return sym

@@ -58,6 +58,8 @@
 #include <stdlib.h>
 #include <string.h>
 
+#include "wf_rans.h"
+
 typedef struct {
     int32_t H, W, M, B, K;      /* rows, cols, channels, images, mixture comps */
     int32_t d1, d2;             /* hidden widths of the parameter network     */
@@ -353,6 +355,54 @@ int oracle_run(const oracle_model *m, const float *psi, int32_t *sym,
         }
     }
     free(scratch); free(mu); free(sigma); free(weight); free(cmean); free(index);
+    return rc;
+}
+
+/*
+ * Decode with the symbols taken from rANS streams (wf_rans.c): in raster
+ * order, each latent's parameters give its scale indices, and with them the
+ * next symbol of the stream of its (image, grid row, channel) is decoded
+ * before y_hat = s + mean is written.  K = 1 only.  sym_out receives the
+ * decoded symbols.  Returns 0, or -1 on a bad argument or a malformed stream.
+ */
+int oracle_run_bits(const oracle_model *m, const float *psi, const uint32_t *bits,
+                    const uint32_t *offsets, int32_t *sym_out, const oracle_out *out)
+{
+    if (!m || !psi || !bits || !offsets || !sym_out || !out || !out->y_hat) return -1;
+    if (m->K != 1) return -1;
+    const size_t M = m->M;
+    const size_t total = (size_t)m->B * m->H * m->W;
+    const size_t nstreams = (size_t)m->B * m->H * M;
+    rans_tables t;
+    if (rans_tables_build(m->table, m->L, &t)) return -1;
+    float *scratch = malloc(scratch_floats(m) * sizeof(float));
+    float *mu = malloc(M * sizeof(float));
+    float *sigma = malloc(M * sizeof(float));
+    float *weight = malloc(M * sizeof(float));
+    float *cmean = malloc(M * sizeof(float));
+    int32_t *index = malloc(M * sizeof(int32_t));
+    rans_dec *dec = malloc(nstreams * sizeof(rans_dec));
+    int rc = 0;
+    if (!scratch || !mu || !sigma || !weight || !cmean || !index || !dec) rc = -1;
+    for (size_t k = 0; k < nstreams && !rc; ++k)
+        if (rans_dec_init(&dec[k], bits + offsets[k], (int64_t)offsets[k + 1] - offsets[k])) rc = -1;
+    if (!rc) memset(out->y_hat, 0, total * M * sizeof(float));
+    for (size_t lat = 0; lat < total && !rc; ++lat) {
+        int b = (int)(lat / ((size_t)m->H * m->W));
+        int i = (int)((lat / m->W) % m->H);
+        int j = (int)(lat % m->W);
+        latent_params(m, out->y_hat, psi, b, i, j, mu, sigma, index, weight, cmean, scratch);
+        store_params(m, out, lat, mu, sigma, index, weight, cmean);
+        for (size_t c = 0; c < M; ++c) {
+            rans_dec *d = &dec[((size_t)b * m->H + i) * M + c];
+            int32_t s;
+            if (rans_dec_symbol(d, &t, index[c], &s)) { rc = -1; break; }
+            sym_out[lat * M + c] = s;
+            out->y_hat[lat * M + c] = (float)s + mu[c];
+        }
+    }
+    free(scratch); free(mu); free(sigma); free(weight); free(cmean); free(index); free(dec);
+    rans_tables_free(&t);
     return rc;
 }
 
