@@ -299,6 +299,8 @@ def main():
                     help="context approximation: decode N wavefronts per step (1: exact decode)")
     ap.add_argument("--cpu-rows", type=int, default=16, help="grid rows of the CPU-oracle sample (0: skip)")
     ap.add_argument("--no-encode", action="store_true")
+    ap.add_argument("--no-entropy", action="store_true",
+                    help="skip the decode from rANS streams (measured by default when the plan allows it)")
     ap.add_argument("--summarize-traffic", nargs=4, metavar=("FETCH_DIR", "WRITE_DIR", "CAL_FETCH_DIR", "CAL_WRITE_DIR"),
                     help="write the traffic summary of this workload/precision/driver from rocprofv3 outputs")
     ap.add_argument("--cal-bytes", type=float, default=float(1 << 30))
@@ -383,6 +385,34 @@ def main():
     node_us, bar_us = plan.measure_floor()
     plan.close()
 
+    # the decode that reads every symbol from its rANS stream inside the step loop
+    rec_ec = None
+    if not args.no_entropy and cfg["K"] == 1 and args.group <= 1 and args.driver in ("stream", "graph"):
+        pe = wf.Plan(w, table, cfg["H"], cfg["W"], cfg["B"], cfg["K"], mask=mask_of(cfg), precision=args.precision,
+                     driver=args.driver, entropy_coder="rans")
+        u = inputs.make_noise(cfg["B"], cfg["H"], cfg["W"], cfg["M"])
+        y_d = (torch.from_numpy(sym.astype(np.float32) + u).cuda() + out["mean"]).contiguous()
+        bits = torch.zeros((2 + 4 * cfg["W"]) * cfg["B"] * cfg["H"] * cfg["M"], dtype=torch.int32, device="cuda")
+        _, sym_e, offs = pe.encode_bits(psi_d, y_d, bits, stream=stream)
+        pe.sync(stream)
+        n_words = int(offs[-1].item())
+        out_b = pe.alloc_out()
+        sym_b = torch.empty_like(sym_d)
+
+        def dec_bits():
+            pe.decode_bits(psi_d, bits, offs, out=out_b, sym_out=sym_b, n_words=n_words, stream=stream)
+
+        dec_bits()
+        pe.sync(stream)
+        bwall, bper = timed_calls(dec_bits, args.steps, stream, torch)
+        pe.sync(stream)
+        pe.close()
+        rec_ec = {"ms_per_image": bwall * 1e3 / args.steps / cfg["B"], "launch_ms_events": float(np.mean(bper)),
+                  "stream_words": n_words, "bits_per_symbol": 32.0 * n_words / sym.size,
+                  "symbols_match": bool(torch.equal(sym_b, sym_d)) and bool(torch.equal(sym_e, sym_d)),
+                  "streams": "one per (image, grid row, channel); 64-bit rANS state, 32-bit words, 2^-16 Gaussian tables"}
+        del bits
+
     lat = cfg["B"] * cfg["H"] * cfg["W"]
     ms = wall * 1e3 / args.steps
     value = lat / (ms * 1e-3)
@@ -432,6 +462,7 @@ def main():
         "latents_per_s": value,
         "ms_per_image": ms / cfg["B"],
         "encode": rec_enc,
+        "entropy_decode": rec_ec,
     }
     if args.cpu_rows > 0:
         rec["cpu_baseline"] = cpu_baseline(args.workload, args.cpu_rows, args.mask)

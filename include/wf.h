@@ -41,8 +41,17 @@ typedef enum {
     WF_E_UNSUPPORTED = -2,  /* valid but not supported by this build           */
     WF_E_HIP = -3,          /* a HIP runtime call failed                       */
     WF_E_NOMEM = -4,        /* device or host allocation failed                */
-    WF_E_TIMEOUT = -5       /* a device-side wait exceeded its spin budget     */
+    WF_E_TIMEOUT = -5,      /* a device-side wait exceeded its spin budget     */
+    WF_E_STREAM = -6,       /* a malformed rANS stream (decode from streams)   */
+    WF_E_CAPACITY = -7      /* encoded streams larger than the caller's buffer */
 } wf_status;
+
+/* Entropy coder of the symbols (wf_desc.entropy_coder). */
+typedef enum {
+    WF_EC_NONE = 0,         /* symbols are passed as int32 arrays                      */
+    WF_EC_RANS = 1          /* also wf_encode_bits / wf_decode_bits: rANS streams, K = 1,
+                               stream or graph driver, exact decode (group <= 1)         */
+} wf_entropy_coder;
 
 /* Causal masks (Def. 1: a (2R+1)x(2R+1) kernel keeps the R rows above within
  * horizontal offset R, and the R latents to the left; least shear R + 1). */
@@ -117,6 +126,7 @@ typedef struct {
                                when none is decoded).  N > 1 needs the stream or graph
                                driver (WF_E_UNSUPPORTED otherwise).                      */
     int32_t param_order;    /* wf_param_order: block order of the rows of w3 and b3        */
+    int32_t entropy_coder;  /* wf_entropy_coder                                             */
 } wf_desc;
 
 /*
@@ -192,6 +202,56 @@ int wf_encode(wf_plan_t plan, const float *psi, const float *y, int32_t *sym_out
               const wf_out *out, hipStream_t stream);
 
 /*
+ * Entropy coding with rANS (plans built with entropy_coder = WF_EC_RANS).
+ * The entropy model is the discretised Gaussian of the symbol's scale level
+ * (Sec. II-A; the paper pairs the wavefront decode with rANS, Sec. III-C).
+ * Per level l, with T_l the level's table value: support n_l =
+ * max(1, ceil(6 T_l)), symbols -n_l..n_l and an escape for |s| > n_l whose
+ * excess follows in 15-bit chunks; frequencies in units of 2^-16,
+ * f = 1 + floor(p (2^16 - 2 n_l - 2)) for the Gaussian mass p of
+ * [s - 1/2, s + 1/2], the remainder added to s = 0.  Coder: 64-bit state in
+ * [2^31, 2^63), 32-bit words.
+ * Streams: one per (image b, grid row i, channel c), index k = (b*H + i)*M + c,
+ * holding the row's symbols in column order (one per wavefront step); stream
+ * k occupies words [offsets[k], offsets[k+1]) of `bits`: the final state
+ * (high, low word) and then the renormalisation words in decoding order.
+ *
+ * wf_ec_tables (host only): the frequency tables of a scale table:
+ * n[L], base[L+1] (first cumulative entry of each level), and, when cum is
+ * non-NULL, the cumulative frequencies (base[L] entries, 2 n_l + 3 per level,
+ * from 0 to 2^16).  Errors: WF_E_INVALID (NULL table, L outside [2, 256],
+ * cum_cap < base[L]); WF_E_UNSUPPORTED when a level needs n_l > 16383.
+ */
+int wf_ec_tables(const float *scale_table, int32_t L, int32_t *n, int64_t *base,
+                 uint32_t *cum, int64_t cum_cap);
+
+/*
+ * Encode (as wf_encode) and code the symbols into rANS streams.
+ *   bits     DEVICE uint32, bits_capacity words
+ *   offsets  DEVICE uint32 [B*H*M + 1]; offsets[B*H*M] = total words
+ * The total is always written; when it exceeds bits_capacity nothing is
+ * written to bits and the next wf_plan_sync returns WF_E_CAPACITY.
+ * Asynchronous on `stream`.
+ */
+int wf_encode_bits(wf_plan_t plan, const float *psi, const float *y, int32_t *sym_out,
+                   const wf_out *out, uint32_t *bits, int64_t bits_capacity,
+                   uint32_t *offsets, hipStream_t stream);
+
+/*
+ * Decode with every symbol read from its rANS stream inside the step loop:
+ * at the step of latent (b,i,j) the symbol of each channel c is decoded from
+ * stream (b*H + i)*M + c at the latent's scale level, then
+ * y_hat = symbol + mean.  sym_out [B][H][W][M] (DEVICE int32) receives the
+ * decoded symbols.  `bits` (DEVICE, n_words words) and `offsets` (DEVICE
+ * [B*H*M + 1]) are as written by wf_encode_bits.  Reads never go past a
+ * stream's end or n_words; a malformed stream makes the next wf_plan_sync
+ * return WF_E_STREAM (the outputs are then unspecified).  Asynchronous.
+ */
+int wf_decode_bits(wf_plan_t plan, const float *psi, const uint32_t *bits, int64_t n_words,
+                   const uint32_t *offsets, int32_t *sym_out, const wf_out *out,
+                   hipStream_t stream);
+
+/*
  * Measurement hook of the persistent and dataflow drivers (WF_E_UNSUPPORTED
  * for the others).  With `stamps` non-NULL (DEVICE int64 array of `capacity`
  * entries) every later call records the device wall clock (100 MHz ticks):
@@ -224,8 +284,9 @@ int wf_measure_floor(wf_plan_t plan, float *node_us, float *barrier_us);
 
 /*
  * Wait for `stream` and report a device-side error recorded by the plan's
- * kernels (WF_E_TIMEOUT when a bounded device-wide wait gave up).  Clears the
- * recorded error.
+ * kernels (WF_E_TIMEOUT when a bounded device-wide wait gave up, WF_E_STREAM
+ * for a malformed rANS stream, WF_E_CAPACITY when encoded streams did not
+ * fit).  Clears the recorded error.
  */
 int wf_plan_sync(wf_plan_t plan, hipStream_t stream);
 

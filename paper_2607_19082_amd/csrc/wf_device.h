@@ -323,7 +323,7 @@ __host__ __device__ __forceinline__ int phase_cols(const StepArgs& a, int ph) {
     switch (ph) {
         case PH_A: return a.Np1 / kTile / P::kC;
         case PH_B: return a.Np2 / kTile / P::kC;
-        default: return 2 * a.M / kTile;   // PH_C: value group x channel tile
+        default: return (a.ec ? 1 : 2) * a.M / kTile;   // PH_C: value group x channel tile (ec: channel tile)
     }
 }
 template <class P>
@@ -958,6 +958,146 @@ __device__ __forceinline__ void l3_job(const StepArgs& a, const StepRows& s, int
 }
 
 // ---------------------------------------------------------------------------
+// Entropy decoding inside the wavefront loop (rANS; K = 1).  Each symbol is
+// coded with the discretised Gaussian of its scale level, one stream per
+// (image, grid row, channel) holding the row's symbols in column order, so a
+// step decodes at most one symbol of every stream.  Decoder state: x in
+// [2^31, 2^63); pos, end: the stream's next word and its end (the init kernel
+// clamps both to the caller's buffer).  A read past the end records a stream
+// error and reads zero.
+__device__ __forceinline__ void ec_renorm(const CallPtrs* cp, uint64_t& x, uint32_t& pos, uint32_t end,
+                                          uint32_t& wnext, bool& bad) {
+    if (x < (1ull << 31)) {
+        bad |= pos >= end;
+        x = (x << 32) | wnext;
+        pos += pos < end ? 1u : 0u;
+        wnext = pos < end ? cp->bits[pos] : 0u;   // (only an escape needs it this step)
+    }
+}
+// Decode the next symbol at scale level lvl; wnext = bits[pos] (prefetched).
+__device__ __forceinline__ int32_t ec_decode(const CallPtrs* cp, int lvl, uint64_t& x, uint32_t& pos, uint32_t end,
+                                             uint32_t wnext, bool& bad) {
+    const int n = cp->ec_n[lvl];
+    const uint32_t* cum = cp->ec_cum + cp->ec_base[lvl];
+    const uint32_t slot = (uint32_t)x & ((1u << kEcPrecBits) - 1u);
+    int u = cp->ec_lut[(size_t)lvl * kEcLut + (slot >> kEcLutShift)];
+    uint32_t c0 = cum[u], c1 = cum[u + 1];
+    // at most 15 symbols start inside a bucket after its first
+    for (int g = 0; g < (1 << kEcLutShift) && c1 <= slot; ++g) {
+        ++u;
+        c0 = c1;
+        c1 = cum[u + 1];
+    }
+    x = (uint64_t)(c1 - c0) * (x >> kEcPrecBits) + slot - c0;
+    ec_renorm(cp, x, pos, end, wnext, bad);
+    if (u <= 2 * n) return u - n;
+    // escape: the excess in 15-bit chunks, low first, each a uniform 16-bit value
+    uint64_t e = 0;
+    for (int q = 0; q < 5; ++q) {
+        const uint32_t ch = (uint32_t)x & 0xffffu;
+        x >>= kEcPrecBits;
+        ec_renorm(cp, x, pos, end, wnext, bad);
+        e |= (uint64_t)(ch & 0x7fffu) << (15 * q);
+        if (!(ch & 0x8000u)) {
+            const int64_t mag = (int64_t)(e >> 1) + n + 1;
+            return (int32_t)((e & 1u) ? -mag : mag);
+        }
+    }
+    bad = true;
+    return 0;
+}
+
+// Phase C with entropy decoding: job column cg computes the mean and the
+// scale tile of channel tile cg together, so that the symbol's scale level,
+// the symbol (from its stream) and y_hat = s + mean come out of one job.
+template <class P, bool COH>
+__device__ __forceinline__ void l3_ec_tile(const StepArgs& a, const StepRows& s, Job jb, f4 (*red)[64],
+                                           const float* tab) {
+    using A = typename P::A;
+    using Bw = typename P::B;
+    constexpr int KBW = P::kL3Kbw1 / 2;
+    const int M = a.M, G = M / kTile, cg = jb.ct, rt = jb.rt;
+    const int wave = wave_id(), lane = threadIdx.x & 63, kq = lane >> 4;
+    const CallPtrs* cp = a.cp;
+    const int c = cg * kTile + (lane & 15);
+    const int ro = wave < 4 ? rt * kTile + kq * 4 + wave : s.nrows;   // epilogue row of this wave
+    const Row v = step_row(a, s, ro);
+    // the lane's stream: state and next word first, off the critical path
+    const size_t k = ((size_t)v.b * a.H + v.i) * M + c;
+    uint64_t x = 0;
+    uint32_t pos = 0, end = 0, wnext = 0;
+    if (v.valid) {
+        x = cp->ec_x[k];
+        pos = cp->ec_pos[k];
+        end = cp->ec_end[k];
+        wnext = pos < end ? cp->bits[pos] : 0u;
+    }
+    const float bias0 = a.b3[c], bias1 = a.b3[M + c];
+
+    const int nkb = a.Np2 / P::kK;
+    const int per = (nkb + kWaves - 1) / kWaves;
+    const int kb0 = min(nkb, wave * per), kb1 = min(nkb, kb0 + per);
+    const int r = rt * kTile + (lane & 15);
+    const bool valid = r < s.nrows;
+    const Bw* __restrict__ w0 = static_cast<const Bw*>(a.wp3) + (size_t)cg * nkb * 64 + lane;
+    const Bw* __restrict__ w1 = static_cast<const Bw*>(a.wp3) + (size_t)(G + cg) * nkb * 64 + lane;
+    const void* h2 = h2_of(a, s);
+    f4 acc0 = zero4(), acc1 = zero4();
+    for (int kc = kb0; kc < kb1; kc += KBW) {
+        A av[KBW];
+        Bw b0[KBW], b1[KBW];
+#pragma unroll
+        for (int u = 0; u < KBW; ++u) {
+            const int kk = min(kc + u, kb1 - 1);
+            av[u] = ld_tile<P, COH>(h2, rt, a.Np2, kk, valid);
+            b0[u] = w0[(size_t)kk * 64];
+            b1[u] = w1[(size_t)kk * 64];
+        }
+#pragma unroll
+        for (int u = 0; u < KBW; ++u)
+            if (kc + u < kb1) {
+                acc0 = P::mma(av[u], b0[u], acc0);
+                acc1 = P::mma(av[u], b1[u], acc1);
+            }
+    }
+    red[wave * 2][lane] = acc0;
+    red[wave * 2 + 1][lane] = acc1;
+    __syncthreads();
+    float mu = bias0, sr = bias1;
+    if (wave < 4) {
+#pragma unroll
+        for (int w2 = 0; w2 < kWaves; ++w2) {
+            mu += red[w2 * 2][lane][wave];
+            sr += red[w2 * 2 + 1][lane][wave];
+        }
+    }
+    __syncthreads();
+    if (!v.valid) return;
+
+    const size_t oq = v.lat * M + c;
+    const float sg = sr > tab[0] ? sr : tab[0];
+    const int lvl = scale_index(tab, a.L, sg);
+    cp->scale[oq] = sg;
+    cp->idx[oq] = lvl;
+    bool bad = false;
+    const int32_t sv = ec_decode(cp, lvl, x, pos, end, wnext, bad);
+    cp->ec_x[k] = x;
+    cp->ec_pos[k] = pos;
+    if (bad) __hip_atomic_store(cp->err, kErrStream, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    cp->sym_out[oq] = sv;
+    cp->mean[oq] = mu;
+    const float yv = (float)sv + mu;
+    st1<COH>(cp->y_hat, oq, yv);
+    if constexpr (P::kBf16) st_pair_row<COH>(a.ybf, v.lat * 2 * M, c, yv);
+}
+template <class P, bool COH>
+__device__ __forceinline__ void l3_ec_job(const StepArgs& a, const StepRows& s, int b, f4 (*red)[64],
+                                          const float* tab) {
+    const Job jb = xcd_job(b, a.M / kTile, ntiles(s.nrows));
+    if (jb.valid) l3_ec_tile<P, COH>(a, s, jb, red, tab);
+}
+
+// ---------------------------------------------------------------------------
 // Context approximation (Sec. III-D): a step is a group of N wavefronts.  A
 // tap of the latent's own group is not decoded yet and is replaced, channel by
 // channel, by the mean of the latent's decoded in-image taps (zero when none
@@ -1129,6 +1269,12 @@ __device__ __forceinline__ void phase_job(int ph, const StepArgs& a, const StepR
         const Job jb = xcd_job(b, a.Np1 / kTile / P::kC, ntiles(s.nrows));
         if (jb.valid) l1_group_tile<P, COH>(a, s, jb, red);
         return;
+    }
+    if constexpr (KC == 1) {
+        if (ph == PH_C && a.ec) {
+            l3_ec_job<P, COH>(a, s, b, red, sm.tab);
+            return;
+        }
     }
     if constexpr (P::kBf16) {
         if (ph == PH_A) l1_fold_bf16_job<COH>(a, s, b, red);

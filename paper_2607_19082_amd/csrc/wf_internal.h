@@ -14,6 +14,15 @@ namespace wf {
 constexpr int kMaxTaps = 24;         // the 7x7 causal mask
 constexpr int kTaps5x5 = 12;         // the 5x5 causal mask
 constexpr int kMaxRadius = 3;
+// rANS (entropy coding of the symbols): probabilities in units of 2^-16, a
+// 64-bit state in [2^31, 2^63) renormalised by 32-bit words, and per level a
+// table of the symbol at the start of each 16-slot bucket.
+constexpr int kEcPrecBits = 16;
+constexpr int kEcLutShift = 4;
+constexpr int kEcLut = 1 << (kEcPrecBits - kEcLutShift);
+constexpr int kEcMaxSupport = 16383;   // support half-width bound (symbol indices fit 16 bits)
+// device error word values
+constexpr int kErrTimeout = 1, kErrStream = 2, kErrCapacity = 3;
 constexpr int kMaxNew = 2;           // taps written by the immediately preceding step
 constexpr int kTile = 16;            // MFMA tile edge (rows and columns)
 constexpr int kJobWaves = 4;         // waves of one job's workgroup
@@ -70,10 +79,20 @@ struct CallPtrs {
     const float* psi;       // [B][H][W][2M]
     const int32_t* sym;     // decode input
     const float* y;         // encode input
-    int32_t* sym_out;       // encode output
+    int32_t* sym_out;       // encode output; decode from streams: the decoded symbols
     float *y_hat, *mean, *scale, *weight, *cmean;
     int32_t* idx;
     int encode;
+    // Decode from rANS streams (StepArgs::ec): the caller's words, the plan's
+    // per-stream decoder state and tables, and the device error word.
+    const uint32_t* bits;
+    uint64_t* ec_x;         // [B*H*M] decoder states
+    uint32_t *ec_pos, *ec_end;   // [B*H*M] next word, one past the stream's last
+    const int32_t* ec_n;    // [L] support half-width per level
+    const int32_t* ec_base; // [L] first cumulative entry per level
+    const uint32_t* ec_cum; // cumulative frequencies
+    const uint16_t* ec_lut; // [L][kEcLut] symbol at the start of each slot bucket
+    int* err;
 };
 
 // Plan constants passed by value to every step kernel.
@@ -116,6 +135,7 @@ struct StepArgs {
     // mask order: row_w taps in each of rows -R..-1 from dx = -R, then the R
     // taps (0,-R)..(0,-1)) with same-group taps filled, in gparts k-parts.
     int group, row_w, gparts;
+    int ec;                 // 1: phase C decodes each symbol from its rANS stream (K = 1)
     const int* rowlat;      // nullptr: rows of wavefront t by grid row
     const void* wp_all;     // packed Wc over all taps, channel-chunk-major k   [2M/16][(n_old+2)*M/kb]
     const void* wp_hoist;   // packed W1[:, :2M]                           [Np1/16][2M/kb]
@@ -174,12 +194,27 @@ struct Plan {
     hipStream_t cap_stream = nullptr;
     hipGraph_t graph = nullptr;
     hipGraphExec_t graph_exec = nullptr;
+    // entropy coding (rANS): tables, decoder states, encoder scratch and, for
+    // the graph driver, the graph of the decode from streams
+    int ec = 0;
+    int32_t *ec_n = nullptr, *ec_base = nullptr;
+    uint32_t* ec_cum = nullptr;
+    uint16_t* ec_lut = nullptr;
+    uint64_t* ec_x = nullptr;
+    uint32_t *ec_pos = nullptr, *ec_end = nullptr, *ec_len = nullptr, *ec_words = nullptr;
+    hipGraph_t graph_ec = nullptr;
+    hipGraphExec_t graph_exec_ec = nullptr;
 };
 
 // Enqueue the kernels of one call after its pointers were published to
 // p.d_call (used directly by the stream driver and captured by the graph
 // driver).
-int enqueue_steps(Plan& p, hipStream_t stream);
+int enqueue_steps(Plan& p, hipStream_t stream, bool ec = false);
+// entropy coding (wf_ec.hip)
+int build_ec(Plan* p, const float* scale_table, int L);
+int enqueue_ec_init(Plan& p, const uint32_t* bits, int64_t n_words, const uint32_t* offsets, hipStream_t stream);
+int enqueue_ec_encode(Plan& p, const int32_t* sym, const int32_t* idx, uint32_t* bits, int64_t cap,
+                      uint32_t* offsets, hipStream_t stream);
 // Publish the call's pointers to p.d_call on `stream`.
 int enqueue_set_call(Plan& p, const CallPtrs& c, hipStream_t stream);
 // The pre-loop product of the hyperprior half of layer 1.

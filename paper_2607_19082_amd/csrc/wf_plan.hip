@@ -104,6 +104,14 @@ static int check_desc(const wf_desc* d) {
     if (d->group < 0) return fail(WF_E_INVALID, "group must be >= 0");
     if (d->param_order != WF_ORDER_NATIVE && d->param_order != WF_ORDER_SCALES_FIRST)
         return fail(WF_E_INVALID, "unknown param_order");
+    if (d->entropy_coder != WF_EC_NONE && d->entropy_coder != WF_EC_RANS)
+        return fail(WF_E_INVALID, "unknown entropy_coder");
+    if (d->entropy_coder == WF_EC_RANS) {
+        if (d->K != 1) return fail(WF_E_UNSUPPORTED, "entropy coding needs K = 1 (the Gaussian model)");
+        if (d->group > 1) return fail(WF_E_UNSUPPORTED, "entropy coding needs the exact decode (group <= 1)");
+        if (d->driver != WF_DRIVER_STREAM && d->driver != WF_DRIVER_GRAPH)
+            return fail(WF_E_UNSUPPORTED, "entropy coding needs the stream or graph driver");
+    }
     if (d->group > 1 && d->driver != WF_DRIVER_STREAM && d->driver != WF_DRIVER_GRAPH)
         return fail(WF_E_UNSUPPORTED, "context approximation (group > 1) needs the stream or graph driver");
     if (d->M % kTile != 0) return fail(WF_E_UNSUPPORTED, "M must be a multiple of 16");
@@ -196,6 +204,8 @@ static void free_plan(Plan* p) {
     if (!p) return;
     if (p->graph_exec) (void)hipGraphExecDestroy(p->graph_exec);
     if (p->graph) (void)hipGraphDestroy(p->graph);
+    if (p->graph_exec_ec) (void)hipGraphExecDestroy(p->graph_exec_ec);
+    if (p->graph_ec) (void)hipGraphDestroy(p->graph_ec);
     if (p->cap_stream) (void)hipStreamDestroy(p->cap_stream);
     for (void* q : p->owned)
         if (q) (void)hipFree(q);
@@ -477,6 +487,7 @@ static int build_plan(const wf_desc* d, Plan* p) {
         p->df.ncrit = p->grid >= 2 * kXcds ? p->grid / 2 / kXcds * kXcds : p->grid;
         if (p->df.ncrit == p->grid) return fail(WF_E_UNSUPPORTED, "dataflow driver needs at least 16 workgroups");
     }
+    if (d->entropy_coder == WF_EC_RANS && (rc = build_ec(p, d->scale_table, d->L)) != WF_OK) return rc;
     WF_HIP(hipDeviceSynchronize());
 
     if (p->driver == WF_DRIVER_GRAPH) {
@@ -494,6 +505,20 @@ static int build_plan(const wf_desc* d, Plan* p) {
         if (e != hipSuccess) return fail(WF_E_HIP, std::string("graph capture: ") + hipGetErrorString(e));
         p->graph = g;
         WF_HIP(hipGraphInstantiate(&p->graph_exec, p->graph, nullptr, nullptr, 0));
+        if (p->ec) {
+            // the decode from streams: the same steps with the entropy-decoding phase C
+            WF_HIP(hipStreamBeginCapture(p->cap_stream, hipStreamCaptureModeThreadLocal));
+            erc = enqueue_steps(*p, p->cap_stream, true);
+            g = nullptr;
+            e = hipStreamEndCapture(p->cap_stream, &g);
+            if (erc != WF_OK) {
+                if (g) (void)hipGraphDestroy(g);
+                return erc;
+            }
+            if (e != hipSuccess) return fail(WF_E_HIP, std::string("graph capture: ") + hipGetErrorString(e));
+            p->graph_ec = g;
+            WF_HIP(hipGraphInstantiate(&p->graph_exec_ec, p->graph_ec, nullptr, nullptr, 0));
+        }
     }
     return WF_OK;
 }
@@ -560,13 +585,14 @@ static int check_out(const Plan* p, const wf_out* out) {
     return WF_OK;
 }
 
-static int run_call(Plan* p, const CallPtrs& c, hipStream_t stream) {
+static int run_call(Plan* p, const CallPtrs& c, hipStream_t stream, bool ec = false) {
     int rc = enqueue_set_call(*p, c, stream);
     if (rc != WF_OK) return rc;
     if (p->driver == WF_DRIVER_GRAPH) {
-        WF_HIP(hipGraphLaunch(p->graph_exec, stream));
+        WF_HIP(hipGraphLaunch(ec ? p->graph_exec_ec : p->graph_exec, stream));
         return WF_OK;
     }
+    if (ec) return enqueue_steps(*p, stream, true);
     if (p->driver == WF_DRIVER_PERSISTENT) return enqueue_persistent(*p, stream);
     if (p->driver == WF_DRIVER_DATAFLOW) return enqueue_dataflow(*p, stream);
     return enqueue_steps(*p, stream);
@@ -579,6 +605,14 @@ static CallPtrs call_ptrs(const float* psi, const int32_t* sym, const float* y, 
     c.y_hat = out->y_hat; c.mean = out->mean; c.scale = out->scale; c.idx = out->idx;
     c.weight = out->weight; c.cmean = out->comp_mean;
     return c;
+}
+
+// the plan's entropy-decoding state in a call's pointers
+static void ec_ptrs(const Plan* p, CallPtrs& c, const uint32_t* bits) {
+    c.bits = bits;
+    c.ec_x = p->ec_x; c.ec_pos = p->ec_pos; c.ec_end = p->ec_end;
+    c.ec_n = p->ec_n; c.ec_base = p->ec_base; c.ec_cum = p->ec_cum; c.ec_lut = p->ec_lut;
+    c.err = p->d_err;
 }
 
 int wf_decode(wf_plan_t plan, const float* psi, const int32_t* sym, const wf_out* out,
@@ -597,6 +631,34 @@ int wf_encode(wf_plan_t plan, const float* psi, const float* y, int32_t* sym_out
     int rc = check_out(p, out);
     if (rc != WF_OK) return rc;
     return run_call(p, call_ptrs(psi, nullptr, y, sym_out, out), stream);
+}
+
+int wf_encode_bits(wf_plan_t plan, const float* psi, const float* y, int32_t* sym_out, const wf_out* out,
+                   uint32_t* bits, int64_t bits_capacity, uint32_t* offsets, hipStream_t stream) {
+    if (!plan || !psi || !y || !sym_out || !bits || !offsets)
+        return fail(WF_E_INVALID, "plan, psi, y, sym_out, bits or offsets is NULL");
+    Plan* p = reinterpret_cast<Plan*>(plan);
+    if (!p->ec) return fail(WF_E_UNSUPPORTED, "the plan was built without entropy coding");
+    if (bits_capacity < 0) return fail(WF_E_INVALID, "negative capacity");
+    int rc = check_out(p, out);
+    if (rc != WF_OK) return rc;
+    if ((rc = run_call(p, call_ptrs(psi, nullptr, y, sym_out, out), stream)) != WF_OK) return rc;
+    return enqueue_ec_encode(*p, sym_out, out->idx, bits, bits_capacity, offsets, stream);
+}
+
+int wf_decode_bits(wf_plan_t plan, const float* psi, const uint32_t* bits, int64_t n_words, const uint32_t* offsets,
+                   int32_t* sym_out, const wf_out* out, hipStream_t stream) {
+    if (!plan || !psi || !bits || !offsets || !sym_out)
+        return fail(WF_E_INVALID, "plan, psi, bits, offsets or sym_out is NULL");
+    Plan* p = reinterpret_cast<Plan*>(plan);
+    if (!p->ec) return fail(WF_E_UNSUPPORTED, "the plan was built without entropy coding");
+    if (n_words < 0) return fail(WF_E_INVALID, "negative word count");
+    int rc = check_out(p, out);
+    if (rc != WF_OK) return rc;
+    if ((rc = enqueue_ec_init(*p, bits, n_words, offsets, stream)) != WF_OK) return rc;
+    CallPtrs c = call_ptrs(psi, nullptr, nullptr, sym_out, out);
+    ec_ptrs(p, c, bits);
+    return run_call(p, c, stream, true);
 }
 
 int wf_plan_trace(wf_plan_t plan, int64_t* stamps, int64_t capacity, int64_t* needed, int32_t* grid) {
@@ -633,6 +695,8 @@ int wf_plan_sync(wf_plan_t plan, hipStream_t stream) {
     WF_HIP(hipMemcpy(&err, p->d_err, sizeof(int), hipMemcpyDeviceToHost));
     if (err) {
         WF_HIP(hipMemset(p->d_err, 0, sizeof(int)));
+        if (err == kErrStream) return fail(WF_E_STREAM, "a malformed rANS stream (or a scale level out of range)");
+        if (err == kErrCapacity) return fail(WF_E_CAPACITY, "the encoded streams exceed the bits buffer");
         return fail(WF_E_TIMEOUT, "a device-wide wait exceeded its spin budget");
     }
     return WF_OK;

@@ -94,8 +94,9 @@ static void launch_groups(Plan& p, hipStream_t stream) {
 }
 
 template <class P, int KC>
-static void launch_steps(Plan& p, hipStream_t stream) {
-    const StepArgs& a = p.args;
+static void launch_steps(Plan& p, hipStream_t stream, bool ec) {
+    StepArgs a = p.args;
+    a.ec = ec ? 1 : 0;
     if (p.group > 1) {
         launch_groups<P, KC>(p, stream);
         return;
@@ -119,18 +120,18 @@ static void launch_steps(Plan& p, hipStream_t stream) {
         for (int ph = P::kFirst; ph < kMaxPhases; ++ph) {
             const int n = w.nb[ph] + w.cut[ph + 1] - w.cut[ph];
             hipLaunchKernelGGL((k_phase<P, KC>), dim3(n), dim3(kThreads), 0, stream, ph, s, s1, w.nb[ph],
-                               w.cut[ph], w.nc, p.args);
+                               w.cut[ph], w.nc, a);
         }
     }
 }
 
-int enqueue_steps(Plan& p, hipStream_t stream) {
+int enqueue_steps(Plan& p, hipStream_t stream, bool ec) {
     if (p.precision == WF_BF16) {
-        if (p.K == 1) launch_steps<PBF16, 1>(p, stream);
-        else launch_steps<PBF16, 3>(p, stream);
+        if (p.K == 1) launch_steps<PBF16, 1>(p, stream, ec);
+        else launch_steps<PBF16, 3>(p, stream, ec);
     } else {
-        if (p.K == 1) launch_steps<PF32, 1>(p, stream);
-        else launch_steps<PF32, 3>(p, stream);
+        if (p.K == 1) launch_steps<PF32, 1>(p, stream, ec);
+        else launch_steps<PF32, 3>(p, stream, ec);
     }
     hipError_t err = hipGetLastError();
     if (err != hipSuccess) return fail(WF_E_HIP, std::string("kernel launch: ") + hipGetErrorString(err));

@@ -13,6 +13,8 @@ _PKG = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_PKG, "libwf.so")
 
 WF_OK, WF_E_INVALID, WF_E_UNSUPPORTED, WF_E_HIP, WF_E_NOMEM, WF_E_TIMEOUT = 0, -1, -2, -3, -4, -5
+WF_E_STREAM, WF_E_CAPACITY = -6, -7
+ENTROPY_CODER = {None: 0, "none": 0, "rans": 1}
 MASK = {"full": 0, "relaxed": 1, "3x3": 2, "7x7": 3}
 PARAM_ORDER = {"native": 0, "scales_first": 1}
 KERNEL = {"full": 5, "relaxed": 5, "3x3": 3, "7x7": 7}   # ctx_w's spatial size per mask
@@ -20,8 +22,8 @@ PRECISION = {"fp32": 0, "bf16": 1}
 DRIVER = {"stream": 0, "graph": 1, "persistent": 2, "dataflow": 3}
 
 EXPORTS = ["wf_schedule", "wf_validate", "wf_plan", "wf_plan_schedule", "wf_decode",
-           "wf_encode", "wf_plan_trace", "wf_measure_floor", "wf_plan_sync", "wf_plan_destroy",
-           "wf_last_error"]
+           "wf_encode", "wf_ec_tables", "wf_encode_bits", "wf_decode_bits", "wf_plan_trace",
+           "wf_measure_floor", "wf_plan_sync", "wf_plan_destroy", "wf_last_error"]
 
 
 class WfError(RuntimeError):
@@ -43,6 +45,7 @@ class Desc(ctypes.Structure):
         ("w3", ctypes.c_void_p), ("b3", ctypes.c_void_p),
         ("scale_table", ctypes.c_void_p), ("L", ctypes.c_int32),
         ("group", ctypes.c_int32), ("param_order", ctypes.c_int32),
+        ("entropy_coder", ctypes.c_int32),
     ]
 
 
@@ -70,6 +73,9 @@ def lib():
         L.wf_plan_schedule.argtypes = [P, P, P]
         L.wf_decode.argtypes = [P, P, P, ctypes.POINTER(Out), P]
         L.wf_encode.argtypes = [P, P, P, P, ctypes.POINTER(Out), P]
+        L.wf_ec_tables.argtypes = [P, ctypes.c_int32, P, P, P, ctypes.c_int64]
+        L.wf_encode_bits.argtypes = [P, P, P, P, ctypes.POINTER(Out), P, ctypes.c_int64, P, P]
+        L.wf_decode_bits.argtypes = [P, P, P, ctypes.c_int64, P, P, ctypes.POINTER(Out), P]
         L.wf_plan_trace.argtypes = [P, P, ctypes.c_int64, P, P]
         L.wf_measure_floor.argtypes = [P, P, P]
         L.wf_plan_sync.argtypes = [P, P]
@@ -97,7 +103,7 @@ def schedule(H, W, mask="full"):
 
 
 def make_desc(weights, table, H, W, B=1, K=1, mask="full", precision="fp32", driver="stream",
-              slope=0.01, group=1, param_order="native"):
+              slope=0.01, group=1, param_order="native", entropy_coder=None):
     """Build a Desc plus the host arrays it points to (keep both alive)."""
     arrs = {k: np.ascontiguousarray(v, dtype=np.float32) for k, v in weights.items()}
     arrs["table"] = np.ascontiguousarray(table, dtype=np.float32)
@@ -111,7 +117,8 @@ def make_desc(weights, table, H, W, B=1, K=1, mask="full", precision="fp32", dri
              arrs["w1"].ctypes.data, arrs["b1"].ctypes.data,
              arrs["w2"].ctypes.data, arrs["b2"].ctypes.data,
              arrs["w3"].ctypes.data, arrs["b3"].ctypes.data,
-             arrs["table"].ctypes.data, len(arrs["table"]), group, PARAM_ORDER[param_order])
+             arrs["table"].ctypes.data, len(arrs["table"]), group, PARAM_ORDER[param_order],
+             ENTROPY_CODER[entropy_coder])
     return d, arrs
 
 
@@ -131,9 +138,9 @@ class Plan:
     current) torch stream."""
 
     def __init__(self, weights, table, H, W, B=1, K=1, mask="full", precision="fp32",
-                 driver="stream", slope=0.01, group=1, param_order="native"):
+                 driver="stream", slope=0.01, group=1, param_order="native", entropy_coder=None):
         self.desc, self._arrs = make_desc(weights, table, H, W, B, K, mask, precision, driver, slope, group,
-                                          param_order)
+                                          param_order, entropy_coder)
         self.group = group
         self.H, self.W, self.B, self.K = H, W, B, K
         self.M = self.desc.M
@@ -220,6 +227,44 @@ class Plan:
         _check(lib().wf_encode(self._h, p_psi, p_y, p_s, ctypes.byref(o), _stream_handle(stream)))
         return out, sym_out
 
+    def encode_bits(self, psi, y, bits, out=None, sym_out=None, stream=None):
+        """Encode and code the symbols into rANS streams: `bits` is a uint32
+        (int32 view) CUDA tensor of any length; returns (out, sym_out,
+        offsets) with offsets [B*H*M + 1] (int32 view of uint32; the last
+        entry is the total word count, valid after sync)."""
+        import torch
+        B, H, W, M = self.B, self.H, self.W, self.M
+        out = out if out is not None else self.alloc_out()
+        if sym_out is None:
+            sym_out = torch.empty((B, H, W, M), dtype=torch.int32, device=y.device)
+        offsets = torch.empty(B * H * M + 1, dtype=torch.int32, device=y.device)
+        p_psi = self._check_tensor(psi, (B, H, W, 2 * M), torch.float32, "psi")
+        p_y = self._check_tensor(y, (B, H, W, M), torch.float32, "y")
+        p_s = self._check_tensor(sym_out, (B, H, W, M), torch.int32, "sym_out")
+        p_b = self._check_tensor(bits, (bits.numel(),), torch.int32, "bits")
+        p_o = self._check_tensor(offsets, (B * H * M + 1,), torch.int32, "offsets")
+        o = self._out_struct(out)
+        _check(lib().wf_encode_bits(self._h, p_psi, p_y, p_s, ctypes.byref(o), p_b, bits.numel(), p_o,
+                                    _stream_handle(stream)))
+        return out, sym_out, offsets
+
+    def decode_bits(self, psi, bits, offsets, out=None, sym_out=None, n_words=None, stream=None):
+        """Decode with the symbols read from rANS streams (`bits`, `offsets`
+        as written by encode_bits, int32 views).  Returns (out, sym_out)."""
+        import torch
+        B, H, W, M = self.B, self.H, self.W, self.M
+        out = out if out is not None else self.alloc_out()
+        if sym_out is None:
+            sym_out = torch.empty((B, H, W, M), dtype=torch.int32, device=psi.device)
+        p_psi = self._check_tensor(psi, (B, H, W, 2 * M), torch.float32, "psi")
+        p_b = self._check_tensor(bits, (bits.numel(),), torch.int32, "bits")
+        p_o = self._check_tensor(offsets, (B * H * M + 1,), torch.int32, "offsets")
+        p_s = self._check_tensor(sym_out, (B, H, W, M), torch.int32, "sym_out")
+        o = self._out_struct(out)
+        n = bits.numel() if n_words is None else n_words
+        _check(lib().wf_decode_bits(self._h, p_psi, p_b, n, p_o, p_s, ctypes.byref(o), _stream_handle(stream)))
+        return out, sym_out
+
     def trace(self, stamps=None):
         """Record barrier timestamps of later calls into the int64 CUDA tensor
         `stamps` (None: stop).  Returns (entries needed per call, grid)."""
@@ -239,3 +284,16 @@ class Plan:
 
     def sync(self, stream=None):
         _check(lib().wf_plan_sync(self._h, _stream_handle(stream)))
+
+
+def ec_tables(table):
+    """The library's rANS frequency tables of a scale table (host only):
+    (n [L], base [L+1], cum [base[L]] uint32)."""
+    table = np.ascontiguousarray(table, dtype=np.float32)
+    L = len(table)
+    n = np.zeros(L, np.int32)
+    base = np.zeros(L + 1, np.int64)
+    _check(lib().wf_ec_tables(table.ctypes.data, L, n.ctypes.data, base.ctypes.data, None, 0))
+    cum = np.zeros(int(base[-1]), np.uint32)
+    _check(lib().wf_ec_tables(table.ctypes.data, L, None, None, cum.ctypes.data, len(cum)))
+    return n, base, cum

@@ -173,3 +173,29 @@ def test_masks_of_any_radius(lib, mask, R, W_min):
     other = inputs.make_weights(16, 1, radius=1 if R != 1 else 2)
     with pytest.raises(ValueError):
         wf.make_desc(other, inputs.scale_table(), 4, W_min, mask=mask)
+
+
+def test_entropy_coder_validation(lib):
+    d, keep = _desc(entropy_coder="rans", driver="graph")
+    assert wf.validate(d) == wf.WF_OK
+    d.entropy_coder = 2
+    assert wf.validate(d) == wf.WF_E_INVALID
+    for kw in (dict(K=3), dict(group=2), dict(driver="persistent"), dict(driver="dataflow")):
+        args = dict(entropy_coder="rans", driver="graph")
+        args.update(kw)
+        d, keep = _desc(**args)
+        assert wf.validate(d) == wf.WF_E_UNSUPPORTED, kw
+        assert b"entropy" in lib.wf_last_error()
+
+
+def test_entropy_tables_match_the_oracle(lib):
+    """The library builds its rANS tables itself; they must equal the
+    oracle's, entry for entry (the coder's bits depend on every one)."""
+    import oracle
+    for table in (inputs.scale_table(), inputs.scale_table(levels=17, lo=0.5, hi=40.0)):
+        n, base, cum = wf.ec_tables(table)
+        on, obase, ocum = oracle.rans_tables(table)
+        assert np.array_equal(n, on) and np.array_equal(base, obase) and np.array_equal(cum, ocum)
+    with pytest.raises(wf.WfError) as e:
+        wf.ec_tables(np.array([1.0, 3000.0], np.float32))
+    assert e.value.code == wf.WF_E_UNSUPPORTED
