@@ -391,26 +391,37 @@ def main():
         pe = wf.Plan(w, table, cfg["H"], cfg["W"], cfg["B"], cfg["K"], mask=mask_of(cfg), precision=args.precision,
                      driver=args.driver, entropy_coder="rans")
         u = inputs.make_noise(cfg["B"], cfg["H"], cfg["W"], cfg["M"])
-        y_d = (torch.from_numpy(sym.astype(np.float32) + u).cuda() + out["mean"]).contiguous()
         bits = torch.zeros((2 + 4 * cfg["W"]) * cfg["B"] * cfg["H"] * cfg["M"], dtype=torch.int32, device="cuda")
-        _, sym_e, offs = pe.encode_bits(psi_d, y_d, bits, stream=stream)
-        pe.sync(stream)
-        n_words = int(offs[-1].item())
         out_b = pe.alloc_out()
         sym_b = torch.empty_like(sym_d)
 
-        def dec_bits():
-            pe.decode_bits(psi_d, bits, offs, out=out_b, sym_out=sym_b, n_words=n_words, stream=stream)
+        def measure(sym_np):
+            # encoder input whose symbols are sym_np, then the timed decodes from its streams
+            s_d = torch.from_numpy(sym_np).cuda()
+            m = pe.decode(psi_d, s_d, stream=stream)["mean"]
+            y_d = (torch.from_numpy(sym_np.astype(np.float32) + u).cuda() + m).contiguous()
+            _, sym_e, offs = pe.encode_bits(psi_d, y_d, bits, stream=stream)
+            pe.sync(stream)
+            n_words = int(offs[-1].item())
 
-        dec_bits()
-        pe.sync(stream)
-        bwall, bper = timed_calls(dec_bits, args.steps, stream, torch)
-        pe.sync(stream)
+            def dec_bits():
+                pe.decode_bits(psi_d, bits, offs, out=out_b, sym_out=sym_b, n_words=n_words, stream=stream)
+
+            dec_bits()
+            pe.sync(stream)
+            bwall, bper = timed_calls(dec_bits, args.steps, stream, torch)
+            pe.sync(stream)
+            return {"ms_per_image": bwall * 1e3 / args.steps / cfg["B"], "launch_ms_events": float(np.mean(bper)),
+                    "stream_words": n_words, "bits_per_symbol": 32.0 * n_words / sym_np.size,
+                    "symbols_match": bool(torch.equal(sym_b, s_d)) and bool(torch.equal(sym_e, s_d))}
+
+        rec_ec = measure(sym)
+        # symbols in {-1, 0, 1} lie inside every level's support: no escapes
+        rec_ec["no_escapes"] = measure(np.clip(sym, -1, 1).astype(np.int32))
+        rec_ec["streams"] = ("one per (image, grid row, channel); 64-bit rANS state, 32-bit words, 2^-16 Gaussian "
+                             "tables; the workload's symbols do not follow the random model's scales, so most of "
+                             "them escape")
         pe.close()
-        rec_ec = {"ms_per_image": bwall * 1e3 / args.steps / cfg["B"], "launch_ms_events": float(np.mean(bper)),
-                  "stream_words": n_words, "bits_per_symbol": 32.0 * n_words / sym.size,
-                  "symbols_match": bool(torch.equal(sym_b, sym_d)) and bool(torch.equal(sym_e, sym_d)),
-                  "streams": "one per (image, grid row, channel); 64-bit rANS state, 32-bit words, 2^-16 Gaussian tables"}
         del bits
 
     lat = cfg["B"] * cfg["H"] * cfg["W"]

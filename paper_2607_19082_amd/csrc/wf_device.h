@@ -978,15 +978,19 @@ __device__ __forceinline__ void ec_renorm(const CallPtrs* cp, uint64_t& x, uint3
 __device__ __forceinline__ int32_t ec_decode(const CallPtrs* cp, int lvl, uint64_t& x, uint32_t& pos, uint32_t end,
                                              uint32_t wnext, bool& bad) {
     const int n = cp->ec_n[lvl];
-    const uint32_t* cum = cp->ec_cum + cp->ec_base[lvl];
     const uint32_t slot = (uint32_t)x & ((1u << kEcPrecBits) - 1u);
-    int u = cp->ec_lut[(size_t)lvl * kEcLut + (slot >> kEcLutShift)];
-    uint32_t c0 = cum[u], c1 = cum[u + 1];
-    // at most 15 symbols start inside a bucket after its first
-    for (int g = 0; g < (1 << kEcLutShift) && c1 <= slot; ++g) {
-        ++u;
-        c0 = c1;
-        c1 = cum[u + 1];
+    // the bucket's first symbol and its interval: one load in the common case
+    const uint64_t ent = cp->ec_lut[(size_t)lvl * kEcLut + (slot >> kEcLutShift)];
+    int u = (int)(ent & 0xffffu);
+    uint32_t c0 = (uint32_t)(ent >> 16) & 0xffffu, c1 = (uint32_t)(ent >> 32);
+    if (c1 <= slot) {
+        // a later symbol of the bucket: at most 15 start inside it after its first
+        const uint32_t* cum = cp->ec_cum + cp->ec_base[lvl];
+        for (int g = 0; g < (1 << kEcLutShift) && c1 <= slot; ++g) {
+            ++u;
+            c0 = c1;
+            c1 = cum[u + 1];
+        }
     }
     x = (uint64_t)(c1 - c0) * (x >> kEcPrecBits) + slot - c0;
     ec_renorm(cp, x, pos, end, wnext, bad);
@@ -1015,7 +1019,7 @@ __device__ __forceinline__ void l3_ec_tile(const StepArgs& a, const StepRows& s,
                                            const float* tab) {
     using A = typename P::A;
     using Bw = typename P::B;
-    constexpr int KBW = P::kL3Kbw1 / 2;
+    constexpr int KBW = P::kL3Kbw1;   // one batch per wave, as in l3_tile
     const int M = a.M, G = M / kTile, cg = jb.ct, rt = jb.rt;
     const int wave = wave_id(), lane = threadIdx.x & 63, kq = lane >> 4;
     const CallPtrs* cp = a.cp;
@@ -1261,8 +1265,9 @@ __device__ __forceinline__ void l1_group_tile(const StepArgs& a, const StepRows&
     }
 }
 
-// The main job of phase ph (sm.tab must hold the scale table for PH_C).
-template <class P, int KC, bool COH>
+// The main job of phase ph (sm.tab must hold the scale table for PH_C); EC:
+// phase C decodes the symbols from their rANS streams (a.ec set, K = 1).
+template <class P, int KC, bool COH, bool EC = false>
 __device__ __forceinline__ void phase_job(int ph, const StepArgs& a, const StepRows& s, int b, f4 (*red)[64],
                                           L3Smem<KC>& sm) {
     if (ph == PH_GA) {
@@ -1270,8 +1275,8 @@ __device__ __forceinline__ void phase_job(int ph, const StepArgs& a, const StepR
         if (jb.valid) l1_group_tile<P, COH>(a, s, jb, red);
         return;
     }
-    if constexpr (KC == 1) {
-        if (ph == PH_C && a.ec) {
+    if constexpr (EC && KC == 1) {
+        if (ph == PH_C) {
             l3_ec_job<P, COH>(a, s, b, red, sm.tab);
             return;
         }

@@ -53,9 +53,10 @@ static double level_mass(int u, int n, double sigma) {
 
 // Frequency tables of a scale table: n [L], base [L+1] (first cumulative
 // entry of each level), cum (2n+3 entries per level) and, when lut != NULL,
-// the symbol holding the first slot of every 16-slot bucket [L][kEcLut].
+// for every 16-slot bucket [L][kEcLut] the symbol u holding its first slot
+// with cum[u] and cum[u + 1], packed as u | cum[u] << 16 | cum[u + 1] << 32.
 static int ec_tables(const float* table, int L, std::vector<int32_t>& n, std::vector<int64_t>& base,
-                     std::vector<uint32_t>& cum, std::vector<uint16_t>* lut) {
+                     std::vector<uint32_t>& cum, std::vector<uint64_t>* lut) {
     n.assign(L, 0);
     base.assign(L + 1, 0);
     for (int l = 0; l < L; ++l) {
@@ -79,12 +80,12 @@ static int ec_tables(const float* table, int L, std::vector<int32_t>& n, std::ve
         uint32_t* c = cum.data() + base[l];
         for (int u = 0; u < K; ++u) c[u + 1] = c[u] + f[u];
         if (lut) {
-            uint16_t* q = lut->data() + (size_t)l * kEcLut;
+            uint64_t* q = lut->data() + (size_t)l * kEcLut;
             int u = 0;
             for (int b = 0; b < kEcLut; ++b) {
                 const uint32_t slot = (uint32_t)b << kEcLutShift;
                 while (c[u + 1] <= slot) ++u;
-                q[b] = (uint16_t)u;
+                q[b] = (uint64_t)u | ((uint64_t)c[u] << 16) | ((uint64_t)c[u + 1] << 32);
             }
         }
     }
@@ -111,7 +112,7 @@ int build_ec(Plan* p, const float* scale_table, int L) {
     std::vector<int32_t> n;
     std::vector<int64_t> base;
     std::vector<uint32_t> cum;
-    std::vector<uint16_t> lut;
+    std::vector<uint64_t> lut;
     int rc = ec_tables(scale_table, L, n, base, cum, &lut);
     if (rc != WF_OK) return rc;
     std::vector<int32_t> base32(L);

@@ -91,7 +91,7 @@ struct CallPtrs {
     const int32_t* ec_n;    // [L] support half-width per level
     const int32_t* ec_base; // [L] first cumulative entry per level
     const uint32_t* ec_cum; // cumulative frequencies
-    const uint16_t* ec_lut; // [L][kEcLut] symbol at the start of each slot bucket
+    const uint64_t* ec_lut; // [L][kEcLut] per slot bucket: its first slot's symbol u, cum[u], cum[u + 1]
     int* err;
 };
 
@@ -199,7 +199,7 @@ struct Plan {
     int ec = 0;
     int32_t *ec_n = nullptr, *ec_base = nullptr;
     uint32_t* ec_cum = nullptr;
-    uint16_t* ec_lut = nullptr;
+    uint64_t* ec_lut = nullptr;
     uint64_t* ec_x = nullptr;
     uint32_t *ec_pos = nullptr, *ec_end = nullptr, *ec_len = nullptr, *ec_words = nullptr;
     hipGraph_t graph_ec = nullptr;

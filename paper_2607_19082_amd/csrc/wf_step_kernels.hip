@@ -26,8 +26,9 @@ __global__ __launch_bounds__(kThreads) void k_gctx(StepRows s, int nc, StepArgs 
 }
 
 // Phase ph of step s (blocks [0, nb)), then old-tap context jobs [j0, ...)
-// of step s1.
-template <class P, int KC>
+// of step s1.  EC: the decode from rANS streams (its phase C job holds more
+// registers, so it is a kernel of its own).
+template <class P, int KC, bool EC = false>
 __global__ __launch_bounds__(kThreads) void k_phase(int ph, StepRows s, StepRows s1, int nb, int j0, int nc,
                                                     StepArgs a) {
     __shared__ f4 red[kWaves * kMaxC][64];
@@ -40,7 +41,7 @@ __global__ __launch_bounds__(kThreads) void k_phase(int ph, StepRows s, StepRows
         for (int l = threadIdx.x; l < a.L; l += blockDim.x) sm.tab[l] = a.table[l];
         __syncthreads();
     }
-    phase_job<P, KC, false>(ph, a, s, blockIdx.x, red, sm);
+    phase_job<P, KC, false, EC>(ph, a, s, blockIdx.x, red, sm);
 }
 
 __global__ void k_set_call(CallPtrs* dst, CallPtrs v) {
@@ -119,8 +120,12 @@ static void launch_steps(Plan& p, hipStream_t stream, bool ec) {
         const StepWork w = step_work<P>(a, s, s1);
         for (int ph = P::kFirst; ph < kMaxPhases; ++ph) {
             const int n = w.nb[ph] + w.cut[ph + 1] - w.cut[ph];
-            hipLaunchKernelGGL((k_phase<P, KC>), dim3(n), dim3(kThreads), 0, stream, ph, s, s1, w.nb[ph],
-                               w.cut[ph], w.nc, a);
+            if (ec && ph == PH_C)
+                hipLaunchKernelGGL((k_phase<P, KC, true>), dim3(n), dim3(kThreads), 0, stream, ph, s, s1, w.nb[ph],
+                                   w.cut[ph], w.nc, a);
+            else
+                hipLaunchKernelGGL((k_phase<P, KC>), dim3(n), dim3(kThreads), 0, stream, ph, s, s1, w.nb[ph],
+                                   w.cut[ph], w.nc, a);
         }
     }
 }
