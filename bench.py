@@ -180,6 +180,14 @@ def summarize_stats(stats_dir, log, out, command):
               f"HIP-event time of one decode (under the profiler) was {rec['roofline']['launch_ms_events']:.3f} ms; "
               f"bench line: {rec['ms_per_step']:.3f} ms per decode, {rec['value']:.0f} latents/s.  For the graph "
               "and stream drivers the difference is the gaps between kernels."]
+    ec = rec.get("entropy_decode")
+    if ec:
+        lines += ["", "This run also times the decode from rANS streams (`entropy_decode` in the bench line: "
+                  f"{ec['ms_per_image']:.3f} ms per image, {ec['no_escapes']['ms_per_image']:.3f} ms for a stream "
+                  "without escapes; the stream encoder "
+                  f"{ec['encode_bits_ms_per_image']:.3f} ms).  Its phase C runs as `k_phase<…, true>` (one launch "
+                  "per step), its stream set-up as `k_ec_init`; the stream encoder is `k_ec_encode`, `k_ec_scan`, "
+                  "`k_ec_compact`.  The per-call line above then mixes both decodes."]
     with open(out, "w") as f:
         f.write("\n".join(lines) + "\n")
     print(json.dumps({"calls": calls, "decode_kernel_ms_per_call": dec / max(calls, 1) / 1e6}))
@@ -403,6 +411,9 @@ def main():
             _, sym_e, offs = pe.encode_bits(psi_d, y_d, bits, stream=stream)
             pe.sync(stream)
             n_words = int(offs[-1].item())
+            n_enc = max(3, args.steps // 4)
+            ewall, _ = timed_calls(lambda: pe.encode_bits(psi_d, y_d, bits, stream=stream), n_enc, stream, torch)
+            pe.sync(stream)
 
             def dec_bits():
                 pe.decode_bits(psi_d, bits, offs, out=out_b, sym_out=sym_b, n_words=n_words, stream=stream)
@@ -412,6 +423,7 @@ def main():
             bwall, bper = timed_calls(dec_bits, args.steps, stream, torch)
             pe.sync(stream)
             return {"ms_per_image": bwall * 1e3 / args.steps / cfg["B"], "launch_ms_events": float(np.mean(bper)),
+                    "encode_bits_ms_per_image": ewall * 1e3 / n_enc / cfg["B"],
                     "stream_words": n_words, "bits_per_symbol": 32.0 * n_words / sym_np.size,
                     "symbols_match": bool(torch.equal(sym_b, s_d)) and bool(torch.equal(sym_e, s_d))}
 
