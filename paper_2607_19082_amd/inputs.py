@@ -18,7 +18,11 @@ nor the trained weights are used here; seeded draws stand in for them:
 * encoder noise u ~ U(-0.5 + g, 0.5 - g), seed 3 (the encoder input is
   symbol + u + mean of the matching decode);
 * the scale table: 64 levels spaced evenly in log between 0.11 and 256,
-  computed in fp64 and rounded to fp32 once.
+  computed in fp64 and rounded to fp32 once;
+* transform weights (hyper-decoder and synthesis, for timing only), seed 4:
+  conv weights ~ N(0, 1/fan_in), biases from the same law, GDN beta ~
+  1 + U(0, 0.1) and gamma = 0.1 I + U(0, 0.01 / N) (positive, as GDN needs);
+* the quantised hyper-latent z_hat: N(0, 2) rounded half-to-even, seed 5.
 """
 import numpy as np
 
@@ -114,3 +118,34 @@ def make_inputs(name, H=None, W=None, B=None):
     psi = make_psi(cfg["B"], cfg["H"], cfg["W"], cfg["M"])
     sym = make_symbols(cfg["B"], cfg["H"], cfg["W"], cfg["M"], cfg["lap_b"], cfg["clip"])
     return cfg, w, scale_table(), psi, sym
+
+
+def make_transform_weights(N, M, seed=4):
+    """Random weights of the hyper-decoder (hs1..hs3) and the synthesis
+    transform (gs1..gs4 with GDN parameters gdn1..gdn3), PyTorch layouts:
+    transposed convs [in][out][5][5], the 3x3 conv [out][in][3][3]."""
+    rng = np.random.default_rng(seed)
+
+    def draw(shape, fan_in):
+        return (rng.standard_normal(shape) / np.sqrt(fan_in)).astype(np.float32)
+
+    w = {}
+    c = M * 3 // 2
+    for name, cin, cout in (("hs1", N, M), ("hs2", M, c)):
+        w[name + "_w"] = draw((cin, cout, 5, 5), cin * 25 // 4)
+        w[name + "_b"] = draw((cout,), cin * 25 // 4)
+    w["hs3_w"] = draw((2 * M, c, 3, 3), c * 9)
+    w["hs3_b"] = draw((2 * M,), c * 9)
+    for k, (cin, cout) in enumerate(((M, N), (N, N), (N, N), (N, 3)), start=1):
+        w[f"gs{k}_w"] = draw((cin, cout, 5, 5), cin * 25 // 4)
+        w[f"gs{k}_b"] = draw((cout,), cin * 25 // 4)
+        if k < 4:
+            w[f"gdn{k}_beta"] = (1.0 + 0.1 * rng.random(cout)).astype(np.float32)
+            w[f"gdn{k}_gamma"] = (0.1 * np.eye(cout) + (0.01 / cout) * rng.random((cout, cout))).astype(np.float32)
+    return w
+
+
+def make_zhat(B, Hz, Wz, N, seed=5):
+    """Quantised hyper-latent [B][Hz][Wz][N] (integer values as fp32)."""
+    rng = np.random.default_rng(seed)
+    return np.rint(rng.normal(scale=2.0, size=(B, Hz, Wz, N))).astype(np.float32)
