@@ -219,6 +219,25 @@ def mask_of(cfg):
     return cfg.get("mask") or ("relaxed" if cfg["relaxed"] else "full")
 
 
+# transform channels N of the hyper-latent and the synthesis (M -> N)
+XFORM_N = {192: 128, 320: 192}
+
+
+def synthesis_flops(N, M, lat):
+    """2 x MACs of g_s per image of `lat` latents: four stride-2 transposed
+    convs (25/4 taps per output pixel) and three inverse GDNs (N x N)."""
+    px = [4 * lat, 16 * lat, 64 * lat, 256 * lat]
+    macs = px[0] * N * M * 25 / 4 + (px[1] + px[2]) * N * N * 25 / 4 + px[3] * 3 * N * 25 / 4
+    macs += (px[0] + px[1] + px[2]) * N * N
+    return 2 * macs
+
+
+def hyper_flops(N, M, lat):
+    """2 x MACs of h_s (on the 4x-upsampled z grid, ~lat latents)."""
+    c = M * 3 // 2
+    return 2 * (lat / 4 * M * N * 25 / 4 + lat * c * M * 25 / 4 + lat * 2 * M * c * 9)
+
+
 def flops_per_latent(cfg):
     """Algorithmic FLOPs of one latent (2 x MACs): the context product over the
     causal taps and the three layers of the entropy-parameter network."""
@@ -307,6 +326,8 @@ def main():
                     help="context approximation: decode N wavefronts per step (1: exact decode)")
     ap.add_argument("--cpu-rows", type=int, default=16, help="grid rows of the CPU-oracle sample (0: skip)")
     ap.add_argument("--no-encode", action="store_true")
+    ap.add_argument("--no-transforms", action="store_true",
+                    help="skip the hyper-decoder and synthesis timing (end-to-end decode)")
     ap.add_argument("--no-entropy", action="store_true",
                     help="skip the decode from rANS streams (measured by default when the plan allows it)")
     ap.add_argument("--summarize-traffic", nargs=4, metavar=("FETCH_DIR", "WRITE_DIR", "CAL_FETCH_DIR", "CAL_WRITE_DIR"),
@@ -436,6 +457,35 @@ def main():
         pe.close()
         del bits
 
+    # the transforms around the decode: hyper-decoder (z_hat -> psi) and
+    # synthesis (y_hat -> image), random weights, for an end-to-end timing
+    rec_e2e = None
+    if not args.no_transforms and args.group <= 1:
+        N = XFORM_N.get(cfg["M"], 192)
+        xf = wf.Xform(inputs.make_transform_weights(N, cfg["M"]), N, cfg["M"], cfg["B"], cfg["H"], cfg["W"],
+                      args.precision)
+        z_d = torch.from_numpy(inputs.make_zhat(cfg["B"], -(-cfg["H"] // 4), -(-cfg["W"] // 4), N)).cuda()
+        psi_x = torch.empty_like(psi_d)
+        img = torch.empty((cfg["B"], 16 * cfg["H"], 16 * cfg["W"], 3), dtype=torch.float32, device="cuda")
+        xf.hyper_synthesis(z_d, psi=psi_x, stream=stream)
+        xf.synthesis(out["y_hat"], image=img, stream=stream)
+        torch.cuda.synchronize()
+        n_x = max(3, args.steps // 4)
+        hwall, hper = timed_calls(lambda: xf.hyper_synthesis(z_d, psi=psi_x, stream=stream), n_x, stream, torch)
+        gwall, gper = timed_calls(lambda: xf.synthesis(out["y_hat"], image=img, stream=stream), n_x, stream, torch)
+        finite = bool(torch.isfinite(img).all().item()) and bool(torch.isfinite(psi_x).all().item())
+        xf.close()
+        hs_ms, gs_ms = hwall * 1e3 / n_x / cfg["B"], gwall * 1e3 / n_x / cfg["B"]
+        dec_img_ms = wall * 1e3 / args.steps / cfg["B"]
+        rec_e2e = {"hyper_decoder_ms_per_image": hs_ms, "synthesis_ms_per_image": gs_ms,
+                   "ar_decode_ms_per_image": dec_img_ms, "ms_per_image": hs_ms + dec_img_ms + gs_ms,
+                   "N": N, "outputs_finite": finite,
+                   "synthesis_gflop": synthesis_flops(N, cfg["M"], cfg["B"] * cfg["H"] * cfg["W"]) / 1e9,
+                   "hyper_decoder_gflop": hyper_flops(N, cfg["M"], cfg["B"] * cfg["H"] * cfg["W"]) / 1e9}
+        if rec_ec is not None:
+            rec_e2e["ms_per_image_with_entropy_decode"] = hs_ms + rec_ec["ms_per_image"] + gs_ms
+        del img
+
     lat = cfg["B"] * cfg["H"] * cfg["W"]
     ms = wall * 1e3 / args.steps
     value = lat / (ms * 1e-3)
@@ -486,6 +536,7 @@ def main():
         "ms_per_image": ms / cfg["B"],
         "encode": rec_enc,
         "entropy_decode": rec_ec,
+        "end_to_end": rec_e2e,
     }
     if args.cpu_rows > 0:
         rec["cpu_baseline"] = cpu_baseline(args.workload, args.cpu_rows, args.mask)

@@ -290,6 +290,50 @@ int wf_measure_floor(wf_plan_t plan, float *node_us, float *barrier_us);
  */
 int wf_plan_sync(wf_plan_t plan, hipStream_t stream);
 
+/*
+ * The transforms around the autoregressive decode, for an end-to-end decode
+ * timing (the latent pipeline of Sec. II-A; random weights, as no trained
+ * ones are used): the hyper-decoder h_s (z_hat -> psi, the hyperprior half
+ * of the entropy parameters) and the synthesis transform g_s (y_hat ->
+ * image).  Layers (the mean-scale hyperprior model family the workloads are
+ * named after; PyTorch weight layouts, HOST arrays copied by the plan):
+ *   h_s: hs_w[0] [N][M][5][5]      transposed conv 5x5 s2 (padding 2, output
+ *                                  padding 1), + hs_b[0] [M], ReLU
+ *        hs_w[1] [M][3M/2][5][5]   the same, + hs_b[1], ReLU
+ *        hs_w[2] [2M][3M/2][3][3]  conv 3x3 s1 (padding 1), + hs_b[2] [2M]
+ *   g_s: gs_w[k] [Cin][Cout][5][5] transposed conv 5x5 s2 + gs_b[k], for
+ *        (Cin, Cout) = (M, N), (N, N), (N, N), (N, 3); after each of the first
+ *        three: inverse GDN, out_c = x_c sqrt(gdn_beta[k][c] +
+ *        sum_j gdn_gamma[k][c][j] x_j^2)
+ * z_hat has ceil(H/4) x ceil(W/4) pixels; psi is the top-left H x W of h_s's
+ * output.  N, M and 3M/2 must be multiples of 16 (fp32) or 32 (bf16).
+ */
+typedef struct {
+    int32_t N, M;           /* channels of z_hat and of y_hat                       */
+    int32_t B, H, W;        /* images and the latent grid of y_hat                  */
+    int32_t precision;      /* wf_precision (bf16: bf16 weights, activations as pairs) */
+    const float *hs_w[3], *hs_b[3];
+    const float *gs_w[4], *gs_b[4];
+    const float *gdn_beta[3], *gdn_gamma[3];
+} wf_xform_desc;
+
+typedef struct wf_xform_s *wf_xform_t;
+
+/* Build the transform plan (packed weights and workspace, ~2 x B*64*H*W*N
+ * floats).  Synchronous; errors as wf_plan (WF_E_UNSUPPORTED for channel
+ * counts off the k-block or activations beyond the 2 GiB buffer window). */
+int wf_xform_plan(const wf_xform_desc *desc, wf_xform_t *out);
+
+/* psi [B][H][W][2M] = h_s(z_hat [B][ceil(H/4)][ceil(W/4)][N]); DEVICE fp32,
+ * asynchronous on `stream`, one call in flight per plan. */
+int wf_hyper_synthesis(wf_xform_t plan, const float *z_hat, float *psi, hipStream_t stream);
+
+/* image [B][16H][16W][3] = g_s(y_hat [B][H][W][M]); DEVICE fp32, asynchronous. */
+int wf_synthesis(wf_xform_t plan, const float *y_hat, float *image, hipStream_t stream);
+
+/* Release a transform plan.  NULL is ignored. */
+void wf_xform_destroy(wf_xform_t plan);
+
 /* Release everything the plan owns.  NULL is ignored. */
 void wf_plan_destroy(wf_plan_t plan);
 

@@ -23,7 +23,8 @@ DRIVER = {"stream": 0, "graph": 1, "persistent": 2, "dataflow": 3}
 
 EXPORTS = ["wf_schedule", "wf_validate", "wf_plan", "wf_plan_schedule", "wf_decode",
            "wf_encode", "wf_ec_tables", "wf_encode_bits", "wf_decode_bits", "wf_plan_trace",
-           "wf_measure_floor", "wf_plan_sync", "wf_plan_destroy", "wf_last_error"]
+           "wf_measure_floor", "wf_plan_sync", "wf_xform_plan", "wf_hyper_synthesis", "wf_synthesis",
+           "wf_xform_destroy", "wf_plan_destroy", "wf_last_error"]
 
 
 class WfError(RuntimeError):
@@ -46,6 +47,16 @@ class Desc(ctypes.Structure):
         ("scale_table", ctypes.c_void_p), ("L", ctypes.c_int32),
         ("group", ctypes.c_int32), ("param_order", ctypes.c_int32),
         ("entropy_coder", ctypes.c_int32),
+    ]
+
+
+class XformDesc(ctypes.Structure):
+    _fields_ = [
+        ("N", ctypes.c_int32), ("M", ctypes.c_int32), ("B", ctypes.c_int32),
+        ("H", ctypes.c_int32), ("W", ctypes.c_int32), ("precision", ctypes.c_int32),
+        ("hs_w", ctypes.c_void_p * 3), ("hs_b", ctypes.c_void_p * 3),
+        ("gs_w", ctypes.c_void_p * 4), ("gs_b", ctypes.c_void_p * 4),
+        ("gdn_beta", ctypes.c_void_p * 3), ("gdn_gamma", ctypes.c_void_p * 3),
     ]
 
 
@@ -76,6 +87,10 @@ def lib():
         L.wf_ec_tables.argtypes = [P, ctypes.c_int32, P, P, P, ctypes.c_int64]
         L.wf_encode_bits.argtypes = [P, P, P, P, ctypes.POINTER(Out), P, ctypes.c_int64, P, P]
         L.wf_decode_bits.argtypes = [P, P, P, ctypes.c_int64, P, P, ctypes.POINTER(Out), P]
+        L.wf_xform_plan.argtypes = [ctypes.POINTER(XformDesc), ctypes.POINTER(ctypes.c_void_p)]
+        L.wf_hyper_synthesis.argtypes = [P, P, P, P]
+        L.wf_synthesis.argtypes = [P, P, P, P]
+        L.wf_xform_destroy.argtypes = [P]
         L.wf_plan_trace.argtypes = [P, P, ctypes.c_int64, P, P]
         L.wf_measure_floor.argtypes = [P, P, P]
         L.wf_plan_sync.argtypes = [P, P]
@@ -84,6 +99,7 @@ def lib():
         L.wf_last_error.restype = ctypes.c_char_p
         for name in EXPORTS[:-2]:
             getattr(L, name).restype = ctypes.c_int
+        L.wf_xform_destroy.restype = None
         _lib = L
     return _lib
 
@@ -297,3 +313,68 @@ def ec_tables(table):
     cum = np.zeros(int(base[-1]), np.uint32)
     _check(lib().wf_ec_tables(table.ctypes.data, L, None, None, cum.ctypes.data, len(cum)))
     return n, base, cum
+
+
+class Xform:
+    """The hyper-decoder and synthesis transforms on the GPU (weights as drawn
+    by inputs.make_transform_weights, PyTorch layouts).  Calls take and return
+    torch tensors on the current HIP device, asynchronously on the stream."""
+
+    def __init__(self, weights, N, M, B, H, W, precision="fp32"):
+        a = {k: np.ascontiguousarray(v, dtype=np.float32) for k, v in weights.items()}
+        M2 = M * 3 // 2
+        shapes = {"hs1_w": (N, M, 5, 5), "hs2_w": (M, M2, 5, 5), "hs3_w": (2 * M, M2, 3, 3),
+                  "gs1_w": (M, N, 5, 5), "gs2_w": (N, N, 5, 5), "gs3_w": (N, N, 5, 5), "gs4_w": (N, 3, 5, 5)}
+        for k, shp in shapes.items():
+            if a[k].shape != shp:
+                raise ValueError(f"{k} must have shape {shp}, got {a[k].shape}")
+        d = XformDesc(N, M, B, H, W, PRECISION[precision])
+        for k in range(3):
+            d.hs_w[k] = a[f"hs{k + 1}_w"].ctypes.data
+            d.hs_b[k] = a[f"hs{k + 1}_b"].ctypes.data
+            d.gdn_beta[k] = a[f"gdn{k + 1}_beta"].ctypes.data
+            d.gdn_gamma[k] = a[f"gdn{k + 1}_gamma"].ctypes.data
+        for k in range(4):
+            d.gs_w[k] = a[f"gs{k + 1}_w"].ctypes.data
+            d.gs_b[k] = a[f"gs{k + 1}_b"].ctypes.data
+        h = ctypes.c_void_p()
+        _check(lib().wf_xform_plan(ctypes.byref(d), ctypes.byref(h)))
+        self._h = h
+        self.N, self.M, self.B, self.H, self.W = N, M, B, H, W
+
+    def close(self):
+        if getattr(self, "_h", None):
+            lib().wf_xform_destroy(self._h)
+            self._h = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+    @staticmethod
+    def _ptr(t, shape, name):
+        import torch
+        if not isinstance(t, torch.Tensor) or not t.is_cuda or t.dtype != torch.float32 or \
+                tuple(t.shape) != tuple(shape) or not t.is_contiguous():
+            raise ValueError(f"{name}: expected a contiguous fp32 CUDA tensor {tuple(shape)}")
+        return ctypes.c_void_p(t.data_ptr())
+
+    def hyper_synthesis(self, z_hat, psi=None, stream=None):
+        import torch
+        B, H, W, N, M = self.B, self.H, self.W, self.N, self.M
+        if psi is None:
+            psi = torch.empty((B, H, W, 2 * M), dtype=torch.float32, device=z_hat.device)
+        _check(lib().wf_hyper_synthesis(self._h, self._ptr(z_hat, (B, -(-H // 4), -(-W // 4), N), "z_hat"),
+                                        self._ptr(psi, (B, H, W, 2 * M), "psi"), _stream_handle(stream)))
+        return psi
+
+    def synthesis(self, y_hat, image=None, stream=None):
+        import torch
+        B, H, W, M = self.B, self.H, self.W, self.M
+        if image is None:
+            image = torch.empty((B, 16 * H, 16 * W, 3), dtype=torch.float32, device=y_hat.device)
+        _check(lib().wf_synthesis(self._h, self._ptr(y_hat, (B, H, W, M), "y_hat"),
+                                  self._ptr(image, (B, 16 * H, 16 * W, 3), "image"), _stream_handle(stream)))
+        return image

@@ -199,3 +199,32 @@ def test_entropy_tables_match_the_oracle(lib):
     with pytest.raises(wf.WfError) as e:
         wf.ec_tables(np.array([1.0, 3000.0], np.float32))
     assert e.value.code == wf.WF_E_UNSUPPORTED
+
+
+def test_xform_validation(lib):
+    """The transform plan refuses bad descriptions before touching the GPU."""
+    w = inputs.make_transform_weights(32, 64)
+    x = wf.XformDesc(32, 64, 1, 5, 7, 0)
+    keep = {k: np.ascontiguousarray(v, np.float32) for k, v in w.items()}
+    for k in range(3):
+        x.hs_w[k] = keep[f"hs{k + 1}_w"].ctypes.data
+        x.hs_b[k] = keep[f"hs{k + 1}_b"].ctypes.data
+        x.gdn_beta[k] = keep[f"gdn{k + 1}_beta"].ctypes.data
+        x.gdn_gamma[k] = keep[f"gdn{k + 1}_gamma"].ctypes.data
+    for k in range(4):
+        x.gs_w[k] = keep[f"gs{k + 1}_w"].ctypes.data
+        x.gs_b[k] = keep[f"gs{k + 1}_b"].ctypes.data
+    h = ctypes.c_void_p()
+    for field, value, want in (("N", 24, wf.WF_E_UNSUPPORTED), ("precision", 5, wf.WF_E_INVALID),
+                               ("H", 0, wf.WF_E_INVALID), ("W", 100000, wf.WF_E_UNSUPPORTED)):
+        old = getattr(x, field)
+        setattr(x, field, value)
+        assert lib.wf_xform_plan(ctypes.byref(x), ctypes.byref(h)) == want, field
+        setattr(x, field, old)
+    x.precision = 1
+    x.M = 48   # 3M/2 = 72 is not a multiple of the bf16 k-block
+    assert lib.wf_xform_plan(ctypes.byref(x), ctypes.byref(h)) == wf.WF_E_UNSUPPORTED
+    x.M, x.precision = 64, 0
+    x.gs_w[2] = None
+    assert lib.wf_xform_plan(ctypes.byref(x), ctypes.byref(h)) == wf.WF_E_INVALID
+    assert lib.wf_xform_plan(None, ctypes.byref(h)) == wf.WF_E_INVALID
