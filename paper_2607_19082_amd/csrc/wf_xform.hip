@@ -18,7 +18,11 @@
 // pairs, tap-major.  Inverse GDN is the same product over the channels of
 // the squared input, x_c sqrt(beta_c + sum_j gamma_cj x_j^2), with gamma^T
 // as the weight panel.  Weights are packed per layer and class in the operand
-// order of the step kernels.
+// order of the step kernels.  A transposed conv with at most 4 output
+// channels (the image's 3) puts all four classes into the columns instead:
+// rows are input pixels, columns (class, channel), k the 3x3 input
+// neighbourhood (taps a class does not use have zero weights), so one
+// 16-column tile carries all 12 outputs of an input pixel.
 #include <cmath>
 #include <vector>
 
@@ -27,7 +31,7 @@
 
 namespace wf {
 
-enum { XM_DECONV = 0, XM_CONV3 = 1, XM_GDN = 2 };
+enum { XM_DECONV = 0, XM_CONV3 = 1, XM_GDN = 2, XM_DECONV4 = 3 };
 
 struct ConvArgs {
     const float* in;
@@ -56,8 +60,8 @@ __global__ __launch_bounds__(kThreads) void k_conv(ConvArgs a) {
     using S = ConvShape<CTW, WCOL>;
     constexpr int KB = P::kBf16 ? 6 : 8;   // k-blocks in flight per wave
     const int cls = blockIdx.z, py = cls >> 1, px = cls & 1;
-    const int nky = MODE == XM_DECONV ? (py ? 2 : 3) : (MODE == XM_CONV3 ? 3 : 1);
-    const int nkx = MODE == XM_DECONV ? (px ? 2 : 3) : (MODE == XM_CONV3 ? 3 : 1);
+    const int nky = MODE == XM_DECONV ? (py ? 2 : 3) : (MODE == XM_GDN ? 1 : 3);
+    const int nkx = MODE == XM_DECONV ? (px ? 2 : 3) : (MODE == XM_GDN ? 1 : 3);
     const int cbn = a.Ci / P::kK;                        // k-blocks per tap
     const int nkb = nky * nkx * cbn;
     const int nrows = a.B * a.Hq * a.Wq, nct = a.Cop / kTile;
@@ -95,7 +99,7 @@ __global__ __launch_bounds__(kThreads) void k_conv(ConvArgs a) {
             const int ty = t / nkx;
             dy = 1 - ty;
             dx = 1 - (t - ty * nkx);
-        } else if (MODE == XM_CONV3) {
+        } else if (MODE == XM_CONV3 || MODE == XM_DECONV4) {
             const int ty = t / 3;
             dy = ty - 1;
             dx = t - ty * 3 - 1;
@@ -143,8 +147,10 @@ __global__ __launch_bounds__(kThreads) void k_conv(ConvArgs a) {
     // lane holds rows 4*(lane/16) + q of each row tile, column lane%16
 #pragma unroll
     for (int j = 0; j < CTW; ++j) {
-        const int c = (ct0 + j) * kTile + (lane & 15);
-        if (!cv[j] || c >= a.Co) continue;
+        const int cc = (ct0 + j) * kTile + (lane & 15);   // column: channel, or (class, channel)
+        const int ccls = MODE == XM_DECONV4 ? cc / a.Co : 0;
+        const int c = MODE == XM_DECONV4 ? cc - ccls * a.Co : cc;
+        if (!cv[j] || c >= a.Co || ccls >= 4) continue;
         const float add = MODE == XM_GDN ? a.beta[c] : a.bias[c];
 #pragma unroll
         for (int i = 0; i < 2; ++i)
@@ -154,7 +160,14 @@ __global__ __launch_bounds__(kThreads) void k_conv(ConvArgs a) {
                 if (ro >= nrows) continue;
                 const int b = ro / (a.Hq * a.Wq), rem = ro - b * a.Hq * a.Wq;
                 const int qy = rem / a.Wq, qx = rem - qy * a.Wq;
-                const int oy = MODE == XM_DECONV ? 2 * qy + py : qy, ox = MODE == XM_DECONV ? 2 * qx + px : qx;
+                int oy = qy, ox = qx;
+                if (MODE == XM_DECONV) {
+                    oy = 2 * qy + py;
+                    ox = 2 * qx + px;
+                } else if (MODE == XM_DECONV4) {
+                    oy = 2 * qy + (ccls >> 1);
+                    ox = 2 * qx + (ccls & 1);
+                }
                 if (oy >= a.Ho || ox >= a.Wo) continue;
                 float v = acc[i][j][q] + add;
                 if (MODE == XM_GDN) {
@@ -213,12 +226,13 @@ static int xf_pack(Xform* x, Layer& L, int nclass, F wt) {
     const bool bf = x->precision == WF_BF16;
     for (int c = 0; c < nclass; ++c) {
         const int py = c >> 1, px = c & 1;
-        const int nky = L.mode == XM_DECONV ? (py ? 2 : 3) : (L.mode == XM_CONV3 ? 3 : 1);
-        const int nkx = L.mode == XM_DECONV ? (px ? 2 : 3) : (L.mode == XM_CONV3 ? 3 : 1);
+        const int nky = L.mode == XM_DECONV ? (py ? 2 : 3) : (L.mode == XM_GDN ? 1 : 3);
+        const int nkx = L.mode == XM_DECONV ? (px ? 2 : 3) : (L.mode == XM_GDN ? 1 : 3);
         const int K = nky * nkx * L.Ci;
         auto f = [&](int k, int n) { return wt(c, k / L.Ci, nkx, k % L.Ci, n); };
-        int rc = bf ? xf_upload(x, reinterpret_cast<const uint16_t**>(&L.wp[c]), pack_panel_bf16(K, L.Co, K, L.Cop, f))
-                    : xf_upload(x, reinterpret_cast<const float**>(&L.wp[c]), pack_panel(K, L.Co, K, L.Cop, f));
+        const int ncol = L.mode == XM_DECONV4 ? 4 * L.Co : L.Co;   // columns that carry weights
+        int rc = bf ? xf_upload(x, reinterpret_cast<const uint16_t**>(&L.wp[c]), pack_panel_bf16(K, ncol, K, L.Cop, f))
+                    : xf_upload(x, reinterpret_cast<const float**>(&L.wp[c]), pack_panel(K, ncol, K, L.Cop, f));
         if (rc != WF_OK) return rc;
     }
     for (int c = nclass; c < 4; ++c) L.wp[c] = L.wp[0];
@@ -231,6 +245,22 @@ static int xf_deconv(Xform* x, Layer& L, const float* w, const float* b, int Ci,
     L.mode = XM_DECONV; L.Ci = Ci; L.Co = Co; L.Cop = (Co + kTile - 1) / kTile * kTile; L.relu = relu;
     int rc = xf_pack(x, L, 4, [&](int c, int t, int nkx, int ci, int co) {
         const int ky = (c >> 1) + 2 * (t / nkx), kx = (c & 1) + 2 * (t % nkx);
+        return w[(((size_t)ci * Co + co) * 5 + ky) * 5 + kx];
+    });
+    if (rc != WF_OK) return rc;
+    return xf_upload(x, &L.bias, std::vector<float>(b, b + Co));
+}
+
+// All four classes in the columns (Co <= 4): column n = class * Co + co, tap
+// (dy, dx) = (t / 3 - 1, t % 3 - 1) of the input neighbourhood, which class
+// (py, px) reaches through (ky, kx) = (py + 2 - 2 dy, px + 2 - 2 dx) when both
+// are at most 4 (zero weight otherwise).
+static int xf_deconv4(Xform* x, Layer& L, const float* w, const float* b, int Ci, int Co) {
+    L.mode = XM_DECONV4; L.Ci = Ci; L.Co = Co; L.Cop = (4 * Co + kTile - 1) / kTile * kTile; L.relu = 0;
+    int rc = xf_pack(x, L, 1, [&](int, int t, int, int ci, int n) -> float {
+        const int cls = n / Co, co = n - cls * Co;
+        const int ky = (cls >> 1) + 2 - 2 * (t / 3 - 1), kx = (cls & 1) + 2 - 2 * (t % 3 - 1);
+        if (ky > 4 || kx > 4) return 0.0f;
         return w[(((size_t)ci * Co + co) * 5 + ky) * 5 + kx];
     });
     if (rc != WF_OK) return rc;
@@ -279,6 +309,7 @@ static void run_layer(const Layer& L, const float* in, float* out, int B, int Hi
                       hipStream_t st) {
     if (L.mode == XM_DECONV) launch_layer<P, XM_DECONV>(L, in, out, B, Hi, Wi, Hi, Wi, Ho, Wo, st);
     else if (L.mode == XM_CONV3) launch_layer<P, XM_CONV3>(L, in, out, B, Hi, Wi, Ho, Wo, Ho, Wo, st);
+    else if (L.mode == XM_DECONV4) launch_layer<P, XM_DECONV4>(L, in, out, B, Hi, Wi, Hi, Wi, Ho, Wo, st);
     else launch_layer<P, XM_GDN>(L, in, out, B, Hi, Wi, Hi, Wi, Hi, Wi, st);
 }
 
@@ -350,7 +381,8 @@ int wf_xform_plan(const wf_xform_desc* d, wf_xform_t* out) {
     if (rc == WF_OK) rc = xf_conv3(x, x->hs[2], d->hs_w[2], d->hs_b[2], C, 2 * M);
     const int gi[4] = {M, N, N, N}, go[4] = {N, N, N, 3};
     for (int k = 0; k < 4 && rc == WF_OK; ++k) {
-        rc = xf_deconv(x, x->gs[k], d->gs_w[k], d->gs_b[k], gi[k], go[k], 0);
+        rc = go[k] <= 4 ? xf_deconv4(x, x->gs[k], d->gs_w[k], d->gs_b[k], gi[k], go[k])
+                        : xf_deconv(x, x->gs[k], d->gs_w[k], d->gs_b[k], gi[k], go[k], 0);
         if (rc == WF_OK && k < 3) rc = xf_gdn(x, x->gdn[k], d->gdn_beta[k], d->gdn_gamma[k], N);
     }
     const size_t B = d->B;
