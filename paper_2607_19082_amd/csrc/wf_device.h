@@ -570,7 +570,7 @@ __device__ __forceinline__ void hoist_job(const StepArgs& a, int b) {
 // Tap gather of k-block kb of a row's taps (fp32: y_hat, bf16: its pair
 // form), for the old taps (tap-major, `old` true) or the new taps.  A k-block
 // never straddles two taps (M is a multiple of the k-block).
-template <class P, bool COH>
+template <class P, bool COH, bool R3 = true>
 __device__ __forceinline__ typename P::A ld_tap(const StepArgs& a, const Row& w, int kb, int kq, bool old) {
     const int M = a.M;
     const int tap = kb * P::kK / M;
@@ -580,8 +580,9 @@ __device__ __forceinline__ typename P::A ld_tap(const StepArgs& a, const Row& w,
         // the tap's row (0 = row -R) and the row's first tap, wave-uniform
         // (nested selects: a loop here costs the old-tap jobs many SGPRs)
         static_assert(kMaxRadius == 3, "rows -3..0");
-        const int row = tap < a.old_start[0] ? 0 : (tap < a.old_start[1] ? 1 : (tap < a.old_start[2] ? 2 : 3));
-        const int first = row == 0 ? 0 : (row == 1 ? a.old_start[0] : (row == 2 ? a.old_start[1] : a.old_start[2]));
+        // (R3 false: masks of radius at most 2, whose old taps lie in three rows)
+        const int row = tap < a.old_start[0] ? 0 : (tap < a.old_start[1] ? 1 : (!R3 || tap < a.old_start[2] ? 2 : 3));
+        const int first = row == 0 ? 0 : (row == 1 ? a.old_start[0] : (!R3 || row == 2 ? a.old_start[1] : a.old_start[2]));
         dy = row - a.R;
         dx = tap - first - a.R;
     } else {
@@ -629,10 +630,15 @@ __device__ __forceinline__ void ctxo_tile(const StepArgs& a, const StepRows& s, 
         }
     }
     const Row w = step_row(a, s, jb.rt * kTile + (lane & 15));
-    auto la = [&](int kb) { return ld_tap<P, COH>(a, w, kb, kq, true); };
     const int nkb = a.n_old * M / P::kK;
     const int klo = nkb * part / NP, khi = nkb * (part + 1) / NP;
-    block_tiles<P>(red, a.wp_old, nkb, jb.ct, la, v, klo, khi);
+    if (a.R == kMaxRadius) {   // (wave-uniform)
+        auto la = [&](int kb) { return ld_tap<P, COH, true>(a, w, kb, kq, true); };
+        block_tiles<P>(red, a.wp_old, nkb, jb.ct, la, v, klo, khi);
+    } else {
+        auto la = [&](int kb) { return ld_tap<P, COH, false>(a, w, kb, kq, true); };
+        block_tiles<P>(red, a.wp_old, nkb, jb.ct, la, v, klo, khi);
+    }
     if (vo) {
 #pragma unroll
         for (int c = 0; c < C; ++c)
