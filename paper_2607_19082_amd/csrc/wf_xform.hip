@@ -46,19 +46,19 @@ struct ConvArgs {
     int relu;
 };
 
-// Rows: 2 row tiles per wave, 4 / WCOL waves along the rows; columns: CTW
+// Rows: RTW row tiles per wave, 4 / WCOL waves along the rows; columns: CTW
 // column tiles per wave, WCOL waves along the columns.
-template <int CTW, int WCOL>
+template <int RTW, int CTW, int WCOL>
 struct ConvShape {
-    static constexpr int kRowTiles = 2 * (4 / WCOL), kColTiles = CTW * WCOL;
+    static constexpr int kRowTiles = RTW * (4 / WCOL), kColTiles = CTW * WCOL;
 };
 
-template <class P, int MODE, int CTW, int WCOL>
+template <class P, int MODE, int RTW, int CTW, int WCOL>
 __global__ __launch_bounds__(kThreads) void k_conv(ConvArgs a) {
     using A = typename P::A;
     using Bw = typename P::B;
-    using S = ConvShape<CTW, WCOL>;
-    constexpr int KB = P::kBf16 ? 6 : 8;   // k-blocks in flight per wave
+    using S = ConvShape<RTW, CTW, WCOL>;
+    constexpr int KB = RTW == 4 || P::kBf16 ? 6 : 8;   // k-blocks in flight per wave
     const int cls = blockIdx.z, py = cls >> 1, px = cls & 1;
     const int nky = MODE == XM_DECONV ? (py ? 2 : 3) : (MODE == XM_GDN ? 1 : 3);
     const int nkx = MODE == XM_DECONV ? (px ? 2 : 3) : (MODE == XM_GDN ? 1 : 3);
@@ -69,13 +69,13 @@ __global__ __launch_bounds__(kThreads) void k_conv(ConvArgs a) {
     const int cb = blockIdx.x % ncb, rb = blockIdx.x / ncb;
     const int wave = wave_id(), lane = threadIdx.x & 63, kq = lane >> 4;
     const int wr = wave / WCOL, wc = wave % WCOL;
-    const int rt0 = rb * S::kRowTiles + wr * 2, ct0 = cb * S::kColTiles + wc * CTW;
+    const int rt0 = rb * S::kRowTiles + wr * RTW, ct0 = cb * S::kColTiles + wc * CTW;
     if (rt0 * kTile >= nrows) return;                    // (whole wave past the rows; no barrier below)
 
-    int rb_[2], ry[2], rx[2];
-    bool rv[2];
+    int rb_[RTW], ry[RTW], rx[RTW];
+    bool rv[RTW];
 #pragma unroll
-    for (int i = 0; i < 2; ++i) {
+    for (int i = 0; i < RTW; ++i) {
         const int r = (rt0 + i) * kTile + (lane & 15);
         rv[i] = r < nrows;
         const int rr = rv[i] ? r : 0;
@@ -120,19 +120,19 @@ __global__ __launch_bounds__(kThreads) void k_conv(ConvArgs a) {
             return u;
         }
     };
-    f4 acc[2][CTW];
+    f4 acc[RTW][CTW];
 #pragma unroll
-    for (int i = 0; i < 2; ++i)
+    for (int i = 0; i < RTW; ++i)
 #pragma unroll
         for (int j = 0; j < CTW; ++j) acc[i][j] = zero4();
     for (int kc = 0; kc < nkb; kc += KB) {
-        A av[KB][2];
+        A av[KB][RTW];
         Bw bv[KB][CTW];
 #pragma unroll
         for (int u = 0; u < KB; ++u) {
             const int k = min(kc + u, nkb - 1);
 #pragma unroll
-            for (int i = 0; i < 2; ++i) av[u][i] = la(i, k);
+            for (int i = 0; i < RTW; ++i) av[u][i] = la(i, k);
 #pragma unroll
             for (int j = 0; j < CTW; ++j) bv[u][j] = w[j][(size_t)k * 64];
         }
@@ -140,7 +140,7 @@ __global__ __launch_bounds__(kThreads) void k_conv(ConvArgs a) {
         for (int u = 0; u < KB; ++u)
             if (kc + u < nkb)
 #pragma unroll
-                for (int i = 0; i < 2; ++i)
+                for (int i = 0; i < RTW; ++i)
 #pragma unroll
                     for (int j = 0; j < CTW; ++j) acc[i][j] = P::mma(av[u][i], bv[u][j], acc[i][j]);
     }
@@ -153,7 +153,7 @@ __global__ __launch_bounds__(kThreads) void k_conv(ConvArgs a) {
         if (!cv[j] || c >= a.Co || ccls >= 4) continue;
         const float add = MODE == XM_GDN ? a.beta[c] : a.bias[c];
 #pragma unroll
-        for (int i = 0; i < 2; ++i)
+        for (int i = 0; i < RTW; ++i)
 #pragma unroll
             for (int q = 0; q < 4; ++q) {
                 const int ro = (rt0 + i) * kTile + kq * 4 + q;
@@ -292,15 +292,20 @@ static void launch_layer(const Layer& L, const float* in, float* out, int B, int
     a.B = B; a.Hi = Hi; a.Wi = Wi; a.Ci = L.Ci; a.Hq = Hq; a.Wq = Wq;
     a.Co = L.Co; a.Cop = L.Cop; a.Ho = Ho; a.Wo = Wo; a.relu = L.relu;
     const int nrows = B * Hq * Wq, nct = L.Cop / kTile, ncls = MODE == XM_DECONV ? 4 : 1;
-    if (nct <= 1) {   // narrow output (the image's 3 channels): 8 row tiles x 1 column tile per workgroup
-        using S = ConvShape<1, 1>;
+    // Row tiles per wave: 4 with fp32 operands (each weight operand then feeds
+    // four MFMA chains, which halves the weight reads against 2); bf16 pairs
+    // already hold twice the registers per operand and keep 2 (measured:
+    // 4 was 5% slower there).
+    constexpr int RTW = P::kBf16 ? 2 : 4;
+    if (nct <= 1) {   // narrow output (the image's 3 channels): 4 RTW row tiles x 1 column tile per workgroup
+        using S = ConvShape<RTW, 1, 1>;
         const int nb = ((nrows + S::kRowTiles * kTile - 1) / (S::kRowTiles * kTile)) * nct;
-        hipLaunchKernelGGL((k_conv<P, MODE, 1, 1>), dim3(nb, 1, ncls), dim3(kThreads), 0, st, a);
-    } else {          // 4 row tiles x 4 column tiles per workgroup
-        using S = ConvShape<2, 2>;
+        hipLaunchKernelGGL((k_conv<P, MODE, RTW, 1, 1>), dim3(nb, 1, ncls), dim3(kThreads), 0, st, a);
+    } else {          // 2 RTW row tiles x 4 column tiles per workgroup
+        using S = ConvShape<RTW, 2, 2>;
         const int nb = ((nrows + S::kRowTiles * kTile - 1) / (S::kRowTiles * kTile)) *
                        ((nct + S::kColTiles - 1) / S::kColTiles);
-        hipLaunchKernelGGL((k_conv<P, MODE, 2, 2>), dim3(nb, 1, ncls), dim3(kThreads), 0, st, a);
+        hipLaunchKernelGGL((k_conv<P, MODE, RTW, 2, 2>), dim3(nb, 1, ncls), dim3(kThreads), 0, st, a);
     }
 }
 
