@@ -44,10 +44,17 @@ DECODE_KERNELS = ("wf::k_phase", "wf::k_hoist", "wf::k_ctxo", "wf::k_set_call", 
                   "wf::k_dataflow", "wf::k_zero_u128")
 
 
+# sources that no decode from symbols runs (the transforms, the entropy coder)
+NOT_DECODE = ("wf_xform.hip", "wf_ec.hip")
+
+
 def source_hash():
-    """sha256 over the kernel sources: counters taken on other sources are stale."""
+    """sha256 over the sources of the decode's kernels and plan: counters taken
+    on other sources are stale."""
     h = hashlib.sha256()
     for f in sorted(glob.glob(os.path.join(CSRC, "*.h")) + glob.glob(os.path.join(CSRC, "*.hip"))):
+        if os.path.basename(f) in NOT_DECODE:
+            continue
         h.update(os.path.basename(f).encode())
         with open(f, "rb") as fh:
             h.update(fh.read())
@@ -188,6 +195,13 @@ def summarize_stats(stats_dir, log, out, command):
                   f"{ec['encode_bits_ms_per_image']:.3f} ms).  Its phase C runs as `k_phase<…, true>` (one launch "
                   "per step), its stream set-up as `k_ec_init`; the stream encoder is `k_ec_encode`, `k_ec_scan`, "
                   "`k_ec_compact`.  The per-call line above then mixes both decodes."]
+    e2e = rec.get("end_to_end")
+    if e2e:
+        lines += ["", "This run also times the transforms (`end_to_end` in the bench line): the hyper-decoder "
+                  f"{e2e['hyper_decoder_ms_per_image']:.3f} ms and the synthesis {e2e['synthesis_ms_per_image']:.3f} "
+                  f"ms per image ({e2e['ms_per_image']:.3f} ms end to end with the decode); their layers run as "
+                  "`k_conv<P, mode, row tiles, column tiles, column waves>` (mode 0: transposed conv by output "
+                  "class, 1: 3x3 conv, 2: inverse GDN, 3: the image layer with the classes as columns)."]
     with open(out, "w") as f:
         f.write("\n".join(lines) + "\n")
     print(json.dumps({"calls": calls, "decode_kernel_ms_per_call": dec / max(calls, 1) / 1e6}))
