@@ -44,6 +44,15 @@ DECODE_KERNELS = ("wf::k_phase", "wf::k_hoist", "wf::k_ctxo", "wf::k_set_call", 
                   "wf::k_dataflow", "wf::k_zero_u128")
 
 
+# kernels of the bench's per-step latency leg (one traced decode by the
+# persistent driver); when another driver is timed they stay out of its summaries
+LEG_KERNELS = ("wf::k_persistent", "wf::k_zero_u32")
+
+
+def leg_kernel(k, driver):
+    return driver != "persistent" and any(x in k for x in LEG_KERNELS)
+
+
 # sources that no decode from symbols runs (the transforms, the entropy coder)
 NOT_DECODE = ("wf_xform.hip", "wf_ec.hip")
 
@@ -88,7 +97,7 @@ def _pmc_rows(d):
     return list(con.execute("select kernel_name, counter_name, value from counters_collection"))
 
 
-def summarize_traffic(fetch_dir, write_dir, cal_fetch_dir, cal_write_dir, cal_bytes, out, command):
+def summarize_traffic(fetch_dir, write_dir, cal_fetch_dir, cal_write_dir, cal_bytes, out, command, driver):
     """Per-decode HBM bytes from rocprofv3 --pmc FETCH_SIZE / WRITE_SIZE runs
     (KiB per dispatch), each scaled by the same counter's reading for a plain
     copy of cal_bytes bytes."""
@@ -97,8 +106,10 @@ def summarize_traffic(fetch_dir, write_dir, cal_fetch_dir, cal_write_dir, cal_by
     is_copy = lambda k: "copyBuffer" in k or "copy" in k.lower()
     f_cal = cal_bytes / (1024.0 * total(cal_fetch_dir, "FETCH_SIZE", is_copy))
     w_cal = cal_bytes / (1024.0 * total(cal_write_dir, "WRITE_SIZE", is_copy))
-    is_dec = lambda k: any(x in k for x in DECODE_KERNELS)
-    decodes = sum(1 for k, c, v in _pmc_rows(fetch_dir) if c == "FETCH_SIZE" and "k_set_call" in k)
+    is_dec = lambda k: any(x in k for x in DECODE_KERNELS) and not leg_kernel(k, driver)
+    fetch_rows = _pmc_rows(fetch_dir)
+    decodes = sum(1 for k, c, v in fetch_rows if c == "FETCH_SIZE" and "k_set_call" in k) - \
+        sum(1 for k, c, v in fetch_rows if c == "FETCH_SIZE" and "wf::k_persistent" in k and leg_kernel(k, driver))
     fetch = total(fetch_dir, "FETCH_SIZE", is_dec) * 1024.0 * f_cal / decodes
     write = total(write_dir, "WRITE_SIZE", is_dec) * 1024.0 * w_cal / decodes
     with open(out, "w") as f:
@@ -113,7 +124,7 @@ def summarize_traffic(fetch_dir, write_dir, cal_fetch_dir, cal_write_dir, cal_by
                       "decodes": decodes}))
 
 
-def summarize_counters(dirs, out, command):
+def summarize_counters(dirs, out, command, driver):
     """MFMA utilisation and L2 hit rate of the decode's dispatches from
     rocprofv3 --pmc runs (one counter set per run): MfmaUtil (percent of the
     SIMDs' cycles with the matrix unit busy) weighted by dispatch duration,
@@ -124,7 +135,7 @@ def summarize_counters(dirs, out, command):
         db = glob.glob(os.path.join(d, "**", "*results.db"), recursive=True)[0]
         con = sqlite3.connect(db)
         rows += list(con.execute("select kernel_name, counter_name, value, duration from counters_collection"))
-    is_dec = lambda k: any(x in k for x in DECODE_KERNELS)
+    is_dec = lambda k: any(x in k for x in DECODE_KERNELS) and not leg_kernel(k, driver)
     short = lambda k: k.split("(")[0].replace("void ", "")
     per = {}
     for k, c, v, dur in rows:
@@ -158,23 +169,30 @@ def summarize_counters(dirs, out, command):
     print(json.dumps({"mfma_util_percent": mfma, "l2_hit_rate": hit}))
 
 
-def summarize_stats(stats_dir, log, out, command):
+def summarize_stats(stats_dir, log, out, command, l_floor_us=None):
     """Kernel statistics of a profiled bench run (rocprofv3 --kernel-trace
     --stats): the per-kernel table, and the decode kernels' time per call next
     to the HIP-event time of one decode from the same run's bench line."""
     import csv
     rows = list(csv.DictReader(open(glob.glob(os.path.join(stats_dir, "**", "*kernel_stats.csv"), recursive=True)[0])))
     rec = json.loads([l for l in open(log) if l.startswith('{"metric"')][-1])
-    calls = sum(int(r["Calls"]) for r in rows if "k_set_call" in r["Name"])
-    dec = sum(float(r["TotalDurationNs"]) for r in rows if any(x in r["Name"] for x in DECODE_KERNELS))
     cfg = rec["config"]
+    leg = [r for r in rows if leg_kernel(r["Name"], cfg["driver"])]
+    leg_calls = sum(int(r["Calls"]) for r in leg if "wf::k_persistent" in r["Name"])
+    rows = [r for r in rows if r not in leg]
+    calls = sum(int(r["Calls"]) for r in rows if "k_set_call" in r["Name"]) - leg_calls
+    dec = sum(float(r["TotalDurationNs"]) for r in rows if any(x in r["Name"] for x in DECODE_KERNELS))
     lines = [f"# Kernel statistics: {cfg['workload']}, {cfg['precision']}, {cfg['driver']} driver"
              + (f", context approximation N = {cfg['context_approximation_group']}"
                 if cfg.get("context_approximation_group", 1) > 1 else "")
-             + (f", {cfg['mask']} mask" if cfg.get("mask") not in (None, "full", "relaxed") else ""), "",
+             + (f", {cfg['mask']} mask" if cfg.get("mask") not in (None, "full", "relaxed") else "")
+             + (", with the decode from rANS streams" if rec.get("entropy_decode") else "")
+             + (", with the transforms" if rec.get("end_to_end") else ""), "",
              "Command (on one MI355X, from the repository root):", "", "```", command, "```", "",
              f"The run makes {calls} decode/encode calls (warm-up, timed decodes, encodes); per-call kernels appear "
-             f"that many times.  k_empty and k_barrier_rounds are the latency-floor probes of the bench.", "",
+             f"that many times.  k_empty and k_barrier_rounds are the latency-floor probes of the bench."
+             + (f"  The {leg_calls} traced decodes of the persistent driver (the bench's per-step latency leg) "
+                "are left out of this table." if leg_calls else ""), "",
              "| Kernel | Calls | Total (ms) | Average (us) | Min (us) | Max (us) | % |", "|---|---|---|---|---|---|---|"]
     for r in rows:
         if float(r["Percentage"]) < 0.05:
@@ -187,6 +205,21 @@ def summarize_stats(stats_dir, log, out, command):
               f"HIP-event time of one decode (under the profiler) was {rec['roofline']['launch_ms_events']:.3f} ms; "
               f"bench line: {rec['ms_per_step']:.3f} ms per decode, {rec['value']:.0f} latents/s.  For the graph "
               "and stream drivers the difference is the gaps between kernels."]
+    trace = glob.glob(os.path.join(stats_dir, "**", "*kernel_trace.csv"), recursive=True)
+    traced_floor = rec.get("latency_roofline", {}).get("L_floor_us")
+    lfloor = l_floor_us or traced_floor
+    # the bench's first calls are its warm-up and timed decodes: take the last timed one
+    hist = trace_step_latency(trace[0], rec["warmup"] + rec["steps"] - 1, cfg["steps_T"], lfloor) \
+        if trace and lfloor and cfg["driver"] in ("graph", "stream") else None
+    if hist:
+        busy, span = hist
+        src = (f"measured by a bench run without the profiler (the same probe under the tracer read "
+               f"{traced_floor:.2f} us)" if l_floor_us else "measured in this run, under the tracer")
+        lines += ["", "Per-step latency of the last timed decode in the trace, in multiples of the latency floor "
+                  f"L_floor = {lfloor:.2f} us, one dependent hop between graph nodes, {src}.  Busy: the sum of "
+                  "the step's phase kernels' durations.  Span: start of the step's first phase kernel to the "
+                  "start of the next step's, gaps included (the tracer lengthens the gaps).", ""]
+        lines += histogram_table(busy, "busy") + [""] + histogram_table(span, "span")
     ec = rec.get("entropy_decode")
     if ec:
         lines += ["", "This run also times the decode from rANS streams (`entropy_decode` in the bench line: "
@@ -202,6 +235,8 @@ def summarize_stats(stats_dir, log, out, command):
                   f"ms per image ({e2e['ms_per_image']:.3f} ms end to end with the decode); their layers run as "
                   "`k_conv<P, mode, row tiles, column tiles, column waves>` (mode 0: transposed conv by output "
                   "class, 1: 3x3 conv, 2: inverse GDN, 3: the image layer with the classes as columns)."]
+    # runs that also time the rANS decode or the transforms get a summary of their own
+    out = out[:-len(".md")] + ("_entropy" if ec else "") + ("_transforms" if e2e else "") + ".md"
     with open(out, "w") as f:
         f.write("\n".join(lines) + "\n")
     print(json.dumps({"calls": calls, "decode_kernel_ms_per_call": dec / max(calls, 1) / 1e6}))
@@ -312,6 +347,92 @@ def cpu_baseline(name, rows, mask=None):
             "ms_per_image_extrapolated": dt * 1e3 * (cfg["H"] / rows)}
 
 
+# bin edges of the per-step latency histograms, in multiples of L_floor
+HIST_EDGES = (0, 1, 2, 4, 8, 16, 32, 64, float("inf"))
+
+
+def latency_histogram(us, lfloor):
+    """Per-step latencies (microseconds) against the latency floor L_floor:
+    percentiles, and counts in bins of [a, b) x L_floor."""
+    us = np.asarray(us, dtype=np.float64)
+    x = us / lfloor
+    counts = [int(((x >= a) & (x < b)).sum()) for a, b in zip(HIST_EDGES[:-1], HIST_EDGES[1:])]
+    pct = (0, 10, 50, 90, 99, 100)
+    return {"L_floor_us": lfloor, "steps": int(us.size), "sum_ms": float(us.sum()) / 1e3,
+            "percentiles_us": {f"p{q}": round(float(v), 3) for q, v in zip(pct, np.percentile(us, pct))},
+            "median_over_L_floor": round(float(np.median(x)), 2),
+            "bins_in_L_floor": [f"[{a:g}, {b:g})" for a, b in zip(HIST_EDGES[:-1], HIST_EDGES[1:])],
+            "counts": counts}
+
+
+def histogram_table(h, what):
+    lines = [f"| {what} | " + " | ".join(h["bins_in_L_floor"]) + " |",
+             "|---|" + "---|" * len(h["counts"]),
+             "| steps | " + " | ".join(str(c) for c in h["counts"]) + " |"]
+    p = h["percentiles_us"]
+    lines += ["", f"{h['steps']} steps, {h['sum_ms']:.3f} ms in all; percentiles (us): "
+              + ", ".join(f"{k} {v:.2f}" for k, v in p.items())
+              + f"; median {h['median_over_L_floor']:.1f} x L_floor ({h['L_floor_us']:.2f} us)."]
+    return lines
+
+
+def trace_step_latency(trace_csv, call, T, lfloor):
+    """Per-step latencies of decode call number `call` (0-based, in launch
+    order) in a rocprofv3 kernel trace of the graph or stream driver: its
+    phase kernels, in launch order, are an equal number per step for its T
+    steps; a step's busy time is the sum of its phase kernels' durations, its
+    span the time from the start of its first phase kernel to the start of the
+    next step's (the last: to its last kernel's end), gaps included."""
+    import csv
+    rows = sorted(csv.DictReader(open(trace_csv)), key=lambda r: int(r["Start_Timestamp"]))
+    calls = [i for i, r in enumerate(rows) if "wf::k_set_call" in r["Kernel_Name"]]
+    if call >= len(calls):
+        return None
+    ph = []
+    for r in rows[calls[call] + 1:]:
+        k = r["Kernel_Name"]
+        if "wf::k_set_call" in k:
+            break
+        if "wf::k_phase" in k:
+            ph.append((int(r["Start_Timestamp"]), int(r["End_Timestamp"])))
+    if not ph or len(ph) % T:
+        return None
+    s = np.array([a for a, _ in ph], dtype=np.float64).reshape(T, -1)
+    e = np.array([b for _, b in ph], dtype=np.float64).reshape(T, -1)
+    busy = (e - s).sum(1) / 1e3
+    span = np.diff(np.append(s[:, 0], e[-1, -1])) / 1e3
+    return latency_histogram(busy, lfloor), latency_histogram(span, lfloor)
+
+
+def persistent_step_latency(w, table, cfg, precision, psi_d, sym_d, lfloor, torch, wf):
+    """Per-step latencies of one decode by the persistent driver, from the
+    device wall clock (100 MHz) that its trace hook records when workgroup 0
+    leaves each device-wide barrier: steps begin at the release of the
+    barrier before their first phase."""
+    pp = wf.Plan(w, table, cfg["H"], cfg["W"], cfg["B"], cfg["K"], mask=mask_of(cfg), precision=precision,
+                 driver="persistent")
+    try:
+        out = pp.alloc_out()
+        needed, G = pp.trace(None)
+        st = torch.zeros(needed, dtype=torch.int64, device="cuda")
+        for _ in range(2):
+            pp.decode(psi_d, sym_d, out=out)
+        pp.sync()
+        pp.trace(st)
+        pp.decode(psi_d, sym_d, out=out)
+        pp.sync()
+        pp.trace(None)
+        rel = st.cpu().numpy().reshape(-1, G + 1)[:, G].astype(np.float64)
+    finally:
+        pp.close()
+    # two barriers before the first step, then one after each of a step's phases
+    T = len(step_rows(cfg))
+    phases = (rel.size - 2) // T
+    assert rel.size == 2 + phases * T, (rel.size, T)
+    starts = rel[1 + phases * np.arange(T + 1)]
+    return latency_histogram(np.diff(starts) / 100.0, lfloor)
+
+
 def timed_calls(fn, steps, stream, torch):
     ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
           for _ in range(steps)]
@@ -342,6 +463,8 @@ def main():
     ap.add_argument("--no-encode", action="store_true")
     ap.add_argument("--no-transforms", action="store_true",
                     help="skip the hyper-decoder and synthesis timing (end-to-end decode)")
+    ap.add_argument("--no-step-latency", action="store_true",
+                    help="skip the per-step latency histogram (one traced decode by the persistent driver)")
     ap.add_argument("--no-entropy", action="store_true",
                     help="skip the decode from rANS streams (measured by default when the plan allows it)")
     ap.add_argument("--summarize-traffic", nargs=4, metavar=("FETCH_DIR", "WRITE_DIR", "CAL_FETCH_DIR", "CAL_WRITE_DIR"),
@@ -355,6 +478,8 @@ def main():
     ap.add_argument("--summarize-counters", nargs="+", metavar="PMC_DIR",
                     help="write the MFMA-utilisation / L2-hit summary of this workload/precision/driver "
                          "from rocprofv3 --pmc outputs (MfmaUtil; TCC_HIT_sum TCC_MISS_sum)")
+    ap.add_argument("--l-floor-us", type=float, default=None,
+                    help="latency floor of an unprofiled bench run for --summarize-stats' step histograms")
     ap.add_argument("--command", default="", help="the commands that made the counter outputs (recorded)")
     args = ap.parse_args()
     if args.copy_calibration:
@@ -365,19 +490,19 @@ def main():
         mk = f"_mask{args.mask}" if args.mask else ""
         summarize_stats(*args.summarize_stats,
                         os.path.join(PROFILES, f"kernels_{args.workload}_{args.precision}_{args.driver}{mk}{g}.md"),
-                        args.command)
+                        args.command, args.l_floor_us)
         return
     if args.summarize_counters:
         summarize_counters(args.summarize_counters,
                            os.path.join(PROFILES, f"counters_{args.workload}_{args.precision}_{args.driver}.md"),
-                           args.command)
+                           args.command, args.driver)
         return
     if args.summarize_traffic:
         summarize_traffic(*args.summarize_traffic, args.cal_bytes,
-                          traffic_file(args.workload, args.precision, args.driver), args.command)
+                          traffic_file(args.workload, args.precision, args.driver), args.command, args.driver)
         return
     if args.gpus != 1:
-        print(json.dumps({"error": "this build runs on one GPU only (--gpus 1); a multi-GPU run is not "
+        print(json.dumps({"error": "bench.py runs the decode on one GPU only (--gpus 1); a multi-GPU run is not "
                                    "part of it"}))
         sys.exit(2)
 
@@ -427,6 +552,13 @@ def main():
 
     node_us, bar_us = plan.measure_floor()
     plan.close()
+    lfloor = min(x for x in (node_us, bar_us) if x > 0)
+
+    rec_hist = None
+    if not args.no_step_latency and args.group <= 1:
+        rec_hist = {"driver": "persistent (device clock at each device-wide barrier; the graph driver's "
+                              "histogram is in its committed kernel-trace summary)",
+                    **persistent_step_latency(w, table, cfg, args.precision, psi_d, sym_d, lfloor, torch, wf)}
 
     # the decode that reads every symbol from its rANS stream inside the step loop
     rec_ec = None
@@ -510,7 +642,6 @@ def main():
     rows = step_rows(cfg, args.group)
     # the committed counter summaries cover the exact decode with the workload's own mask only
     traffic = read_traffic(args.workload, args.precision, args.driver) if args.group == 1 and own_mask else None
-    lfloor = min(x for x in (node_us, bar_us) if x > 0)
     f_step = rows * (flops_per_latent(cfg) - hoistable_flops_per_latent(cfg))
     t_roof_s = (hoistable_flops_per_latent(cfg) * lat) / (peak * 1e12) + np.maximum(
         f_step / (peak * 1e12), lfloor * 1e-6).sum()
@@ -545,8 +676,12 @@ def main():
                      "mfma_floor_ms": fl / (peak * 1e12) * 1e3},
         "latency_roofline": {"L_floor_us": lfloor, "graph_node_us": node_us, "barrier_round_us": bar_us,
                              "hops_per_step_algorithmic": 1, "T_roof_ms": t_roof_s * 1e3,
-                             "frac": t_roof_s * 1e3 / dec_ms},
+                             "frac": t_roof_s * 1e3 / dec_ms,
+                             "T_mfma_over_T_meas": fl / (peak * 1e12) * 1e3 / dec_ms,
+                             "T_L_floor_over_T_meas": T * lfloor * 1e-3 / dec_ms},
         "latents_per_s": value,
+        "symbols_per_s": value * cfg["M"],
+        "step_latency": rec_hist,
         "ms_per_image": ms / cfg["B"],
         "encode": rec_enc,
         "entropy_decode": rec_ec,

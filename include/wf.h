@@ -257,8 +257,9 @@ int wf_decode_bits(wf_plan_t plan, const float *psi, const uint32_t *bits, int64
  * entries) every later call records the device wall clock (100 MHz ticks):
  *  - persistent: at each device-wide barrier k = 0, 1, ...: entry k*(G+1) + g
  *    is the time workgroup g arrived at barrier k, entry k*(G+1) + G the time
- *    workgroup 0 left it.  A call has 2 + 3*T barriers with fp32 operands (two
- *    before the first step, then one per phase) and 1 + 4*T with bf16.
+ *    workgroup 0 left it.  A call has 2 + 3*T barriers (two before the first
+ *    step, then one after each of a step's three phases), with either
+ *    precision.
  *  - dataflow: three entries per job, 3*j + {0, 1, 2} = the time the job's
  *    workgroup started waiting for its inputs, the time they were complete,
  *    and the time its results had landed; j is the job's position in the
