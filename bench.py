@@ -124,11 +124,18 @@ def summarize_traffic(fetch_dir, write_dir, cal_fetch_dir, cal_write_dir, cal_by
                       "decodes": decodes}))
 
 
+# wave-state counters of one --pmc pass (eight SQ counters at most; the
+# pass also takes SQ_BUSY_CYCLES, which counts per shader engine, not per wave)
+WAVE_STATE = ("SQ_WAVE_CYCLES", "SQ_WAIT_ANY", "SQ_WAIT_INST_ANY", "SQ_ACTIVE_INST_ANY", "SQ_ACTIVE_INST_VALU",
+              "SQ_ACTIVE_INST_VMEM", "SQ_ACTIVE_INST_LDS")
+
+
 def summarize_counters(dirs, out, command, driver):
     """MFMA utilisation and L2 hit rate of the decode's dispatches from
     rocprofv3 --pmc runs (one counter set per run): MfmaUtil (percent of the
     SIMDs' cycles with the matrix unit busy) weighted by dispatch duration,
-    and TCC_HIT_sum / (TCC_HIT_sum + TCC_MISS_sum), overall and per kernel."""
+    and TCC_HIT_sum / (TCC_HIT_sum + TCC_MISS_sum), overall and per kernel;
+    with a pass of the WAVE_STATE counters also where the waves' cycles go."""
     import sqlite3
     rows = []
     for d in dirs:
@@ -151,6 +158,8 @@ def summarize_counters(dirs, out, command, driver):
             e["hit"] += v
         elif c == "TCC_MISS_sum":
             e["miss"] += v
+        elif c in WAVE_STATE:
+            e[c] = e.get(c, 0.0) + v
     tot = {k: sum(e[k] for e in per.values()) for k in ("dur", "mfma_w", "mfma_dur", "hit", "miss")}
     mfma = tot["mfma_w"] / tot["mfma_dur"] if tot["mfma_dur"] else float("nan")
     hit = tot["hit"] / (tot["hit"] + tot["miss"]) if tot["hit"] + tot["miss"] else float("nan")
@@ -165,6 +174,14 @@ def summarize_counters(dirs, out, command, driver):
             mu = e["mfma_w"] / e["mfma_dur"] if e["mfma_dur"] else float("nan")
             hr = e["hit"] / (e["hit"] + e["miss"]) if e["hit"] + e["miss"] else float("nan")
             f.write(f"| `{k}` | {e['n']} | {mu:.2f} | {hr:.4f} |\n")
+        if any("SQ_WAVE_CYCLES" in e for e in per.values()):
+            f.write("\nWave state (share of SQ_WAVE_CYCLES, the cycles waves were resident; the SQ_ACTIVE_INST_* "
+                    "shares overlap with each other):\n\n| Kernel | " + " | ".join(WAVE_STATE[1:]) + " |\n|---|"
+                    + "---|" * (len(WAVE_STATE) - 1) + "\n")
+            for k, e in sorted(per.items(), key=lambda kv: -kv[1]["dur"]):
+                if e.get("SQ_WAVE_CYCLES"):
+                    f.write(f"| `{k}` | " + " | ".join(f"{e.get(c, 0.0) / e['SQ_WAVE_CYCLES']:.3f}"
+                                                       for c in WAVE_STATE[1:]) + " |\n")
         f.write("\nCommands:\n\n```\n" + command + "\n```\n")
     print(json.dumps({"mfma_util_percent": mfma, "l2_hit_rate": hit}))
 
