@@ -696,7 +696,11 @@ __device__ __forceinline__ void l1_fold_job(const StepArgs& a, const StepRows& s
 // W1[:, 2M:]; the context bias is folded into P1.
 template <bool COH>
 __device__ __forceinline__ void l1_fold_bf16_tile(const StepArgs& a, const StepRows& s, Job jb, f4 (*red)[64]) {
-    constexpr int C = PBF16::kC, KBW = 5;
+    // k-blocks a wave loads before its MFMAs: all ten of a 4K step's wave in
+    // one batch in the phase kernels (245 registers, still two waves per
+    // SIMD); five in the persistent and dataflow kernels, whose loop state
+    // would otherwise spill
+    constexpr int C = PBF16::kC, KBW = COH ? 5 : 10;
     const int wave = wave_id(), lane = threadIdx.x & 63, kq = lane >> 4;
     const int M = a.M;
     // epilogue operands first: the hoisted part of this wave's row
