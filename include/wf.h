@@ -38,7 +38,7 @@ extern "C" {
 typedef enum {
     WF_OK = 0,
     WF_E_INVALID = -1,      /* bad argument (NULL, non-positive size, ...)     */
-    WF_E_UNSUPPORTED = -2,  /* valid but not supported by this build           */
+    WF_E_UNSUPPORTED = -2,  /* valid but not supported by this library         */
     WF_E_HIP = -3,          /* a HIP runtime call failed                       */
     WF_E_NOMEM = -4,        /* device or host allocation failed                */
     WF_E_TIMEOUT = -5,      /* a device-side wait exceeded its spin budget     */

@@ -228,3 +228,17 @@ def test_xform_validation(lib):
     x.gs_w[2] = None
     assert lib.wf_xform_plan(ctypes.byref(x), ctypes.byref(h)) == wf.WF_E_INVALID
     assert lib.wf_xform_plan(None, ctypes.byref(h)) == wf.WF_E_INVALID
+
+
+def test_size_limit(lib):
+    """The largest problem a plan accepts: every array the kernels address
+    through one raw-buffer window (0x7fff0000 bytes) must fit it; with M = 16
+    the binding one is the layer-1 activations, B*H*W rows of d1 = 53 values
+    padded to 64 fp32."""
+    d, keep = _desc(H=1, W=0x7fff0000 // 256 - 1)
+    assert wf.validate(d) == wf.WF_OK
+    d, keep = _desc(H=1, W=0x7fff0000 // 256)
+    assert wf.validate(d) == wf.WF_E_UNSUPPORTED
+    assert b"too large" in lib.wf_last_error()
+    d, keep = _desc(H=4096, W=4096, B=4)
+    assert wf.validate(d) == wf.WF_E_UNSUPPORTED
