@@ -482,41 +482,46 @@ __device__ __forceinline__ int group_col(int cg, int c) {
 // ---------------------------------------------------------------------------
 // Pre-loop job b: P1[lat][n] = b_hoist[n] + sum_k psi[lat][k] * W1[n][k]
 // (k < 2M), a plain dense product over all latents.  A workgroup computes a
-// 64-latent x 64-column block; each wave a 32 x 32 quarter (2 x 2 MFMA tiles)
-// over the whole K, so every operand load feeds two MFMA chains and no
-// cross-wave reduction is needed.  Column blocks are placed XCD-aware.
-constexpr int kHoistTiles = 4;   // 16-row / 16-column tiles per workgroup edge
+// (32 RT)-latent x 64-column block; its four waves form a 2 x 2 grid, each
+// wave RT row tiles x 2 column tiles over the whole K, so every activation
+// load feeds two MFMA chains and every weight load RT, and no cross-wave
+// reduction is needed.  Column blocks are placed XCD-aware.
+constexpr int kHoistCols = 4;    // 16-column tiles per workgroup
 
+template <int RT>
 __host__ __device__ __forceinline__ int hoist_blocks(const StepArgs& a) {
-    const int ncb = (a.Np1 / kTile + kHoistTiles - 1) / kHoistTiles;
-    const int nrb = (a.B * a.H * a.W + kTile * kHoistTiles - 1) / (kTile * kHoistTiles);
+    const int ncb = (a.Np1 / kTile + kHoistCols - 1) / kHoistCols;
+    const int nrb = (a.B * a.H * a.W + kTile * 2 * RT - 1) / (kTile * 2 * RT);
     return xcd_blocks(ncb, nrb);
 }
 
-template <class P, bool COH>
+// RT row tiles per wave, KB k-blocks in flight per wave.
+template <class P, bool COH, int RT, int KB>
 __device__ __forceinline__ void hoist_job(const StepArgs& a, int b) {
     using A = typename P::A;
     using Bw = typename P::B;
-    constexpr int KB = P::kBf16 ? 6 : 8;   // k-blocks in flight per wave
     const int nlat = a.B * a.H * a.W;
     const int nct = a.Np1 / kTile;
-    const int ncb = (nct + kHoistTiles - 1) / kHoistTiles;
-    const Job jb = xcd_job(b, ncb, (nlat + kTile * kHoistTiles - 1) / (kTile * kHoistTiles));
+    const int ncb = (nct + kHoistCols - 1) / kHoistCols;
+    const Job jb = xcd_job(b, ncb, (nlat + kTile * 2 * RT - 1) / (kTile * 2 * RT));
     if (!jb.valid) return;
     const int wave = wave_id(), lane = threadIdx.x & 63, kq = lane >> 4;
-    const int rt0 = jb.rt * kHoistTiles + (wave >> 1) * 2;      // this wave's two row tiles
-    const int ct0 = jb.ct * kHoistTiles + (wave & 1) * 2;       // and two column tiles
+    const int rt0 = jb.rt * 2 * RT + (wave >> 1) * RT;          // this wave's RT row tiles
+    const int ct0 = jb.ct * kHoistCols + (wave & 1) * 2;        // and two column tiles
     const float* psi = a.cp->psi;
     const int nkb = 2 * a.M / P::kK;
-    int r[2];
-    bool rv[2], cv[2];
+    int r[RT];
+    bool rv[RT], cv[2];
     const Bw* w[2];
 #pragma unroll
-    for (int i = 0; i < 2; ++i) {
+    for (int i = 0; i < RT; ++i) {
         r[i] = (rt0 + i) * kTile + (lane & 15);
         rv[i] = r[i] < nlat;
-        cv[i] = ct0 + i < nct;                                   // wave-uniform
-        w[i] = static_cast<const Bw*>(a.wp_hoist) + (size_t)(cv[i] ? ct0 + i : 0) * nkb * 64 + lane;
+    }
+#pragma unroll
+    for (int j = 0; j < 2; ++j) {
+        cv[j] = ct0 + j < nct;                                   // wave-uniform
+        w[j] = static_cast<const Bw*>(a.wp_hoist) + (size_t)(cv[j] ? ct0 + j : 0) * nkb * 64 + lane;
     }
     auto la = [&](int i, int kb) -> A {
         if constexpr (P::kBf16) {
@@ -526,28 +531,27 @@ __device__ __forceinline__ void hoist_job(const StepArgs& a, int b) {
             return ld4<false>(psi, (size_t)r[i] * 2 * a.M + kb * kTile + kq * 4, rv[i]);
         }
     };
-    f4 acc[2][2];
+    f4 acc[RT][2];
 #pragma unroll
-    for (int i = 0; i < 2; ++i)
+    for (int i = 0; i < RT; ++i)
 #pragma unroll
         for (int j = 0; j < 2; ++j) acc[i][j] = zero4();
     for (int kc = 0; kc < nkb; kc += KB) {
-        A av[KB][2];
+        A av[KB][RT];
         Bw bv[KB][2];
 #pragma unroll
         for (int u = 0; u < KB; ++u) {
             const int k = min(kc + u, nkb - 1);
 #pragma unroll
-            for (int i = 0; i < 2; ++i) {
-                av[u][i] = la(i, k);
-                bv[u][i] = w[i][(size_t)k * 64];
-            }
+            for (int i = 0; i < RT; ++i) av[u][i] = la(i, k);
+#pragma unroll
+            for (int j = 0; j < 2; ++j) bv[u][j] = w[j][(size_t)k * 64];
         }
 #pragma unroll
         for (int u = 0; u < KB; ++u)
             if (kc + u < nkb)
 #pragma unroll
-                for (int i = 0; i < 2; ++i)
+                for (int i = 0; i < RT; ++i)
 #pragma unroll
                     for (int j = 0; j < 2; ++j) acc[i][j] = P::mma(av[u][i], bv[u][j], acc[i][j]);
     }
@@ -558,7 +562,7 @@ __device__ __forceinline__ void hoist_job(const StepArgs& a, int b) {
         const int n = (ct0 + j) * kTile + (lane & 15);
         const float bias = a.b_hoist[n];
 #pragma unroll
-        for (int i = 0; i < 2; ++i)
+        for (int i = 0; i < RT; ++i)
 #pragma unroll
             for (int q = 0; q < 4; ++q) {
                 const int ro = (rt0 + i) * kTile + kq * 4 + q;

@@ -73,8 +73,8 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2))
     // old-tap context of step 0 (no old tap of step 0 lies in the grid, but
     // the general form keeps the loop uniform)
     {
-        const int nh = hoist_blocks(a);
-        for (int b = blockIdx.x; b < nh; b += G) hoist_job<P, true>(a, b);
+        const int nh = hoist_blocks<2>(a);
+        for (int b = blockIdx.x; b < nh; b += G) hoist_job<P, true, 2, P::kBf16 ? 6 : 8>(a, b);
         const StepRows s0 = step_rows(a.H, a.W, a.B, a.lambda, 0);
         const int nc = ctxo_blocks<P>(a, s0);
         // the last part adds the others, so it runs after them

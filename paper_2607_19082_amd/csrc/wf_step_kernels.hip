@@ -4,10 +4,12 @@
 
 namespace wf {
 
-// Pre-loop: the hyperprior half of layer 1 for every latent.
+// Pre-loop: the hyperprior half of layer 1 for every latent, four row tiles
+// per wave (every weight operand feeds four MFMA chains).
+constexpr int kHoistRt = 4;
 template <class P>
 __global__ __launch_bounds__(kThreads) void k_hoist(StepArgs a) {
-    hoist_job<P, false>(a, blockIdx.x);
+    hoist_job<P, false, kHoistRt, P::kBf16 ? 3 : 4>(a, blockIdx.x);
 }
 
 // Old-tap context jobs [j0, ...) of step s1 only (before the first step).
@@ -55,7 +57,7 @@ int enqueue_set_call(Plan& p, const CallPtrs& c, hipStream_t stream) {
 
 template <class P>
 static void launch_hoist(Plan& p, hipStream_t stream) {
-    hipLaunchKernelGGL(k_hoist<P>, dim3(hoist_blocks(p.args)), dim3(kThreads), 0, stream, p.args);
+    hipLaunchKernelGGL(k_hoist<P>, dim3(hoist_blocks<kHoistRt>(p.args)), dim3(kThreads), 0, stream, p.args);
 }
 
 int enqueue_hoist(Plan& p, hipStream_t stream) {
