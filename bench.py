@@ -211,13 +211,16 @@ def summarize_stats(stats_dir, log, out, command, l_floor_us=None):
              + (f"  The {leg_calls} traced decodes of the persistent driver (the bench's per-step latency leg) "
                 "are left out of this table." if leg_calls else ""), "",
              "| Kernel | Calls | Total (ms) | Average (us) | Min (us) | Max (us) | % |", "|---|---|---|---|---|---|---|"]
+    # shares of the kernels in the table (the left-out leg's time excluded)
+    total_ns = sum(float(r["TotalDurationNs"]) for r in rows)
     for r in rows:
-        if float(r["Percentage"]) < 0.05:
+        pct = 100.0 * float(r["TotalDurationNs"]) / total_ns
+        if pct < 0.05:
             continue
         name = r["Name"].split("(")[0].replace("void ", "")
         lines.append(f"| `{name}` | {r['Calls']} | {float(r['TotalDurationNs']) / 1e6:.2f} | "
                      f"{float(r['AverageNs']) / 1e3:.2f} | {float(r['MinNs']) / 1e3:.2f} | "
-                     f"{float(r['MaxNs']) / 1e3:.2f} | {float(r['Percentage']):.2f} |")
+                     f"{float(r['MaxNs']) / 1e3:.2f} | {pct:.2f} |")
     lines += ["", f"Decode kernels per call: {dec / max(calls, 1) / 1e6:.3f} ms of kernel time.  The same run's "
               f"HIP-event time of one decode (under the profiler) was {rec['roofline']['launch_ms_events']:.3f} ms; "
               f"bench line: {rec['ms_per_step']:.3f} ms per decode, {rec['value']:.0f} latents/s.  For the graph "
