@@ -344,7 +344,8 @@ __host__ __device__ __forceinline__ int ctxo_blocks(const StepArgs& a, const Ste
 // jobs are shared evenly among the phases as far as the slots left free in
 // the last round of each phase's own jobs allow (a.slots workgroups run at
 // once), then fill the remaining free slots; only what is left adds rounds,
-// spread evenly over the phases.  With fp32 the last part's jobs all run in
+// spread over the phases (phase A, whose own jobs are the longest, takes
+// three quarters of an even share).  With fp32 the last part's jobs all run in
 // the last phase, after the other parts, and add them in (see ctxo_job).
 // Cuts are multiples of 8, which keeps every job on the XCD its column tile
 // belongs to (nc and every phase's block count are multiples of 8).
@@ -394,7 +395,11 @@ __host__ __device__ __forceinline__ StepWork step_work(const StepArgs& a, const 
 #pragma unroll
     for (int ph = 0; ph < kMaxPhases; ++ph) {
         if (ph >= P::kFirst && ph < last) {
-            const int e = left < extra ? left : extra;
+            // layer 1's own jobs are the longest, so phase A takes three
+            // quarters of an even share and the phase before C the rest
+            int e = left < extra ? left : extra;
+            if (ph == PH_A) e = e * 3 / 4 / kXcds * kXcds;
+            if (ph == last - 1) e = left;
             take[ph] += e;
             left -= e;
         }
