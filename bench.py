@@ -335,10 +335,41 @@ def step_rows(cfg, group=1):
     return rows
 
 
-def cpu_baseline(name, rows, mask=None):
+def parity_record(got, ref, table, tol):
+    """Element-wise comparison of the timed decode's outputs with the oracle's
+    decode of the same latents: the largest absolute error per output, the
+    scale indices within 1e-4 relative of a table level (where the index is
+    excused and counted) and the index mismatches outside them."""
+    rec = {"bar_abs": tol}
+    errs = {}
+    for k in ("y_hat", "mean", "scale", "weight", "comp_mean"):
+        if k in got and k in ref and got[k] is not None:
+            g, r = np.asarray(got[k], np.float64), np.asarray(ref[k], np.float64)
+            errs[k] = float(np.abs(g - r).max()) if g.size else 0.0
+    rec["max_abs_err"] = errs
+    t = np.asarray(table, np.float64)[:-1]
+    s = np.asarray(ref["scale"], np.float64).reshape(-1)
+    near = np.zeros(s.shape, bool)
+    pos = np.searchsorted(t, s)
+    for off in (-1, 0):
+        q = np.clip(pos + off, 0, len(t) - 1)
+        near |= np.abs(s - t[q]) <= 1e-4 * t[q]
+    near &= s != np.float64(table[0])
+    mism = (np.asarray(got["idx"]).reshape(-1) != np.asarray(ref["idx"]).reshape(-1))
+    rec["idx_boundary_cases"] = int(near.sum())
+    rec["idx_mismatch_at_boundary"] = int((mism & near).sum())
+    rec["idx_mismatch_unexcused"] = int((mism & ~near).sum())
+    rec["within_bar"] = bool(all(v <= tol for v in errs.values()) and rec["idx_mismatch_unexcused"] == 0)
+    return rec
+
+
+def cpu_baseline(name, rows, mask=None, group=1, precision="fp32", got=None):
     """Time the CPU oracle decoding the top `rows` grid rows of the same
     workload (the causal taps point up and left, so this is an exact decode of
-    those latents)."""
+    those latents).  With `got` (the timed decode's outputs, host arrays) the
+    same oracle decode is also the parity reference of those rows; for bf16 the
+    oracle's bf16 mode is run as well (the parity reference) and the distance
+    to the fp32 oracle is reported beside it."""
     import oracle
     from paper_2607_19082_amd import inputs
     cfg, w, table, psi, sym = inputs.make_inputs(name)
@@ -346,9 +377,9 @@ def cpu_baseline(name, rows, mask=None):
         cfg["relaxed"] = mask == "relaxed"
         w = inputs.make_weights(cfg["M"], cfg["K"], radius=MASK_RADIUS[mask])
     psi, sym = psi[:, :rows].copy(), sym[:, :rows].copy()
-    m = oracle.Model(w, table, rows, cfg["W"], cfg["B"], cfg["K"], relaxed=cfg["relaxed"])
+    m = oracle.Model(w, table, rows, cfg["W"], cfg["B"], cfg["K"], relaxed=cfg["relaxed"], group=group)
     t0 = time.perf_counter()
-    m.decode(psi, sym)
+    ref = m.decode(psi, sym)
     dt = time.perf_counter() - t0
     n = cfg["B"] * rows * cfg["W"]
     cpu = platform.processor() or platform.machine()
@@ -360,11 +391,26 @@ def cpu_baseline(name, rows, mask=None):
                     break
     except OSError:
         pass
-    return {"value": n / dt, "unit": "latents/s", "cores": 1, "kind": "oracle",
-            "sample": f"sequential raster decode (fp64 accumulate) of the top {rows} grid rows "
-                      f"({n} latents) of {name}, one thread, {dt:.1f} s, on {cpu} "
-                      f"({os.cpu_count()} logical cpus)",
-            "ms_per_image_extrapolated": dt * 1e3 * (cfg["H"] / rows)}
+    rec = {"value": n / dt, "unit": "latents/s", "cores": 1, "kind": "oracle",
+           "sample": f"sequential raster decode (fp64 accumulate) of the top {rows} grid rows "
+                     f"({n} latents) of {name}, one thread, {dt:.1f} s, on {cpu} "
+                     f"({os.cpu_count()} logical cpus)",
+           "ms_per_image_extrapolated": dt * 1e3 * (cfg["H"] / rows)}
+    par = None
+    if got is not None:
+        top = {k: v[:, :rows] for k, v in got.items()}
+        if precision == "bf16":
+            mb = oracle.Model(w, table, rows, cfg["W"], cfg["B"], cfg["K"], relaxed=cfg["relaxed"], group=group,
+                              bf16=True)
+            par = parity_record(top, mb.decode(psi, sym), table, 1e-3)
+            par["reference"] = "the oracle's bf16 mode (bf16 weights, bf16-pair activations)"
+            par["max_abs_vs_fp32_oracle"] = parity_record(top, ref, table, 1e-2)["max_abs_err"]
+        else:
+            par = parity_record(top, ref, table, 1e-4)
+            par["reference"] = "the oracle (fp64 accumulation)"
+        par["latents"] = n
+        par["rows"] = f"top {rows} grid rows of the last timed decode"
+    return rec, par
 
 
 # bin edges of the per-step latency histograms, in multiples of L_floor
@@ -570,6 +616,8 @@ def main():
         rec_enc = {"ms_per_image": ewall * 1e3 / max(3, args.steps // 4) / cfg["B"],
                    "symbols_match_decode": bool(torch.equal(sym_o, sym_d))}
 
+    # the last timed decode's top grid rows, for the parity record of the CPU-baseline leg
+    got_host = {k: v[:, :args.cpu_rows].cpu().numpy() for k, v in out.items()} if args.cpu_rows > 0 else None
     node_us, bar_us = plan.measure_floor()
     plan.close()
     lfloor = min(x for x in (node_us, bar_us) if x > 0)
@@ -711,7 +759,8 @@ def main():
         "end_to_end": rec_e2e,
     }
     if args.cpu_rows > 0:
-        rec["cpu_baseline"] = cpu_baseline(args.workload, args.cpu_rows, args.mask)
+        rec["cpu_baseline"], rec["parity"] = cpu_baseline(args.workload, args.cpu_rows, args.mask, args.group,
+                                                          args.precision, got_host)
     print(json.dumps(rec), flush=True)
 
 

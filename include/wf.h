@@ -172,6 +172,12 @@ int wf_validate(const wf_desc *desc);
  * tile layouts on the device, the scale table, the workspace, and (for the
  * graph driver) the instantiated graph.  Synchronous; uses the current HIP
  * device.  On success *out owns all of it until wf_plan_destroy.
+ * The schedule is the linear rank of Sec. III-B (Eq. 5-7) with its step
+ * lists (the wavefronts of Sec. III-A, Eq. 4; Appendix A, Thm. 1); the
+ * weights are those of the masked-conv context model and the entropy-
+ * parameter network of Sec. II-B (Eq. 1).
+ * Errors: those of wf_validate; WF_E_NOMEM / WF_E_HIP when a device
+ * allocation or copy fails (nothing is left allocated).
  */
 int wf_plan(const wf_desc *desc, wf_plan_t *out);
 
@@ -181,9 +187,10 @@ int wf_plan(const wf_desc *desc, wf_plan_t *out);
 int wf_plan_schedule(wf_plan_t plan, int32_t *step_of, int32_t *n_steps);
 
 /*
- * Decode: for every step t = 0..T-1 and every latent on wavefront t, compute
- * the parameters from the already written y_hat and write
- * y_hat = (float)sym + mean.
+ * Decode (Sec. III-A, Eq. 2 evaluated in the wavefront order of Eq. 4; the
+ * per-step batched gather and products of Sec. III-C): for every step
+ * t = 0..T-1 and every latent on wavefront t, compute the parameters from the
+ * already written y_hat and write y_hat = (float)sym + mean (Sec. II-A).
  *   psi [B][H][W][2M] DEVICE fp32 hyperprior parameters
  *   sym [B][H][W][M]  DEVICE int32 symbols
  * Asynchronous on `stream`; one call in flight per plan (the plan's
@@ -193,8 +200,10 @@ int wf_decode(wf_plan_t plan, const float *psi, const int32_t *sym,
               const wf_out *out, hipStream_t stream);
 
 /*
- * Encode: as decode, but the symbol is sym_out = rint(y - mean) (fp32
- * subtract, round half to even) and y_hat = (float)sym_out + mean.
+ * Encode (the quantiser of Sec. II-A run in the same wavefront order, so the
+ * encoder sees exactly the context the decoder will): as decode, but the
+ * symbol is sym_out = rint(y - mean) (fp32 subtract, round half to even) and
+ * y_hat = (float)sym_out + mean.
  *   y       [B][H][W][M] DEVICE fp32 latents
  *   sym_out [B][H][W][M] DEVICE int32
  */

@@ -277,7 +277,9 @@ class Plan:
         p_o = self._check_tensor(offsets, (B * H * M + 1,), torch.int32, "offsets")
         p_s = self._check_tensor(sym_out, (B, H, W, M), torch.int32, "sym_out")
         o = self._out_struct(out)
-        n = bits.numel() if n_words is None else n_words
+        n = bits.numel() if n_words is None else int(n_words)
+        if not 0 <= n <= bits.numel():
+            raise ValueError(f"n_words must lie in [0, bits.numel()] = [0, {bits.numel()}], got {n}")
         _check(lib().wf_decode_bits(self._h, p_psi, p_b, n, p_o, p_s, ctypes.byref(o), _stream_handle(stream)))
         return out, sym_out
 

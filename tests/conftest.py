@@ -10,3 +10,10 @@ if ROOT not in sys.path:
 
 def pytest_configure(config):
     config.addinivalue_line("markers", "gpu: needs an MI355X (gfx950) GPU")
+
+
+def pytest_sessionfinish(session, exitstatus):
+    # oracle references still queued for tests that did not run are dropped
+    mod = sys.modules.get("oracle_refs")
+    if mod is not None:
+        mod.shutdown()

@@ -6,7 +6,14 @@ import oracle
 from paper_2607_19082_amd import inputs, wf
 
 FP32_TOL = 1e-4
-BF16_TOL = 1e-2
+# The bf16 variant is compared with the oracle's bf16 mode (bf16 weights,
+# activations as bf16 pairs).  The two evaluate the same function with
+# different summation orders and one extra pair rounding on the oracle's side
+# (its context vector), measured at about 1e-4; the bar is 1e-3, which a
+# single-rounded activation (a dropped lo half, ~1e-2) does not meet.  The
+# workload's own bf16 ceiling, 1e-2, is not used as a bar.
+BF16_TOL = 1e-3
+BF16_CEILING = 1e-2
 BOUNDARY_REL = 1e-4
 
 
@@ -64,10 +71,15 @@ def compare(gpu, ref, table, K, tol=FP32_TOL, keys=("y_hat", "mean", "scale", "w
     assert stats["idx_inconsistent_with_own_scale"] == 0, stats
     mism = gi != ri
     nb = near_boundary(table, ref["scale"])
-    if tol > FP32_TOL:
-        nb = nb | bracketed(table, gpu["scale"], ref["scale"])
     stats["idx_mismatch"] = int(mism.sum())
     stats["idx_boundary_cases"] = int(nb.sum())
+    stats["idx_mismatch_at_boundary"] = int((mism & nb).sum())
+    if tol > FP32_TOL:
+        # bf16: also excused where a level lies between the two scales (which
+        # agree to the float bar), counted on their own
+        br = bracketed(table, gpu["scale"], ref["scale"]) & ~nb
+        stats["idx_mismatch_bracketed"] = int((mism & br).sum())
+        nb = nb | br
     stats["idx_mismatch_unexcused"] = int((mism & ~nb).sum())
     if check_idx:
         assert stats["idx_mismatch_unexcused"] == 0, stats
@@ -118,13 +130,21 @@ def teacher_forced(cfg, gpu, psi, sym, model, lats, table, tol=FP32_TOL, check_i
     return stats
 
 
-def top_rows_check(cfg, w, table, psi, sym, got, rows, bf16=False, tol=FP32_TOL, check_idx=True):
+def top_rows_check(cfg, w, table, psi, sym, got, rows, bf16=False, tol=FP32_TOL, check_idx=True, ref=None):
     """The causal taps of a latent lie in its own row and the rows above, so
     the first `rows` grid rows of a full-size decode are exactly the decode
-    of those rows alone: the oracle decodes them from the seeded inputs and
-    every output there is compared element by element."""
-    sub = dict(cfg, H=rows)
-    ref = oracle.Model(w, table, rows, cfg["W"], cfg["B"], cfg["K"], relaxed=cfg["relaxed"],
-                       bf16=bf16).decode(psi[:, :rows].copy(), sym[:, :rows].copy())
+    of those rows alone: the oracle decodes them from the seeded inputs (or
+    `ref` is that decode, computed beforehand) and every output there is
+    compared element by element."""
+    if ref is None:
+        ref = oracle.Model(w, table, rows, cfg["W"], cfg["B"], cfg["K"], relaxed=cfg["relaxed"],
+                           bf16=bf16).decode(psi[:, :rows].copy(), sym[:, :rows].copy())
     part = {k: v[:, :rows] for k, v in got.items()}
-    return compare(part, ref, table, sub["K"], tol=tol, check_idx=check_idx)
+    stats = compare(part, ref, table, cfg["K"], tol=tol, check_idx=check_idx)
+    stats["rows_compared"] = rows
+    return stats
+
+
+def max_rows_per_step(H, W, lam):
+    """Latents on the widest wavefront t = lam*i + j of an H x W grid."""
+    return max(sum(1 for i in range(H) if 0 <= t - lam * i < W) for t in range(W + lam * (H - 1)))

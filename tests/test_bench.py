@@ -155,3 +155,29 @@ def test_stats_summary_leaves_out_the_persistent_leg(tmp_path):
     # (24 + 4) ms of phase and hoist kernels plus the set-call kernels over 4 calls
     assert "Decode kernels per call: 7.001 ms" in txt
     assert "L_floor = 1.50 us" in txt and "| steps | 0 | 0 | 1 | 1 | 0 | 0 | 0 | 0 |" in txt
+
+
+def test_parity_record():
+    import bench
+    rng = np.random.default_rng(0)
+    table = np.exp(np.linspace(np.log(0.11), np.log(256.0), 64)).astype(np.float32)
+    sc = rng.uniform(0.2, 50.0, size=(1, 3, 5, 1, 4)).astype(np.float32)
+    idx = np.searchsorted(table[:-1], sc, side="left").astype(np.int32)
+    ref = {"y_hat": rng.normal(size=(1, 3, 5, 4)), "mean": rng.normal(size=(1, 3, 5, 4)), "scale": sc, "idx": idx}
+    got = {k: v.copy() for k, v in ref.items()}
+    r = bench.parity_record(got, ref, table, 1e-4)
+    assert r["within_bar"] and r["idx_mismatch_unexcused"] == 0
+    assert all(v == 0.0 for v in r["max_abs_err"].values())
+    got["mean"] = got["mean"] + 2e-4
+    r = bench.parity_record(got, ref, table, 1e-4)
+    assert not r["within_bar"] and abs(r["max_abs_err"]["mean"] - 2e-4) < 1e-9
+    # an index flip at a scale sitting on a level is excused and counted
+    got = {k: v.copy() for k, v in ref.items()}
+    ref["scale"][0, 0, 0, 0, 0] = table[10]
+    ref["idx"][0, 0, 0, 0, 0] = 10
+    got["idx"][0, 0, 0, 0, 0] = 11
+    got["scale"][0, 0, 0, 0, 0] = table[10]
+    r = bench.parity_record(got, ref, table, 1e-4)
+    assert r["idx_mismatch_at_boundary"] == 1 and r["idx_mismatch_unexcused"] == 0 and r["within_bar"]
+    got["idx"][0, 1, 1, 0, 1] += 1
+    assert bench.parity_record(got, ref, table, 1e-4)["idx_mismatch_unexcused"] == 1

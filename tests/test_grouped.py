@@ -16,6 +16,13 @@ outside it:
 * fill = mean of the decoded taps: on a constant reconstruction the grouped
   context equals the exact one wherever some tap is decoded, and the
   zero-context one where none is;
+* the averaging itself, on a random reconstruction: the grouped context built
+  with numpy from its definition (dependence vectors, group status, per-channel
+  mean of the decoded in-image taps, zero when none), then fp64 matmuls, gives
+  the oracle's parameters at every latent, for K = 1 and 3, the 5x5 full and
+  relaxed, 3x3 and 7x7 masks and N = 2, 3, 4; mutants of the averaging set
+  (no right column, row -1 only, all in-image taps, the in-image count as the
+  denominator, zero fill) give different parameters;
 * one group holding every wavefront fills every tap with zero: the decode
   equals the exact decode of the same model with its conv weights zeroed;
 * encode/decode round trip with the same N.
@@ -183,3 +190,122 @@ def test_group_encode_roundtrip(N):
     enc, s = m.encode(psi, y)
     assert np.array_equal(s, sym)
     assert same(enc, dec)
+
+
+# ---------------------------------------------------------------------------
+# The fill on a non-constant reconstruction.  On a constant field every convex
+# combination of the decoded taps gives the same value, so the pin above fixes
+# which taps are known but not how they are averaged.  Here the grouped
+# context is built with numpy from a random reconstruction, straight from its
+# definition (Sec. III-D, Fig. 3(b)): the taps are the mask's dependence
+# vectors, a tap is decoded when its group floor((lambda i + j) / N) is earlier
+# than the latent's, a same-group tap is the per-channel mean of the decoded
+# in-image taps (zero when there is none), an out-of-image tap is zero.  The
+# layers after it are plain fp64 matmuls.  Each mutant of the averaging set
+# must give a different result, so a wrong set in the oracle would fail here.
+
+def _taps(R, relaxed):
+    return [(-di, -dj) for di, dj in S.dependence_vectors(2 * R + 1, relaxed)]
+
+
+def grouped_context(w, y_hat, R, relaxed, N, averaging="decoded"):
+    """ctx [B][H][W][2M] of the context-approximation decode, fp64.
+    `averaging` names the set the fill averages over: "decoded" (the
+    definition) or a mutant."""
+    B, H, W, M = y_hat.shape
+    lam = 2 if relaxed else R + 1
+    taps = _taps(R, relaxed)
+    cw = w["ctx_w"].astype(np.float64)
+    y = y_hat.astype(np.float64)
+    ctx = np.zeros((B, H, W, 2 * M))
+    for b in range(B):
+        for i in range(H):
+            for j in range(W):
+                g = S.group_of(i, j, lam, N)
+                inside = [(dy, dx) for dy, dx in taps if 0 <= i + dy < H and 0 <= j + dx < W]
+                known = [(dy, dx) for dy, dx in inside if S.group_of(i + dy, j + dx, lam, N) < g]
+                if averaging == "decoded":
+                    pool, den = known, len(known)
+                elif averaging == "no_right_column":
+                    right = max(dx for _, dx in taps)
+                    pool = [t for t in known if t[1] != right]
+                    den = len(pool)
+                elif averaging == "row_above_only":
+                    pool = [t for t in known if t[0] == -1]
+                    den = len(pool)
+                elif averaging == "all_inside":
+                    pool, den = inside, len(inside)
+                elif averaging == "inside_denominator":
+                    pool, den = known, len(inside)
+                elif averaging == "zero":
+                    pool, den = [], 0
+                else:
+                    raise ValueError(averaging)
+                fill = np.zeros(M)
+                if den:
+                    for dy, dx in pool:
+                        fill += y[b, i + dy, j + dx]
+                    fill /= den
+                acc = w["ctx_b"].astype(np.float64).copy()
+                for dy, dx in inside:
+                    x = y[b, i + dy, j + dx] if (dy, dx) in known else fill
+                    acc += cw[:, :, dy + R, dx + R] @ x
+                ctx[b, i, j] = acc
+    return ctx
+
+
+def params_from_context(w, table, ctx, psi, K, slope=0.01):
+    """The entropy-parameter network and the parameter epilogue, fp64 numpy."""
+    M = psi.shape[-1] // 2
+
+    def layer(h, wm, bv, act):
+        z = h @ wm.astype(np.float64).T + bv.astype(np.float64)
+        return np.where(z >= 0, z, slope * z) if act else z
+
+    h0 = np.concatenate([psi.astype(np.float64), ctx], axis=-1)
+    o = layer(layer(layer(h0, w["w1"], w["b1"], True), w["w2"], w["b2"], True), w["w3"], w["b3"], False)
+    if K == 1:
+        mu, sig = o[..., :M], o[..., M:2 * M][..., None, :]
+        wgt, cm = np.ones_like(sig), mu[..., None, :]
+    else:
+        sh = o.shape[:-1] + (3, M)
+        lg, cm, sig = (o[..., k * 3 * M:(k + 1) * 3 * M].reshape(sh) for k in range(3))
+        e = np.exp(lg - lg.max(axis=-2, keepdims=True))
+        wgt = e / e.sum(axis=-2, keepdims=True)
+        mu = (wgt * cm).sum(axis=-2)
+    sig = np.maximum(sig, np.float64(table[0]))
+    idx = np.searchsorted(table[:-1].astype(np.float64), sig, side="left")
+    return dict(mean=mu, scale=sig, idx=idx, weight=wgt, comp_mean=cm)
+
+
+@pytest.mark.parametrize("N", [2, 3, 4])
+@pytest.mark.parametrize("K,R,relaxed", [(1, 2, False), (3, 2, False), (1, 2, True), (1, 1, False),
+                                         (1, 3, False)])
+def test_fill_average_on_random_reconstruction(K, R, relaxed, N):
+    H, W, B, M = 7, 11, 2, 8
+    w = inputs.make_weights(M, K, seed=0, radius=R)
+    table = inputs.scale_table()
+    psi = inputs.make_psi(B, H, W, M, seed=1)
+    rng = np.random.default_rng(17)
+    y_hat = rng.normal(scale=3.0, size=(B, H, W, M)).astype(np.float32)
+    got = oracle.Model(w, table, H, W, B, K, relaxed=relaxed, group=N).eval(y_hat, psi)
+    ref = params_from_context(w, table, grouped_context(w, y_hat, R, relaxed, N), psi, K)
+    flat = {k: v.reshape((B * H * W,) + v.shape[3:]) for k, v in ref.items()}
+    for k in ("mean", "scale", "weight", "comp_mean"):
+        np.testing.assert_allclose(got[k], flat[k], rtol=0, atol=2e-5, err_msg=k)
+    near = np.zeros(got["scale"].shape, bool)
+    t = table[:-1].astype(np.float64)
+    for lvl in t:
+        near |= np.abs(got["scale"].astype(np.float64) - lvl) <= 1e-5 * lvl
+    assert np.array_equal(got["idx"][~near], flat["idx"][~near])
+    # the definition is not satisfied by a different averaging set
+    for mutant in ("no_right_column", "row_above_only", "all_inside", "inside_denominator", "zero"):
+        if mutant in ("no_right_column", "row_above_only") and R == 1:
+            # these two mutants drop only a one-step-old tap of the 3x3 mask
+            # ((-1, +1), resp. (0, -1)); when such a tap is decoded every tap
+            # is and nothing is filled, so they provably coincide with the
+            # definition there
+            continue
+        bad = params_from_context(w, table, grouped_context(w, y_hat, R, relaxed, N, mutant), psi, K)
+        diff = np.abs(bad["mean"].reshape(got["mean"].shape) - got["mean"]).max()
+        assert diff > 1e-3, (mutant, diff)

@@ -321,3 +321,57 @@ def test_teacher_forced_eval_matches_run():
     for k in ("mean", "scale", "idx", "weight", "comp_mean"):
         flat = out[k].reshape((H * W,) + out[k].shape[3:])
         assert np.array_equal(ev[k], flat[lats]), k
+
+
+# ---------------------------------------------------------------------------
+# The power of the bf16 parity bar.  The GPU's bf16 variant is compared with
+# the oracle's bf16 mode to 1e-3 absolute.  A copy of the oracle with one
+# planted mistake -- every activation rounded to a single bf16 value, i.e. the
+# lo half of each pair dropped -- must miss that bar, so a kernel that dropped
+# the lo halves could not pass it.
+
+def _planted_oracle(tmp_path, old, new, tag):
+    import ctypes
+    import shutil
+    import subprocess
+    tmp_path = tmp_path / tag   # one directory (and library path) per copy
+    tmp_path.mkdir()
+    here = os.path.dirname(oracle.__file__)
+    src = open(os.path.join(here, "wf_oracle.c")).read()
+    assert src.count(old) == 1
+    (tmp_path / "wf_oracle.c").write_text(src.replace(old, new))
+    for f in ("wf_rans.c", "wf_rans.h"):
+        shutil.copy(os.path.join(here, f), tmp_path / f)
+    so = str(tmp_path / "libplanted.so")
+    subprocess.run(["gcc", "-O2", "-std=c11", "-fPIC", "-shared", "-fno-fast-math", "-ffp-contract=off",
+                    "-o", so, str(tmp_path / "wf_oracle.c"), str(tmp_path / "wf_rans.c"), "-lm"], check=True)
+    lib = ctypes.CDLL(so)
+    lib.oracle_run.argtypes = [ctypes.POINTER(oracle._Model), ctypes.c_void_p, ctypes.c_void_p,
+                               ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int64, ctypes.POINTER(oracle._Out)]
+    lib.oracle_run.restype = ctypes.c_int
+
+    def decode(m, psi, sym):
+        import ctypes as C
+        psi = np.ascontiguousarray(psi, np.float32)
+        sym = np.ascontiguousarray(sym, np.int32).copy()
+        n = m.B * m.H * m.W
+        outs, c = m._alloc(n)
+        assert lib.oracle_run(C.byref(m._m), psi.ctypes.data, sym.ctypes.data, None, None, n, C.byref(c)) == 0
+        return m._shape(outs)
+    return decode
+
+
+@pytest.mark.parametrize("name,H,W", [("minnen-hr-4k-240x135-m320", 3, 10), ("cheng-gmm3-1080p-120x68-m192", 4, 10)])
+def test_bf16_bar_rejects_single_rounded_activations(tmp_path, name, H, W):
+    bar = 1e-3   # the GPU bf16 bar against the oracle's bf16 mode
+    cfg, w, table, psi, sym = inputs.make_inputs(name, H=H, W=W)
+    m = oracle.Model(w, table, H, W, 1, cfg["K"], bf16=True)
+    pair = m.decode(psi, sym)
+    single = _planted_oracle(tmp_path, "    return (double)hi + (double)lo;", "    (void)lo;\n    return (double)hi;",
+                             "single")(m, psi, sym)
+    err = max(float(np.abs(single[k].astype(np.float64) - pair[k]).max()) for k in ("mean", "scale"))
+    assert err > 10 * bar, err
+    # the unmodified copy reproduces the oracle bit for bit
+    same_copy = _planted_oracle(tmp_path, "    return (double)hi + (double)lo;", "    return (double)hi + (double)lo;",
+                                "copy")(m, psi, sym)
+    assert all(np.array_equal(same_copy[k], pair[k]) for k in pair)

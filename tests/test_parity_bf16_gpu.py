@@ -3,12 +3,17 @@ hi+lo pairs, every product on bf16 MFMA with fp32 accumulation) against the
 oracle's matching bf16 mode on the same seeded inputs.
 
 Bars, as for fp32 but with the bf16 tolerance: means, scales and y_hat within
-1e-2 absolute of the bf16 oracle's whole decode (and encode); encode symbols
-bit-exact; scale indices identical except scales within 1e-4 relative of a
-table level (counted).  At the full 3840x2160 size the oracle decodes the top
-grid rows (an exact sub-decode) and its per-latent function is evaluated on
-the GPU's own reconstruction at sampled latents.  The distance to the fp32
-oracle (the effect of bf16 weights, not of the kernels) is logged.
+1e-3 absolute of the bf16 oracle's whole decode (and encode); the two evaluate
+the same bf16 function in different summation orders, measured ~1e-4 apart,
+and a single-rounded activation misses this bar by an order of magnitude
+(tests/test_oracle.py).  Encode symbols bit-exact; scale indices identical
+except scales within 1e-4 relative of a table level, and, counted apart,
+where a level lies between the GPU's and the oracle's scales.  The wide grids
+(40 x 120) put three row tiles on a wavefront; at the full 3840x2160 size the
+oracle decodes the top 33 grid rows (an exact sub-decode, three row tiles of
+the widest steps) and its per-latent function is evaluated on the GPU's own
+reconstruction at sampled latents.  The distance to the fp32 oracle (the
+effect of the bf16 weights, not of the kernels) is logged beside it.
 """
 import sys
 
@@ -17,12 +22,21 @@ import pytest
 
 from paper_2607_19082_amd import inputs, wf
 
-from gpu_helpers import (BF16_TOL, compare, gpu_plan, make_case, oracle_model, sample_latents,
-                         teacher_forced, to_np, top_rows_check)
+import oracle_refs
+from gpu_helpers import (BF16_TOL, compare, gpu_plan, make_case, max_rows_per_step, oracle_model,
+                         sample_latents, teacher_forced, to_np, top_rows_check)
 
 pytestmark = pytest.mark.gpu
 
 torch = pytest.importorskip("torch")
+
+WIDE = [("cheng-gmm3-1080p-120x68-m192", 40, 120), ("minnen-hr-4k-240x135-m320", 40, 120)]
+ROWS_4K = 33
+
+if torch.cuda.is_available():
+    oracle_refs.prefetch([("minnen-hr-4k-240x135-m320", None, None, None, ROWS_4K, True)]
+                         + [(n, H, W, None, None, True) for n, H, W in WIDE]
+                         + [(n, H, W, None, None, False) for n, H, W in WIDE])
 
 
 @pytest.fixture(scope="module", autouse=True)
@@ -57,8 +71,9 @@ def encode(cfg, w, table, psi, y, driver):
     return res, s
 
 
-def vs_fp32(cfg, w, table, psi, sym, got):
-    ref = oracle_model(cfg, w, table).decode(psi, sym)
+def vs_fp32(cfg, w, table, psi, sym, got, ref=None):
+    if ref is None:
+        ref = oracle_model(cfg, w, table).decode(psi, sym)
     return {k: float(np.abs(got[k].astype(np.float64) - ref[k]).max()) for k in ("y_hat", "mean", "scale")}
 
 
@@ -103,6 +118,25 @@ def test_bf16_reduced_global(name, H, W, B, driver):
 
 
 @pytest.mark.parametrize("driver", ["graph", "persistent", "dataflow"])
+@pytest.mark.parametrize("name,H,W", WIDE)
+def test_bf16_wide_global(name, H, W, driver):
+    log(f"bf16 case {name} wide H={H} W={W} driver={driver}")
+    cfg, w, table, psi, sym = make_case(name, H=H, W=W)
+    assert max_rows_per_step(H, W, 3) == 40
+    got = decode(cfg, w, table, psi, sym, driver)
+    ref = oracle_refs.ref_decode(name, H, W, bf16=True).result()
+    log(compare(got, ref, table, cfg["K"], tol=BF16_TOL))
+    ref32 = oracle_refs.ref_decode(name, H, W).result()
+    log({"max_abs_vs_fp32_oracle": vs_fp32(cfg, w, table, psi, sym, got, ref32)})
+    if driver == "graph":
+        u = inputs.make_noise(cfg["B"], cfg["H"], cfg["W"], cfg["M"])
+        y = inputs.encoder_input(sym, u, ref["mean"])
+        got_e, s = encode(cfg, w, table, psi, y, driver)
+        assert np.array_equal(s, sym)
+        log(compare(got_e, ref, table, cfg["K"], tol=BF16_TOL))
+
+
+@pytest.mark.parametrize("driver", ["graph", "persistent", "dataflow"])
 def test_bf16_4k_full_size(driver):
     # the 3840x2160 workload (240x135 latents, M = 320) at its full size: the
     # top rows against the bf16 oracle's decode of them, teacher-forced
@@ -111,7 +145,8 @@ def test_bf16_4k_full_size(driver):
     log(f"bf16 case {name} full size driver={driver}")
     cfg, w, table, psi, sym = make_case(name)
     got = decode(cfg, w, table, psi, sym, driver)
-    log(top_rows_check(cfg, w, table, psi, sym, got, 4, bf16=True, tol=BF16_TOL))
+    ref = oracle_refs.ref_decode(name, rows=ROWS_4K, bf16=True).result()
+    log(top_rows_check(cfg, w, table, psi, sym, got, ROWS_4K, bf16=True, tol=BF16_TOL, ref=ref))
     model = oracle_model(cfg, w, table, bf16=True)
     log(teacher_forced(cfg, got, psi, sym, model, sample_latents(cfg, 300), table, tol=BF16_TOL))
     u = inputs.make_noise(cfg["B"], cfg["H"], cfg["W"], cfg["M"])

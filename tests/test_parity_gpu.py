@@ -2,10 +2,15 @@
 same seeded inputs.
 
 Global parity compares every output of a whole decode (and encode) with the
-oracle's sequential raster decode.  At the full workload sizes, where the
-oracle's whole decode is too slow for a test, the oracle's per-latent function
-is evaluated on the GPU's own final reconstruction at sampled latents
-(teacher-forced), which also catches any tap read before it was written.
+oracle's sequential raster decode.  The "wide" grids (40 x 120 latents) put 40
+latents on a wavefront, three 16-row tiles, at K = 3 and at M = 320.  At the
+full workload sizes the oracle decodes the top grid rows (an exact
+sub-decode: every tap lies in the latent's row or above); for the 4K workload
+65 rows, so that all five row tiles of its widest steps are compared element
+by element.  In addition the oracle's per-latent function is evaluated on the
+GPU's own final reconstruction at sampled latents (teacher-forced), which also
+catches any tap read before it was written.  The oracle references are
+computed on host threads while the GPU tests run (oracle_refs).
 Bars: 1e-4 absolute on floats; symbols bit-exact; scale indices identical
 except scales within 1e-4 relative of a table level (counted).
 """
@@ -16,12 +21,26 @@ import pytest
 
 from paper_2607_19082_amd import inputs, wf
 
-from gpu_helpers import (compare, gpu_plan, make_case, oracle_model, sample_latents,
+import oracle_refs
+from gpu_helpers import (compare, gpu_plan, make_case, max_rows_per_step, oracle_model, sample_latents,
                          teacher_forced, to_np, top_rows_check)
 
 pytestmark = pytest.mark.gpu
 
 torch = pytest.importorskip("torch")
+
+WIDE = [
+    # (workload, H, W): 40 latents per wavefront, three 16-row tiles per step
+    ("cheng-gmm3-1080p-120x68-m192", 40, 120),
+    ("minnen-hr-4k-240x135-m320", 40, 120),
+]
+TOP_ROWS = {"cheng-gmm3-1080p-120x68-m192": 20, "minnen-relaxed-b8-120x68-m192": 3,
+            "minnen-hr-4k-240x135-m320": 65}
+
+if torch.cuda.is_available():
+    oracle_refs.prefetch([("minnen-hr-4k-240x135-m320", None, None, None, 65, False)]
+                         + [(n, H, W, None, None, False) for n, H, W in WIDE]
+                         + [(n, None, None, None, r, False) for n, r in TOP_ROWS.items()])
 
 
 @pytest.fixture(scope="module", autouse=True)
@@ -59,7 +78,8 @@ def run_encode(cfg, w, table, psi, y, driver="stream", precision="fp32"):
 
 
 SMALL = [
-    # (workload, H, W, B): ragged grids that span several 16-row tiles
+    # (workload, H, W, B): ragged grids, at most 16 latents per wavefront
+    # (one row tile; the wide cases below span three)
     ("minnen-16x16-m192", 7, 9, 1),
     ("minnen-16x16-m192", 5, 3, 2),
     ("cheng-gmm3-1080p-120x68-m192", 6, 11, 1),
@@ -117,17 +137,37 @@ def test_reduced_global(name, H, W, B, driver):
     log(compare(got, ref, table, cfg["K"]))
 
 
-@pytest.mark.parametrize("name,n,rows", [
-    ("cheng-gmm3-1080p-120x68-m192", 600, 6),
-    ("minnen-relaxed-b8-120x68-m192", 600, 3),
-    ("minnen-hr-4k-240x135-m320", 300, 5),
+@pytest.mark.parametrize("name,H,W", WIDE)
+@pytest.mark.parametrize("driver", ["graph", "persistent", "dataflow"])
+def test_wide_global(name, H, W, driver):
+    # every output of a decode whose wavefronts span three row tiles
+    log(f"case {name} wide H={H} W={W} driver={driver}")
+    cfg, w, table, psi, sym = make_case(name, H=H, W=W)
+    assert max_rows_per_step(H, W, 3) == 40
+    got = run_decode(cfg, w, table, psi, sym, driver)
+    ref = oracle_refs.ref_decode(name, H, W).result()
+    log(compare(got, ref, table, cfg["K"]))
+    if driver == "graph":
+        u = inputs.make_noise(cfg["B"], cfg["H"], cfg["W"], cfg["M"])
+        y = inputs.encoder_input(sym, u, ref["mean"])
+        got_e, s = run_encode(cfg, w, table, psi, y, driver)
+        assert np.array_equal(s, sym)
+        log(compare(got_e, ref, table, cfg["K"]))
+
+
+@pytest.mark.parametrize("name,n", [
+    ("cheng-gmm3-1080p-120x68-m192", 600),
+    ("minnen-relaxed-b8-120x68-m192", 600),
+    ("minnen-hr-4k-240x135-m320", 300),
 ])
 @pytest.mark.parametrize("driver", ["graph", "persistent", "dataflow"])
-def test_full_size_teacher_forced(name, n, rows, driver):
+def test_full_size_teacher_forced(name, n, driver):
+    rows = TOP_ROWS[name]
     log(f"case {name} full size, top {rows} rows + teacher-forced sample of {n}, driver={driver}")
     cfg, w, table, psi, sym = make_case(name)
     got = run_decode(cfg, w, table, psi, sym, driver)
-    log(top_rows_check(cfg, w, table, psi, sym, got, rows))
+    ref = oracle_refs.ref_decode(name, rows=rows).result()
+    log(top_rows_check(cfg, w, table, psi, sym, got, rows, ref=ref))
     model = oracle_model(cfg, w, table)
     lats = sample_latents(cfg, n)
     log(teacher_forced(cfg, got, psi, sym, model, lats, table))
