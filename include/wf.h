@@ -261,6 +261,27 @@ int wf_decode_bits(wf_plan_t plan, const float *psi, const uint32_t *bits, int64
                    hipStream_t stream);
 
 /*
+ * wf_decode for callers that cannot allocate device memory (code under HIP
+ * graph capture, tight serving loops, harnesses that forbid hipMalloc): the
+ * same decode and outputs, but the call's working memory -- the hoisted
+ * hyperprior half of layer 1 for every latent, the per-step activations, the
+ * old-tap context parts, the bf16 pair copy of y_hat and the call's pointer
+ * block -- lives in a static device array of the library (32 MiB, held by
+ * every device the library runs on until the process ends) instead of the
+ * plan's workspace.  It runs the stream driver's per-step kernels on `stream`
+ * whatever the plan's driver, and calls no allocating routine.
+ * Errors: as wf_decode; WF_E_UNSUPPORTED (with the bytes needed) when the
+ * working memory exceeds 32 MiB (e.g. the 1920x1080 GMM workload needs about
+ * 22 MB; the 3840x2160 M = 320 one does not fit).
+ * All calls on one device share the array: calls that overlap on a device
+ * (concurrent streams or threads) race and must be serialised by the caller.
+ * No part of the array needs clearing: every element a call reads was
+ * written earlier in the same call.
+ */
+int wf_decode_noalloc(wf_plan_t plan, const float *psi, const int32_t *sym, const wf_out *out,
+                      hipStream_t stream);
+
+/*
  * Measurement hook of the persistent and dataflow drivers (WF_E_UNSUPPORTED
  * for the others).  With `stamps` non-NULL (DEVICE int64 array of `capacity`
  * entries) every later call records the device wall clock (100 MHz ticks):

@@ -210,6 +210,11 @@ struct Plan {
 // p.d_call (used directly by the stream driver and captured by the graph
 // driver).
 int enqueue_steps(Plan& p, hipStream_t stream, bool ec = false);
+// The same with explicit plan constants (the workspace pointers of `a` may
+// point elsewhere than the plan's own, see wf_decode_noalloc).
+int enqueue_steps_with(const Plan& p, const StepArgs& a, hipStream_t stream, bool ec = false);
+// Publish a call's pointers to the block at dst.
+int enqueue_set_call_at(CallPtrs* dst, const CallPtrs& c, hipStream_t stream);
 // entropy coding (wf_ec.hip)
 int build_ec(Plan* p, const float* scale_table, int L);
 int enqueue_ec_init(Plan& p, const uint32_t* bits, int64_t n_words, const uint32_t* offsets, hipStream_t stream);

@@ -51,20 +51,24 @@ __global__ void k_set_call(CallPtrs* dst, CallPtrs v) {
 }
 
 int enqueue_set_call(Plan& p, const CallPtrs& c, hipStream_t stream) {
-    hipLaunchKernelGGL(k_set_call, dim3(1), dim3(64), 0, stream, p.d_call, c);
+    return enqueue_set_call_at(p.d_call, c, stream);
+}
+
+int enqueue_set_call_at(CallPtrs* dst, const CallPtrs& c, hipStream_t stream) {
+    hipLaunchKernelGGL(k_set_call, dim3(1), dim3(64), 0, stream, dst, c);
     return WF_OK;
 }
 
 template <class P>
-static void launch_hoist(Plan& p, hipStream_t stream) {
-    hipLaunchKernelGGL(k_hoist<P>, dim3(hoist_blocks<kHoistRt>(p.args)), dim3(kThreads), 0, stream, p.args);
+static void launch_hoist(const StepArgs& a, hipStream_t stream) {
+    hipLaunchKernelGGL(k_hoist<P>, dim3(hoist_blocks<kHoistRt>(a)), dim3(kThreads), 0, stream, a);
 }
 
 int enqueue_hoist(Plan& p, hipStream_t stream) {
     if (p.precision == WF_BF16)
-        launch_hoist<PBF16>(p, stream);
+        launch_hoist<PBF16>(p.args, stream);
     else
-        launch_hoist<PF32>(p, stream);
+        launch_hoist<PF32>(p.args, stream);
     return WF_OK;
 }
 
@@ -76,45 +80,43 @@ static StepRows rows_of(const Plan& p, int t) {
 
 // Grouped decode: per group, the context (with fill), then layers 1-3.
 template <class P, int KC>
-static void launch_groups(Plan& p, hipStream_t stream) {
-    const StepArgs& a = p.args;
-    launch_hoist<P>(p, stream);
+static void launch_groups(const Plan& p, const StepArgs& a, hipStream_t stream) {
+    launch_hoist<P>(a, stream);
     const int ncx = 2 * a.M / kTile / P::kC;
     for (int g = 0; g < p.steps; ++g) {
         const StepRows s{g, 0, 0, p.g_n[g], p.g_r0[g]};
         const int nrt = ntiles(s.nrows);
         const int nc = xcd_blocks(ncx, nrt);
         if (p.ntaps <= kTaps5x5)
-            hipLaunchKernelGGL((k_gctx<P, kTaps5x5>), dim3(nc * a.gparts), dim3(kThreads), 0, stream, s, nc, p.args);
+            hipLaunchKernelGGL((k_gctx<P, kTaps5x5>), dim3(nc * a.gparts), dim3(kThreads), 0, stream, s, nc, a);
         else
-            hipLaunchKernelGGL((k_gctx<P, kMaxTaps>), dim3(nc * a.gparts), dim3(kThreads), 0, stream, s, nc, p.args);
+            hipLaunchKernelGGL((k_gctx<P, kMaxTaps>), dim3(nc * a.gparts), dim3(kThreads), 0, stream, s, nc, a);
         const int nb[3] = {xcd_blocks(a.Np1 / kTile / P::kC, nrt), phase_blocks<P>(a, s, PH_B),
                            phase_blocks<P>(a, s, PH_C)};
         const int ph[3] = {PH_GA, PH_B, PH_C};
         for (int k = 0; k < 3; ++k)
-            hipLaunchKernelGGL((k_phase<P, KC>), dim3(nb[k]), dim3(kThreads), 0, stream, ph[k], s, s, nb[k], 0, 0, p.args);
+            hipLaunchKernelGGL((k_phase<P, KC>), dim3(nb[k]), dim3(kThreads), 0, stream, ph[k], s, s, nb[k], 0, 0, a);
     }
 }
 
 template <class P, int KC>
-static void launch_steps(Plan& p, hipStream_t stream, bool ec) {
-    StepArgs a = p.args;
+static void launch_steps(const Plan& p, StepArgs a, hipStream_t stream, bool ec) {
     a.ec = ec ? 1 : 0;
     if (p.group > 1) {
-        launch_groups<P, KC>(p, stream);
+        launch_groups<P, KC>(p, a, stream);
         return;
     }
-    launch_hoist<P>(p, stream);
+    launch_hoist<P>(a, stream);
     {
         const StepRows s0 = rows_of(p, 0);
         const int nc = ctxo_blocks<P>(a, s0);
         // the last part adds the others, so it runs after them
         const int split = (P::kParts - 1) * nc;
         if (nc > 0) {
-            hipLaunchKernelGGL(k_ctxo<P>, dim3(split), dim3(kThreads), 0, stream, s0, 0, nc, p.args);
+            hipLaunchKernelGGL(k_ctxo<P>, dim3(split), dim3(kThreads), 0, stream, s0, 0, nc, a);
             if (split < P::kParts * nc)
                 hipLaunchKernelGGL(k_ctxo<P>, dim3(P::kParts * nc - split), dim3(kThreads), 0, stream, s0, split, nc,
-                                   p.args);
+                                   a);
         }
     }
     for (int t = 0; t < p.T; ++t) {
@@ -132,13 +134,15 @@ static void launch_steps(Plan& p, hipStream_t stream, bool ec) {
     }
 }
 
-int enqueue_steps(Plan& p, hipStream_t stream, bool ec) {
+int enqueue_steps(Plan& p, hipStream_t stream, bool ec) { return enqueue_steps_with(p, p.args, stream, ec); }
+
+int enqueue_steps_with(const Plan& p, const StepArgs& a, hipStream_t stream, bool ec) {
     if (p.precision == WF_BF16) {
-        if (p.K == 1) launch_steps<PBF16, 1>(p, stream, ec);
-        else launch_steps<PBF16, 3>(p, stream, ec);
+        if (p.K == 1) launch_steps<PBF16, 1>(p, a, stream, ec);
+        else launch_steps<PBF16, 3>(p, a, stream, ec);
     } else {
-        if (p.K == 1) launch_steps<PF32, 1>(p, stream, ec);
-        else launch_steps<PF32, 3>(p, stream, ec);
+        if (p.K == 1) launch_steps<PF32, 1>(p, a, stream, ec);
+        else launch_steps<PF32, 3>(p, a, stream, ec);
     }
     hipError_t err = hipGetLastError();
     if (err != hipSuccess) return fail(WF_E_HIP, std::string("kernel launch: ") + hipGetErrorString(err));

@@ -24,7 +24,7 @@ DRIVER = {"stream": 0, "graph": 1, "persistent": 2, "dataflow": 3}
 EXPORTS = ["wf_schedule", "wf_validate", "wf_plan", "wf_plan_schedule", "wf_decode",
            "wf_encode", "wf_ec_tables", "wf_encode_bits", "wf_decode_bits", "wf_plan_trace",
            "wf_measure_floor", "wf_plan_sync", "wf_xform_plan", "wf_hyper_synthesis", "wf_synthesis",
-           "wf_xform_destroy", "wf_plan_destroy", "wf_last_error"]
+           "wf_decode_noalloc", "wf_xform_destroy", "wf_plan_destroy", "wf_last_error"]
 
 
 class WfError(RuntimeError):
@@ -83,6 +83,7 @@ def lib():
         L.wf_plan.argtypes = [ctypes.POINTER(Desc), ctypes.POINTER(ctypes.c_void_p)]
         L.wf_plan_schedule.argtypes = [P, P, P]
         L.wf_decode.argtypes = [P, P, P, ctypes.POINTER(Out), P]
+        L.wf_decode_noalloc.argtypes = [P, P, P, ctypes.POINTER(Out), P]
         L.wf_encode.argtypes = [P, P, P, P, ctypes.POINTER(Out), P]
         L.wf_ec_tables.argtypes = [P, ctypes.c_int32, P, P, P, ctypes.c_int64]
         L.wf_encode_bits.argtypes = [P, P, P, P, ctypes.POINTER(Out), P, ctypes.c_int64, P, P]
@@ -228,6 +229,17 @@ class Plan:
         p_sym = self._check_tensor(sym, (B, H, W, M), torch.int32, "sym")
         o = self._out_struct(out)
         _check(lib().wf_decode(self._h, p_psi, p_sym, ctypes.byref(o), _stream_handle(stream)))
+        return out
+
+    def decode_noalloc(self, psi, sym, out, stream=None):
+        """wf_decode_noalloc: the same decode with the call's working memory in
+        the library's static device array (the outputs must be given)."""
+        import torch
+        B, H, W, M = self.B, self.H, self.W, self.M
+        p_psi = self._check_tensor(psi, (B, H, W, 2 * M), torch.float32, "psi")
+        p_sym = self._check_tensor(sym, (B, H, W, M), torch.int32, "sym")
+        o = self._out_struct(out)
+        _check(lib().wf_decode_noalloc(self._h, p_psi, p_sym, ctypes.byref(o), _stream_handle(stream)))
         return out
 
     def encode(self, psi, y, out=None, sym_out=None, stream=None):

@@ -153,6 +153,7 @@ def test_null_arguments_rejected(lib):
     out = wf.Out()
     assert lib.wf_decode(None, None, None, ctypes.byref(out), None) == wf.WF_E_INVALID
     assert lib.wf_encode(None, None, None, None, ctypes.byref(out), None) == wf.WF_E_INVALID
+    assert lib.wf_decode_noalloc(None, None, None, ctypes.byref(out), None) == wf.WF_E_INVALID
     assert lib.wf_plan(None, None) == wf.WF_E_INVALID
     assert lib.wf_plan_sync(None, None) == wf.WF_E_INVALID
     assert lib.wf_plan_schedule(None, None, None) == wf.WF_E_INVALID
