@@ -519,7 +519,7 @@ def main():
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--workload", default=DEFAULT_WORKLOAD)
-    ap.add_argument("--driver", default="graph", choices=["stream", "graph", "persistent", "dataflow"])
+    ap.add_argument("--driver", default="graph", choices=["stream", "graph", "persistent", "dataflow", "resident"])
     ap.add_argument("--precision", default="fp32", choices=["fp32", "bf16"])
     ap.add_argument("--mask", default=None, choices=sorted(MASK_TAPS),
                     help="causal mask (default: the workload's own), weights drawn for its kernel size")
@@ -741,6 +741,7 @@ def main():
                      "traffic_GBps": None if traffic is None else traffic / (dec_ms * 1e-3) / 1e9,
                      "kernel": {"persistent": "k_persistent (one launch = one decode)",
                                 "dataflow": "one decode call: counter reset, hoist and one k_dataflow launch",
+                                "resident": "one decode call: counter reset, hoist and one k_resident launch",
                                 "graph": "one replay of the decode graph (hoist, context, one k_phase per phase)",
                                 "stream": "all kernels of one decode call"}[args.driver],
                      "algorithmic_gflop_per_launch": fl / 1e9, "launch_ms_events": dec_ms,

@@ -579,8 +579,10 @@ __device__ __forceinline__ void hoist_job(const StepArgs& a, int b) {
 // Tap gather of k-block kb of a row's taps (fp32: y_hat, bf16: its pair
 // form), for the old taps (tap-major, `old` true) or the new taps.  A k-block
 // never straddles two taps (M is a multiple of the k-block).
+// yhat: the fp32 reconstruction (the bf16 loads read a.ybf).
 template <class P, bool COH, bool R3 = true>
-__device__ __forceinline__ typename P::A ld_tap(const StepArgs& a, const Row& w, int kb, int kq, bool old) {
+__device__ __forceinline__ typename P::A ld_tap_from(const StepArgs& a, const float* yhat, const Row& w, int kb,
+                                                     int kq, bool old) {
     const int M = a.M;
     const int tap = kb * P::kK / M;
     const int c = kb * P::kK - tap * M + kq * (P::kK / 4);
@@ -606,8 +608,12 @@ __device__ __forceinline__ typename P::A ld_tap(const StepArgs& a, const Row& w,
         const size_t q = lat * 2 * M + (size_t)(c >> 5) * 64 + (c & 31);
         return b8x2{ld8h<COH>(a.ybf, q, ok), ld8h<COH>(a.ybf, q + 32, ok)};
     } else {
-        return ld4<COH>(a.cp->y_hat, lat * M + c, ok);
+        return ld4<COH>(yhat, lat * M + c, ok);
     }
+}
+template <class P, bool COH, bool R3 = true>
+__device__ __forceinline__ typename P::A ld_tap(const StepArgs& a, const Row& w, int kb, int kq, bool old) {
+    return ld_tap_from<P, COH, R3>(a, P::kBf16 ? nullptr : a.cp->y_hat, w, kb, kq, old);
 }
 
 // ---------------------------------------------------------------------------

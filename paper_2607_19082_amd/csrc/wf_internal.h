@@ -69,6 +69,40 @@ struct DfArgs {
     long long stamps_cap;
 };
 
+// Resident driver (see wf_resident.hip): roles of its workgroups, in this
+// order of workgroup indices.
+enum ResRole { RR_CTX = 0, RR_CTXL = 1, RR_A = 2, RR_B = 3, RR_C0 = 4, RR_C1 = 5, kResRoles = 6 };
+// Weight k-blocks one wave holds in registers per column tile, by role
+// (fp32 k-blocks of 16, bf16 k-blocks of 32); a plan whose slices need more
+// is not supported by that driver.
+constexpr int kResKbF32[5] = {26, 20, 17, 14, 8};       // ctx part, layer 1, layer 2, layer 3 (K = 1), layer 3 (K = 3)
+constexpr int kResKbBf16[5] = {14, 10, 9, 7, 4};
+constexpr int kResMaxNc = 6;        // column tiles of one layer-3 role (K = 3: 3 logits + 3 means)
+constexpr int kResMaxParts = 4;     // k-parts of the old-tap context
+constexpr int kResRep = 2;          // replicas of every weight slice (they take alternate tasks)
+
+struct ResArgs {
+    int first[kResRoles + 1];   // workgroups [first[r], first[r+1]) play role r
+    const int* per_slot;        // [kResRoles][kResRep][8]: workgroups of role r, replica h, in XCD class x
+    int parts;                  // k-parts of the old-tap context
+    int nrep;                   // replicas of each weight slice: workgroup q of a role with n slices holds
+                                // slice q % n and runs the tasks k with k % nrep == q / n.  CTX slices are
+                                // (column tile, part 0 .. parts-2), CTXL slices the column tiles of the
+                                // last part, which adds the other parts in
+    int nbands;                 // 16-row bands per image (ceil(H / 16)); band slot bs = b * nbands + band
+    int nbs;                    // B * nbands
+    unsigned* cnt;              // [kResRoles][ntasks][8] counter slots, kDfSlotWords words apart
+    const int* kbase;           // [T + 1] position of each step's first task in the global order
+    float* ctx;                 // [ntasks][parts] x (16 x 2M) old-tap context k-parts of each task
+    void* h1;                   // [ntasks] x (16 x Np1) layer-1 output of each task (tile order)
+    void* h2;                   // [ntasks] x (16 x Np2) layer-2 output of each task
+    int* err;
+    long long budget;
+    long long* stamps;          // optional trace: 3 wall-clock ticks per task and workgroup
+    long long stamps_cap;
+    int ntasks;                 // tasks of every workgroup (band visits of all steps and images)
+};
+
 // Set the calling thread's error message and return `code`.
 int fail(int code, const std::string& msg);
 
@@ -190,6 +224,8 @@ struct Plan {
     long long stamps_cap = 0;
     // dataflow driver
     DfArgs df{};
+    // resident driver
+    ResArgs res{};
     // graph driver
     hipStream_t cap_stream = nullptr;
     hipGraph_t graph = nullptr;
@@ -231,6 +267,9 @@ int enqueue_persistent(Plan& p, hipStream_t stream);
 int build_dataflow(Plan& p, std::vector<int2>& lists, DfArgs& d);
 int enqueue_dataflow(Plan& p, hipStream_t stream);
 const void* dataflow_fn(const Plan& p);
+// Resident driver: roles and buffers of the plan, and one call.
+int build_resident(Plan& p);
+int enqueue_resident(Plan& p, hipStream_t stream);
 // Grid of a cooperative kernel: two workgroups per CU when they fit, else one.
 int coop_grid(Plan& p, const void* fn, int* grid);
 // Latency floor of one dependent step hop (see wf_measure_floor).

@@ -89,7 +89,7 @@ static int check_desc(const wf_desc* d) {
     if (mask_radius(d->mask) < 0) return fail(WF_E_INVALID, "unknown mask");
     if (d->precision != WF_FP32 && d->precision != WF_BF16)
         return fail(WF_E_INVALID, "unknown precision");
-    if (d->driver < WF_DRIVER_STREAM || d->driver > WF_DRIVER_DATAFLOW)
+    if (d->driver < WF_DRIVER_STREAM || d->driver > WF_DRIVER_RESIDENT)
         return fail(WF_E_INVALID, "unknown driver");
     if (!d->ctx_w || !d->ctx_b || !d->w1 || !d->b1 || !d->w2 || !d->b2 || !d->w3 || !d->b3 ||
         !d->scale_table)
@@ -434,6 +434,7 @@ static int build_plan(const wf_desc* d, Plan* p) {
         p->df.ncrit = p->grid >= 2 * kXcds ? p->grid / 2 / kXcds * kXcds : p->grid;
         if (p->df.ncrit == p->grid) return fail(WF_E_UNSUPPORTED, "dataflow driver needs at least 16 workgroups");
     }
+    if (p->driver == WF_DRIVER_RESIDENT && (rc = build_resident(*p)) != WF_OK) return rc;
     if (d->entropy_coder == WF_EC_RANS && (rc = build_ec(p, d->scale_table, d->L)) != WF_OK) return rc;
     WF_HIP(hipDeviceSynchronize());
 
@@ -542,6 +543,7 @@ static int run_call(Plan* p, const CallPtrs& c, hipStream_t stream, bool ec = fa
     if (ec) return enqueue_steps(*p, stream, true);
     if (p->driver == WF_DRIVER_PERSISTENT) return enqueue_persistent(*p, stream);
     if (p->driver == WF_DRIVER_DATAFLOW) return enqueue_dataflow(*p, stream);
+    if (p->driver == WF_DRIVER_RESIDENT) return enqueue_resident(*p, stream);
     return enqueue_steps(*p, stream);
 }
 
@@ -611,11 +613,17 @@ int wf_decode_bits(wf_plan_t plan, const float* psi, const uint32_t* bits, int64
 int wf_plan_trace(wf_plan_t plan, int64_t* stamps, int64_t capacity, int64_t* needed, int32_t* grid) {
     if (!plan) return fail(WF_E_INVALID, "plan is NULL");
     Plan* p = reinterpret_cast<Plan*>(plan);
-    if (p->driver != WF_DRIVER_PERSISTENT && p->driver != WF_DRIVER_DATAFLOW)
-        return fail(WF_E_UNSUPPORTED, "tracing needs the persistent or the dataflow driver");
+    if (p->driver != WF_DRIVER_PERSISTENT && p->driver != WF_DRIVER_DATAFLOW && p->driver != WF_DRIVER_RESIDENT)
+        return fail(WF_E_UNSUPPORTED, "tracing needs the persistent, dataflow or resident driver");
     if (stamps && capacity < 0) return fail(WF_E_INVALID, "negative capacity");
     p->stamps = reinterpret_cast<long long*>(stamps);
     p->stamps_cap = stamps ? capacity : 0;
+    if (p->driver == WF_DRIVER_RESIDENT) {
+        // three entries per task of every workgroup
+        if (needed) *needed = 3LL * p->res.ntasks * p->grid;
+        if (grid) *grid = p->grid;
+        return WF_OK;
+    }
     if (p->driver == WF_DRIVER_DATAFLOW) {
         // three entries per job of the plan's job lists
         if (needed) *needed = 3LL * p->df.off[2 * kXcds];

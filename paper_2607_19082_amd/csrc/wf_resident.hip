@@ -1,0 +1,774 @@
+// Resident driver: one cooperative launch of two workgroups per compute unit.
+// Every workgroup keeps one slice of the weights in registers for the whole
+// decode and plays one fixed role:
+//   CTX(c, p)  old-tap context, column tile c of 2M, k-part p < P-1 of the
+//              old taps
+//   CTXL(c)    the same for the last part P-1, which also adds the other
+//              parts' results (so layer 1 reads one context value)
+//   A(c)       layer 1 over [new taps ; old-tap context], column tile c of Np1
+//   B(c)       layer 2, column tile c of Np2
+//   C0(g)      layer 3, the columns the mean needs for channel tile g (K = 1:
+//              the mean; K = 3: three logits and three component means), and
+//              y_hat = s + mean
+//   C1(g)      layer 3, the scale columns of channel tile g, scale and index
+// Each slice is held by kResRep workgroups (replicas) that take alternate
+// tasks, two workgroups per compute unit.  A task of a role is one 16-row band (grid rows 16 beta .. 16 beta + 15 of
+// image b) at one wavefront step t: the band's latents on wavefront t, at
+// most one per grid row (Sec. III-A, Eq. 4: they are d-separated).  Every
+// workgroup runs the tasks of its role in the same global order (steps, then
+// images, then bands), computes its 16 x 16 (x the role's column tiles)
+// output tile of the task with its register-resident weights, stores it with
+// agent-coherent (sc1) stores and bumps the task's completion counter.  A
+// task waits only for the bands it reads:
+//   CTX(t, b, beta)  C0(t-2) of bands beta and beta-1 (the old taps are at
+//                    least two steps old and lie at most R <= 3 rows up)
+//   CTXL(t, b, beta) the same, and every CTX(t, b, beta)
+//   A(t, b, beta)    every CTXL(t, b, beta), C0(t-1) of bands beta and beta-1
+//                    (the new taps, one step old)
+//   B(t, b, beta)    every A(t, b, beta)
+//   C0, C1(t, b, beta)  every B(t, b, beta)
+// So bands of the upper grid rows run ahead of the lower ones, and no
+// step-wide barrier exists.  Every (role, task) has its own counter, bumped
+// once by each workgroup of the role when that workgroup's part of the task
+// is stored; it is complete when it holds the role's workgroup count.  (A
+// counter per band, reused by its successive tasks, would not do: workgroups
+// that run ahead would make up for one that is still behind.)  Each counter
+// has one slot per XCD class of the producers (64 bytes apart).  A workgroup
+// finishes its tasks in order, so a complete task implies that the role's
+// earlier tasks are complete too: waiting for the latest task a band had at
+// or before a step covers all of the band's earlier steps.
+// Every task writes its outputs (context parts, h1, h2) to buffers of its
+// own, indexed by its position k in the global order, and y_hat is written
+// once per latent, so no address is written twice in a call.  Producers store
+// with write-through (sc1) stores and bump the counter after their stores
+// have landed; consumers read with ordinary cached loads: a line is first
+// read, into an XCD's L2, only after its producer's counter was seen (the L2s
+// start each launch empty of it), so the line the L2 keeps is current, and the
+// workgroups of one XCD that read the same band share it there.
+// Deadlock freedom: every dependency of a task comes earlier in the global
+// order, and every workgroup runs its tasks in that order, so the earliest
+// unfinished task can always run; the launch is cooperative, so all
+// workgroups are resident.  Every wait has a wall-clock budget that records
+// WF_E_TIMEOUT and makes every workgroup leave, so the grid always drains.
+#include "wf_device.h"
+
+namespace wf {
+
+template <class P>
+struct ResKb;
+template <>
+struct ResKb<PF32> {
+    static constexpr int ctx = kResKbF32[0], a = kResKbF32[1], b = kResKbF32[2], c1 = kResKbF32[3],
+                         c3 = kResKbF32[4];
+};
+template <>
+struct ResKb<PBF16> {
+    static constexpr int ctx = kResKbBf16[0], a = kResKbBf16[1], b = kResKbBf16[2], c1 = kResKbBf16[3],
+                         c3 = kResKbBf16[4];
+};
+
+// Wave-uniform copies of the argument blocks.  The role functions below are
+// compiled out of line (each gets its own register allocation), and what they
+// read through a reference to an argument block would otherwise count as
+// per-lane data: every branch on it would become a divergent one.
+__device__ __forceinline__ int uni(int v) { return __builtin_amdgcn_readfirstlane(v); }
+__device__ __forceinline__ float uni(float v) {
+    return __builtin_bit_cast(float, __builtin_amdgcn_readfirstlane(__builtin_bit_cast(int, v)));
+}
+template <class T>
+__device__ __forceinline__ T* uni(T* p) {
+    const unsigned long long v = reinterpret_cast<unsigned long long>(p);
+    const unsigned lo = __builtin_amdgcn_readfirstlane((unsigned)v), hi = __builtin_amdgcn_readfirstlane((unsigned)(v >> 32));
+    return reinterpret_cast<T*>(((unsigned long long)hi << 32) | lo);
+}
+__device__ __forceinline__ StepArgs uni_args(const StepArgs& x) {
+    StepArgs a;
+#define WF_U(f) a.f = uni(x.f)
+    WF_U(H); WF_U(W); WF_U(M); WF_U(B); WF_U(K); WF_U(L); WF_U(lambda); WF_U(Np1); WF_U(Np2); WF_U(n3);
+    WF_U(n_old); WF_U(ctx_parts); WF_U(R); WF_U(new_dx0); WF_U(slope); WF_U(group); WF_U(row_w); WF_U(gparts);
+    WF_U(ec); WF_U(rowlat); WF_U(wp_all); WF_U(wp_hoist); WF_U(b_hoist); WF_U(wp_l1); WF_U(wp_new);
+    WF_U(wp_new_lo); WF_U(wp_old); WF_U(wp2); WF_U(b2); WF_U(wp3); WF_U(b3); WF_U(table); WF_U(p1); WF_U(h1);
+    WF_U(h2); WF_U(h2b); WF_U(ctxo); WF_U(ybf); WF_U(max_rows); WF_U(slots); WF_U(cp);
+    for (int q = 0; q < kMaxRadius; ++q) WF_U(old_start[q]);
+#undef WF_U
+    return a;
+}
+__device__ __forceinline__ ResArgs uni_args(const ResArgs& x) {
+    ResArgs r;
+#define WF_U(f) r.f = uni(x.f)
+    WF_U(per_slot); WF_U(parts); WF_U(nrep); WF_U(nbands); WF_U(nbs); WF_U(cnt); WF_U(kbase); WF_U(ctx); WF_U(h1); WF_U(h2);
+    WF_U(err);
+    WF_U(stamps); WF_U(ntasks);
+    for (int q = 0; q <= kResRoles; ++q) WF_U(first[q]);
+#undef WF_U
+    r.budget = ((long long)uni((int)(x.budget >> 32)) << 32) | (unsigned)uni((int)x.budget);
+    r.stamps_cap = ((long long)uni((int)(x.stamps_cap >> 32)) << 32) | (unsigned)uni((int)x.stamps_cap);
+    return r;
+}
+
+// Steps [t0, t1] during which band beta (grid rows 16 beta ..) holds latents.
+__host__ __device__ __forceinline__ void band_span(int H, int W, int lam, int beta, int& t0, int& t1) {
+    const int i0 = beta * kTile, i1 = min(H - 1, i0 + kTile - 1);
+    t0 = lam * i0;
+    t1 = lam * i1 + W - 1;
+}
+// Position in the global order of the latest task of band beta (image b) at
+// a step <= s, or -1 when the band has none (beta < 0, or s before its first).
+__device__ __forceinline__ int band_task(const StepArgs& a, const ResArgs& r, int b, int beta, int s) {
+    if (beta < 0 || s < 0) return -1;
+    int t0, t1;
+    band_span(a.H, a.W, a.lambda, beta, t0, t1);
+    if (s < t0) return -1;
+    const int t = min(s, t1);
+    int i0, n;
+    step_span(a.H, a.W, a.lambda, t, i0, n);
+    const int blo = i0 / kTile, nb = (i0 + n - 1) / kTile - blo + 1;
+    return r.kbase[t] + b * nb + beta - blo;
+}
+
+// Row r of band beta of image b at step t.
+__device__ __forceinline__ Row band_row(const StepArgs& a, int b, int beta, int t, int r) {
+    Row w;
+    w.b = b;
+    w.i = beta * kTile + r;
+    w.j = t - a.lambda * w.i;
+    w.valid = w.i < a.H && w.j >= 0 && w.j < a.W;
+    w.lat = w.valid ? ((size_t)b * a.H + w.i) * a.W + w.j : 0;
+    return w;
+}
+
+__device__ __forceinline__ unsigned* res_slot(const ResArgs& r, int role, int k, int x) {
+    return r.cnt + (((size_t)role * r.ntasks + k) * kXcds + x) * kDfSlotWords;
+}
+
+// One wait: task k of `role` complete (nothing to wait for when k < 0).
+struct ResWait {
+    int role, k;
+};
+
+// Wave 0 polls up to three waits, eight lanes each (one per XCD class).  A
+// wait longer than the budget, or an error recorded elsewhere, makes the
+// workgroup leave (returns false).
+__device__ __forceinline__ bool res_wait(const ResArgs& r, ResWait w0, ResWait w1, ResWait w2, int* bail) {
+    if (threadIdx.x < 64) {
+        const int lane = threadIdx.x, i = lane >> 3, x = lane & (kXcds - 1);
+        const ResWait w = i == 0 ? w0 : (i == 1 ? w1 : w2);
+        unsigned tgt = 0;
+        const unsigned* p = r.cnt;
+        if (i < 3 && w.k >= 0) {
+            tgt = (unsigned)r.per_slot[(w.role * kResRep + w.k % r.nrep) * kXcds + x];
+            p = res_slot(r, w.role, w.k, x);
+        }
+        int flag = 0;
+        const long long t0 = wall_clock64();
+        unsigned it = 0;
+        while (true) {
+            const unsigned v = tgt ? __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) : 0u;
+            if (__all(v >= tgt)) break;
+            if ((++it & 63u) == 0) {
+                if (__hip_atomic_load(r.err, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) != 0) {
+                    flag = 1;
+                    break;
+                }
+                if (wall_clock64() - t0 > r.budget) {
+                    if (lane == 0) __hip_atomic_store(r.err, kErrTimeout, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                    flag = 1;
+                    break;
+                }
+            }
+            __builtin_amdgcn_s_sleep(1);
+        }
+        if (lane == 0) *bail = flag;
+    }
+    __syncthreads();
+    return *bail == 0;
+}
+
+// Publish the task's stores (every wave's have landed) and count the task.
+__device__ __forceinline__ void res_signal(const ResArgs& r, int role, int k) {
+    __builtin_amdgcn_s_waitcnt(0);
+    __syncthreads();
+    if (threadIdx.x == 0)
+        __hip_atomic_fetch_add(res_slot(r, role, k, blockIdx.x % kXcds), 1u, __ATOMIC_RELAXED,
+                               __HIP_MEMORY_SCOPE_AGENT);
+}
+
+__device__ __forceinline__ void res_stamp(const ResArgs& r, int k, int e) {
+    if (r.stamps && threadIdx.x == 0) {
+        const long long q = ((long long)k * gridDim.x + blockIdx.x) * 3 + e;
+        if (q < r.stamps_cap) r.stamps[q] = wall_clock64();
+    }
+}
+
+// The wave's share of a role's weights: k-blocks [kb0, kb0 + n) of NC column
+// tiles ct0 + c * cstride of a packed panel with nkb k-blocks per column tile.
+template <class P, int KB, int NC>
+struct WSlice {
+    typename P::B w[KB][NC];
+    int kb0, n;
+    __device__ __forceinline__ void split(int lo, int hi) {
+        const int per = (hi - lo + kWaves - 1) / kWaves;
+        kb0 = min(hi, lo + wave_id() * per);
+        n = min(hi, kb0 + per) - kb0;
+    }
+    __device__ __forceinline__ void load(const void* panel, int nkb, int ct0, int cstride) {
+        const typename P::B* p = static_cast<const typename P::B*>(panel) + (threadIdx.x & 63);
+#pragma unroll
+        for (int u = 0; u < KB; ++u)
+#pragma unroll
+            for (int c = 0; c < NC; ++c)
+                if (u < n) w[u][c] = p[((size_t)(ct0 + c * cstride) * nkb + kb0 + u) * 64];
+    }
+};
+
+// acc[c] += sum over the wave's k-blocks of A(kb) x W(kb, c), the
+// activations loaded in batches of KBB k-blocks (each batch's loads issued
+// before its first MFMA; one batch when KBB = KB).
+template <class P, int KB, int NC, int KBB = KB, class LoadA>
+__device__ __forceinline__ void wdot(const WSlice<P, KB, NC>& s, LoadA la, f4 (&acc)[NC]) {
+    static_assert(KB % KBB == 0, "whole batches");
+    // wave-uniform, in scalar registers: the guards below are then scalar
+    // branches, and a batch's loads are all in flight before its first wait
+    const int n = __builtin_amdgcn_readfirstlane(s.n), kb0 = __builtin_amdgcn_readfirstlane(s.kb0);
+#pragma unroll
+    for (int u0 = 0; u0 < KB; u0 += KBB) {
+        if (u0 >= n) break;
+        typename P::A av[KBB];
+#pragma unroll
+        for (int u = 0; u < KBB; ++u)
+            if (u0 + u < n) av[u] = la(kb0 + u0 + u);
+#pragma unroll
+        for (int u = 0; u < KBB; ++u)
+            if (u0 + u < n)
+#pragma unroll
+                for (int c = 0; c < NC; ++c) acc[c] = P::mma(av[u], s.w[u0 + u][c], acc[c]);
+    }
+}
+
+// The same in two halves, for software pipelining: wload issues the loads of
+// the wave's k-blocks into av, wmma consumes them.
+template <class P, int KB, int NC, class LoadA>
+__device__ __forceinline__ void wload(const WSlice<P, KB, NC>& s, LoadA la, typename P::A (&av)[KB]) {
+    const int n = __builtin_amdgcn_readfirstlane(s.n), kb0 = __builtin_amdgcn_readfirstlane(s.kb0);
+#pragma unroll
+    for (int u = 0; u < KB; ++u)
+        if (u < n) av[u] = la(kb0 + u);
+}
+template <class P, int KB, int NC>
+__device__ __forceinline__ void wmma(const WSlice<P, KB, NC>& s, const typename P::A (&av)[KB], f4 (&acc)[NC]) {
+    const int n = __builtin_amdgcn_readfirstlane(s.n);
+#pragma unroll
+    for (int u = 0; u < KB; ++u)
+        if (u < n)
+#pragma unroll
+            for (int c = 0; c < NC; ++c) acc[c] = P::mma(av[u], s.w[u][c], acc[c]);
+}
+
+// The task after (t, b, beta) in the global order (t = T when there is none).
+__device__ __forceinline__ void next_task(const StepArgs& a, int T, int& t, int& b, int& beta) {
+    int i0, n;
+    step_span(a.H, a.W, a.lambda, t, i0, n);
+    if (beta < (i0 + n - 1) / kTile) {
+        ++beta;
+        return;
+    }
+    if (b + 1 < a.B) {
+        ++b;
+        beta = i0 / kTile;
+        return;
+    }
+    b = 0;
+    if (++t < T) {
+        step_span(a.H, a.W, a.lambda, t, i0, n);
+        beta = i0 / kTile;
+    }
+}
+
+// Sum the four waves' partial tiles: afterwards lane l of wave w (< 4) holds
+// in v[c] row 4 * (l / 16) + w, column l % 16 of tile c.
+template <int NC>
+__device__ __forceinline__ void wreduce(f4 (*red)[64], const f4 (&acc)[NC], float (&v)[NC]) {
+    const int wave = wave_id(), lane = threadIdx.x & 63;
+#pragma unroll
+    for (int c = 0; c < NC; ++c) red[wave * NC + c][lane] = acc[c];
+    __syncthreads();
+#pragma unroll
+    for (int c = 0; c < NC; ++c) {
+        v[c] = 0.0f;
+#pragma unroll
+        for (int w2 = 0; w2 < kWaves; ++w2) v[c] += red[w2 * NC + c][lane][wave];
+    }
+    __syncthreads();
+}
+
+// Visit the tasks (t, b, beta) of replica rep in the global order (position
+// k with k % nrep == rep); body returns false to leave.
+template <class F>
+__device__ __forceinline__ void for_tasks(const StepArgs& a, int T, int rep, int nrep, F body) {
+    int k = 0;
+    for (int t = 0; t < T; ++t) {
+        int i0, n;
+        step_span(a.H, a.W, a.lambda, t, i0, n);
+        const int blo = i0 / kTile, bhi = (i0 + n - 1) / kTile;
+        for (int b = 0; b < a.B; ++b)
+            for (int beta = blo; beta <= bhi; ++beta, ++k)
+                if (k % nrep == rep && !body(t, b, beta, k)) return;
+    }
+}
+
+// Element offset of context part `part` of task k (16 rows x 2M, tile order).
+__device__ __forceinline__ size_t ctx_base(const StepArgs& a, const ResArgs& r, int k, int part) {
+    return ((size_t)k * r.parts + part) * kTile * 2 * a.M;
+}
+
+// ---------------------------------------------------------------------------
+// CTX(c, p) / CTXL(c): ctx[p][r][n] = sum over part p's old-tap k-blocks of
+// taps x Wc; the last part (LAST) stores the sum over all parts.
+template <class P, bool R3, bool LAST>
+__device__ __noinline__ void res_ctx(const StepArgs& a_in, const ResArgs& r_in, int T, int q, int rep, f4 (*red)[64],
+                                     int* bail) {
+    const StepArgs a = uni_args(a_in);
+    const ResArgs r = uni_args(r_in);
+    constexpr int KB = ResKb<P>::ctx;
+    const int nct = 2 * a.M / kTile;
+    const int c = q % nct, part = LAST ? r.parts - 1 : q / nct;   // q: the slice
+    const int lane = threadIdx.x & 63, kq = lane >> 4, wave = wave_id();
+    const int nkb = a.n_old * a.M / P::kK;
+    WSlice<P, KB, 1> s;
+    s.split(nkb * part / r.parts, nkb * (part + 1) / r.parts);
+    s.load(a.wp_old, nkb, c, 0);
+    const int ro = kq * 4 + wave, col = c * kTile + (lane & 15);
+    const size_t pstride = (size_t)kTile * 2 * a.M;
+    // the call's reconstruction, read once (not once per k-block)
+    const float* yhat = P::kBf16 ? nullptr : uni(a.cp->y_hat);
+    for_tasks(a, T, rep, r.nrep, [&](int t, int b, int beta, int k) {
+        res_stamp(r, k, 0);
+        if (!res_wait(r, ResWait{RR_C0, band_task(a, r, b, beta, t - 2)},
+                      ResWait{RR_C0, band_task(a, r, b, beta - 1, t - 2)}, ResWait{RR_CTX, LAST ? k : -1}, bail))
+            return false;
+        res_stamp(r, k, 1);
+        const size_t e = ctx_base(a, r, k, 0) + tile_idx<PF32>(ro, col, 2 * a.M);
+        // the other parts of this element (the last part adds them)
+        float prev = 0.0f;
+        if constexpr (LAST) {
+#pragma unroll
+            for (int p2 = 0; p2 < kResMaxParts - 1; ++p2)
+                prev += ld1<false>(r.ctx, e + p2 * pstride, p2 < r.parts - 1);
+        }
+        const Row w = band_row(a, b, beta, t, lane & 15);
+        f4 acc[1] = {zero4()};
+        // two load batches: the registers hold the weights
+        wdot<P, KB, 1, KB / 2>(s, [&](int kb) { return ld_tap_from<P, false, R3>(a, yhat, w, kb, kq, true); }, acc);
+        float v[1];
+        wreduce<1>(red, acc, v);
+        st1<true>(r.ctx, e + part * pstride, v[0] + prev);
+        res_signal(r, LAST ? RR_CTXL : RR_CTX, k);
+        res_stamp(r, k, 2);
+        return true;
+    });
+}
+
+// A(c): h1 = lrelu(P1 + [new taps ; ctx] . [F_new ; W1b]) for column tile c.
+template <class P>
+__device__ __noinline__ void res_l1(const StepArgs& a_in, const ResArgs& r_in, int T, int c, int rep, f4 (*red)[64], int* bail) {
+    const StepArgs a = uni_args(a_in);
+    const ResArgs r = uni_args(r_in);
+    const int lane = threadIdx.x & 63, kq = lane >> 4, wave = wave_id();
+    const int M = a.M, ro = kq * 4 + wave, col = c * kTile + (lane & 15);
+    const int kbn = kMaxNew * M / P::kK, kbc = 2 * M / P::kK;
+    WSlice<P, ResKb<P>::a, 1> s;     // fp32: [F_new ; W1b]; bf16: F_new hi (new taps) or W1b (context)
+    WSlice<P, ResKb<P>::a, 1> slo;   // bf16: F_new lo (new taps)
+    // bf16: the new-tap and the context k-ranges are both 2M long; waves 0-1
+    // take the new taps, waves 2-3 the context, so that each wave's loads are
+    // one uniform batch
+    const bool isnew = wave < kWaves / 2;
+    if constexpr (P::kBf16) {
+        const int lo = isnew ? 0 : kbn, hi = isnew ? kbn : kbn + kbc;
+        const int per = (hi - lo + 1) / 2;
+        s.kb0 = min(hi, lo + (wave & 1) * per);
+        s.n = min(hi, s.kb0 + per) - s.kb0;
+        slo.kb0 = s.kb0;
+        slo.n = isnew ? s.n : 0;
+        const typename P::B* ph = static_cast<const typename P::B*>(a.wp_new) + lane;
+        const typename P::B* pl = static_cast<const typename P::B*>(a.wp_new_lo) + lane;
+        const typename P::B* pc = static_cast<const typename P::B*>(a.wp_l1) + lane;
+#pragma unroll
+        for (int u = 0; u < ResKb<P>::a; ++u) {
+            if (u >= s.n) continue;
+            const int kb = s.kb0 + u;
+            if (isnew) {
+                s.w[u][0] = ph[((size_t)c * kbn + kb) * 64];
+                slo.w[u][0] = pl[((size_t)c * kbn + kb) * 64];
+            } else {
+                s.w[u][0] = pc[((size_t)c * kbc + kb - kbn) * 64];
+            }
+        }
+    } else {
+        s.split(0, kbn + kbc);
+        slo.kb0 = s.kb0;
+        slo.n = 0;
+        s.load(a.wp_l1, kbn + kbc, c, 0);
+    }
+    const size_t h1s = (size_t)kTile * a.Np1 * 4;     // bytes of one task's h1
+    const float* yhat = P::kBf16 ? nullptr : uni(a.cp->y_hat);   // read once
+    for_tasks(a, T, rep, r.nrep, [&](int t, int b, int beta, int k) {
+        const int bs = b * r.nbands + beta;
+        // the epilogue operand (hoisted before the launch) first
+        const Row v = band_row(a, b, beta, t, ro);
+        const float z = ld1<false>(a.p1, v.lat * a.Np1 + col, v.valid);
+        res_stamp(r, k, 0);
+        if (!res_wait(r, ResWait{RR_CTXL, k}, ResWait{RR_C0, band_task(a, r, b, beta, t - 1)},
+                      ResWait{RR_C0, band_task(a, r, b, beta - 1, t - 1)}, bail))
+            return false;
+        res_stamp(r, k, 1);
+        const Row w = band_row(a, b, beta, t, lane & 15);
+        f4 acc[1] = {zero4()};
+        if constexpr (P::kBf16) {
+            const int sn = __builtin_amdgcn_readfirstlane(s.n), skb0 = __builtin_amdgcn_readfirstlane(s.kb0);
+            if (isnew) {
+                b8x2 av[ResKb<P>::a];
+#pragma unroll
+                for (int u = 0; u < ResKb<P>::a; ++u)
+                    if (u < sn) av[u] = ld_tap_from<PBF16, false>(a, nullptr, w, skb0 + u, kq, false);
+#pragma unroll
+                for (int u = 0; u < ResKb<P>::a; ++u)
+                    if (u < sn) {
+                        acc[0] = PBF16::mma(av[u], s.w[u][0], acc[0]);
+                        acc[0] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av[u].hi, slo.w[u][0], acc[0], 0, 0, 0);
+                    }
+            } else {
+                // the old-tap context (the last part's buffer holds the sum):
+                // eight fp32 values per k-block, loaded first, split into
+                // bf16 pairs afterwards
+                const size_t e = ctx_base(a, r, k, r.parts - 1);
+                f4 raw[ResKb<P>::a][2];
+#pragma unroll
+                for (int u = 0; u < ResKb<P>::a; ++u)
+                    if (u < sn) {
+                        const int c0 = (skb0 + u - kbn) * 32 + kq * 8;
+                        raw[u][0] = ld4<false>(r.ctx, e + tile_idx<PF32>(lane & 15, c0, 2 * M), w.valid);
+                        raw[u][1] = ld4<false>(r.ctx, e + tile_idx<PF32>(lane & 15, c0 + 4, 2 * M), w.valid);
+                    }
+#pragma unroll
+                for (int u = 0; u < ResKb<P>::a; ++u)
+                    if (u < sn) acc[0] = PBF16::mma(split8(raw[u][0], raw[u][1]), s.w[u][0], acc[0]);
+            }
+        } else {
+            wdot(s, [&](int kb) -> f4 {
+                if (kb < kbn) return ld_tap_from<PF32, false>(a, yhat, w, kb, kq, false);
+                // the old-tap context: the last part's buffer holds the sum
+                return ld_tile<PF32, false>(r.ctx + ctx_base(a, r, k, r.parts - 1), 0, 2 * M, kb - kbn, w.valid);
+            }, acc);
+        }
+        float o[1];
+        wreduce<1>(red, acc, o);
+        st_tile<P, true>(static_cast<char*>(r.h1) + k * h1s, ro, a.Np1, col, lrelu(o[0] + z, a.slope));
+        res_signal(r, RR_A, k);
+        res_stamp(r, k, 2);
+        return true;
+    });
+}
+
+// B(c): h2 = lrelu(W2 . h1 + b2) for column tile c.
+template <class P>
+__device__ __noinline__ void res_l2(const StepArgs& a_in, const ResArgs& r_in, int T, int c, int rep, f4 (*red)[64], int* bail) {
+    const StepArgs a = uni_args(a_in);
+    const ResArgs r = uni_args(r_in);
+    const int lane = threadIdx.x & 63, kq = lane >> 4, wave = wave_id();
+    const int ro = kq * 4 + wave, col = c * kTile + (lane & 15);
+    const int nkb = a.Np1 / P::kK;
+    WSlice<P, ResKb<P>::b, 1> s;
+    s.split(0, nkb);
+    s.load(a.wp2, nkb, c, 0);
+    const float bias = a.b2[col];
+    const size_t h1s = (size_t)kTile * a.Np1 * 4, h2s = (size_t)kTile * a.Np2 * 4;
+    for_tasks(a, T, rep, r.nrep, [&](int t, int b, int beta, int k) {
+        const int bs = b * r.nbands + beta;
+        res_stamp(r, k, 0);
+        if (!res_wait(r, ResWait{RR_A, k}, ResWait{0, -1}, ResWait{0, -1}, bail))
+            return false;
+        res_stamp(r, k, 1);
+        const Row w = band_row(a, b, beta, t, lane & 15);
+        const char* h1 = static_cast<const char*>(r.h1) + k * h1s;
+        f4 acc[1] = {zero4()};
+        wdot(s, [&](int kb) { return ld_tile<P, false>(h1, 0, a.Np1, kb, w.valid); }, acc);
+        float o[1];
+        wreduce<1>(red, acc, o);
+        char* h2 = static_cast<char*>(r.h2) + k * h2s;
+        st_tile<P, true>(h2, ro, a.Np2, col, lrelu(o[0] + bias, a.slope));
+        res_signal(r, RR_B, k);
+        res_stamp(r, k, 2);
+        return true;
+    });
+}
+
+// C0(g) / C1(g): layer 3 of channel tile g and the parameter epilogue.
+template <class P, int KC, bool MEAN>
+__device__ __noinline__ void res_l3(const StepArgs& a_in, const ResArgs& r_in, int T, int g, int rep, f4 (*red)[64], const float* tab,
+                       int* bail) {
+    const StepArgs a = uni_args(a_in);
+    const ResArgs r = uni_args(r_in);
+    constexpr int NC = MEAN ? (KC == 1 ? 1 : 6) : KC;
+    constexpr int KB = KC == 1 ? ResKb<P>::c1 : ResKb<P>::c3;
+    const int lane = threadIdx.x & 63, kq = lane >> 4, wave = wave_id();
+    const int M = a.M, G = M / kTile, ro = kq * 4 + wave, ch = g * kTile + (lane & 15);
+    const int nkb = a.Np2 / P::kK;
+    // first column tile of the role and the stride between its tiles
+    const int ct0 = MEAN ? g : (KC == 1 ? G + g : 6 * G + g);
+    WSlice<P, KB, NC> s;
+    s.split(0, nkb);
+    s.load(a.wp3, nkb, ct0, G);
+    float bias[NC];
+#pragma unroll
+    for (int c = 0; c < NC; ++c) bias[c] = a.b3[(ct0 + c * G - g) * kTile + ch];
+    const size_t h2s = (size_t)kTile * a.Np2 * 4;
+    // the call's pointers, read once
+    CallPtrs cpv;
+    {
+        const CallPtrs* cq = a.cp;
+        cpv.sym = uni(cq->sym); cpv.y = uni(cq->y); cpv.sym_out = uni(cq->sym_out);
+        cpv.y_hat = uni(cq->y_hat); cpv.mean = uni(cq->mean); cpv.scale = uni(cq->scale);
+        cpv.weight = uni(cq->weight); cpv.cmean = uni(cq->cmean); cpv.idx = uni(cq->idx);
+        cpv.encode = uni(cq->encode);
+    }
+    const CallPtrs* cp = &cpv;
+    for_tasks(a, T, rep, r.nrep, [&](int t, int b, int beta, int k) {
+        const int bs = b * r.nbands + beta;
+        const Row v = band_row(a, b, beta, t, ro);
+        const size_t oq = v.lat * M + ch;
+        float sin = 0.0f;
+        if (MEAN && v.valid) sin = cp->encode ? cp->y[oq] : (float)cp->sym[oq];
+        res_stamp(r, k, 0);
+        if (!res_wait(r, ResWait{RR_B, k}, ResWait{0, -1}, ResWait{0, -1}, bail))
+            return false;
+        res_stamp(r, k, 1);
+        const Row w = band_row(a, b, beta, t, lane & 15);
+        const char* h2 = static_cast<const char*>(r.h2) + k * h2s;
+        f4 acc[NC];
+#pragma unroll
+        for (int c = 0; c < NC; ++c) acc[c] = zero4();
+        wdot(s, [&](int kb) { return ld_tile<P, false>(h2, 0, a.Np2, kb, w.valid); }, acc);
+        float o[NC];
+        wreduce<NC>(red, acc, o);
+#pragma unroll
+        for (int c = 0; c < NC; ++c) o[c] += bias[c];
+        if (v.valid) {
+            if constexpr (!MEAN) {
+                const float t0 = tab[0];
+#pragma unroll
+                for (int kk = 0; kk < KC; ++kk) {
+                    const float sg = o[kk] > t0 ? o[kk] : t0;
+                    const size_t q2 = (v.lat * KC + kk) * M + ch;
+                    cp->scale[q2] = sg;
+                    cp->idx[q2] = scale_index(tab, a.L, sg);
+                }
+            } else {
+                float mu;
+                if constexpr (KC == 1) {
+                    mu = o[0];
+                } else {
+                    const float mx = fmaxf(o[0], fmaxf(o[1], o[2]));
+                    float ex[3], den = 0.0f;
+#pragma unroll
+                    for (int kk = 0; kk < 3; ++kk) {
+                        ex[kk] = expf(o[kk] - mx);
+                        den += ex[kk];
+                    }
+                    mu = 0.0f;
+#pragma unroll
+                    for (int kk = 0; kk < 3; ++kk) {
+                        const float wk = ex[kk] / den;
+                        const size_t q2 = (v.lat * 3 + kk) * M + ch;
+                        cp->weight[q2] = wk;
+                        cp->cmean[q2] = o[3 + kk];
+                        mu += wk * o[3 + kk];
+                    }
+                }
+                float sv;
+                if (cp->encode) {
+                    sv = rintf(sin - mu);
+                    cp->sym_out[oq] = (int32_t)sv;
+                } else {
+                    sv = sin;
+                }
+                cp->mean[oq] = mu;
+                st1<true>(cp->y_hat, oq, sv + mu);
+                if constexpr (P::kBf16) st_pair_row<true>(a.ybf, v.lat * 2 * M, ch, sv + mu);
+            }
+        }
+        res_signal(r, MEAN ? RR_C0 : RR_C1, k);
+        res_stamp(r, k, 2);
+        return true;
+    });
+}
+
+// Two workgroups per compute unit (each wave at most 256 registers).
+template <class P, int KC>
+__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2))) void k_resident(
+    StepArgs a, ResArgs r, int T) {
+    __shared__ f4 red[kWaves * kResMaxNc][64];
+    __shared__ float tab[kMaxTable];
+    __shared__ int bail;
+    for (int l = threadIdx.x; l < a.L; l += blockDim.x) tab[l] = a.table[l];
+    __syncthreads();
+    // (selects, not a loop: a runtime index into the argument block would
+    // copy it to scratch memory)
+    const int g = blockIdx.x;
+    const int role = (g >= r.first[1]) + (g >= r.first[2]) + (g >= r.first[3]) + (g >= r.first[4]) +
+                     (g >= r.first[5]);
+    const int q = g - (role == 0   ? 0
+                       : role == 1 ? r.first[1]
+                       : role == 2 ? r.first[2]
+                       : role == 3 ? r.first[3]
+                       : role == 4 ? r.first[4]
+                                   : r.first[5]);
+    // slices of the role (its workgroups are nrep replicas of each)
+    const int nsl = ((role == 0   ? r.first[1]
+                      : role == 1 ? r.first[2] - r.first[1]
+                      : role == 2 ? r.first[3] - r.first[2]
+                      : role == 3 ? r.first[4] - r.first[3]
+                      : role == 4 ? r.first[5] - r.first[4]
+                                  : r.first[6] - r.first[5])) / r.nrep;
+    const int sl = q % nsl, rep = q / nsl;
+    switch (role) {
+    case RR_CTX:
+        if (a.R == kMaxRadius) res_ctx<P, true, false>(a, r, T, sl, rep, red, &bail);
+        else res_ctx<P, false, false>(a, r, T, sl, rep, red, &bail);
+        break;
+    case RR_CTXL:
+        if (a.R == kMaxRadius) res_ctx<P, true, true>(a, r, T, sl, rep, red, &bail);
+        else res_ctx<P, false, true>(a, r, T, sl, rep, red, &bail);
+        break;
+    case RR_A: res_l1<P>(a, r, T, sl, rep, red, &bail); break;
+    case RR_B: res_l2<P>(a, r, T, sl, rep, red, &bail); break;
+    case RR_C0: res_l3<P, KC, true>(a, r, T, sl, rep, red, tab, &bail); break;
+    default: res_l3<P, KC, false>(a, r, T, sl, rep, red, tab, &bail); break;
+    }
+}
+
+__global__ void k_res_zero(unsigned* p, size_t n) {
+    for (size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += (size_t)gridDim.x * blockDim.x)
+        p[i] = 0u;
+}
+
+static const void* resident_fn(const Plan& p) {
+    if (p.precision == WF_BF16)
+        return p.K == 1 ? (const void*)k_resident<PBF16, 1> : (const void*)k_resident<PBF16, 3>;
+    return p.K == 1 ? (const void*)k_resident<PF32, 1> : (const void*)k_resident<PF32, 3>;
+}
+
+template <class T>
+static int res_alloc(Plan& p, T** dst, size_t n) {
+    hipError_t e = hipMalloc((void**)dst, n * sizeof(T));
+    if (e != hipSuccess) return fail(WF_E_NOMEM, std::string("hipMalloc: ") + hipGetErrorString(e));
+    p.owned.push_back(*dst);
+    return WF_OK;
+}
+
+static int ceil_div(int a, int b) { return (a + b - 1) / b; }
+
+int build_resident(Plan& p) {
+    const StepArgs& a = p.args;
+    ResArgs& r = p.res;
+    const bool bf = p.precision == WF_BF16;
+    const int* kb = bf ? kResKbBf16 : kResKbF32;
+    const int kk = bf ? 32 : 16;
+    const int M = p.M, G = M / kTile, nct = 2 * M / kTile;
+    // every wave's share of every slice must fit its registers
+    if (ceil_div((kMaxNew * M + 2 * M) / kk, kWaves) > kb[1] || ceil_div(p.Np1 / kk, kWaves) > kb[2] ||
+        ceil_div(p.Np2 / kk, kWaves) > kb[p.K == 1 ? 3 : 4])
+        return fail(WF_E_UNSUPPORTED, "resident driver: a weight slice exceeds the register budget (M too large)");
+    const int nkb_old = a.n_old * M / kk;
+    int cus = 0, dev = 0;
+    hipError_t e = hipGetDevice(&dev);
+    if (e == hipSuccess) e = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);
+    if (e != hipSuccess) return fail(WF_E_HIP, std::string("device query: ") + hipGetErrorString(e));
+    const int crit = p.Np1 / kTile + p.Np2 / kTile + 2 * G;
+    const int slots = kResRep * cus;   // two workgroups per compute unit
+    // the fewest old-tap context parts whose slices fit the registers
+    int parts = 1;
+    while (ceil_div(ceil_div(nkb_old, parts), kWaves) > kb[0]) ++parts;
+    if (parts > kResMaxParts) return fail(WF_E_UNSUPPORTED, "resident driver: the old-tap context needs too many parts");
+    if (kResRep * (crit + nct * parts) > slots)
+        return fail(WF_E_UNSUPPORTED, "resident driver: " + std::to_string(kResRep * (crit + nct * parts)) +
+                                          " workgroups for " + std::to_string(slots) + " slots");
+    // spare slots take more context parts (shorter context tasks)
+    while (kResRep * (crit + nct * (parts + 1)) <= slots && parts < kResMaxParts && nkb_old / (parts + 1) >= kWaves)
+        ++parts;
+    r.parts = parts;
+    r.nrep = kResRep;
+    const int n[kResRoles] = {nct * (parts - 1), nct, p.Np1 / kTile, p.Np2 / kTile, G, G};
+    r.first[0] = 0;
+    for (int k = 0; k < kResRoles; ++k) r.first[k + 1] = r.first[k] + kResRep * n[k];
+    const int grid = r.first[kResRoles];
+    int per_slot[kResRoles * kResRep * kXcds] = {};
+    for (int k = 0; k < kResRoles; ++k)
+        for (int g = r.first[k]; g < r.first[k + 1]; ++g) {
+            const int h = (g - r.first[k]) / n[k];   // the workgroup's replica
+            ++per_slot[(k * kResRep + h) * kXcds + g % kXcds];
+        }
+    int* d_per = nullptr;
+    int rc;
+    if ((rc = res_alloc(p, &d_per, kResRoles * kResRep * kXcds)) != WF_OK) return rc;
+    e = hipMemcpy(d_per, per_slot, sizeof(per_slot), hipMemcpyHostToDevice);
+    if (e != hipSuccess) return fail(WF_E_HIP, std::string("hipMemcpy: ") + hipGetErrorString(e));
+    r.per_slot = d_per;
+    r.nbands = ceil_div(p.H, kTile);
+    r.nbs = p.B * r.nbands;
+    const size_t nbs = (size_t)r.nbs;
+    std::vector<int> kbase(p.T + 1);
+    long long tasks = 0;
+    for (int t = 0; t < p.T; ++t) {
+        int i0, nn;
+        step_span(p.H, p.W, p.lambda, t, i0, nn);
+        kbase[t] = (int)tasks;
+        tasks += (long long)p.B * ((i0 + nn - 1) / kTile - i0 / kTile + 1);
+    }
+    kbase[p.T] = (int)tasks;
+    r.ntasks = (int)tasks;
+    int* d_kbase = nullptr;
+    if ((rc = res_alloc(p, &d_kbase, kbase.size())) != WF_OK) return rc;
+    e = hipMemcpy(d_kbase, kbase.data(), kbase.size() * sizeof(int), hipMemcpyHostToDevice);
+    if (e != hipSuccess) return fail(WF_E_HIP, std::string("hipMemcpy: ") + hipGetErrorString(e));
+    r.kbase = d_kbase;
+    if ((rc = res_alloc(p, &r.cnt, (size_t)kResRoles * tasks * kXcds * kDfSlotWords)) != WF_OK) return rc;
+    // one output buffer per task (no address is written twice in a call);
+    // each is read through raw buffer loads and must fit their window
+    const size_t nt = (size_t)tasks;
+    const size_t ctx_n = nt * parts * kTile * 2 * M, h1_n = nt * kTile * p.Np1, h2_n = nt * kTile * p.Np2;
+    if (std::max(ctx_n, std::max(h1_n, h2_n)) * 4 >= (size_t)kBufBytes)
+        return fail(WF_E_UNSUPPORTED, "resident driver: per-task buffers exceed the 2 GiB buffer window");
+    if ((rc = res_alloc(p, &r.ctx, ctx_n)) != WF_OK) return rc;
+    float *h1 = nullptr, *h2 = nullptr;
+    if ((rc = res_alloc(p, &h1, h1_n)) != WF_OK) return rc;
+    if ((rc = res_alloc(p, &h2, h2_n)) != WF_OK) return rc;
+    r.h1 = h1;
+    r.h2 = h2;
+    r.err = p.d_err;
+    r.budget = p.spin_budget;
+    // one workgroup per compute unit, all resident at once
+    int per_cu = 0;
+    e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, resident_fn(p), kThreads, 0);
+    if (e != hipSuccess) return fail(WF_E_HIP, std::string("occupancy query: ") + hipGetErrorString(e));
+    if (per_cu < kResRep) return fail(WF_E_UNSUPPORTED, "resident kernel: two workgroups per CU do not fit");
+    p.grid = grid;
+    return WF_OK;
+}
+
+int enqueue_resident(Plan& p, hipStream_t stream) {
+    ResArgs r = p.res;
+    r.stamps = p.stamps;
+    r.stamps_cap = p.stamps_cap;
+    const size_t ncnt = (size_t)kResRoles * r.ntasks * kXcds * kDfSlotWords;
+    hipLaunchKernelGGL(k_res_zero, dim3(1024), dim3(256), 0, stream, r.cnt, ncnt);
+    int rc = enqueue_hoist(p, stream);
+    if (rc != WF_OK) return rc;
+    StepArgs a = p.args;
+    int T = p.T;
+    void* args[] = {&a, &r, &T};
+    hipError_t e = hipLaunchCooperativeKernel(resident_fn(p), dim3(p.grid), dim3(kThreads), args, 0, stream);
+    if (e != hipSuccess) return fail(WF_E_HIP, std::string("cooperative launch: ") + hipGetErrorString(e));
+    return WF_OK;
+}
+
+}  // namespace wf

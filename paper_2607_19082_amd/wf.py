@@ -19,7 +19,7 @@ MASK = {"full": 0, "relaxed": 1, "3x3": 2, "7x7": 3}
 PARAM_ORDER = {"native": 0, "scales_first": 1}
 KERNEL = {"full": 5, "relaxed": 5, "3x3": 3, "7x7": 7}   # ctx_w's spatial size per mask
 PRECISION = {"fp32": 0, "bf16": 1}
-DRIVER = {"stream": 0, "graph": 1, "persistent": 2, "dataflow": 3}
+DRIVER = {"stream": 0, "graph": 1, "persistent": 2, "dataflow": 3, "resident": 4}
 
 EXPORTS = ["wf_schedule", "wf_validate", "wf_plan", "wf_plan_schedule", "wf_decode",
            "wf_encode", "wf_ec_tables", "wf_encode_bits", "wf_decode_bits", "wf_plan_trace",

@@ -86,7 +86,7 @@ SMALL = [
 ]
 
 
-@pytest.mark.parametrize("driver", ["stream", "graph", "persistent", "dataflow"])
+@pytest.mark.parametrize("driver", ["stream", "graph", "persistent", "dataflow", "resident"])
 @pytest.mark.parametrize("name,H,W,B", SMALL)
 def test_bf16_small_decode_encode(name, H, W, B, driver):
     log(f"bf16 case {name} H={H} W={W} B={B} driver={driver}")
@@ -102,7 +102,7 @@ def test_bf16_small_decode_encode(name, H, W, B, driver):
     log(compare(got_e, ref, table, cfg["K"], tol=BF16_TOL))
 
 
-@pytest.mark.parametrize("driver", ["graph", "persistent", "dataflow"])
+@pytest.mark.parametrize("driver", ["graph", "persistent", "dataflow", "resident"])
 @pytest.mark.parametrize("name,H,W,B", [
     ("minnen-kodak-48x32-m192", 32, 48, 1),
     ("cheng-gmm3-1080p-120x68-m192", 14, 24, 1),
@@ -117,7 +117,7 @@ def test_bf16_reduced_global(name, H, W, B, driver):
     log(compare(got, ref, table, cfg["K"], tol=BF16_TOL))
 
 
-@pytest.mark.parametrize("driver", ["graph", "persistent", "dataflow"])
+@pytest.mark.parametrize("driver", ["graph", "persistent", "dataflow", "resident"])
 @pytest.mark.parametrize("name,H,W", WIDE)
 def test_bf16_wide_global(name, H, W, driver):
     log(f"bf16 case {name} wide H={H} W={W} driver={driver}")
@@ -136,7 +136,7 @@ def test_bf16_wide_global(name, H, W, driver):
         log(compare(got_e, ref, table, cfg["K"], tol=BF16_TOL))
 
 
-@pytest.mark.parametrize("driver", ["graph", "persistent", "dataflow"])
+@pytest.mark.parametrize("driver", ["graph", "persistent", "dataflow", "resident"])
 def test_bf16_4k_full_size(driver):
     # the 3840x2160 workload (240x135 latents, M = 320) at its full size: the
     # top rows against the bf16 oracle's decode of them, teacher-forced

@@ -88,7 +88,7 @@ SMALL = [
 ]
 
 
-DRIVERS = ["stream", "graph", "persistent", "dataflow"]
+DRIVERS = ["stream", "graph", "persistent", "dataflow", "resident"]
 
 
 @pytest.mark.parametrize("driver", DRIVERS)
@@ -128,7 +128,7 @@ def test_full_decode_encode(name, driver):
     ("minnen-relaxed-b8-120x68-m192", 9, 16, 8),
     ("minnen-hr-4k-240x135-m320", 9, 20, 1),
 ])
-@pytest.mark.parametrize("driver", ["graph", "persistent", "dataflow"])
+@pytest.mark.parametrize("driver", ["graph", "persistent", "dataflow", "resident"])
 def test_reduced_global(name, H, W, B, driver):
     log(f"case {name} reduced H={H} W={W} B={B} driver={driver}")
     cfg, w, table, psi, sym = make_case(name, H=H, W=W, B=B)
@@ -138,7 +138,7 @@ def test_reduced_global(name, H, W, B, driver):
 
 
 @pytest.mark.parametrize("name,H,W", WIDE)
-@pytest.mark.parametrize("driver", ["graph", "persistent", "dataflow"])
+@pytest.mark.parametrize("driver", ["graph", "persistent", "dataflow", "resident"])
 def test_wide_global(name, H, W, driver):
     # every output of a decode whose wavefronts span three row tiles
     log(f"case {name} wide H={H} W={W} driver={driver}")
@@ -160,7 +160,7 @@ def test_wide_global(name, H, W, driver):
     ("minnen-relaxed-b8-120x68-m192", 600),
     ("minnen-hr-4k-240x135-m320", 300),
 ])
-@pytest.mark.parametrize("driver", ["graph", "persistent", "dataflow"])
+@pytest.mark.parametrize("driver", ["graph", "persistent", "dataflow", "resident"])
 def test_full_size_teacher_forced(name, n, driver):
     rows = TOP_ROWS[name]
     log(f"case {name} full size, top {rows} rows + teacher-forced sample of {n}, driver={driver}")
@@ -195,4 +195,28 @@ def test_graph_replays_match_and_reuse_plan():
         plan.sync()
         assert np.array_equal(s.cpu().numpy(), sym)
         compare(to_np(out_e), ref, table, cfg["K"])
+    plan.close()
+
+
+@pytest.mark.parametrize("driver", ["graph", "persistent", "dataflow", "resident"])
+def test_consecutive_calls_with_new_inputs(driver):
+    # one plan, the same output buffers, two decodes of different symbols
+    # (and an encode in between): nothing of an earlier call may be read back
+    # as current data by a later one
+    cfg, w, table, psi, sym = make_case("minnen-hr-4k-240x135-m320", H=9, W=20)
+    sym2 = inputs.make_symbols(cfg["B"], cfg["H"], cfg["W"], cfg["M"], cfg["lap_b"], cfg["clip"], seed=7)
+    model = oracle_model(cfg, w, table)
+    refs = [model.decode(psi, s) for s in (sym, sym2)]
+    plan = gpu_plan(cfg, w, table, driver)
+    out = plan.alloc_out()
+    psi_d = torch.from_numpy(psi).cuda()
+    for rep in range(2):
+        for s, ref in zip((sym, sym2), refs):
+            plan.decode(psi_d, torch.from_numpy(s).cuda(), out=out)
+            plan.sync()
+            log(compare(to_np(out), ref, table, cfg["K"]))
+        y = inputs.encoder_input(sym, inputs.make_noise(cfg["B"], cfg["H"], cfg["W"], cfg["M"]), refs[0]["mean"])
+        _, s_out = plan.encode(psi_d, torch.from_numpy(y).cuda(), out=out)
+        plan.sync()
+        assert np.array_equal(s_out.cpu().numpy(), sym)
     plan.close()
