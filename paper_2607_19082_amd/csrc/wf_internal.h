@@ -96,6 +96,8 @@ struct ResArgs {
     float* ctx;                 // [ntasks][parts] x (16 x 2M) old-tap context k-parts of each task
     void* h1;                   // [ntasks] x (16 x Np1) layer-1 output of each task (tile order)
     void* h2;                   // [ntasks] x (16 x Np2) layer-2 output of each task
+    void* ytile;                // [ntasks] x (16 x M) y_hat of each task's latents (tile order; bf16: pairs),
+                                // the source of the next step's new taps
     int* err;
     long long budget;
     long long* stamps;          // optional trace: 3 wall-clock ticks per task and workgroup

@@ -97,6 +97,7 @@ __device__ __forceinline__ ResArgs uni_args(const ResArgs& x) {
     ResArgs r;
 #define WF_U(f) r.f = uni(x.f)
     WF_U(per_slot); WF_U(parts); WF_U(nrep); WF_U(nbands); WF_U(nbs); WF_U(cnt); WF_U(kbase); WF_U(ctx); WF_U(h1); WF_U(h2);
+    WF_U(ytile);
     WF_U(err);
     WF_U(stamps); WF_U(ntasks);
     for (int q = 0; q <= kResRoles; ++q) WF_U(first[q]);
@@ -316,6 +317,51 @@ __device__ __forceinline__ void for_tasks(const StepArgs& a, int T, int rep, int
     }
 }
 
+// Where the two new taps of one lane's row come from.  Both were decoded at
+// the step before (they are one step old): the left tap (0, -1) in the same
+// grid row, so row r of the band's task there; the upper tap (-1, new_dx0)
+// in grid row i-1, so row r-1 of that task or, for r = 0, row 15 of the task
+// of the band above.  Layer 3 keeps each task's y_hat as a 16 x M tile (tile
+// order; bf16 as pairs), so a new-tap k-block is one 1 KB tile block read.
+// Taps outside the grid (and rows without a latent) read zero.
+struct NewSrc {
+    size_t base[2];   // element offset of the source tile block of each tap
+    bool ok[2];
+};
+// kself / kup: the band's task and the band above's task at step t-1 (-1: none).
+template <class P>
+__device__ __forceinline__ NewSrc new_src(const StepArgs& a, const Row& w, int kself, int kup) {
+    const int rr = threadIdx.x & 15;
+    NewSrc n;
+#pragma unroll
+    for (int tap = 0; tap < 2; ++tap) {
+        const int ii = w.i + tap - 1, jj = w.j + (tap ? -1 : a.new_dx0);
+        const int kt = (tap == 1 || rr > 0) ? kself : kup;
+        const int row = tap == 1 ? rr : (rr + 15) & 15;
+        n.ok[tap] = w.valid && ii >= 0 && jj >= 0 && jj < a.W && kt >= 0;
+        // one task's tile: 16 x M values (bf16: pairs of halves)
+        const size_t tb = (size_t)(kt >= 0 ? kt : 0) * kTile * a.M * (P::kBf16 ? 2 : 1);
+        n.base[tap] = tb + tile_idx<P>(row, 0, a.M);
+    }
+    return n;
+}
+// k-block kb (of the 2 M new-tap channels) of the lane's row.
+template <class P>
+__device__ __forceinline__ typename P::A ld_new_tap(const ResArgs& r, const NewSrc& n, int M, int kb) {
+    const int tap = kb * P::kK >= M;
+    const int cb = kb - (tap ? M / P::kK : 0);          // k-block within the tap's M channels
+    const int lane = threadIdx.x & 63;
+    if constexpr (P::kBf16) {
+        const uint16_t* y = static_cast<const uint16_t*>(r.ytile);
+        // block cb of the tile row: 1 KB of hi halves, then 1 KB of lo halves
+        const size_t q = n.base[tap] + (size_t)cb * 1024 + (lane >> 4) * 128;
+        return b8x2{ld8h<false>(y, q, n.ok[tap]), ld8h<false>(y, q + 512, n.ok[tap])};
+    } else {
+        return ld4<false>(static_cast<const float*>(r.ytile), n.base[tap] + (size_t)cb * 256 + (lane >> 4) * 64,
+                          n.ok[tap]);
+    }
+}
+
 // Element offset of context part `part` of task k (16 rows x 2M, tile order).
 __device__ __forceinline__ size_t ctx_base(const StepArgs& a, const ResArgs& r, int k, int part) {
     return ((size_t)k * r.parts + part) * kTile * 2 * a.M;
@@ -410,18 +456,18 @@ __device__ __noinline__ void res_l1(const StepArgs& a_in, const ResArgs& r_in, i
         s.load(a.wp_l1, kbn + kbc, c, 0);
     }
     const size_t h1s = (size_t)kTile * a.Np1 * 4;     // bytes of one task's h1
-    const float* yhat = P::kBf16 ? nullptr : uni(a.cp->y_hat);   // read once
     for_tasks(a, T, rep, r.nrep, [&](int t, int b, int beta, int k) {
         const int bs = b * r.nbands + beta;
         // the epilogue operand (hoisted before the launch) first
         const Row v = band_row(a, b, beta, t, ro);
         const float z = ld1<false>(a.p1, v.lat * a.Np1 + col, v.valid);
         res_stamp(r, k, 0);
-        if (!res_wait(r, ResWait{RR_CTXL, k}, ResWait{RR_C0, band_task(a, r, b, beta, t - 1)},
-                      ResWait{RR_C0, band_task(a, r, b, beta - 1, t - 1)}, bail))
+        const int kself = band_task(a, r, b, beta, t - 1), kup = band_task(a, r, b, beta - 1, t - 1);
+        if (!res_wait(r, ResWait{RR_CTXL, k}, ResWait{RR_C0, kself}, ResWait{RR_C0, kup}, bail))
             return false;
         res_stamp(r, k, 1);
         const Row w = band_row(a, b, beta, t, lane & 15);
+        const NewSrc ns = new_src<P>(a, w, kself, kup);
         f4 acc[1] = {zero4()};
         if constexpr (P::kBf16) {
             const int sn = __builtin_amdgcn_readfirstlane(s.n), skb0 = __builtin_amdgcn_readfirstlane(s.kb0);
@@ -429,7 +475,7 @@ __device__ __noinline__ void res_l1(const StepArgs& a_in, const ResArgs& r_in, i
                 b8x2 av[ResKb<P>::a];
 #pragma unroll
                 for (int u = 0; u < ResKb<P>::a; ++u)
-                    if (u < sn) av[u] = ld_tap_from<PBF16, false>(a, nullptr, w, skb0 + u, kq, false);
+                    if (u < sn) av[u] = ld_new_tap<PBF16>(r, ns, M, skb0 + u);
 #pragma unroll
                 for (int u = 0; u < ResKb<P>::a; ++u)
                     if (u < sn) {
@@ -455,7 +501,7 @@ __device__ __noinline__ void res_l1(const StepArgs& a_in, const ResArgs& r_in, i
             }
         } else {
             wdot(s, [&](int kb) -> f4 {
-                if (kb < kbn) return ld_tap_from<PF32, false>(a, yhat, w, kb, kq, false);
+                if (kb < kbn) return ld_new_tap<PF32>(r, ns, M, kb);
                 // the old-tap context: the last part's buffer holds the sum
                 return ld_tile<PF32, false>(r.ctx + ctx_base(a, r, k, r.parts - 1), 0, 2 * M, kb - kbn, w.valid);
             }, acc);
@@ -594,6 +640,8 @@ __device__ __noinline__ void res_l3(const StepArgs& a_in, const ResArgs& r_in, i
                 cp->mean[oq] = mu;
                 st1<true>(cp->y_hat, oq, sv + mu);
                 if constexpr (P::kBf16) st_pair_row<true>(a.ybf, v.lat * 2 * M, ch, sv + mu);
+                // the task's tile of y_hat, the next step's new taps
+                st_tile<P, true>(static_cast<char*>(r.ytile) + (size_t)k * kTile * M * 4, ro, M, ch, sv + mu);
             }
         }
         res_signal(r, MEAN ? RR_C0 : RR_C1, k);
@@ -739,11 +787,13 @@ int build_resident(Plan& p) {
     if (std::max(ctx_n, std::max(h1_n, h2_n)) * 4 >= (size_t)kBufBytes)
         return fail(WF_E_UNSUPPORTED, "resident driver: per-task buffers exceed the 2 GiB buffer window");
     if ((rc = res_alloc(p, &r.ctx, ctx_n)) != WF_OK) return rc;
-    float *h1 = nullptr, *h2 = nullptr;
+    float *h1 = nullptr, *h2 = nullptr, *yt = nullptr;
     if ((rc = res_alloc(p, &h1, h1_n)) != WF_OK) return rc;
     if ((rc = res_alloc(p, &h2, h2_n)) != WF_OK) return rc;
+    if ((rc = res_alloc(p, &yt, nt * kTile * M)) != WF_OK) return rc;
     r.h1 = h1;
     r.h2 = h2;
+    r.ytile = yt;
     r.err = p.d_err;
     r.budget = p.spin_budget;
     // one workgroup per compute unit, all resident at once
