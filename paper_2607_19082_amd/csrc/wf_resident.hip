@@ -362,6 +362,87 @@ __device__ __forceinline__ typename P::A ld_new_tap(const ResArgs& r, const NewS
     }
 }
 
+// The old-tap gathers of a context slice.  A wave's k-blocks [kb0, kb0 + n)
+// cover at most kResSeg consecutive taps (segments); per task each lane
+// computes one byte offset per segment, and k-block u of the wave then reads
+// at off[seg(u)] + u * (bytes per k-block): the address arithmetic of a load
+// is a select and an add.  Lanes whose tap lies outside the grid (or whose
+// row has no latent) get an offset at or past the end of the buffer window,
+// which the buffer unit answers with zeros.
+constexpr int kResSeg = 4;
+template <class P>
+struct OldSrc {
+    static constexpr int kKbBytes = P::kBf16 ? 128 : 64;   // one k-block of one row (bf16: hi and lo halves)
+    // first wave k-block of segments 1-3 (uniform); the lane's byte offset of
+    // segment 0 minus u * kKbBytes, and of segment q the difference to q - 1.
+    // (Masked sums, not selects: the compiler turns a select chain over these
+    // fields into a load through scratch memory.)
+    int us1, us2, us3;
+    int o0, d1, d2, d3;
+    __device__ __forceinline__ int at(int u) const {
+        return o0 + (d1 & -(int)(u >= us1)) + (d2 & -(int)(u >= us2)) + (d3 & -(int)(u >= us3)) + u * kKbBytes;
+    }
+};
+// Row and column offset of old tap `tap` (taps in row-major order from row -R).
+__device__ __forceinline__ void old_tap_dydx(const StepArgs& a, int tap, int& dy, int& dx) {
+    static_assert(kMaxRadius == 3, "rows -3..0");
+    const int row = tap < a.old_start[0] ? 0 : (tap < a.old_start[1] ? 1 : (tap < a.old_start[2] ? 2 : 3));
+    const int first = row == 0 ? 0 : (row == 1 ? a.old_start[0] : (row == 2 ? a.old_start[1] : a.old_start[2]));
+    dy = row - a.R;
+    dx = tap - first - a.R;
+}
+// kb0: the wave's first old-tap k-block (uniform); w: the lane's row.
+template <class P>
+__device__ __forceinline__ OldSrc<P> old_src(const StepArgs& a, const Row& w, int kb0) {
+    const int M = a.M, tapkb = M / P::kK, kq = (threadIdx.x & 63) >> 4;
+    const int tap0 = kb0 / tapkb;
+    int us[kResSeg], off[kResSeg];
+#pragma unroll
+    for (int q = 0; q < kResSeg; ++q) {
+        const int tap = min(tap0 + q, a.n_old - 1);
+        // (past the wave's range when tap0 + q is past the taps)
+        us[q] = q == 0 ? 0 : (tap0 + q) * tapkb - kb0;
+        int dy, dx;
+        old_tap_dydx(a, tap, dy, dx);
+        const int ii = w.i + dy, jj = w.j + dx;
+        const bool ok = w.valid && ii >= 0 && jj >= 0 && jj < a.W;
+        const int lat = ok ? (w.b * a.H + ii) * a.W + jj : 0;
+        // element of the lane's first channel of the tap's k-block kb0 (may
+        // be negative for q > 0; the segment's own k-blocks are not)
+        int e;
+        if constexpr (P::kBf16)
+            e = lat * 2 * M + (kb0 - tap * tapkb) * 64 + kq * 8;    // pairs: 32 hi, 32 lo per k-block
+        else
+            e = lat * M + (kb0 - tap * tapkb) * P::kK + kq * 4;
+        off[q] = ok ? e * (P::kBf16 ? 2 : 4) : kBufBytes - us[q] * OldSrc<P>::kKbBytes;
+    }
+    OldSrc<P> o;
+    o.us1 = us[1]; o.us2 = us[2]; o.us3 = us[3];
+    o.o0 = off[0]; o.d1 = off[1] - off[0]; o.d2 = off[2] - off[1]; o.d3 = off[3] - off[2];
+    return o;
+}
+// acc += the wave's old-tap k-blocks x its weight slice, all loads issued
+// before the first MFMA.
+template <class P, int KB>
+__device__ __forceinline__ void wdot_old(const WSlice<P, KB, 1>& s, const void* src, OldSrc<P> os, f4 (&acc)[1]) {
+    const int n = __builtin_amdgcn_readfirstlane(s.n);
+    const auto rs = rsrc(src);
+    typename P::A av[KB];
+#pragma unroll
+    for (int u = 0; u < KB; ++u)
+        if (u < n) {
+            const int off = os.at(u);
+            if constexpr (P::kBf16)
+                av[u] = b8x2{__builtin_bit_cast(b8, __builtin_amdgcn_raw_buffer_load_b128(rs, off, 0, 0)),
+                             __builtin_bit_cast(b8, __builtin_amdgcn_raw_buffer_load_b128(rs, off + 64, 0, 0))};
+            else
+                av[u] = __builtin_bit_cast(f4, __builtin_amdgcn_raw_buffer_load_b128(rs, off, 0, 0));
+        }
+#pragma unroll
+    for (int u = 0; u < KB; ++u)
+        if (u < n) acc[0] = P::mma(av[u], s.w[u][0], acc[0]);
+}
+
 // Element offset of context part `part` of task k (16 rows x 2M, tile order).
 __device__ __forceinline__ size_t ctx_base(const StepArgs& a, const ResArgs& r, int k, int part) {
     return ((size_t)k * r.parts + part) * kTile * 2 * a.M;
@@ -370,7 +451,7 @@ __device__ __forceinline__ size_t ctx_base(const StepArgs& a, const ResArgs& r, 
 // ---------------------------------------------------------------------------
 // CTX(c, p) / CTXL(c): ctx[p][r][n] = sum over part p's old-tap k-blocks of
 // taps x Wc; the last part (LAST) stores the sum over all parts.
-template <class P, bool R3, bool LAST>
+template <class P, bool LAST>
 __device__ __noinline__ void res_ctx(const StepArgs& a_in, const ResArgs& r_in, int T, int q, int rep, f4 (*red)[64],
                                      int* bail) {
     const StepArgs a = uni_args(a_in);
@@ -385,8 +466,10 @@ __device__ __noinline__ void res_ctx(const StepArgs& a_in, const ResArgs& r_in, 
     s.load(a.wp_old, nkb, c, 0);
     const int ro = kq * 4 + wave, col = c * kTile + (lane & 15);
     const size_t pstride = (size_t)kTile * 2 * a.M;
-    // the call's reconstruction, read once (not once per k-block)
-    const float* yhat = P::kBf16 ? nullptr : uni(a.cp->y_hat);
+    // the tap source, read once (not once per k-block): the call's
+    // reconstruction (bf16: its pair copy)
+    const void* src = P::kBf16 ? static_cast<const void*>(a.ybf) : static_cast<const void*>(uni(a.cp->y_hat));
+    const int skb0 = __builtin_amdgcn_readfirstlane(s.kb0);
     for_tasks(a, T, rep, r.nrep, [&](int t, int b, int beta, int k) {
         res_stamp(r, k, 0);
         if (!res_wait(r, ResWait{RR_C0, band_task(a, r, b, beta, t - 2)},
@@ -402,9 +485,10 @@ __device__ __noinline__ void res_ctx(const StepArgs& a_in, const ResArgs& r_in, 
                 prev += ld1<false>(r.ctx, e + p2 * pstride, p2 < r.parts - 1);
         }
         const Row w = band_row(a, b, beta, t, lane & 15);
+        const OldSrc<P> os = old_src<P>(a, w, skb0);
         f4 acc[1] = {zero4()};
-        // two load batches: the registers hold the weights
-        wdot<P, KB, 1, KB / 2>(s, [&](int kb) { return ld_tap_from<P, false, R3>(a, yhat, w, kb, kq, true); }, acc);
+        // one load batch (the registers hold the weights and all of them)
+        wdot_old<P, KB>(s, src, os, acc);
         float v[1];
         wreduce<1>(red, acc, v);
         st1<true>(r.ctx, e + part * pstride, v[0] + prev);
@@ -680,12 +764,10 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2))
     const int sl = q % nsl, rep = q / nsl;
     switch (role) {
     case RR_CTX:
-        if (a.R == kMaxRadius) res_ctx<P, true, false>(a, r, T, sl, rep, red, &bail);
-        else res_ctx<P, false, false>(a, r, T, sl, rep, red, &bail);
+        res_ctx<P, false>(a, r, T, sl, rep, red, &bail);
         break;
     case RR_CTXL:
-        if (a.R == kMaxRadius) res_ctx<P, true, true>(a, r, T, sl, rep, red, &bail);
-        else res_ctx<P, false, true>(a, r, T, sl, rep, red, &bail);
+        res_ctx<P, true>(a, r, T, sl, rep, red, &bail);
         break;
     case RR_A: res_l1<P>(a, r, T, sl, rep, red, &bail); break;
     case RR_B: res_l2<P>(a, r, T, sl, rep, red, &bail); break;
@@ -743,6 +825,18 @@ int build_resident(Plan& p) {
     // spare slots take more context parts (shorter context tasks)
     while (kResRep * (crit + nct * (parts + 1)) <= slots && parts < kResMaxParts && nkb_old / (parts + 1) >= kWaves)
         ++parts;
+    // a wave's old-tap k-blocks must lie in at most kResSeg taps
+    {
+        const int tapkb = M / kk;
+        for (int q = 0; q < parts; ++q) {
+            const int lo = nkb_old * q / parts, hi = nkb_old * (q + 1) / parts, per = ceil_div(hi - lo, kWaves);
+            for (int wv = 0; wv < kWaves; ++wv) {
+                const int k0 = std::min(hi, lo + wv * per), k1 = std::min(hi, k0 + per);
+                if (k1 > k0 && (k1 - 1) / tapkb - k0 / tapkb + 1 > kResSeg)
+                    return fail(WF_E_UNSUPPORTED, "resident driver: a context slice spans too many taps (M too small)");
+            }
+        }
+    }
     r.parts = parts;
     r.nrep = kResRep;
     const int n[kResRoles] = {nct * (parts - 1), nct, p.Np1 / kTile, p.Np2 / kTile, G, G};
