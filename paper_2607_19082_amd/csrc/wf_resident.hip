@@ -345,22 +345,6 @@ __device__ __forceinline__ NewSrc new_src(const StepArgs& a, const Row& w, int k
     }
     return n;
 }
-// k-block kb (of the 2 M new-tap channels) of the lane's row.
-template <class P>
-__device__ __forceinline__ typename P::A ld_new_tap(const ResArgs& r, const NewSrc& n, int M, int kb) {
-    const int tap = kb * P::kK >= M;
-    const int cb = kb - (tap ? M / P::kK : 0);          // k-block within the tap's M channels
-    const int lane = threadIdx.x & 63;
-    if constexpr (P::kBf16) {
-        const uint16_t* y = static_cast<const uint16_t*>(r.ytile);
-        // block cb of the tile row: 1 KB of hi halves, then 1 KB of lo halves
-        const size_t q = n.base[tap] + (size_t)cb * 1024 + (lane >> 4) * 128;
-        return b8x2{ld8h<false>(y, q, n.ok[tap]), ld8h<false>(y, q + 512, n.ok[tap])};
-    } else {
-        return ld4<false>(static_cast<const float*>(r.ytile), n.base[tap] + (size_t)cb * 256 + (lane >> 4) * 64,
-                          n.ok[tap]);
-    }
-}
 
 // The old-tap gathers of a context slice.  A wave's k-blocks [kb0, kb0 + n)
 // cover at most kResSeg consecutive taps (segments); per task each lane
@@ -505,7 +489,7 @@ __device__ __noinline__ void res_l1(const StepArgs& a_in, const ResArgs& r_in, i
     const ResArgs r = uni_args(r_in);
     const int lane = threadIdx.x & 63, kq = lane >> 4, wave = wave_id();
     const int M = a.M, ro = kq * 4 + wave, col = c * kTile + (lane & 15);
-    const int kbn = kMaxNew * M / P::kK, kbc = 2 * M / P::kK;
+    const int kbn = kMaxNew * M / P::kK, kbc = 2 * M / P::kK, tapkb = M / P::kK;
     WSlice<P, ResKb<P>::a, 1> s;     // fp32: [F_new ; W1b]; bf16: F_new hi (new taps) or W1b (context)
     WSlice<P, ResKb<P>::a, 1> slo;   // bf16: F_new lo (new taps)
     // bf16: the new-tap and the context k-ranges are both 2M long; waves 0-1
@@ -556,10 +540,15 @@ __device__ __noinline__ void res_l1(const StepArgs& a_in, const ResArgs& r_in, i
         if constexpr (P::kBf16) {
             const int sn = __builtin_amdgcn_readfirstlane(s.n), skb0 = __builtin_amdgcn_readfirstlane(s.kb0);
             if (isnew) {
+                // the wave's k-blocks are those of one tap (two waves, two taps)
+                const int tap = skb0 >= tapkb;
+                const uint16_t* y = static_cast<const uint16_t*>(r.ytile);
+                const size_t e = (tap ? ns.base[1] : ns.base[0]) + (size_t)(skb0 - tap * tapkb) * 1024 + kq * 128;
+                const bool ok = tap ? ns.ok[1] : ns.ok[0];
                 b8x2 av[ResKb<P>::a];
 #pragma unroll
                 for (int u = 0; u < ResKb<P>::a; ++u)
-                    if (u < sn) av[u] = ld_new_tap<PBF16>(r, ns, M, skb0 + u);
+                    if (u < sn) av[u] = b8x2{ld8h<false>(y, e + u * 1024, ok), ld8h<false>(y, e + u * 1024 + 512, ok)};
 #pragma unroll
                 for (int u = 0; u < ResKb<P>::a; ++u)
                     if (u < sn) {
@@ -584,11 +573,34 @@ __device__ __noinline__ void res_l1(const StepArgs& a_in, const ResArgs& r_in, i
                     if (u < sn) acc[0] = PBF16::mma(split8(raw[u][0], raw[u][1]), s.w[u][0], acc[0]);
             }
         } else {
-            wdot(s, [&](int kb) -> f4 {
-                if (kb < kbn) return ld_new_tap<PF32>(r, ns, M, kb);
-                // the old-tap context: the last part's buffer holds the sum
-                return ld_tile<PF32, false>(r.ctx + ctx_base(a, r, k, r.parts - 1), 0, 2 * M, kb - kbn, w.valid);
-            }, acc);
+            // the 4 M k-values split into four equal shares, so each wave's
+            // k-blocks are those of one new tap or of half the old-tap
+            // context (the last part's buffer holds its sum): one base, and
+            // block u 1 KB further
+            const int skb0 = __builtin_amdgcn_readfirstlane(s.kb0);
+            const float* src;
+            size_t e;
+            bool ok;
+            if (skb0 < kbn) {
+                const int tap = skb0 >= tapkb;
+                src = static_cast<const float*>(r.ytile);
+                e = (tap ? ns.base[1] : ns.base[0]) + (size_t)(skb0 - tap * tapkb) * 256 + kq * 64;
+                ok = tap ? ns.ok[1] : ns.ok[0];
+            } else {
+                src = r.ctx;
+                e = ctx_base(a, r, k, r.parts - 1) + (size_t)(skb0 - kbn) * 256 + lane * 4;
+                ok = w.valid;
+            }
+            const int off = ok ? (int)(e * 4) : kBufBytes;   // (past the window: zeros)
+            const int n = __builtin_amdgcn_readfirstlane(s.n);
+            const auto rs = rsrc(src);
+            f4 av[ResKb<P>::a];
+#pragma unroll
+            for (int u = 0; u < ResKb<P>::a; ++u)
+                if (u < n) av[u] = __builtin_bit_cast(f4, __builtin_amdgcn_raw_buffer_load_b128(rs, off + u * 1024, 0, 0));
+#pragma unroll
+            for (int u = 0; u < ResKb<P>::a; ++u)
+                if (u < n) acc[0] = PF32::mma(av[u], s.w[u][0], acc[0]);
         }
         float o[1];
         wreduce<1>(red, acc, o);
