@@ -7,9 +7,16 @@ y_hat write, plus the pre-loop hyperprior product.  Inputs are seeded
 synthetic arrays (weights N(0, 1/fan_in), hyperprior params N(0, 1), Laplace
 symbols) already resident in HBM.  Prints one JSON line.
 
-roofline: one decode is one launch of the plan's HIP graph (graph driver: the
-hoist, two context kernels and one kernel per phase of every step) or of
-k_persistent (persistent driver), timed with HIP events on the launch stream;
+The default driver is the resident one (one cooperative k_resident launch per
+decode, each workgroup's weight slice held in registers for the whole decode);
+--driver picks another, and the context approximation (--group > 1) runs on
+the graph driver.
+
+roofline: one decode is one decode call (resident driver: counter reset,
+hoist and the k_resident launch, which takes nearly all of it), one launch of
+the plan's HIP graph (graph driver: the hoist, two context kernels and one
+kernel per phase of every step) or of k_persistent (persistent driver), timed
+with HIP events on the launch stream;
 achieved = algorithmic FLOPs of a decode / that time, against the dense fp32
 (or bf16) MFMA peak.  traffic = HBM bytes of one decode from the committed
 rocprofv3 FETCH_SIZE / WRITE_SIZE summary for this workload, precision and
@@ -41,7 +48,7 @@ CSRC = os.path.join(ROOT, "paper_2607_19082_amd", "csrc")
 PROFILES = os.path.join(ROOT, "profiles")
 # kernels of one decode call (the rest of a bench run: the floor probes, torch)
 DECODE_KERNELS = ("wf::k_phase", "wf::k_hoist", "wf::k_ctxo", "wf::k_set_call", "wf::k_persistent", "wf::k_zero_u32",
-                  "wf::k_dataflow", "wf::k_zero_u128")
+                  "wf::k_dataflow", "wf::k_zero_u128", "wf::k_resident", "wf::k_res_zero")
 
 
 # kernels of the bench's per-step latency leg (one traced decode by the
@@ -519,7 +526,8 @@ def main():
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--workload", default=DEFAULT_WORKLOAD)
-    ap.add_argument("--driver", default="graph", choices=["stream", "graph", "persistent", "dataflow", "resident"])
+    ap.add_argument("--driver", default=None, choices=["stream", "graph", "persistent", "dataflow", "resident"],
+                    help="decode driver (default: resident; graph for --group > 1)")
     ap.add_argument("--precision", default="fp32", choices=["fp32", "bf16"])
     ap.add_argument("--mask", default=None, choices=sorted(MASK_TAPS),
                     help="causal mask (default: the workload's own), weights drawn for its kernel size")
@@ -548,6 +556,8 @@ def main():
                     help="latency floor of an unprofiled bench run for --summarize-stats' step histograms")
     ap.add_argument("--command", default="", help="the commands that made the counter outputs (recorded)")
     args = ap.parse_args()
+    if args.driver is None:
+        args.driver = "resident" if args.group <= 1 else "graph"
     if args.copy_calibration:
         copy_calibration(args.cal_bytes)
         return
@@ -628,11 +638,12 @@ def main():
                               "histogram is in its committed kernel-trace summary)",
                     **persistent_step_latency(w, table, cfg, args.precision, psi_d, sym_d, lfloor, torch, wf)}
 
-    # the decode that reads every symbol from its rANS stream inside the step loop
+    # the decode that reads every symbol from its rANS stream inside the step
+    # loop (on the per-step kernels: the graph driver unless stream is timed)
     rec_ec = None
-    if not args.no_entropy and cfg["K"] == 1 and args.group <= 1 and args.driver in ("stream", "graph"):
+    if not args.no_entropy and cfg["K"] == 1 and args.group <= 1:
         pe = wf.Plan(w, table, cfg["H"], cfg["W"], cfg["B"], cfg["K"], mask=mask_of(cfg), precision=args.precision,
-                     driver=args.driver, entropy_coder="rans")
+                     driver="stream" if args.driver == "stream" else "graph", entropy_coder="rans")
         u = inputs.make_noise(cfg["B"], cfg["H"], cfg["W"], cfg["M"])
         bits = torch.zeros((2 + 4 * cfg["W"]) * cfg["B"] * cfg["H"] * cfg["M"], dtype=torch.int32, device="cuda")
         out_b = pe.alloc_out()
