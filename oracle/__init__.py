@@ -15,7 +15,9 @@ and this package never imports the GPU path.
   Gaussian model (Sec. II-A; the coder the paper pairs with the wavefront
   decode, Sec. III-C): per-level frequency tables built from the scale
   table, one stream per (image, grid row, channel), and the model decode that
-  takes its symbols from those streams.
+  takes its symbols from those streams; for the 3-component mixture model,
+  the same streams with per-latent mixture frequencies built in integer
+  arithmetic from quantised parameters.
 * ``schedule.py`` -- the dependency DAG of the mask (Eq. 3, Def. 1), its ASAP
   levels and critical path, and a brute-force search over linear schedules
   (Sec. III-B, Eq. 5-7; Appendix A, Thm. 1).
@@ -94,6 +96,19 @@ def _load():
         lib.oracle_rans_decode.argtypes = [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p] + [ctypes.c_int] * 4 + [
             ctypes.c_void_p, ctypes.c_int, ctypes.c_void_p]
         lib.oracle_rans_decode.restype = ctypes.c_int
+        lib.oracle_mix_tables.argtypes = [ctypes.c_void_p, ctypes.c_int, ctypes.c_void_p, ctypes.c_void_p,
+                                          ctypes.c_void_p, ctypes.c_int64]
+        lib.oracle_mix_tables.restype = ctypes.c_int64
+        lib.oracle_mix_encode.argtypes = [ctypes.c_void_p] * 5 + [ctypes.c_int] * 4 + [
+            ctypes.c_void_p, ctypes.c_int, ctypes.c_void_p, ctypes.c_int64, ctypes.c_void_p]
+        lib.oracle_mix_encode.restype = ctypes.c_int64
+        lib.oracle_mix_decode.argtypes = [ctypes.c_void_p] * 6 + [ctypes.c_int] * 4 + [
+            ctypes.c_void_p, ctypes.c_int, ctypes.c_void_p]
+        lib.oracle_mix_decode.restype = ctypes.c_int
+        lib.oracle_mix_latent.argtypes = [ctypes.c_void_p, ctypes.c_int, ctypes.c_void_p, ctypes.c_void_p,
+                                          ctypes.c_float, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p,
+                                          ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int64]
+        lib.oracle_mix_latent.restype = ctypes.c_int
         _lib = lib
     return _lib
 
@@ -193,7 +208,8 @@ class Model:
 
     def decode_bits(self, psi, bits, offsets):
         """Decode with the symbols read from rANS streams (``rans_encode``'s
-        layout); K = 1.  Returns (outputs, decoded symbols)."""
+        layout for K = 1, ``mix_encode``'s for K = 3).  Returns (outputs,
+        decoded symbols)."""
         psi = _f32(psi)
         bits = np.ascontiguousarray(bits, dtype=np.uint32)
         offsets = np.ascontiguousarray(offsets, dtype=np.uint32)
@@ -276,4 +292,84 @@ def rans_decode(bits, offsets, idx, table):
     if _load().oracle_rans_decode(bits.ctypes.data, offsets.ctypes.data, idx.ctypes.data, B, H, W, M,
                                   table.ctypes.data, len(table), sym.ctypes.data) != 0:
         raise RuntimeError("oracle_rans_decode failed")
+    return sym
+
+
+def mix_tables(table):
+    """The mixture coder's level tables: (X [L], base [L+1], G [base[L]]),
+    G_l(x) for x = -X_l..X_l at base[l] + x + X_l."""
+    table = _f32(table)
+    L = len(table)
+    X = np.zeros(L, np.int32)
+    base = np.zeros(L + 1, np.int64)
+    total = _load().oracle_mix_tables(table.ctypes.data, L, X.ctypes.data, base.ctypes.data, None, 0)
+    if total < 0:
+        raise RuntimeError("oracle_mix_tables failed")
+    G = np.zeros(total, np.uint32)
+    _load().oracle_mix_tables(table.ctypes.data, L, None, None, G.ctypes.data, total)
+    return X, base, G
+
+
+def mix_latent(table, w, cm, mu, lvl):
+    """One latent channel's quantised mixture parameters and cumulative
+    frequencies: dict(v, q, lo, hi, cum) with cum[u] = cum(lo + u), u = 0..S."""
+    table = _f32(table)
+    w = _f32(np.asarray(w).reshape(3))
+    cm = _f32(np.asarray(cm).reshape(3))
+    lvl = np.ascontiguousarray(np.asarray(lvl).reshape(3), dtype=np.int32)
+    v = np.zeros(3, np.uint32)
+    q = np.zeros(3, np.int32)
+    lohi = np.zeros(2, np.int32)
+    cap = 1 << 16
+    cum = np.zeros(cap, np.uint32)
+    S = _load().oracle_mix_latent(table.ctypes.data, len(table), w.ctypes.data, cm.ctypes.data, float(np.float32(mu)),
+                                  lvl.ctypes.data, v.ctypes.data, q.ctypes.data, lohi.ctypes.data, cum.ctypes.data,
+                                  cap)
+    if S < 0:
+        raise RuntimeError("oracle_mix_latent failed")
+    return {"v": v, "q": q, "lo": int(lohi[0]), "hi": int(lohi[1]), "cum": cum[:S + 1].copy()}
+
+
+def _mix_args(weight, cmean, mean, idx):
+    weight = _f32(weight)
+    cmean = _f32(cmean)
+    mean = _f32(mean)
+    idx = np.ascontiguousarray(idx, dtype=np.int32)
+    B, H, W, K, M = weight.shape
+    if K != 3 or cmean.shape != weight.shape or idx.shape != weight.shape or mean.shape != (B, H, W, M):
+        raise ValueError("weight, comp_mean, idx: [B][H][W][3][M]; mean: [B][H][W][M]")
+    return weight, cmean, mean, idx, (B, H, W, M)
+
+
+def mix_encode(sym, weight, cmean, mean, idx, table):
+    """rANS streams of symbols sym [B][H][W][M] under the 3-component mixture
+    of weight, comp_mean, idx [B][H][W][3][M] and mixture mean [B][H][W][M]:
+    one stream per (image, grid row, channel).  Returns (bits, offsets)."""
+    weight, cmean, mean, idx, (B, H, W, M) = _mix_args(weight, cmean, mean, idx)
+    sym = np.ascontiguousarray(sym, dtype=np.int32)
+    table = _f32(table)
+    offsets = np.zeros(B * H * M + 1, np.uint32)
+    lib = _load()
+    args = (sym.ctypes.data, weight.ctypes.data, cmean.ctypes.data, mean.ctypes.data, idx.ctypes.data, B, H, W, M,
+            table.ctypes.data, len(table))
+    total = lib.oracle_mix_encode(*args, None, 0, offsets.ctypes.data)
+    if total < 0:
+        raise RuntimeError("oracle_mix_encode failed")
+    bits = np.zeros(max(int(total), 1), np.uint32)
+    if lib.oracle_mix_encode(*args, bits.ctypes.data, len(bits), offsets.ctypes.data) != total:
+        raise RuntimeError("oracle_mix_encode failed")
+    return bits[:total], offsets
+
+
+def mix_decode(bits, offsets, weight, cmean, mean, idx, table):
+    """Symbols of mixture-coded streams given every latent's parameters."""
+    weight, cmean, mean, idx, (B, H, W, M) = _mix_args(weight, cmean, mean, idx)
+    bits = np.ascontiguousarray(bits, dtype=np.uint32)
+    offsets = np.ascontiguousarray(offsets, dtype=np.uint32)
+    table = _f32(table)
+    sym = np.zeros((B, H, W, M), np.int32)
+    if _load().oracle_mix_decode(bits.ctypes.data, offsets.ctypes.data, weight.ctypes.data, cmean.ctypes.data,
+                                 mean.ctypes.data, idx.ctypes.data, B, H, W, M, table.ctypes.data, len(table),
+                                 sym.ctypes.data) != 0:
+        raise RuntimeError("oracle_mix_decode failed")
     return sym

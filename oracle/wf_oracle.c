@@ -362,25 +362,28 @@ int oracle_run(const oracle_model *m, const float *psi, int32_t *sym,
  * Decode with the symbols taken from rANS streams (wf_rans.c): in raster
  * order, each latent's parameters give its scale indices, and with them the
  * next symbol of the stream of its (image, grid row, channel) is decoded
- * before y_hat = s + mean is written.  K = 1 only.  sym_out receives the
- * decoded symbols.  Returns 0, or -1 on a bad argument or a malformed stream.
+ * before y_hat = s + mean is written (K = 1: the Gaussian of the scale
+ * level; K = 3: the mixture of the three components, wf_rans.c).  sym_out
+ * receives the decoded symbols.  Returns 0, or -1 on a bad argument or a malformed stream.
  */
 int oracle_run_bits(const oracle_model *m, const float *psi, const uint32_t *bits,
                     const uint32_t *offsets, int32_t *sym_out, const oracle_out *out)
 {
     if (!m || !psi || !bits || !offsets || !sym_out || !out || !out->y_hat) return -1;
-    if (m->K != 1) return -1;
+    if (m->K != 1 && m->K != 3) return -1;
+    const int K = m->K;
     const size_t M = m->M;
     const size_t total = (size_t)m->B * m->H * m->W;
     const size_t nstreams = (size_t)m->B * m->H * M;
     rans_tables t;
-    if (rans_tables_build(m->table, m->L, &t)) return -1;
+    mix_tables mt;
+    if (K == 1 ? rans_tables_build(m->table, m->L, &t) : mix_tables_build(m->table, m->L, &mt)) return -1;
     float *scratch = malloc(scratch_floats(m) * sizeof(float));
     float *mu = malloc(M * sizeof(float));
-    float *sigma = malloc(M * sizeof(float));
-    float *weight = malloc(M * sizeof(float));
-    float *cmean = malloc(M * sizeof(float));
-    int32_t *index = malloc(M * sizeof(int32_t));
+    float *sigma = malloc(K * M * sizeof(float));
+    float *weight = malloc(K * M * sizeof(float));
+    float *cmean = malloc(K * M * sizeof(float));
+    int32_t *index = malloc(K * M * sizeof(int32_t));
     rans_dec *dec = malloc(nstreams * sizeof(rans_dec));
     int rc = 0;
     if (!scratch || !mu || !sigma || !weight || !cmean || !index || !dec) rc = -1;
@@ -396,13 +399,23 @@ int oracle_run_bits(const oracle_model *m, const float *psi, const uint32_t *bit
         for (size_t c = 0; c < M; ++c) {
             rans_dec *d = &dec[((size_t)b * m->H + i) * M + c];
             int32_t s;
-            if (rans_dec_symbol(d, &t, index[c], &s)) { rc = -1; break; }
+            if (K == 1) {
+                if (rans_dec_symbol(d, &t, index[c], &s)) { rc = -1; break; }
+            } else {
+                /* the mixture of the channel's three components */
+                const float w3[3] = {weight[c], weight[M + c], weight[2 * M + c]};
+                const float m3[3] = {cmean[c], cmean[M + c], cmean[2 * M + c]};
+                const int32_t l3[3] = {index[c], index[M + c], index[2 * M + c]};
+                mix_param p;
+                if (mix_params(&mt, w3, m3, mu[c], l3, &p) || mix_dec_symbol(d, &mt, &p, &s)) { rc = -1; break; }
+            }
             sym_out[lat * M + c] = s;
             out->y_hat[lat * M + c] = (float)s + mu[c];
         }
     }
     free(scratch); free(mu); free(sigma); free(weight); free(cmean); free(index); free(dec);
-    rans_tables_free(&t);
+    if (K == 1) rans_tables_free(&t);
+    else mix_tables_free(&mt);
     return rc;
 }
 
