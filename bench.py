@@ -520,6 +520,57 @@ def timed_calls(fn, steps, stream, torch):
     return wall, [a.elapsed_time(b) for a, b in ev]
 
 
+GMM_WORKLOAD = "cheng-gmm3-1080p-120x68-m192"
+
+
+def entropy_leg(cfg, w, table, psi_d, sym, mask, precision, driver, steps, stream, torch, wf, inputs):
+    """Time the decode that reads every symbol from its rANS stream (and the
+    stream encoder) on one workload; the streams are those of an encode whose
+    symbols are `sym`, and again of one whose symbols lie in {-1, 0, 1}."""
+    pe = wf.Plan(w, table, cfg["H"], cfg["W"], cfg["B"], cfg["K"], mask=mask, precision=precision, driver=driver,
+                 entropy_coder="rans")
+    u = inputs.make_noise(cfg["B"], cfg["H"], cfg["W"], cfg["M"])
+    bits = torch.zeros((2 + 4 * cfg["W"]) * cfg["B"] * cfg["H"] * cfg["M"], dtype=torch.int32, device="cuda")
+    out_b = pe.alloc_out()
+    sym_b = torch.empty(sym.shape, dtype=torch.int32, device="cuda")
+
+    def measure(sym_np):
+        # encoder input whose symbols are sym_np, then the timed decodes from its streams
+        s_d = torch.from_numpy(sym_np).cuda()
+        m = pe.decode(psi_d, s_d, stream=stream)["mean"]
+        y_d = (torch.from_numpy(sym_np.astype(np.float32) + u).cuda() + m).contiguous()
+        _, sym_e, offs = pe.encode_bits(psi_d, y_d, bits, stream=stream)
+        pe.sync(stream)
+        n_words = int(offs[-1].item())
+        n_enc = max(3, steps // 4)
+        ewall, _ = timed_calls(lambda: pe.encode_bits(psi_d, y_d, bits, stream=stream), n_enc, stream, torch)
+        pe.sync(stream)
+
+        def dec_bits():
+            pe.decode_bits(psi_d, bits, offs, out=out_b, sym_out=sym_b, n_words=n_words, stream=stream)
+
+        dec_bits()
+        pe.sync(stream)
+        bwall, bper = timed_calls(dec_bits, steps, stream, torch)
+        pe.sync(stream)
+        return {"ms_per_image": bwall * 1e3 / steps / cfg["B"], "launch_ms_events": float(np.mean(bper)),
+                "encode_bits_ms_per_image": ewall * 1e3 / n_enc / cfg["B"],
+                "stream_words": n_words, "bits_per_symbol": 32.0 * n_words / sym_np.size,
+                "symbols_match": bool(torch.equal(sym_b, s_d)) and bool(torch.equal(sym_e, s_d))}
+
+    rec = measure(sym)
+    # symbols in {-1, 0, 1} lie inside every latent's coded symbols: no escapes
+    rec["no_escapes"] = measure(np.clip(sym, -1, 1).astype(np.int32))
+    rec["driver"] = driver
+    rec["streams"] = ("one per (image, grid row, channel); 64-bit rANS state, 32-bit words, "
+                      + ("2^-16 Gaussian tables per scale level" if cfg["K"] == 1 else
+                         "2^-16 mixture frequencies per latent from quantised weights, offsets and scale levels")
+                      + "; the workload's symbols do not follow the random model, so many of them escape")
+    pe.close()
+    del bits
+    return rec
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -639,48 +690,33 @@ def main():
                     **persistent_step_latency(w, table, cfg, args.precision, psi_d, sym_d, lfloor, torch, wf)}
 
     # the decode that reads every symbol from its rANS stream inside the step
-    # loop (on the per-step kernels: the graph driver unless stream is timed)
-    rec_ec = None
-    if not args.no_entropy and cfg["K"] == 1 and args.group <= 1:
-        pe = wf.Plan(w, table, cfg["H"], cfg["W"], cfg["B"], cfg["K"], mask=mask_of(cfg), precision=args.precision,
-                     driver="stream" if args.driver == "stream" else "graph", entropy_coder="rans")
-        u = inputs.make_noise(cfg["B"], cfg["H"], cfg["W"], cfg["M"])
-        bits = torch.zeros((2 + 4 * cfg["W"]) * cfg["B"] * cfg["H"] * cfg["M"], dtype=torch.int32, device="cuda")
-        out_b = pe.alloc_out()
-        sym_b = torch.empty_like(sym_d)
-
-        def measure(sym_np):
-            # encoder input whose symbols are sym_np, then the timed decodes from its streams
-            s_d = torch.from_numpy(sym_np).cuda()
-            m = pe.decode(psi_d, s_d, stream=stream)["mean"]
-            y_d = (torch.from_numpy(sym_np.astype(np.float32) + u).cuda() + m).contiguous()
-            _, sym_e, offs = pe.encode_bits(psi_d, y_d, bits, stream=stream)
-            pe.sync(stream)
-            n_words = int(offs[-1].item())
-            n_enc = max(3, args.steps // 4)
-            ewall, _ = timed_calls(lambda: pe.encode_bits(psi_d, y_d, bits, stream=stream), n_enc, stream, torch)
-            pe.sync(stream)
-
-            def dec_bits():
-                pe.decode_bits(psi_d, bits, offs, out=out_b, sym_out=sym_b, n_words=n_words, stream=stream)
-
-            dec_bits()
-            pe.sync(stream)
-            bwall, bper = timed_calls(dec_bits, args.steps, stream, torch)
-            pe.sync(stream)
-            return {"ms_per_image": bwall * 1e3 / args.steps / cfg["B"], "launch_ms_events": float(np.mean(bper)),
-                    "encode_bits_ms_per_image": ewall * 1e3 / n_enc / cfg["B"],
-                    "stream_words": n_words, "bits_per_symbol": 32.0 * n_words / sym_np.size,
-                    "symbols_match": bool(torch.equal(sym_b, s_d)) and bool(torch.equal(sym_e, s_d))}
-
-        rec_ec = measure(sym)
-        # symbols in {-1, 0, 1} lie inside every level's support: no escapes
-        rec_ec["no_escapes"] = measure(np.clip(sym, -1, 1).astype(np.int32))
-        rec_ec["streams"] = ("one per (image, grid row, channel); 64-bit rANS state, 32-bit words, 2^-16 Gaussian "
-                             "tables; the workload's symbols do not follow the random model's scales, so most of "
-                             "them escape")
-        pe.close()
-        del bits
+    # loop (on the per-step kernels: the graph driver unless stream is timed),
+    # for this workload and, when it is another, the 3-component mixture
+    # model at 1080p
+    rec_ec = rec_ec_gmm = None
+    if not args.no_entropy and args.group <= 1:
+        ec_driver = "stream" if args.driver == "stream" else "graph"
+        rec_ec = entropy_leg(cfg, w, table, psi_d, sym, mask_of(cfg), args.precision, ec_driver, args.steps, stream,
+                             torch, wf, inputs)
+        if cfg["K"] == 1:
+            g_cfg, g_w, g_table, g_psi, g_sym = inputs.make_inputs(GMM_WORKLOAD)
+            g_psi_d = torch.from_numpy(g_psi).cuda()
+            rec_ec_gmm = entropy_leg(g_cfg, g_w, g_table, g_psi_d, g_sym, mask_of(g_cfg), args.precision, ec_driver,
+                                     args.steps, stream, torch, wf, inputs)
+            # the same workload's decode from symbols, for comparison
+            gp = wf.Plan(g_w, g_table, g_cfg["H"], g_cfg["W"], g_cfg["B"], g_cfg["K"], mask=mask_of(g_cfg),
+                         precision=args.precision, driver=args.driver)
+            g_out = gp.alloc_out()
+            g_sym_d = torch.from_numpy(g_sym).cuda()
+            gp.decode(g_psi_d, g_sym_d, out=g_out, stream=stream)
+            gp.sync(stream)
+            gwall, _ = timed_calls(lambda: gp.decode(g_psi_d, g_sym_d, out=g_out, stream=stream), args.steps, stream,
+                                   torch)
+            gp.sync(stream)
+            gp.close()
+            rec_ec_gmm["workload"] = GMM_WORKLOAD
+            rec_ec_gmm["decode_from_symbols_ms_per_image"] = gwall * 1e3 / args.steps / g_cfg["B"]
+            rec_ec_gmm["decode_from_symbols_driver"] = args.driver
 
     # the transforms around the decode: hyper-decoder (z_hat -> psi) and
     # synthesis (y_hat -> image), random weights, for an end-to-end timing
@@ -768,6 +804,7 @@ def main():
         "ms_per_image": ms / cfg["B"],
         "encode": rec_enc,
         "entropy_decode": rec_ec,
+        "entropy_decode_gmm": rec_ec_gmm,
         "end_to_end": rec_e2e,
     }
     if args.cpu_rows > 0:

@@ -49,8 +49,9 @@ typedef enum {
 /* Entropy coder of the symbols (wf_desc.entropy_coder). */
 typedef enum {
     WF_EC_NONE = 0,         /* symbols are passed as int32 arrays                      */
-    WF_EC_RANS = 1          /* also wf_encode_bits / wf_decode_bits: rANS streams, K = 1,
-                               stream or graph driver, exact decode (group <= 1)         */
+    WF_EC_RANS = 1          /* also wf_encode_bits / wf_decode_bits: rANS streams (K = 1:
+                               the Gaussian coder, K = 3: the mixture coder), stream or
+                               graph driver, exact decode (group <= 1)                   */
 } wf_entropy_coder;
 
 /* Causal masks (Def. 1: a (2R+1)x(2R+1) kernel keeps the R rows above within
@@ -228,6 +229,17 @@ int wf_encode(wf_plan_t plan, const float *psi, const float *y, int32_t *sym_out
  * f = 1 + floor(p (2^16 - 2 n_l - 2)) for the Gaussian mass p of
  * [s - 1/2, s + 1/2], the remainder added to s = 0.  Coder: 64-bit state in
  * [2^31, 2^63), 32-bit words.
+ * K = 3 (the 3-component mixture): a symbol is coded with the mixture of its
+ * channel's three Gaussians around the mixture mean, with frequencies built
+ * in integer arithmetic from quantised parameters: weights
+ * v_k = 1 + floor(4093 w_k) (the rest of 4096 to the largest), offsets
+ * q_k = rint(16 (mu_k - mu)) in sixteenths of a symbol (within +-2^14), and
+ * per level an integer CDF on sixteenths, G_l(x) = floor(2^20 Phi(x / (16 T_l))
+ * + 1/2) for |x| < X_l = 16 (n_l + 1) (0 and 2^20 beyond).  With
+ * F(s) = sum_k v_k G_{l_k}(16 s + 8 - q_k), symbols s_lo..s_hi that cover
+ * every component's table and S of them, cum(s) = (s - s_lo) +
+ * floor(F(s - 1) (2^16 - S - 1) / 2^32); the last slot (frequency 1) is the
+ * escape, whose excess follows in 15-bit chunks.
  * Streams: one per (image b, grid row i, channel c), index k = (b*H + i)*M + c,
  * holding the row's symbols in column order (one per wavefront step); stream
  * k occupies words [offsets[k], offsets[k+1]) of `bits`: the final state
@@ -241,6 +253,15 @@ int wf_encode(wf_plan_t plan, const float *psi, const float *y, int32_t *sym_out
  */
 int wf_ec_tables(const float *scale_table, int32_t L, int32_t *n, int64_t *base,
                  uint32_t *cum, int64_t cum_cap);
+
+/*
+ * wf_mix_tables (host only): the mixture coder's level tables of a scale
+ * table (K = 3; the CDFs G_l above): X[L], base[L+1] (first entry of each
+ * level) and, when G is non-NULL, G_l(x) for x = -X_l..X_l at
+ * base[l] + x + X_l (base[L] entries).  Errors as for wf_ec_tables.
+ */
+int wf_mix_tables(const float *scale_table, int32_t L, int32_t *X, int64_t *base,
+                  uint32_t *G, int64_t G_cap);
 
 /*
  * Encode (as wf_encode) and code the symbols into rANS streams.
@@ -257,8 +278,8 @@ int wf_encode_bits(wf_plan_t plan, const float *psi, const float *y, int32_t *sy
 /*
  * Decode with every symbol read from its rANS stream inside the step loop:
  * at the step of latent (b,i,j) the symbol of each channel c is decoded from
- * stream (b*H + i)*M + c at the latent's scale level, then
- * y_hat = symbol + mean.  sym_out [B][H][W][M] (DEVICE int32) receives the
+ * stream (b*H + i)*M + c at the latent's scale level (K = 3: under the
+ * mixture of its three components), then y_hat = symbol + mean.  sym_out [B][H][W][M] (DEVICE int32) receives the
  * decoded symbols.  `bits` (DEVICE, n_words words) and `offsets` (DEVICE
  * [B*H*M + 1]) are as written by wf_encode_bits.  Reads never go past a
  * stream's end or n_words; a malformed stream makes the next wf_plan_sync

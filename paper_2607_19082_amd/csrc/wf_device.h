@@ -1127,6 +1127,245 @@ __device__ __forceinline__ void l3_ec_job(const StepArgs& a, const StepRows& s, 
 }
 
 // ---------------------------------------------------------------------------
+// Entropy decoding for the 3-component mixture model (K = 3).  A symbol is
+// coded with the mixture of its channel's three Gaussians around the mixture
+// mean; the frequencies are built in integer arithmetic from quantised
+// parameters, so that the encoder and the decoder agree bit for bit:
+//   v_k = 1 + floor(4093 w_k) (4093 w_k clamped to [0, 4093]), and what
+//   is left of 4096 added to the largest v_k (the first of equals);
+//   q_k = rint(16 (mu_k - mu)) clamped to +-2^14 (NaN: -2^14), the
+//   component's offset in sixteenths of a symbol;
+//   G_l(x): the plan's integer CDF of level l on sixteenths (2^20 scale,
+//   0 at and below -X_l, 2^20 at and above X_l), l = the component's level;
+//   F(s) = sum_k v_k G_{l_k}(16 s + 8 - q_k), the mixture CDF at the upper
+//   edge of symbol s (2^32 = all of the mass);
+//   coded symbols s_lo..s_hi, s_lo = min_k floor((q_k - X_k) / 16),
+//   s_hi = max_k ceil((q_k + X_k) / 16), S = s_hi - s_lo + 1, with
+//   cum(s) = (s - s_lo) + floor(F(s - 1) (2^16 - S - 1) / 2^32);
+//   the last slot (2^16 - 1, frequency 1) is the escape of a symbol outside,
+//   whose excess e = 2 (s_lo - 1 - s) + 1 below or 2 (s - s_hi - 1) above
+//   follows in 15-bit chunks as for one Gaussian.
+struct MixParam {
+    uint32_t v[3];
+    int q[3], l[3];
+    int lo, hi;
+};
+// The quantised parameters of one channel (weights w, component means cm,
+// mixture mean mu, levels l, all as the epilogue computed them).
+__device__ __forceinline__ MixParam mix_param(const CallPtrs* cp, const float (&w)[3], const float (&cm)[3], float mu,
+                                              const int (&l)[3]) {
+    MixParam p;
+    uint32_t sum = 0, vtop = 0;
+    int top = 0;
+#pragma unroll
+    for (int k = 0; k < 3; ++k) {
+        float wf = w[k] * 4093.0f;
+        if (!(wf >= 0.0f)) wf = 0.0f;
+        wf = fminf(wf, 4093.0f);
+        p.v[k] = 1u + (uint32_t)floorf(wf);
+        sum += p.v[k];
+        if (p.v[k] > vtop) {
+            vtop = p.v[k];
+            top = k;
+        }
+        float d = rintf((cm[k] - mu) * (float)kMixFine);
+        if (!(fabsf(d) <= (float)kMixQmax)) d = d > 0.0f ? (float)kMixQmax : -(float)kMixQmax;
+        p.q[k] = (int)d;
+        p.l[k] = l[k];
+    }
+#pragma unroll
+    for (int k = 0; k < 3; ++k)
+        if (k == top) p.v[k] += 4096u - sum;
+    int lo = 0x7fffffff, hi = -0x7fffffff;
+#pragma unroll
+    for (int k = 0; k < 3; ++k) {
+        const int X = cp->mix_X[p.l[k]];
+        lo = min(lo, (p.q[k] - X) >> 4);          // floor division by 16
+        hi = max(hi, -((-(p.q[k] + X)) >> 4));    // ceil
+    }
+    p.lo = lo;
+    p.hi = hi;
+    return p;
+}
+// F(s), in units of 2^-32 of the mass.
+__device__ __forceinline__ uint64_t mix_F(const CallPtrs* cp, const MixParam& p, int s) {
+    uint64_t f = 0;
+#pragma unroll
+    for (int k = 0; k < 3; ++k) {
+        const int X = cp->mix_X[p.l[k]];
+        const int x = kMixFine * s + kMixFine / 2 - p.q[k];
+        const uint32_t g = x <= -X ? 0u : (x >= X ? (1u << kMixCdfBits) : cp->mix_G[cp->mix_base[p.l[k]] + x + X]);
+        f += (uint64_t)p.v[k] * g;
+    }
+    return f;
+}
+__device__ __forceinline__ uint32_t mix_cum(const CallPtrs* cp, const MixParam& p, int s) {
+    const uint64_t R = (1u << kEcPrecBits) - (uint64_t)(p.hi - p.lo + 1) - 1u;
+    return (uint32_t)(s - p.lo) + (uint32_t)((mix_F(cp, p, s - 1) * R) >> 32);
+}
+// Decode the next symbol of a stream coded under the mixture p.
+__device__ __forceinline__ int32_t ec_decode_mix(const CallPtrs* cp, const MixParam& p, uint64_t& x, uint32_t& pos,
+                                                 uint32_t end, uint32_t wnext, bool& bad) {
+    bad |= p.hi - p.lo + 1 > kMixMaxSymbols;
+    const uint32_t slot = (uint32_t)x & ((1u << kEcPrecBits) - 1u);
+    if (slot != (1u << kEcPrecBits) - 1u) {
+        // bisection: the largest s with cum(s) <= slot (cum(s_lo) = 0)
+        int lo = p.lo, hi = p.hi;
+        uint32_t clo = 0;
+        while (lo < hi) {
+            const int mid = lo + ((hi - lo + 1) >> 1);
+            const uint32_t cm = mix_cum(cp, p, mid);
+            if (cm <= slot) {
+                lo = mid;
+                clo = cm;
+            } else {
+                hi = mid - 1;
+            }
+        }
+        const uint32_t c1 = mix_cum(cp, p, lo + 1);
+        x = (uint64_t)(c1 - clo) * (x >> kEcPrecBits) + slot - clo;
+        ec_renorm(cp, x, pos, end, wnext, bad);
+        return lo;
+    }
+    // escape (frequency 1), then the excess in 15-bit chunks, low first
+    x >>= kEcPrecBits;
+    ec_renorm(cp, x, pos, end, wnext, bad);
+    uint64_t e = 0;
+    for (int q = 0; q < 5; ++q) {
+        const uint32_t ch = (uint32_t)x & 0xffffu;
+        x >>= kEcPrecBits;
+        ec_renorm(cp, x, pos, end, wnext, bad);
+        e |= (uint64_t)(ch & 0x7fffu) << (15 * q);
+        if (!(ch & 0x8000u)) {
+            const int64_t v = (e & 1u) ? (int64_t)p.lo - 1 - (int64_t)(e >> 1) : (int64_t)p.hi + 1 + (int64_t)(e >> 1);
+            bad |= v < -2147483648LL || v > 2147483647LL;
+            return (int32_t)v;
+        }
+    }
+    bad = true;
+    return 0;
+}
+
+// Phase C with entropy decoding, K = 3: job column cg computes all nine
+// column tiles of channel tile cg (3 logits, 3 component means, 3 scales),
+// so that a lane holds its channel's whole mixture, decodes the symbol from
+// its stream and writes y_hat = s + mean in the same job.
+template <class P, bool COH>
+__device__ __forceinline__ void l3_ec3_tile(const StepArgs& a, const StepRows& s, Job jb, L3Smem<3>& sm) {
+    using A = typename P::A;
+    using Bw = typename P::B;
+    constexpr int KBW = 2;   // k-blocks a wave loads before its MFMAs (nine weight operands each)
+    constexpr int NT = 9;
+    const int M = a.M, G = M / kTile, cg = jb.ct, rt = jb.rt;
+    const int wave = wave_id(), lane = threadIdx.x & 63, kq = lane >> 4;
+    const CallPtrs* cp = a.cp;
+    const int c = cg * kTile + (lane & 15);
+    const int ro = wave < 4 ? rt * kTile + kq * 4 + wave : s.nrows;   // epilogue row of this wave
+    const Row v = step_row(a, s, ro);
+    const size_t k = ((size_t)v.b * a.H + v.i) * M + c;
+    uint64_t x = 0;
+    uint32_t pos = 0, end = 0, wnext = 0;
+    if (v.valid) {
+        x = cp->ec_x[k];
+        pos = cp->ec_pos[k];
+        end = cp->ec_end[k];
+        wnext = pos < end ? cp->bits[pos] : 0u;
+    }
+    float bias[NT];
+#pragma unroll
+    for (int t = 0; t < NT; ++t) bias[t] = a.b3[t * M + c];
+
+    const int nkb = a.Np2 / P::kK;
+    const int per = (nkb + kWaves - 1) / kWaves;
+    const int kb0 = min(nkb, wave * per), kb1 = min(nkb, kb0 + per);
+    const int r = rt * kTile + (lane & 15);
+    const bool valid = r < s.nrows;
+    const Bw* __restrict__ wv = static_cast<const Bw*>(a.wp3) + lane;
+    const void* h2 = h2_of(a, s);
+    f4 acc[NT];
+#pragma unroll
+    for (int t = 0; t < NT; ++t) acc[t] = zero4();
+    for (int kc = kb0; kc < kb1; kc += KBW) {
+        A av[KBW];
+        Bw bv[KBW][NT];
+#pragma unroll
+        for (int u = 0; u < KBW; ++u) {
+            const int kk = min(kc + u, kb1 - 1);
+            av[u] = ld_tile<P, COH>(h2, rt, a.Np2, kk, valid);
+#pragma unroll
+            for (int t = 0; t < NT; ++t) bv[u][t] = wv[((size_t)(t * G + cg) * nkb + kk) * 64];
+        }
+#pragma unroll
+        for (int u = 0; u < KBW; ++u)
+            if (kc + u < kb1)
+#pragma unroll
+                for (int t = 0; t < NT; ++t) acc[t] = P::mma(av[u], bv[u][t], acc[t]);
+    }
+    // the nine tiles' wave sums in two rounds through the six-tile buffer
+    float o[NT];
+#pragma unroll
+    for (int rnd = 0; rnd < 2; ++rnd) {
+        const int t0 = rnd * 6, nt = rnd ? NT - 6 : 6;
+#pragma unroll
+        for (int t = 0; t < 6; ++t)
+            if (t < nt) sm.red[wave][t][lane] = acc[t0 + t];
+        __syncthreads();
+#pragma unroll
+        for (int t = 0; t < 6; ++t)
+            if (t < nt) {
+                o[t0 + t] = bias[t0 + t];
+                if (wave < 4) {
+#pragma unroll
+                    for (int w2 = 0; w2 < kWaves; ++w2) o[t0 + t] += sm.red[w2][t][lane][wave];
+                }
+            }
+        __syncthreads();
+    }
+    if (!v.valid) return;
+
+    const size_t lat = v.lat, oq = lat * M + c;
+    const float mx = fmaxf(o[0], fmaxf(o[1], o[2]));
+    float ex[3], den = 0.0f;
+#pragma unroll
+    for (int kk = 0; kk < 3; ++kk) {
+        ex[kk] = expf(o[kk] - mx);
+        den += ex[kk];
+    }
+    float w3[3], m3[3], mu = 0.0f;
+    int l3[3];
+    const float t0 = sm.tab[0];
+#pragma unroll
+    for (int kk = 0; kk < 3; ++kk) {
+        w3[kk] = ex[kk] / den;
+        m3[kk] = o[3 + kk];
+        mu += w3[kk] * m3[kk];
+        const float sg = o[6 + kk] > t0 ? o[6 + kk] : t0;
+        l3[kk] = scale_index(sm.tab, a.L, sg);
+        const size_t q = (lat * 3 + kk) * M + c;
+        cp->weight[q] = w3[kk];
+        cp->cmean[q] = m3[kk];
+        cp->scale[q] = sg;
+        cp->idx[q] = l3[kk];
+    }
+    bool bad = false;
+    const MixParam mp = mix_param(cp, w3, m3, mu, l3);
+    const int32_t sv = ec_decode_mix(cp, mp, x, pos, end, wnext, bad);
+    cp->ec_x[k] = x;
+    cp->ec_pos[k] = pos;
+    if (bad) __hip_atomic_store(cp->err, kErrStream, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    cp->sym_out[oq] = sv;
+    cp->mean[oq] = mu;
+    const float yv = (float)sv + mu;
+    st1<COH>(cp->y_hat, oq, yv);
+    if constexpr (P::kBf16) st_pair_row<COH>(a.ybf, lat * 2 * M, c, yv);
+}
+template <class P, bool COH>
+__device__ __forceinline__ void l3_ec3_job(const StepArgs& a, const StepRows& s, int b, L3Smem<3>& sm) {
+    const Job jb = xcd_job(b, a.M / kTile, ntiles(s.nrows));
+    if (jb.valid) l3_ec3_tile<P, COH>(a, s, jb, sm);
+}
+
+// ---------------------------------------------------------------------------
 // Context approximation (Sec. III-D): a step is a group of N wavefronts.  A
 // tap of the latent's own group is not decoded yet and is replaced, channel by
 // channel, by the mean of the latent's decoded in-image taps (zero when none
@@ -1291,7 +1530,7 @@ __device__ __forceinline__ void l1_group_tile(const StepArgs& a, const StepRows&
 }
 
 // The main job of phase ph (sm.tab must hold the scale table for PH_C); EC:
-// phase C decodes the symbols from their rANS streams (a.ec set, K = 1).
+// phase C decodes the symbols from their rANS streams (a.ec set).
 template <class P, int KC, bool COH, bool EC = false>
 __device__ __forceinline__ void phase_job(int ph, const StepArgs& a, const StepRows& s, int b, f4 (*red)[64],
                                           L3Smem<KC>& sm) {
@@ -1303,6 +1542,12 @@ __device__ __forceinline__ void phase_job(int ph, const StepArgs& a, const StepR
     if constexpr (EC && KC == 1) {
         if (ph == PH_C) {
             l3_ec_job<P, COH>(a, s, b, red, sm.tab);
+            return;
+        }
+    }
+    if constexpr (EC && KC == 3) {
+        if (ph == PH_C) {
+            l3_ec3_job<P, COH>(a, s, b, sm);
             return;
         }
     }

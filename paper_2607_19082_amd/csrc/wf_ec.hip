@@ -19,11 +19,17 @@
 // + (s < 0) in 15-bit chunks, low first, each a uniform 16-bit value whose
 // top bit marks another chunk.
 //
+// The 3-component mixture (K = 3) codes each symbol with the mixture of its
+// channel's components around the mixture mean; its per-latent frequencies
+// come from quantised parameters and the per-level integer CDFs built here
+// (mix_tables; the arithmetic is with the decode, next to mix_param).
+//
 // Coder: state x in [2^31, 2^63), 32-bit renormalisation words.  Encoding a
 // symbol of frequency f and cumulative frequency c emits the low word of x
 // (x >>= 32) when x >= f 2^47, then x = floor(x / f) 2^16 + (x mod f) + c;
 // decoding inverts it.  A stream is the final state (high word, low word)
 // followed by the emitted words in reverse order of emission.
+#include <algorithm>
 #include <cmath>
 #include <vector>
 
@@ -92,6 +98,31 @@ static int ec_tables(const float* table, int L, std::vector<int32_t>& n, std::ve
     return WF_OK;
 }
 
+// The mixture coder's level tables (K = 3): X_l = 16 (n_l + 1) and the
+// integer CDF on sixteenths of a symbol, G_l(x) = floor(2^20 Phi(x / (16 T_l))
+// + 1/2) for x = -X_l..X_l (Phi(z) = erfc(-z / sqrt 2) / 2), level after level.
+static int mix_tables(const float* table, int L, std::vector<int32_t>& X, std::vector<int64_t>& base,
+                      std::vector<uint32_t>& G) {
+    X.assign(L, 0);
+    base.assign(L + 1, 0);
+    for (int l = 0; l < L; ++l) {
+        const int n = support_of(table[l]);
+        if (n > kEcMaxSupport) return fail(WF_E_UNSUPPORTED, "entropy coding: a scale level is too wide");
+        X[l] = kMixFine * (n + 1);
+        base[l + 1] = base[l] + 2 * (int64_t)X[l] + 1;
+    }
+    G.assign((size_t)base[L], 0u);
+    for (int l = 0; l < L; ++l) {
+        const double r = kMixFine * (double)table[l] * std::sqrt(2.0);
+        uint32_t* g = G.data() + base[l];
+        for (int x = -X[l]; x <= X[l]; ++x) {
+            const double phi = 0.5 * std::erfc(-(double)x / r);
+            g[x + X[l]] = (uint32_t)std::floor(phi * (double)(1u << kMixCdfBits) + 0.5);
+        }
+    }
+    return WF_OK;
+}
+
 template <class T>
 static int ec_alloc(Plan* p, T** dst, size_t count) {
     hipError_t e = hipMalloc((void**)dst, count * sizeof(T));
@@ -109,19 +140,36 @@ static int ec_upload(Plan* p, T** dst, const std::vector<T>& v) {
 }
 
 int build_ec(Plan* p, const float* scale_table, int L) {
-    std::vector<int32_t> n;
-    std::vector<int64_t> base;
-    std::vector<uint32_t> cum;
-    std::vector<uint64_t> lut;
-    int rc = ec_tables(scale_table, L, n, base, cum, &lut);
-    if (rc != WF_OK) return rc;
-    std::vector<int32_t> base32(L);
-    for (int l = 0; l < L; ++l) base32[l] = (int32_t)base[l];
+    int rc;
+    if (p->K == 1) {
+        std::vector<int32_t> n;
+        std::vector<int64_t> base;
+        std::vector<uint32_t> cum;
+        std::vector<uint64_t> lut;
+        if ((rc = ec_tables(scale_table, L, n, base, cum, &lut)) != WF_OK) return rc;
+        std::vector<int32_t> base32(L);
+        for (int l = 0; l < L; ++l) base32[l] = (int32_t)base[l];
+        if ((rc = ec_upload(p, &p->ec_n, n)) != WF_OK || (rc = ec_upload(p, &p->ec_base, base32)) != WF_OK ||
+            (rc = ec_upload(p, &p->ec_cum, cum)) != WF_OK || (rc = ec_upload(p, &p->ec_lut, lut)) != WF_OK)
+            return rc;
+    } else {
+        std::vector<int32_t> X;
+        std::vector<int64_t> base;
+        std::vector<uint32_t> G;
+        if ((rc = mix_tables(scale_table, L, X, base, G)) != WF_OK) return rc;
+        // every latent's coded symbols must number at most kMixMaxSymbols
+        const int Xmax = *std::max_element(X.begin(), X.end());
+        if ((2 * (int64_t)kMixQmax + 2 * (int64_t)Xmax) / kMixFine + 2 > kMixMaxSymbols)
+            return fail(WF_E_UNSUPPORTED, "entropy coding: the scale table is too wide for the mixture coder");
+        if (base[L] >= (int64_t)1 << 31) return fail(WF_E_UNSUPPORTED, "entropy coding: mixture tables too large");
+        std::vector<int32_t> base32(L);
+        for (int l = 0; l < L; ++l) base32[l] = (int32_t)base[l];
+        if ((rc = ec_upload(p, &p->mix_X, X)) != WF_OK || (rc = ec_upload(p, &p->mix_base, base32)) != WF_OK ||
+            (rc = ec_upload(p, &p->mix_G, G)) != WF_OK)
+            return rc;
+    }
     const size_t ns = (size_t)p->B * p->H * p->M;
     const size_t per = 2 + (size_t)(1 + kEcMaxEscapeWords) * p->W;   // words one stream can take
-    if ((rc = ec_upload(p, &p->ec_n, n)) != WF_OK || (rc = ec_upload(p, &p->ec_base, base32)) != WF_OK ||
-        (rc = ec_upload(p, &p->ec_cum, cum)) != WF_OK || (rc = ec_upload(p, &p->ec_lut, lut)) != WF_OK)
-        return rc;
     if ((rc = ec_alloc(p, &p->ec_x, ns)) != WF_OK || (rc = ec_alloc(p, &p->ec_pos, ns)) != WF_OK ||
         (rc = ec_alloc(p, &p->ec_end, ns)) != WF_OK || (rc = ec_alloc(p, &p->ec_len, ns)) != WF_OK ||
         (rc = ec_alloc(p, &p->ec_words, ns * per)) != WF_OK)
@@ -215,6 +263,64 @@ __global__ void k_ec_encode(const int32_t* __restrict__ sym, const int32_t* __re
     if (bad) __hip_atomic_store(err, kErrStream, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
+// The same for the 3-component mixture: each symbol's frequencies from the
+// encode's weights, component means, mixture mean and scale levels.
+__global__ void k_ec_encode_mix(const int32_t* __restrict__ sym, const float* __restrict__ weight,
+                                const float* __restrict__ cmean, const float* __restrict__ mean,
+                                const int32_t* __restrict__ idx, int H, int W, int M, int ns, int L,
+                                const int32_t* __restrict__ tX, const int32_t* __restrict__ tbase,
+                                const uint32_t* __restrict__ tG, uint32_t* __restrict__ words, int per,
+                                uint64_t* __restrict__ xs, uint32_t* __restrict__ len, int* err) {
+    const int k = blockIdx.x * blockDim.x + threadIdx.x;
+    if (k >= ns) return;
+    CallPtrs t{};
+    t.mix_X = tX;
+    t.mix_base = tbase;
+    t.mix_G = tG;
+    const int c = k % M, row = k / M;   // row = b * H + i
+    uint32_t* w = words + (size_t)k * per;
+    uint64_t x = 1ull << 31;
+    uint32_t n = 0;
+    bool bad = false;
+    for (int j = W - 1; j >= 0; --j) {
+        const size_t lat = (size_t)row * W + j;
+        float w3[3], m3[3];
+        int l3[3];
+#pragma unroll
+        for (int kk = 0; kk < 3; ++kk) {
+            const size_t q = (lat * 3 + kk) * M + c;
+            w3[kk] = weight[q];
+            m3[kk] = cmean[q];
+            l3[kk] = idx[q];
+            bad |= l3[kk] < 0 || l3[kk] >= L;
+        }
+        if (bad) break;
+        const MixParam p = mix_param(&t, w3, m3, mean[lat * M + c], l3);
+        if (p.hi - p.lo + 1 > kMixMaxSymbols) {
+            bad = true;
+            break;
+        }
+        const int32_t s = sym[lat * M + c];
+        if (s >= p.lo && s <= p.hi) {
+            const uint32_t c0 = mix_cum(&t, p, s), c1 = mix_cum(&t, p, s + 1);
+            ec_push(x, c0, c1 - c0, w, n);
+            continue;
+        }
+        const uint64_t e = s < p.lo ? 2u * (uint64_t)((int64_t)p.lo - 1 - s) + 1u
+                                    : 2u * (uint64_t)((int64_t)s - p.hi - 1);
+        int nc = 1;
+        while (nc < kEcMaxEscapeWords && (e >> (15 * nc))) ++nc;
+        for (int q2 = nc - 1; q2 >= 0; --q2) {
+            const uint32_t ch = (uint32_t)((e >> (15 * q2)) & 0x7fffu) | (q2 < nc - 1 ? 0x8000u : 0u);
+            ec_push(x, ch, 1u, w, n);
+        }
+        ec_push(x, (1u << kEcPrecBits) - 1u, 1u, w, n);
+    }
+    xs[k] = x;
+    len[k] = n;
+    if (bad) __hip_atomic_store(err, kErrStream, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
 // Offsets of the streams (exclusive prefix sum of 2 + emitted words) in one
 // workgroup; offsets[ns] is the total.  A total above the caller's capacity
 // records a capacity error (the streams are then not written).
@@ -264,13 +370,18 @@ __global__ void k_ec_compact(const uint32_t* __restrict__ words, int per, const 
     for (uint32_t q = 0; q < n; ++q) bits[o + 2 + q] = w[n - 1 - q];
 }
 
-int enqueue_ec_encode(Plan& p, const int32_t* sym, const int32_t* idx, uint32_t* bits, int64_t cap, uint32_t* offsets,
+int enqueue_ec_encode(Plan& p, const int32_t* sym, const wf_out& out, uint32_t* bits, int64_t cap, uint32_t* offsets,
                       hipStream_t stream) {
     const int ns = p.B * p.H * p.M;
     const int per = 2 + (1 + kEcMaxEscapeWords) * p.W;
     const dim3 g((ns + 255) / 256), b(256);
-    hipLaunchKernelGGL(k_ec_encode, g, b, 0, stream, sym, idx, p.H, p.W, p.M, ns, p.L, p.ec_n, p.ec_base, p.ec_cum,
-                       p.ec_words, per, p.ec_x, p.ec_len, p.d_err);
+    if (p.K == 1)
+        hipLaunchKernelGGL(k_ec_encode, g, b, 0, stream, sym, out.idx, p.H, p.W, p.M, ns, p.L, p.ec_n, p.ec_base,
+                           p.ec_cum, p.ec_words, per, p.ec_x, p.ec_len, p.d_err);
+    else
+        hipLaunchKernelGGL(k_ec_encode_mix, g, b, 0, stream, sym, out.weight, out.comp_mean, out.mean, out.idx, p.H,
+                           p.W, p.M, ns, p.L, p.mix_X, p.mix_base, p.mix_G, p.ec_words, per, p.ec_x, p.ec_len,
+                           p.d_err);
     hipLaunchKernelGGL(k_ec_scan, dim3(1), dim3(kScanThreads), 0, stream, p.ec_len, ns, offsets, (long long)cap,
                        p.d_err);
     hipLaunchKernelGGL(k_ec_compact, g, b, 0, stream, p.ec_words, per, p.ec_x, p.ec_len, offsets, ns, (long long)cap,
@@ -297,6 +408,23 @@ extern "C" int wf_ec_tables(const float* scale_table, int32_t L, int32_t* n_out,
     if (cum) {
         if (cum_cap < base[L]) return fail(WF_E_INVALID, "cum holds fewer entries than the tables");
         std::copy(c.begin(), c.end(), cum);
+    }
+    return WF_OK;
+}
+
+extern "C" int wf_mix_tables(const float* scale_table, int32_t L, int32_t* X_out, int64_t* base_out, uint32_t* G,
+                             int64_t G_cap) {
+    if (!scale_table || L < 2 || L > kMaxTable) return fail(WF_E_INVALID, "scale table pointer or length");
+    std::vector<int32_t> X;
+    std::vector<int64_t> base;
+    std::vector<uint32_t> g;
+    const int rc = mix_tables(scale_table, L, X, base, g);
+    if (rc != WF_OK) return rc;
+    if (X_out) std::copy(X.begin(), X.end(), X_out);
+    if (base_out) std::copy(base.begin(), base.end(), base_out);
+    if (G) {
+        if (G_cap < base[L]) return fail(WF_E_INVALID, "G holds fewer entries than the tables");
+        std::copy(g.begin(), g.end(), G);
     }
     return WF_OK;
 }

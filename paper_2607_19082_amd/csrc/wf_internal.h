@@ -21,6 +21,10 @@ constexpr int kEcPrecBits = 16;
 constexpr int kEcLutShift = 4;
 constexpr int kEcLut = 1 << (kEcPrecBits - kEcLutShift);
 constexpr int kEcMaxSupport = 16383;   // support half-width bound (symbol indices fit 16 bits)
+// the 3-component mixture's coder: sixteenths of a symbol, offsets within
+// +-2^14 of them, weights summing to 2^12, CDFs scaled by 2^20, at most 2^15
+// coded symbols per latent
+constexpr int kMixFine = 16, kMixQmax = 1 << 14, kMixCdfBits = 20, kMixMaxSymbols = 1 << 15;
 // device error word values
 constexpr int kErrTimeout = 1, kErrStream = 2, kErrCapacity = 3;
 constexpr int kMaxNew = 2;           // taps written by the immediately preceding step
@@ -128,6 +132,11 @@ struct CallPtrs {
     const int32_t* ec_base; // [L] first cumulative entry per level
     const uint32_t* ec_cum; // cumulative frequencies
     const uint64_t* ec_lut; // [L][kEcLut] per slot bucket: its first slot's symbol u, cum[u], cum[u + 1]
+    // the 3-component mixture (K = 3): per level l the half-width X_l of its
+    // integer CDF on sixteenths of a symbol, its first entry, and the CDFs
+    const int32_t* mix_X;   // [L]
+    const int32_t* mix_base;// [L]
+    const uint32_t* mix_G;  // G_l(x), x = -X_l..X_l, at mix_base[l] + x + X_l
     int* err;
 };
 
@@ -240,6 +249,8 @@ struct Plan {
     uint64_t* ec_lut = nullptr;
     uint64_t* ec_x = nullptr;
     uint32_t *ec_pos = nullptr, *ec_end = nullptr, *ec_len = nullptr, *ec_words = nullptr;
+    int32_t *mix_X = nullptr, *mix_base = nullptr;   // K = 3: the mixture's level CDFs
+    uint32_t* mix_G = nullptr;
     hipGraph_t graph_ec = nullptr;
     hipGraphExec_t graph_exec_ec = nullptr;
 };
@@ -256,7 +267,9 @@ int enqueue_set_call_at(CallPtrs* dst, const CallPtrs& c, hipStream_t stream);
 // entropy coding (wf_ec.hip)
 int build_ec(Plan* p, const float* scale_table, int L);
 int enqueue_ec_init(Plan& p, const uint32_t* bits, int64_t n_words, const uint32_t* offsets, hipStream_t stream);
-int enqueue_ec_encode(Plan& p, const int32_t* sym, const int32_t* idx, uint32_t* bits, int64_t cap,
+// (the encode's outputs give each symbol's parameters: idx, and for K = 3
+// weight, comp_mean and mean)
+int enqueue_ec_encode(Plan& p, const int32_t* sym, const wf_out& out, uint32_t* bits, int64_t cap,
                       uint32_t* offsets, hipStream_t stream);
 // Publish the call's pointers to p.d_call on `stream`.
 int enqueue_set_call(Plan& p, const CallPtrs& c, hipStream_t stream);

@@ -108,7 +108,6 @@ static int check_desc(const wf_desc* d) {
     if (d->entropy_coder != WF_EC_NONE && d->entropy_coder != WF_EC_RANS)
         return fail(WF_E_INVALID, "unknown entropy_coder");
     if (d->entropy_coder == WF_EC_RANS) {
-        if (d->K != 1) return fail(WF_E_UNSUPPORTED, "entropy coding needs K = 1 (the Gaussian model)");
         if (d->group > 1) return fail(WF_E_UNSUPPORTED, "entropy coding needs the exact decode (group <= 1)");
         if (d->driver != WF_DRIVER_STREAM && d->driver != WF_DRIVER_GRAPH)
             return fail(WF_E_UNSUPPORTED, "entropy coding needs the stream or graph driver");
@@ -561,6 +560,7 @@ static void ec_ptrs(const Plan* p, CallPtrs& c, const uint32_t* bits) {
     c.bits = bits;
     c.ec_x = p->ec_x; c.ec_pos = p->ec_pos; c.ec_end = p->ec_end;
     c.ec_n = p->ec_n; c.ec_base = p->ec_base; c.ec_cum = p->ec_cum; c.ec_lut = p->ec_lut;
+    c.mix_X = p->mix_X; c.mix_base = p->mix_base; c.mix_G = p->mix_G;
     c.err = p->d_err;
 }
 
@@ -592,7 +592,7 @@ int wf_encode_bits(wf_plan_t plan, const float* psi, const float* y, int32_t* sy
     int rc = check_out(p, out);
     if (rc != WF_OK) return rc;
     if ((rc = run_call(p, call_ptrs(psi, nullptr, y, sym_out, out), stream)) != WF_OK) return rc;
-    return enqueue_ec_encode(*p, sym_out, out->idx, bits, bits_capacity, offsets, stream);
+    return enqueue_ec_encode(*p, sym_out, *out, bits, bits_capacity, offsets, stream);
 }
 
 int wf_decode_bits(wf_plan_t plan, const float* psi, const uint32_t* bits, int64_t n_words, const uint32_t* offsets,

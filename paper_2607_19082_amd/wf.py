@@ -22,7 +22,7 @@ PRECISION = {"fp32": 0, "bf16": 1}
 DRIVER = {"stream": 0, "graph": 1, "persistent": 2, "dataflow": 3, "resident": 4}
 
 EXPORTS = ["wf_schedule", "wf_validate", "wf_plan", "wf_plan_schedule", "wf_decode",
-           "wf_encode", "wf_ec_tables", "wf_encode_bits", "wf_decode_bits", "wf_plan_trace",
+           "wf_encode", "wf_ec_tables", "wf_mix_tables", "wf_encode_bits", "wf_decode_bits", "wf_plan_trace",
            "wf_measure_floor", "wf_plan_sync", "wf_xform_plan", "wf_hyper_synthesis", "wf_synthesis",
            "wf_decode_noalloc", "wf_xform_destroy", "wf_plan_destroy", "wf_last_error"]
 
@@ -86,6 +86,7 @@ def lib():
         L.wf_decode_noalloc.argtypes = [P, P, P, ctypes.POINTER(Out), P]
         L.wf_encode.argtypes = [P, P, P, P, ctypes.POINTER(Out), P]
         L.wf_ec_tables.argtypes = [P, ctypes.c_int32, P, P, P, ctypes.c_int64]
+        L.wf_mix_tables.argtypes = [P, ctypes.c_int32, P, P, P, ctypes.c_int64]
         L.wf_encode_bits.argtypes = [P, P, P, P, ctypes.POINTER(Out), P, ctypes.c_int64, P, P]
         L.wf_decode_bits.argtypes = [P, P, P, ctypes.c_int64, P, P, ctypes.POINTER(Out), P]
         L.wf_xform_plan.argtypes = [ctypes.POINTER(XformDesc), ctypes.POINTER(ctypes.c_void_p)]
@@ -327,6 +328,19 @@ def ec_tables(table):
     cum = np.zeros(int(base[-1]), np.uint32)
     _check(lib().wf_ec_tables(table.ctypes.data, L, None, None, cum.ctypes.data, len(cum)))
     return n, base, cum
+
+
+def mix_tables(table):
+    """The library's mixture-coder level tables of a scale table (host only):
+    (X [L], base [L+1], G [base[L]] uint32)."""
+    table = np.ascontiguousarray(table, dtype=np.float32)
+    L = len(table)
+    X = np.zeros(L, np.int32)
+    base = np.zeros(L + 1, np.int64)
+    _check(lib().wf_mix_tables(table.ctypes.data, L, X.ctypes.data, base.ctypes.data, None, 0))
+    G = np.zeros(int(base[-1]), np.uint32)
+    _check(lib().wf_mix_tables(table.ctypes.data, L, None, None, G.ctypes.data, len(G)))
+    return X, base, G
 
 
 class Xform:

@@ -181,7 +181,9 @@ def test_entropy_coder_validation(lib):
     assert wf.validate(d) == wf.WF_OK
     d.entropy_coder = 2
     assert wf.validate(d) == wf.WF_E_INVALID
-    for kw in (dict(K=3), dict(group=2), dict(driver="persistent"), dict(driver="dataflow")):
+    d, keep = _desc(entropy_coder="rans", driver="graph", K=3)   # the mixture coder
+    assert wf.validate(d) == wf.WF_OK
+    for kw in (dict(group=2), dict(driver="persistent"), dict(driver="dataflow"), dict(driver="resident")):
         args = dict(entropy_coder="rans", driver="graph")
         args.update(kw)
         d, keep = _desc(**args)
@@ -199,6 +201,19 @@ def test_entropy_tables_match_the_oracle(lib):
         assert np.array_equal(n, on) and np.array_equal(base, obase) and np.array_equal(cum, ocum)
     with pytest.raises(wf.WfError) as e:
         wf.ec_tables(np.array([1.0, 3000.0], np.float32))
+    assert e.value.code == wf.WF_E_UNSUPPORTED
+
+
+def test_mixture_tables_match_the_oracle(lib):
+    """The mixture coder's level CDFs (K = 3), built by the library itself,
+    equal the oracle's entry for entry."""
+    import oracle
+    for table in (inputs.scale_table(), inputs.scale_table(levels=17, lo=0.5, hi=40.0)):
+        X, base, G = wf.mix_tables(table)
+        oX, obase, oG = oracle.mix_tables(table)
+        assert np.array_equal(X, oX) and np.array_equal(base, obase) and np.array_equal(G, oG)
+    with pytest.raises(wf.WfError) as e:
+        wf.mix_tables(np.array([1.0, 3000.0], np.float32))
     assert e.value.code == wf.WF_E_UNSUPPORTED
 
 

@@ -2,8 +2,9 @@
 wavefront decode, Sec. III-C; Gaussian model of Sec. II-A), through the C-ABI.
 
 * wf_encode_bits: the streams and offsets are bit-identical to the oracle's
-  coder run on the same symbols and scale levels (those of the GPU encode,
-  whose parameters meet the usual bar against the oracle);
+  coder run on the same symbols and scale levels (K = 3: weights, component
+  means, mixture mean and levels), those of the GPU encode, whose parameters
+  meet the usual bar against the oracle;
 * wf_decode_bits: every symbol comes back exactly, and every output is
   bit-identical to the GPU decode given the symbols themselves;
 * a truncated buffer makes the decode report WF_E_STREAM (reads stay inside
@@ -47,7 +48,8 @@ def plan(cfg, w, table, driver, precision):
 def round_trip(cfg, w, table, psi, sym, driver, precision, check_oracle_model=True):
     B, H, W, M = cfg["B"], cfg["H"], cfg["W"], cfg["M"]
     bf = precision == "bf16"
-    ref = oracle.Model(w, table, H, W, B, 1, relaxed=cfg["relaxed"], bf16=bf).decode(psi, sym) \
+    K = cfg["K"]
+    ref = oracle.Model(w, table, H, W, B, K, relaxed=cfg["relaxed"], bf16=bf).decode(psi, sym) \
         if check_oracle_model else None
     p = plan(cfg, w, table, driver, precision)
     psi_d = torch.from_numpy(psi).cuda()
@@ -61,12 +63,15 @@ def round_trip(cfg, w, table, psi, sym, driver, precision, check_oracle_model=Tr
     assert np.array_equal(s_e, sym)
     enc = to_np(out_e)
     if ref is not None:
-        log(compare(enc, ref, table, 1, tol=BF16_TOL if bf else FP32_TOL))
+        log(compare(enc, ref, table, K, tol=BF16_TOL if bf else FP32_TOL))
     offs_np = offs.cpu().numpy().view(np.uint32)
     total = int(offs_np[-1])
     got_bits = bits[:total].cpu().numpy().view(np.uint32)
-    # the oracle's coder on the same symbols and levels gives the same words
-    obits, ooffs = oracle.rans_encode(s_e, enc["idx"][..., 0, :], table)
+    # the oracle's coder on the same symbols and parameters gives the same words
+    if K == 1:
+        obits, ooffs = oracle.rans_encode(s_e, enc["idx"][..., 0, :], table)
+    else:
+        obits, ooffs = oracle.mix_encode(s_e, enc["weight"], enc["comp_mean"], enc["mean"], enc["idx"], table)
     assert np.array_equal(ooffs, offs_np) and np.array_equal(obits, got_bits)
     log(f"streams: {total} words, {32.0 * total / sym.size:.3f} bits per symbol")
     # decode from the streams
@@ -86,6 +91,8 @@ CASES = [
     ("minnen-16x16-m192", 7, 9, 1),
     ("minnen-relaxed-b8-120x68-m192", 5, 7, 3),
     ("minnen-hr-4k-240x135-m320", 4, 10, 2),
+    # the 3-component mixture (K = 3; its full size, 40 rows per step, below)
+    ("cheng-gmm3-1080p-120x68-m192", 6, 11, 2),
 ]
 
 
@@ -112,6 +119,19 @@ def test_rans_escapes_and_extremes():
     round_trip(cfg, w, table, psi, sym, "graph", "fp32", check_oracle_model=False)
 
 
+def test_rans_mixture_escapes():
+    """The mixture coder's escapes below and above a latent's coded symbols,
+    of one and two chunks."""
+    cfg, w, table, psi, sym = make_case("cheng-gmm3-1080p-120x68-m192", H=5, W=8, B=1)
+    sym = sym.copy()
+    flat = sym.reshape(-1)
+    rng = np.random.default_rng(5)
+    pos = rng.choice(flat.size, size=6, replace=False)
+    flat[pos] = [40000, -40000, 131075, -131075, 5000, -1700]
+    log("rans mixture escapes case")
+    round_trip(cfg, w, table, psi, sym, "graph", "fp32", check_oracle_model=False)
+
+
 def test_rans_errors_are_reported():
     cfg, w, table, psi, sym = make_case("minnen-16x16-m192", H=4, W=6, B=1)
     total, bits, offs = round_trip(cfg, w, table, psi, sym, "stream", "fp32", check_oracle_model=False)
@@ -134,6 +154,14 @@ def test_rans_errors_are_reported():
     assert int(offs2[-1].item()) == total
     assert int(small.abs().sum().item()) == 0
     p.close()
+
+
+@pytest.mark.parametrize("precision", ["fp32", "bf16"])
+def test_rans_gmm_1080p_full_size(precision):
+    name = "cheng-gmm3-1080p-120x68-m192"
+    log(f"rans case {name} full size precision={precision}")
+    cfg, w, table, psi, sym = make_case(name)
+    round_trip(cfg, w, table, psi, sym, "graph", precision, check_oracle_model=False)
 
 
 @pytest.mark.parametrize("precision", ["fp32", "bf16"])
