@@ -136,6 +136,10 @@ typedef struct {
                                driver (WF_E_UNSUPPORTED otherwise).                      */
     int32_t param_order;    /* wf_param_order: block order of the rows of w3 and b3        */
     int32_t entropy_coder;  /* wf_entropy_coder                                             */
+    int32_t cu_limit;       /* 0: plan the in-launch drivers (persistent, dataflow,
+                               resident) for every compute unit; N > 0: for at most N
+                               (a plan that then cannot be resident is refused with
+                               WF_E_UNSUPPORTED)                                        */
 } wf_desc;
 
 /*
@@ -194,6 +198,63 @@ int wf_plan(const wf_desc *desc, wf_plan_t *out);
  * of every latent (its wavefront t, or its group floor(t / N) under context
  * approximation) and the number of steps. */
 int wf_plan_schedule(wf_plan_t plan, int32_t *step_of, int32_t *n_steps);
+
+/*
+ * Race checking (host only; no device is touched): the dependency structure
+ * that the in-launch drivers' kernels follow for the plan `desc` describes,
+ * computed by the same functions the kernels call.  The causality of the
+ * wavefront decode (Sec. III-A, Eq. 3-4: a latent is decoded after every
+ * latent of its mask) then rests on these waits, which the test suite checks
+ * by simulation.  desc->driver selects the layout of `out` (int32):
+ *   WF_DRIVER_DATAFLOW: per job of the plan's job lists, in list order,
+ *     {t, kind (0 CTX, 1 CTXL, 2 A, 3 B, 4 C0, 5 C1), part, row tile,
+ *     column tile, list (0-7 critical, 8-15 context, by column tile mod 8),
+ *     position in the global order, number of waits, then three waits
+ *     (counter group, column tiles lo, hi, multiplicity)}: a wait holds
+ *     until, for every class x, the group's counter of class x reaches the
+ *     multiplicity times the number of column tiles in [lo, hi) of class x.
+ *     A finished job bumps the counter of its class (column tile mod 8) in
+ *     group (t*6 + kind)*(nrt_max + 1) + row tile and, for C0 and C1, in
+ *     group (t*6 + kind)*(nrt_max + 1) + nrt_max.  The last entry is nrt_max.
+ *   WF_DRIVER_RESIDENT: per task (step t, image b, 16-row band beta) in the
+ *     global order, {t, b, beta, then for each role (0 CTX, 1 CTXL, 2 A, 3 B,
+ *     4 C0, 5 C1) three waits (role, task), role -1 for none}.
+ * *needed receives the number of entries; out (HOST, capacity entries) may
+ * be NULL.  Errors: WF_E_INVALID (desc, needed, capacity),
+ * WF_E_UNSUPPORTED (another driver; any plan the driver refuses).
+ */
+int wf_plan_deps(const wf_desc *desc, int32_t *out, int64_t capacity, int64_t *needed);
+
+/*
+ * The bounded waits of the in-launch drivers (persistent, dataflow,
+ * resident), for the calls after this one: spin_budget_ticks is the longest
+ * one wait may spin, in ticks of the 100 MHz wall clock (<= 0: the default,
+ * 1 s).  A wait past its budget, or one that sees an error recorded by
+ * another workgroup, leaves the kernel, so the grid always drains and the
+ * next wf_plan_sync returns WF_E_TIMEOUT; the next call starts afresh.
+ * stall = 1 (for tests of that path) makes every counter and barrier wait
+ * unreachable, so the calls time out by construction; stall = 0 restores
+ * them.  The stream and graph drivers do not wait and ignore both.
+ * Errors: WF_E_INVALID (NULL plan, stall not 0 or 1).
+ */
+int wf_plan_set_waits(wf_plan_t plan, int64_t spin_budget_ticks, int32_t stall);
+
+/*
+ * Coherence litmus test of the exchange inside one launch that the
+ * persistent, dataflow and resident drivers rely on (the causality of
+ * Sec. III-A, Eq. 4 across workgroups): `pairs` producer workgroups each
+ * store `rounds` blocks of 1024 words with agent-coherent stores, wait for
+ * them to land and bump a per-block counter (relaxed, agent scope); as many
+ * consumer workgroups, each reading the blocks of a producer dealt to
+ * another XCD, poll the counter (bounded, 1 s) and check every word.
+ * mode 0: agent-coherent loads (buffers reused within a launch); mode 1:
+ * ordinary cached loads of addresses written once per launch.
+ * *mismatches receives the number of words read wrong (0 when the exchange
+ * is coherent).  Synchronous (returns after the kernel finished on
+ * `stream`).  Errors: WF_E_INVALID, WF_E_UNSUPPORTED (more workgroups than
+ * can be resident), WF_E_NOMEM, WF_E_TIMEOUT (a consumer waited too long).
+ */
+int wf_litmus(int32_t mode, int32_t pairs, int32_t rounds, uint64_t *mismatches, hipStream_t stream);
 
 /*
  * Decode (Sec. III-A, Eq. 2 evaluated in the wavefront order of Eq. 4; the

@@ -55,8 +55,8 @@ __device__ __forceinline__ unsigned* df_slot(unsigned* cnt, int g, int x) {
     return cnt + ((size_t)g * kXcds + x) * kDfSlotWords;
 }
 
-__device__ __forceinline__ int df_group(const DfArgs& d, int t, int kind, int rt) {
-    return (t * kJobKinds + kind) * (d.nrt_max + 1) + rt;
+__host__ __device__ __forceinline__ int df_group(int nrt_max, int t, int kind, int rt) {
+    return (t * kJobKinds + kind) * (nrt_max + 1) + rt;
 }
 
 // Jobs of one wait: counter group g must reach, in every class x, mult times
@@ -64,6 +64,48 @@ __device__ __forceinline__ int df_group(const DfArgs& d, int t, int kind, int rt
 struct DfWait {
     int g, lo, hi, mult;
 };
+
+// The plan constants the waits depend on.
+struct DfGeom {
+    int H, W, B, lambda, nrt_max, G, nct_ctx, nct_a, nct_b, npx;
+};
+
+// The waits of job (t, kind, rt): at most three, into w; returns their
+// number.  (Host and device: the kernel takes its waits from here, and the
+// race checks of the test suite read the same ones through wf_plan_deps.)
+__host__ __device__ __forceinline__ int df_waits(const DfGeom& g, int t, int kind, int rt, DfWait (&w)[3]) {
+    int nw = 0;
+    auto step_total = [&](int tt, int k, int lo, int hi) {
+        const int nrt = ntiles(step_rows(g.H, g.W, g.B, g.lambda, tt).nrows);
+        w[nw++] = DfWait{df_group(g.nrt_max, tt, k, g.nrt_max), lo, hi, nrt};
+    };
+    switch (kind) {
+        case JK_CTX:
+            if (t >= 2) step_total(t - 2, JK_C0, 0, g.G);
+            break;
+        case JK_CTXL:
+            w[nw++] = DfWait{df_group(g.nrt_max, t, JK_CTX, rt), 0, g.nct_ctx, g.npx};
+            break;
+        case JK_A:
+            w[nw++] = DfWait{df_group(g.nrt_max, t, JK_CTXL, rt), 0, g.nct_ctx, 1};
+            if (t >= 1) step_total(t - 1, JK_C0, 0, g.G);
+            break;
+        case JK_B:
+            w[nw++] = DfWait{df_group(g.nrt_max, t, JK_A, rt), 0, g.nct_a, 1};
+            if (t >= 2) step_total(t - 2, JK_C1, g.G, 2 * g.G);
+            break;
+        default:   // JK_C0, JK_C1
+            w[nw++] = DfWait{df_group(g.nrt_max, t, JK_B, rt), 0, g.nct_b, 1};
+            break;
+    }
+    return nw;
+}
+// The plan constants of the waits, for job columns of C column tiles.
+__host__ __device__ __forceinline__ DfGeom df_geom(const StepArgs& a, int nrt_max, int C) {
+    const int nct_n = 2 * a.M / kTile / C;
+    return DfGeom{a.H, a.W, a.B, a.lambda, nrt_max, a.M / kTile, a.n_old > 0 ? nct_n : 0, a.Np1 / kTile / C,
+                  a.Np2 / kTile / C, a.ctx_parts - 1};
+}
 
 // Wave 0 polls the (up to 3) waits; lanes 0..7 each watch one class.  A wait
 // longer than `budget` wall-clock ticks, or an error recorded by another
@@ -74,7 +116,8 @@ __device__ __forceinline__ bool df_wait_all(const DfArgs& d, const DfWait* w, in
         const int lane = threadIdx.x;
         int flag = 0;
         for (int i = 0; i < nw && !flag; ++i) {
-            const unsigned tgt = lane < kXcds ? (unsigned)(w[i].mult * cnt_range(w[i].lo, w[i].hi, lane)) : 0u;
+            const unsigned tgt =
+                lane < kXcds ? (unsigned)(w[i].mult * cnt_range(w[i].lo, w[i].hi, lane) + d.stall) : 0u;
             const unsigned* p = df_slot(d.cnt, w[i].g, lane & (kXcds - 1));
             const long long t0 = wall_clock64();
             unsigned it = 0;
@@ -116,40 +159,13 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2))
     const int li = crit ? x : kXcds + x;
     const int2* list = d.jobs + d.off[li];
     const int n = d.off[li + 1] - d.off[li];
-    const int G = a.M / kTile;                           // mean (and scale) column tiles of layer 3
-    const int nct_n = 2 * a.M / kTile / P::kC;           // column groups of the context products
-    const int nct_ctx = a.n_old > 0 ? nct_n : 0;         // (the old-tap part exists unless no tap is old)
-    const int nct_a = a.Np1 / kTile / P::kC, nct_b = a.Np2 / kTile / P::kC;
-    const int NPX = a.ctx_parts - 1;                     // CTX parts (the last one is CTXL)
+    const DfGeom geo = df_geom(a, d.nrt_max, P::kC);
     for (int p = lw; p < n; p += nwg) {
         const int2 c = list[p];
         const int t = c.x, kind = c.y & 15, part = (c.y >> 4) & 15, rt = (c.y >> 8) & 255, ct = c.y >> 16;
         const StepRows s = step_rows(a.H, a.W, a.B, a.lambda, t);
         DfWait w[3];
-        int nw = 0;
-        auto step_total = [&](int tt, int k, int lo, int hi) {
-            const int nrt = ntiles(step_rows(a.H, a.W, a.B, a.lambda, tt).nrows);
-            w[nw++] = DfWait{df_group(d, tt, k, d.nrt_max), lo, hi, nrt};
-        };
-        switch (kind) {
-            case JK_CTX:
-                if (t >= 2) step_total(t - 2, JK_C0, 0, G);
-                break;
-            case JK_CTXL:
-                w[nw++] = DfWait{df_group(d, t, JK_CTX, rt), 0, nct_ctx, NPX};
-                break;
-            case JK_A:
-                w[nw++] = DfWait{df_group(d, t, JK_CTXL, rt), 0, nct_ctx, 1};
-                if (t >= 1) step_total(t - 1, JK_C0, 0, G);
-                break;
-            case JK_B:
-                w[nw++] = DfWait{df_group(d, t, JK_A, rt), 0, nct_a, 1};
-                if (t >= 2) step_total(t - 2, JK_C1, G, 2 * G);
-                break;
-            default:   // JK_C0, JK_C1
-                w[nw++] = DfWait{df_group(d, t, JK_B, rt), 0, nct_b, 1};
-                break;
-        }
+        const int nw = df_waits(geo, t, kind, rt, w);
         const long long e = 3LL * (d.off[li] + p);
         const bool rec = d.stamps && e + 2 < d.stamps_cap && threadIdx.x == 0;
         if (rec) d.stamps[e] = wall_clock64();
@@ -178,11 +194,11 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2))
         if (rec) d.stamps[e + 2] = wall_clock64();
         if (threadIdx.x == 0) {
             const int cx = ct % kXcds;
-            __hip_atomic_fetch_add(df_slot(d.cnt, df_group(d, t, kind, rt), cx), 1u, __ATOMIC_RELAXED,
+            __hip_atomic_fetch_add(df_slot(d.cnt, df_group(d.nrt_max, t, kind, rt), cx), 1u, __ATOMIC_RELAXED,
                                    __HIP_MEMORY_SCOPE_AGENT);
             if (kind == JK_C0 || kind == JK_C1)
-                __hip_atomic_fetch_add(df_slot(d.cnt, df_group(d, t, kind, d.nrt_max), cx), 1u, __ATOMIC_RELAXED,
-                                       __HIP_MEMORY_SCOPE_AGENT);
+                __hip_atomic_fetch_add(df_slot(d.cnt, df_group(d.nrt_max, t, kind, d.nrt_max), cx), 1u,
+                                       __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
         }
     }
 }
@@ -201,7 +217,7 @@ const void* dataflow_fn(const Plan& p) {
 }
 
 // The job lists of a plan, in the topological order described above.
-int build_dataflow(Plan& p, std::vector<int2>& lists, DfArgs& d) {
+int build_dataflow(Plan& p, std::vector<int2>& lists, DfArgs& d, std::vector<int>* order) {
     const StepArgs& a = p.args;
     const bool bf = p.precision == WF_BF16;
     const int C = bf ? kColsBf16 : kColsF32;
@@ -211,9 +227,12 @@ int build_dataflow(Plan& p, std::vector<int2>& lists, DfArgs& d) {
     const int nct_ctx = a.n_old > 0 ? nct_n : 0;
     const int nct_a = p.Np1 / kTile / C, nct_b = p.Np2 / kTile / C, nct_c = 2 * (p.M / kTile);
     std::vector<std::vector<int2>> q(2 * kXcds);
+    std::vector<std::vector<int>> qo(2 * kXcds);   // each entry's position in the global order
+    int nglobal = 0;
     auto push = [&](int t, int kind, int part, int rt, int ct) {
         const int pool = kind == JK_CTX || kind == JK_CTXL ? 1 : 0;
         q[pool * kXcds + ct % kXcds].push_back(int2{t, kind | (part << 4) | (rt << 8) | (ct << 16)});
+        qo[pool * kXcds + ct % kXcds].push_back(nglobal++);
     };
     auto nrt = [&](int t) { return ntiles(step_rows(p.H, p.W, p.B, p.lambda, t).nrows); };
     auto tiles = [&](int t, int kind, int part, int lo, int hi) {
@@ -234,9 +253,11 @@ int build_dataflow(Plan& p, std::vector<int2>& lists, DfArgs& d) {
         tiles(t, JK_C1, 0, nct_c / 2, nct_c);
     }
     lists.clear();
+    if (order) order->clear();
     d.off[0] = 0;
     for (int x = 0; x < 2 * kXcds; ++x) {
         lists.insert(lists.end(), q[x].begin(), q[x].end());
+        if (order) order->insert(order->end(), qo[x].begin(), qo[x].end());
         if (lists.size() > (size_t)INT32_MAX) return fail(WF_E_UNSUPPORTED, "too many dataflow jobs");
         d.off[x + 1] = (int)lists.size();
     }
@@ -257,11 +278,42 @@ int enqueue_dataflow(Plan& p, hipStream_t stream) {
     DfArgs d = p.df;
     d.stamps = p.stamps;
     d.stamps_cap = p.stamps_cap;
+    d.stall = p.stall;
     int* err = p.d_err;
     long long budget = p.spin_budget;
     void* args[] = {&a, &d, &err, &budget};
     hipError_t e = hipLaunchCooperativeKernel(dataflow_fn(p), dim3(p.grid), dim3(kThreads), args, 0, stream);
     if (e != hipSuccess) return fail(WF_E_HIP, std::string("cooperative launch: ") + hipGetErrorString(e));
+    return WF_OK;
+}
+
+// The job lists and waits of a plan's geometry (host only, for the race
+// checks): per job in list order, {t, kind, part, rt, ct, list, global
+// position, number of waits, then three (group, lo, hi, mult)}; the counter
+// groups it bumps are (t, kind, rt) and, for C0 and C1, (t, kind, nrt_max).
+int dataflow_deps(Plan& p, std::vector<int32_t>& out) {
+    std::vector<int2> lists;
+    std::vector<int> order;
+    DfArgs d{};
+    int rc = build_dataflow(p, lists, d, &order);
+    if (rc != WF_OK) return rc;
+    const int C = p.precision == WF_BF16 ? kColsBf16 : kColsF32;
+    const DfGeom geo = df_geom(p.args, d.nrt_max, C);
+    out.clear();
+    for (int li = 0; li < 2 * kXcds; ++li)
+        for (int e = d.off[li]; e < d.off[li + 1]; ++e) {
+            const int2 c = lists[e];
+            const int t = c.x, kind = c.y & 15, part = (c.y >> 4) & 15, rt = (c.y >> 8) & 255, ct = c.y >> 16;
+            DfWait w[3] = {};
+            const int nw = df_waits(geo, t, kind, rt, w);
+            const int32_t head[8] = {t, kind, part, rt, ct, li, order[e], nw};
+            out.insert(out.end(), head, head + 8);
+            for (int i = 0; i < 3; ++i) {
+                const int32_t q[4] = {w[i].g, w[i].lo, w[i].hi, w[i].mult};
+                out.insert(out.end(), q, q + 4);
+            }
+        }
+    out.push_back(d.nrt_max);   // the last entry: nrt_max
     return WF_OK;
 }
 

@@ -71,6 +71,7 @@ struct DfArgs {
     int nrt_max;            // 16-row tiles of the widest step
     long long* stamps;      // optional trace: 3 wall-clock ticks per job (see wf_plan_trace)
     long long stamps_cap;
+    int stall;              // test hook: every wait's target one more than it can reach
 };
 
 // Resident driver (see wf_resident.hip): roles of its workgroups, in this
@@ -107,6 +108,7 @@ struct ResArgs {
     long long* stamps;          // optional trace: 3 wall-clock ticks per task and workgroup
     long long stamps_cap;
     int ntasks;                 // tasks of every workgroup (band visits of all steps and images)
+    int stall;                  // test hook: every wait's target one more than it can reach
 };
 
 // Set the calling thread's error message and return `code`.
@@ -180,7 +182,7 @@ struct StepArgs {
     // mask order: row_w taps in each of rows -R..-1 from dx = -R, then the R
     // taps (0,-R)..(0,-1)) with same-group taps filled, in gparts k-parts.
     int group, row_w, gparts;
-    int ec;                 // 1: phase C decodes each symbol from its rANS stream (K = 1)
+    int ec;                 // 1: phase C decodes each symbol from its rANS stream
     const int* rowlat;      // nullptr: rows of wavefront t by grid row
     const void* wp_all;     // packed Wc over all taps, channel-chunk-major k   [2M/16][(n_old+2)*M/kb]
     const void* wp_hoist;   // packed W1[:, :2M]                           [Np1/16][2M/kb]
@@ -231,6 +233,8 @@ struct Plan {
     unsigned* d_bar = nullptr;
     int grid = 0;
     long long spin_budget = 100000000;   // wall-clock ticks (100 MHz): 1 s
+    int stall = 0;                        // test hook: every in-launch wait unreachable
+    int cu_limit = 0;                     // plan for at most this many CUs (0: all)
     long long* stamps = nullptr;         // optional barrier trace
     long long stamps_cap = 0;
     // dataflow driver
@@ -279,11 +283,16 @@ int enqueue_hoist(Plan& p, hipStream_t stream);
 int persistent_grid(Plan& p, int* grid);
 int enqueue_persistent(Plan& p, hipStream_t stream);
 // Dataflow driver: job lists of the plan, and one call.
-int build_dataflow(Plan& p, std::vector<int2>& lists, DfArgs& d);
+// (order: optionally each list entry's position in the global order)
+int build_dataflow(Plan& p, std::vector<int2>& lists, DfArgs& d, std::vector<int>* order = nullptr);
+// Job lists and waits of a plan's geometry, flattened (host only; wf_plan_deps).
+int dataflow_deps(Plan& p, std::vector<int32_t>& out);
 int enqueue_dataflow(Plan& p, hipStream_t stream);
 const void* dataflow_fn(const Plan& p);
 // Resident driver: roles and buffers of the plan, and one call.
 int build_resident(Plan& p);
+// Tasks and waits of a plan's geometry, flattened (host only; wf_plan_deps).
+int resident_deps(const Plan& p, std::vector<int32_t>& out);
 int enqueue_resident(Plan& p, hipStream_t stream);
 // Grid of a cooperative kernel: two workgroups per CU when they fit, else one.
 int coop_grid(Plan& p, const void* fn, int* grid);

@@ -18,6 +18,7 @@ namespace wf {
 struct Trace {
     long long* stamps;   // optional: arrival/leave wall-clock ticks per barrier
     long long cap;
+    unsigned stall;      // test hook: 1 makes every barrier wait unreachable
 };
 
 __device__ __forceinline__ bool grid_barrier(unsigned* ctr, unsigned k, int* err, long long budget,
@@ -37,7 +38,7 @@ __device__ __forceinline__ bool grid_barrier(unsigned* ctr, unsigned k, int* err
         int flag = 0;
         const long long t0 = wall_clock64();
         unsigned it = 0;
-        while (__hip_atomic_load(ctr, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) < k * ng) {
+        while (__hip_atomic_load(ctr, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) < k * ng + tr.stall) {
             if ((++it & 255u) == 0) {
                 if (__hip_atomic_load(err, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) != 0) {
                     flag = 1;
@@ -117,14 +118,15 @@ static const void* persistent_fn(const Plan& p) {
 int persistent_grid(Plan& p, int* grid) { return coop_grid(p, persistent_fn(p), grid); }
 
 int coop_grid(Plan& p, const void* fn, int* grid) {
-    (void)p;
     int dev = 0, cus = 0, per_cu = 0;
     hipError_t e = hipGetDevice(&dev);
     if (e == hipSuccess) e = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);
     if (e == hipSuccess)
         e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, fn, kThreads, 0);
     if (e != hipSuccess) return fail(WF_E_HIP, std::string("occupancy query: ") + hipGetErrorString(e));
-    if (per_cu < 1 || cus < kXcds) return fail(WF_E_UNSUPPORTED, "persistent kernel cannot be resident");
+    if (p.cu_limit > 0 && p.cu_limit < cus) cus = p.cu_limit;
+    if (per_cu < 1 || cus < kXcds)
+        return fail(WF_E_UNSUPPORTED, "cooperative kernel cannot be resident (fewer than 8 compute units)");
     *grid = cus * (per_cu >= 2 ? 2 : 1) / kXcds * kXcds;
     return WF_OK;
 }
@@ -136,7 +138,7 @@ int enqueue_persistent(Plan& p, hipStream_t stream) {
     unsigned* ctr = p.d_bar;
     int* err = p.d_err;
     long long budget = p.spin_budget;
-    Trace tr{p.stamps, p.stamps_cap};
+    Trace tr{p.stamps, p.stamps_cap, (unsigned)p.stall};
     void* args[] = {&a, &T, &ctr, &err, &budget, &tr};
     hipError_t e = hipLaunchCooperativeKernel(persistent_fn(p), dim3(p.grid), dim3(kThreads), args, 0, stream);
     if (e != hipSuccess) return fail(WF_E_HIP, std::string("cooperative launch: ") + hipGetErrorString(e));
@@ -150,7 +152,7 @@ __global__ void k_empty(int* p) {
 // `rounds` empty device-wide barrier rounds over the whole grid.
 __global__ __launch_bounds__(kThreads) void k_barrier_rounds(unsigned* ctr, int* err, long long budget, int rounds) {
     __shared__ int bail;
-    const Trace tr{nullptr, 0};
+    const Trace tr{nullptr, 0, 0u};
     for (int r = 1; r <= rounds; ++r)
         if (!grid_barrier(ctr, (unsigned)r, err, budget, &bail, tr)) return;
 }

@@ -115,6 +115,7 @@ static int check_desc(const wf_desc* d) {
     if (d->group > 1 && d->driver != WF_DRIVER_STREAM && d->driver != WF_DRIVER_GRAPH)
         return fail(WF_E_UNSUPPORTED, "context approximation (group > 1) needs the stream or graph driver");
     if (d->M % kTile != 0) return fail(WF_E_UNSUPPORTED, "M must be a multiple of 16");
+    if (d->cu_limit < 0) return fail(WF_E_INVALID, "cu_limit must be >= 0");
     int dy[kMaxTaps], dx[kMaxTaps];
     int nt = mask_taps(d->mask, dy, dx);
     int lam = least_shear(nt, dy, dx);
@@ -182,11 +183,14 @@ static void fold_tap(const wf_desc* d, int dy, int dx, bool bf, std::vector<doub
     }
 }
 
-static int build_plan(const wf_desc* d, Plan* p) {
+// geometry_only: stop after the schedule, the tap split and the step
+// arguments (host only; nothing is allocated on the device).
+static int build_plan(const wf_desc* d, Plan* p, bool geometry_only = false) {
     p->H = d->H; p->W = d->W; p->M = d->M; p->B = d->B; p->K = d->K;
     p->d1 = d->d1; p->d2 = d->d2; p->n3 = (d->K == 1 ? 2 : 9) * d->M;
     p->mask = d->mask; p->precision = d->precision; p->driver = d->driver;
     p->L = d->L; p->slope = d->lrelu_slope;
+    p->cu_limit = d->cu_limit;
     p->ntaps = mask_taps(d->mask, p->dy, p->dx);
     p->lambda = schedule_shear(least_shear(p->ntaps, p->dy, p->dx), d->W);
     const int H = p->H, W = p->W, M = p->M, lam = p->lambda;
@@ -282,6 +286,7 @@ static int build_plan(const wf_desc* d, Plan* p) {
     }
     if (p->dy[new_taps[0]] != -1 || p->dy[new_taps[1]] != 0 || p->dx[new_taps[1]] != -1)
         return fail(WF_E_UNSUPPORTED, "unexpected new taps");
+    if (geometry_only) return WF_OK;
 
     WF_HIP(hipGetDevice(&p->device));
     int rc;
@@ -513,6 +518,39 @@ int wf_plan(const wf_desc* desc, wf_plan_t* out) {
         return rc;
     }
     *out = reinterpret_cast<wf_plan_t>(p);
+    return WF_OK;
+}
+
+int wf_plan_deps(const wf_desc* desc, int32_t* out, int64_t capacity, int64_t* needed) {
+    if (!needed) return fail(WF_E_INVALID, "needed is NULL");
+    int rc = check_desc(desc);
+    if (rc != WF_OK) return rc;
+    if (desc->driver != WF_DRIVER_DATAFLOW && desc->driver != WF_DRIVER_RESIDENT)
+        return fail(WF_E_UNSUPPORTED, "dependency lists exist for the dataflow and resident drivers");
+    if (capacity < 0) return fail(WF_E_INVALID, "negative capacity");
+    Plan p;
+    std::vector<int32_t> v;
+    try {
+        rc = build_plan(desc, &p, true);
+        if (rc == WF_OK) rc = desc->driver == WF_DRIVER_DATAFLOW ? dataflow_deps(p, v) : resident_deps(p, v);
+    } catch (const std::bad_alloc&) {
+        rc = fail(WF_E_NOMEM, "host allocation failed");
+    }
+    if (rc != WF_OK) return rc;
+    *needed = (int64_t)v.size();
+    if (out) {
+        if (capacity < (int64_t)v.size()) return fail(WF_E_INVALID, "out holds fewer entries than needed");
+        std::copy(v.begin(), v.end(), out);
+    }
+    return WF_OK;
+}
+
+int wf_plan_set_waits(wf_plan_t plan, int64_t spin_budget_ticks, int32_t stall) {
+    if (!plan) return fail(WF_E_INVALID, "plan is NULL");
+    if (stall != 0 && stall != 1) return fail(WF_E_INVALID, "stall must be 0 or 1");
+    Plan* p = reinterpret_cast<Plan*>(plan);
+    p->spin_budget = spin_budget_ticks > 0 ? spin_budget_ticks : 100000000;
+    p->stall = stall;
     return WF_OK;
 }
 

@@ -99,7 +99,7 @@ __device__ __forceinline__ ResArgs uni_args(const ResArgs& x) {
     WF_U(per_slot); WF_U(parts); WF_U(nrep); WF_U(nbands); WF_U(nbs); WF_U(cnt); WF_U(kbase); WF_U(ctx); WF_U(h1); WF_U(h2);
     WF_U(ytile);
     WF_U(err);
-    WF_U(stamps); WF_U(ntasks);
+    WF_U(stamps); WF_U(ntasks); WF_U(stall);
     for (int q = 0; q <= kResRoles; ++q) WF_U(first[q]);
 #undef WF_U
     r.budget = ((long long)uni((int)(x.budget >> 32)) << 32) | (unsigned)uni((int)x.budget);
@@ -115,16 +115,62 @@ __host__ __device__ __forceinline__ void band_span(int H, int W, int lam, int be
 }
 // Position in the global order of the latest task of band beta (image b) at
 // a step <= s, or -1 when the band has none (beta < 0, or s before its first).
-__device__ __forceinline__ int band_task(const StepArgs& a, const ResArgs& r, int b, int beta, int s) {
+// kbase[t]: the position of step t's first task (kbase[T]: the number of tasks).
+__host__ __device__ __forceinline__ int band_task_of(int H, int W, int lam, const int* kbase, int b, int beta, int s) {
     if (beta < 0 || s < 0) return -1;
     int t0, t1;
-    band_span(a.H, a.W, a.lambda, beta, t0, t1);
+    band_span(H, W, lam, beta, t0, t1);
     if (s < t0) return -1;
-    const int t = min(s, t1);
+    const int t = s < t1 ? s : t1;
     int i0, n;
-    step_span(a.H, a.W, a.lambda, t, i0, n);
+    step_span(H, W, lam, t, i0, n);
     const int blo = i0 / kTile, nb = (i0 + n - 1) / kTile - blo + 1;
-    return r.kbase[t] + b * nb + beta - blo;
+    return kbase[t] + b * nb + beta - blo;
+}
+
+// One wait: task k of `role` complete (nothing to wait for when k < 0).
+struct ResWait {
+    int role, k;
+};
+// The completions task k = (t, b, beta) of a role waits for (at most three;
+// host and device: the roles take their waits from here, and the race checks
+// of the test suite read the same ones through wf_plan_deps).  The old-tap
+// context of step t reads y_hat of steps <= t-2 in the band's rows and the
+// (up to R) rows above, the band above's at most: its latest tasks of step
+// t-2 (each implies every earlier task of its band: C0(t') <- B(t') <- A(t')
+// <- C0 of the band at t'-1).  Layer 1 reads the two new taps, from step t-1
+// (the band's task and the band above's), and the task's context; layers 2
+// and 3 the layer before of the same task.
+struct ResDeps {
+    ResWait w[3];
+};
+__host__ __device__ __forceinline__ ResDeps res_deps(int H, int W, int lam, const int* kbase, int role, int t, int b,
+                                                     int beta, int k) {
+    ResDeps d{{{0, -1}, {0, -1}, {0, -1}}};
+    switch (role) {
+        case RR_CTX:
+        case RR_CTXL:
+            d.w[0] = ResWait{RR_C0, band_task_of(H, W, lam, kbase, b, beta, t - 2)};
+            d.w[1] = ResWait{RR_C0, band_task_of(H, W, lam, kbase, b, beta - 1, t - 2)};
+            if (role == RR_CTXL) d.w[2] = ResWait{RR_CTX, k};   // the other parts, which it adds
+            break;
+        case RR_A:
+            d.w[0] = ResWait{RR_CTXL, k};
+            d.w[1] = ResWait{RR_C0, band_task_of(H, W, lam, kbase, b, beta, t - 1)};
+            d.w[2] = ResWait{RR_C0, band_task_of(H, W, lam, kbase, b, beta - 1, t - 1)};
+            break;
+        case RR_B:
+            d.w[0] = ResWait{RR_A, k};
+            break;
+        default:   // RR_C0, RR_C1
+            d.w[0] = ResWait{RR_B, k};
+            break;
+    }
+    return d;
+}
+__device__ __forceinline__ ResDeps res_deps(const StepArgs& a, const ResArgs& r, int role, int t, int b, int beta,
+                                            int k) {
+    return res_deps(a.H, a.W, a.lambda, r.kbase, role, t, b, beta, k);
 }
 
 // Row r of band beta of image b at step t.
@@ -142,11 +188,6 @@ __device__ __forceinline__ unsigned* res_slot(const ResArgs& r, int role, int k,
     return r.cnt + (((size_t)role * r.ntasks + k) * kXcds + x) * kDfSlotWords;
 }
 
-// One wait: task k of `role` complete (nothing to wait for when k < 0).
-struct ResWait {
-    int role, k;
-};
-
 // Wave 0 polls up to three waits, eight lanes each (one per XCD class).  A
 // wait longer than the budget, or an error recorded elsewhere, makes the
 // workgroup leave (returns false).
@@ -157,7 +198,7 @@ __device__ __forceinline__ bool res_wait(const ResArgs& r, ResWait w0, ResWait w
         unsigned tgt = 0;
         const unsigned* p = r.cnt;
         if (i < 3 && w.k >= 0) {
-            tgt = (unsigned)r.per_slot[(w.role * kResRep + w.k % r.nrep) * kXcds + x];
+            tgt = (unsigned)r.per_slot[(w.role * kResRep + w.k % r.nrep) * kXcds + x] + (unsigned)r.stall;
             p = res_slot(r, w.role, w.k, x);
         }
         int flag = 0;
@@ -456,9 +497,8 @@ __device__ __noinline__ void res_ctx(const StepArgs& a_in, const ResArgs& r_in, 
     const int skb0 = __builtin_amdgcn_readfirstlane(s.kb0);
     for_tasks(a, T, rep, r.nrep, [&](int t, int b, int beta, int k) {
         res_stamp(r, k, 0);
-        if (!res_wait(r, ResWait{RR_C0, band_task(a, r, b, beta, t - 2)},
-                      ResWait{RR_C0, band_task(a, r, b, beta - 1, t - 2)}, ResWait{RR_CTX, LAST ? k : -1}, bail))
-            return false;
+        const ResDeps dp = res_deps(a, r, LAST ? RR_CTXL : RR_CTX, t, b, beta, k);
+        if (!res_wait(r, dp.w[0], dp.w[1], dp.w[2], bail)) return false;
         res_stamp(r, k, 1);
         const size_t e = ctx_base(a, r, k, 0) + tile_idx<PF32>(ro, col, 2 * a.M);
         // the other parts of this element (the last part adds them)
@@ -530,9 +570,9 @@ __device__ __noinline__ void res_l1(const StepArgs& a_in, const ResArgs& r_in, i
         const Row v = band_row(a, b, beta, t, ro);
         const float z = ld1<false>(a.p1, v.lat * a.Np1 + col, v.valid);
         res_stamp(r, k, 0);
-        const int kself = band_task(a, r, b, beta, t - 1), kup = band_task(a, r, b, beta - 1, t - 1);
-        if (!res_wait(r, ResWait{RR_CTXL, k}, ResWait{RR_C0, kself}, ResWait{RR_C0, kup}, bail))
-            return false;
+        const ResDeps dp = res_deps(a, r, RR_A, t, b, beta, k);
+        const int kself = dp.w[1].k, kup = dp.w[2].k;   // the new taps' tasks
+        if (!res_wait(r, dp.w[0], dp.w[1], dp.w[2], bail)) return false;
         res_stamp(r, k, 1);
         const Row w = band_row(a, b, beta, t, lane & 15);
         const NewSrc ns = new_src<P>(a, w, kself, kup);
@@ -627,8 +667,8 @@ __device__ __noinline__ void res_l2(const StepArgs& a_in, const ResArgs& r_in, i
     for_tasks(a, T, rep, r.nrep, [&](int t, int b, int beta, int k) {
         const int bs = b * r.nbands + beta;
         res_stamp(r, k, 0);
-        if (!res_wait(r, ResWait{RR_A, k}, ResWait{0, -1}, ResWait{0, -1}, bail))
-            return false;
+        const ResDeps dp = res_deps(a, r, RR_B, t, b, beta, k);
+        if (!res_wait(r, dp.w[0], dp.w[1], dp.w[2], bail)) return false;
         res_stamp(r, k, 1);
         const Row w = band_row(a, b, beta, t, lane & 15);
         const char* h1 = static_cast<const char*>(r.h1) + k * h1s;
@@ -681,8 +721,8 @@ __device__ __noinline__ void res_l3(const StepArgs& a_in, const ResArgs& r_in, i
         float sin = 0.0f;
         if (MEAN && v.valid) sin = cp->encode ? cp->y[oq] : (float)cp->sym[oq];
         res_stamp(r, k, 0);
-        if (!res_wait(r, ResWait{RR_B, k}, ResWait{0, -1}, ResWait{0, -1}, bail))
-            return false;
+        const ResDeps dp = res_deps(a, r, MEAN ? RR_C0 : RR_C1, t, b, beta, k);
+        if (!res_wait(r, dp.w[0], dp.w[1], dp.w[2], bail)) return false;
         res_stamp(r, k, 1);
         const Row w = band_row(a, b, beta, t, lane & 15);
         const char* h2 = static_cast<const char*>(r.h2) + k * h2s;
@@ -809,6 +849,49 @@ static int res_alloc(Plan& p, T** dst, size_t n) {
 
 static int ceil_div(int a, int b) { return (a + b - 1) / b; }
 
+// kbase[t] = the position of step t's first task in the global order (t, b,
+// band), kbase[T] = the number of tasks; returns that number.
+static long long res_kbase(const Plan& p, std::vector<int>& kbase) {
+    kbase.assign(p.T + 1, 0);
+    long long tasks = 0;
+    for (int t = 0; t < p.T; ++t) {
+        int i0, nn;
+        step_span(p.H, p.W, p.lambda, t, i0, nn);
+        kbase[t] = (int)tasks;
+        tasks += (long long)p.B * ((i0 + nn - 1) / kTile - i0 / kTile + 1);
+    }
+    kbase[p.T] = (int)tasks;
+    return tasks;
+}
+
+// The tasks and waits of a plan's geometry (host only, for the race checks):
+// per task in the global order {t, b, band, then for each role its three
+// waits as (role, task)}.
+int resident_deps(const Plan& p, std::vector<int32_t>& out) {
+    std::vector<int> kbase;
+    const long long tasks = res_kbase(p, kbase);
+    if (tasks > INT32_MAX / 64) return fail(WF_E_UNSUPPORTED, "too many resident tasks");
+    out.clear();
+    int k = 0;
+    for (int t = 0; t < p.T; ++t) {
+        int i0, n;
+        step_span(p.H, p.W, p.lambda, t, i0, n);
+        for (int b = 0; b < p.B; ++b)
+            for (int beta = i0 / kTile; beta <= (i0 + n - 1) / kTile; ++beta, ++k) {
+                const int32_t head[3] = {t, b, beta};
+                out.insert(out.end(), head, head + 3);
+                for (int role = 0; role < kResRoles; ++role) {
+                    const ResDeps d = res_deps(p.H, p.W, p.lambda, kbase.data(), role, t, b, beta, k);
+                    for (int i = 0; i < 3; ++i) {
+                        out.push_back(d.w[i].k >= 0 ? d.w[i].role : -1);
+                        out.push_back(d.w[i].k);
+                    }
+                }
+            }
+    }
+    return WF_OK;
+}
+
 int build_resident(Plan& p) {
     const StepArgs& a = p.args;
     ResArgs& r = p.res;
@@ -825,6 +908,7 @@ int build_resident(Plan& p) {
     hipError_t e = hipGetDevice(&dev);
     if (e == hipSuccess) e = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);
     if (e != hipSuccess) return fail(WF_E_HIP, std::string("device query: ") + hipGetErrorString(e));
+    if (p.cu_limit > 0 && p.cu_limit < cus) cus = p.cu_limit;
     const int crit = p.Np1 / kTile + p.Np2 / kTile + 2 * G;
     const int slots = kResRep * cus;   // two workgroups per compute unit
     // the fewest old-tap context parts whose slices fit the registers
@@ -870,15 +954,8 @@ int build_resident(Plan& p) {
     r.nbands = ceil_div(p.H, kTile);
     r.nbs = p.B * r.nbands;
     const size_t nbs = (size_t)r.nbs;
-    std::vector<int> kbase(p.T + 1);
-    long long tasks = 0;
-    for (int t = 0; t < p.T; ++t) {
-        int i0, nn;
-        step_span(p.H, p.W, p.lambda, t, i0, nn);
-        kbase[t] = (int)tasks;
-        tasks += (long long)p.B * ((i0 + nn - 1) / kTile - i0 / kTile + 1);
-    }
-    kbase[p.T] = (int)tasks;
+    std::vector<int> kbase;
+    const long long tasks = res_kbase(p, kbase);
     r.ntasks = (int)tasks;
     int* d_kbase = nullptr;
     if ((rc = res_alloc(p, &d_kbase, kbase.size())) != WF_OK) return rc;
@@ -915,6 +992,8 @@ int enqueue_resident(Plan& p, hipStream_t stream) {
     ResArgs r = p.res;
     r.stamps = p.stamps;
     r.stamps_cap = p.stamps_cap;
+    r.budget = p.spin_budget;
+    r.stall = p.stall;
     const size_t ncnt = (size_t)kResRoles * r.ntasks * kXcds * kDfSlotWords;
     hipLaunchKernelGGL(k_res_zero, dim3(1024), dim3(256), 0, stream, r.cnt, ncnt);
     int rc = enqueue_hoist(p, stream);

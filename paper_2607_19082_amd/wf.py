@@ -21,7 +21,7 @@ KERNEL = {"full": 5, "relaxed": 5, "3x3": 3, "7x7": 7}   # ctx_w's spatial size 
 PRECISION = {"fp32": 0, "bf16": 1}
 DRIVER = {"stream": 0, "graph": 1, "persistent": 2, "dataflow": 3, "resident": 4}
 
-EXPORTS = ["wf_schedule", "wf_validate", "wf_plan", "wf_plan_schedule", "wf_decode",
+EXPORTS = ["wf_schedule", "wf_validate", "wf_plan", "wf_plan_schedule", "wf_plan_deps", "wf_plan_set_waits", "wf_litmus", "wf_decode",
            "wf_encode", "wf_ec_tables", "wf_mix_tables", "wf_encode_bits", "wf_decode_bits", "wf_plan_trace",
            "wf_measure_floor", "wf_plan_sync", "wf_xform_plan", "wf_hyper_synthesis", "wf_synthesis",
            "wf_decode_noalloc", "wf_xform_destroy", "wf_plan_destroy", "wf_last_error"]
@@ -46,7 +46,7 @@ class Desc(ctypes.Structure):
         ("w3", ctypes.c_void_p), ("b3", ctypes.c_void_p),
         ("scale_table", ctypes.c_void_p), ("L", ctypes.c_int32),
         ("group", ctypes.c_int32), ("param_order", ctypes.c_int32),
-        ("entropy_coder", ctypes.c_int32),
+        ("entropy_coder", ctypes.c_int32), ("cu_limit", ctypes.c_int32),
     ]
 
 
@@ -82,6 +82,9 @@ def lib():
         L.wf_validate.argtypes = [ctypes.POINTER(Desc)]
         L.wf_plan.argtypes = [ctypes.POINTER(Desc), ctypes.POINTER(ctypes.c_void_p)]
         L.wf_plan_schedule.argtypes = [P, P, P]
+        L.wf_plan_deps.argtypes = [ctypes.POINTER(Desc), P, ctypes.c_int64, P]
+        L.wf_litmus.argtypes = [ctypes.c_int32, ctypes.c_int32, ctypes.c_int32, P, P]
+        L.wf_plan_set_waits.argtypes = [P, ctypes.c_int64, ctypes.c_int32]
         L.wf_decode.argtypes = [P, P, P, ctypes.POINTER(Out), P]
         L.wf_decode_noalloc.argtypes = [P, P, P, ctypes.POINTER(Out), P]
         L.wf_encode.argtypes = [P, P, P, P, ctypes.POINTER(Out), P]
@@ -121,7 +124,7 @@ def schedule(H, W, mask="full"):
 
 
 def make_desc(weights, table, H, W, B=1, K=1, mask="full", precision="fp32", driver="stream",
-              slope=0.01, group=1, param_order="native", entropy_coder=None):
+              slope=0.01, group=1, param_order="native", entropy_coder=None, cu_limit=0):
     """Build a Desc plus the host arrays it points to (keep both alive)."""
     arrs = {k: np.ascontiguousarray(v, dtype=np.float32) for k, v in weights.items()}
     arrs["table"] = np.ascontiguousarray(table, dtype=np.float32)
@@ -136,7 +139,7 @@ def make_desc(weights, table, H, W, B=1, K=1, mask="full", precision="fp32", dri
              arrs["w2"].ctypes.data, arrs["b2"].ctypes.data,
              arrs["w3"].ctypes.data, arrs["b3"].ctypes.data,
              arrs["table"].ctypes.data, len(arrs["table"]), group, PARAM_ORDER[param_order],
-             ENTROPY_CODER[entropy_coder])
+             ENTROPY_CODER[entropy_coder], cu_limit)
     return d, arrs
 
 
@@ -156,9 +159,9 @@ class Plan:
     current) torch stream."""
 
     def __init__(self, weights, table, H, W, B=1, K=1, mask="full", precision="fp32",
-                 driver="stream", slope=0.01, group=1, param_order="native", entropy_coder=None):
+                 driver="stream", slope=0.01, group=1, param_order="native", entropy_coder=None, cu_limit=0):
         self.desc, self._arrs = make_desc(weights, table, H, W, B, K, mask, precision, driver, slope, group,
-                                          param_order, entropy_coder)
+                                          param_order, entropy_coder, cu_limit)
         self.group = group
         self.H, self.W, self.B, self.K = H, W, B, K
         self.M = self.desc.M
@@ -177,6 +180,11 @@ class Plan:
             self.close()
         except Exception:
             pass
+
+    def set_waits(self, spin_budget_ticks=0, stall=0):
+        """The in-launch drivers' wait budget (100 MHz ticks; 0: 1 s) and the
+        stall test hook (wf_plan_set_waits), for the calls that follow."""
+        _check(lib().wf_plan_set_waits(self._h, int(spin_budget_ticks), int(stall)))
 
     def schedule(self):
         step = np.zeros((self.H, self.W), np.int32)
@@ -328,6 +336,24 @@ def ec_tables(table):
     cum = np.zeros(int(base[-1]), np.uint32)
     _check(lib().wf_ec_tables(table.ctypes.data, L, None, None, cum.ctypes.data, len(cum)))
     return n, base, cum
+
+
+def plan_deps(desc):
+    """The dependency lists of the dataflow or resident driver for a plan
+    description (host only): the flat int32 array of wf_plan_deps."""
+    n = ctypes.c_int64(0)
+    _check(lib().wf_plan_deps(ctypes.byref(desc), None, 0, ctypes.byref(n)))
+    out = np.zeros(n.value, np.int32)
+    _check(lib().wf_plan_deps(ctypes.byref(desc), out.ctypes.data, len(out), ctypes.byref(n)))
+    return out
+
+
+def litmus(mode, pairs, rounds, stream=None):
+    """The cross-XCD coherence litmus test (wf_litmus): the number of words
+    a consumer read wrong."""
+    n = ctypes.c_uint64(0)
+    _check(lib().wf_litmus(mode, pairs, rounds, ctypes.byref(n), _stream_handle(stream)))
+    return n.value
 
 
 def mix_tables(table):
