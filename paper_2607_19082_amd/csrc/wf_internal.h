@@ -40,7 +40,7 @@ constexpr int kColsF32 = 1;          // column tiles of one job, fp32 operands
 constexpr int kColsBf16 = 2;         // the same, bf16 operands
 constexpr int kMaxTable = 256;
 constexpr int kXcds = 8;             // accelerator complex dies of an MI355X
-constexpr int kBarrierWords = 512;   // barrier counters of the persistent driver
+constexpr int kBarrierWords = 4096;  // barrier counters of the persistent driver
 constexpr int kBufBytes = 0x7fff0000; // window of a raw buffer access (arrays must fit)
 constexpr int kDfSlotWords = 16;     // dataflow counter slots: one per 64 bytes
 

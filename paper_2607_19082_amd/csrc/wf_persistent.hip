@@ -9,10 +9,14 @@
 
 namespace wf {
 
-// Two-level barrier: the workgroups of residue class x = block % 8 count into
-// counter x; the last of them bumps the top counter, which every workgroup
-// waits on.  Counters only grow: barrier k completes when the top counter
-// reaches k * (number of classes).  A wait longer than `budget` wall-clock
+// Device-wide barrier, a three-level arrival tree and a release word per
+// XCD class.  Workgroup g counts into group counter q = g % 64 (at most
+// ceil(G / 64) arrivals per address); the last arrival of a group counts
+// into class counter q % 8, the last of a class into the top counter, and
+// the last arrival there publishes the round in eight release words, one per
+// class g % 8, which that class's workgroups poll (at most G / 8 pollers per
+// address).  Counters only grow: a round k completes when every level has
+// counted k times its arrivals.  A wait longer than `budget` wall-clock
 // ticks records WF_E_TIMEOUT in *err; every workgroup that sees a recorded
 // error leaves the kernel at its next barrier, so the grid always drains.
 struct Trace {
@@ -20,6 +24,15 @@ struct Trace {
     long long cap;
     unsigned stall;      // test hook: 1 makes every barrier wait unreachable
 };
+
+constexpr int kBarGroups = 64;                // first-level counters
+constexpr int kBarSlot = 32;                  // words between counters (128 bytes)
+// layout (in slots): groups [0, 64), classes [64, 72), top 72, release [73, 81)
+static_assert((kBarGroups + 2 * kXcds + 1) * kBarSlot <= kBarrierWords, "barrier words");
+
+__device__ __forceinline__ unsigned bar_count(unsigned G, unsigned q, unsigned stride) {
+    return q < G ? (G - q + stride - 1) / stride : 0u;   // members of residue class q modulo stride
+}
 
 __device__ __forceinline__ bool grid_barrier(unsigned* ctr, unsigned k, int* err, long long budget,
                                              int* bail, const Trace& tr) {
@@ -29,16 +42,24 @@ __device__ __forceinline__ bool grid_barrier(unsigned* ctr, unsigned k, int* err
         const long long slot = (long long)(k - 1) * (gridDim.x + 1);
         if (tr.stamps && slot + gridDim.x < tr.cap) tr.stamps[slot + blockIdx.x] = wall_clock64();
         const unsigned G = gridDim.x;
-        const unsigned x = blockIdx.x % kXcds;
-        const unsigned ng = G < (unsigned)kXcds ? G : (unsigned)kXcds;
-        const unsigned per = (G - x + kXcds - 1) / kXcds;
-        const unsigned old = __hip_atomic_fetch_add(ctr + 32 * (1 + x), 1u, __ATOMIC_RELAXED,
-                                                    __HIP_MEMORY_SCOPE_AGENT);
-        if (old + 1 == k * per) __hip_atomic_fetch_add(ctr, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        const unsigned q = blockIdx.x % kBarGroups, x = q % kXcds;
+        const unsigned ngroups = G < (unsigned)kBarGroups ? G : (unsigned)kBarGroups;
+        const unsigned nclass = ngroups < (unsigned)kXcds ? ngroups : (unsigned)kXcds;
+        unsigned* rel = ctr + (kBarGroups + kXcds + 1) * kBarSlot;
+        if (__hip_atomic_fetch_add(ctr + q * kBarSlot, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) + 1 ==
+                k * bar_count(G, q, kBarGroups) &&
+            __hip_atomic_fetch_add(ctr + (kBarGroups + x) * kBarSlot, 1u, __ATOMIC_RELAXED,
+                                   __HIP_MEMORY_SCOPE_AGENT) + 1 == k * bar_count(ngroups, x, kXcds) &&
+            __hip_atomic_fetch_add(ctr + (kBarGroups + kXcds) * kBarSlot, 1u, __ATOMIC_RELAXED,
+                                   __HIP_MEMORY_SCOPE_AGENT) + 1 == k * nclass) {
+            for (int y = 0; y < kXcds; ++y)
+                __hip_atomic_store(rel + y * kBarSlot, k, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        }
         int flag = 0;
         const long long t0 = wall_clock64();
         unsigned it = 0;
-        while (__hip_atomic_load(ctr, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) < k * ng + tr.stall) {
+        const unsigned* mine = rel + (blockIdx.x % kXcds) * kBarSlot;
+        while (__hip_atomic_load(mine, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) < k + tr.stall) {
             if ((++it & 255u) == 0) {
                 if (__hip_atomic_load(err, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) != 0) {
                     flag = 1;
@@ -202,10 +223,16 @@ int measure_floor(Plan& p, float* node_us, float* barrier_us) {
         long long budget = p.spin_budget;
         int r = rounds;
         void* args[] = {&ctr, &err, &budget, &r};
-        hipError_t e = hipMemsetAsync(ctr, 0, kBarrierWords * sizeof(unsigned), st);
-        if (e == hipSuccess) e = hipEventRecord(e0, st);
-        if (e == hipSuccess)
-            e = hipLaunchCooperativeKernel((const void*)k_barrier_rounds, dim3(grid), dim3(kThreads), args, 0, st);
+        // one untimed launch first: the first cooperative launch of a process
+        // pays one-time costs (code object, first touch) that no decode pays
+        hipError_t e = hipSuccess;
+        for (int pass = 0; pass < 2 && e == hipSuccess; ++pass) {
+            e = hipMemsetAsync(ctr, 0, kBarrierWords * sizeof(unsigned), st);
+            if (e == hipSuccess && pass == 1) e = hipEventRecord(e0, st);
+            if (e == hipSuccess)
+                e = hipLaunchCooperativeKernel((const void*)k_barrier_rounds, dim3(grid), dim3(kThreads), args, 0,
+                                               st);
+        }
         if (e == hipSuccess) e = hipEventRecord(e1, st);
         if (e == hipSuccess) e = hipEventSynchronize(e1);
         if (e == hipSuccess) e = hipEventElapsedTime(&ms, e0, e1);
