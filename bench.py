@@ -607,6 +607,7 @@ def main():
                     help="latency floor of an unprofiled bench run for --summarize-stats' step histograms")
     ap.add_argument("--command", default="", help="the commands that made the counter outputs (recorded)")
     args = ap.parse_args()
+    driver_given = args.driver is not None
     if args.driver is None:
         args.driver = "resident" if args.group <= 1 else "graph"
     if args.copy_calibration:
@@ -644,8 +645,17 @@ def main():
         cfg["mask"] = args.mask
         cfg["relaxed"] = args.mask == "relaxed"
         w = inputs.make_weights(cfg["M"], cfg["K"], radius=MASK_RADIUS[args.mask])
-    plan = wf.Plan(w, table, cfg["H"], cfg["W"], cfg["B"], cfg["K"], mask=mask_of(cfg), precision=args.precision,
-                   driver=args.driver, group=args.group)
+    try:
+        plan = wf.Plan(w, table, cfg["H"], cfg["W"], cfg["B"], cfg["K"], mask=mask_of(cfg), precision=args.precision,
+                       driver=args.driver, group=args.group)
+    except wf.WfError as e:
+        # the resident driver refuses plans whose weight slices exceed its
+        # registers (e.g. the 7x7 mask at M = 320): by default, the graph driver
+        if driver_given or e.code != wf.WF_E_UNSUPPORTED:
+            raise
+        args.driver = "graph"
+        plan = wf.Plan(w, table, cfg["H"], cfg["W"], cfg["B"], cfg["K"], mask=mask_of(cfg), precision=args.precision,
+                       driver=args.driver, group=args.group)
     psi_d = torch.from_numpy(psi).cuda()
     sym_d = torch.from_numpy(sym).cuda()
     out = plan.alloc_out()

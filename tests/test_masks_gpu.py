@@ -5,10 +5,12 @@ narrower than a mask's shear, which every mask decodes in raster order (the
 earliest-possible schedule there).
 
 Every driver runs the exact decode and encode; the stream and graph drivers
-also run the context-approximation decode (Sec. III-D).  Bars as for the 5x5
-mask: floats within 1e-4 (fp32) or 1e-2 (bf16, against the oracle's bf16
-mode), encode symbols bit-exact, scale indices identical except counted
-boundary cases.  At the 3840x2160 size the oracle decodes the top grid rows
+also run the context-approximation decode (Sec. III-D).  The resident driver
+refuses the 7x7 mask at M = 320 (its context slices would need more k-parts
+than its registers and workgroup slots allow), which is checked too.  Bars as
+for the 5x5 mask: floats within 1e-4 (fp32) or 1e-3 (bf16, against the
+oracle's bf16 mode), encode symbols bit-exact, scale indices identical except
+counted boundary cases.  At the 3840x2160 size the oracle decodes the top grid rows
 (an exact sub-decode: taps lie at or above their latent's row) and its
 per-latent function is evaluated on the GPU's own reconstruction at sampled
 latents.
@@ -89,20 +91,29 @@ def decode_encode(cfg, w, table, psi, sym, mask, driver, precision, group):
 
 
 SMALL = [
-    # (workload, H, W, B): ragged grids spanning several 16-row tiles
+    # (workload, H, W, B): ragged grids (at most 16 rows, one row tile, per step)
     ("minnen-16x16-m192", 7, 9, 1),
     ("cheng-gmm3-1080p-120x68-m192", 6, 11, 1),
     ("minnen-hr-4k-240x135-m320", 4, 10, 2),
 ]
 
 
-@pytest.mark.parametrize("driver", ["stream", "graph", "persistent", "dataflow"])
+def resident_refuses(cfg, mask):
+    return mask == "7x7" and cfg["M"] == 320
+
+
+@pytest.mark.parametrize("driver", ["stream", "graph", "persistent", "dataflow", "resident"])
 @pytest.mark.parametrize("precision", ["fp32", "bf16"])
 @pytest.mark.parametrize("mask", ["3x3", "7x7"])
 @pytest.mark.parametrize("name,H,W,B", SMALL)
 def test_mask_small(name, H, W, B, mask, precision, driver):
     log(f"mask case {name} H={H} W={W} B={B} mask={mask} precision={precision} driver={driver}")
     cfg, w, table, psi, sym = case(name, mask, H, W, B)
+    if driver == "resident" and resident_refuses(cfg, mask):
+        with pytest.raises(wf.WfError) as e:
+            plan(cfg, w, table, mask, driver, precision)
+        assert e.value.code == wf.WF_E_UNSUPPORTED and "resident" in str(e.value)
+        return
     decode_encode(cfg, w, table, psi, sym, mask, driver, precision, 1)
 
 
@@ -125,7 +136,7 @@ def test_mask_grid_as_wide_as_the_shear():
         decode_encode(cfg, w, table, psi, sym, mask, "graph", "fp32", 1)
 
 
-@pytest.mark.parametrize("driver", ["stream", "graph", "persistent", "dataflow"])
+@pytest.mark.parametrize("driver", ["stream", "graph", "persistent", "dataflow", "resident"])
 @pytest.mark.parametrize("precision", ["fp32", "bf16"])
 @pytest.mark.parametrize("mask", ["full", "relaxed", "3x3", "7x7"])
 def test_grid_narrower_than_the_shear(mask, precision, driver):
