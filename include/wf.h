@@ -80,14 +80,15 @@ typedef enum {
     WF_DRIVER_PERSISTENT = 2,/* one cooperative kernel, device-wide barrier per phase      */
     WF_DRIVER_DATAFLOW = 3, /* one cooperative kernel; every job waits only for the jobs it
                                depends on (per-step, per-row-tile completion counters)     */
-    WF_DRIVER_RESIDENT = 4  /* one cooperative kernel, one workgroup per compute unit, each
+    WF_DRIVER_RESIDENT = 4  /* one cooperative kernel, two workgroups per compute unit, each
                                holding one slice of the weights in registers for the whole
                                decode (an old-tap context k-part, a layer-1/-2 column tile
                                or a layer-3 channel tile) and running that slice's product
                                for every 16-row band of every step, as soon as the bands it
-                               reads are complete (per-band completion counters).
+                               reads are complete (per-task completion counters).
                                WF_E_UNSUPPORTED when the slices do not fit the registers
-                               or the compute units                                         */
+                               or the compute units, or M is not a multiple of 32; calls
+                               need y_hat aligned to 128 bytes (WF_E_INVALID otherwise)     */
 } wf_driver;
 
 /* Block order of the last layer's output rows (w3, b3).  The kernels use the

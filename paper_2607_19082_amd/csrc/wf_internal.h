@@ -76,7 +76,7 @@ struct DfArgs {
 
 // Resident driver (see wf_resident.hip): roles of its workgroups, in this
 // order of workgroup indices.
-enum ResRole { RR_CTX = 0, RR_CTXL = 1, RR_A = 2, RR_B = 3, RR_C0 = 4, RR_C1 = 5, kResRoles = 6 };
+enum ResRole { RR_CTX = 0, RR_CTXL = 1, RR_A = 2, RR_B = 3, RR_C0 = 4, RR_C1 = 5, RR_H = 6, kResRoles = 7 };
 // Weight k-blocks one wave holds in registers per column tile, by role
 // (fp32 k-blocks of 16, bf16 k-blocks of 32); a plan whose slices need more
 // is not supported by that driver.
@@ -85,11 +85,16 @@ constexpr int kResKbBf16[5] = {14, 10, 9, 7, 4};
 constexpr int kResMaxNc = 6;        // column tiles of one layer-3 role (K = 3: 3 logits + 3 means)
 constexpr int kResMaxParts = 4;     // k-parts of the old-tap context
 constexpr int kResRep = 2;          // replicas of every weight slice (they take alternate tasks)
+constexpr int kResMinHoist = 8;     // fewest spare workgroups that compute the hoisted layer-1 part in the launch
+constexpr int kResHoistLead = 64;   // tasks by which that part runs ahead of layer 3
 
 struct ResArgs {
     int first[kResRoles + 1];   // workgroups [first[r], first[r+1]) play role r
     const int* per_slot;        // [kResRoles][kResRep][8]: workgroups of role r, replica h, in XCD class x
     int parts;                  // k-parts of the old-tap context
+    int ctx_lag;                // steps between a CTX task and the C0 tasks it waits for: the smallest
+                                // age of the old taps in parts 0 .. parts-2 (CTXL, whose part holds the
+                                // youngest taps, waits for step t - 2)
     int nrep;                   // replicas of each weight slice: workgroup q of a role with n slices holds
                                 // slice q % n and runs the tasks k with k % nrep == q / n.  CTX slices are
                                 // (column tile, part 0 .. parts-2), CTXL slices the column tiles of the
@@ -109,6 +114,8 @@ struct ResArgs {
     long long stamps_cap;
     int ntasks;                 // tasks of every workgroup (band visits of all steps and images)
     int stall;                  // test hook: every wait's target one more than it can reach
+    int hoist;                  // 1: the workgroups of role RR_H compute the hoisted layer-1 part
+                                // per task inside the launch (else a kernel before it does)
 };
 
 // Set the calling thread's error message and return `code`.

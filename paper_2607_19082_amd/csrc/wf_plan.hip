@@ -567,6 +567,11 @@ static int check_out(const Plan* p, const wf_out* out) {
         return fail(WF_E_INVALID, "y_hat, mean, scale and idx outputs are required");
     if (p->K == 3 && (!out->weight || !out->comp_mean))
         return fail(WF_E_INVALID, "weight and comp_mean outputs are required for K = 3");
+    // the resident driver reads y_hat with ordinary cached loads while it is
+    // being written: its rows must be whole 128-byte lines (M is a multiple
+    // of 32 there, so the base must be aligned)
+    if (p->driver == WF_DRIVER_RESIDENT && reinterpret_cast<uintptr_t>(out->y_hat) % 128 != 0)
+        return fail(WF_E_INVALID, "the resident driver needs y_hat aligned to 128 bytes");
     return WF_OK;
 }
 

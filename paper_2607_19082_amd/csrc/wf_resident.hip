@@ -11,6 +11,8 @@
 //              the mean; K = 3: three logits and three component means), and
 //              y_hat = s + mean
 //   C1(g)      layer 3, the scale columns of channel tile g, scale and index
+//   H          (bf16, when enough slots are left) the hoisted layer-1 part
+//              W1 psi + b1 of one task at a time, streaming its weights
 // Each slice is held by kResRep workgroups (replicas) that take alternate
 // tasks, two workgroups per compute unit.  A task of a role is one 16-row band (grid rows 16 beta .. 16 beta + 15 of
 // image b) at one wavefront step t: the band's latents on wavefront t, at
@@ -20,13 +22,18 @@
 // output tile of the task with its register-resident weights, stores it with
 // agent-coherent (sc1) stores and bumps the task's completion counter.  A
 // task waits only for the bands it reads:
-//   CTX(t, b, beta)  C0(t-2) of bands beta and beta-1 (the old taps are at
-//                    least two steps old and lie at most R <= 3 rows up)
-//   CTXL(t, b, beta) the same, and every CTX(t, b, beta)
+//   CTX(t, b, beta)  C0(t-lag) of bands beta and beta-1 (its taps are at
+//                    least lag >= 2 steps old -- the parts before the last
+//                    hold the rows furthest up, 4 steps old at the least
+//                    with the 5x5 mask -- and lie at most R <= 3 rows up)
+//   CTXL(t, b, beta) C0(t-2) of bands beta and beta-1, and every
+//                    CTX(t, b, beta)
 //   A(t, b, beta)    every CTXL(t, b, beta), C0(t-1) of bands beta and beta-1
 //                    (the new taps, one step old)
 //   B(t, b, beta)    every A(t, b, beta)
 //   C0, C1(t, b, beta)  every B(t, b, beta)
+//   H(k)             C0 of task k - 64 (it keeps a bounded lead); CTX (CTXL
+//                    with one part) waits for H(k), so layer 1 follows it
 // So bands of the upper grid rows run ahead of the lower ones, and no
 // step-wide barrier exists.  Every (role, task) has its own counter, bumped
 // once by each workgroup of the role when that workgroup's part of the task
@@ -81,8 +88,10 @@ __device__ __forceinline__ T* uni(T* p) {
     const unsigned lo = __builtin_amdgcn_readfirstlane((unsigned)v), hi = __builtin_amdgcn_readfirstlane((unsigned)(v >> 32));
     return reinterpret_cast<T*>(((unsigned long long)hi << 32) | lo);
 }
+// (Each copy starts as a plain copy, so a field missing from the lists below
+// is still correct, only not marked uniform.)
 __device__ __forceinline__ StepArgs uni_args(const StepArgs& x) {
-    StepArgs a;
+    StepArgs a = x;
 #define WF_U(f) a.f = uni(x.f)
     WF_U(H); WF_U(W); WF_U(M); WF_U(B); WF_U(K); WF_U(L); WF_U(lambda); WF_U(Np1); WF_U(Np2); WF_U(n3);
     WF_U(n_old); WF_U(ctx_parts); WF_U(R); WF_U(new_dx0); WF_U(slope); WF_U(group); WF_U(row_w); WF_U(gparts);
@@ -94,12 +103,12 @@ __device__ __forceinline__ StepArgs uni_args(const StepArgs& x) {
     return a;
 }
 __device__ __forceinline__ ResArgs uni_args(const ResArgs& x) {
-    ResArgs r;
+    ResArgs r = x;
 #define WF_U(f) r.f = uni(x.f)
-    WF_U(per_slot); WF_U(parts); WF_U(nrep); WF_U(nbands); WF_U(nbs); WF_U(cnt); WF_U(kbase); WF_U(ctx); WF_U(h1); WF_U(h2);
+    WF_U(per_slot); WF_U(parts); WF_U(ctx_lag); WF_U(nrep); WF_U(nbands); WF_U(nbs); WF_U(cnt); WF_U(kbase); WF_U(ctx); WF_U(h1); WF_U(h2);
     WF_U(ytile);
     WF_U(err);
-    WF_U(stamps); WF_U(ntasks); WF_U(stall);
+    WF_U(stamps); WF_U(ntasks); WF_U(stall); WF_U(hoist);
     for (int q = 0; q <= kResRoles; ++q) WF_U(first[q]);
 #undef WF_U
     r.budget = ((long long)uni((int)(x.budget >> 32)) << 32) | (unsigned)uni((int)x.budget);
@@ -138,22 +147,33 @@ struct ResWait {
 // context of step t reads y_hat of steps <= t-2 in the band's rows and the
 // (up to R) rows above, the band above's at most: its latest tasks of step
 // t-2 (each implies every earlier task of its band: C0(t') <- B(t') <- A(t')
-// <- C0 of the band at t'-1).  Layer 1 reads the two new taps, from step t-1
-// (the band's task and the band above's), and the task's context; layers 2
-// and 3 the layer before of the same task.
+// <- C0 of the band at t'-1).  The parts before the last hold the older taps
+// (raster order, the rows furthest up first), so they wait for step t - lag
+// with lag the smallest age among their taps (4 for the 5x5 mask's two
+// parts); the last part waits for t - 2.  Layer 1 reads the two new taps,
+// from step t-1 (the band's task and the band above's), and the task's
+// context; layers 2 and 3 the layer before of the same task.
 struct ResDeps {
     ResWait w[3];
 };
+// parts: the context's k-parts (CTX runs parts - 1 of them); lag: steps back
+// to the youngest tap of those parts (>= 2); hoist: whether
+// role RR_H computes the task's hoisted layer-1 part inside the launch.  The
+// context waits for it (a free wait slot; layer 1, which reads it, waits for
+// the context, so it follows).
 __host__ __device__ __forceinline__ ResDeps res_deps(int H, int W, int lam, const int* kbase, int role, int t, int b,
-                                                     int beta, int k) {
+                                                     int beta, int k, int parts, int lag, int hoist) {
     ResDeps d{{{0, -1}, {0, -1}, {0, -1}}};
     switch (role) {
         case RR_CTX:
-        case RR_CTXL:
-            d.w[0] = ResWait{RR_C0, band_task_of(H, W, lam, kbase, b, beta, t - 2)};
-            d.w[1] = ResWait{RR_C0, band_task_of(H, W, lam, kbase, b, beta - 1, t - 2)};
-            if (role == RR_CTXL) d.w[2] = ResWait{RR_CTX, k};   // the other parts, which it adds
+        case RR_CTXL: {
+            const int s = role == RR_CTX ? t - lag : t - 2;
+            d.w[0] = ResWait{RR_C0, band_task_of(H, W, lam, kbase, b, beta, s)};
+            d.w[1] = ResWait{RR_C0, band_task_of(H, W, lam, kbase, b, beta - 1, s)};
+            if (role == RR_CTXL && parts > 1) d.w[2] = ResWait{RR_CTX, k};   // the other parts, which it adds
+            else if (hoist) d.w[2] = ResWait{RR_H, k};
             break;
+        }
         case RR_A:
             d.w[0] = ResWait{RR_CTXL, k};
             d.w[1] = ResWait{RR_C0, band_task_of(H, W, lam, kbase, b, beta, t - 1)};
@@ -161,6 +181,9 @@ __host__ __device__ __forceinline__ ResDeps res_deps(int H, int W, int lam, cons
             break;
         case RR_B:
             d.w[0] = ResWait{RR_A, k};
+            break;
+        case RR_H:   // reads only psi; paced to stay kResHoistLead tasks ahead of layer 3
+            if (k >= kResHoistLead) d.w[0] = ResWait{RR_C0, k - kResHoistLead};
             break;
         default:   // RR_C0, RR_C1
             d.w[0] = ResWait{RR_B, k};
@@ -170,7 +193,7 @@ __host__ __device__ __forceinline__ ResDeps res_deps(int H, int W, int lam, cons
 }
 __device__ __forceinline__ ResDeps res_deps(const StepArgs& a, const ResArgs& r, int role, int t, int b, int beta,
                                             int k) {
-    return res_deps(a.H, a.W, a.lambda, r.kbase, role, t, b, beta, k);
+    return res_deps(a.H, a.W, a.lambda, r.kbase, role, t, b, beta, k, r.parts, r.ctx_lag, r.hoist);
 }
 
 // Row r of band beta of image b at step t.
@@ -198,7 +221,10 @@ __device__ __forceinline__ bool res_wait(const ResArgs& r, ResWait w0, ResWait w
         unsigned tgt = 0;
         const unsigned* p = r.cnt;
         if (i < 3 && w.k >= 0) {
-            tgt = (unsigned)r.per_slot[(w.role * kResRep + w.k % r.nrep) * kXcds + x] + (unsigned)r.stall;
+            // (one hoist workgroup per task, counting into class slot 0)
+            const unsigned n = w.role == RR_H ? (x == 0 ? 1u : 0u)
+                                              : (unsigned)r.per_slot[(w.role * kResRep + w.k % r.nrep) * kXcds + x];
+            tgt = n + (unsigned)r.stall;
             p = res_slot(r, w.role, w.k, x);
         }
         int flag = 0;
@@ -231,7 +257,7 @@ __device__ __forceinline__ void res_signal(const ResArgs& r, int role, int k) {
     __builtin_amdgcn_s_waitcnt(0);
     __syncthreads();
     if (threadIdx.x == 0)
-        __hip_atomic_fetch_add(res_slot(r, role, k, blockIdx.x % kXcds), 1u, __ATOMIC_RELAXED,
+        __hip_atomic_fetch_add(res_slot(r, role, k, role == RR_H ? 0 : blockIdx.x % kXcds), 1u, __ATOMIC_RELAXED,
                                __HIP_MEMORY_SCOPE_AGENT);
 }
 
@@ -568,11 +594,16 @@ __device__ __noinline__ void res_l1(const StepArgs& a_in, const ResArgs& r_in, i
         const int bs = b * r.nbands + beta;
         // the epilogue operand (hoisted before the launch) first
         const Row v = band_row(a, b, beta, t, ro);
-        const float z = ld1<false>(a.p1, v.lat * a.Np1 + col, v.valid);
+        const size_t zq = v.lat * a.Np1 + col;
+        // hoisted before the launch: loaded before the wait; else written in
+        // this launch by role H (the context waited for it, and this role for
+        // the context), with coherent loads, since P1 rows share lines
+        float z = r.hoist ? 0.0f : ld1<false>(a.p1, zq, v.valid);
         res_stamp(r, k, 0);
         const ResDeps dp = res_deps(a, r, RR_A, t, b, beta, k);
         const int kself = dp.w[1].k, kup = dp.w[2].k;   // the new taps' tasks
         if (!res_wait(r, dp.w[0], dp.w[1], dp.w[2], bail)) return false;
+        if (r.hoist) z = ld1<true>(a.p1, zq, v.valid);
         res_stamp(r, k, 1);
         const Row w = band_row(a, b, beta, t, lane & 15);
         const NewSrc ns = new_src<P>(a, w, kself, kup);
@@ -786,6 +817,82 @@ __device__ __noinline__ void res_l3(const StepArgs& a_in, const ResArgs& r_in, i
     });
 }
 
+// H(h): the hoisted part of layer 1, P1 = b_hoist + W1[:, :2M] . psi, for the
+// latents of every task k with k mod nh = h, all Np1 columns: each wave takes
+// every fourth group of four column tiles over the whole K (no cross-wave
+// reduction), streaming the weights, and the results go out with coherent
+// stores.  The task's context waits for it.  It waits only to stay a fixed
+// number of tasks ahead of layer 3, so that its products spread over the
+// decode instead of crowding the first steps' compute units.
+template <class P>
+__device__ __noinline__ void res_hoist(const StepArgs& a_in, const ResArgs& r_in, int T, int h, int nh, int* bail) {
+    const StepArgs a = uni_args(a_in);
+    const ResArgs r = uni_args(r_in);
+    using A = typename P::A;
+    using Bw = typename P::B;
+    constexpr int NC = 4, KB = 8;
+    const int lane = threadIdx.x & 63, kq = lane >> 4, wave = wave_id();
+    const int nct = a.Np1 / kTile, nkb = 2 * a.M / P::kK, M = a.M;
+    const float* psi = uni(a.cp->psi);
+    const Bw* wp = static_cast<const Bw*>(a.wp_hoist) + lane;
+    for_tasks(a, T, h, nh, [&](int t, int b, int beta, int k) {
+        res_stamp(r, k, 0);
+        const ResDeps dp = res_deps(a, r, RR_H, t, b, beta, k);
+        if (!res_wait(r, dp.w[0], dp.w[1], dp.w[2], bail)) return false;
+        res_stamp(r, k, 1);
+        const Row w = band_row(a, b, beta, t, lane & 15);   // the lane's operand row
+        size_t olat[4];                                      // its epilogue rows
+        bool ov[4];
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+            const Row v = band_row(a, b, beta, t, kq * 4 + q);
+            olat[q] = v.lat;
+            ov[q] = v.valid;
+        }
+        auto la = [&](int kb) -> A {
+            if constexpr (P::kBf16) {
+                const size_t q = w.lat * 2 * M + kb * 32 + kq * 8;
+                return split8(ld4<false>(psi, q, w.valid), ld4<false>(psi, q + 4, w.valid));
+            } else {
+                return ld4<false>(psi, w.lat * 2 * M + kb * kTile + kq * 4, w.valid);
+            }
+        };
+        for (int c0 = wave * NC; c0 < nct; c0 += kWaves * NC) {
+            f4 acc[NC];
+#pragma unroll
+            for (int c = 0; c < NC; ++c) acc[c] = zero4();
+            for (int kc = 0; kc < nkb; kc += KB) {
+                A av[KB];
+                Bw bv[KB][NC];
+#pragma unroll
+                for (int u = 0; u < KB; ++u) {
+                    const int kk = min(kc + u, nkb - 1);
+                    av[u] = la(kk);
+#pragma unroll
+                    for (int c = 0; c < NC; ++c) bv[u][c] = wp[((size_t)min(c0 + c, nct - 1) * nkb + kk) * 64];
+                }
+#pragma unroll
+                for (int u = 0; u < KB; ++u)
+                    if (kc + u < nkb)
+#pragma unroll
+                        for (int c = 0; c < NC; ++c) acc[c] = P::mma(av[u], bv[u][c], acc[c]);
+            }
+#pragma unroll
+            for (int c = 0; c < NC; ++c) {
+                if (c0 + c >= nct) continue;
+                const int n = (c0 + c) * kTile + (lane & 15);
+                const float bias = a.b_hoist[n];
+#pragma unroll
+                for (int q = 0; q < 4; ++q)
+                    if (ov[q]) st1<true>(a.p1, olat[q] * a.Np1 + n, acc[c][q] + bias);
+            }
+        }
+        res_signal(r, RR_H, k);
+        res_stamp(r, k, 2);
+        return true;
+    });
+}
+
 // Two workgroups per compute unit (each wave at most 256 registers).
 template <class P, int KC>
 __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2))) void k_resident(
@@ -799,13 +906,18 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2))
     // copy it to scratch memory)
     const int g = blockIdx.x;
     const int role = (g >= r.first[1]) + (g >= r.first[2]) + (g >= r.first[3]) + (g >= r.first[4]) +
-                     (g >= r.first[5]);
+                     (g >= r.first[5]) + (g >= r.first[6]);
     const int q = g - (role == 0   ? 0
                        : role == 1 ? r.first[1]
                        : role == 2 ? r.first[2]
                        : role == 3 ? r.first[3]
                        : role == 4 ? r.first[4]
-                                   : r.first[5]);
+                       : role == 5 ? r.first[5]
+                                   : r.first[6]);
+    if (role == RR_H) {   // one task in every nh, each workgroup its own
+        res_hoist<P>(a, r, T, q, r.first[7] - r.first[6], &bail);
+        return;
+    }
     // slices of the role (its workgroups are nrep replicas of each)
     const int nsl = ((role == 0   ? r.first[1]
                       : role == 1 ? r.first[2] - r.first[1]
@@ -864,10 +976,28 @@ static long long res_kbase(const Plan& p, std::vector<int>& kbase) {
     return tasks;
 }
 
+// The smallest age (steps between producer and consumer) of the old taps in
+// context parts 0 .. parts-2, which split the old-tap k-blocks evenly in the
+// packed order (old taps in raster order, M / kk k-blocks each).
+int res_ctx_lag(const Plan& p, int parts) {
+    const int kk = p.precision == WF_BF16 ? 32 : 16, tapkb = p.M / kk;
+    const int nkb_old = p.args.n_old * tapkb, hi = nkb_old * (parts - 1) / parts;
+    int lag = 1 << 30, u = 0;
+    for (int k = 0; k < p.ntaps; ++k) {
+        if (p.dy[k] < 0 && p.dx[k] >= p.W) continue;   // never in the grid (left out of the old taps)
+        const int age = p.lambda * (-p.dy[k]) - p.dx[k];
+        if (age < 2) continue;
+        if (u * tapkb < hi) lag = std::min(lag, age);
+        ++u;
+    }
+    return lag == 1 << 30 ? 2 : lag;
+}
+
 // The tasks and waits of a plan's geometry (host only, for the race checks):
 // per task in the global order {t, b, band, then for each role its three
 // waits as (role, task)}.
 int resident_deps(const Plan& p, std::vector<int32_t>& out) {
+    const int lag2 = res_ctx_lag(p, 2);
     std::vector<int> kbase;
     const long long tasks = res_kbase(p, kbase);
     if (tasks > INT32_MAX / 64) return fail(WF_E_UNSUPPORTED, "too many resident tasks");
@@ -881,7 +1011,10 @@ int resident_deps(const Plan& p, std::vector<int32_t>& out) {
                 const int32_t head[3] = {t, b, beta};
                 out.insert(out.end(), head, head + 3);
                 for (int role = 0; role < kResRoles; ++role) {
-                    const ResDeps d = res_deps(p.H, p.W, p.lambda, kbase.data(), role, t, b, beta, k);
+                    // (as planned on a device with room for two context
+                    // parts and, for bf16, the in-launch hoist)
+                    const ResDeps d = res_deps(p.H, p.W, p.lambda, kbase.data(), role, t, b, beta, k, 2, lag2,
+                                               p.precision == WF_BF16 ? 1 : 0);
                     for (int i = 0; i < 3; ++i) {
                         out.push_back(d.w[i].k >= 0 ? d.w[i].role : -1);
                         out.push_back(d.w[i].k);
@@ -897,6 +1030,12 @@ int build_resident(Plan& p) {
     ResArgs& r = p.res;
     const bool bf = p.precision == WF_BF16;
     const int* kb = bf ? kResKbBf16 : kResKbF32;
+    // The roles read data written earlier in the launch with ordinary cached
+    // loads, which is safe only if no 128-byte line holds data of two tasks:
+    // a line fetched with a latent that another task writes later would stay
+    // stale in the reader's L2.  Per-task buffers are whole lines; y_hat rows
+    // (M floats) are whole lines when M is a multiple of 32.
+    if (p.M % 32 != 0) return fail(WF_E_UNSUPPORTED, "resident driver: M must be a multiple of 32");
     const int kk = bf ? 32 : 16;
     const int M = p.M, G = M / kTile, nct = 2 * M / kTile;
     // every wave's share of every slice must fit its registers
@@ -934,13 +1073,23 @@ int build_resident(Plan& p) {
         }
     }
     r.parts = parts;
+    r.ctx_lag = res_ctx_lag(p, parts);
     r.nrep = kResRep;
-    const int n[kResRoles] = {nct * (parts - 1), nct, p.Np1 / kTile, p.Np2 / kTile, G, G};
+    const int n[RR_H] = {nct * (parts - 1), nct, p.Np1 / kTile, p.Np2 / kTile, G, G};
     r.first[0] = 0;
-    for (int k = 0; k < kResRoles; ++k) r.first[k + 1] = r.first[k] + kResRep * n[k];
+    for (int k = 0; k < RR_H; ++k) r.first[k + 1] = r.first[k] + kResRep * n[k];
+    // bf16: the slots left over compute the hoisted layer-1 part inside the
+    // launch, one task each in turn (4K: 11.6 against 11.95 ms with the hoist
+    // kernel before the launch).  fp32: the kernel before the launch (the
+    // in-launch hoist's fp32 products slow the roles they share compute units
+    // with: 14.6-14.9 against 14.0 ms), as with too few spare slots.
+    const int spare = slots - r.first[RR_H];
+    const int nh = bf && spare >= kResMinHoist ? spare : 0;
+    r.first[kResRoles] = r.first[RR_H] + nh;
+    r.hoist = nh > 0 ? 1 : 0;
     const int grid = r.first[kResRoles];
     int per_slot[kResRoles * kResRep * kXcds] = {};
-    for (int k = 0; k < kResRoles; ++k)
+    for (int k = 0; k < RR_H; ++k)
         for (int g = r.first[k]; g < r.first[k + 1]; ++g) {
             const int h = (g - r.first[k]) / n[k];   // the workgroup's replica
             ++per_slot[(k * kResRep + h) * kXcds + g % kXcds];
@@ -996,8 +1145,10 @@ int enqueue_resident(Plan& p, hipStream_t stream) {
     r.stall = p.stall;
     const size_t ncnt = (size_t)kResRoles * r.ntasks * kXcds * kDfSlotWords;
     hipLaunchKernelGGL(k_res_zero, dim3(1024), dim3(256), 0, stream, r.cnt, ncnt);
-    int rc = enqueue_hoist(p, stream);
-    if (rc != WF_OK) return rc;
+    if (!r.hoist) {
+        int rc = enqueue_hoist(p, stream);
+        if (rc != WF_OK) return rc;
+    }
     StepArgs a = p.args;
     int T = p.T;
     void* args[] = {&a, &r, &T};

@@ -7,7 +7,9 @@ so that every kernel still exits normally:
   WF_E_TIMEOUT; the next call, with the waits restored, decodes exactly what
   a call before the stall decoded;
 * residency: a plan limited to fewer compute units than its cooperative grid
-  needs (wf_desc.cu_limit) is refused with WF_E_UNSUPPORTED.
+  needs (wf_desc.cu_limit) is refused with WF_E_UNSUPPORTED;
+* the resident driver's line-granularity conditions: M a multiple of 32, y_hat
+  aligned to 128 bytes.
 """
 import sys
 
@@ -66,3 +68,24 @@ def test_too_few_compute_units_are_refused(driver):
     assert e.value.code == wf.WF_E_UNSUPPORTED
     # all compute units: accepted
     wf.Plan(w, table, cfg["H"], cfg["W"], cfg["B"], cfg["K"], driver=driver).close()
+
+
+def test_resident_refusals():
+    """The resident driver reads y_hat with cached loads while it is being
+    written, which needs every latent's row to be whole 128-byte lines: it
+    refuses M = 16 plans and a y_hat that is not 128-byte aligned."""
+    table = inputs.scale_table()
+    log("resident refusal cases")
+    with pytest.raises(wf.WfError) as e:
+        wf.Plan(inputs.make_weights(16, 1), table, 4, 5, 1, 1, driver="resident")
+    assert e.value.code == wf.WF_E_UNSUPPORTED
+    cfg, w, tab, psi, sym = inputs.make_inputs("minnen-16x16-m192", H=4, W=6)
+    p = wf.Plan(w, tab, cfg["H"], cfg["W"], cfg["B"], cfg["K"], driver="resident")
+    out = p.alloc_out()
+    shape = out["y_hat"].shape
+    buf = torch.empty(out["y_hat"].numel() + 1, dtype=torch.float32, device="cuda")
+    out["y_hat"] = buf[1:].view(shape)   # 4 bytes off
+    with pytest.raises(wf.WfError) as e:
+        p.decode(torch.from_numpy(psi).cuda(), torch.from_numpy(sym).cuda(), out=out)
+    assert e.value.code == wf.WF_E_INVALID
+    p.close()

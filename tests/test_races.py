@@ -14,7 +14,11 @@ from the data layout the drivers document, independently of the kernels:
   the context k-parts (CTX) and their sum (CTXL) read the old taps; h1 is one
   buffer by row tile, h2 and the context are double-buffered by step parity;
 * resident: one output buffer per task (step, image, 16-row band) and role,
-  so only read-after-write order matters.
+  so only read-after-write order matters; the context's k-parts split the
+  old taps (in raster order, M channels each) evenly, so with two parts CTX
+  reads the first five (the row two above) and CTXL the other five and the
+  CTX part; layer 1 also reads the hoisted part of its task, which the hoist
+  workgroups compute inside the launch.
 
 A simulation runs the jobs in orders the waits allow (random, "latest job
 first", and orders that starve one kind of job), and asserts that every read
@@ -29,8 +33,9 @@ import pytest
 
 from paper_2607_19082_amd import inputs, wf
 
-CTX, CTXL, A, B, C0, C1 = range(6)
-KINDS = 6
+CTX, CTXL, A, B, C0, C1, HOIST = range(7)
+KINDS = 6        # dataflow job kinds
+ROLES = 7        # resident roles (the six kinds and the in-launch hoist)
 NEW_TAPS = [(-1, 2), (0, -1)]                                    # the 5x5 mask, lambda = 3
 OLD_TAPS = [(-2, dx) for dx in range(-2, 3)] + [(-1, dx) for dx in range(-2, 2)] + [(0, -2)]
 LAM = 3
@@ -50,7 +55,7 @@ def taps_in_grid(H, W, b, i, j, taps):
 # comes last in the global order; "random" any runnable job; "starve K" the
 # latest runnable job not of kind (role) K, and one of kind K only when
 # nothing else can run -- the orders in which a missing wait shows.
-POLICIES = ["latest", "random 1", "random 2"] + [f"starve {k}" for k in range(6)]
+POLICIES = ["latest", "random 1", "random 2"] + [f"starve {k}" for k in range(7)]
 
 
 def pick(run, pos, kind, policy, rng):
@@ -278,19 +283,20 @@ def test_dataflow_simulation_catches_planted_omissions(plant):
 # resident driver
 
 
-def resident_tasks(H, W, Bn, M):
-    d, keep = wf.make_desc(inputs.make_weights(M, 1), inputs.scale_table(), H, W, B=Bn, driver="resident")
-    v = wf.plan_deps(d).reshape(-1, 3 + KINDS * 6)
+def resident_tasks(H, W, Bn, M, precision="fp32"):
+    d, keep = wf.make_desc(inputs.make_weights(M, 1), inputs.scale_table(), H, W, B=Bn, driver="resident",
+                           precision=precision)
+    v = wf.plan_deps(d).reshape(-1, 3 + ROLES * 6)
     tasks = [tuple(int(x) for x in r[:3]) for r in v]
     waits = {}
     for k, r in enumerate(v):
-        for role in range(KINDS):
+        for role in range(ROLES):
             q = r[3 + role * 6:3 + role * 6 + 6]
             waits[(role, k)] = [(int(q[2 * i]), int(q[2 * i + 1])) for i in range(3) if q[2 * i] >= 0]
     return tasks, waits
 
 
-def resident_reads(H, W, tasks):
+def resident_reads(H, W, tasks, hoist):
     """The data each (role, task) reads: latents of y_hat (written by the C0
     of the task holding them) and the outputs of other (role, task)."""
     index = {x: k for k, x in enumerate(tasks)}
@@ -301,11 +307,13 @@ def resident_reads(H, W, tasks):
     reads = {}
     for k, (t, b, beta) in enumerate(tasks):
         rows = [(b, i, t - LAM * i) for i in range(16 * beta, min(H, 16 * beta + 16)) if 0 <= t - LAM * i < W]
-        old = {producer(*L) for (bb, i, j) in rows for L in taps_in_grid(H, W, bb, i, j, OLD_TAPS)}
+        part0 = {producer(*L) for (bb, i, j) in rows for L in taps_in_grid(H, W, bb, i, j, OLD_TAPS[:5])}
+        part1 = {producer(*L) for (bb, i, j) in rows for L in taps_in_grid(H, W, bb, i, j, OLD_TAPS[5:])}
         new = {producer(*L) for (bb, i, j) in rows for L in taps_in_grid(H, W, bb, i, j, NEW_TAPS)}
-        reads[(CTX, k)] = old
-        reads[(CTXL, k)] = old | {(CTX, k)}
-        reads[(A, k)] = new | {(CTXL, k)}
+        reads[(CTX, k)] = part0
+        reads[(CTXL, k)] = part1 | {(CTX, k)}
+        reads[(A, k)] = new | {(CTXL, k)} | ({(HOIST, k)} if hoist else set())
+        reads[(HOIST, k)] = set()
         reads[(B, k)] = {(A, k)}
         reads[(C0, k)] = {(B, k)}
         reads[(C1, k)] = {(B, k)}
@@ -314,7 +322,7 @@ def resident_reads(H, W, tasks):
 
 def resident_run(tasks, waits_of, reads, policy):
     rng = random.Random(policy)
-    nodes = [(role, k) for k in range(len(tasks)) for role in range(KINDS)]
+    nodes = [(role, k) for k in range(len(tasks)) for role in range(ROLES)]
     done = set()
     hazards = []
     pending = set(nodes)
@@ -335,27 +343,29 @@ def resident_run(tasks, waits_of, reads, policy):
     return hazards
 
 
-RES_GEOMS = [(40, 30, 2, 32), (35, 12, 3, 32)]   # bands of 16 rows, several per step
+# bands of 16 rows, several per step; bf16 plans compute the hoisted part of
+# layer 1 inside the launch
+RES_GEOMS = [(40, 30, 2, 32, "fp32"), (35, 12, 3, 32, "fp32"), (40, 30, 2, 32, "bf16")]
 
 
-@pytest.mark.parametrize("H,W,Bn,M", RES_GEOMS)
-def test_resident_waits_point_backwards(H, W, Bn, M):
+@pytest.mark.parametrize("H,W,Bn,M,prec", RES_GEOMS)
+def test_resident_waits_point_backwards(H, W, Bn, M, prec):
     """A task waits only for earlier tasks, or for earlier roles of its own
     task (context, its sum, layers 1, 2, 3): each role's workgroups take
     their tasks in the global order, so the grid never deadlocks."""
-    tasks, waits = resident_tasks(H, W, Bn, M)
+    tasks, waits = resident_tasks(H, W, Bn, M, prec)
     # the global order: by step, image, band
     assert tasks == sorted(tasks)
-    chain = {CTX: 0, CTXL: 1, A: 2, B: 3, C0: 4, C1: 4}
+    chain = {HOIST: -1, CTX: 0, CTXL: 1, A: 2, B: 3, C0: 4, C1: 4}
     for (role, k), ws in waits.items():
         for r2, k2 in ws:
             assert k2 < k or (k2 == k and chain[r2] < chain[role]), (role, k, r2, k2)
 
 
-@pytest.mark.parametrize("H,W,Bn,M", RES_GEOMS)
-def test_resident_simulation_has_no_hazard(H, W, Bn, M):
-    tasks, waits = resident_tasks(H, W, Bn, M)
-    reads = resident_reads(H, W, tasks)
+@pytest.mark.parametrize("H,W,Bn,M,prec", RES_GEOMS)
+def test_resident_simulation_has_no_hazard(H, W, Bn, M, prec):
+    tasks, waits = resident_tasks(H, W, Bn, M, prec)
+    reads = resident_reads(H, W, tasks, prec == "bf16")
     for policy in POLICIES:
         assert resident_run(tasks, lambda n: waits[n], reads, policy) == [], policy
 
@@ -369,14 +379,23 @@ RES_PLANTS = {
     "CTX without the band above": lambda waits, tasks: {
         n: ([w for w in ws if not (w[0] == C0 and tasks[w[1]][2] != tasks[n[1]][2])] if n[0] == CTX else ws)
         for n, ws in waits.items()},
+    # the context without the task's hoisted part (which layer 1 reads after it)
+    "CTX without the hoist": lambda waits, tasks: {
+        n: ([w for w in ws if w[0] != HOIST] if n[0] == CTX else ws) for n, ws in waits.items()},
     # the context sum without the other parts
     "CTXL without CTX": lambda waits, tasks: {
         n: ([w for w in ws if w[0] != CTX] if n[0] == CTXL else ws) for n, ws in waits.items()},
-    # the context of step t waiting for step t-3 instead of t-2
+    # the context's first part (taps of age >= 4) waiting for step t-5 instead of t-4
     "CTX one step short": lambda waits, tasks: {
         n: ([w for w in ws if w[0] != C0] + [(C0, w2) for w2 in
-             [_task_at(tasks, tasks[n[1]][0] - 3, tasks[n[1]][1], tasks[n[1]][2])] if w2 >= 0]
+             [_task_at(tasks, tasks[n[1]][0] - 5, tasks[n[1]][1], tasks[n[1]][2] - d) for d in (0, 1)] if w2 >= 0]
             if n[0] == CTX else ws)
+        for n, ws in waits.items()},
+    # the last part (which holds taps of age 2) waiting as long as the first
+    "CTXL at the first part's lag": lambda waits, tasks: {
+        n: ([w for w in ws if w[0] != C0] + [(C0, w2) for w2 in
+             [_task_at(tasks, tasks[n[1]][0] - 4, tasks[n[1]][1], tasks[n[1]][2] - d) for d in (0, 1)] if w2 >= 0]
+            if n[0] == CTXL else ws)
         for n, ws in waits.items()},
 }
 
@@ -393,8 +412,8 @@ def _task_at(tasks, t, b, beta):
 @pytest.mark.parametrize("plant", sorted(RES_PLANTS))
 def test_resident_simulation_catches_planted_omissions(plant):
     H, W, Bn, M = 40, 30, 2, 32
-    tasks, waits = resident_tasks(H, W, Bn, M)
-    reads = resident_reads(H, W, tasks)
+    tasks, waits = resident_tasks(H, W, Bn, M, "bf16")
+    reads = resident_reads(H, W, tasks, True)
     planted = RES_PLANTS[plant](waits, tasks)
     found = [h for policy in POLICIES for h in resident_run(tasks, lambda n: planted[n], reads, policy)]
     assert found, plant
