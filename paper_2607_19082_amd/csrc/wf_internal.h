@@ -80,8 +80,8 @@ enum ResRole { RR_CTX = 0, RR_CTXL = 1, RR_A = 2, RR_B = 3, RR_C0 = 4, RR_C1 = 5
 // Weight k-blocks one wave holds in registers per column tile, by role
 // (fp32 k-blocks of 16, bf16 k-blocks of 32); a plan whose slices need more
 // is not supported by that driver.
-constexpr int kResKbF32[5] = {26, 20, 17, 14, 8};       // ctx part, layer 1, layer 2, layer 3 (K = 1), layer 3 (K = 3)
-constexpr int kResKbBf16[5] = {14, 10, 9, 7, 4};
+constexpr int kResKbF32[5] = {25, 20, 17, 14, 8};       // ctx part, layer 1, layer 2, layer 3 (K = 1), layer 3 (K = 3)
+constexpr int kResKbBf16[5] = {13, 10, 9, 7, 4};
 constexpr int kResMaxNc = 6;        // column tiles of one layer-3 role (K = 3: 3 logits + 3 means)
 constexpr int kResMaxParts = 4;     // k-parts of the old-tap context
 constexpr int kResRep = 2;          // replicas of every weight slice (they take alternate tasks)

@@ -207,8 +207,21 @@ __device__ __forceinline__ Row band_row(const StepArgs& a, int b, int beta, int 
     return w;
 }
 
-__device__ __forceinline__ unsigned* res_slot(const ResArgs& r, int role, int k, int x) {
-    return r.cnt + (((size_t)role * r.ntasks + k) * kXcds + x) * kDfSlotWords;
+// The counters, the error word and the stamps are reached through global
+// (address space 1) pointers and the bail flag through an LDS one: through
+// generic pointers they would be flat accesses, and a flat access in flight
+// makes the compiler wait for every load of a batch before its first MFMA
+// (it cannot tell which counter a flat access is counted by).
+typedef __attribute__((address_space(1))) unsigned gu32;
+typedef __attribute__((address_space(1))) int gi32;
+typedef __attribute__((address_space(3))) int li32;
+template <class T>
+__device__ __forceinline__ __attribute__((address_space(1))) T* glb(T* p) {
+    return (__attribute__((address_space(1))) T*)p;
+}
+
+__device__ __forceinline__ gu32* res_slot(const ResArgs& r, int role, int k, int x) {
+    return (gu32*)(r.cnt + (((size_t)role * r.ntasks + k) * kXcds + x) * kDfSlotWords);
 }
 
 // Wave 0 polls up to three waits, eight lanes each (one per XCD class).  A
@@ -219,11 +232,12 @@ __device__ __forceinline__ bool res_wait(const ResArgs& r, ResWait w0, ResWait w
         const int lane = threadIdx.x, i = lane >> 3, x = lane & (kXcds - 1);
         const ResWait w = i == 0 ? w0 : (i == 1 ? w1 : w2);
         unsigned tgt = 0;
-        const unsigned* p = r.cnt;
+        const gu32* p = (const gu32*)r.cnt;
         if (i < 3 && w.k >= 0) {
             // (one hoist workgroup per task, counting into class slot 0)
-            const unsigned n = w.role == RR_H ? (x == 0 ? 1u : 0u)
-                                              : (unsigned)r.per_slot[(w.role * kResRep + w.k % r.nrep) * kXcds + x];
+            const unsigned n =
+                w.role == RR_H ? (x == 0 ? 1u : 0u)
+                               : (unsigned)((const gi32*)r.per_slot)[(w.role * kResRep + w.k % r.nrep) * kXcds + x];
             tgt = n + (unsigned)r.stall;
             p = res_slot(r, w.role, w.k, x);
         }
@@ -234,22 +248,23 @@ __device__ __forceinline__ bool res_wait(const ResArgs& r, ResWait w0, ResWait w
             const unsigned v = tgt ? __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) : 0u;
             if (__all(v >= tgt)) break;
             if ((++it & 63u) == 0) {
-                if (__hip_atomic_load(r.err, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) != 0) {
+                if (__hip_atomic_load((gi32*)r.err, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) != 0) {
                     flag = 1;
                     break;
                 }
                 if (wall_clock64() - t0 > r.budget) {
-                    if (lane == 0) __hip_atomic_store(r.err, kErrTimeout, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                    if (lane == 0)
+                        __hip_atomic_store((gi32*)r.err, kErrTimeout, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
                     flag = 1;
                     break;
                 }
             }
             __builtin_amdgcn_s_sleep(1);
         }
-        if (lane == 0) *bail = flag;
+        if (lane == 0) *(li32*)bail = flag;
     }
     __syncthreads();
-    return *bail == 0;
+    return *(li32*)bail == 0;
 }
 
 // Publish the task's stores (every wave's have landed) and count the task.
@@ -264,7 +279,7 @@ __device__ __forceinline__ void res_signal(const ResArgs& r, int role, int k) {
 __device__ __forceinline__ void res_stamp(const ResArgs& r, int k, int e) {
     if (r.stamps && threadIdx.x == 0) {
         const long long q = ((long long)k * gridDim.x + blockIdx.x) * 3 + e;
-        if (q < r.stamps_cap) r.stamps[q] = wall_clock64();
+        if (q < r.stamps_cap) ((__attribute__((address_space(1))) long long*)r.stamps)[q] = wall_clock64();
     }
 }
 
@@ -298,6 +313,22 @@ __device__ __forceinline__ void wdot(const WSlice<P, KB, NC>& s, LoadA la, f4 (&
     // wave-uniform, in scalar registers: the guards below are then scalar
     // branches, and a batch's loads are all in flight before its first wait
     const int n = __builtin_amdgcn_readfirstlane(s.n), kb0 = __builtin_amdgcn_readfirstlane(s.kb0);
+    if (n == KB) {
+        // a full share: no guards, so each MFMA waits only for its own load
+        // (with guards the compiler waits for every load before the first)
+#pragma unroll
+        for (int u0 = 0; u0 < KB; u0 += KBB) {
+            typename P::A av[KBB];
+#pragma unroll
+            for (int u = 0; u < KBB; ++u) av[u] = la(kb0 + u0 + u);
+            __builtin_amdgcn_sched_barrier(0);   // (all loads in flight before the first MFMA)
+#pragma unroll
+            for (int u = 0; u < KBB; ++u)
+#pragma unroll
+                for (int c = 0; c < NC; ++c) acc[c] = P::mma(av[u], s.w[u0 + u][c], acc[c]);
+        }
+        return;
+    }
 #pragma unroll
     for (int u0 = 0; u0 < KB; u0 += KBB) {
         if (u0 >= n) break;
@@ -479,16 +510,26 @@ __device__ __forceinline__ void wdot_old(const WSlice<P, KB, 1>& s, const void* 
     const int n = __builtin_amdgcn_readfirstlane(s.n);
     const auto rs = rsrc(src);
     typename P::A av[KB];
+    auto load = [&](int u) {
+        const int off = os.at(u);
+        if constexpr (P::kBf16)
+            av[u] = b8x2{__builtin_bit_cast(b8, __builtin_amdgcn_raw_buffer_load_b128(rs, off, 0, 0)),
+                         __builtin_bit_cast(b8, __builtin_amdgcn_raw_buffer_load_b128(rs, off + 64, 0, 0))};
+        else
+            av[u] = __builtin_bit_cast(f4, __builtin_amdgcn_raw_buffer_load_b128(rs, off, 0, 0));
+    };
+    if (n == KB) {   // a full share: each MFMA waits only for its own load
+#pragma unroll
+        for (int u = 0; u < KB; ++u) load(u);
+        // (keeps the scheduler from sinking each load next to its MFMA)
+        __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+        for (int u = 0; u < KB; ++u) acc[0] = P::mma(av[u], s.w[u][0], acc[0]);
+        return;
+    }
 #pragma unroll
     for (int u = 0; u < KB; ++u)
-        if (u < n) {
-            const int off = os.at(u);
-            if constexpr (P::kBf16)
-                av[u] = b8x2{__builtin_bit_cast(b8, __builtin_amdgcn_raw_buffer_load_b128(rs, off, 0, 0)),
-                             __builtin_bit_cast(b8, __builtin_amdgcn_raw_buffer_load_b128(rs, off + 64, 0, 0))};
-            else
-                av[u] = __builtin_bit_cast(f4, __builtin_amdgcn_raw_buffer_load_b128(rs, off, 0, 0));
-        }
+        if (u < n) load(u);
 #pragma unroll
     for (int u = 0; u < KB; ++u)
         if (u < n) acc[0] = P::mma(av[u], s.w[u][0], acc[0]);
@@ -521,12 +562,19 @@ __device__ __noinline__ void res_ctx(const StepArgs& a_in, const ResArgs& r_in, 
     // reconstruction (bf16: its pair copy)
     const void* src = P::kBf16 ? static_cast<const void*>(a.ybf) : static_cast<const void*>(uni(a.cp->y_hat));
     const int skb0 = __builtin_amdgcn_readfirstlane(s.kb0);
+    // the weight slice is in registers before the first task (else the
+    // compiler, seeing its loads possibly in flight at every task, waits for
+    // every load of each batch before its first MFMA)
+    __builtin_amdgcn_s_waitcnt(0);
     for_tasks(a, T, rep, r.nrep, [&](int t, int b, int beta, int k) {
         res_stamp(r, k, 0);
+        // the addresses depend on the task only: computed before the wait
+        const size_t e = ctx_base(a, r, k, 0) + tile_idx<PF32>(ro, col, 2 * a.M);
+        const Row w = band_row(a, b, beta, t, lane & 15);
+        const OldSrc<P> os = old_src<P>(a, w, skb0);
         const ResDeps dp = res_deps(a, r, LAST ? RR_CTXL : RR_CTX, t, b, beta, k);
         if (!res_wait(r, dp.w[0], dp.w[1], dp.w[2], bail)) return false;
         res_stamp(r, k, 1);
-        const size_t e = ctx_base(a, r, k, 0) + tile_idx<PF32>(ro, col, 2 * a.M);
         // the other parts of this element (the last part adds them)
         float prev = 0.0f;
         if constexpr (LAST) {
@@ -534,8 +582,6 @@ __device__ __noinline__ void res_ctx(const StepArgs& a_in, const ResArgs& r_in, 
             for (int p2 = 0; p2 < kResMaxParts - 1; ++p2)
                 prev += ld1<false>(r.ctx, e + p2 * pstride, p2 < r.parts - 1);
         }
-        const Row w = band_row(a, b, beta, t, lane & 15);
-        const OldSrc<P> os = old_src<P>(a, w, skb0);
         f4 acc[1] = {zero4()};
         // one load batch (the registers hold the weights and all of them)
         wdot_old<P, KB>(s, src, os, acc);
@@ -590,6 +636,10 @@ __device__ __noinline__ void res_l1(const StepArgs& a_in, const ResArgs& r_in, i
         s.load(a.wp_l1, kbn + kbc, c, 0);
     }
     const size_t h1s = (size_t)kTile * a.Np1 * 4;     // bytes of one task's h1
+    // the weight slice is in registers before the first task (else the
+    // compiler, seeing its loads possibly in flight at every task, waits for
+    // every load of each batch before its first MFMA)
+    __builtin_amdgcn_s_waitcnt(0);
     for_tasks(a, T, rep, r.nrep, [&](int t, int b, int beta, int k) {
         const int bs = b * r.nbands + beta;
         // the epilogue operand (hoisted before the launch) first
@@ -598,15 +648,18 @@ __device__ __noinline__ void res_l1(const StepArgs& a_in, const ResArgs& r_in, i
         // hoisted before the launch: loaded before the wait; else written in
         // this launch by role H (the context waited for it, and this role for
         // the context), with coherent loads, since P1 rows share lines
-        float z = r.hoist ? 0.0f : ld1<false>(a.p1, zq, v.valid);
+        // (both loads are issued in either case, one of them masked: a load
+        // under a branch would keep the compiler from counting the batch's)
+        float z = ld1<false>(a.p1, zq, v.valid && !r.hoist);
         res_stamp(r, k, 0);
         const ResDeps dp = res_deps(a, r, RR_A, t, b, beta, k);
         const int kself = dp.w[1].k, kup = dp.w[2].k;   // the new taps' tasks
-        if (!res_wait(r, dp.w[0], dp.w[1], dp.w[2], bail)) return false;
-        if (r.hoist) z = ld1<true>(a.p1, zq, v.valid);
-        res_stamp(r, k, 1);
+        // (the addresses depend on the task only: computed before the wait)
         const Row w = band_row(a, b, beta, t, lane & 15);
         const NewSrc ns = new_src<P>(a, w, kself, kup);
+        if (!res_wait(r, dp.w[0], dp.w[1], dp.w[2], bail)) return false;
+        z += ld1<true>(a.p1, zq, v.valid && r.hoist);
+        res_stamp(r, k, 1);
         f4 acc[1] = {zero4()};
         if constexpr (P::kBf16) {
             const int sn = __builtin_amdgcn_readfirstlane(s.n), skb0 = __builtin_amdgcn_readfirstlane(s.kb0);
@@ -617,31 +670,51 @@ __device__ __noinline__ void res_l1(const StepArgs& a_in, const ResArgs& r_in, i
                 const size_t e = (tap ? ns.base[1] : ns.base[0]) + (size_t)(skb0 - tap * tapkb) * 1024 + kq * 128;
                 const bool ok = tap ? ns.ok[1] : ns.ok[0];
                 b8x2 av[ResKb<P>::a];
+                auto load = [&](int u) { av[u] = b8x2{ld8h<false>(y, e + u * 1024, ok), ld8h<false>(y, e + u * 1024 + 512, ok)}; };
+                auto mma = [&](int u) {
+                    acc[0] = PBF16::mma(av[u], s.w[u][0], acc[0]);
+                    acc[0] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av[u].hi, slo.w[u][0], acc[0], 0, 0, 0);
+                };
+                if (sn == ResKb<P>::a) {   // a full share: each MFMA waits only for its own load
 #pragma unroll
-                for (int u = 0; u < ResKb<P>::a; ++u)
-                    if (u < sn) av[u] = b8x2{ld8h<false>(y, e + u * 1024, ok), ld8h<false>(y, e + u * 1024 + 512, ok)};
+                    for (int u = 0; u < ResKb<P>::a; ++u) load(u);
+                    __builtin_amdgcn_sched_barrier(0);   // (all loads in flight before the first MFMA)
 #pragma unroll
-                for (int u = 0; u < ResKb<P>::a; ++u)
-                    if (u < sn) {
-                        acc[0] = PBF16::mma(av[u], s.w[u][0], acc[0]);
-                        acc[0] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av[u].hi, slo.w[u][0], acc[0], 0, 0, 0);
-                    }
+                    for (int u = 0; u < ResKb<P>::a; ++u) mma(u);
+                } else {
+#pragma unroll
+                    for (int u = 0; u < ResKb<P>::a; ++u)
+                        if (u < sn) load(u);
+#pragma unroll
+                    for (int u = 0; u < ResKb<P>::a; ++u)
+                        if (u < sn) mma(u);
+                }
             } else {
                 // the old-tap context (the last part's buffer holds the sum):
                 // eight fp32 values per k-block, loaded first, split into
                 // bf16 pairs afterwards
                 const size_t e = ctx_base(a, r, k, r.parts - 1);
                 f4 raw[ResKb<P>::a][2];
+                auto load = [&](int u) {
+                    const int c0 = (skb0 + u - kbn) * 32 + kq * 8;
+                    raw[u][0] = ld4<false>(r.ctx, e + tile_idx<PF32>(lane & 15, c0, 2 * M), w.valid);
+                    raw[u][1] = ld4<false>(r.ctx, e + tile_idx<PF32>(lane & 15, c0 + 4, 2 * M), w.valid);
+                };
+                if (sn == ResKb<P>::a) {   // a full share: each MFMA waits only for its own loads
 #pragma unroll
-                for (int u = 0; u < ResKb<P>::a; ++u)
-                    if (u < sn) {
-                        const int c0 = (skb0 + u - kbn) * 32 + kq * 8;
-                        raw[u][0] = ld4<false>(r.ctx, e + tile_idx<PF32>(lane & 15, c0, 2 * M), w.valid);
-                        raw[u][1] = ld4<false>(r.ctx, e + tile_idx<PF32>(lane & 15, c0 + 4, 2 * M), w.valid);
-                    }
+                    for (int u = 0; u < ResKb<P>::a; ++u) load(u);
+                    __builtin_amdgcn_sched_barrier(0);   // (all loads in flight before the first MFMA)
 #pragma unroll
-                for (int u = 0; u < ResKb<P>::a; ++u)
-                    if (u < sn) acc[0] = PBF16::mma(split8(raw[u][0], raw[u][1]), s.w[u][0], acc[0]);
+                    for (int u = 0; u < ResKb<P>::a; ++u)
+                        acc[0] = PBF16::mma(split8(raw[u][0], raw[u][1]), s.w[u][0], acc[0]);
+                } else {
+#pragma unroll
+                    for (int u = 0; u < ResKb<P>::a; ++u)
+                        if (u < sn) load(u);
+#pragma unroll
+                    for (int u = 0; u < ResKb<P>::a; ++u)
+                        if (u < sn) acc[0] = PBF16::mma(split8(raw[u][0], raw[u][1]), s.w[u][0], acc[0]);
+                }
             }
         } else {
             // the 4 M k-values split into four equal shares, so each wave's
@@ -666,12 +739,21 @@ __device__ __noinline__ void res_l1(const StepArgs& a_in, const ResArgs& r_in, i
             const int n = __builtin_amdgcn_readfirstlane(s.n);
             const auto rs = rsrc(src);
             f4 av[ResKb<P>::a];
+            if (n == ResKb<P>::a) {   // a full share: each MFMA waits only for its own load
 #pragma unroll
-            for (int u = 0; u < ResKb<P>::a; ++u)
-                if (u < n) av[u] = __builtin_bit_cast(f4, __builtin_amdgcn_raw_buffer_load_b128(rs, off + u * 1024, 0, 0));
+                for (int u = 0; u < ResKb<P>::a; ++u)
+                    av[u] = __builtin_bit_cast(f4, __builtin_amdgcn_raw_buffer_load_b128(rs, off + u * 1024, 0, 0));
+                __builtin_amdgcn_sched_barrier(0);   // (all loads in flight before the first MFMA)
 #pragma unroll
-            for (int u = 0; u < ResKb<P>::a; ++u)
-                if (u < n) acc[0] = PF32::mma(av[u], s.w[u][0], acc[0]);
+                for (int u = 0; u < ResKb<P>::a; ++u) acc[0] = PF32::mma(av[u], s.w[u][0], acc[0]);
+            } else {
+#pragma unroll
+                for (int u = 0; u < ResKb<P>::a; ++u)
+                    if (u < n) av[u] = __builtin_bit_cast(f4, __builtin_amdgcn_raw_buffer_load_b128(rs, off + u * 1024, 0, 0));
+#pragma unroll
+                for (int u = 0; u < ResKb<P>::a; ++u)
+                    if (u < n) acc[0] = PF32::mma(av[u], s.w[u][0], acc[0]);
+            }
         }
         float o[1];
         wreduce<1>(red, acc, o);
@@ -695,6 +777,10 @@ __device__ __noinline__ void res_l2(const StepArgs& a_in, const ResArgs& r_in, i
     s.load(a.wp2, nkb, c, 0);
     const float bias = a.b2[col];
     const size_t h1s = (size_t)kTile * a.Np1 * 4, h2s = (size_t)kTile * a.Np2 * 4;
+    // the weight slice is in registers before the first task (else the
+    // compiler, seeing its loads possibly in flight at every task, waits for
+    // every load of each batch before its first MFMA)
+    __builtin_amdgcn_s_waitcnt(0);
     for_tasks(a, T, rep, r.nrep, [&](int t, int b, int beta, int k) {
         const int bs = b * r.nbands + beta;
         res_stamp(r, k, 0);
@@ -745,12 +831,22 @@ __device__ __noinline__ void res_l3(const StepArgs& a_in, const ResArgs& r_in, i
         cpv.encode = uni(cq->encode);
     }
     const CallPtrs* cp = &cpv;
+    // the weight slice is in registers before the first task (else the
+    // compiler, seeing its loads possibly in flight at every task, waits for
+    // every load of each batch before its first MFMA)
+    __builtin_amdgcn_s_waitcnt(0);
     for_tasks(a, T, rep, r.nrep, [&](int t, int b, int beta, int k) {
         const int bs = b * r.nbands + beta;
         const Row v = band_row(a, b, beta, t, ro);
         const size_t oq = v.lat * M + ch;
+        // the symbol (or, encoding, y): both loads issued, one masked
         float sin = 0.0f;
-        if (MEAN && v.valid) sin = cp->encode ? cp->y[oq] : (float)cp->sym[oq];
+        if constexpr (MEAN) {
+            const float yv = ld1<false>(cp->y, oq, v.valid && cp->encode);
+            const float sv = (float)__builtin_bit_cast(
+                int32_t, ld1<false>(reinterpret_cast<const float*>(cp->sym), oq, v.valid && !cp->encode));
+            sin = cp->encode ? yv : sv;
+        }
         res_stamp(r, k, 0);
         const ResDeps dp = res_deps(a, r, MEAN ? RR_C0 : RR_C1, t, b, beta, k);
         if (!res_wait(r, dp.w[0], dp.w[1], dp.w[2], bail)) return false;
@@ -772,8 +868,8 @@ __device__ __noinline__ void res_l3(const StepArgs& a_in, const ResArgs& r_in, i
                 for (int kk = 0; kk < KC; ++kk) {
                     const float sg = o[kk] > t0 ? o[kk] : t0;
                     const size_t q2 = (v.lat * KC + kk) * M + ch;
-                    cp->scale[q2] = sg;
-                    cp->idx[q2] = scale_index(tab, a.L, sg);
+                    glb(cp->scale)[q2] = sg;
+                    glb(cp->idx)[q2] = scale_index(tab, a.L, sg);
                 }
             } else {
                 float mu;
@@ -792,19 +888,19 @@ __device__ __noinline__ void res_l3(const StepArgs& a_in, const ResArgs& r_in, i
                     for (int kk = 0; kk < 3; ++kk) {
                         const float wk = ex[kk] / den;
                         const size_t q2 = (v.lat * 3 + kk) * M + ch;
-                        cp->weight[q2] = wk;
-                        cp->cmean[q2] = o[3 + kk];
+                        glb(cp->weight)[q2] = wk;
+                        glb(cp->cmean)[q2] = o[3 + kk];
                         mu += wk * o[3 + kk];
                     }
                 }
                 float sv;
                 if (cp->encode) {
                     sv = rintf(sin - mu);
-                    cp->sym_out[oq] = (int32_t)sv;
+                    glb(cp->sym_out)[oq] = (int32_t)sv;
                 } else {
                     sv = sin;
                 }
-                cp->mean[oq] = mu;
+                glb(cp->mean)[oq] = mu;
                 st1<true>(cp->y_hat, oq, sv + mu);
                 if constexpr (P::kBf16) st_pair_row<true>(a.ybf, v.lat * 2 * M, ch, sv + mu);
                 // the task's tile of y_hat, the next step's new taps
@@ -834,7 +930,9 @@ __device__ __noinline__ void res_hoist(const StepArgs& a_in, const ResArgs& r_in
     const int lane = threadIdx.x & 63, kq = lane >> 4, wave = wave_id();
     const int nct = a.Np1 / kTile, nkb = 2 * a.M / P::kK, M = a.M;
     const float* psi = uni(a.cp->psi);
-    const Bw* wp = static_cast<const Bw*>(a.wp_hoist) + lane;
+    // (global, not generic: flat loads would keep the compiler from counting
+    // the batch's loads one by one)
+    const __attribute__((address_space(1))) Bw* wp = (const __attribute__((address_space(1))) Bw*)a.wp_hoist + lane;
     for_tasks(a, T, h, nh, [&](int t, int b, int beta, int k) {
         res_stamp(r, k, 0);
         const ResDeps dp = res_deps(a, r, RR_H, t, b, beta, k);
