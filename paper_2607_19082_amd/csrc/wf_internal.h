@@ -80,10 +80,14 @@ enum ResRole { RR_CTX = 0, RR_CTXL = 1, RR_A = 2, RR_B = 3, RR_C0 = 4, RR_C1 = 5
 // Weight k-blocks one wave holds in registers per column tile, by role
 // (fp32 k-blocks of 16, bf16 k-blocks of 32); a plan whose slices need more
 // is not supported by that driver.
-constexpr int kResKbF32[5] = {25, 20, 17, 14, 8};       // ctx part, layer 1, layer 2, layer 3 (K = 1), layer 3 (K = 3)
-constexpr int kResKbBf16[5] = {13, 10, 9, 7, 4};
+// per-wave k-blocks of a slice: context part (kResCtxNc column tiles), layer 1,
+// layer 2, layer 3 (K = 1), layer 3 (K = 3), last context part (kResCtxlNc tiles)
+constexpr int kResKbF32[6] = {6, 20, 17, 14, 8, 10};
+constexpr int kResKbBf16[6] = {6, 10, 9, 7, 4, 10};
+constexpr int kResCtxNc = 4;       // column tiles of a context part's slice (64 of the 2M columns)
+constexpr int kResCtxlNc = 2;      // column tiles of a last-part slice
 constexpr int kResMaxNc = 6;        // column tiles of one layer-3 role (K = 3: 3 logits + 3 means)
-constexpr int kResMaxParts = 4;     // k-parts of the old-tap context
+constexpr int kResMaxParts = 12;    // k-parts of the old-tap context (the last one included)
 constexpr int kResRep = 2;          // replicas of every weight slice (they take alternate tasks)
 constexpr int kResMinHoist = 8;     // fewest spare workgroups that compute the hoisted layer-1 part in the launch
 constexpr int kResHoistLead = 64;   // tasks by which that part runs ahead of layer 3
@@ -91,10 +95,12 @@ constexpr int kResHoistLead = 64;   // tasks by which that part runs ahead of la
 struct ResArgs {
     int first[kResRoles + 1];   // workgroups [first[r], first[r+1]) play role r
     const int* per_slot;        // [kResRoles][kResRep][8]: workgroups of role r, replica h, in XCD class x
-    int parts;                  // k-parts of the old-tap context
+    int parts;                  // k-parts of the old-tap context: parts - 1 split the old taps before the
+                                // first one of age 2 (raster order; k-blocks [0, pre_kb)) evenly, the
+                                // last one (CTXL) holds the rest, [pre_kb, n_old M / kK)
+    int pre_kb;
     int ctx_lag;                // steps between a CTX task and the C0 tasks it waits for: the smallest
-                                // age of the old taps in parts 0 .. parts-2 (CTXL, whose part holds the
-                                // youngest taps, waits for step t - 2)
+                                // age of the old taps before pre_kb (CTXL waits for step t - 2)
     int nrep;                   // replicas of each weight slice: workgroup q of a role with n slices holds
                                 // slice q % n and runs the tasks k with k % nrep == q / n.  CTX slices are
                                 // (column tile, part 0 .. parts-2), CTXL slices the column tiles of the

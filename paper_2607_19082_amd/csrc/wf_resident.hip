@@ -66,12 +66,12 @@ struct ResKb;
 template <>
 struct ResKb<PF32> {
     static constexpr int ctx = kResKbF32[0], a = kResKbF32[1], b = kResKbF32[2], c1 = kResKbF32[3],
-                         c3 = kResKbF32[4];
+                         c3 = kResKbF32[4], ctxl = kResKbF32[5];
 };
 template <>
 struct ResKb<PBF16> {
     static constexpr int ctx = kResKbBf16[0], a = kResKbBf16[1], b = kResKbBf16[2], c1 = kResKbBf16[3],
-                         c3 = kResKbBf16[4];
+                         c3 = kResKbBf16[4], ctxl = kResKbBf16[5];
 };
 
 // Wave-uniform copies of the argument blocks.  The role functions below are
@@ -105,7 +105,7 @@ __device__ __forceinline__ StepArgs uni_args(const StepArgs& x) {
 __device__ __forceinline__ ResArgs uni_args(const ResArgs& x) {
     ResArgs r = x;
 #define WF_U(f) r.f = uni(x.f)
-    WF_U(per_slot); WF_U(parts); WF_U(ctx_lag); WF_U(nrep); WF_U(nbands); WF_U(nbs); WF_U(cnt); WF_U(kbase); WF_U(ctx); WF_U(h1); WF_U(h2);
+    WF_U(per_slot); WF_U(parts); WF_U(pre_kb); WF_U(ctx_lag); WF_U(nrep); WF_U(nbands); WF_U(nbs); WF_U(cnt); WF_U(kbase); WF_U(ctx); WF_U(h1); WF_U(h2);
     WF_U(ytile);
     WF_U(err);
     WF_U(stamps); WF_U(ntasks); WF_U(stall); WF_U(hoist);
@@ -505,8 +505,8 @@ __device__ __forceinline__ OldSrc<P> old_src(const StepArgs& a, const Row& w, in
 }
 // acc += the wave's old-tap k-blocks x its weight slice, all loads issued
 // before the first MFMA.
-template <class P, int KB>
-__device__ __forceinline__ void wdot_old(const WSlice<P, KB, 1>& s, const void* src, OldSrc<P> os, f4 (&acc)[1]) {
+template <class P, int KB, int NC>
+__device__ __forceinline__ void wdot_old(const WSlice<P, KB, NC>& s, const void* src, OldSrc<P> os, f4 (&acc)[NC]) {
     const int n = __builtin_amdgcn_readfirstlane(s.n);
     const auto rs = rsrc(src);
     typename P::A av[KB];
@@ -524,7 +524,9 @@ __device__ __forceinline__ void wdot_old(const WSlice<P, KB, 1>& s, const void* 
         // (keeps the scheduler from sinking each load next to its MFMA)
         __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
-        for (int u = 0; u < KB; ++u) acc[0] = P::mma(av[u], s.w[u][0], acc[0]);
+        for (int u = 0; u < KB; ++u)
+#pragma unroll
+            for (int c = 0; c < NC; ++c) acc[c] = P::mma(av[u], s.w[u][c], acc[c]);
         return;
     }
 #pragma unroll
@@ -532,7 +534,9 @@ __device__ __forceinline__ void wdot_old(const WSlice<P, KB, 1>& s, const void* 
         if (u < n) load(u);
 #pragma unroll
     for (int u = 0; u < KB; ++u)
-        if (u < n) acc[0] = P::mma(av[u], s.w[u][0], acc[0]);
+        if (u < n)
+#pragma unroll
+            for (int c = 0; c < NC; ++c) acc[c] = P::mma(av[u], s.w[u][c], acc[c]);
 }
 
 // Element offset of context part `part` of task k (16 rows x 2M, tile order).
@@ -542,21 +546,28 @@ __device__ __forceinline__ size_t ctx_base(const StepArgs& a, const ResArgs& r, 
 
 // ---------------------------------------------------------------------------
 // CTX(c, p) / CTXL(c): ctx[p][r][n] = sum over part p's old-tap k-blocks of
-// taps x Wc; the last part (LAST) stores the sum over all parts.
+// taps x Wc for the NC column tiles of column group c; the last part (LAST)
+// stores the sum over all parts.  A part's slice spans several column tiles
+// so that each activation load feeds NC MFMAs (the activations of a task are
+// the same for every column group, the weights differ).
 template <class P, bool LAST>
 __device__ __noinline__ void res_ctx(const StepArgs& a_in, const ResArgs& r_in, int T, int q, int rep, f4 (*red)[64],
                                      int* bail) {
     const StepArgs a = uni_args(a_in);
     const ResArgs r = uni_args(r_in);
-    constexpr int KB = ResKb<P>::ctx;
-    const int nct = 2 * a.M / kTile;
-    const int c = q % nct, part = LAST ? r.parts - 1 : q / nct;   // q: the slice
+    constexpr int KB = LAST ? ResKb<P>::ctxl : ResKb<P>::ctx;
+    constexpr int NC = LAST ? kResCtxlNc : kResCtxNc;
+    const int ncg = 2 * a.M / (kTile * NC);
+    const int c = q % ncg, part = LAST ? r.parts - 1 : q / ncg;   // q: the slice
     const int lane = threadIdx.x & 63, kq = lane >> 4, wave = wave_id();
-    const int nkb = a.n_old * a.M / P::kK;
-    WSlice<P, KB, 1> s;
-    s.split(nkb * part / r.parts, nkb * (part + 1) / r.parts);
-    s.load(a.wp_old, nkb, c, 0);
-    const int ro = kq * 4 + wave, col = c * kTile + (lane & 15);
+    const int nkb = a.n_old * a.M / P::kK, np = r.parts - 1;
+    WSlice<P, KB, NC> s;
+    if (LAST)
+        s.split(r.pre_kb, nkb);
+    else
+        s.split(r.pre_kb * part / np, r.pre_kb * (part + 1) / np);
+    s.load(a.wp_old, nkb, c * NC, 1);
+    const int ro = kq * 4 + wave;
     const size_t pstride = (size_t)kTile * 2 * a.M;
     // the tap source, read once (not once per k-block): the call's
     // reconstruction (bf16: its pair copy)
@@ -569,25 +580,33 @@ __device__ __noinline__ void res_ctx(const StepArgs& a_in, const ResArgs& r_in, 
     for_tasks(a, T, rep, r.nrep, [&](int t, int b, int beta, int k) {
         res_stamp(r, k, 0);
         // the addresses depend on the task only: computed before the wait
-        const size_t e = ctx_base(a, r, k, 0) + tile_idx<PF32>(ro, col, 2 * a.M);
+        const size_t e = ctx_base(a, r, k, 0) + tile_idx<PF32>(ro, c * NC * kTile + (lane & 15), 2 * a.M);
         const Row w = band_row(a, b, beta, t, lane & 15);
         const OldSrc<P> os = old_src<P>(a, w, skb0);
         const ResDeps dp = res_deps(a, r, LAST ? RR_CTXL : RR_CTX, t, b, beta, k);
         if (!res_wait(r, dp.w[0], dp.w[1], dp.w[2], bail)) return false;
         res_stamp(r, k, 1);
-        // the other parts of this element (the last part adds them)
-        float prev = 0.0f;
+        // the other parts of these elements (the last part adds them; column
+        // tile cc of the group is 256 elements of the tile order further)
+        float prev[NC];
+#pragma unroll
+        for (int cc = 0; cc < NC; ++cc) prev[cc] = 0.0f;
         if constexpr (LAST) {
 #pragma unroll
             for (int p2 = 0; p2 < kResMaxParts - 1; ++p2)
-                prev += ld1<false>(r.ctx, e + p2 * pstride, p2 < r.parts - 1);
+#pragma unroll
+                for (int cc = 0; cc < NC; ++cc)
+                    prev[cc] += ld1<false>(r.ctx, e + p2 * pstride + cc * 256, p2 < np);
         }
-        f4 acc[1] = {zero4()};
+        f4 acc[NC];
+#pragma unroll
+        for (int cc = 0; cc < NC; ++cc) acc[cc] = zero4();
         // one load batch (the registers hold the weights and all of them)
-        wdot_old<P, KB>(s, src, os, acc);
-        float v[1];
-        wreduce<1>(red, acc, v);
-        st1<true>(r.ctx, e + part * pstride, v[0] + prev);
+        wdot_old<P, KB, NC>(s, src, os, acc);
+        float v[NC];
+        wreduce<NC>(red, acc, v);
+#pragma unroll
+        for (int cc = 0; cc < NC; ++cc) st1<true>(r.ctx, e + part * pstride + cc * 256, v[cc] + prev[cc]);
         res_signal(r, LAST ? RR_CTXL : RR_CTX, k);
         res_stamp(r, k, 2);
         return true;
@@ -1074,28 +1093,42 @@ static long long res_kbase(const Plan& p, std::vector<int>& kbase) {
     return tasks;
 }
 
-// The smallest age (steps between producer and consumer) of the old taps in
-// context parts 0 .. parts-2, which split the old-tap k-blocks evenly in the
-// packed order (old taps in raster order, M / kk k-blocks each).
-int res_ctx_lag(const Plan& p, int parts) {
-    const int kk = p.precision == WF_BF16 ? 32 : 16, tapkb = p.M / kk;
-    const int nkb_old = p.args.n_old * tapkb, hi = nkb_old * (parts - 1) / parts;
-    int lag = 1 << 30, u = 0;
+// The split of the old taps between the context parts: the last part takes
+// the taps (raster order) from the first one of age 2 -- the steps between
+// producer and consumer -- on, or as many of the last taps as its slice holds
+// when those are more; the parts before it take the rest.  Returns their
+// k-blocks (pre_kb) and the smallest age among them (lag: 3 or more when the
+// taps of age 2 are all in the last part, else 2).
+void res_ctx_split(const Plan& p, int& pre_kb, int& lag) {
+    const bool bf = p.precision == WF_BF16;
+    const int kk = bf ? 32 : 16, tapkb = p.M / kk;
+    const int last_max = kWaves * (bf ? kResKbBf16[5] : kResKbF32[5]) / tapkb;   // taps a last-part slice holds
+    std::vector<int> ages;
     for (int k = 0; k < p.ntaps; ++k) {
         if (p.dy[k] < 0 && p.dx[k] >= p.W) continue;   // never in the grid (left out of the old taps)
         const int age = p.lambda * (-p.dy[k]) - p.dx[k];
-        if (age < 2) continue;
-        if (u * tapkb < hi) lag = std::min(lag, age);
-        ++u;
+        if (age >= 2) ages.push_back(age);
     }
-    return lag == 1 << 30 ? 2 : lag;
+    const int n = (int)ages.size();
+    int pre = n;
+    for (int u = 0; u < n; ++u)
+        if (ages[u] == 2) {
+            pre = u;
+            break;
+        }
+    pre = std::max(pre, n - last_max);
+    lag = 1 << 30;
+    for (int u = 0; u < pre; ++u) lag = std::min(lag, ages[u]);
+    if (lag == 1 << 30) lag = 2;
+    pre_kb = pre * tapkb;
 }
 
 // The tasks and waits of a plan's geometry (host only, for the race checks):
 // per task in the global order {t, b, band, then for each role its three
 // waits as (role, task)}.
 int resident_deps(const Plan& p, std::vector<int32_t>& out) {
-    const int lag2 = res_ctx_lag(p, 2);
+    int pre_kb, lag2;
+    res_ctx_split(p, pre_kb, lag2);
     std::vector<int> kbase;
     const long long tasks = res_kbase(p, kbase);
     if (tasks > INT32_MAX / 64) return fail(WF_E_UNSUPPORTED, "too many resident tasks");
@@ -1109,10 +1142,11 @@ int resident_deps(const Plan& p, std::vector<int32_t>& out) {
                 const int32_t head[3] = {t, b, beta};
                 out.insert(out.end(), head, head + 3);
                 for (int role = 0; role < kResRoles; ++role) {
-                    // (as planned on a device with room for two context
-                    // parts and, for bf16, the in-launch hoist)
-                    const ResDeps d = res_deps(p.H, p.W, p.lambda, kbase.data(), role, t, b, beta, k, 2, lag2,
-                                               p.precision == WF_BF16 ? 1 : 0);
+                    // (as planned on a device with room for the context
+                    // parts before the last and, for bf16, the in-launch
+                    // hoist)
+                    const ResDeps d = res_deps(p.H, p.W, p.lambda, kbase.data(), role, t, b, beta, k,
+                                               pre_kb > 0 ? 2 : 1, lag2, p.precision == WF_BF16 ? 1 : 0);
                     for (int i = 0; i < 3; ++i) {
                         out.push_back(d.w[i].k >= 0 ? d.w[i].role : -1);
                         out.push_back(d.w[i].k);
@@ -1135,12 +1169,15 @@ int build_resident(Plan& p) {
     // (M floats) are whole lines when M is a multiple of 32.
     if (p.M % 32 != 0) return fail(WF_E_UNSUPPORTED, "resident driver: M must be a multiple of 32");
     const int kk = bf ? 32 : 16;
-    const int M = p.M, G = M / kTile, nct = 2 * M / kTile;
+    const int M = p.M, G = M / kTile, ncg = 2 * M / (kTile * kResCtxNc), ncgl = 2 * M / (kTile * kResCtxlNc);
+    const int nkb_old = a.n_old * M / kk;
+    int pre_kb, lag;
+    res_ctx_split(p, pre_kb, lag);
     // every wave's share of every slice must fit its registers
     if (ceil_div((kMaxNew * M + 2 * M) / kk, kWaves) > kb[1] || ceil_div(p.Np1 / kk, kWaves) > kb[2] ||
-        ceil_div(p.Np2 / kk, kWaves) > kb[p.K == 1 ? 3 : 4])
+        ceil_div(p.Np2 / kk, kWaves) > kb[p.K == 1 ? 3 : 4] || ceil_div(nkb_old - pre_kb, kWaves) > kb[5] ||
+        (2 * M) % (kTile * kResCtxNc) != 0)
         return fail(WF_E_UNSUPPORTED, "resident driver: a weight slice exceeds the register budget (M too large)");
-    const int nkb_old = a.n_old * M / kk;
     int cus = 0, dev = 0;
     hipError_t e = hipGetDevice(&dev);
     if (e == hipSuccess) e = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);
@@ -1148,21 +1185,27 @@ int build_resident(Plan& p) {
     if (p.cu_limit > 0 && p.cu_limit < cus) cus = p.cu_limit;
     const int crit = p.Np1 / kTile + p.Np2 / kTile + 2 * G;
     const int slots = kResRep * cus;   // two workgroups per compute unit
-    // the fewest old-tap context parts whose slices fit the registers
-    int parts = 1;
-    while (ceil_div(ceil_div(nkb_old, parts), kWaves) > kb[0]) ++parts;
-    if (parts > kResMaxParts) return fail(WF_E_UNSUPPORTED, "resident driver: the old-tap context needs too many parts");
-    if (kResRep * (crit + nct * parts) > slots)
-        return fail(WF_E_UNSUPPORTED, "resident driver: " + std::to_string(kResRep * (crit + nct * parts)) +
-                                          " workgroups for " + std::to_string(slots) + " slots");
-    // spare slots take more context parts (shorter context tasks)
-    while (kResRep * (crit + nct * (parts + 1)) <= slots && parts < kResMaxParts && nkb_old / (parts + 1) >= kWaves)
-        ++parts;
+    // the fewest parts before the last whose slices fit the registers
+    int np = 0;
+    if (pre_kb > 0)
+        for (np = 1; ceil_div(ceil_div(pre_kb, np), kWaves) > kb[0];) ++np;
+    if (np + 1 > kResMaxParts) return fail(WF_E_UNSUPPORTED, "resident driver: the old-tap context needs too many parts");
+    auto need = [&](int n_) { return kResRep * (crit + ncg * n_ + ncgl); };
+    if (need(np) > slots)
+        return fail(WF_E_UNSUPPORTED, "resident driver: " + std::to_string(need(np)) + " workgroups for " +
+                                          std::to_string(slots) + " slots");
+    // fp32: spare slots take more context parts (shorter context tasks);
+    // bf16: they compute the hoisted layer-1 part in the launch (4K: 9.74 ms
+    // with 68 such workgroups and the fewest parts, 9.87 with 48, 11.0 with
+    // 28 and two more parts)
+    while (!bf && np > 0 && need(np + 1) <= slots && np + 2 <= kResMaxParts && pre_kb / (np + 1) >= kWaves) ++np;
+    const int parts = np + 1;
     // a wave's old-tap k-blocks must lie in at most kResSeg taps
     {
         const int tapkb = M / kk;
         for (int q = 0; q < parts; ++q) {
-            const int lo = nkb_old * q / parts, hi = nkb_old * (q + 1) / parts, per = ceil_div(hi - lo, kWaves);
+            const int lo = q < np ? pre_kb * q / np : pre_kb, hi = q < np ? pre_kb * (q + 1) / np : nkb_old;
+            const int per = ceil_div(hi - lo, kWaves);
             for (int wv = 0; wv < kWaves; ++wv) {
                 const int k0 = std::min(hi, lo + wv * per), k1 = std::min(hi, k0 + per);
                 if (k1 > k0 && (k1 - 1) / tapkb - k0 / tapkb + 1 > kResSeg)
@@ -1171,16 +1214,18 @@ int build_resident(Plan& p) {
         }
     }
     r.parts = parts;
-    r.ctx_lag = res_ctx_lag(p, parts);
+    r.pre_kb = pre_kb;
+    r.ctx_lag = lag;
     r.nrep = kResRep;
-    const int n[RR_H] = {nct * (parts - 1), nct, p.Np1 / kTile, p.Np2 / kTile, G, G};
+    const int n[RR_H] = {ncg * np, ncgl, p.Np1 / kTile, p.Np2 / kTile, G, G};
     r.first[0] = 0;
     for (int k = 0; k < RR_H; ++k) r.first[k + 1] = r.first[k] + kResRep * n[k];
     // bf16: the slots left over compute the hoisted layer-1 part inside the
-    // launch, one task each in turn (4K: 11.6 against 11.95 ms with the hoist
+    // launch, one task each in turn (4K: 9.74 against 10.19 ms with the hoist
     // kernel before the launch).  fp32: the kernel before the launch (the
     // in-launch hoist's fp32 products slow the roles they share compute units
-    // with: 14.6-14.9 against 14.0 ms), as with too few spare slots.
+    // with: 14.6-14.9 against 14.0 ms, measured before the context parts were
+    // re-blocked), as with too few spare slots.
     const int spare = slots - r.first[RR_H];
     const int nh = bf && spare >= kResMinHoist ? spare : 0;
     r.first[kResRoles] = r.first[RR_H] + nh;

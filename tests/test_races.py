@@ -14,11 +14,11 @@ from the data layout the drivers document, independently of the kernels:
   the context k-parts (CTX) and their sum (CTXL) read the old taps; h1 is one
   buffer by row tile, h2 and the context are double-buffered by step parity;
 * resident: one output buffer per task (step, image, 16-row band) and role,
-  so only read-after-write order matters; the context's k-parts split the
-  old taps (in raster order, M channels each) evenly, so with two parts CTX
-  reads the first five (the row two above) and CTXL the other five and the
-  CTX part; layer 1 also reads the hoisted part of its task, which the hoist
-  workgroups compute inside the launch.
+  so only read-after-write order matters; the context parts before the last
+  (CTX) read the old taps (in raster order) before the first one of age 2,
+  i.e. the eight of ages 3 to 8, and the last part (CTXL) the other two and
+  the CTX parts; layer 1 also reads the hoisted part of its task, which the
+  hoist workgroups compute inside the launch.
 
 A simulation runs the jobs in orders the waits allow (random, "latest job
 first", and orders that starve one kind of job), and asserts that every read
@@ -307,8 +307,8 @@ def resident_reads(H, W, tasks, hoist):
     reads = {}
     for k, (t, b, beta) in enumerate(tasks):
         rows = [(b, i, t - LAM * i) for i in range(16 * beta, min(H, 16 * beta + 16)) if 0 <= t - LAM * i < W]
-        part0 = {producer(*L) for (bb, i, j) in rows for L in taps_in_grid(H, W, bb, i, j, OLD_TAPS[:5])}
-        part1 = {producer(*L) for (bb, i, j) in rows for L in taps_in_grid(H, W, bb, i, j, OLD_TAPS[5:])}
+        part0 = {producer(*L) for (bb, i, j) in rows for L in taps_in_grid(H, W, bb, i, j, OLD_TAPS[:8])}
+        part1 = {producer(*L) for (bb, i, j) in rows for L in taps_in_grid(H, W, bb, i, j, OLD_TAPS[8:])}
         new = {producer(*L) for (bb, i, j) in rows for L in taps_in_grid(H, W, bb, i, j, NEW_TAPS)}
         reads[(CTX, k)] = part0
         reads[(CTXL, k)] = part1 | {(CTX, k)}
@@ -385,16 +385,16 @@ RES_PLANTS = {
     # the context sum without the other parts
     "CTXL without CTX": lambda waits, tasks: {
         n: ([w for w in ws if w[0] != CTX] if n[0] == CTXL else ws) for n, ws in waits.items()},
-    # the context's first part (taps of age >= 4) waiting for step t-5 instead of t-4
+    # the parts before the last (taps of age >= 3) waiting for step t-4 instead of t-3
     "CTX one step short": lambda waits, tasks: {
         n: ([w for w in ws if w[0] != C0] + [(C0, w2) for w2 in
-             [_task_at(tasks, tasks[n[1]][0] - 5, tasks[n[1]][1], tasks[n[1]][2] - d) for d in (0, 1)] if w2 >= 0]
+             [_task_at(tasks, tasks[n[1]][0] - 4, tasks[n[1]][1], tasks[n[1]][2] - d) for d in (0, 1)] if w2 >= 0]
             if n[0] == CTX else ws)
         for n, ws in waits.items()},
-    # the last part (which holds taps of age 2) waiting as long as the first
-    "CTXL at the first part's lag": lambda waits, tasks: {
+    # the last part (which holds the taps of age 2) waiting as long as the others
+    "CTXL at the other parts' lag": lambda waits, tasks: {
         n: ([w for w in ws if w[0] != C0] + [(C0, w2) for w2 in
-             [_task_at(tasks, tasks[n[1]][0] - 4, tasks[n[1]][1], tasks[n[1]][2] - d) for d in (0, 1)] if w2 >= 0]
+             [_task_at(tasks, tasks[n[1]][0] - 3, tasks[n[1]][1], tasks[n[1]][2] - d) for d in (0, 1)] if w2 >= 0]
             if n[0] == CTXL else ws)
         for n, ws in waits.items()},
 }
