@@ -89,6 +89,7 @@ constexpr int kResCtxlNc = 2;      // column tiles of a last-part slice
 constexpr int kResMaxNc = 6;        // column tiles of one layer-3 role (K = 3: 3 logits + 3 means)
 constexpr int kResMaxParts = 12;    // k-parts of the old-tap context (the last one included)
 constexpr int kResRep = 2;          // replicas of every weight slice (they take alternate tasks)
+constexpr int kResKbaseLds = 4096;  // largest T + 1 of a resident plan (its step table sits in LDS)
 constexpr int kResMinHoist = 8;     // fewest spare workgroups that compute the hoisted layer-1 part in the launch
 constexpr int kResHoistLead = 64;   // tasks by which that part runs ahead of layer 3
 

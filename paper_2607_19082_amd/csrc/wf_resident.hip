@@ -125,7 +125,8 @@ __host__ __device__ __forceinline__ void band_span(int H, int W, int lam, int be
 // Position in the global order of the latest task of band beta (image b) at
 // a step <= s, or -1 when the band has none (beta < 0, or s before its first).
 // kbase[t]: the position of step t's first task (kbase[T]: the number of tasks).
-__host__ __device__ __forceinline__ int band_task_of(int H, int W, int lam, const int* kbase, int b, int beta, int s) {
+template <class KB>
+__host__ __device__ __forceinline__ int band_task_of(int H, int W, int lam, KB kbase, int b, int beta, int s) {
     if (beta < 0 || s < 0) return -1;
     int t0, t1;
     band_span(H, W, lam, beta, t0, t1);
@@ -161,7 +162,8 @@ struct ResDeps {
 // role RR_H computes the task's hoisted layer-1 part inside the launch.  The
 // context waits for it (a free wait slot; layer 1, which reads it, waits for
 // the context, so it follows).
-__host__ __device__ __forceinline__ ResDeps res_deps(int H, int W, int lam, const int* kbase, int role, int t, int b,
+template <class KB>
+__host__ __device__ __forceinline__ ResDeps res_deps(int H, int W, int lam, KB kbase, int role, int t, int b,
                                                      int beta, int k, int parts, int lag, int hoist) {
     ResDeps d{{{0, -1}, {0, -1}, {0, -1}}};
     switch (role) {
@@ -191,9 +193,15 @@ __host__ __device__ __forceinline__ ResDeps res_deps(int H, int W, int lam, cons
     }
     return d;
 }
+// The step table kbase, copied to LDS at the start of the launch: the waits
+// of every task read it, and from LDS that costs no memory round trip.
+__shared__ int res_kbase_lds[kResKbaseLds];
+// and the per-slot workgroup counts of the roles (the waits' targets)
+__shared__ int res_per_slot_lds[kResRoles * kResRep * kXcds];
+
 __device__ __forceinline__ ResDeps res_deps(const StepArgs& a, const ResArgs& r, int role, int t, int b, int beta,
                                             int k) {
-    return res_deps(a.H, a.W, a.lambda, r.kbase, role, t, b, beta, k, r.parts, r.ctx_lag, r.hoist);
+    return res_deps(a.H, a.W, a.lambda, res_kbase_lds, role, t, b, beta, k, r.parts, r.ctx_lag, r.hoist);
 }
 
 // Row r of band beta of image b at step t.
@@ -237,7 +245,7 @@ __device__ __forceinline__ bool res_wait(const ResArgs& r, ResWait w0, ResWait w
             // (one hoist workgroup per task, counting into class slot 0)
             const unsigned n =
                 w.role == RR_H ? (x == 0 ? 1u : 0u)
-                               : (unsigned)((const gi32*)r.per_slot)[(w.role * kResRep + w.k % r.nrep) * kXcds + x];
+                               : (unsigned)res_per_slot_lds[(w.role * kResRep + w.k % r.nrep) * kXcds + x];
             tgt = n + (unsigned)r.stall;
             p = res_slot(r, w.role, w.k, x);
         }
@@ -1018,6 +1026,8 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2))
     __shared__ float tab[kMaxTable];
     __shared__ int bail;
     for (int l = threadIdx.x; l < a.L; l += blockDim.x) tab[l] = a.table[l];
+    for (int l = threadIdx.x; l <= T; l += blockDim.x) res_kbase_lds[l] = r.kbase[l];   // (T < kResKbaseLds)
+    for (int l = threadIdx.x; l < kResRoles * kResRep * kXcds; l += blockDim.x) res_per_slot_lds[l] = r.per_slot[l];
     __syncthreads();
     // (selects, not a loop: a runtime index into the argument block would
     // copy it to scratch memory)
@@ -1246,6 +1256,8 @@ int build_resident(Plan& p) {
     r.nbands = ceil_div(p.H, kTile);
     r.nbs = p.B * r.nbands;
     const size_t nbs = (size_t)r.nbs;
+    if (p.T + 1 > kResKbaseLds)
+        return fail(WF_E_UNSUPPORTED, "resident driver: more than " + std::to_string(kResKbaseLds - 1) + " wavefront steps");
     std::vector<int> kbase;
     const long long tasks = res_kbase(p, kbase);
     r.ntasks = (int)tasks;
