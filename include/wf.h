@@ -87,8 +87,9 @@ typedef enum {
                                for every 16-row band of every step, as soon as the bands it
                                reads are complete (per-task completion counters).
                                WF_E_UNSUPPORTED when the slices do not fit the registers
-                               or the compute units, or M is not a multiple of 32; calls
-                               need y_hat aligned to 128 bytes (WF_E_INVALID otherwise)     */
+                               or the compute units, M is not a multiple of 32 or the
+                               schedule has more than 4095 steps; calls need y_hat
+                               aligned to 128 bytes (WF_E_INVALID otherwise)                */
 } wf_driver;
 
 /* Block order of the last layer's output rows (w3, b3).  The kernels use the
@@ -219,7 +220,9 @@ int wf_plan_schedule(wf_plan_t plan, int32_t *step_of, int32_t *n_steps);
  *     group (t*6 + kind)*(nrt_max + 1) + nrt_max.  The last entry is nrt_max.
  *   WF_DRIVER_RESIDENT: per task (step t, image b, 16-row band beta) in the
  *     global order, {t, b, beta, then for each role (0 CTX, 1 CTXL, 2 A, 3 B,
- *     4 C0, 5 C1) three waits (role, task), role -1 for none}.
+ *     4 C0, 5 C1, 6 H: the in-launch hoist of bf16 plans) three waits
+ *     (role, task), role -1 for none}, as planned with the context parts
+ *     before the last taking the taps older than two steps.
  * *needed receives the number of entries; out (HOST, capacity entries) may
  * be NULL.  Errors: WF_E_INVALID (desc, needed, capacity),
  * WF_E_UNSUPPORTED (another driver; any plan the driver refuses).
@@ -373,8 +376,8 @@ int wf_decode_noalloc(wf_plan_t plan, const float *psi, const int32_t *sym, cons
                       hipStream_t stream);
 
 /*
- * Measurement hook of the persistent and dataflow drivers (WF_E_UNSUPPORTED
- * for the others).  With `stamps` non-NULL (DEVICE int64 array of `capacity`
+ * Measurement hook of the persistent, dataflow and resident drivers
+ * (WF_E_UNSUPPORTED for the others).  With `stamps` non-NULL (DEVICE int64 array of `capacity`
  * entries) every later call records the device wall clock (100 MHz ticks):
  *  - persistent: at each device-wide barrier k = 0, 1, ...: entry k*(G+1) + g
  *    is the time workgroup g arrived at barrier k, entry k*(G+1) + G the time
@@ -385,6 +388,12 @@ int wf_decode_noalloc(wf_plan_t plan, const float *psi, const int32_t *sym, cons
  *    workgroup started waiting for its inputs, the time they were complete,
  *    and the time its results had landed; j is the job's position in the
  *    plan's job lists (XCD classes 0..7 in turn, each in its topological order).
+ *  - resident: three entries per task k (global order) and workgroup g,
+ *    3*(k*G + g) + {0, 1, 2}: the times g started waiting for the task's
+ *    inputs, found them complete and had its results published (0 where g's
+ *    role and replica do not run task k); workgroups are in role order (the
+ *    context parts, the last part, layers 1, 2, 3 mean and scale columns, the
+ *    in-launch hoist).
  * G is the grid size written to *grid; *needed receives the entries a call
  * takes (either output may be NULL).  Entries past `capacity` are not
  * written.  stamps == NULL turns recording off.  The array stays owned by
