@@ -506,6 +506,44 @@ def persistent_step_latency(w, table, cfg, precision, psi_d, sym_d, lfloor, torc
     return latency_histogram(np.diff(starts) / 100.0, lfloor)
 
 
+def resident_step_latency(w, table, cfg, precision, psi_d, sym_d, lfloor, torch, wf):
+    """Per-step latencies of one decode by the resident driver, from the
+    device wall clock (100 MHz) that its trace hook records per task and
+    workgroup: a step is done when the last workgroup has published its part
+    of the step's last task, and the latency of step t is the time from step
+    t-1 done to step t done (the bands of a step overlap the steps around it,
+    so this is the rate at which steps complete, not one step's span)."""
+    pr = wf.Plan(w, table, cfg["H"], cfg["W"], cfg["B"], cfg["K"], mask=mask_of(cfg), precision=precision,
+                 driver="resident")
+    try:
+        out = pr.alloc_out()
+        needed, G = pr.trace(None)
+        st = torch.zeros(needed, dtype=torch.int64, device="cuda")
+        for _ in range(2):
+            pr.decode(psi_d, sym_d, out=out)
+        pr.sync()
+        pr.trace(st)
+        pr.decode(psi_d, sym_d, out=out)
+        pr.sync()
+        pr.trace(None)
+        ends = st.cpu().numpy().reshape(-1, G, 3)[:, :, 2].max(axis=1).astype(np.float64)
+    finally:
+        pr.close()
+    # tasks of each step in the global order: (image, 16-row band) pairs
+    # holding a latent of the step
+    H, W, B = cfg["H"], cfg["W"], cfg["B"]
+    lam = MASK_SHEAR[mask_of(cfg)]
+    T = W + lam * (H - 1)
+    ntask = []
+    for t in range(T):
+        i0, i1 = max(0, -(-(t - W + 1) // lam)), min(H - 1, t // lam)
+        ntask.append(B * (i1 // 16 - i0 // 16 + 1))
+    assert sum(ntask) == ends.size, (sum(ntask), ends.size)
+    kb = np.concatenate([[0], np.cumsum(ntask)])
+    done = np.maximum.accumulate(np.array([ends[kb[t]:kb[t + 1]].max() for t in range(T)]))
+    return latency_histogram(np.diff(done) / 100.0, lfloor)
+
+
 def timed_calls(fn, steps, stream, torch):
     ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
           for _ in range(steps)]
@@ -589,7 +627,8 @@ def main():
     ap.add_argument("--no-transforms", action="store_true",
                     help="skip the hyper-decoder and synthesis timing (end-to-end decode)")
     ap.add_argument("--no-step-latency", action="store_true",
-                    help="skip the per-step latency histogram (one traced decode by the persistent driver)")
+                    help="skip the per-step latency histogram (one traced decode by the resident driver when it "
+                         "is the one timed, else by the persistent driver)")
     ap.add_argument("--no-entropy", action="store_true",
                     help="skip the decode from rANS streams (measured by default when the plan allows it)")
     ap.add_argument("--summarize-traffic", nargs=4, metavar=("FETCH_DIR", "WRITE_DIR", "CAL_FETCH_DIR", "CAL_WRITE_DIR"),
@@ -694,7 +733,11 @@ def main():
     lfloor = min(x for x in (node_us, bar_us) if x > 0)
 
     rec_hist = None
-    if not args.no_step_latency and args.group <= 1:
+    if not args.no_step_latency and args.group <= 1 and args.driver == "resident":
+        rec_hist = {"driver": "resident (device clock per task and workgroup; a step's latency is the time "
+                              "between the completions of consecutive steps)",
+                    **resident_step_latency(w, table, cfg, args.precision, psi_d, sym_d, lfloor, torch, wf)}
+    elif not args.no_step_latency and args.group <= 1:
         rec_hist = {"driver": "persistent (device clock at each device-wide barrier; the graph driver's "
                               "histogram is in its committed kernel-trace summary)",
                     **persistent_step_latency(w, table, cfg, args.precision, psi_d, sym_d, lfloor, torch, wf)}
