@@ -342,11 +342,12 @@ def step_rows(cfg, group=1):
     return rows
 
 
-def parity_record(got, ref, table, tol):
+def parity_record(got, ref, table, tol, bf16=False):
     """Element-wise comparison of the timed decode's outputs with the oracle's
     decode of the same latents: the largest absolute error per output, the
     scale indices within 1e-4 relative of a table level (where the index is
-    excused and counted) and the index mismatches outside them."""
+    excused and counted), for bf16 also those where a level lies between the
+    two scales (counted apart), and the index mismatches outside them."""
     rec = {"bar_abs": tol}
     errs = {}
     for k in ("y_hat", "mean", "scale", "weight", "comp_mean"):
@@ -362,11 +363,27 @@ def parity_record(got, ref, table, tol):
         q = np.clip(pos + off, 0, len(t) - 1)
         near |= np.abs(s - t[q]) <= 1e-4 * t[q]
     near &= s != np.float64(table[0])
-    mism = (np.asarray(got["idx"]).reshape(-1) != np.asarray(ref["idx"]).reshape(-1))
+    gi = np.asarray(got["idx"]).reshape(-1)
+    mism = gi != np.asarray(ref["idx"]).reshape(-1)
     rec["idx_boundary_cases"] = int(near.sum())
     rec["idx_mismatch_at_boundary"] = int((mism & near).sum())
-    rec["idx_mismatch_unexcused"] = int((mism & ~near).sum())
-    rec["within_bar"] = bool(all(v <= tol for v in errs.values()) and rec["idx_mismatch_unexcused"] == 0)
+    # the index decided on the timed decode's own scale (in fp32, as the
+    # kernel decides it) must hold exactly
+    own = np.searchsorted(np.asarray(table, np.float32)[:-1],
+                          np.asarray(got["scale"], np.float32).reshape(-1), side="left")
+    rec["idx_inconsistent_with_own_scale"] = int((own != gi).sum())
+    excused = near
+    if bf16:
+        # bf16: also where a level lies between the two scales (which agree to
+        # the float bar), so that either side's decision is right; counted apart
+        g = np.asarray(got["scale"], np.float64).reshape(-1)
+        lo, hi = np.minimum(g, s), np.maximum(g, s)
+        br = (np.searchsorted(t, hi, side="right") > np.searchsorted(t, lo, side="left")) & ~near
+        rec["idx_mismatch_bracketed"] = int((mism & br).sum())
+        excused = near | br
+    rec["idx_mismatch_unexcused"] = int((mism & ~excused).sum())
+    rec["within_bar"] = bool(all(v <= tol for v in errs.values()) and rec["idx_mismatch_unexcused"] == 0
+                             and rec["idx_inconsistent_with_own_scale"] == 0)
     return rec
 
 
@@ -409,9 +426,9 @@ def cpu_baseline(name, rows, mask=None, group=1, precision="fp32", got=None):
         if precision == "bf16":
             mb = oracle.Model(w, table, rows, cfg["W"], cfg["B"], cfg["K"], relaxed=cfg["relaxed"], group=group,
                               bf16=True)
-            par = parity_record(top, mb.decode(psi, sym), table, 1e-3)
+            par = parity_record(top, mb.decode(psi, sym), table, 1e-3, bf16=True)
             par["reference"] = "the oracle's bf16 mode (bf16 weights, bf16-pair activations)"
-            par["max_abs_vs_fp32_oracle"] = parity_record(top, ref, table, 1e-2)["max_abs_err"]
+            par["max_abs_vs_fp32_oracle"] = parity_record(top, ref, table, 1e-2, bf16=True)["max_abs_err"]
         else:
             par = parity_record(top, ref, table, 1e-4)
             par["reference"] = "the oracle (fp64 accumulation)"

@@ -176,8 +176,24 @@ def test_parity_record():
     ref["scale"][0, 0, 0, 0, 0] = table[10]
     ref["idx"][0, 0, 0, 0, 0] = 10
     got["idx"][0, 0, 0, 0, 0] = 11
-    got["scale"][0, 0, 0, 0, 0] = table[10]
+    got["scale"][0, 0, 0, 0, 0] = table[10] * np.float32(1 + 5e-5)   # (its own decision: 11)
     r = bench.parity_record(got, ref, table, 1e-4)
     assert r["idx_mismatch_at_boundary"] == 1 and r["idx_mismatch_unexcused"] == 0 and r["within_bar"]
+    assert r["idx_inconsistent_with_own_scale"] == 0
+    # an index that does not follow the decode's own scale fails the bar
+    bad = {k: v.copy() for k, v in got.items()}
+    bad["idx"][0, 2, 2, 0, 2] += 1
+    r = bench.parity_record(bad, ref, table, 1e-4)
+    assert r["idx_inconsistent_with_own_scale"] == 1 and not r["within_bar"]
+    # bf16: a level between the two scales (1e-3 apart, outside 1e-4 of the
+    # level) excuses the flip and is counted apart; fp32 does not excuse it
+    g2, r2 = {k: v.copy() for k, v in got.items()}, {k: v.copy() for k, v in ref.items()}
+    r2["scale"][0, 1, 2, 0, 3] = table[20] * np.float32(1 - 1e-3)
+    r2["idx"][0, 1, 2, 0, 3] = 20
+    g2["scale"][0, 1, 2, 0, 3] = table[20] * np.float32(1 + 1e-3)
+    g2["idx"][0, 1, 2, 0, 3] = 21
+    rb = bench.parity_record(g2, r2, table, 1e-2, bf16=True)
+    assert rb["idx_mismatch_bracketed"] == 1 and rb["idx_mismatch_unexcused"] == 0 and rb["within_bar"]
+    assert bench.parity_record(g2, r2, table, 1e-2)["idx_mismatch_unexcused"] == 1
     got["idx"][0, 1, 1, 0, 1] += 1
     assert bench.parity_record(got, ref, table, 1e-4)["idx_mismatch_unexcused"] == 1
