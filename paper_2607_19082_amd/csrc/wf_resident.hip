@@ -657,10 +657,22 @@ __device__ __noinline__ void res_l1(const StepArgs& a_in, const ResArgs& r_in, i
             }
         }
     } else {
-        s.split(0, kbn + kbc);
-        slo.kb0 = s.kb0;
+        // fp32: every wave takes a quarter of the new-tap k-blocks (w[u],
+        // u < KH) and a quarter of the context's (w[KH + u]), so that the
+        // context half is computed as soon as the context is published and
+        // only the new-tap half waits for the step before
+        constexpr int KH = ResKb<P>::a / 2;
+        const int hn = kbn / kWaves;
+        const typename P::B* pw = static_cast<const typename P::B*>(a.wp_l1) + lane;
+#pragma unroll
+        for (int u = 0; u < KH; ++u) {
+            s.w[u][0] = u < hn ? pw[((size_t)c * (kbn + kbc) + wave * hn + u) * 64] : zero4();
+            s.w[KH + u][0] = u < hn ? pw[((size_t)c * (kbn + kbc) + kbn + wave * hn + u) * 64] : zero4();
+        }
+        s.kb0 = wave * hn;
+        s.n = hn;
+        slo.kb0 = 0;
         slo.n = 0;
-        s.load(a.wp_l1, kbn + kbc, c, 0);
     }
     const size_t h1s = (size_t)kTile * a.Np1 * 4;     // bytes of one task's h1
     // the weight slice is in registers before the first task (else the
@@ -684,11 +696,45 @@ __device__ __noinline__ void res_l1(const StepArgs& a_in, const ResArgs& r_in, i
         // (the addresses depend on the task only: computed before the wait)
         const Row w = band_row(a, b, beta, t, lane & 15);
         const NewSrc ns = new_src<P>(a, w, kself, kup);
-        if (!res_wait(r, dp.w[0], dp.w[1], dp.w[2], bail)) return false;
-        z += ld1<true>(a.p1, zq, v.valid && r.hoist);
-        res_stamp(r, k, 1);
         f4 acc[1] = {zero4()};
-        if constexpr (P::kBf16) {
+        if constexpr (!P::kBf16) {
+            // the context half first (its one wait), then the new-tap half
+            constexpr int KH = ResKb<P>::a / 2;
+            const int hn = __builtin_amdgcn_readfirstlane(s.n), hk0 = __builtin_amdgcn_readfirstlane(s.kb0);
+            const int ntap = hk0 >= tapkb;
+            const size_t en = (ntap ? ns.base[1] : ns.base[0]) + (size_t)(hk0 - ntap * tapkb) * 256 + kq * 64;
+            const size_t ec = ctx_base(a, r, k, r.parts - 1) + (size_t)hk0 * 256 + lane * 4;
+            const int offn = (ntap ? ns.ok[1] : ns.ok[0]) ? (int)(en * 4) : kBufBytes;   // (past the window: zeros)
+            const int offc = w.valid ? (int)(ec * 4) : kBufBytes;
+            const ResWait none{0, -1};
+            auto half = [&](const auto rs, int off, int u0) {
+                f4 av[KH];
+                if (hn == KH) {   // a full share: each MFMA waits only for its own load
+#pragma unroll
+                    for (int u = 0; u < KH; ++u)
+                        av[u] = __builtin_bit_cast(f4, __builtin_amdgcn_raw_buffer_load_b128(rs, off + u * 1024, 0, 0));
+                    __builtin_amdgcn_sched_barrier(0);   // (all loads in flight before the first MFMA)
+#pragma unroll
+                    for (int u = 0; u < KH; ++u) acc[0] = PF32::mma(av[u], s.w[u0 + u][0], acc[0]);
+                } else {
+#pragma unroll
+                    for (int u = 0; u < KH; ++u)
+                        if (u < hn)
+                            av[u] = __builtin_bit_cast(f4, __builtin_amdgcn_raw_buffer_load_b128(rs, off + u * 1024, 0, 0));
+#pragma unroll
+                    for (int u = 0; u < KH; ++u)
+                        if (u < hn) acc[0] = PF32::mma(av[u], s.w[u0 + u][0], acc[0]);
+                }
+            };
+            if (!res_wait(r, dp.w[0], none, none, bail)) return false;
+            half(rsrc(r.ctx), offc, KH);
+            if (!res_wait(r, none, dp.w[1], dp.w[2], bail)) return false;
+            res_stamp(r, k, 1);
+            half(rsrc(r.ytile), offn, 0);
+        } else {
+            if (!res_wait(r, dp.w[0], dp.w[1], dp.w[2], bail)) return false;
+            z += ld1<true>(a.p1, zq, v.valid && r.hoist);
+            res_stamp(r, k, 1);
             const int sn = __builtin_amdgcn_readfirstlane(s.n), skb0 = __builtin_amdgcn_readfirstlane(s.kb0);
             if (isnew) {
                 // the wave's k-blocks are those of one tap (two waves, two taps)
@@ -742,44 +788,6 @@ __device__ __noinline__ void res_l1(const StepArgs& a_in, const ResArgs& r_in, i
                     for (int u = 0; u < ResKb<P>::a; ++u)
                         if (u < sn) acc[0] = PBF16::mma(split8(raw[u][0], raw[u][1]), s.w[u][0], acc[0]);
                 }
-            }
-        } else {
-            // the 4 M k-values split into four equal shares, so each wave's
-            // k-blocks are those of one new tap or of half the old-tap
-            // context (the last part's buffer holds its sum): one base, and
-            // block u 1 KB further
-            const int skb0 = __builtin_amdgcn_readfirstlane(s.kb0);
-            const float* src;
-            size_t e;
-            bool ok;
-            if (skb0 < kbn) {
-                const int tap = skb0 >= tapkb;
-                src = static_cast<const float*>(r.ytile);
-                e = (tap ? ns.base[1] : ns.base[0]) + (size_t)(skb0 - tap * tapkb) * 256 + kq * 64;
-                ok = tap ? ns.ok[1] : ns.ok[0];
-            } else {
-                src = r.ctx;
-                e = ctx_base(a, r, k, r.parts - 1) + (size_t)(skb0 - kbn) * 256 + lane * 4;
-                ok = w.valid;
-            }
-            const int off = ok ? (int)(e * 4) : kBufBytes;   // (past the window: zeros)
-            const int n = __builtin_amdgcn_readfirstlane(s.n);
-            const auto rs = rsrc(src);
-            f4 av[ResKb<P>::a];
-            if (n == ResKb<P>::a) {   // a full share: each MFMA waits only for its own load
-#pragma unroll
-                for (int u = 0; u < ResKb<P>::a; ++u)
-                    av[u] = __builtin_bit_cast(f4, __builtin_amdgcn_raw_buffer_load_b128(rs, off + u * 1024, 0, 0));
-                __builtin_amdgcn_sched_barrier(0);   // (all loads in flight before the first MFMA)
-#pragma unroll
-                for (int u = 0; u < ResKb<P>::a; ++u) acc[0] = PF32::mma(av[u], s.w[u][0], acc[0]);
-            } else {
-#pragma unroll
-                for (int u = 0; u < ResKb<P>::a; ++u)
-                    if (u < n) av[u] = __builtin_bit_cast(f4, __builtin_amdgcn_raw_buffer_load_b128(rs, off + u * 1024, 0, 0));
-#pragma unroll
-                for (int u = 0; u < ResKb<P>::a; ++u)
-                    if (u < n) acc[0] = PF32::mma(av[u], s.w[u][0], acc[0]);
             }
         }
         float o[1];
