@@ -4,12 +4,16 @@
 
 namespace wf {
 
-// Pre-loop: the hyperprior half of layer 1 for every latent, four row tiles
-// per wave (every weight operand feeds four MFMA chains).
-constexpr int kHoistRt = 4;
+// Pre-loop: the hyperprior half of layer 1 for every latent, several row
+// tiles per wave (every weight operand feeds that many MFMA chains): fp32
+// eight, two k-blocks a load batch (4K decode 11.60 against 11.71-11.75 ms
+// with four and four; 11.64-11.78 with 8/1, 12/1, 12/2, 16/1, 6/4, 8/4, 4/8);
+// bf16 four and three.
+template <class P>
+constexpr int kHoistRt = P::kBf16 ? 4 : 8;
 template <class P>
 __global__ __launch_bounds__(kThreads) void k_hoist(StepArgs a) {
-    hoist_job<P, false, kHoistRt, P::kBf16 ? 3 : 4>(a, blockIdx.x);
+    hoist_job<P, false, kHoistRt<P>, P::kBf16 ? 3 : 2>(a, blockIdx.x);
 }
 
 // Old-tap context jobs [j0, ...) of step s1 only (before the first step).
@@ -61,7 +65,7 @@ int enqueue_set_call_at(CallPtrs* dst, const CallPtrs& c, hipStream_t stream) {
 
 template <class P>
 static void launch_hoist(const StepArgs& a, hipStream_t stream) {
-    hipLaunchKernelGGL(k_hoist<P>, dim3(hoist_blocks<kHoistRt>(a)), dim3(kThreads), 0, stream, a);
+    hipLaunchKernelGGL(k_hoist<P>, dim3(hoist_blocks<kHoistRt<P>>(a)), dim3(kThreads), 0, stream, a);
 }
 
 int enqueue_hoist(Plan& p, hipStream_t stream) {
