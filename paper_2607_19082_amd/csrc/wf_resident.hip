@@ -1061,6 +1061,11 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2))
                       : role == 4 ? r.first[5] - r.first[4]
                                   : r.first[6] - r.first[5])) / r.nrep;
     const int sl = q % nsl, rep = q / nsl;
+    // Layer 1 issues ahead of the other workgroup on its compute unit (a
+    // context part or a layer-3 half): its tasks are short and every step's
+    // chain runs through them. Raising layer 2 or 3 as well, or the context
+    // above layers 2-3, made the decode slower.
+    if (role == RR_A) __builtin_amdgcn_s_setprio(2);
     switch (role) {
     case RR_CTX:
         res_ctx<P, false>(a, r, T, sl, rep, red, &bail);
