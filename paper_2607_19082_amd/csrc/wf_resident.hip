@@ -47,11 +47,21 @@
 // Every task writes its outputs (context parts, h1, h2) to buffers of its
 // own, indexed by its position k in the global order, and y_hat is written
 // once per latent, so no address is written twice in a call.  Producers store
-// with write-through (sc1) stores and bump the counter after their stores
-// have landed; consumers read with ordinary cached loads: a line is first
-// read, into an XCD's L2, only after its producer's counter was seen (the L2s
-// start each launch empty of it), so the line the L2 keeps is current, and the
-// workgroups of one XCD that read the same band share it there.
+// with write-through (sc1) stores.  The context roles and layer 3 bump the
+// counter after their stores have landed, and their consumers read with
+// ordinary cached loads: a line is first read, into an XCD's L2, only after
+// its producer's counter was seen (the L2s start each launch empty of it), so
+// the line the L2 keeps is current, and the workgroups of one XCD that read
+// the same band share it there.  Layers 1 and 2 bump it as soon as every wave
+// has issued its stores, without waiting for them to land: h1 and h2 are
+// filled with an all-ones pattern before the launch (a NaN that lrelu of
+// finite values never yields, in fp32 and in either bf16 half), and layers 2
+// and 3 read them with agent-coherent (sc1) loads, which an XCD's L2 does not
+// answer from a stale line, and load again until no value holds the pattern.
+// A store's value is then seen by the first load after it lands, without the
+// store acknowledgement and the counter bump in between.  This holds for fp32
+// (kResChecked); in bf16 the decode came out slower (9.5 against 9.3 ms at
+// 4K), so there layers 1 and 2 publish as the other roles do.
 // Deadlock freedom: every dependency of a task comes earlier in the global
 // order, and every workgroup runs its tasks in that order, so the earliest
 // unfinished task can always run; the launch is cooperative, so all
@@ -275,6 +285,15 @@ __device__ __forceinline__ bool res_wait(const ResArgs& r, ResWait w0, ResWait w
     return *(li32*)bail == 0;
 }
 
+// Count the task once every wave has issued its stores (their readers check
+// the values; see the top of the file).
+__device__ __forceinline__ void res_signal_issued(const ResArgs& r, int role, int k) {
+    __builtin_amdgcn_s_barrier();
+    if (threadIdx.x == 0)
+        __hip_atomic_fetch_add(res_slot(r, role, k, blockIdx.x % kXcds), 1u, __ATOMIC_RELAXED,
+                               __HIP_MEMORY_SCOPE_AGENT);
+}
+
 // Publish the task's stores (every wave's have landed) and count the task.
 __device__ __forceinline__ void res_signal(const ResArgs& r, int role, int k) {
     __builtin_amdgcn_s_waitcnt(0);
@@ -308,9 +327,68 @@ struct WSlice {
         for (int u = 0; u < KB; ++u)
 #pragma unroll
             for (int c = 0; c < NC; ++c)
-                if (u < n) w[u][c] = p[((size_t)(ct0 + c * cstride) * nkb + kb0 + u) * 64];
+                w[u][c] = u < n ? p[((size_t)(ct0 + c * cstride) * nkb + kb0 + u) * 64] : typename P::B{};
     }
 };
+
+// Whether an activation operand holds the fill pattern of h1 / h2 (an
+// all-ones fp32 word, or an all-ones bf16 half).
+constexpr unsigned kResFill = 0xFFFFFFFFu;
+template <class P>
+constexpr bool kResChecked = !P::kBf16;
+__device__ __forceinline__ bool holds_fill(const f4& v) {
+    bool f = false;
+#pragma unroll
+    for (int j = 0; j < 4; ++j) f |= __builtin_bit_cast(unsigned, v[j]) == kResFill;
+    return f;
+}
+__device__ __forceinline__ bool holds_fill(const b8x2& v) {
+    typedef unsigned u4 __attribute__((ext_vector_type(4)));
+    const u4 h = __builtin_bit_cast(u4, v.hi), l = __builtin_bit_cast(u4, v.lo);
+    bool f = false;
+#pragma unroll
+    for (int j = 0; j < 4; ++j)
+        f |= (h[j] & 0xFFFFu) == 0xFFFFu || (h[j] >> 16) == 0xFFFFu || (l[j] & 0xFFFFu) == 0xFFFFu ||
+             (l[j] >> 16) == 0xFFFFu;
+    return f;
+}
+
+// acc = the wave's k-blocks of a task's h1 / h2 tile (h, ncols columns) times
+// its weight slice, read with agent-coherent loads until no value holds the
+// fill pattern (the producers count their task before their stores land).
+// The MFMAs run on every pass, each waiting only for its own load; the check
+// follows them.  Past the wave's share the loads are masked (zeros) and the
+// weights zero.  A pass count past the wall-clock budget records
+// WF_E_TIMEOUT and ends the loop (the next wait then makes the workgroup
+// leave).
+template <class P, int KB, int NC>
+__device__ __forceinline__ void wdot_checked(const WSlice<P, KB, NC>& s, const void* h, int ncols, bool valid,
+                                             const ResArgs& r, f4 (&acc)[NC]) {
+    const int n = __builtin_amdgcn_readfirstlane(s.n), kb0 = __builtin_amdgcn_readfirstlane(s.kb0);
+    const long long t0 = wall_clock64();
+    for (int it = 0;; ++it) {
+        typename P::A av[KB];
+#pragma unroll
+        for (int u = 0; u < KB; ++u) av[u] = ld_tile<P, true>(h, 0, ncols, kb0 + u, valid && u < n);
+        __builtin_amdgcn_sched_barrier(0);   // (all loads in flight before the first MFMA)
+#pragma unroll
+        for (int c = 0; c < NC; ++c) acc[c] = zero4();
+#pragma unroll
+        for (int u = 0; u < KB; ++u)
+#pragma unroll
+            for (int c = 0; c < NC; ++c) acc[c] = P::mma(av[u], s.w[u][c], acc[c]);
+        bool seen = false;
+#pragma unroll
+        for (int u = 0; u < KB; ++u) seen |= holds_fill(av[u]);
+        if (!__any(seen)) break;
+        if ((it & 15) == 15 && wall_clock64() - t0 > r.budget) {
+            if ((threadIdx.x & 63) == 0)
+                __hip_atomic_store((gi32*)r.err, kErrTimeout, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            break;
+        }
+        __builtin_amdgcn_s_sleep(1);
+    }
+}
 
 // acc[c] += sum over the wave's k-blocks of A(kb) x W(kb, c), the
 // activations loaded in batches of KBB k-blocks (each batch's loads issued
@@ -793,7 +871,8 @@ __device__ __noinline__ void res_l1(const StepArgs& a_in, const ResArgs& r_in, i
         float o[1];
         wreduce<1>(red, acc, o);
         st_tile<P, true>(static_cast<char*>(r.h1) + k * h1s, ro, a.Np1, col, lrelu(o[0] + z, a.slope));
-        res_signal(r, RR_A, k);
+        if constexpr (kResChecked<P>) res_signal_issued(r, RR_A, k);
+        else res_signal(r, RR_A, k);
         res_stamp(r, k, 2);
         return true;
     });
@@ -825,12 +904,14 @@ __device__ __noinline__ void res_l2(const StepArgs& a_in, const ResArgs& r_in, i
         const Row w = band_row(a, b, beta, t, lane & 15);
         const char* h1 = static_cast<const char*>(r.h1) + k * h1s;
         f4 acc[1] = {zero4()};
-        wdot(s, [&](int kb) { return ld_tile<P, false>(h1, 0, a.Np1, kb, w.valid); }, acc);
+        if constexpr (kResChecked<P>) wdot_checked(s, h1, a.Np1, w.valid, r, acc);
+        else wdot(s, [&](int kb) { return ld_tile<P, false>(h1, 0, a.Np1, kb, w.valid); }, acc);
         float o[1];
         wreduce<1>(red, acc, o);
         char* h2 = static_cast<char*>(r.h2) + k * h2s;
         st_tile<P, true>(h2, ro, a.Np2, col, lrelu(o[0] + bias, a.slope));
-        res_signal(r, RR_B, k);
+        if constexpr (kResChecked<P>) res_signal_issued(r, RR_B, k);
+        else res_signal(r, RR_B, k);
         res_stamp(r, k, 2);
         return true;
     });
@@ -891,7 +972,8 @@ __device__ __noinline__ void res_l3(const StepArgs& a_in, const ResArgs& r_in, i
         f4 acc[NC];
 #pragma unroll
         for (int c = 0; c < NC; ++c) acc[c] = zero4();
-        wdot(s, [&](int kb) { return ld_tile<P, false>(h2, 0, a.Np2, kb, w.valid); }, acc);
+        if constexpr (kResChecked<P>) wdot_checked(s, h2, a.Np2, w.valid, r, acc);
+        else wdot(s, [&](int kb) { return ld_tile<P, false>(h2, 0, a.Np2, kb, w.valid); }, acc);
         float o[NC];
         wreduce<NC>(red, acc, o);
 #pragma unroll
@@ -1078,6 +1160,11 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2))
     case RR_C0: res_l3<P, KC, true>(a, r, T, sl, rep, red, tab, &bail); break;
     default: res_l3<P, KC, false>(a, r, T, sl, rep, red, tab, &bail); break;
     }
+}
+
+__global__ void k_res_fill(unsigned* p, size_t n) {
+    for (size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += (size_t)gridDim.x * blockDim.x)
+        p[i] = kResFill;
 }
 
 __global__ void k_res_zero(unsigned* p, size_t n) {
@@ -1313,6 +1400,13 @@ int enqueue_resident(Plan& p, hipStream_t stream) {
     r.stall = p.stall;
     const size_t ncnt = (size_t)kResRoles * r.ntasks * kXcds * kDfSlotWords;
     hipLaunchKernelGGL(k_res_zero, dim3(1024), dim3(256), 0, stream, r.cnt, ncnt);
+    // fp32: h1 and h2 to the fill pattern their readers check for
+    if (p.precision != WF_BF16) {
+        hipLaunchKernelGGL(k_res_fill, dim3(2048), dim3(256), 0, stream, static_cast<unsigned*>(r.h1),
+                           (size_t)r.ntasks * kTile * p.Np1);
+        hipLaunchKernelGGL(k_res_fill, dim3(2048), dim3(256), 0, stream, static_cast<unsigned*>(r.h2),
+                           (size_t)r.ntasks * kTile * p.Np2);
+    }
     if (!r.hoist) {
         int rc = enqueue_hoist(p, stream);
         if (rc != WF_OK) return rc;

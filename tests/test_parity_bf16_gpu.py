@@ -102,6 +102,25 @@ def test_bf16_small_decode_encode(name, H, W, B, driver):
     log(compare(got_e, ref, table, cfg["K"], tol=BF16_TOL))
 
 
+@pytest.mark.parametrize("driver", ["graph", "resident"])
+def test_bf16_consecutive_calls_with_new_inputs(driver):
+    # one plan, the same output buffers, decodes of two different symbol sets
+    # in turn: no activation of an earlier call may be read as current data
+    cfg, w, table, psi, sym = make_case("minnen-hr-4k-240x135-m320", H=9, W=20)
+    sym2 = inputs.make_symbols(cfg["B"], cfg["H"], cfg["W"], cfg["M"], cfg["lap_b"], cfg["clip"], seed=7)
+    model = oracle_model(cfg, w, table, bf16=True)
+    refs = [model.decode(psi, s) for s in (sym, sym2)]
+    plan = gpu_plan(cfg, w, table, driver, precision="bf16")
+    out = plan.alloc_out()
+    psi_d = torch.from_numpy(psi).cuda()
+    for rep in range(2):
+        for s, ref in zip((sym, sym2), refs):
+            plan.decode(psi_d, torch.from_numpy(s).cuda(), out=out)
+            plan.sync()
+            log(compare(to_np(out), ref, table, cfg["K"], tol=BF16_TOL))
+    plan.close()
+
+
 @pytest.mark.parametrize("driver", ["graph", "persistent", "dataflow", "resident"])
 @pytest.mark.parametrize("name,H,W,B", [
     ("minnen-kodak-48x32-m192", 32, 48, 1),
