@@ -110,6 +110,7 @@ struct ResArgs {
     int nbs;                    // B * nbands
     unsigned* cnt;              // [kResRoles][ntasks][8] counter slots, kDfSlotWords words apart
     const int* kbase;           // [T + 1] position of each step's first task in the global order
+    const int* steps;           // [T] first band of each step | its bands per image << 16
     float* ctx;                 // [ntasks][parts] x (16 x 2M) old-tap context k-parts of each task
     void* h1;                   // [ntasks] x (16 x Np1) layer-1 output of each task (tile order)
     void* h2;                   // [ntasks] x (16 x Np2) layer-2 output of each task

@@ -115,7 +115,7 @@ __device__ __forceinline__ StepArgs uni_args(const StepArgs& x) {
 __device__ __forceinline__ ResArgs uni_args(const ResArgs& x) {
     ResArgs r = x;
 #define WF_U(f) r.f = uni(x.f)
-    WF_U(per_slot); WF_U(parts); WF_U(pre_kb); WF_U(ctx_lag); WF_U(nrep); WF_U(nbands); WF_U(nbs); WF_U(cnt); WF_U(kbase); WF_U(ctx); WF_U(h1); WF_U(h2);
+    WF_U(per_slot); WF_U(parts); WF_U(pre_kb); WF_U(ctx_lag); WF_U(nrep); WF_U(nbands); WF_U(nbs); WF_U(cnt); WF_U(kbase); WF_U(steps); WF_U(ctx); WF_U(h1); WF_U(h2);
     WF_U(ytile);
     WF_U(err);
     WF_U(stamps); WF_U(ntasks); WF_U(stall); WF_U(hoist);
@@ -134,18 +134,19 @@ __host__ __device__ __forceinline__ void band_span(int H, int W, int lam, int be
 }
 // Position in the global order of the latest task of band beta (image b) at
 // a step <= s, or -1 when the band has none (beta < 0, or s before its first).
-// kbase[t]: the position of step t's first task (kbase[T]: the number of tasks).
-template <class KB>
-__host__ __device__ __forceinline__ int band_task_of(int H, int W, int lam, KB kbase, int b, int beta, int s) {
+// kbase[t]: the position of step t's first task (kbase[T]: the number of
+// tasks); steps[t]: step t's first band | its bands per image << 16 (tables,
+// so that no wait divides by lambda).
+template <class KB, class ST>
+__host__ __device__ __forceinline__ int band_task_of(int H, int W, int lam, KB kbase, ST steps, int b, int beta,
+                                                     int s) {
     if (beta < 0 || s < 0) return -1;
     int t0, t1;
     band_span(H, W, lam, beta, t0, t1);
     if (s < t0) return -1;
     const int t = s < t1 ? s : t1;
-    int i0, n;
-    step_span(H, W, lam, t, i0, n);
-    const int blo = i0 / kTile, nb = (i0 + n - 1) / kTile - blo + 1;
-    return kbase[t] + b * nb + beta - blo;
+    const int st = steps[t];
+    return kbase[t] + b * (st >> 16) + beta - (st & 0xFFFF);
 }
 
 // One wait: task k of `role` complete (nothing to wait for when k < 0).
@@ -172,24 +173,24 @@ struct ResDeps {
 // role RR_H computes the task's hoisted layer-1 part inside the launch.  The
 // context waits for it (a free wait slot; layer 1, which reads it, waits for
 // the context, so it follows).
-template <class KB>
-__host__ __device__ __forceinline__ ResDeps res_deps(int H, int W, int lam, KB kbase, int role, int t, int b,
+template <class KB, class ST>
+__host__ __device__ __forceinline__ ResDeps res_deps(int H, int W, int lam, KB kbase, ST steps, int role, int t, int b,
                                                      int beta, int k, int parts, int lag, int hoist) {
     ResDeps d{{{0, -1}, {0, -1}, {0, -1}}};
     switch (role) {
         case RR_CTX:
         case RR_CTXL: {
             const int s = role == RR_CTX ? t - lag : t - 2;
-            d.w[0] = ResWait{RR_C0, band_task_of(H, W, lam, kbase, b, beta, s)};
-            d.w[1] = ResWait{RR_C0, band_task_of(H, W, lam, kbase, b, beta - 1, s)};
+            d.w[0] = ResWait{RR_C0, band_task_of(H, W, lam, kbase, steps, b, beta, s)};
+            d.w[1] = ResWait{RR_C0, band_task_of(H, W, lam, kbase, steps, b, beta - 1, s)};
             if (role == RR_CTXL && parts > 1) d.w[2] = ResWait{RR_CTX, k};   // the other parts, which it adds
             else if (hoist) d.w[2] = ResWait{RR_H, k};
             break;
         }
         case RR_A:
             d.w[0] = ResWait{RR_CTXL, k};
-            d.w[1] = ResWait{RR_C0, band_task_of(H, W, lam, kbase, b, beta, t - 1)};
-            d.w[2] = ResWait{RR_C0, band_task_of(H, W, lam, kbase, b, beta - 1, t - 1)};
+            d.w[1] = ResWait{RR_C0, band_task_of(H, W, lam, kbase, steps, b, beta, t - 1)};
+            d.w[2] = ResWait{RR_C0, band_task_of(H, W, lam, kbase, steps, b, beta - 1, t - 1)};
             break;
         case RR_B:
             d.w[0] = ResWait{RR_A, k};
@@ -206,12 +207,15 @@ __host__ __device__ __forceinline__ ResDeps res_deps(int H, int W, int lam, KB k
 // The step table kbase, copied to LDS at the start of the launch: the waits
 // of every task read it, and from LDS that costs no memory round trip.
 __shared__ int res_kbase_lds[kResKbaseLds];
+// and the per-step band table (first band | bands per image << 16)
+__shared__ int res_steps_lds[kResKbaseLds];
 // and the per-slot workgroup counts of the roles (the waits' targets)
 __shared__ int res_per_slot_lds[kResRoles * kResRep * kXcds];
 
 __device__ __forceinline__ ResDeps res_deps(const StepArgs& a, const ResArgs& r, int role, int t, int b, int beta,
                                             int k) {
-    return res_deps(a.H, a.W, a.lambda, res_kbase_lds, role, t, b, beta, k, r.parts, r.ctx_lag, r.hoist);
+    return res_deps(a.H, a.W, a.lambda, res_kbase_lds, res_steps_lds, role, t, b, beta, k, r.parts, r.ctx_lag,
+                    r.hoist);
 }
 
 // Row r of band beta of image b at step t.
@@ -492,11 +496,9 @@ template <class F>
 __device__ __forceinline__ void for_tasks(const StepArgs& a, int T, int rep, int nrep, F body) {
     int k = 0;
     for (int t = 0; t < T; ++t) {
-        int i0, n;
-        step_span(a.H, a.W, a.lambda, t, i0, n);
-        const int blo = i0 / kTile, bhi = (i0 + n - 1) / kTile;
+        const int st = res_steps_lds[t], blo = st & 0xFFFF, bend = blo + (st >> 16);
         for (int b = 0; b < a.B; ++b)
-            for (int beta = blo; beta <= bhi; ++beta, ++k)
+            for (int beta = blo; beta < bend; ++beta, ++k)
                 if (k % nrep == rep && !body(t, b, beta, k)) return;
     }
 }
@@ -559,29 +561,45 @@ __device__ __forceinline__ void old_tap_dydx(const StepArgs& a, int tap, int& dy
     dy = row - a.R;
     dx = tap - first - a.R;
 }
-// kb0: the wave's first old-tap k-block (uniform); w: the lane's row.
+// The wave's tap segments, the same for every task: their taps' offsets
+// and first k-blocks, and each one's element offset within a latent.
+struct OldTaps {
+    int dy[kResSeg], dx[kResSeg], us[kResSeg], ke[kResSeg];
+};
+// kb0: the wave's first old-tap k-block (uniform).
 template <class P>
-__device__ __forceinline__ OldSrc<P> old_src(const StepArgs& a, const Row& w, int kb0) {
+__device__ __forceinline__ OldTaps old_taps(const StepArgs& a, int kb0) {
     const int M = a.M, tapkb = M / P::kK, kq = (threadIdx.x & 63) >> 4;
     const int tap0 = kb0 / tapkb;
-    int us[kResSeg], off[kResSeg];
+    OldTaps o;
 #pragma unroll
     for (int q = 0; q < kResSeg; ++q) {
         const int tap = min(tap0 + q, a.n_old - 1);
         // (past the wave's range when tap0 + q is past the taps)
-        us[q] = q == 0 ? 0 : (tap0 + q) * tapkb - kb0;
-        int dy, dx;
-        old_tap_dydx(a, tap, dy, dx);
-        const int ii = w.i + dy, jj = w.j + dx;
+        o.us[q] = q == 0 ? 0 : (tap0 + q) * tapkb - kb0;
+        old_tap_dydx(a, tap, o.dy[q], o.dx[q]);
+        // element of the lane's first channel of the tap's k-block kb0 within
+        // the latent (may be negative for q > 0; the segment's own k-blocks
+        // are not)
+        if constexpr (P::kBf16)
+            o.ke[q] = (kb0 - tap * tapkb) * 64 + kq * 8;    // pairs: 32 hi, 32 lo per k-block
+        else
+            o.ke[q] = (kb0 - tap * tapkb) * P::kK + kq * 4;
+    }
+    return o;
+}
+// w: the lane's row.
+template <class P>
+__device__ __forceinline__ OldSrc<P> old_src(const StepArgs& a, const Row& w, const OldTaps& ot) {
+    const int M = a.M;
+    int us[kResSeg], off[kResSeg];
+#pragma unroll
+    for (int q = 0; q < kResSeg; ++q) {
+        us[q] = ot.us[q];
+        const int ii = w.i + ot.dy[q], jj = w.j + ot.dx[q];
         const bool ok = w.valid && ii >= 0 && jj >= 0 && jj < a.W;
         const int lat = ok ? (w.b * a.H + ii) * a.W + jj : 0;
-        // element of the lane's first channel of the tap's k-block kb0 (may
-        // be negative for q > 0; the segment's own k-blocks are not)
-        int e;
-        if constexpr (P::kBf16)
-            e = lat * 2 * M + (kb0 - tap * tapkb) * 64 + kq * 8;    // pairs: 32 hi, 32 lo per k-block
-        else
-            e = lat * M + (kb0 - tap * tapkb) * P::kK + kq * 4;
+        const int e = lat * (P::kBf16 ? 2 * M : M) + ot.ke[q];
         off[q] = ok ? e * (P::kBf16 ? 2 : 4) : kBufBytes - us[q] * OldSrc<P>::kKbBytes;
     }
     OldSrc<P> o;
@@ -659,6 +677,7 @@ __device__ __noinline__ void res_ctx(const StepArgs& a_in, const ResArgs& r_in, 
     // reconstruction (bf16: its pair copy)
     const void* src = P::kBf16 ? static_cast<const void*>(a.ybf) : static_cast<const void*>(uni(a.cp->y_hat));
     const int skb0 = __builtin_amdgcn_readfirstlane(s.kb0);
+    const OldTaps ot = old_taps<P>(a, skb0);
     // the weight slice is in registers before the first task (else the
     // compiler, seeing its loads possibly in flight at every task, waits for
     // every load of each batch before its first MFMA)
@@ -668,7 +687,7 @@ __device__ __noinline__ void res_ctx(const StepArgs& a_in, const ResArgs& r_in, 
         // the addresses depend on the task only: computed before the wait
         const size_t e = ctx_base(a, r, k, 0) + tile_idx<PF32>(ro, c * NC * kTile + (lane & 15), 2 * a.M);
         const Row w = band_row(a, b, beta, t, lane & 15);
-        const OldSrc<P> os = old_src<P>(a, w, skb0);
+        const OldSrc<P> os = old_src<P>(a, w, ot);
         const ResDeps dp = res_deps(a, r, LAST ? RR_CTXL : RR_CTX, t, b, beta, k);
         if (!res_wait(r, dp.w[0], dp.w[1], dp.w[2], bail)) return false;
         res_stamp(r, k, 1);
@@ -1117,6 +1136,7 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2))
     __shared__ int bail;
     for (int l = threadIdx.x; l < a.L; l += blockDim.x) tab[l] = a.table[l];
     for (int l = threadIdx.x; l <= T; l += blockDim.x) res_kbase_lds[l] = r.kbase[l];   // (T < kResKbaseLds)
+    for (int l = threadIdx.x; l < T; l += blockDim.x) res_steps_lds[l] = r.steps[l];
     for (int l = threadIdx.x; l < kResRoles * kResRep * kXcds; l += blockDim.x) res_per_slot_lds[l] = r.per_slot[l];
     __syncthreads();
     // (selects, not a loop: a runtime index into the argument block would
@@ -1189,15 +1209,19 @@ static int res_alloc(Plan& p, T** dst, size_t n) {
 static int ceil_div(int a, int b) { return (a + b - 1) / b; }
 
 // kbase[t] = the position of step t's first task in the global order (t, b,
-// band), kbase[T] = the number of tasks; returns that number.
-static long long res_kbase(const Plan& p, std::vector<int>& kbase) {
+// band), kbase[T] = the number of tasks; steps[t] = step t's first band |
+// its bands per image << 16; returns the number of tasks.
+static long long res_kbase(const Plan& p, std::vector<int>& kbase, std::vector<int>& steps) {
     kbase.assign(p.T + 1, 0);
+    steps.assign(p.T, 0);
     long long tasks = 0;
     for (int t = 0; t < p.T; ++t) {
         int i0, nn;
         step_span(p.H, p.W, p.lambda, t, i0, nn);
+        const int blo = i0 / kTile, nb = (i0 + nn - 1) / kTile - blo + 1;
         kbase[t] = (int)tasks;
-        tasks += (long long)p.B * ((i0 + nn - 1) / kTile - i0 / kTile + 1);
+        steps[t] = blo | nb << 16;
+        tasks += (long long)p.B * nb;
     }
     kbase[p.T] = (int)tasks;
     return tasks;
@@ -1239,8 +1263,8 @@ void res_ctx_split(const Plan& p, int& pre_kb, int& lag) {
 int resident_deps(const Plan& p, std::vector<int32_t>& out) {
     int pre_kb, lag2;
     res_ctx_split(p, pre_kb, lag2);
-    std::vector<int> kbase;
-    const long long tasks = res_kbase(p, kbase);
+    std::vector<int> kbase, steps;
+    const long long tasks = res_kbase(p, kbase, steps);
     if (tasks > INT32_MAX / 64) return fail(WF_E_UNSUPPORTED, "too many resident tasks");
     out.clear();
     int k = 0;
@@ -1255,7 +1279,7 @@ int resident_deps(const Plan& p, std::vector<int32_t>& out) {
                     // (as planned on a device with room for the context
                     // parts before the last and, for bf16, the in-launch
                     // hoist)
-                    const ResDeps d = res_deps(p.H, p.W, p.lambda, kbase.data(), role, t, b, beta, k,
+                    const ResDeps d = res_deps(p.H, p.W, p.lambda, kbase.data(), steps.data(), role, t, b, beta, k,
                                                pre_kb > 0 ? 2 : 1, lag2, p.precision == WF_BF16 ? 1 : 0);
                     for (int i = 0; i < 3; ++i) {
                         out.push_back(d.w[i].k >= 0 ? d.w[i].role : -1);
@@ -1358,14 +1382,18 @@ int build_resident(Plan& p) {
     const size_t nbs = (size_t)r.nbs;
     if (p.T + 1 > kResKbaseLds)
         return fail(WF_E_UNSUPPORTED, "resident driver: more than " + std::to_string(kResKbaseLds - 1) + " wavefront steps");
-    std::vector<int> kbase;
-    const long long tasks = res_kbase(p, kbase);
+    std::vector<int> kbase, steps;
+    const long long tasks = res_kbase(p, kbase, steps);
     r.ntasks = (int)tasks;
-    int* d_kbase = nullptr;
+    int *d_kbase = nullptr, *d_steps = nullptr;
     if ((rc = res_alloc(p, &d_kbase, kbase.size())) != WF_OK) return rc;
     e = hipMemcpy(d_kbase, kbase.data(), kbase.size() * sizeof(int), hipMemcpyHostToDevice);
     if (e != hipSuccess) return fail(WF_E_HIP, std::string("hipMemcpy: ") + hipGetErrorString(e));
+    if ((rc = res_alloc(p, &d_steps, steps.size())) != WF_OK) return rc;
+    e = hipMemcpy(d_steps, steps.data(), steps.size() * sizeof(int), hipMemcpyHostToDevice);
+    if (e != hipSuccess) return fail(WF_E_HIP, std::string("hipMemcpy: ") + hipGetErrorString(e));
     r.kbase = d_kbase;
+    r.steps = d_steps;
     if ((rc = res_alloc(p, &r.cnt, (size_t)kResRoles * tasks * kXcds * kDfSlotWords)) != WF_OK) return rc;
     // one output buffer per task (no address is written twice in a call);
     // each is read through raw buffer loads and must fit their window
