@@ -89,7 +89,12 @@ typedef enum {
                                WF_E_UNSUPPORTED when the slices do not fit the registers
                                or the compute units, M is not a multiple of 32 or the
                                schedule has more than 4095 steps; calls need y_hat
-                               aligned to 128 bytes (WF_E_INVALID otherwise)                */
+                               aligned to 128 bytes (WF_E_INVALID otherwise).  fp32:
+                               layer-1 and -2 outputs are read until no value holds an
+                               all-ones fill word, a NaN that finite inputs never yield;
+                               inputs holding NaNs with that exact bit pattern can make
+                               a call end in WF_E_TIMEOUT (after the wait budget of
+                               wf_plan_set_waits) instead of returning NaNs               */
 } wf_driver;
 
 /* Block order of the last layer's output rows (w3, b3).  The kernels use the
