@@ -257,7 +257,11 @@ int wf_plan_set_waits(wf_plan_t plan, int64_t spin_budget_ticks, int32_t stall);
  * consumer workgroups, each reading the blocks of a producer dealt to
  * another XCD, poll the counter (bounded, 1 s) and check every word.
  * mode 0: agent-coherent loads (buffers reused within a launch); mode 1:
- * ordinary cached loads of addresses written once per launch.
+ * ordinary cached loads of addresses written once per launch; mode 2: the
+ * producer bumps the counter once its stores are issued (no wait for them
+ * to land), the blocks start filled with an all-ones word, and the consumer
+ * reads agent-coherent, reading again each word that still holds the fill
+ * (bounded, 1 s) -- the resident driver's fp32 layer-1 and -2 outputs.
  * *mismatches receives the number of words read wrong (0 when the exchange
  * is coherent).  Synchronous (returns after the kernel finished on
  * `stream`).  Errors: WF_E_INVALID, WF_E_UNSUPPORTED (more workgroups than
