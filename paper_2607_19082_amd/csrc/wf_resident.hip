@@ -55,7 +55,7 @@
 // the same band share it there.  Layers 1 and 2 bump it as soon as every wave
 // has issued its stores, without waiting for them to land: h1 and h2 are
 // filled with an all-ones pattern before the launch (a NaN that lrelu of
-// finite values never yields, in fp32 and in either bf16 half), and layers 2
+// finite values never yields), and layers 2
 // and 3 read them with agent-coherent (sc1) loads, which an XCD's L2 does not
 // answer from a stale line, and load again until no value holds the pattern.
 // A store's value is then seen by the first load after it lands, without the
@@ -335,8 +335,8 @@ struct WSlice {
     }
 };
 
-// Whether an activation operand holds the fill pattern of h1 / h2 (an
-// all-ones fp32 word, or an all-ones bf16 half).
+// Whether an fp32 activation operand holds the fill pattern of h1 / h2 (an
+// all-ones word).
 constexpr unsigned kResFill = 0xFFFFFFFFu;
 template <class P>
 constexpr bool kResChecked = !P::kBf16;
@@ -346,17 +346,6 @@ __device__ __forceinline__ bool holds_fill(const f4& v) {
     for (int j = 0; j < 4; ++j) f |= __builtin_bit_cast(unsigned, v[j]) == kResFill;
     return f;
 }
-__device__ __forceinline__ bool holds_fill(const b8x2& v) {
-    typedef unsigned u4 __attribute__((ext_vector_type(4)));
-    const u4 h = __builtin_bit_cast(u4, v.hi), l = __builtin_bit_cast(u4, v.lo);
-    bool f = false;
-#pragma unroll
-    for (int j = 0; j < 4; ++j)
-        f |= (h[j] & 0xFFFFu) == 0xFFFFu || (h[j] >> 16) == 0xFFFFu || (l[j] & 0xFFFFu) == 0xFFFFu ||
-             (l[j] >> 16) == 0xFFFFu;
-    return f;
-}
-
 // acc = the wave's k-blocks of a task's h1 / h2 tile (h, ncols columns) times
 // its weight slice, read with agent-coherent loads until no value holds the
 // fill pattern (the producers count their task before their stores land).
