@@ -88,6 +88,11 @@ constexpr int kResCtxNc = 4;       // column tiles of a context part's slice (64
 constexpr int kResCtxlNc = 2;      // column tiles of a last-part slice
 constexpr int kResMaxNc = 6;        // column tiles of one layer-3 role (K = 3: 3 logits + 3 means)
 constexpr int kResMaxParts = 12;    // k-parts of the old-tap context (the last one included)
+// Resident completion counters: one slot every 256 bytes.  With the slots
+// 64 bytes apart (four in a 256-byte block) the 4K decode took 10.29 ms
+// fp32 / 9.19 bf16, 256 bytes apart 9.92 / 8.45, 512 or 1024 no better;
+// 32 bytes apart, or packed, 12.4-16.5 ms.
+constexpr int kResSlotWords = 64;
 constexpr int kResRep = 2;          // replicas of every weight slice (they take alternate tasks)
 constexpr int kResKbaseLds = 4096;  // largest T + 1 of a resident plan (its step table sits in LDS)
 constexpr int kResMinHoist = 8;     // fewest spare workgroups that compute the hoisted layer-1 part in the launch
@@ -108,7 +113,7 @@ struct ResArgs {
                                 // last part, which adds the other parts in
     int nbands;                 // 16-row bands per image (ceil(H / 16)); band slot bs = b * nbands + band
     int nbs;                    // B * nbands
-    unsigned* cnt;              // [kResRoles][ntasks][8] counter slots, kDfSlotWords words apart
+    unsigned* cnt;              // [kResRoles][ntasks][8] counter slots, kResSlotWords words apart
     const int* kbase;           // [T + 1] position of each step's first task in the global order
     const int* steps;           // [T] first band of each step | its bands per image << 16
     float* ctx;                 // [ntasks][parts] x (16 x 2M) old-tap context k-parts of each task

@@ -40,7 +40,7 @@
 // is stored; it is complete when it holds the role's workgroup count.  (A
 // counter per band, reused by its successive tasks, would not do: workgroups
 // that run ahead would make up for one that is still behind.)  Each counter
-// has one slot per XCD class of the producers (64 bytes apart).  A workgroup
+// has one slot per XCD class of the producers (256 bytes apart).  A workgroup
 // finishes its tasks in order, so a complete task implies that the role's
 // earlier tasks are complete too: waiting for the latest task a band had at
 // or before a step covers all of the band's earlier steps.
@@ -243,7 +243,7 @@ __device__ __forceinline__ __attribute__((address_space(1))) T* glb(T* p) {
 }
 
 __device__ __forceinline__ gu32* res_slot(const ResArgs& r, int role, int k, int x) {
-    return (gu32*)(r.cnt + (((size_t)role * r.ntasks + k) * kXcds + x) * kDfSlotWords);
+    return (gu32*)(r.cnt + (((size_t)role * r.ntasks + k) * kXcds + x) * kResSlotWords);
 }
 
 // Wave 0 polls up to three waits, eight lanes each (one per XCD class).  A
@@ -1176,9 +1176,10 @@ __global__ void k_res_fill(unsigned* p, size_t n) {
         p[i] = kResFill;
 }
 
+// Zero the n counter slots (only their first words).
 __global__ void k_res_zero(unsigned* p, size_t n) {
     for (size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += (size_t)gridDim.x * blockDim.x)
-        p[i] = 0u;
+        p[i * kResSlotWords] = 0u;
 }
 
 static const void* resident_fn(const Plan& p) {
@@ -1383,7 +1384,7 @@ int build_resident(Plan& p) {
     if (e != hipSuccess) return fail(WF_E_HIP, std::string("hipMemcpy: ") + hipGetErrorString(e));
     r.kbase = d_kbase;
     r.steps = d_steps;
-    if ((rc = res_alloc(p, &r.cnt, (size_t)kResRoles * tasks * kXcds * kDfSlotWords)) != WF_OK) return rc;
+    if ((rc = res_alloc(p, &r.cnt, (size_t)kResRoles * tasks * kXcds * kResSlotWords)) != WF_OK) return rc;
     // one output buffer per task (no address is written twice in a call);
     // each is read through raw buffer loads and must fit their window
     const size_t nt = (size_t)tasks;
@@ -1415,7 +1416,7 @@ int enqueue_resident(Plan& p, hipStream_t stream) {
     r.stamps_cap = p.stamps_cap;
     r.budget = p.spin_budget;
     r.stall = p.stall;
-    const size_t ncnt = (size_t)kResRoles * r.ntasks * kXcds * kDfSlotWords;
+    const size_t ncnt = (size_t)kResRoles * r.ntasks * kXcds;
     hipLaunchKernelGGL(k_res_zero, dim3(1024), dim3(256), 0, stream, r.cnt, ncnt);
     // fp32: h1 and h2 to the fill pattern their readers check for
     if (p.precision != WF_BF16) {
