@@ -281,7 +281,9 @@ __device__ __forceinline__ bool res_wait(const ResArgs& r, ResWait w0, ResWait w
                     break;
                 }
             }
-            __builtin_amdgcn_s_sleep(1);
+            // (a longer sleep between polls thins the polls' memory traffic:
+            // 4K 9.82 against 9.92 ms with sleep 1; 32 was slower again)
+            __builtin_amdgcn_s_sleep(8);
         }
         if (lane == 0) *(li32*)bail = flag;
     }
